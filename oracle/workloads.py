@@ -1,0 +1,173 @@
+"""Compositions of the oracle's CKKS operations (test infrastructure only):
+the plaintext-matrix x ciphertext projection and the scan-contract slice.
+
+Projection (Appendix "Projection Kernel Breakdown"): slots are viewed as
+segments, idx(r, s) = s * seg_len + r; the whole-segment shift Phi^delta is
+one rotation by delta * seg_len.  Input block g packs X[r, g*C + c] at
+idx(r, c); with complex pairing the ciphertext carries x^(2u) + i x^(2u+1).
+For output block b, giant step p and baby step q,
+
+    c~_p = sum_u sum_q Phi^q(x~_u) * D~_{b,u,p,q},     y = sum_p Phi^(p n1)(c~_p),
+
+and the real lane is extracted as c + conj(c).  The paper leaves the content
+of D~ implicit ("the two real weight slices"); the reading used here is
+
+    diag_t^(g,b)[idx(r, s)] = W[g*C + (s + t) mod C, b*C + s]   (0 if out of range)
+    D~_{b,u,p,q} = Phi^(-p n1)( (diag_{p n1 + q}^(2u,b) - i diag_{p n1 + q}^(2u+1,b)) / 2 )
+
+so that Re(x~ * D~) is the paired sum and one extraction c + conj(c) of the
+sum over giant steps yields the real projection (extraction is linear, so one
+conjugation per output block replaces one per giant step).  Without pairing
+D_{b,g,p,q} = Phi^(-p n1)(diag_{p n1+q}^(g,b)) and no extraction is done.
+When the slot count exceeds the packed width (n_slots > C * seg_len) the
+segment index is taken modulo C, i.e. the vector is replicated, which is how a
+short vector is made rotation-periodic.
+
+Scan-contract slice (Eq. "hescan-contract-output" and Appendix "Complex-Packed
+Reduction Accounting"): per token and state chunk, t1 = RS(relin(a * h)),
+t2 = RS(relin(t1 * C)); chunks (2l, 2l+1) are packed as chi = t2^(2l) + i
+t2^(2l+1) (i = X^(N/2), exact), reduced over the d_s axis by a rotate-and-add
+tree with steps d_s/2, ..., 1, and split by one conjugation:
+Re = Xi + conj(Xi) = 2 Sigma(v0), Im = -i (Xi - conj(Xi)) = 2 Sigma(v1).  The
+factor 2 is carried in the tracked scale (no constant multiplication).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+
+from . import ckks as C
+
+
+@dataclass
+class MatvecDesc:
+    level: int
+    n_in: int
+    n_out: int
+    n1: int
+    n2: int
+    unit: int            # slots per segment (Phi^1 = rotation by `unit`)
+    real_extract: bool
+    rescale: bool
+
+    def baby_steps(self):
+        return [q * self.unit for q in range(self.n1)]
+
+    def giant_steps(self):
+        return [p * self.n1 * self.unit for p in range(self.n2)]
+
+
+def required_rotations(desc: MatvecDesc, n_slots: int) -> set:
+    r = {s % n_slots for s in desc.baby_steps() + desc.giant_steps()}
+    r.discard(0)
+    return r
+
+
+def bsgs_matvec(P: C.Params, desc: MatvecDesc, ins: list, diag, keys: dict,
+                blocks=None) -> list:
+    """``diag(b, p, u, q)`` returns the evaluation-form plaintext D~_{b,u,p,q}
+    (``u64[level][N]``).  Baby steps are hoisted (one ModUp per input); giant
+    steps and the conjugation are ordinary key switches."""
+    assert len(ins) == desc.n_in
+    baby = [C.rotate_hoisted(P, x, desc.baby_steps(), keys) for x in ins]
+    outs = []
+    for b in (range(desc.n_out) if blocks is None else blocks):
+        y = None
+        for p in range(desc.n2):
+            acc = None
+            for u in range(desc.n_in):
+                for q in range(desc.n1):
+                    t = C.mul_plain(P, baby[u][q], diag(b, p, u, q))
+                    acc = t if acc is None else C.ct_add(P, acc, t)
+            acc = C.rotate(P, acc, desc.giant_steps()[p], keys)
+            y = acc if y is None else C.ct_add(P, y, acc)
+        if desc.real_extract:
+            y = C.ct_add(P, y, C.conjugate(P, y, keys))
+        if desc.rescale:
+            y = C.rescale(P, y)
+        outs.append(y)
+    return outs
+
+
+# ---------------------------------------------------- slot-domain packing
+
+
+def segment_indices(n_slots: int, seg_len: int, C_: int):
+    """(r, s) of every slot: r = j mod seg_len, s = (j div seg_len) mod C."""
+    j = np.arange(n_slots)
+    return j % seg_len, (j // seg_len) % C_
+
+
+def pack_input(X: np.ndarray, n_slots: int, seg_len: int, C_: int, g: int) -> np.ndarray:
+    """x^(g)[idx(r, c)] = X[r, g*C + c] (zero outside X)."""
+    T, d_in = X.shape
+    r, s = segment_indices(n_slots, seg_len, C_)
+    col = g * C_ + s
+    ok = (r < T) & (col < d_in)
+    out = np.zeros(n_slots)
+    out[ok] = X[r[ok], col[ok]]
+    return out
+
+
+def diagonal(W: np.ndarray, n_slots: int, seg_len: int, C_: int, g: int, b: int,
+             t: int) -> np.ndarray:
+    """diag_t^(g,b)[idx(r, s)] = W[g*C + (s + t) mod C, b*C + s]."""
+    d_in, d_out = W.shape
+    _, s = segment_indices(n_slots, seg_len, C_)
+    row = g * C_ + (s + t) % C_
+    col = b * C_ + s
+    ok = (row < d_in) & (col < d_out)
+    out = np.zeros(n_slots)
+    out[ok] = W[row[ok], col[ok]]
+    return out
+
+
+def shift_segments(v: np.ndarray, delta: int, seg_len: int) -> np.ndarray:
+    """Phi^delta in slots: left rotation by delta * seg_len."""
+    return np.roll(v, -delta * seg_len)
+
+
+def bsgs_diagonal_slots(W, n_slots, seg_len, C_, n1, b, p, u, q, paired: bool):
+    t = p * n1 + q
+    if paired:
+        d = 0.5 * (diagonal(W, n_slots, seg_len, C_, 2 * u, b, t)
+                   - 1j * diagonal(W, n_slots, seg_len, C_, 2 * u + 1, b, t))
+    else:
+        d = diagonal(W, n_slots, seg_len, C_, u, b, t).astype(np.complex128)
+    return shift_segments(d, -p * n1, seg_len)
+
+
+# -------------------------------------------------- scan-contract slice
+
+
+def reduce_axis(P: C.Params, ct: np.ndarray, d: int, keys: dict) -> np.ndarray:
+    """Rotate-and-add over a contiguous axis of length d (a power of two):
+    slot e*d then holds sum_i v[e*d + i]."""
+    step = d // 2
+    while step >= 1:
+        ct = C.ct_add(P, ct, C.rotate(P, ct, step, keys))
+        step //= 2
+    return ct
+
+
+def scan_contract_token(P: C.Params, h: list, decay: list, cfac: list, rlk, keys: dict,
+                        d_s: int) -> list:
+    """One token of the scan-contract slice.  h, decay, cfac: per-chunk
+    ciphertexts at the same level.  Returns [Re_0, Im_0, Re_1, Im_1, ...]."""
+    K = len(h)
+    t2 = []
+    for k in range(K):
+        t1 = C.rescale(P, C.mul_relin(P, decay[k], h[k], rlk))
+        c = cfac[k][: t1.shape[0]]
+        t2.append(C.rescale(P, C.mul_relin(P, t1, c, rlk)))
+    outs = []
+    for l in range(K // 2):
+        chi = C.ct_add(P, t2[2 * l], C.mul_monomial(P, t2[2 * l + 1], P.n // 2))
+        xi = reduce_axis(P, chi, d_s, keys)
+        xc = C.conjugate(P, xi, keys)
+        outs.append(C.ct_add(P, xi, xc))
+        outs.append(C.mul_monomial(P, C.ct_sub(P, xi, xc), 3 * P.n // 2))
+    if K % 2:
+        outs.append(reduce_axis(P, t2[-1], d_s, keys))
+    return outs

@@ -1,0 +1,277 @@
+"""Pins of the oracle's CKKS layer: encoding against the O(N^2) definition
+and the ring homomorphism; rescale and ModDown against big-integer division;
+every operation against the plaintext result after decryption."""
+import numpy as np
+import pytest
+
+import synth
+from oracle import ckks as C
+from oracle import encoding as E
+
+# small ring with multi-prime digits: N = 2^10, L = 5, alpha = 2 (dnum = 3)
+SMALL = dict(log_n=10, bits=50, L=5, alpha=2)
+
+
+@pytest.fixture(scope="module")
+def small():
+    P = C.params_small(**SMALL)
+    sk = C.secret_key(P, synth.secret(5, P.n))
+    return P, sk
+
+
+def _z(seed, n_slots, complex_=True):
+    re = synth.uniform_pm1(seed, "z-re", n_slots)
+    im = synth.uniform_pm1(seed, "z-im", n_slots) if complex_ else 0.0
+    return re + 1j * im
+
+
+def _enc(P, sk, z, scale, level, tag, idx=0):
+    a, e = synth.encrypt_draws(77, P.qs(level), P.n, tag, idx)
+    return C.encrypt(P, sk, C.encode_plain(P, z, scale, level), level, a, e)
+
+
+def _negacyclic_int(a, b):
+    n = len(a)
+    full = np.convolve(np.asarray(a, dtype=object), np.asarray(b, dtype=object))
+    out = full[:n].copy()
+    out[: n - 1] -= full[n:]
+    return out
+
+
+# ------------------------------------------------------------ encoding
+
+
+@pytest.mark.parametrize("log_n", [3, 4, 6])
+def test_encode_matches_direct_definition(log_n):
+    n = 1 << log_n
+    z = _z(log_n, n // 2)
+    zeta = np.exp(1j * np.pi / n)
+    e = [pow(5, j, 2 * n) for j in range(n // 2)]
+    direct = np.array([(2.0 / n) * sum(z[j] * zeta ** (-e[j] * k) for j in range(n // 2)).real
+                       for k in range(n)])
+    np.testing.assert_allclose(E.encode_real_coeffs(z, 1.0, n), direct, atol=1e-12)
+    # decode is evaluation at zeta^(5^j)
+    m = direct
+    ev = np.array([sum(m[k] * zeta ** (e[j] * k) for k in range(n)) for j in range(n // 2)])
+    np.testing.assert_allclose(E.decode_coeffs(m, 1.0, n), ev, atol=1e-12)
+    np.testing.assert_allclose(ev, z, atol=1e-12)
+
+
+def test_encode_rounding_half_away_from_zero():
+    n = 8
+    x = np.array([0.5, -0.5, 1.5, -1.5, 2.4999, -2.5001, 0.0, 3.0])
+    np.testing.assert_array_equal(E._round_half_away(x), [1, -1, 2, -2, 2, -3, 0, 3])
+    assert E.encode(np.zeros(n // 2), 2.0 ** 30, n).dtype == np.int64
+
+
+def test_encoding_is_a_ring_homomorphism():
+    """encode(z1) * encode(z2) (negacyclic) decodes to z1 * z2;
+    X -> X^(5^r) rotates left by r; X -> X^(2N-1) conjugates;
+    X^(N/2) multiplies every slot by i."""
+    n = 256
+    z1, z2 = _z(1, n // 2), _z(2, n // 2)
+    d = 2.0 ** 20
+    m1, m2 = E.encode(z1, d, n), E.encode(z2, d, n)
+    prod = _negacyclic_int(m1, m2)
+    np.testing.assert_allclose(E.decode_coeffs(prod, d * d, n), z1 * z2, atol=1e-4)
+    for r in [1, 5, 17, n // 2 - 1]:
+        g = pow(5, r, 2 * n)
+        mg = np.zeros(n, dtype=object)
+        for k in range(n):
+            t = k * g % (2 * n)
+            if t < n:
+                mg[t] += int(m1[k])
+            else:
+                mg[t - n] -= int(m1[k])
+        np.testing.assert_allclose(E.decode_coeffs(mg, d, n), np.roll(z1, -r), atol=1e-5)
+    mc = np.zeros(n, dtype=object)
+    for k in range(n):
+        t = k * (2 * n - 1) % (2 * n)
+        if t < n:
+            mc[t] += int(m1[k])
+        else:
+            mc[t - n] -= int(m1[k])
+    np.testing.assert_allclose(E.decode_coeffs(mc, d, n), np.conj(z1), atol=1e-5)
+    mono = np.zeros(n, dtype=object)
+    mono[n // 2] = 1
+    np.testing.assert_allclose(E.decode_coeffs(_negacyclic_int(m1, mono), d, n), 1j * z1,
+                               atol=1e-5)
+
+
+# ------------------------------------------------------- exact RNS steps
+
+
+def _bigint_rows(res, mods):
+    return [int(v) for v in E.crt_centered(res, mods)]
+
+
+def test_rescale_is_rounded_division(small):
+    P, sk = small
+    level = 4
+    rnd = np.random.default_rng(3)
+    ct = np.stack([np.stack([rnd.integers(0, q, size=P.n, dtype=np.uint64) for _ in range(2)])
+                   for q in P.qs(level)])
+    out = C.rescale(P, ct)
+    assert out.shape == (level - 1, 2, P.n)
+    Q = 1
+    for q in P.qs(level):
+        Q *= q
+    ql = P.q[level - 1]
+    for t in range(2):
+        c = C.intt(P, ct[:, t], P.qs(level))
+        big = [int(v) % Q for v in E.crt_centered(c, P.qs(level))]
+        want = [(2 * v + ql) // (2 * ql) for v in big]  # round(v / ql), ties impossible (ql odd)
+        got = C.intt(P, out[:, t], P.qs(level - 1))
+        Qp = Q // ql
+        gotb = [int(v) % Qp for v in E.crt_centered(got, P.qs(level - 1))]
+        assert gotb == [w % Qp for w in want]
+
+
+def test_moddown_is_exact_division_of_acc_minus_bconv(small):
+    P, sk = small
+    level = 3
+    ext = P.ext(level)
+    rnd = np.random.default_rng(4)
+    acc = np.stack([rnd.integers(0, m, size=P.n, dtype=np.uint64) for m in ext])
+    out = C.moddown(P, C.ntt(P, acc, ext), level)
+    # integer semantics: (A - y) / P with y = centred FastBConv(A mod P), A the
+    # lift over Q*P of the coefficient form
+    QP = 1
+    for m in ext:
+        QP *= m
+    Q = QP // P.P
+    A = [int(v) % QP for v in E.crt_centered(acc, ext)]
+    got = [int(v) % Q for v in E.crt_centered(C.intt(P, out, P.qs(level)), P.qs(level))]
+    for k in range(P.n):
+        y = 0
+        for i, p in enumerate(P.p):
+            ph = P.P // p
+            xi = A[k] % p * pow(ph, -1, p) % p
+            if xi > p // 2:
+                xi -= p
+            y += xi * ph
+        assert (A[k] - y) % P.P == 0
+        assert got[k] == ((A[k] - y) // P.P) % Q
+        assert abs(y) < P.alpha * P.P // 2
+
+
+# --------------------------------------------- decrypt-based operation pins
+
+
+def test_encrypt_decrypt(small):
+    P, sk = small
+    z = _z(20, P.n // 2)
+    for level in [1, 3, P.L]:
+        ct = _enc(P, sk, z, 2.0 ** 40, level, "encdec", level)
+        assert ct.shape == (level, 2, P.n)
+        np.testing.assert_allclose(C.decrypt(P, sk, ct, 2.0 ** 40), z, atol=2.0 ** -25)
+
+
+def test_mul_plain_add_sub_monomial(small):
+    P, sk = small
+    z1, z2, w = _z(21, P.n // 2), _z(22, P.n // 2), _z(23, P.n // 2)
+    level = 4
+    c1 = _enc(P, sk, z1, 2.0 ** 40, level, "ops", 1)
+    c2 = _enc(P, sk, z2, 2.0 ** 40, level, "ops", 2)
+    pt = C.encode_plain(P, w, 2.0 ** 30, level)
+    dec = lambda ct, s: C.decrypt(P, sk, ct, s)
+    np.testing.assert_allclose(dec(C.mul_plain(P, c1, pt), 2.0 ** 70), z1 * w, atol=2.0 ** -20)
+    np.testing.assert_allclose(dec(C.ct_add(P, c1, c2), 2.0 ** 40), z1 + z2, atol=2.0 ** -25)
+    np.testing.assert_allclose(dec(C.ct_sub(P, c1, c2), 2.0 ** 40), z1 - z2, atol=2.0 ** -25)
+    np.testing.assert_allclose(dec(C.mul_monomial(P, c1, P.n // 2), 2.0 ** 40), 1j * z1,
+                               atol=2.0 ** -25)
+    np.testing.assert_allclose(dec(C.mul_monomial(P, c1, 3 * P.n // 2), 2.0 ** 40), -1j * z1,
+                               atol=2.0 ** -25)
+    # X^k on the decrypted coefficients is the exact negacyclic shift
+    m = C.decrypt_coeffs(P, sk, c1)
+    m3 = C.decrypt_coeffs(P, sk, C.mul_monomial(P, c1, 3))
+    want = np.concatenate([-m[-3:], m[:-3]])
+    assert [int(v) for v in m3] == [int(v) for v in want]
+
+
+def test_rescale_decrypts(small):
+    P, sk = small
+    z, w = _z(24, P.n // 2), _z(25, P.n // 2)
+    level = 4
+    ct = _enc(P, sk, z, 2.0 ** 40, level, "rs")
+    ql = P.q[level - 1]
+    prod = C.mul_plain(P, ct, C.encode_plain(P, w, float(ql), level))
+    rs = C.rescale(P, prod)
+    np.testing.assert_allclose(C.decrypt(P, sk, rs, 2.0 ** 40), z * w, atol=2.0 ** -25)
+
+
+def test_key_switch_decrypts_to_c_times_s_from(small):
+    """dec_s(KS(c)) = c * s' + small, checked on the integer coefficients."""
+    P, sk = small
+    level = 5
+    g = P.galois_elt(3)
+    a, e = synth.switch_key_draws(9, P.ext(P.L), P.n, P.dnum, g)
+    key = C.galois_key(P, sk, g, a, e)
+    rnd = np.random.default_rng(5)
+    c = np.stack([rnd.integers(0, q, size=P.n, dtype=np.uint64) for q in P.qs(level)])
+    kb, ka = C.key_switch(P, c, key, level)
+    qs = P.qs(level)
+    s = sk.ntt_ext[:level]
+    mods_all = P.ext(P.L)
+    s_g = C.ntt(P, C.automorph_coef(P, C.lift(sk.coeffs.astype(np.int64), mods_all), mods_all,
+                                     g), mods_all)[:level]
+    lhs = C.padd(kb, C.pmul(ka, s, qs), qs)
+    rhs = C.pmul(c, s_g, qs)
+    diff = E.crt_centered(C.intt(P, C.psub(lhs, rhs, qs), qs), qs)
+    assert max(abs(int(v)) for v in diff) < 2 ** 30
+
+
+def test_key_switch_at_every_level(small):
+    P, sk = small
+    rlk = C.keygen_from_seed(P, sk, 3, 0)
+    for level in range(1, P.L + 1):
+        z1, z2 = _z(30 + level, P.n // 2), _z(40 + level, P.n // 2)
+        # product scale 2^44 stays below q_0 / 2 ~ 2^49 at level 1
+        c1 = _enc(P, sk, z1, 2.0 ** 22, level, "lv1", level)
+        c2 = _enc(P, sk, z2, 2.0 ** 22, level, "lv2", level)
+        out = C.mul_relin(P, c1, c2, rlk)
+        np.testing.assert_allclose(C.decrypt(P, sk, out, 2.0 ** 44), z1 * z2, atol=2.0 ** -12)
+
+
+def test_rotate_conjugate_hoisted(small):
+    P, sk = small
+    level = 5
+    z = _z(50, P.n // 2)
+    ct = _enc(P, sk, z, 2.0 ** 40, level, "rot")
+    rs = [1, 2, 7, P.n // 2 - 1, P.n // 2, 0]
+    keys = {g: C.keygen_from_seed(P, sk, 3, g)
+            for g in {P.galois_elt(r) for r in rs if r % (P.n // 2)} | {P.conj_elt}}
+    hoisted = C.rotate_hoisted(P, ct, rs, keys)
+    for r, h in zip(rs, hoisted):
+        plain = C.rotate(P, ct, r, keys)
+        # key-switch noise ~ N sigma dnum (Q_j / P) per coefficient: 2^-22 here
+        np.testing.assert_allclose(C.decrypt(P, sk, plain, 2.0 ** 40), np.roll(z, -r),
+                                   atol=2.0 ** -20)
+        np.testing.assert_allclose(C.decrypt(P, sk, h, 2.0 ** 40), np.roll(z, -r),
+                                   atol=2.0 ** -20)
+        # centred basis conversion is an odd map, so it commutes with the
+        # signed coefficient permutation: both routes give the same residues
+        np.testing.assert_array_equal(plain, h)
+        if r % (P.n // 2) == 0:
+            np.testing.assert_array_equal(h, ct)
+    cj = C.conjugate(P, ct, keys)
+    np.testing.assert_allclose(C.decrypt(P, sk, cj, 2.0 ** 40), np.conj(z), atol=2.0 ** -20)
+    # rot_a o rot_b = rot_{a+b} in value
+    r12 = C.rotate(P, C.rotate(P, ct, 1, keys), 2, keys)
+    k3 = {P.galois_elt(3): C.keygen_from_seed(P, sk, 3, P.galois_elt(3))}
+    np.testing.assert_allclose(C.decrypt(P, sk, r12, 2.0 ** 40),
+                               C.decrypt(P, sk, C.rotate(P, ct, 3, k3), 2.0 ** 40),
+                               atol=2.0 ** -20)
+
+
+def test_p12_parameters_roundtrip():
+    """The N = 2^12 ring: alpha = 1, three single-prime digits."""
+    P = C.params_p12()
+    assert (P.L, P.alpha, P.dnum) == (3, 1, 3)
+    sk = C.secret_key(P, synth.secret(0, P.n))
+    z = _z(60, P.n // 2, complex_=False)
+    ct = _enc(P, sk, z, float(P.q[2]), 3, "p12")
+    keys = {P.galois_elt(1): C.keygen_from_seed(P, sk, 0, P.galois_elt(1))}
+    out = C.rotate_hoisted(P, ct, [1], keys)[0]
+    np.testing.assert_allclose(C.decrypt(P, sk, out, float(P.q[2])), np.roll(z, -1),
+                               atol=2.0 ** -20)

@@ -1,0 +1,136 @@
+"""Pins of the oracle's compositions: the decrypted projection equals the fp64
+matrix product and the decrypted scan-contract slice equals the fp64
+contraction, on small rings; the diagonal construction is checked in the slot
+domain against the matrix product with no encryption at all."""
+import numpy as np
+import pytest
+
+import synth
+from oracle import ckks as C
+from oracle import workloads as W
+
+
+def _keys(P, sk, seed, rots, conj=False):
+    elts = {P.galois_elt(r) for r in rots if r % (P.n // 2)}
+    if conj:
+        elts.add(P.conj_elt)
+    return {g: C.keygen_from_seed(P, sk, seed, g) for g in elts}
+
+
+def _slot_matvec(Wm, X, n_slots, seg_len, Cc, n1, n2, paired):
+    """The BSGS algebra evaluated on plain slot vectors."""
+    G = -(-Wm.shape[0] // Cc)
+    B = -(-Wm.shape[1] // Cc)
+    n_in = G // 2 if paired else G
+    xs = []
+    for u in range(n_in):
+        if paired:
+            xs.append(W.pack_input(X, n_slots, seg_len, Cc, 2 * u)
+                      + 1j * W.pack_input(X, n_slots, seg_len, Cc, 2 * u + 1))
+        else:
+            xs.append(W.pack_input(X, n_slots, seg_len, Cc, u).astype(complex))
+    ys = []
+    for b in range(B):
+        y = 0
+        for p in range(n2):
+            acc = 0
+            for u in range(n_in):
+                for q in range(n1):
+                    acc = acc + W.shift_segments(xs[u], q, seg_len) * W.bsgs_diagonal_slots(
+                        Wm, n_slots, seg_len, Cc, n1, b, p, u, q, paired)
+            y = y + W.shift_segments(acc, p * n1, seg_len)
+        if paired:
+            y = y + np.conj(y)
+        ys.append(y)
+    return ys
+
+
+@pytest.mark.parametrize("paired", [False, True])
+def test_bsgs_slot_algebra_is_the_matrix_product(paired):
+    n_slots, seg_len, Cc = 256, 8, 32
+    T, d_in, d_out = 8, 128, 64
+    X = synth.normal(1, "X", (T, d_in))
+    Wm = synth.normal(1, "W", (d_in, d_out), 0.1)
+    Y = X @ Wm
+    for n1, n2 in [(8, 4), (32, 1), (4, 8)]:
+        ys = _slot_matvec(Wm, X, n_slots, seg_len, Cc, n1, n2, paired)
+        for b, y in enumerate(ys):
+            r, s = W.segment_indices(n_slots, seg_len, Cc)
+            np.testing.assert_allclose(y.real, Y[r, b * Cc + s], atol=1e-12)
+            np.testing.assert_allclose(y.imag, 0, atol=1e-12)
+
+
+def test_replicated_diagonal_method_slot_algebra():
+    """cfg1 shape: U x with x replicated to fill the slots, n1 = d, n2 = 1."""
+    d, n_slots = 16, 128
+    U = synth.uniform_pm1(2, "U", (d, d))
+    x = synth.uniform_pm1(2, "x", d)
+    ys = _slot_matvec(U.T, x[None, :], n_slots, 1, d, d, 1, False)
+    np.testing.assert_allclose(ys[0].real, np.tile(U @ x, n_slots // d), atol=1e-12)
+
+
+def test_encrypted_bsgs_matvec_paired():
+    P = C.params_small(10, 50, 4, 2)
+    sk = C.secret_key(P, synth.secret(3, P.n))
+    n_slots, seg_len, Cc = P.n // 2, 16, 32
+    T, d_in, d_out = 16, 128, 64
+    n1, n2 = 8, 4
+    level = 4
+    X = synth.normal(3, "X", (T, d_in))
+    Wm = synth.normal(3, "W", (d_in, d_out), 0.02)
+    desc = W.MatvecDesc(level, d_in // Cc // 2, -(-d_out // Cc), n1, n2, seg_len, True, True)
+    keys = _keys(P, sk, 3, W.required_rotations(desc, n_slots), conj=True)
+    ins = []
+    for u in range(desc.n_in):
+        z = (W.pack_input(X, n_slots, seg_len, Cc, 2 * u)
+             + 1j * W.pack_input(X, n_slots, seg_len, Cc, 2 * u + 1))
+        a, e = synth.encrypt_draws(3, P.qs(level), P.n, "x", u)
+        ins.append(C.encrypt(P, sk, C.encode_plain(P, z, 2.0 ** 40, level), level, a, e))
+    ql = float(P.q[level - 1])
+    diag = lambda b, p, u, q: C.encode_plain(
+        P, W.bsgs_diagonal_slots(Wm, n_slots, seg_len, Cc, n1, b, p, u, q, True), ql, level)
+    outs = W.bsgs_matvec(P, desc, ins, diag, keys)
+    Y = X @ Wm
+    r, s = W.segment_indices(n_slots, seg_len, Cc)
+    for b, y in enumerate(outs):
+        assert y.shape[0] == level - 1
+        dec = C.decrypt(P, sk, y, 2.0 ** 40)
+        np.testing.assert_allclose(dec.real, Y[r, b * Cc + s], atol=2.0 ** -15)
+        np.testing.assert_allclose(dec.imag, 0, atol=2.0 ** -15)
+
+
+def test_scan_contract_slice_small():
+    P = C.params_small(10, 50, 4, 2)
+    sk = C.secret_key(P, synth.secret(4, P.n))
+    n_slots = P.n // 2
+    d_s, head_dim, K = 8, 16, 4
+    c_state = n_slots // d_s                      # channels per chunk
+    E = K * c_state
+    level = 4
+    z = synth.normal(4, "z", E // head_dim)
+    a = 1.0 / (1.0 + np.exp(z))                   # exp(-softplus(z))
+    Cv = synth.normal(4, "C", d_s)
+    H = synth.normal(4, "h", (E, d_s))
+    want = (a[np.arange(E) // head_dim][:, None] * H * Cv[None, :]).sum(axis=1)
+    rlk = C.keygen_from_seed(P, sk, 4, 0)
+    keys = _keys(P, sk, 4, [1, 2, 4], conj=True)
+    hs, ds, cs = [], [], []
+    j = np.arange(n_slots)
+    for k in range(K):
+        e_idx = k * c_state + j // d_s
+        i_idx = j % d_s
+        enc = lambda vals, scale, tag: C.encrypt(
+            P, sk, C.encode_plain(P, vals.astype(complex), scale, level), level,
+            *synth.encrypt_draws(4, P.qs(level), P.n, tag, k))
+        hs.append(enc(H[e_idx, i_idx], 2.0 ** 40, "h"))
+        ds.append(enc(a[e_idx // head_dim], float(P.q[3]), "a"))
+        cs.append(enc(Cv[i_idx], float(P.q[2]), "C"))
+    outs = W.scan_contract_token(P, hs, ds, cs, rlk, keys, d_s)
+    assert len(outs) == K
+    for l in range(K // 2):
+        for half in range(2):
+            k = 2 * l + half
+            dec = C.decrypt(P, sk, outs[2 * l + half], 2.0 * 2.0 ** 40)
+            assert outs[2 * l + half].shape[0] == 2
+            got = dec.real[:: d_s]
+            np.testing.assert_allclose(got, want[k * c_state:(k + 1) * c_state], atol=2.0 ** -15)
