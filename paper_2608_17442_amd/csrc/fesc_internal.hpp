@@ -1,0 +1,135 @@
+// Internal definitions shared by the HIP kernels and the host-side library.
+//
+// Residue arithmetic runs in IEEE fp64 on the VALU: every prime is below 2^50,
+// so residues, sums of a few residues and the exact low half of a product
+// (recovered with one FMA) are all exact integers in a double.  A modular
+// product x*w mod q with a precomputed w' = w/q (Shoup's method carried over
+// to floating point, cf. van der Hoeven, Lecerf and Quintin, "Modular SIMD
+// arithmetic in Mathemagix", ACM TOMS 2016) is
+//     h = x*w;  l = fma(x, w, -h);  c = rint(x*w');  r = fma(-c, q, h) + l
+// which is exact and lands in (-1.5q, 1.5q) for |x| < 3q.  Values inside a
+// kernel live in this signed, lazily reduced form; only stores to caller
+// memory are reduced to the canonical range [0, q) and converted to uint64.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+#include <map>
+#include <string>
+#include <vector>
+
+#include "fesc.h"
+
+namespace fesc {
+
+// ------------------------------------------------------------ device math
+
+struct PrimeK {        // per-prime constants read by kernels
+  double q;            // the prime
+  double qinv;         // fl(1/q)
+  double ninv, ninvp;  // N^-1 mod q and fl(N^-1 / q)
+  uint64_t qu;         // the prime as an integer
+  uint64_t pad[3];
+};
+
+__device__ __forceinline__ double mm_shoup(double x, double w, double wp, double q) {
+  double h = x * w;
+  double l = __builtin_fma(x, w, -h);
+  double c = __builtin_rint(x * wp);
+  double d = __builtin_fma(-c, q, h);
+  return d + l;
+}
+
+__device__ __forceinline__ double mm_var(double x, double y, double q, double qinv) {
+  double h = x * y;
+  double l = __builtin_fma(x, y, -h);
+  double c = __builtin_rint(h * qinv);
+  double d = __builtin_fma(-c, q, h);
+  return d + l;
+}
+
+// |x| < 2^52 -> congruent value in [-q/2 - eps, q/2 + eps]
+__device__ __forceinline__ double red_bal(double x, double q, double qinv) {
+  return __builtin_fma(-__builtin_rint(x * qinv), q, x);
+}
+
+// |x| < 2^52 -> canonical representative in [0, q)
+__device__ __forceinline__ double red_full(double x, double q, double qinv) {
+  double r = red_bal(x, q, qinv);
+  return r < 0.0 ? r + q : r;
+}
+
+// centred representative in (-q/2, q/2) of a canonical value in [0, q)
+__device__ __forceinline__ double center(double x, double q) {
+  return x > 0.5 * q ? x - q : x;
+}
+
+__device__ __forceinline__ double u2d(uint64_t x) {
+  return __builtin_fma((double)(uint32_t)(x >> 32), 4294967296.0, (double)(uint32_t)x);
+}
+
+// r: non-negative integer below 2^53
+__device__ __forceinline__ uint64_t d2u(double r) {
+  double hi = __builtin_floor(r * (1.0 / 4294967296.0));
+  double lo = __builtin_fma(-hi, 4294967296.0, r);
+  return ((uint64_t)(uint32_t)hi << 32) | (uint64_t)(uint32_t)lo;
+}
+
+// ------------------------------------------------------------- host side
+
+#define FESC_MAX_PRIMES 64
+
+struct Context {
+  int device = 0;
+  uint32_t log_n = 0, n = 0;
+  uint32_t L = 0, alpha = 0, dnum = 0;
+  std::vector<uint64_t> primes;   // ext order: q_0..q_{L-1}, p_0..p_{alpha-1}
+  std::vector<uint64_t> psi;      // smallest primitive 2N-th root per prime
+  PrimeK* d_pk = nullptr;         // [L+alpha]
+  double2* d_tw_fwd = nullptr;    // [L+alpha][N] {psi^brv(i), /q}
+  double2* d_tw_inv = nullptr;    // [L+alpha][N] {psi^-brv(i), /q}
+  // keys: Galois element (0 = relinearisation) -> device [dnum][L+alpha][2][N]
+  std::map<uint32_t, uint64_t*> keys;
+  // basis-conversion constant tables, built on first use per (level, kind)
+  std::map<uint64_t, void*> tables;
+  // scratch (grown on demand, freed with the context)
+  void* scratch = nullptr;
+  size_t scratch_bytes = 0;
+  hipStream_t stream = nullptr;   // default stream when callers pass null
+
+  size_t ext_count() const { return primes.size(); }
+};
+
+// thread-local error message, set by fail()
+int fail(int code, const std::string& msg);
+int hip_check(hipError_t e, const char* what);
+
+void* scratch_get(Context* c, size_t bytes, int* err);
+
+// host number theory
+uint64_t h_mulmod(uint64_t a, uint64_t b, uint64_t m);
+uint64_t h_powmod(uint64_t a, uint64_t e, uint64_t m);
+uint64_t h_inv(uint64_t a, uint64_t p);
+bool h_is_prime(uint64_t n);
+uint64_t h_min_root(uint64_t q, uint32_t log_n);
+
+// kernel launchers (ntt.hip)
+hipError_t launch_ntt(const Context* c, uint64_t* d, uint32_t batch, size_t batch_stride,
+                      uint32_t limbs, size_t limb_stride, uint32_t prime0, bool inverse,
+                      hipStream_t s);
+
+}  // namespace fesc
+
+// The opaque handle of the C ABI is the context itself.
+struct fesc_ctx : public fesc::Context {};
+
+namespace fesc {
+int create(const fesc_params* p, fesc_ctx** out);
+void destroy(Context* c);
+const char* last_error();
+hipError_t launch_mac(const Context* c, const uint64_t* a, const uint64_t* b, uint64_t* out,
+                      uint32_t pairs, size_t pair_stride, uint32_t limbs, uint32_t prime0,
+                      hipStream_t s);
+}  // namespace fesc

@@ -1,0 +1,147 @@
+"""GPU parity of the transforms and the Hadamard multiply-accumulate against
+the oracle: bit-exact residues, every row."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+import synth.workloads as WL
+from oracle import ckks as C
+from tests.gpu_helpers import first_mismatch, need_gpu, step, to_dev, to_host
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    need_gpu()
+
+
+def _ctx(P):
+    from paper_2608_17442_amd import fesc as F
+    return F.Context(P.log_n, P.q, P.p)
+
+
+def test_context_psi_matches_oracle():
+    for P in [C.params_p12(), C.params_p16()]:
+        step(f"ctx psi log_n={P.log_n}")
+        ctx = _ctx(P)
+        for i, m in enumerate(P.q + P.p):
+            assert ctx.psi(i) == P.psi[m]
+
+
+@pytest.mark.parametrize("log_n", [12, 13, 14, 15, 16])
+def test_ntt_roundtrip_all_sizes(log_n):
+    P = C.params_small(log_n, 50, 3, 2)
+    ctx = _ctx(P)
+    mods = P.ext(P.L)            # q0 q1 q2 p0 p1
+    batch, limbs, prime0 = 3, 4, 1
+    rows = mods[prime0:prime0 + limbs]
+    a = np.stack([synth.uniform_residues(10 + log_n, "ntt", rows, P.n, b) for b in range(batch)])
+    a[0, 0, :5] = [0, 1, rows[0] - 1, 2, rows[0] - 2]
+    want = np.stack([C.ntt(P, a[b], rows) for b in range(batch)])
+    d = to_dev(a)
+    step(f"ntt_fwd log_n={log_n}")
+    ctx.ntt_fwd(d, batch, limbs * P.n, limbs, P.n, prime0)
+    got = to_host(d)
+    assert np.array_equal(got, want), first_mismatch(got, want)
+    step(f"ntt_inv log_n={log_n}")
+    ctx.ntt_inv(d, batch, limbs * P.n, limbs, P.n, prime0)
+    got = to_host(d)
+    assert np.array_equal(got, a), first_mismatch(got, a)
+    # inverse of arbitrary residues against the oracle's inverse
+    wantinv = np.stack([C.intt(P, a[b], rows) for b in range(batch)])
+    d = to_dev(a)
+    ctx.ntt_inv(d, batch, limbs * P.n, limbs, P.n, prime0)
+    got = to_host(d)
+    assert np.array_equal(got, wantinv), first_mismatch(got, wantinv)
+
+
+def test_ntt_strided_rows_leave_gaps_untouched():
+    P = C.params_small(14, 50, 4, 1)
+    ctx = _ctx(P)
+    n = P.n
+    limbs, batch = 2, 2
+    limb_stride, batch_stride = n + 512, 3 * (n + 512)
+    buf = np.full(batch * batch_stride, 7, dtype=np.uint64)
+    rows = P.q[1:3]
+    data = {}
+    for b in range(batch):
+        for i in range(limbs):
+            r = synth.uniform_residues(3, "gap", [rows[i]], n, b, i)[0]
+            o = b * batch_stride + i * limb_stride
+            buf[o:o + n] = r
+            data[(b, i)] = r
+    d = to_dev(buf)
+    step("ntt_fwd strided")
+    ctx.ntt_fwd(d, batch, batch_stride, limbs, limb_stride, 1)
+    got = to_host(d)
+    mask = np.ones_like(buf, dtype=bool)
+    for (b, i), r in data.items():
+        o = b * batch_stride + i * limb_stride
+        mask[o:o + n] = False
+        want = C.ntt(P, r[None], [rows[i]])[0]
+        assert np.array_equal(got[o:o + n], want)
+    assert np.all(got[mask] == 7)
+
+
+def test_bad_prime_range_is_rejected_before_launch():
+    from paper_2608_17442_amd import fesc as F
+    P = C.params_small(12, 50, 2, 1)
+    ctx = _ctx(P)
+    d = to_dev(np.zeros(4 * P.n, dtype=np.uint64))
+    with pytest.raises(F.FescError) as e:
+        ctx.ntt_fwd(d, 1, 0, 4, P.n, 0)   # only 3 primes
+    assert e.value.code == -1
+    assert np.all(to_host(d) == 0)
+
+
+@pytest.mark.parametrize("pairs", [1, 3, 8])
+def test_mac_small(pairs):
+    P = C.params_small(12, 50, 3, 1)
+    ctx = _ctx(P)
+    mods = P.q
+    a = np.stack([synth.uniform_residues(5, "macA", mods, P.n, j) for j in range(pairs)])
+    b = np.stack([synth.uniform_residues(5, "macB", mods, P.n, j) for j in range(pairs)])
+    a[0, :, :3] = np.array(mods, dtype=np.uint64)[:, None] - 1
+    b[0, :, :3] = np.array(mods, dtype=np.uint64)[:, None] - 1
+    want = np.zeros((len(mods), P.n), dtype=np.uint64)
+    for j in range(pairs):
+        want = C.padd(want, C.pmul(a[j], b[j], mods), mods)
+    out = torch.zeros(len(mods) * P.n, dtype=torch.int64, device="cuda")
+    step(f"mac pairs={pairs}")
+    ctx.mac(to_dev(a), to_dev(b), out, pairs, len(mods) * P.n, len(mods), 0)
+    got = to_host(out).reshape(len(mods), P.n)
+    assert np.array_equal(got, want), first_mismatch(got, want)
+
+
+def test_cfg2_full_size():
+    """64 polynomials x 24 limbs x 2^16: forward transform, inverse, and the
+    64-pair multiply-accumulate, compared on every residue."""
+    P = C.params_p16()
+    ctx = _ctx(P)
+    mods = P.q
+    B, Lm, n = WL.CFG2["batch"], WL.CFG2["limbs"], P.n
+    A = WL.cfg2_polys("A", mods, n, B)
+    Bm = WL.cfg2_polys("B", mods, n, B)
+    d = to_dev(A)
+    step("cfg2 ntt_fwd 64x24x2^16")
+    ctx.ntt_fwd(d, B, Lm * n, Lm, n, 0)
+    got = to_host(d)
+    want = C.ntt(P, A.reshape(B * Lm, n), mods * B).reshape(B, Lm, n)
+    assert np.array_equal(got, want), first_mismatch(got, want)
+    del want
+    step("cfg2 mac 64 pairs")
+    out = torch.zeros(Lm * n, dtype=torch.int64, device="cuda")
+    db = to_dev(Bm)
+    ctx.mac(d, db, out, B, Lm * n, Lm, 0)
+    gotm = to_host(out).reshape(Lm, n)
+    wantm = np.zeros((Lm, n), dtype=np.uint64)
+    from oracle import _native as nat
+    nat.lib().or_mac_rows(nat.u64p(np.ascontiguousarray(got)), nat.u64p(Bm),
+                          nat.u64p(wantm), B, Lm, n, nat.u64p(nat.moduli(mods)))
+    assert np.array_equal(gotm, wantm), first_mismatch(gotm, wantm)
+    step("cfg2 ntt_inv 64x24x2^16")
+    ctx.ntt_inv(d, B, Lm * n, Lm, n, 0)
+    back = to_host(d)
+    assert np.array_equal(back, A), first_mismatch(back, A)

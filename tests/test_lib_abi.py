@@ -1,0 +1,54 @@
+"""CPU checks of the C ABI: the library loads, exports every symbol that
+include/fesc.h declares, and its host-side parameter helpers agree with the
+oracle's (no compute call needs a GPU here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fesc.h")
+LIB = os.path.join(ROOT, "paper_2608_17442_amd", "libfesc.so")
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fesc_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LIB):
+        from paper_2608_17442_amd import build
+        build.build()
+    return ctypes.CDLL(LIB)
+
+
+def test_header_declares_the_boundary():
+    syms = declared_symbols()
+    for name in ["fesc_ntt_fwd", "fesc_ntt_inv", "fesc_mac"]:
+        assert name in syms
+
+
+def test_every_declared_symbol_is_exported(lib):
+    missing = [s for s in declared_symbols() if not hasattr(lib, s)]
+    assert not missing, missing
+
+
+def test_prime_search_and_roots_match_oracle():
+    from oracle import ckks as C
+    from paper_2608_17442_amd import fesc as F
+    for log_n, bits, count in [(12, 36, 4), (16, 50, 32), (13, 45, 6)]:
+        ps = F.find_primes(log_n, bits, count)
+        assert ps == C.find_primes(log_n, bits, count)
+        for q in ps:
+            assert F.root_of_unity(log_n, q) == C.min_psi(q, log_n)
+
+
+def test_host_helpers_reject_bad_input():
+    from paper_2608_17442_amd import fesc as F
+    with pytest.raises(F.FescError) as e:
+        F.root_of_unity(12, 1000003)   # prime, but not 1 mod 2N
+    assert e.value.code == -1
