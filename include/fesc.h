@@ -99,6 +99,132 @@ int fesc_mac(fesc_ctx* ctx, const uint64_t* a, const uint64_t* b, uint64_t* out,
              uint32_t pairs, size_t pair_stride, uint32_t limbs, uint32_t prime0,
              void* stream);
 
+/* ------------------------------------------------------------------------
+ * Ciphertext operations (paper Sec. 4.1 table: add, ptmul, ctmul, rot, conj;
+ * Sec. 2.1: rescale drops one prime).  `level` l counts the primes in use
+ * (1 <= l <= L); FESC_ERR_LEVEL otherwise.  Unless stated, `out` may alias an
+ * input (element-by-element operations).
+ * ------------------------------------------------------------------------ */
+
+/* add: out = a + b;  sub: out = a - b  (ciphertexts [l][2][N]). */
+int fesc_add(fesc_ctx* ctx, const uint64_t* a, const uint64_t* b, uint64_t* out,
+             uint32_t level, void* stream);
+int fesc_sub(fesc_ctx* ctx, const uint64_t* a, const uint64_t* b, uint64_t* out,
+             uint32_t level, void* stream);
+
+/* ptmul: out = (c0 * pt, c1 * pt), pt a plaintext with at least l limbs
+ * (its first l limbs are used).  The scale of the result is the product of
+ * the scales; no rescale. */
+int fesc_mul_plain(fesc_ctx* ctx, const uint64_t* ct, const uint64_t* pt, uint64_t* out,
+                   uint32_t level, void* stream);
+
+/* out = in * X^k (k taken mod 2N).  X^(N/2) multiplies every slot by i, so
+ * k = N/2 and k = 3N/2 are the exact plaintext constants i and -i. */
+int fesc_mul_monomial(fesc_ctx* ctx, const uint64_t* in, uint64_t* out, uint32_t level,
+                      uint32_t k, void* stream);
+
+/* ctmul with relinearisation: tensor (a0 b0, a0 b1 + a1 b0, a1 b1), then a
+ * hybrid key switch of the s^2 part with the relinearisation key (Galois
+ * element 0).  No rescale.  FESC_ERR_NO_KEY without the key. */
+int fesc_mul_relin(fesc_ctx* ctx, const uint64_t* a, const uint64_t* b, uint64_t* out,
+                   uint32_t level, void* stream);
+
+/* Rescale: out = round(in / q_{l-1}) at level l-1 (written as [l-1][2][N]);
+ * l >= 2.  Computed as (c_i - [c mod q_{l-1}]_centred) * q_{l-1}^-1 mod q_i. */
+int fesc_rescale(fesc_ctx* ctx, const uint64_t* in, uint64_t* out, uint32_t level,
+                 void* stream);
+
+/* Galois element of a rotation: 5^(step mod N/2) mod 2N (1 for the identity),
+ * 2N-1 for step == FESC_CONJ. */
+#define FESC_CONJ INT32_MIN
+int fesc_galois_element(const fesc_ctx* ctx, int32_t step, uint32_t* elt);
+
+/* rot: out = rho(in; step), the left rotation of the N/2 slots by `step`
+ * (negative steps rotate right); step = 0 mod N/2 is an exact copy with no
+ * key switch; step == FESC_CONJ conjugates.  The automorphism is applied as
+ * an evaluation-form index permutation and the c1 part is key-switched with
+ * the Galois key sigma_g(s) -> s (hybrid, centred basis conversion).
+ * FESC_ERR_NO_KEY without the key.  out may alias in. */
+int fesc_rotate(fesc_ctx* ctx, const uint64_t* in, uint64_t* out, uint32_t level, int32_t step,
+                void* stream);
+
+/* Hoisted rotations: `count` rotations of one ciphertext sharing a single
+ * ModUp; steps is a host array, outs a host array of device pointers (each a
+ * [l][2][N] ciphertext).  Results equal fesc_rotate residue for residue. */
+int fesc_rotate_hoisted(fesc_ctx* ctx, const uint64_t* in, uint32_t count, const int32_t* steps,
+                        uint64_t* const* outs, uint32_t level, void* stream);
+
+/* Switching-key generation on the device from caller-drawn randomness:
+ * s: int8[N] ternary secret coefficients; a: uint64[dnum][L+alpha][N] uniform
+ * residues (evaluation form); e: int64[dnum][N] error coefficients.  For
+ * digit j and extended prime i:
+ *   b_j = -a_j s + e_j + [P]_{q_i} s'   (q_i in digit j)
+ *   b_j = -a_j s + e_j                  (otherwise)
+ * with s' = s^2 (galois_elt == 0, relinearisation) or sigma_g(s).  The key is
+ * kept in context memory (allocated on first use, replaced on repeat). */
+int fesc_keygen(fesc_ctx* ctx, uint32_t galois_elt, const int8_t* s, const uint64_t* a,
+                const int64_t* e, void* stream);
+
+/* Copy a key (layout above, device memory) into / out of the context. */
+int fesc_key_load(fesc_ctx* ctx, uint32_t galois_elt, const uint64_t* key, void* stream);
+int fesc_key_store(fesc_ctx* ctx, uint32_t galois_elt, uint64_t* key, void* stream);
+
+/* Secret-key encryption from caller-drawn randomness: c1 = a,
+ * c0 = -a s + m + e.  s: int8[N]; m: int64[N] plaintext coefficients;
+ * a: uint64[l][N] uniform (evaluation form); e: int64[N]. */
+int fesc_encrypt_sk(fesc_ctx* ctx, const int8_t* s, const int64_t* m, const uint64_t* a,
+                    const int64_t* e, uint64_t* ct, uint32_t level, void* stream);
+
+/* Plaintext [l][N] from signed integer coefficients (reduce, transform). */
+int fesc_plain_from_coeffs(fesc_ctx* ctx, const int64_t* m, uint64_t* pt, uint32_t level,
+                           void* stream);
+
+/* ------------------------------------------------------------------------
+ * Plaintext-matrix x ciphertext projection (paper Appendix "Projection
+ * Kernel Breakdown": segment view idx(r, s) = s * unit + r, whole-segment
+ * shift Phi^d = rotation by d * unit slots, BSGS with n1 * n2 = C):
+ *     c~_{b,p} = sum_{u < n_in} sum_{q < n1} Phi^q(x~_u) * D~[b][p][u][q]
+ *     y_b      = sum_{p < n2} Phi^(p n1)(c~_{b,p})
+ *     y_b     += conj(y_b)            if real_extract
+ *     y_b      = rescale(y_b)         if rescale  (output at level - 1)
+ * Baby steps are hoisted (one ModUp per input); giant steps and the
+ * conjugation are single key switches.  With real_extract the caller folds
+ * the 1/2 of the real-part extraction into the diagonals.
+ * ------------------------------------------------------------------------ */
+typedef struct fesc_matvec_desc {
+  uint32_t level;        /* level of the inputs (and diagonals) */
+  uint32_t n_in;         /* input ciphertexts x~_u */
+  uint32_t n_out;        /* output ciphertexts y_b */
+  uint32_t n1, n2;       /* baby and giant steps */
+  uint32_t unit;         /* slots per segment */
+  uint32_t real_extract; /* 0 or 1 */
+  uint32_t rescale;      /* 0 or 1 */
+} fesc_matvec_desc;
+
+typedef struct fesc_matvec_plan fesc_matvec_plan;
+
+/* Plan: `diags` is a host array of n_out*n2*n_in*n1 device pointers to
+ * plaintexts ([level][N], evaluation form), indexed [b][p][u][q]; they must
+ * stay valid for the plan's lifetime.  Allocates the plan's workspace (the
+ * baby-step and partial-sum ciphertexts).  FESC_ERR_NO_KEY if a rotation or
+ * conjugation key the schedule needs is not loaded. */
+int fesc_matvec_plan_create(fesc_ctx* ctx, const fesc_matvec_desc* desc,
+                            const uint64_t* const* diags, fesc_matvec_plan** plan);
+void fesc_matvec_plan_destroy(fesc_matvec_plan* plan);
+
+/* in: host array of n_in device ciphertexts [level][2][N]; out: host array of
+ * n_out device ciphertexts ([level-1][2][N] with rescale, else [level][2][N]).
+ * Outputs must not alias inputs. */
+int fesc_ptct_matvec(fesc_ctx* ctx, fesc_matvec_plan* plan, const uint64_t* const* in,
+                     uint64_t* const* out, void* stream);
+
+/* Host helper: CKKS encoding of n = N/2 complex slots (re, im host arrays;
+ * im may be NULL) at scale Delta into int64 coefficients, rounded half away
+ * from zero; slot j is the evaluation at exp(i pi 5^j / N).  FESC_ERR_ARG if
+ * a coefficient does not fit in int64. */
+int fesc_encode(uint32_t log_n, const double* re, const double* im, double scale,
+                int64_t* coeffs);
+
 #ifdef __cplusplus
 }
 #endif

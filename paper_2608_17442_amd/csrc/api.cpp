@@ -86,3 +86,163 @@ int fesc_mac(fesc_ctx* ctx, const uint64_t* a, const uint64_t* b, uint64_t* out,
 }
 
 }  // extern "C"
+
+// ------------------------------------------------------ ciphertext operations
+
+namespace fesc {
+int op_rotate_many(Context* c, const uint64_t* in, uint32_t count, const int32_t* steps,
+                   uint64_t* const* outs, uint32_t level, hipStream_t s);
+int op_mul_relin(Context* c, const uint64_t* a, const uint64_t* b, uint64_t* out,
+                 uint32_t level, hipStream_t s);
+int op_rescale(Context* c, const uint64_t* in, uint64_t* out, uint32_t level, hipStream_t s);
+int op_keygen(Context* c, uint32_t galois, const int8_t* sk, const uint64_t* a, const int64_t* e,
+              hipStream_t s);
+int op_encrypt(Context* c, const int8_t* sk, const int64_t* m, const uint64_t* a,
+               const int64_t* e, uint64_t* ct, uint32_t level, hipStream_t s);
+int op_plain_from_coeffs(Context* c, const int64_t* m, uint64_t* pt, uint32_t level,
+                         hipStream_t s);
+uint32_t galois_of_step(const Context* c, int32_t step);
+int encode(uint32_t log_n, const double* re, const double* im, double scale, int64_t* out);
+}  // namespace fesc
+
+#include "ops.hpp"
+
+namespace {
+
+int check_level(const fesc_ctx* c, uint32_t level, uint32_t min_level = 1) {
+  if (!c) return fail(FESC_ERR_ARG, "null context");
+  if (level < min_level || level > c->L)
+    return fail(FESC_ERR_LEVEL, "level " + std::to_string(level) + " outside [" +
+                                    std::to_string(min_level) + ", " + std::to_string(c->L) + "]");
+  return FESC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int fesc_add(fesc_ctx* ctx, const uint64_t* a, const uint64_t* b, uint64_t* out, uint32_t level,
+             void* stream) {
+  int rc = check_level(ctx, level);
+  if (rc) return rc;
+  if (!a || !b || !out) return fail(FESC_ERR_ARG, "null buffer");
+  return hip_check(k_binary_launch(ctx, a, b, out, 2 * level, 1, 0, S(stream)), "add");
+}
+
+int fesc_sub(fesc_ctx* ctx, const uint64_t* a, const uint64_t* b, uint64_t* out, uint32_t level,
+             void* stream) {
+  int rc = check_level(ctx, level);
+  if (rc) return rc;
+  if (!a || !b || !out) return fail(FESC_ERR_ARG, "null buffer");
+  return hip_check(k_binary_launch(ctx, a, b, out, 2 * level, 1, 1, S(stream)), "sub");
+}
+
+int fesc_mul_plain(fesc_ctx* ctx, const uint64_t* ct, const uint64_t* pt, uint64_t* out,
+                   uint32_t level, void* stream) {
+  int rc = check_level(ctx, level);
+  if (rc) return rc;
+  if (!ct || !pt || !out) return fail(FESC_ERR_ARG, "null buffer");
+  return hip_check(k_mul_plain_launch(ctx, ct, pt, out, level, S(stream)), "mul_plain");
+}
+
+int fesc_mul_monomial(fesc_ctx* ctx, const uint64_t* in, uint64_t* out, uint32_t level,
+                      uint32_t k, void* stream) {
+  int rc = check_level(ctx, level);
+  if (rc) return rc;
+  if (!in || !out) return fail(FESC_ERR_ARG, "null buffer");
+  return hip_check(k_monomial_launch(ctx, in, out, level, k % (2 * ctx->n), S(stream)),
+                   "mul_monomial");
+}
+
+int fesc_mul_relin(fesc_ctx* ctx, const uint64_t* a, const uint64_t* b, uint64_t* out,
+                   uint32_t level, void* stream) {
+  int rc = check_level(ctx, level);
+  if (rc) return rc;
+  if (!a || !b || !out) return fail(FESC_ERR_ARG, "null buffer");
+  return op_mul_relin(ctx, a, b, out, level, S(stream));
+}
+
+int fesc_rescale(fesc_ctx* ctx, const uint64_t* in, uint64_t* out, uint32_t level,
+                 void* stream) {
+  int rc = check_level(ctx, level, 2);
+  if (rc) return rc;
+  if (!in || !out) return fail(FESC_ERR_ARG, "null buffer");
+  return op_rescale(ctx, in, out, level, S(stream));
+}
+
+int fesc_galois_element(const fesc_ctx* ctx, int32_t step, uint32_t* elt) {
+  if (!ctx || !elt) return fail(FESC_ERR_ARG, "null argument");
+  *elt = galois_of_step(ctx, step);
+  return FESC_OK;
+}
+
+int fesc_rotate(fesc_ctx* ctx, const uint64_t* in, uint64_t* out, uint32_t level, int32_t step,
+                void* stream) {
+  int rc = check_level(ctx, level);
+  if (rc) return rc;
+  if (!in || !out) return fail(FESC_ERR_ARG, "null buffer");
+  uint64_t* outs[1] = {out};
+  return op_rotate_many(ctx, in, 1, &step, outs, level, S(stream));
+}
+
+int fesc_rotate_hoisted(fesc_ctx* ctx, const uint64_t* in, uint32_t count, const int32_t* steps,
+                        uint64_t* const* outs, uint32_t level, void* stream) {
+  int rc = check_level(ctx, level);
+  if (rc) return rc;
+  if (!in || !steps || !outs || count == 0) return fail(FESC_ERR_ARG, "bad hoisted arguments");
+  for (uint32_t r = 0; r < count; ++r)
+    if (!outs[r]) return fail(FESC_ERR_ARG, "null output");
+  return op_rotate_many(ctx, in, count, steps, outs, level, S(stream));
+}
+
+int fesc_keygen(fesc_ctx* ctx, uint32_t galois_elt, const int8_t* s, const uint64_t* a,
+                const int64_t* e, void* stream) {
+  if (!ctx || !s || !a || !e) return fail(FESC_ERR_ARG, "null argument");
+  if (galois_elt != 0 && (galois_elt % 2 == 0 || galois_elt >= 2 * ctx->n || galois_elt == 1))
+    return fail(FESC_ERR_ARG, "Galois element must be odd, in (1, 2N)");
+  return op_keygen(ctx, galois_elt, s, a, e, S(stream));
+}
+
+int fesc_key_load(fesc_ctx* ctx, uint32_t galois_elt, const uint64_t* key, void* stream) {
+  if (!ctx || !key) return fail(FESC_ERR_ARG, "null argument");
+  const size_t bytes = (size_t)ctx->dnum * (ctx->L + ctx->alpha) * 2 * ctx->n * 8;
+  uint64_t*& dst = ctx->keys[galois_elt];
+  if (!dst && hipMalloc(&dst, bytes) != hipSuccess) {
+    ctx->keys.erase(galois_elt);
+    return fail(FESC_ERR_OOM, "key allocation failed");
+  }
+  return hip_check(hipMemcpyAsync(dst, key, bytes, hipMemcpyDeviceToDevice, S(stream)),
+                   "key_load");
+}
+
+int fesc_key_store(fesc_ctx* ctx, uint32_t galois_elt, uint64_t* key, void* stream) {
+  if (!ctx || !key) return fail(FESC_ERR_ARG, "null argument");
+  auto it = ctx->keys.find(galois_elt);
+  if (it == ctx->keys.end()) return fail(FESC_ERR_NO_KEY, "no such key");
+  const size_t bytes = (size_t)ctx->dnum * (ctx->L + ctx->alpha) * 2 * ctx->n * 8;
+  return hip_check(hipMemcpyAsync(key, it->second, bytes, hipMemcpyDeviceToDevice, S(stream)),
+                   "key_store");
+}
+
+int fesc_encrypt_sk(fesc_ctx* ctx, const int8_t* s, const int64_t* m, const uint64_t* a,
+                    const int64_t* e, uint64_t* ct, uint32_t level, void* stream) {
+  int rc = check_level(ctx, level);
+  if (rc) return rc;
+  if (!s || !m || !a || !e || !ct) return fail(FESC_ERR_ARG, "null buffer");
+  return op_encrypt(ctx, s, m, a, e, ct, level, S(stream));
+}
+
+int fesc_plain_from_coeffs(fesc_ctx* ctx, const int64_t* m, uint64_t* pt, uint32_t level,
+                           void* stream) {
+  int rc = check_level(ctx, level);
+  if (rc) return rc;
+  if (!m || !pt) return fail(FESC_ERR_ARG, "null buffer");
+  return op_plain_from_coeffs(ctx, m, pt, level, S(stream));
+}
+
+int fesc_encode(uint32_t log_n, const double* re, const double* im, double scale,
+                int64_t* coeffs) {
+  return encode(log_n, re, im, scale, coeffs);
+}
+
+}  // extern "C"

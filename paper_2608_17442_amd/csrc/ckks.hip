@@ -1,0 +1,293 @@
+// Ciphertext-level elementwise kernels (evaluation form): add / sub, plaintext
+// product, tensor product, monomial product, Galois permutation, lifting of
+// signed integer coefficients, and the combine steps of key generation,
+// encryption and rescaling.
+//
+// Ciphertext layout [l][2][N]: row r = 2*i + t holds component t of limb i,
+// so the prime of row r is r >> 1.
+#include "fesc_internal.hpp"
+#include "ops.hpp"
+
+namespace fesc {
+
+namespace {
+
+constexpr int kThreads = 256;
+
+__device__ __forceinline__ double ld(const uint64_t* p) { return u2d(*p); }
+__device__ __forceinline__ void st(uint64_t* p, double v, double q, double qinv) {
+  *p = d2u(red_full(v, q, qinv));
+}
+
+// index of the evaluation point whose g-th power is the point of index jp:
+// sigma_g(a)[jp] = a[galois_src(jp)]  (g odd, < 2N)
+__device__ __forceinline__ uint32_t galois_src(uint32_t jp, uint32_t g, uint32_t log_n) {
+  const uint32_t b = __builtin_bitreverse32(jp) >> (32 - log_n);
+  const uint32_t e = (g * (2u * b + 1u)) & ((2u << log_n) - 1u);  // wraps mod 2^32 first
+  return __builtin_bitreverse32((e - 1u) >> 1) >> (32 - log_n);
+}
+
+// ---------------------------------------------------------------- binary
+
+// op 0: a + b, op 1: a - b, op 2: a * b (all rows), prime of row r = r >> shift
+__global__ __launch_bounds__(kThreads) void k_binary(const uint64_t* __restrict__ a,
+                                                     const uint64_t* __restrict__ b,
+                                                     uint64_t* out, uint32_t n, uint32_t shift,
+                                                     int op, const PrimeK* __restrict__ pk) {
+  const uint32_t r = blockIdx.y;
+  const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
+  if (k >= n) return;
+  const PrimeK P = pk[r >> shift];
+  const size_t o = (size_t)r * n + k;
+  const double x = ld(a + o), y = ld(b + o);
+  double v = op == 0 ? x + y : op == 1 ? x - y : mm_var(x, y, P.q, P.qinv);
+  st(out + o, v, P.q, P.qinv);
+}
+
+// out[i][t] = ct[i][t] * pt[i]
+__global__ __launch_bounds__(kThreads) void k_mul_plain(const uint64_t* ct,
+                                                        const uint64_t* __restrict__ pt,
+                                                        uint64_t* out, uint32_t n,
+                                                        const PrimeK* __restrict__ pk) {
+  const uint32_t i = blockIdx.y;
+  const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
+  if (k >= n) return;
+  const PrimeK P = pk[i];
+  const double w = ld(pt + (size_t)i * n + k);
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const size_t o = ((size_t)2 * i + t) * n + k;
+    st(out + o, mm_var(ld(ct + o), w, P.q, P.qinv), P.q, P.qinv);
+  }
+}
+
+// (d0, d1) into ct layout `d01`, d2 into poly layout `d2`
+__global__ __launch_bounds__(kThreads) void k_tensor(const uint64_t* a, const uint64_t* b,
+                                                     uint64_t* __restrict__ d01,
+                                                     uint64_t* __restrict__ d2, uint32_t n,
+                                                     const PrimeK* __restrict__ pk) {
+  const uint32_t i = blockIdx.y;
+  const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
+  if (k >= n) return;
+  const PrimeK P = pk[i];
+  const size_t o0 = (size_t)2 * i * n + k, o1 = o0 + n;
+  const double a0 = ld(a + o0), a1 = ld(a + o1), b0 = ld(b + o0), b1 = ld(b + o1);
+  st(d01 + o0, mm_var(a0, b0, P.q, P.qinv), P.q, P.qinv);
+  st(d01 + o1, mm_var(a0, b1, P.q, P.qinv) + mm_var(a1, b0, P.q, P.qinv), P.q, P.qinv);
+  st(d2 + (size_t)i * n + k, mm_var(a1, b1, P.q, P.qinv), P.q, P.qinv);
+}
+
+// multiplication by X^m: the evaluation at psi^(2 brv(j) + 1) scales by
+// psi^e, e = (2 brv(j) + 1) m mod 2N; psi^e = tw[brv(e)] for e < N and
+// -tw[brv(e - N)] otherwise (tw = forward twiddle table).
+__global__ __launch_bounds__(kThreads) void k_monomial(const uint64_t* in, uint64_t* out,
+                                                       uint32_t log_n, uint32_t m,
+                                                       const PrimeK* __restrict__ pk,
+                                                       const double2* __restrict__ twf) {
+  const uint32_t n = 1u << log_n;
+  const uint32_t r = blockIdx.y, i = r >> 1;
+  const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
+  if (k >= n) return;
+  const PrimeK P = pk[i];
+  const uint32_t b = __builtin_bitreverse32(k) >> (32 - log_n);
+  const uint32_t e = ((2u * b + 1u) * m) & (2u * n - 1u);
+  const bool neg = e >= n;
+  const uint32_t eb = __builtin_bitreverse32(neg ? e - n : e) >> (32 - log_n);
+  const double2 w = twf[(size_t)i * n + eb];
+  const size_t o = (size_t)r * n + k;
+  double v = mm_shoup(ld(in + o), w.x, w.y, P.q);
+  st(out + o, neg ? -v : v, P.q, P.qinv);
+}
+
+// out[row][k] = in[row][galois_src(k)]; rows share one prime list (prime of
+// row r = prime0 + r).  out must not alias in.
+__global__ __launch_bounds__(kThreads) void k_galois(const uint64_t* __restrict__ in,
+                                                     uint64_t* __restrict__ out,
+                                                     uint32_t log_n, uint32_t g) {
+  const uint32_t n = 1u << log_n;
+  const uint32_t r = blockIdx.y;
+  const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
+  if (k >= n) return;
+  out[(size_t)r * n + k] = in[(size_t)r * n + galois_src(k, g, log_n)];
+}
+
+// out[r][k] = x[k] mod prime(r) for signed coefficients; x is int64 (or int8
+// when x8 != null).  Row r uses prime prime0 + r for r < split, else
+// prime1 + (r - split).
+__global__ __launch_bounds__(kThreads) void k_lift(const int64_t* __restrict__ x,
+                                                   const int8_t* __restrict__ x8,
+                                                   uint64_t* __restrict__ out, uint32_t n,
+                                                   uint32_t prime0, uint32_t split,
+                                                   uint32_t prime1,
+                                                   const PrimeK* __restrict__ pk) {
+  const uint32_t r = blockIdx.y;
+  const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
+  if (k >= n) return;
+  const PrimeK P = pk[r < split ? prime0 + r : prime1 + (r - split)];
+  const int64_t v = x8 ? (int64_t)x8[k] : x[k];
+  // exact: |v| < 2^63 -> split into hi * 2^32 + lo, reduce each part
+  const double hi = (double)(int32_t)(v >> 32);
+  const double lo = (double)(uint32_t)(v & 0xffffffffu);
+  const double two32 = red_full(4294967296.0, P.q, P.qinv);
+  const double t = mm_var(red_full(hi, P.q, P.qinv), two32, P.q, P.qinv);
+  st(out + (size_t)r * n + k, t + lo, P.q, P.qinv);
+}
+
+// key[j][i][0] = -a*s + e + (i in digit j ? [P]_{q_i} s_from : 0), key[j][i][1] = a.
+// a: [dnum][E][N], e_ntt: [dnum][E][N], s, s_from: [E][N]; E = L + alpha rows.
+__global__ __launch_bounds__(kThreads) void k_keygen(const uint64_t* __restrict__ a,
+                                                     const uint64_t* __restrict__ e_ntt,
+                                                     const uint64_t* __restrict__ s,
+                                                     const uint64_t* __restrict__ s_from,
+                                                     uint64_t* __restrict__ key, uint32_t n,
+                                                     uint32_t L, uint32_t alpha,
+                                                     const double2* __restrict__ pmod,
+                                                     const PrimeK* __restrict__ pk) {
+  const uint32_t i = blockIdx.y, j = blockIdx.z, E = L + alpha;
+  const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
+  if (k >= n) return;
+  const PrimeK P = pk[i];
+  const size_t oj = ((size_t)j * E + i) * n + k;
+  const double av = ld(a + oj);
+  double b = ld(e_ntt + oj) - mm_var(av, ld(s + (size_t)i * n + k), P.q, P.qinv);
+  if (i < L && i >= j * alpha && i < (j + 1) * alpha) {
+    const double2 pm = pmod[i];
+    b += mm_shoup(ld(s_from + (size_t)i * n + k), pm.x, pm.y, P.q);
+  }
+  const size_t ok = (((size_t)j * E + i) * 2) * n + k;
+  st(key + ok, b, P.q, P.qinv);
+  key[ok + n] = a[oj];
+}
+
+// ct[i][0] = -a*s + me, ct[i][1] = a
+__global__ __launch_bounds__(kThreads) void k_encrypt(const uint64_t* __restrict__ a,
+                                                      const uint64_t* __restrict__ s,
+                                                      const uint64_t* __restrict__ me,
+                                                      uint64_t* __restrict__ ct, uint32_t n,
+                                                      const PrimeK* __restrict__ pk) {
+  const uint32_t i = blockIdx.y;
+  const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
+  if (k >= n) return;
+  const PrimeK P = pk[i];
+  const size_t o = (size_t)i * n + k;
+  const double av = ld(a + o);
+  st(ct + 2 * (size_t)i * n + k, ld(me + o) - mm_var(av, ld(s + o), P.q, P.qinv), P.q, P.qinv);
+  ct[(2 * (size_t)i + 1) * n + k] = a[o];
+}
+
+// Rescale, step 1: v = centred coefficients (mod q_last) of the last limb of
+// both components (rows 0, 1 of `v`, coefficient form); write [v]_{q_i} into
+// w[t][i] for i < l - 1.
+__global__ __launch_bounds__(kThreads) void k_rescale_lift(const uint64_t* __restrict__ v,
+                                                           uint64_t* __restrict__ w,
+                                                           uint32_t n, uint32_t last,
+                                                           const PrimeK* __restrict__ pk) {
+  const uint32_t i = blockIdx.y, t = blockIdx.z;
+  const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
+  if (k >= n) return;
+  const double ql = pk[last].q;
+  const double x = center(ld(v + (size_t)t * n + k), ql);
+  const PrimeK P = pk[i];
+  st(w + ((size_t)t * last + i) * n + k, x, P.q, P.qinv);
+}
+
+// Rescale, step 2: out[i][t] = (c[i][t] - w[t][i]) * q_last^-1 mod q_i.
+__global__ __launch_bounds__(kThreads) void k_rescale_combine(const uint64_t* c,
+                                                              const uint64_t* __restrict__ w,
+                                                              uint64_t* out, uint32_t n,
+                                                              uint32_t last,
+                                                              const double2* __restrict__ qlinv,
+                                                              const PrimeK* __restrict__ pk) {
+  const uint32_t i = blockIdx.y;
+  const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
+  if (k >= n) return;
+  const PrimeK P = pk[i];
+  const double2 f = qlinv[i];
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const size_t o = ((size_t)2 * i + t) * n + k;
+    const double d = ld(c + o) - ld(w + ((size_t)t * last + i) * n + k);
+    st(out + o, mm_shoup(d, f.x, f.y, P.q), P.q, P.qinv);
+  }
+}
+
+inline dim3 grid_rows(uint32_t n, uint32_t rows, uint32_t z = 1) {
+  return dim3((n + kThreads - 1) / kThreads, rows, z);
+}
+
+}  // namespace
+
+hipError_t k_binary_launch(const Context* c, const uint64_t* a, const uint64_t* b, uint64_t* out,
+                           uint32_t rows, uint32_t shift, int op, hipStream_t s) {
+  hipLaunchKernelGGL(k_binary, grid_rows(c->n, rows), dim3(kThreads), 0, s, a, b, out, c->n,
+                     shift, op, c->d_pk);
+  return hipGetLastError();
+}
+
+hipError_t k_mul_plain_launch(const Context* c, const uint64_t* ct, const uint64_t* pt,
+                              uint64_t* out, uint32_t level, hipStream_t s) {
+  hipLaunchKernelGGL(k_mul_plain, grid_rows(c->n, level), dim3(kThreads), 0, s, ct, pt, out,
+                     c->n, c->d_pk);
+  return hipGetLastError();
+}
+
+hipError_t k_tensor_launch(const Context* c, const uint64_t* a, const uint64_t* b,
+                           uint64_t* d01, uint64_t* d2, uint32_t level, hipStream_t s) {
+  hipLaunchKernelGGL(k_tensor, grid_rows(c->n, level), dim3(kThreads), 0, s, a, b, d01, d2,
+                     c->n, c->d_pk);
+  return hipGetLastError();
+}
+
+hipError_t k_monomial_launch(const Context* c, const uint64_t* in, uint64_t* out,
+                             uint32_t level, uint32_t m, hipStream_t s) {
+  hipLaunchKernelGGL(k_monomial, grid_rows(c->n, 2 * level), dim3(kThreads), 0, s, in, out,
+                     c->log_n, m, c->d_pk, c->d_tw_fwd);
+  return hipGetLastError();
+}
+
+hipError_t k_galois_launch(const Context* c, const uint64_t* in, uint64_t* out, uint32_t rows,
+                           uint32_t g, hipStream_t s) {
+  hipLaunchKernelGGL(k_galois, grid_rows(c->n, rows), dim3(kThreads), 0, s, in, out, c->log_n,
+                     g);
+  return hipGetLastError();
+}
+
+hipError_t k_lift_launch(const Context* c, const int64_t* x, const int8_t* x8, uint64_t* out,
+                         uint32_t rows, uint32_t prime0, uint32_t split, uint32_t prime1,
+                         hipStream_t s) {
+  hipLaunchKernelGGL(k_lift, grid_rows(c->n, rows), dim3(kThreads), 0, s, x, x8, out, c->n,
+                     prime0, split, prime1, c->d_pk);
+  return hipGetLastError();
+}
+
+hipError_t k_keygen_launch(const Context* c, const uint64_t* a, const uint64_t* e_ntt,
+                           const uint64_t* s, const uint64_t* s_from, uint64_t* key,
+                           const double2* pmod, hipStream_t st) {
+  hipLaunchKernelGGL(k_keygen, grid_rows(c->n, c->L + c->alpha, c->dnum), dim3(kThreads), 0, st,
+                     a, e_ntt, s, s_from, key, c->n, c->L, c->alpha, pmod, c->d_pk);
+  return hipGetLastError();
+}
+
+hipError_t k_encrypt_launch(const Context* c, const uint64_t* a, const uint64_t* s,
+                            const uint64_t* me, uint64_t* ct, uint32_t level, hipStream_t st) {
+  hipLaunchKernelGGL(k_encrypt, grid_rows(c->n, level), dim3(kThreads), 0, st, a, s, me, ct,
+                     c->n, c->d_pk);
+  return hipGetLastError();
+}
+
+hipError_t k_rescale_lift_launch(const Context* c, const uint64_t* v, uint64_t* w,
+                                 uint32_t level, hipStream_t s) {
+  hipLaunchKernelGGL(k_rescale_lift, grid_rows(c->n, level - 1, 2), dim3(kThreads), 0, s, v, w,
+                     c->n, level - 1, c->d_pk);
+  return hipGetLastError();
+}
+
+hipError_t k_rescale_combine_launch(const Context* c, const uint64_t* in, const uint64_t* w,
+                                    uint64_t* out, uint32_t level, const double2* qlinv,
+                                    hipStream_t s) {
+  hipLaunchKernelGGL(k_rescale_combine, grid_rows(c->n, level - 1), dim3(kThreads), 0, s, in, w,
+                     out, c->n, level - 1, qlinv, c->d_pk);
+  return hipGetLastError();
+}
+
+}  // namespace fesc

@@ -80,6 +80,21 @@ __device__ __forceinline__ uint64_t d2u(double r) {
 // ------------------------------------------------------------- host side
 
 #define FESC_MAX_PRIMES 64
+#define FESC_MAX_ALPHA 16
+
+// Per-level constants of basis conversion and rescaling (device arrays
+// carved from one allocation `base`); entries are {v, fl(v / m)}.
+struct LevelTables {
+  void* base = nullptr;
+  uint32_t level = 0;
+  double2* mu_inv = nullptr;   // [dnum][alpha]             (Q_D/q_a)^-1 mod q_a
+  double2* mu_hat = nullptr;   // [dnum][level+alpha][alpha] (Q_D/q_a) mod m_row
+  double2* md_inv = nullptr;   // [alpha]                   (P/p_k)^-1 mod p_k
+  double2* md_hat = nullptr;   // [level][alpha]            (P/p_k) mod q_i
+  double2* md_pinv = nullptr;  // [level]                   P^-1 mod q_i
+  double2* pmod = nullptr;     // [L]                       P mod q_i
+  double2* rs_inv = nullptr;   // [level]                   q_{level-1}^-1 mod q_i
+};
 
 struct Context {
   int device = 0;
@@ -92,8 +107,8 @@ struct Context {
   double2* d_tw_inv = nullptr;    // [L+alpha][N] {psi^-brv(i), /q}
   // keys: Galois element (0 = relinearisation) -> device [dnum][L+alpha][2][N]
   std::map<uint32_t, uint64_t*> keys;
-  // basis-conversion constant tables, built on first use per (level, kind)
-  std::map<uint64_t, void*> tables;
+  // basis-conversion / rescale constants, built on first use per level
+  std::map<uint32_t, LevelTables> level_tabs;
   // scratch (grown on demand, freed with the context)
   void* scratch = nullptr;
   size_t scratch_bytes = 0;
@@ -115,7 +130,20 @@ uint64_t h_inv(uint64_t a, uint64_t p);
 bool h_is_prime(uint64_t n);
 uint64_t h_min_root(uint64_t q, uint32_t log_n);
 
+// Row selection of a batched NTT launch (see ntt.hip).
+struct RowSel {
+  uint64_t* base;
+  size_t batch_stride, limb_stride;
+  uint32_t prime0, split, prime1;
+  uint32_t skip_alpha, skip_limit;
+  __device__ uint64_t* row() const;
+  __device__ uint32_t prime() const;
+  __device__ bool skip() const;
+};
+
 // kernel launchers (ntt.hip)
+hipError_t launch_ntt_rows(const Context* c, const RowSel& rs, uint32_t batch, uint32_t limbs,
+                           bool inverse, hipStream_t s);
 hipError_t launch_ntt(const Context* c, uint64_t* d, uint32_t batch, size_t batch_stride,
                       uint32_t limbs, size_t limb_stride, uint32_t prime0, bool inverse,
                       hipStream_t s);

@@ -148,7 +148,7 @@ void destroy(Context* c) {
   if (!c) return;
   hipDeviceSynchronize();
   for (auto& kv : c->keys) hipFree(kv.second);
-  for (auto& kv : c->tables) hipFree(kv.second);
+  for (auto& kv : c->level_tabs) hipFree(kv.second.base);
   hipFree(c->d_pk);
   hipFree(c->d_tw_fwd);
   hipFree(c->d_tw_inv);
@@ -161,8 +161,9 @@ int create(const fesc_params* p, fesc_ctx** out) {
   *out = nullptr;
   if (p->log_n < 12 || p->log_n > 16)
     return fail(FESC_ERR_ARG, "log_n must lie in [12, 16]");
-  if (p->num_q < 1 || p->num_p < 1 || p->num_q + p->num_p > FESC_MAX_PRIMES || !p->q || !p->p)
-    return fail(FESC_ERR_ARG, "need 1 <= num_q, 1 <= num_p, num_q + num_p <= 64");
+  if (p->num_q < 1 || p->num_p < 1 || p->num_p > FESC_MAX_ALPHA ||
+      p->num_q + p->num_p > FESC_MAX_PRIMES || !p->q || !p->p)
+    return fail(FESC_ERR_ARG, "need 1 <= num_q, 1 <= num_p <= 16, num_q + num_p <= 64");
   const uint32_t dnum = (p->num_q + p->num_p - 1) / p->num_p;
   if (p->dnum != dnum)
     return fail(FESC_ERR_ARG, "dnum must equal ceil(num_q / num_p) = " + std::to_string(dnum));

@@ -1,0 +1,247 @@
+// Hybrid key switching (digit decomposition with special primes): ModUp by
+// fast basis conversion, inner product with the switching key, ModDown.
+//
+// Basis conversion uses centred digits: for a digit D with product Q_D and
+// x_a = [c_a * (Q_D/q_a)^-1]_{q_a} taken in (-q_a/2, q_a/2),
+//     y mod m = sum_a x_a * ((Q_D/q_a) mod m)  mod m.
+// With centred digits the conversion is an odd map, so it commutes with the
+// signed coefficient permutations of the Galois group: ModUp once, then apply
+// sigma_g to the extended digits (evaluation-form index permutation) for any
+// number of rotations of the same ciphertext.
+//
+// Extended basis at level l: rows 0..l-1 are q_0..q_{l-1}, rows l..l+alpha-1
+// are p_0..p_{alpha-1} (extended prime index L + k).
+#include "fesc_internal.hpp"
+#include "ops.hpp"
+
+namespace fesc {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr uint32_t kRowsPerZ = 8;
+
+__device__ __forceinline__ uint32_t ext_prime(uint32_t row, uint32_t level, uint32_t L) {
+  return row < level ? row : L + (row - level);
+}
+
+__device__ __forceinline__ uint32_t galois_src(uint32_t jp, uint32_t g, uint32_t log_n) {
+  const uint32_t b = __builtin_bitreverse32(jp) >> (32 - log_n);
+  const uint32_t e = (g * (2u * b + 1u)) & ((2u << log_n) - 1u);
+  return __builtin_bitreverse32((e - 1u) >> 1) >> (32 - log_n);
+}
+
+// ModUp: coefficient-form input rows cc[0..level) -> ext[j][row] for every row
+// outside digit j (coefficient form; the caller transforms them).
+template <int MAXA>
+__global__ __launch_bounds__(kThreads) void k_modup(const uint64_t* __restrict__ cc,
+                                                    uint64_t* __restrict__ ext, uint32_t level,
+                                                    uint32_t L, uint32_t alpha, uint32_t n,
+                                                    const PrimeK* __restrict__ pk,
+                                                    const double2* __restrict__ mu_inv,
+                                                    const double2* __restrict__ mu_hat) {
+  const uint32_t j = blockIdx.y;
+  const uint32_t lo = j * alpha, hi = min(lo + alpha, level), aj = hi - lo;
+  const uint32_t E = level + alpha;
+  const uint32_t k = 2 * (blockIdx.x * kThreads + threadIdx.x);
+  if (k >= n) return;
+  double x0[MAXA], x1[MAXA];
+#pragma unroll
+  for (int a = 0; a < MAXA; ++a) {
+    x0[a] = x1[a] = 0.0;
+    if (a < (int)aj) {
+      const PrimeK P = pk[lo + a];
+      const double2 f = mu_inv[j * alpha + a];
+      const ulonglong2 v = *reinterpret_cast<const ulonglong2*>(cc + (size_t)(lo + a) * n + k);
+      x0[a] = center(red_full(mm_shoup(u2d(v.x), f.x, f.y, P.q), P.q, P.qinv), P.q);
+      x1[a] = center(red_full(mm_shoup(u2d(v.y), f.x, f.y, P.q), P.q, P.qinv), P.q);
+    }
+  }
+  const uint32_t r0 = blockIdx.z * kRowsPerZ, r1 = min(r0 + kRowsPerZ, E);
+  for (uint32_t row = r0; row < r1; ++row) {
+    if (row >= lo && row < hi) continue;
+    const PrimeK M = pk[ext_prime(row, level, L)];
+    const double2* h = mu_hat + ((size_t)j * E + row) * alpha;
+    double acc0 = 0.0, acc1 = 0.0;
+#pragma unroll
+    for (int a = 0; a < MAXA; ++a) {
+      if (a < (int)aj) {
+        const double2 w = h[a];
+        acc0 += mm_shoup(x0[a], w.x, w.y, M.q);
+        acc1 += mm_shoup(x1[a], w.x, w.y, M.q);
+        if ((a & 7) == 7) {
+          acc0 = red_bal(acc0, M.q, M.qinv);
+          acc1 = red_bal(acc1, M.q, M.qinv);
+        }
+      }
+    }
+    ulonglong2 o;
+    o.x = d2u(red_full(acc0, M.q, M.qinv));
+    o.y = d2u(red_full(acc1, M.q, M.qinv));
+    *reinterpret_cast<ulonglong2*>(ext + ((size_t)j * E + row) * n + k) = o;
+  }
+}
+
+// Inner product with the key, sigma_g applied to the extended digits on the
+// fly: acc[t][row][k] = sum_j d_j[row][src(k)] * key[j][prime(row)][t][k].
+// Own-digit rows of d_j are the input polynomial itself (row i at
+// in + i*in_stride, evaluation form).
+__global__ __launch_bounds__(kThreads) void k_ip(const uint64_t* __restrict__ ext,
+                                                 const uint64_t* __restrict__ in,
+                                                 size_t in_stride,
+                                                 const uint64_t* __restrict__ key,
+                                                 uint64_t* __restrict__ acc, uint32_t level,
+                                                 uint32_t L, uint32_t alpha, uint32_t dnum_l,
+                                                 uint32_t log_n, uint32_t galois,
+                                                 const PrimeK* __restrict__ pk) {
+  const uint32_t n = 1u << log_n;
+  const uint32_t row = blockIdx.y;
+  const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
+  if (k >= n) return;
+  const uint32_t E = level + alpha, KE = L + alpha;
+  const uint32_t prime = ext_prime(row, level, L);
+  const PrimeK M = pk[prime];
+  const uint32_t src = galois ? galois_src(k, galois, log_n) : k;
+  double ab = 0.0, aa = 0.0;
+  for (uint32_t j = 0; j < dnum_l; ++j) {
+    const uint32_t lo = j * alpha, hi = min(lo + alpha, level);
+    const uint64_t dv = (row >= lo && row < hi) ? in[(size_t)row * in_stride + src]
+                                                : ext[((size_t)j * E + row) * n + src];
+    const double d = u2d(dv);
+    const size_t ko = (((size_t)j * KE + prime) * 2) * n + k;
+    ab += mm_var(d, u2d(key[ko]), M.q, M.qinv);
+    aa += mm_var(d, u2d(key[ko + n]), M.q, M.qinv);
+    if ((j & 3) == 3) {
+      ab = red_bal(ab, M.q, M.qinv);
+      aa = red_bal(aa, M.q, M.qinv);
+    }
+  }
+  acc[(size_t)row * n + k] = d2u(red_full(ab, M.q, M.qinv));
+  acc[((size_t)E + row) * n + k] = d2u(red_full(aa, M.q, M.qinv));
+}
+
+// ModDown conversion: P-rows of acc[t] (coefficient form) -> y[t][i], i < level.
+template <int MAXA>
+__global__ __launch_bounds__(kThreads) void k_moddown_bconv(const uint64_t* __restrict__ acc,
+                                                            uint64_t* __restrict__ y,
+                                                            uint32_t level, uint32_t L,
+                                                            uint32_t alpha, uint32_t n,
+                                                            const PrimeK* __restrict__ pk,
+                                                            const double2* __restrict__ md_inv,
+                                                            const double2* __restrict__ md_hat) {
+  const uint32_t t = blockIdx.y;
+  const uint32_t E = level + alpha;
+  const uint32_t k = 2 * (blockIdx.x * kThreads + threadIdx.x);
+  if (k >= n) return;
+  double x0[MAXA], x1[MAXA];
+#pragma unroll
+  for (int a = 0; a < MAXA; ++a) {
+    x0[a] = x1[a] = 0.0;
+    if (a < (int)alpha) {
+      const PrimeK P = pk[L + a];
+      const double2 f = md_inv[a];
+      const ulonglong2 v =
+          *reinterpret_cast<const ulonglong2*>(acc + ((size_t)t * E + level + a) * n + k);
+      x0[a] = center(red_full(mm_shoup(u2d(v.x), f.x, f.y, P.q), P.q, P.qinv), P.q);
+      x1[a] = center(red_full(mm_shoup(u2d(v.y), f.x, f.y, P.q), P.q, P.qinv), P.q);
+    }
+  }
+  const uint32_t i0 = blockIdx.z * kRowsPerZ, i1 = min(i0 + kRowsPerZ, level);
+  for (uint32_t i = i0; i < i1; ++i) {
+    const PrimeK M = pk[i];
+    const double2* h = md_hat + (size_t)i * alpha;
+    double s0 = 0.0, s1 = 0.0;
+#pragma unroll
+    for (int a = 0; a < MAXA; ++a) {
+      if (a < (int)alpha) {
+        const double2 w = h[a];
+        s0 += mm_shoup(x0[a], w.x, w.y, M.q);
+        s1 += mm_shoup(x1[a], w.x, w.y, M.q);
+        if ((a & 7) == 7) {
+          s0 = red_bal(s0, M.q, M.qinv);
+          s1 = red_bal(s1, M.q, M.qinv);
+        }
+      }
+    }
+    ulonglong2 o;
+    o.x = d2u(red_full(s0, M.q, M.qinv));
+    o.y = d2u(red_full(s1, M.q, M.qinv));
+    *reinterpret_cast<ulonglong2*>(y + ((size_t)t * level + i) * n + k) = o;
+  }
+}
+
+// out[i][t] = (acc[t][i] - y[t][i]) * P^-1 (+ add[i][t][src(k)] when bit t of
+// add_mask is set; add row i component t at add + i*2N + t*N).
+__global__ __launch_bounds__(kThreads) void k_ks_combine(const uint64_t* __restrict__ acc,
+                                                         const uint64_t* __restrict__ y,
+                                                         const uint64_t* add,
+                                                         uint32_t add_mask, uint32_t add_galois,
+                                                         uint64_t* out, uint32_t level,
+                                                         uint32_t alpha, uint32_t log_n,
+                                                         const PrimeK* __restrict__ pk,
+                                                         const double2* __restrict__ pinv) {
+  const uint32_t n = 1u << log_n;
+  const uint32_t i = blockIdx.y, t = blockIdx.z;
+  const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
+  if (k >= n) return;
+  const uint32_t E = level + alpha;
+  const PrimeK M = pk[i];
+  const double2 f = pinv[i];
+  const double d = u2d(acc[((size_t)t * E + i) * n + k]) - u2d(y[((size_t)t * level + i) * n + k]);
+  double v = mm_shoup(d, f.x, f.y, M.q);
+  if ((add_mask >> t) & 1u) {
+    const uint32_t src = add_galois ? galois_src(k, add_galois, log_n) : k;
+    v += u2d(add[((size_t)2 * i + t) * n + src]);
+  }
+  out[((size_t)2 * i + t) * n + k] = d2u(red_full(v, M.q, M.qinv));
+}
+
+}  // namespace
+
+hipError_t k_modup_launch(const Context* c, const LevelTables& T, const uint64_t* cc,
+                          uint64_t* ext, uint32_t level, hipStream_t s) {
+  const uint32_t dnum_l = (level + c->alpha - 1) / c->alpha;
+  const uint32_t E = level + c->alpha;
+  dim3 grid((c->n / 2 + kThreads - 1) / kThreads, dnum_l, (E + kRowsPerZ - 1) / kRowsPerZ);
+  if (c->alpha <= 8)
+    hipLaunchKernelGGL(k_modup<8>, grid, dim3(kThreads), 0, s, cc, ext, level, c->L, c->alpha,
+                       c->n, c->d_pk, T.mu_inv, T.mu_hat);
+  else
+    hipLaunchKernelGGL(k_modup<16>, grid, dim3(kThreads), 0, s, cc, ext, level, c->L, c->alpha,
+                       c->n, c->d_pk, T.mu_inv, T.mu_hat);
+  return hipGetLastError();
+}
+
+hipError_t k_ip_launch(const Context* c, const uint64_t* ext, const uint64_t* in,
+                       size_t in_stride, const uint64_t* key, uint64_t* acc, uint32_t level,
+                       uint32_t galois, hipStream_t s) {
+  const uint32_t dnum_l = (level + c->alpha - 1) / c->alpha;
+  dim3 grid((c->n + kThreads - 1) / kThreads, level + c->alpha);
+  hipLaunchKernelGGL(k_ip, grid, dim3(kThreads), 0, s, ext, in, in_stride, key, acc, level, c->L,
+                     c->alpha, dnum_l, c->log_n, galois, c->d_pk);
+  return hipGetLastError();
+}
+
+hipError_t k_moddown_bconv_launch(const Context* c, const LevelTables& T, const uint64_t* acc,
+                                  uint64_t* y, uint32_t level, hipStream_t s) {
+  dim3 grid((c->n / 2 + kThreads - 1) / kThreads, 2, (level + kRowsPerZ - 1) / kRowsPerZ);
+  if (c->alpha <= 8)
+    hipLaunchKernelGGL(k_moddown_bconv<8>, grid, dim3(kThreads), 0, s, acc, y, level, c->L,
+                       c->alpha, c->n, c->d_pk, T.md_inv, T.md_hat);
+  else
+    hipLaunchKernelGGL(k_moddown_bconv<16>, grid, dim3(kThreads), 0, s, acc, y, level, c->L,
+                       c->alpha, c->n, c->d_pk, T.md_inv, T.md_hat);
+  return hipGetLastError();
+}
+
+hipError_t k_ks_combine_launch(const Context* c, const LevelTables& T, const uint64_t* acc,
+                               const uint64_t* y, const uint64_t* add, uint32_t add_mask,
+                               uint32_t add_galois, uint64_t* out, uint32_t level,
+                               hipStream_t s) {
+  dim3 grid((c->n + kThreads - 1) / kThreads, level, 2);
+  hipLaunchKernelGGL(k_ks_combine, grid, dim3(kThreads), 0, s, acc, y, add, add_mask, add_galois,
+                     out, level, c->alpha, c->log_n, c->d_pk, T.md_pinv);
+  return hipGetLastError();
+}
+
+}  // namespace fesc

@@ -1,0 +1,229 @@
+// Plaintext-matrix x ciphertext projection (BSGS diagonal method on the
+// segment view of the slots; paper Appendix "Projection Kernel Breakdown").
+//
+//   c~_{b,p} = sum_u sum_q Phi^q(x~_u) * D~_{b,u,p,q}        (pt-MAC)
+//   y_b      = sum_p Phi^(p n1)(c~_{b,p});  y_b += conj(y_b);  rescale
+//
+// Phi^delta is one rotation by delta * unit slots.  Baby steps Phi^q(x~_u)
+// share one ModUp per input (hoisted); giant steps and the conjugation are
+// ordinary key switches.
+//
+// The pt-MAC streams every plaintext diagonal once.  A thread owns one
+// coefficient of one limb and accumulates G outputs (b, p) at a time, so each
+// baby-step value it loads is reused G times; the diagonals are read with
+// coalesced 8-byte loads and nothing else is written until the final sums.
+#include <string>
+#include <vector>
+
+#include "fesc_internal.hpp"
+#include "ops.hpp"
+
+struct fesc_matvec_plan {
+  fesc_matvec_desc d;
+  std::vector<const uint64_t*> diag;  // host copy of the table [n_out][n2][n_in][n1]
+  const uint64_t** d_diag = nullptr;  // device copy
+  uint64_t* work = nullptr;           // baby [n_in][n1] cts, then c~ [n_out][n2] cts
+  const uint64_t** d_baby = nullptr;  // device table of baby pointers
+  uint64_t** d_ct = nullptr;          // device table of c~ pointers
+  size_t ct_words = 0;
+};
+
+namespace fesc {
+
+int op_rotate_many(Context* c, const uint64_t* in, uint32_t count, const int32_t* steps,
+                   uint64_t* const* outs, uint32_t level, hipStream_t s);
+int op_rescale(Context* c, const uint64_t* in, uint64_t* out, uint32_t level, hipStream_t s);
+uint32_t galois_of_step(const Context* c, int32_t step);
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kGroup = 16;  // outputs accumulated per thread
+
+template <int G>
+__global__ __launch_bounds__(kThreads) void k_ptmac(const uint64_t* const* __restrict__ baby,
+                                                    const uint64_t* const* __restrict__ diag,
+                                                    uint64_t* const* __restrict__ outs,
+                                                    uint32_t n_outputs, uint32_t terms,
+                                                    uint32_t n, const PrimeK* __restrict__ pk) {
+  const uint32_t i = blockIdx.y;
+  const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
+  const uint32_t o0 = blockIdx.z * G;
+  if (k >= n) return;
+  const PrimeK P = pk[i];
+  const uint32_t g_end = min((uint32_t)G, n_outputs - o0);
+  double a0[G], a1[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) a0[g] = a1[g] = 0.0;
+  const size_t pi = (size_t)i * n + k, c0 = (size_t)2 * i * n + k, c1 = c0 + n;
+  for (uint32_t t = 0; t < terms; ++t) {
+    const uint64_t* bp = baby[t];
+    const double x0 = u2d(bp[c0]), x1 = u2d(bp[c1]);
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      if ((uint32_t)g < g_end) {
+        const double w = u2d(diag[(size_t)(o0 + g) * terms + t][pi]);
+        a0[g] += mm_var(x0, w, P.q, P.qinv);
+        a1[g] += mm_var(x1, w, P.q, P.qinv);
+      }
+    }
+    if ((t & 3) == 3) {
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        a0[g] = red_bal(a0[g], P.q, P.qinv);
+        a1[g] = red_bal(a1[g], P.q, P.qinv);
+      }
+    }
+  }
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    if ((uint32_t)g < g_end) {
+      uint64_t* o = outs[o0 + g];
+      o[c0] = d2u(red_full(a0[g], P.q, P.qinv));
+      o[c1] = d2u(red_full(a1[g], P.q, P.qinv));
+    }
+  }
+}
+
+#define HIPCK(expr)                                   \
+  do {                                                \
+    hipError_t e_ = (expr);                           \
+    if (e_ != hipSuccess) return hip_check(e_, #expr); \
+  } while (0)
+
+}  // namespace
+
+int matvec_plan_create(Context* c, const fesc_matvec_desc* d, const uint64_t* const* diags,
+                       fesc_matvec_plan** out) {
+  if (!d || !diags || !out) return fail(FESC_ERR_ARG, "null argument");
+  *out = nullptr;
+  if (d->level < 1 || d->level > c->L) return fail(FESC_ERR_LEVEL, "matvec level out of range");
+  if (d->rescale && d->level < 2) return fail(FESC_ERR_LEVEL, "rescale needs level >= 2");
+  if (!d->n_in || !d->n_out || !d->n1 || !d->n2 || !d->unit)
+    return fail(FESC_ERR_ARG, "matvec sizes must be positive");
+  const size_t n_diag = (size_t)d->n_out * d->n2 * d->n_in * d->n1;
+  for (size_t t = 0; t < n_diag; ++t)
+    if (!diags[t]) return fail(FESC_ERR_ARG, "null diagonal " + std::to_string(t));
+  // every Galois key the schedule needs must be present
+  std::vector<int64_t> steps;
+  for (uint32_t q = 1; q < d->n1; ++q) steps.push_back((int64_t)q * d->unit);
+  for (uint32_t p = 1; p < d->n2; ++p) steps.push_back((int64_t)p * d->n1 * d->unit);
+  for (int64_t st : steps) {
+    const uint32_t g = galois_of_step(c, (int32_t)(st % (c->n / 2)));
+    if (g != 1 && !c->keys.count(g))
+      return fail(FESC_ERR_NO_KEY, "matvec needs the key of rotation " + std::to_string(st));
+  }
+  if (d->real_extract && !c->keys.count(2 * c->n - 1))
+    return fail(FESC_ERR_NO_KEY, "matvec real extraction needs the conjugation key");
+
+  fesc_matvec_plan* p = new fesc_matvec_plan();
+  p->d = *d;
+  p->diag.assign(diags, diags + n_diag);
+  p->ct_words = (size_t)2 * d->level * c->n;
+  const size_t n_baby = (size_t)d->n_in * d->n1, n_ct = (size_t)d->n_out * d->n2;
+  std::vector<const uint64_t*> baby(n_baby);
+  std::vector<uint64_t*> cts(n_ct);
+  bool ok = hipMalloc(&p->work, (n_baby + n_ct + 1) * p->ct_words * 8) == hipSuccess &&
+            hipMalloc(&p->d_diag, n_diag * sizeof(void*)) == hipSuccess &&
+            hipMalloc(&p->d_baby, n_baby * sizeof(void*)) == hipSuccess &&
+            hipMalloc(&p->d_ct, n_ct * sizeof(void*)) == hipSuccess;
+  if (ok) {
+    for (size_t t = 0; t < n_baby; ++t) baby[t] = p->work + t * p->ct_words;
+    for (size_t t = 0; t < n_ct; ++t) cts[t] = p->work + (n_baby + t) * p->ct_words;
+    ok = hipMemcpy(p->d_diag, p->diag.data(), n_diag * sizeof(void*), hipMemcpyHostToDevice) ==
+             hipSuccess &&
+         hipMemcpy(p->d_baby, baby.data(), n_baby * sizeof(void*), hipMemcpyHostToDevice) ==
+             hipSuccess &&
+         hipMemcpy(p->d_ct, cts.data(), n_ct * sizeof(void*), hipMemcpyHostToDevice) == hipSuccess;
+  }
+  if (!ok) {
+    hipFree(p->work);
+    hipFree(p->d_diag);
+    hipFree(p->d_baby);
+    hipFree(p->d_ct);
+    delete p;
+    return fail(FESC_ERR_OOM, "matvec workspace allocation failed");
+  }
+  *out = p;
+  return FESC_OK;
+}
+
+void matvec_plan_destroy(fesc_matvec_plan* p) {
+  if (!p) return;
+  hipDeviceSynchronize();
+  hipFree(p->work);
+  hipFree(p->d_diag);
+  hipFree(p->d_baby);
+  hipFree(p->d_ct);
+  delete p;
+}
+
+int ptct_matvec(Context* c, fesc_matvec_plan* p, const uint64_t* const* in,
+                uint64_t* const* out, hipStream_t s) {
+  const fesc_matvec_desc& d = p->d;
+  const uint32_t level = d.level;
+  const size_t W = p->ct_words, n_baby = (size_t)d.n_in * d.n1;
+  uint64_t* baby = p->work;
+  uint64_t* ct = p->work + n_baby * W;
+  uint64_t* tmp = ct + (size_t)d.n_out * d.n2 * W;
+  int err;
+  // baby steps, hoisted per input
+  std::vector<int32_t> steps(d.n1);
+  std::vector<uint64_t*> bouts(d.n1);
+  for (uint32_t q = 0; q < d.n1; ++q) steps[q] = (int32_t)(((int64_t)q * d.unit) % (c->n / 2));
+  for (uint32_t u = 0; u < d.n_in; ++u) {
+    for (uint32_t q = 0; q < d.n1; ++q) bouts[q] = baby + ((size_t)u * d.n1 + q) * W;
+    if ((err = op_rotate_many(c, in[u], d.n1, steps.data(), bouts.data(), level, s))) return err;
+  }
+  // pt-MAC over all (b, p)
+  const uint32_t n_outputs = d.n_out * d.n2;
+  dim3 grid((c->n + kThreads - 1) / kThreads, level, (n_outputs + kGroup - 1) / kGroup);
+  hipLaunchKernelGGL(k_ptmac<kGroup>, grid, dim3(kThreads), 0, s, p->d_baby, p->d_diag, p->d_ct,
+                     n_outputs, (uint32_t)n_baby, c->n, c->d_pk);
+  HIPCK(hipGetLastError());
+  // giant steps, real extraction, rescale
+  for (uint32_t b = 0; b < d.n_out; ++b) {
+    uint64_t* y = ct + (size_t)b * d.n2 * W;
+    for (uint32_t g = 1; g < d.n2; ++g) {
+      uint64_t* cp = y + (size_t)g * W;
+      const int32_t st = (int32_t)(((int64_t)g * d.n1 * d.unit) % (c->n / 2));
+      if ((err = op_rotate_many(c, cp, 1, &st, &cp, level, s))) return err;
+      HIPCK(k_binary_launch(c, y, cp, y, 2 * level, 1, 0, s));
+    }
+    if (d.real_extract) {
+      const int32_t cj = INT32_MIN;
+      if ((err = op_rotate_many(c, y, 1, &cj, &tmp, level, s))) return err;
+      HIPCK(k_binary_launch(c, y, tmp, y, 2 * level, 1, 0, s));
+    }
+    if (d.rescale) {
+      if ((err = op_rescale(c, y, out[b], level, s))) return err;
+    } else {
+      HIPCK(hipMemcpyAsync(out[b], y, W * 8, hipMemcpyDeviceToDevice, s));
+    }
+  }
+  return FESC_OK;
+}
+
+}  // namespace fesc
+
+extern "C" {
+
+int fesc_matvec_plan_create(fesc_ctx* ctx, const fesc_matvec_desc* desc,
+                            const uint64_t* const* diags, fesc_matvec_plan** plan) {
+  if (!ctx) return fesc::fail(FESC_ERR_ARG, "null context");
+  return fesc::matvec_plan_create(ctx, desc, diags, plan);
+}
+
+void fesc_matvec_plan_destroy(fesc_matvec_plan* plan) { fesc::matvec_plan_destroy(plan); }
+
+int fesc_ptct_matvec(fesc_ctx* ctx, fesc_matvec_plan* plan, const uint64_t* const* in,
+                     uint64_t* const* out, void* stream) {
+  if (!ctx || !plan || !in || !out) return fesc::fail(FESC_ERR_ARG, "null argument");
+  for (uint32_t u = 0; u < plan->d.n_in; ++u)
+    if (!in[u]) return fesc::fail(FESC_ERR_ARG, "null input");
+  for (uint32_t b = 0; b < plan->d.n_out; ++b)
+    if (!out[b]) return fesc::fail(FESC_ERR_ARG, "null output");
+  return fesc::ptct_matvec(ctx, plan, in, out, reinterpret_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"

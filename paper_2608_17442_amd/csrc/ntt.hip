@@ -90,15 +90,29 @@ __device__ __forceinline__ void gs_head(double (&x)[16], const double2* tw, uint
   if constexpr (NST >= 4) gs_stage<8>(x, tw, n, jb, js_log, q, qinv);
 }
 
-struct RowSel {
-  uint64_t* base;
-  size_t batch_stride, limb_stride;
-  uint32_t prime0;
-  __device__ __forceinline__ uint64_t* row() const {
-    return base + (size_t)blockIdx.z * batch_stride + (size_t)blockIdx.y * limb_stride;
-  }
-  __device__ __forceinline__ uint32_t prime() const { return prime0 + blockIdx.y; }
-};
+}  // namespace
+
+// Row selection of a batched transform launch.  blockIdx.y = batch index b,
+// blockIdx.z = limb index i (the batch varies fastest between workgroups, so
+// the twiddle table of one prime stays resident in L2 across the batch).
+// Limb i < split uses prime prime0 + i, limb i >= split prime1 + (i - split).
+// If skip_alpha != 0, limbs [b*skip_alpha, min((b+1)*skip_alpha, skip_limit))
+// of batch element b are left untouched (the own-digit rows of a ModUp).
+__device__ __forceinline__ uint64_t* RowSel::row() const {
+  return base + (size_t)blockIdx.y * batch_stride + (size_t)blockIdx.z * limb_stride;
+}
+__device__ __forceinline__ uint32_t RowSel::prime() const {
+  const uint32_t i = blockIdx.z;
+  return i < split ? prime0 + i : prime1 + (i - split);
+}
+__device__ __forceinline__ bool RowSel::skip() const {
+  if (!skip_alpha) return false;
+  const uint32_t lo = blockIdx.y * skip_alpha;
+  const uint32_t hi = min(lo + skip_alpha, skip_limit);
+  return blockIdx.z >= lo && blockIdx.z < hi;
+}
+
+namespace {
 
 // ---------------------------------------------------------------- forward
 
@@ -111,6 +125,7 @@ __global__ __launch_bounds__(kThreads) void k_fwd_outer(RowSel rs, uint32_t log_
   constexpr int TPS = (1 << LOGM) / 16;
   constexpr int SPW = kThreads / TPS;
   __shared__ double lds[SPW * TPS * 16 + SPW * TPS];
+  if (rs.skip()) return;
   const uint32_t n = 1u << log_n;
   const uint32_t prime = rs.prime();
   const double q = pk[prime].q, qinv = pk[prime].qinv;
@@ -146,6 +161,7 @@ __global__ __launch_bounds__(kThreads) void k_fwd_inner(RowSel rs, uint32_t log_
                                                         const PrimeK* __restrict__ pk,
                                                         const double2* __restrict__ twf) {
   __shared__ double lds[16 * 16 * kPadRow];
+  if (rs.skip()) return;
   const uint32_t n = 1u << log_n;
   const uint32_t prime = rs.prime();
   const double q = pk[prime].q, qinv = pk[prime].qinv;
@@ -182,6 +198,7 @@ __global__ __launch_bounds__(kThreads) void k_inv_inner(RowSel rs, uint32_t log_
                                                         const PrimeK* __restrict__ pk,
                                                         const double2* __restrict__ twi) {
   __shared__ double lds[16 * 16 * kPadRow];
+  if (rs.skip()) return;
   const uint32_t n = 1u << log_n;
   const uint32_t prime = rs.prime();
   const double q = pk[prime].q, qinv = pk[prime].qinv;
@@ -218,6 +235,7 @@ __global__ __launch_bounds__(kThreads) void k_inv_outer(RowSel rs, uint32_t log_
   constexpr int TPS = (1 << LOGM) / 16;
   constexpr int SPW = kThreads / TPS;
   __shared__ double lds[SPW * TPS * 16 + SPW * TPS];
+  if (rs.skip()) return;
   const uint32_t n = 1u << log_n;
   const uint32_t prime = rs.prime();
   const PrimeK P = pk[prime];
@@ -260,14 +278,12 @@ void launch_outer(bool inverse, dim3 grid, hipStream_t s, RowSel rs, uint32_t lo
 
 }  // namespace
 
-hipError_t launch_ntt(const Context* c, uint64_t* d, uint32_t batch, size_t batch_stride,
-                      uint32_t limbs, size_t limb_stride, uint32_t prime0, bool inverse,
-                      hipStream_t s) {
-  RowSel rs{d, batch_stride, limb_stride, prime0};
+hipError_t launch_ntt_rows(const Context* c, const RowSel& rs, uint32_t batch, uint32_t limbs,
+                           bool inverse, hipStream_t s) {
   const uint32_t log_n = c->log_n;
   const double2* tw = inverse ? c->d_tw_inv : c->d_tw_fwd;
-  dim3 inner(c->n / 4096, limbs, batch);
-  dim3 outer(1, limbs, batch);
+  dim3 inner(c->n / 4096, batch, limbs);
+  dim3 outer(1, batch, limbs);
   if (inverse)
     hipLaunchKernelGGL(k_inv_inner, inner, dim3(kThreads), 0, s, rs, log_n, c->d_pk, tw);
   switch (log_n) {
@@ -281,6 +297,13 @@ hipError_t launch_ntt(const Context* c, uint64_t* d, uint32_t batch, size_t batc
   if (!inverse)
     hipLaunchKernelGGL(k_fwd_inner, inner, dim3(kThreads), 0, s, rs, log_n, c->d_pk, tw);
   return hipGetLastError();
+}
+
+hipError_t launch_ntt(const Context* c, uint64_t* d, uint32_t batch, size_t batch_stride,
+                      uint32_t limbs, size_t limb_stride, uint32_t prime0, bool inverse,
+                      hipStream_t s) {
+  RowSel rs{d, batch_stride, limb_stride, prime0, limbs, 0, 0, 0};
+  return launch_ntt_rows(c, rs, batch, limbs, inverse, s);
 }
 
 }  // namespace fesc

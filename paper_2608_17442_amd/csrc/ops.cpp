@@ -1,0 +1,315 @@
+// Host drivers of the ciphertext operations: per-level constant tables,
+// scratch layout, and the launch sequences of key switching, rotation,
+// relinearisation, rescaling, key generation and encryption.  Every launch is
+// asynchronous on the caller's stream; nothing here synchronises.
+#include <string>
+#include <vector>
+
+#include "fesc_internal.hpp"
+#include "ops.hpp"
+
+namespace fesc {
+
+// ------------------------------------------------------------ level tables
+
+namespace {
+
+uint64_t prod_mod_except(const std::vector<uint64_t>& ps, size_t skip, uint64_t m) {
+  uint64_t r = 1 % m;
+  for (size_t b = 0; b < ps.size(); ++b)
+    if (b != skip) r = h_mulmod(r, ps[b] % m, m);
+  return r;
+}
+
+double2 entry(uint64_t v, uint64_t m) { return double2{(double)v, (double)v / (double)m}; }
+
+}  // namespace
+
+const LevelTables* level_tables(Context* c, uint32_t level, int* err) {
+  *err = FESC_OK;
+  auto it = c->level_tabs.find(level);
+  if (it != c->level_tabs.end()) return &it->second;
+  const uint32_t L = c->L, alpha = c->alpha, E = level + alpha;
+  const uint32_t dnum_l = (level + alpha - 1) / alpha;
+  auto ext_prime = [&](uint32_t row) { return c->primes[row < level ? row : L + (row - level)]; };
+  std::vector<uint64_t> ps(c->primes.begin() + L, c->primes.end());
+
+  std::vector<double2> mu_inv((size_t)dnum_l * alpha), mu_hat((size_t)dnum_l * E * alpha);
+  for (uint32_t j = 0; j < dnum_l; ++j) {
+    const uint32_t lo = j * alpha, hi = std::min(lo + alpha, level);
+    std::vector<uint64_t> dq(c->primes.begin() + lo, c->primes.begin() + hi);
+    for (uint32_t a = 0; a < hi - lo; ++a) {
+      mu_inv[j * alpha + a] = entry(h_inv(prod_mod_except(dq, a, dq[a]), dq[a]), dq[a]);
+      for (uint32_t row = 0; row < E; ++row) {
+        const uint64_t m = ext_prime(row);
+        mu_hat[((size_t)j * E + row) * alpha + a] = entry(prod_mod_except(dq, a, m), m);
+      }
+    }
+  }
+  std::vector<double2> md_inv(alpha), md_hat((size_t)level * alpha), md_pinv(level), pmod(L),
+      rs_inv(level);
+  for (uint32_t a = 0; a < alpha; ++a)
+    md_inv[a] = entry(h_inv(prod_mod_except(ps, a, ps[a]), ps[a]), ps[a]);
+  for (uint32_t i = 0; i < L; ++i) {
+    const uint64_t q = c->primes[i];
+    const uint64_t P = prod_mod_except(ps, ps.size(), q);
+    pmod[i] = entry(P, q);
+    if (i < level) {
+      md_pinv[i] = entry(h_inv(P, q), q);
+      for (uint32_t a = 0; a < alpha; ++a) md_hat[(size_t)i * alpha + a] = entry(prod_mod_except(ps, a, q), q);
+      if (i + 1 < level) rs_inv[i] = entry(h_inv(c->primes[level - 1] % q, q), q);
+    }
+  }
+  std::vector<double2> all;
+  LevelTables T;
+  T.level = level;
+  size_t off[7];
+  const std::vector<double2>* parts[7] = {&mu_inv, &mu_hat, &md_inv, &md_hat, &md_pinv, &pmod, &rs_inv};
+  for (int p = 0; p < 7; ++p) {
+    off[p] = all.size();
+    all.insert(all.end(), parts[p]->begin(), parts[p]->end());
+  }
+  double2* d = nullptr;
+  if (hipMalloc(&d, sizeof(double2) * all.size()) != hipSuccess) {
+    *err = fail(FESC_ERR_OOM, "level table allocation failed");
+    return nullptr;
+  }
+  if ((*err = hip_check(hipMemcpy(d, all.data(), sizeof(double2) * all.size(),
+                                  hipMemcpyHostToDevice), "hipMemcpy"))) {
+    hipFree(d);
+    return nullptr;
+  }
+  T.base = d;
+  T.mu_inv = d + off[0];
+  T.mu_hat = d + off[1];
+  T.md_inv = d + off[2];
+  T.md_hat = d + off[3];
+  T.md_pinv = d + off[4];
+  T.pmod = d + off[5];
+  T.rs_inv = d + off[6];
+  return &(c->level_tabs[level] = T);
+}
+
+// ------------------------------------------------------------------ scratch
+
+namespace {
+
+// One scratch layout, sized for the top level, shared by every operation.
+struct Scratch {
+  uint64_t* cin;  // [L][2][N]        private copy of an aliased input
+  uint64_t* cc;   // [L][N]           coefficient form of the switched polynomial
+  uint64_t* ext;  // [dnum][L+a][N]   ModUp output
+  uint64_t* acc;  // [2][L+a][N]      key inner products
+  uint64_t* y;    // [2][L][N]        ModDown conversion
+  uint64_t* d01;  // [L][2][N]        tensor (d0, d1)
+  uint64_t* d2;   // [L][N]           tensor d2
+  uint64_t* v;    // [2][N]           rescale: last limb
+  uint64_t* w;    // [2][L][N]        rescale: lifted last limb
+};
+
+int scratch(Context* c, Scratch* s) {
+  const size_t n = c->n, L = c->L, E = c->L + c->alpha;
+  const size_t sizes[9] = {2 * L * n, L * n, c->dnum * E * n, 2 * E * n, 2 * L * n,
+                           2 * L * n, L * n, 2 * n, 2 * L * n};
+  size_t total = 0;
+  for (size_t x : sizes) total += x;
+  int err;
+  uint64_t* base = static_cast<uint64_t*>(scratch_get(c, total * sizeof(uint64_t), &err));
+  if (!base) return err;
+  uint64_t** dst[9] = {&s->cin, &s->cc, &s->ext, &s->acc, &s->y, &s->d01, &s->d2, &s->v, &s->w};
+  for (int i = 0; i < 9; ++i) {
+    *dst[i] = base;
+    base += sizes[i];
+  }
+  return FESC_OK;
+}
+
+#define HIPCK(expr)                                   \
+  do {                                                \
+    hipError_t e_ = (expr);                           \
+    if (e_ != hipSuccess) return hip_check(e_, #expr); \
+  } while (0)
+
+hipError_t ntt_rows(const Context* c, uint64_t* d, uint32_t batch, size_t batch_stride,
+                    uint32_t limbs, uint32_t prime0, bool inverse, hipStream_t s) {
+  RowSel rs{d, batch_stride, (size_t)c->n, prime0, limbs, 0, 0, 0};
+  return launch_ntt_rows(c, rs, batch, limbs, inverse, s);
+}
+
+// ModUp of the polynomial whose row i is at in + i*in_stride (evaluation
+// form): cc <- inverse transform of a copy, ext <- converted digits, forward
+// transformed (own-digit rows are left to the inner product).
+int modup(Context* c, const LevelTables& T, const Scratch& S, const uint64_t* in,
+          size_t in_stride, uint32_t level, hipStream_t s) {
+  const size_t n = c->n;
+  HIPCK(hipMemcpy2DAsync(S.cc, n * 8, in, in_stride * 8, n * 8, level, hipMemcpyDeviceToDevice, s));
+  HIPCK(ntt_rows(c, S.cc, 1, 0, level, 0, true, s));
+  HIPCK(k_modup_launch(c, T, S.cc, S.ext, level, s));
+  const uint32_t E = level + c->alpha, dnum_l = (level + c->alpha - 1) / c->alpha;
+  RowSel rs{S.ext, (size_t)E * n, n, 0, level, c->L, c->alpha, level};
+  HIPCK(launch_ntt_rows(c, rs, dnum_l, E, false, s));
+  return FESC_OK;
+}
+
+// Inner product with `key` (sigma_g on the digits when galois != 0), ModDown,
+// and the combine into `out` (ciphertext layout).
+int ip_moddown(Context* c, const LevelTables& T, const Scratch& S, const uint64_t* in,
+               size_t in_stride, const uint64_t* key, uint32_t galois, const uint64_t* add,
+               uint32_t add_mask, uint32_t add_galois, uint64_t* out, uint32_t level,
+               hipStream_t s) {
+  const size_t n = c->n;
+  const uint32_t E = level + c->alpha;
+  HIPCK(k_ip_launch(c, S.ext, in, in_stride, key, S.acc, level, galois, s));
+  HIPCK(ntt_rows(c, S.acc + (size_t)level * n, 2, (size_t)E * n, c->alpha, c->L, true, s));
+  HIPCK(k_moddown_bconv_launch(c, T, S.acc, S.y, level, s));
+  HIPCK(ntt_rows(c, S.y, 2, (size_t)level * n, level, 0, false, s));
+  HIPCK(k_ks_combine_launch(c, T, S.acc, S.y, add, add_mask, add_galois, out, level, s));
+  return FESC_OK;
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------- drivers
+
+uint32_t galois_of_step(const Context* c, int32_t step) {
+  const uint64_t two_n = 2ull * c->n;
+  if (step == INT32_MIN) return (uint32_t)(two_n - 1);
+  const int64_t half = c->n / 2;
+  const int64_t r = ((int64_t)step % half + half) % half;
+  if (r == 0) return 1;
+  return (uint32_t)h_powmod(5, (uint64_t)r, two_n);
+}
+
+int op_rotate_many(Context* c, const uint64_t* in, uint32_t count, const int32_t* steps,
+                   uint64_t* const* outs, uint32_t level, hipStream_t s) {
+  const size_t n = c->n, ct_words = (size_t)2 * level * n;
+  std::vector<uint32_t> gal(count);
+  bool any = false;
+  for (uint32_t r = 0; r < count; ++r) {
+    gal[r] = galois_of_step(c, steps[r]);
+    if (gal[r] != 1) {
+      if (!c->keys.count(gal[r]))
+        return fail(FESC_ERR_NO_KEY, "no switching key for Galois element " + std::to_string(gal[r]));
+      any = true;
+    }
+  }
+  int err;
+  const LevelTables* T = level_tables(c, level, &err);
+  if (!T) return err;
+  Scratch S;
+  if ((err = scratch(c, &S))) return err;
+  // an output that aliases the input would be overwritten while later
+  // rotations still read the input: work from a private copy then
+  const uint64_t* src = in;
+  for (uint32_t r = 0; r < count; ++r)
+    if (outs[r] == in) {
+      HIPCK(hipMemcpyAsync(S.cin, in, ct_words * 8, hipMemcpyDeviceToDevice, s));
+      src = S.cin;
+      break;
+    }
+  if (any && (err = modup(c, *T, S, src + n, 2 * n, level, s))) return err;
+  for (uint32_t r = 0; r < count; ++r) {
+    if (gal[r] == 1) {
+      if (outs[r] != src)
+        HIPCK(hipMemcpyAsync(outs[r], src, ct_words * 8, hipMemcpyDeviceToDevice, s));
+      continue;
+    }
+    if ((err = ip_moddown(c, *T, S, src + n, 2 * n, c->keys[gal[r]], gal[r], src, 1u, gal[r],
+                          outs[r], level, s)))
+      return err;
+  }
+  return FESC_OK;
+}
+
+int op_mul_relin(Context* c, const uint64_t* a, const uint64_t* b, uint64_t* out,
+                 uint32_t level, hipStream_t s) {
+  auto it = c->keys.find(0);
+  if (it == c->keys.end()) return fail(FESC_ERR_NO_KEY, "no relinearisation key");
+  int err;
+  const LevelTables* T = level_tables(c, level, &err);
+  if (!T) return err;
+  Scratch S;
+  if ((err = scratch(c, &S))) return err;
+  HIPCK(k_tensor_launch(c, a, b, S.d01, S.d2, level, s));
+  if ((err = modup(c, *T, S, S.d2, c->n, level, s))) return err;
+  return ip_moddown(c, *T, S, S.d2, c->n, it->second, 0, S.d01, 3u, 0, out, level, s);
+}
+
+int op_rescale(Context* c, const uint64_t* in, uint64_t* out, uint32_t level, hipStream_t s) {
+  int err;
+  const LevelTables* T = level_tables(c, level, &err);
+  if (!T) return err;
+  Scratch S;
+  if ((err = scratch(c, &S))) return err;
+  const size_t n = c->n;
+  HIPCK(hipMemcpyAsync(S.v, in + (size_t)2 * (level - 1) * n, 2 * n * 8,
+                       hipMemcpyDeviceToDevice, s));
+  HIPCK(ntt_rows(c, S.v, 2, n, 1, level - 1, true, s));
+  HIPCK(k_rescale_lift_launch(c, S.v, S.w, level, s));
+  HIPCK(ntt_rows(c, S.w, 2, (size_t)(level - 1) * n, level - 1, 0, false, s));
+  HIPCK(k_rescale_combine_launch(c, in, S.w, out, level, T->rs_inv, s));
+  return FESC_OK;
+}
+
+int op_keygen(Context* c, uint32_t galois, const int8_t* sk, const uint64_t* a, const int64_t* e,
+              hipStream_t s) {
+  const size_t n = c->n;
+  const uint32_t E = c->L + c->alpha;
+  int err;
+  const LevelTables* T = level_tables(c, c->L, &err);
+  if (!T) return err;
+  Scratch S;
+  if ((err = scratch(c, &S))) return err;
+  uint64_t* key = nullptr;
+  auto it = c->keys.find(galois);
+  if (it != c->keys.end()) {
+    key = it->second;
+  } else {
+    if (hipMalloc(&key, (size_t)c->dnum * E * 2 * n * 8) != hipSuccess)
+      return fail(FESC_ERR_OOM, "key allocation failed");
+    c->keys[galois] = key;
+  }
+  uint64_t* s_ext = S.acc;            // [E][N]
+  uint64_t* s_from = S.acc + E * n;   // [E][N]
+  uint64_t* e_ntt = S.ext;            // [dnum][E][N]
+  HIPCK(k_lift_launch(c, nullptr, sk, s_ext, E, 0, E, 0, s));
+  HIPCK(ntt_rows(c, s_ext, 1, 0, E, 0, false, s));
+  if (galois == 0)
+    HIPCK(k_binary_launch(c, s_ext, s_ext, s_from, E, 0, 2, s));
+  else
+    HIPCK(k_galois_launch(c, s_ext, s_from, E, galois, s));
+  for (uint32_t j = 0; j < c->dnum; ++j)
+    HIPCK(k_lift_launch(c, e + (size_t)j * n, nullptr, e_ntt + (size_t)j * E * n, E, 0, E, 0, s));
+  HIPCK(ntt_rows(c, e_ntt, c->dnum, (size_t)E * n, E, 0, false, s));
+  HIPCK(k_keygen_launch(c, a, e_ntt, s_ext, s_from, key, T->pmod, s));
+  return FESC_OK;
+}
+
+int op_encrypt(Context* c, const int8_t* sk, const int64_t* m, const uint64_t* a,
+               const int64_t* e, uint64_t* ct, uint32_t level, hipStream_t s) {
+  Scratch S;
+  int err;
+  if ((err = scratch(c, &S))) return err;
+  const size_t n = c->n;
+  uint64_t* me = S.cc;
+  uint64_t* et = S.y;
+  uint64_t* sl = S.d2;
+  HIPCK(k_lift_launch(c, m, nullptr, me, level, 0, level, 0, s));
+  HIPCK(k_lift_launch(c, e, nullptr, et, level, 0, level, 0, s));
+  HIPCK(k_binary_launch(c, me, et, me, level, 0, 0, s));
+  HIPCK(ntt_rows(c, me, 1, 0, level, 0, false, s));
+  HIPCK(k_lift_launch(c, nullptr, sk, sl, level, 0, level, 0, s));
+  HIPCK(ntt_rows(c, sl, 1, 0, level, 0, false, s));
+  HIPCK(k_encrypt_launch(c, a, sl, me, ct, level, s));
+  (void)n;
+  return FESC_OK;
+}
+
+int op_plain_from_coeffs(Context* c, const int64_t* m, uint64_t* pt, uint32_t level,
+                         hipStream_t s) {
+  HIPCK(k_lift_launch(c, m, nullptr, pt, level, 0, level, 0, s));
+  HIPCK(ntt_rows(c, pt, 1, 0, level, 0, false, s));
+  return FESC_OK;
+}
+
+}  // namespace fesc

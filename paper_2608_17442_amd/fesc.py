@@ -40,7 +40,25 @@ _SIGS = {
     "fesc_ntt_fwd": [_vp, _vp, _u32, _sz, _u32, _sz, _u32, _vp],
     "fesc_ntt_inv": [_vp, _vp, _u32, _sz, _u32, _sz, _u32, _vp],
     "fesc_mac": [_vp, _vp, _vp, _vp, _u32, _sz, _u32, _u32, _vp],
+    "fesc_add": [_vp, _vp, _vp, _vp, _u32, _vp],
+    "fesc_sub": [_vp, _vp, _vp, _vp, _u32, _vp],
+    "fesc_mul_plain": [_vp, _vp, _vp, _vp, _u32, _vp],
+    "fesc_mul_monomial": [_vp, _vp, _vp, _u32, _u32, _vp],
+    "fesc_mul_relin": [_vp, _vp, _vp, _vp, _u32, _vp],
+    "fesc_rescale": [_vp, _vp, _vp, _u32, _vp],
+    "fesc_galois_element": [_vp, _i32, ctypes.POINTER(_u32)],
+    "fesc_rotate": [_vp, _vp, _vp, _u32, _i32, _vp],
+    "fesc_rotate_hoisted": [_vp, _vp, _u32, ctypes.POINTER(_i32), ctypes.POINTER(_vp), _u32,
+                            _vp],
+    "fesc_keygen": [_vp, _u32, _vp, _vp, _vp, _vp],
+    "fesc_key_load": [_vp, _u32, _vp, _vp],
+    "fesc_key_store": [_vp, _u32, _vp, _vp],
+    "fesc_encrypt_sk": [_vp, _vp, _vp, _vp, _vp, _vp, _u32, _vp],
+    "fesc_plain_from_coeffs": [_vp, _vp, _vp, _u32, _vp],
+    "fesc_encode": [_u32, _vp, _vp, ctypes.c_double, _vp],
 }
+
+CONJ = -(2 ** 31)
 
 for _name, _args in _SIGS.items():
     _f = getattr(_lib, _name)
@@ -65,8 +83,8 @@ def _check(rc: int) -> int:
 def _ptr(t) -> int:
     if t is None:
         return None
-    assert isinstance(t, torch.Tensor) and t.is_cuda and t.dtype == torch.int64, \
-        "device buffers are CUDA int64 tensors"
+    assert isinstance(t, torch.Tensor) and t.is_cuda and t.dtype in (torch.int64, torch.int8), \
+        "device buffers are CUDA int64 (residues, coefficients) or int8 (secret) tensors"
     assert t.is_contiguous()
     return t.data_ptr()
 
@@ -132,3 +150,117 @@ class Context:
     def mac(self, a, b, out, pairs, pair_stride, limbs, prime0, stream=None):
         _check(_lib.fesc_mac(self._h, _ptr(a), _ptr(b), _ptr(out), pairs, pair_stride, limbs,
                              prime0, _stream(stream)))
+
+    # -- ciphertext operations -------------------------------------------
+
+    def add(self, a, b, out, level, stream=None):
+        _check(_lib.fesc_add(self._h, _ptr(a), _ptr(b), _ptr(out), level, _stream(stream)))
+
+    def sub(self, a, b, out, level, stream=None):
+        _check(_lib.fesc_sub(self._h, _ptr(a), _ptr(b), _ptr(out), level, _stream(stream)))
+
+    def mul_plain(self, ct, pt, out, level, stream=None):
+        _check(_lib.fesc_mul_plain(self._h, _ptr(ct), _ptr(pt), _ptr(out), level,
+                                   _stream(stream)))
+
+    def mul_monomial(self, ct, out, level, k, stream=None):
+        _check(_lib.fesc_mul_monomial(self._h, _ptr(ct), _ptr(out), level, k, _stream(stream)))
+
+    def mul_relin(self, a, b, out, level, stream=None):
+        _check(_lib.fesc_mul_relin(self._h, _ptr(a), _ptr(b), _ptr(out), level,
+                                   _stream(stream)))
+
+    def rescale(self, ct, out, level, stream=None):
+        _check(_lib.fesc_rescale(self._h, _ptr(ct), _ptr(out), level, _stream(stream)))
+
+    def galois_element(self, step: int) -> int:
+        v = _u32()
+        _check(_lib.fesc_galois_element(self._h, step, ctypes.byref(v)))
+        return int(v.value)
+
+    def rotate(self, ct, out, level, step, stream=None):
+        _check(_lib.fesc_rotate(self._h, _ptr(ct), _ptr(out), level, step, _stream(stream)))
+
+    def rotate_hoisted(self, ct, steps, outs, level, stream=None):
+        st = (_i32 * len(steps))(*steps)
+        ptrs = (_vp * len(outs))(*[_ptr(o) for o in outs])
+        _check(_lib.fesc_rotate_hoisted(self._h, _ptr(ct), len(steps), st, ptrs, level,
+                                        _stream(stream)))
+
+    def keygen(self, galois_elt, s, a, e, stream=None):
+        _check(_lib.fesc_keygen(self._h, galois_elt, _ptr(s), _ptr(a), _ptr(e), _stream(stream)))
+
+    def key_load(self, galois_elt, key, stream=None):
+        _check(_lib.fesc_key_load(self._h, galois_elt, _ptr(key), _stream(stream)))
+
+    def key_store(self, galois_elt, key, stream=None):
+        _check(_lib.fesc_key_store(self._h, galois_elt, _ptr(key), _stream(stream)))
+
+    def encrypt_sk(self, s, m, a, e, ct, level, stream=None):
+        _check(_lib.fesc_encrypt_sk(self._h, _ptr(s), _ptr(m), _ptr(a), _ptr(e), _ptr(ct), level,
+                                    _stream(stream)))
+
+    def plain_from_coeffs(self, m, pt, level, stream=None):
+        _check(_lib.fesc_plain_from_coeffs(self._h, _ptr(m), _ptr(pt), level, _stream(stream)))
+
+    def key_words(self) -> int:
+        return self.dnum * (self.L + self.alpha) * 2 * self.n
+
+
+def encode(log_n: int, z, scale: float):
+    """Host encoder: complex slot vector (length N/2) -> int64 coefficients."""
+    import numpy as np
+    z = np.asarray(z, dtype=np.complex128)
+    re = np.ascontiguousarray(z.real)
+    im = np.ascontiguousarray(z.imag)
+    out = np.empty(1 << log_n, dtype=np.int64)
+    _check(_lib.fesc_encode(log_n, re.ctypes.data, im.ctypes.data, float(scale),
+                            out.ctypes.data))
+    return out
+
+
+class _MatvecDesc(ctypes.Structure):
+    _fields_ = [(f, _u32) for f in ("level", "n_in", "n_out", "n1", "n2", "unit",
+                                    "real_extract", "rescale")]
+
+
+_lib.fesc_matvec_plan_create.argtypes = [_vp, ctypes.POINTER(_MatvecDesc), ctypes.POINTER(_vp),
+                                         ctypes.POINTER(_vp)]
+_lib.fesc_matvec_plan_create.restype = ctypes.c_int
+_lib.fesc_matvec_plan_destroy.argtypes = [_vp]
+_lib.fesc_matvec_plan_destroy.restype = None
+_lib.fesc_ptct_matvec.argtypes = [_vp, _vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp), _vp]
+_lib.fesc_ptct_matvec.restype = ctypes.c_int
+
+
+class MatvecPlan:
+    """BSGS projection plan over pre-encoded diagonals ``diags[b][p][u][q]``
+    (a flat list in that order of device plaintexts, kept alive here)."""
+
+    def __init__(self, ctx: Context, level, n_in, n_out, n1, n2, unit, real_extract, rescale,
+                 diags):
+        self.ctx = ctx
+        self.desc = _MatvecDesc(level, n_in, n_out, n1, n2, unit, int(real_extract),
+                                int(rescale))
+        self._diags = list(diags)
+        arr = (_vp * len(self._diags))(*[_ptr(t) for t in self._diags])
+        h = _vp()
+        _check(_lib.fesc_matvec_plan_create(ctx._h, ctypes.byref(self.desc), arr,
+                                            ctypes.byref(h)))
+        self._h = h
+
+    def __call__(self, ins, outs, stream=None):
+        a = (_vp * len(ins))(*[_ptr(t) for t in ins])
+        b = (_vp * len(outs))(*[_ptr(t) for t in outs])
+        _check(_lib.fesc_ptct_matvec(self.ctx._h, self._h, a, b, _stream(stream)))
+
+    def close(self):
+        if getattr(self, "_h", None):
+            _lib.fesc_matvec_plan_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

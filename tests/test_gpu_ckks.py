@@ -1,0 +1,205 @@
+"""GPU parity of the ciphertext operations against the oracle: key
+generation, encryption, add / sub / ptmul / monomial, rescale, rotation
+(plain, hoisted, conjugation, identity, in place) and ctmul + relinearisation.
+Every comparison is on raw residues (bit-exact); a decrypt check confirms the
+values as well."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import ckks as C
+from tests.gpu_helpers import first_mismatch, need_gpu, step, to_dev, to_host
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    need_gpu()
+
+
+class Setup:
+    """One parameter set on both sides, with keys generated from the same
+    draws on the GPU and in the oracle."""
+
+    def __init__(self, P, seed, rot_steps=(), relin=False, conj=False):
+        from paper_2608_17442_amd import fesc as F
+        self.P, self.seed = P, seed
+        self.ctx = F.Context(P.log_n, P.q, P.p)
+        s = synth.secret(seed, P.n)
+        self.s_dev = torch.from_numpy(s).cuda()
+        self.sk = C.secret_key(P, s)
+        elts = {P.galois_elt(r) for r in rot_steps if r % (P.n // 2)}
+        if conj:
+            elts.add(P.conj_elt)
+        if relin:
+            elts.add(0)
+        self.keys = {}
+        for g in sorted(elts):
+            a, e = synth.switch_key_draws(seed, P.ext(P.L), P.n, P.dnum, g)
+            step(f"keygen g={g} log_n={P.log_n}")
+            self.ctx.keygen(g, self.s_dev, to_dev(a), torch.from_numpy(e).cuda())
+            self.keys[g] = C.relin_key(P, self.sk, a, e) if g == 0 else \
+                C.galois_key(P, self.sk, g, a, e)
+
+    def encrypt(self, z, scale, level, idx):
+        """Encrypt on both sides from the same draws; returns (oracle, device)."""
+        P = self.P
+        m = C.enc.encode(np.asarray(z, dtype=np.complex128), scale, P.n)
+        a, e = synth.encrypt_draws(self.seed, P.qs(level), P.n, "gpu", idx)
+        ct_o = C.encrypt(P, self.sk, C.ntt(P, C.lift(m, P.qs(level)), P.qs(level)), level, a, e)
+        ct_d = torch.zeros(level * 2 * P.n, dtype=torch.int64, device="cuda")
+        step(f"encrypt level={level} idx={idx}")
+        self.ctx.encrypt_sk(self.s_dev, torch.from_numpy(m).cuda(), to_dev(a),
+                            torch.from_numpy(e).cuda(), ct_d, level)
+        return ct_o, ct_d
+
+
+def _z(seed, n_slots):
+    return synth.uniform_pm1(seed, "zr", n_slots) + 1j * synth.uniform_pm1(seed, "zi", n_slots)
+
+
+def _eq(dev, want, what):
+    got = to_host(dev).reshape(want.shape)
+    assert np.array_equal(got, want), f"{what}: {first_mismatch(got, want)}"
+
+
+SMALL = [(12, 50, 5, 2), (13, 45, 4, 3)]
+
+
+@pytest.mark.parametrize("log_n,bits,L,alpha", SMALL)
+def test_keygen_encrypt_elementwise_rescale(log_n, bits, L, alpha):
+    P = C.params_small(log_n, bits, L, alpha)
+    S = Setup(P, 11, rot_steps=[3], relin=True)
+    for g, kw in S.keys.items():
+        d = torch.zeros(S.ctx.key_words(), dtype=torch.int64, device="cuda")
+        S.ctx.key_store(g, d)
+        _eq(d, kw, f"switching key g={g}")
+    level = L
+    z1, z2, w = _z(1, P.n // 2), _z(2, P.n // 2), _z(3, P.n // 2)
+    c1o, c1d = S.encrypt(z1, 2.0 ** 30, level, 1)
+    _eq(c1d, c1o, "encrypt")
+    c2o, c2d = S.encrypt(z2, 2.0 ** 30, level, 2)
+    out = torch.zeros_like(c1d)
+    step("add/sub")
+    S.ctx.add(c1d, c2d, out, level)
+    _eq(out, C.ct_add(P, c1o, c2o), "add")
+    S.ctx.sub(c1d, c2d, out, level)
+    _eq(out, C.ct_sub(P, c1o, c2o), "sub")
+    # plaintext from coefficients and ptmul (in place)
+    m = C.enc.encode(w, float(P.q[level - 1]), P.n)
+    pt = torch.zeros(level * P.n, dtype=torch.int64, device="cuda")
+    S.ctx.plain_from_coeffs(torch.from_numpy(m).cuda(), pt, level)
+    pto = C.ntt(P, C.lift(m, P.qs(level)), P.qs(level))
+    _eq(pt, pto, "plaintext")
+    prod = c1d.clone()
+    step("mul_plain in place")
+    S.ctx.mul_plain(prod, pt, prod, level)
+    prod_o = C.mul_plain(P, c1o, pto)
+    _eq(prod, prod_o, "mul_plain")
+    for k in [0, 1, 7, P.n // 2, 3 * P.n // 2, 2 * P.n - 1]:
+        S.ctx.mul_monomial(c1d, out, level, k)
+        _eq(out, C.mul_monomial(P, c1o, k), f"monomial k={k}")
+    step("rescale in place")
+    rs = prod.clone()
+    S.ctx.rescale(rs, rs, level)
+    rs_o = C.rescale(P, prod_o)
+    _eq(rs[: (level - 1) * 2 * P.n], rs_o, "rescale")
+    np.testing.assert_allclose(C.decrypt(P, S.sk, rs_o, 2.0 ** 30), z1 * w, atol=2.0 ** -12)
+
+
+@pytest.mark.parametrize("log_n,bits,L,alpha", SMALL)
+def test_rotations_conjugation_hoisted(log_n, bits, L, alpha):
+    P = C.params_small(log_n, bits, L, alpha)
+    steps = [1, 5, -3, P.n // 2 - 1]
+    S = Setup(P, 12, rot_steps=steps, conj=True)
+    F = S.ctx
+    for level in [L, 2, 1]:
+        z = _z(10 + level, P.n // 2)
+        co, cd = S.encrypt(z, 2.0 ** 30, level, 100 + level)
+        out = torch.zeros_like(cd)
+        for r in steps + [0, P.n // 2]:
+            step(f"rotate level={level} step={r}")
+            F.rotate(cd, out, level, r)
+            want = C.rotate(P, co, r, S.keys)
+            _eq(out, want, f"rotate level={level} step={r}")
+        from paper_2608_17442_amd.fesc import CONJ
+        F.rotate(cd, out, level, CONJ)
+        want_c = C.conjugate(P, co, S.keys)
+        _eq(out, want_c, f"conjugate level={level}")
+        # value check only (scale 2^30 with key-switch noise ~2^16)
+        np.testing.assert_allclose(C.decrypt(P, S.sk, want_c, 2.0 ** 30), np.conj(z),
+                                   atol=2.0 ** -11)
+        # hoisted: all steps from one ModUp, equal to the plain rotations
+        outs = [torch.zeros_like(cd) for _ in steps + [0]]
+        step(f"hoisted level={level}")
+        F.rotate_hoisted(cd, steps + [0], outs, level)
+        wants = C.rotate_hoisted(P, co, steps + [0], S.keys)
+        for r, o, w in zip(steps + [0], outs, wants):
+            _eq(o, w, f"hoisted level={level} step={r}")
+        # in place
+        inplace = cd.clone()
+        F.rotate(inplace, inplace, level, steps[0])
+        _eq(inplace, C.rotate(P, co, steps[0], S.keys), "rotate in place")
+
+
+@pytest.mark.parametrize("log_n,bits,L,alpha", SMALL)
+def test_mul_relin(log_n, bits, L, alpha):
+    P = C.params_small(log_n, bits, L, alpha)
+    S = Setup(P, 13, relin=True)
+    for level in [L, 1]:
+        z1, z2 = _z(20 + level, P.n // 2), _z(30 + level, P.n // 2)
+        ao, ad = S.encrypt(z1, 2.0 ** 20, level, 200 + level)
+        bo, bd = S.encrypt(z2, 2.0 ** 20, level, 300 + level)
+        out = torch.zeros_like(ad)
+        step(f"mul_relin level={level}")
+        S.ctx.mul_relin(ad, bd, out, level)
+        want = C.mul_relin(P, ao, bo, S.keys[0])
+        _eq(out, want, f"mul_relin level={level}")
+        # aliasing the first operand
+        S.ctx.mul_relin(ad, bd, ad, level)
+        _eq(ad, want, "mul_relin in place")
+        # value check only: operands at scale 2^20 carry encryption noise ~2^-15
+        np.testing.assert_allclose(C.decrypt(P, S.sk, want, 2.0 ** 40), z1 * z2, atol=2.0 ** -7)
+
+
+def test_error_codes():
+    from paper_2608_17442_amd import fesc as F
+    P = C.params_small(12, 50, 3, 1)
+    ctx = F.Context(P.log_n, P.q, P.p)
+    ct = torch.zeros(3 * 2 * P.n, dtype=torch.int64, device="cuda")
+    with pytest.raises(F.FescError) as e:
+        ctx.rotate(ct, ct, 3, 1)
+    assert e.value.code == -3          # no key
+    with pytest.raises(F.FescError) as e:
+        ctx.rescale(ct, ct, 1)
+    assert e.value.code == -2          # level
+    with pytest.raises(F.FescError) as e:
+        ctx.mul_plain(ct, ct, ct, 4)
+    assert e.value.code == -2
+    with pytest.raises(F.FescError) as e:
+        ctx.mul_relin(ct, ct, ct, 2)
+    assert e.value.code == -3
+    assert torch.count_nonzero(ct).item() == 0
+
+
+def test_cfg3_full_size_rotations():
+    """N = 2^16, 24 limbs, dnum 3 with 8 special primes: fresh ciphertexts
+    rotated by powers of two (and the identity step 2^15), every residue
+    compared with the oracle."""
+    import synth.workloads as WL
+    P = C.params_p16()
+    idx = [0, 5, 15]                            # steps 1, 32, 2^15 (identity)
+    steps = [WL.cfg3_steps()[i] for i in idx]
+    S = Setup(P, WL.CFG3["seed"], rot_steps=steps)
+    for i, r in zip(idx, steps):
+        z = WL.cfg3_slots(i, P.n // 2)
+        co, cd = S.encrypt(z, 2.0 ** 40, 24, i)
+        out = torch.zeros_like(cd)
+        step(f"cfg3 rotate ct {i} by {r}")
+        S.ctx.rotate(cd, out, 24, r)
+        want = C.rotate(P, co, r, S.keys)
+        _eq(out, want, f"cfg3 rotate {r}")
+        got = C.decrypt(P, S.sk, want, 2.0 ** 40)
+        assert np.max(np.abs(got - np.roll(z, -r))) < 2.0 ** -15

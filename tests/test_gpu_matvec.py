@@ -1,0 +1,97 @@
+"""GPU parity of the plaintext-matrix x ciphertext projection (BSGS) against
+the oracle, on the N = 2^12 diagonal-method workload (64 x 64 matrix, 63
+hoisted rotations, rescale) and on a complex-paired BSGS instance with
+several inputs, outputs and giant steps."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+import synth.workloads as WL
+from oracle import ckks as C
+from oracle import workloads as OW
+from tests.gpu_helpers import first_mismatch, need_gpu, step, to_dev, to_host
+from tests.test_gpu_ckks import Setup
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    need_gpu()
+
+
+def _run(P, S, desc, X_slots, scale_x, diag_slots, scale_d, seed_tag):
+    """Encrypt inputs, encode diagonals, run both sides; returns (oracle outs,
+    device outs)."""
+    from paper_2608_17442_amd import fesc as F
+    level = desc.level
+    ins_o, ins_d = [], []
+    for u, z in enumerate(X_slots):
+        co, cd = S.encrypt(z, scale_x, level, 1000 + u)
+        ins_o.append(co)
+        ins_d.append(cd)
+    keys_needed = OW.required_rotations(desc, P.n // 2)
+    diag_pt = {}
+    flat = []
+    for b in range(desc.n_out):
+        for p in range(desc.n2):
+            for u in range(desc.n_in):
+                for q in range(desc.n1):
+                    pt = C.encode_plain(P, diag_slots(b, p, u, q), scale_d, level)
+                    diag_pt[(b, p, u, q)] = pt
+                    flat.append(to_dev(pt))
+    step(f"matvec plan n_in={desc.n_in} n_out={desc.n_out} n1={desc.n1} n2={desc.n2}")
+    plan = F.MatvecPlan(S.ctx, desc.level, desc.n_in, desc.n_out, desc.n1, desc.n2, desc.unit,
+                        desc.real_extract, desc.rescale, flat)
+    out_level = level - 1 if desc.rescale else level
+    outs_d = [torch.zeros(out_level * 2 * P.n, dtype=torch.int64, device="cuda")
+              for _ in range(desc.n_out)]
+    step("matvec run")
+    plan(ins_d, outs_d)
+    outs_o = OW.bsgs_matvec(P, desc, ins_o, lambda b, p, u, q: diag_pt[(b, p, u, q)], S.keys)
+    assert keys_needed <= {r for r in range(P.n // 2)}
+    return outs_o, outs_d
+
+
+def test_cfg1_diagonal_matvec():
+    """N = 2^12, q0..q2 + one special prime, 64 x 64 U[-1,1] matrix at scale
+    2^30 times x replicated to 2048 slots (ciphertext at scale q_2)."""
+    P = C.params_p12()
+    U, x = WL.cfg1_values()
+    d = WL.CFG1["dim"]
+    n_slots = P.n // 2
+    desc = OW.MatvecDesc(3, 1, 1, d, 1, 1, False, True)
+    S = Setup(P, WL.CFG1["seed"], rot_steps=list(range(1, d)))
+    xs = [np.tile(x, n_slots // d).astype(complex)]
+    diag = lambda b, p, u, q: OW.bsgs_diagonal_slots(U.T, n_slots, 1, d, d, b, p, u, q, False)
+    outs_o, outs_d = _run(P, S, desc, xs, float(P.q[2]), diag, 2.0 ** 30, "cfg1")
+    got = to_host(outs_d[0]).reshape(outs_o[0].shape)
+    assert np.array_equal(got, outs_o[0]), first_mismatch(got, outs_o[0])
+    dec = C.decrypt(P, S.sk, outs_o[0], 2.0 ** 30)
+    err = np.max(np.abs(dec - np.tile(U @ x, n_slots // d)))
+    print(f"cfg1 max |decoded - fp64| = {err:.3e} (2^{np.log2(err):.1f})")
+    assert err <= 2.0 ** -15
+
+
+def test_paired_bsgs_small():
+    P = C.params_small(12, 50, 5, 2)
+    n_slots, seg_len, Cc = P.n // 2, 64, 32
+    T, d_in, d_out, n1, n2 = 64, 128, 64, 8, 4
+    level = 4
+    X = synth.normal(21, "X", (T, d_in))
+    Wm = synth.normal(21, "W", (d_in, d_out), 0.02)
+    desc = OW.MatvecDesc(level, d_in // Cc // 2, d_out // Cc, n1, n2, seg_len, True, True)
+    S = Setup(P, 21, rot_steps=sorted(OW.required_rotations(desc, n_slots)), conj=True)
+    xs = [OW.pack_input(X, n_slots, seg_len, Cc, 2 * u)
+          + 1j * OW.pack_input(X, n_slots, seg_len, Cc, 2 * u + 1) for u in range(desc.n_in)]
+    diag = lambda b, p, u, q: OW.bsgs_diagonal_slots(Wm, n_slots, seg_len, Cc, n1, b, p, u, q,
+                                                     True)
+    outs_o, outs_d = _run(P, S, desc, xs, 2.0 ** 40, diag, float(P.q[level - 1]), "bsgs")
+    Y = X @ Wm
+    r, s = OW.segment_indices(n_slots, seg_len, Cc)
+    for b in range(desc.n_out):
+        got = to_host(outs_d[b]).reshape(outs_o[b].shape)
+        assert np.array_equal(got, outs_o[b]), f"block {b}: {first_mismatch(got, outs_o[b])}"
+        dec = C.decrypt(P, S.sk, outs_o[b], 2.0 ** 40)
+        assert np.max(np.abs(dec.real - Y[r, b * Cc + s])) <= 2.0 ** -15
