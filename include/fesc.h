@@ -218,6 +218,33 @@ void fesc_matvec_plan_destroy(fesc_matvec_plan* plan);
 int fesc_ptct_matvec(fesc_ctx* ctx, fesc_matvec_plan* plan, const uint64_t* const* in,
                      uint64_t* const* out, void* stream);
 
+/* Phase durations of the plan's last completed run, from HIP events recorded
+ * on its stream: baby steps, pt-MAC (one kernel), giant steps + extraction +
+ * rescale.  The caller synchronises first; FESC_ERR_HIP if not complete. */
+int fesc_matvec_phase_ms(const fesc_matvec_plan* plan, float* baby_ms, float* ptmac_ms,
+                         float* tail_ms);
+
+/* ------------------------------------------------------------------------
+ * Scan-contract slice of one token (paper Eq. "hescan-contract-output" and
+ * Appendix "Complex-Packed Reduction Accounting").  For each state chunk k
+ * (inputs at `level` >= 3: state h_k, broadcast decay a_k, broadcast output
+ * factor C_k, each [level][2][N]):
+ *     t_k = RS(relin(RS(relin(a_k * h_k)) * C_k))              (level - 2)
+ * Chunks are paired (2l, 2l+1) as chi = t_2l + i t_2l+1 (i = X^(N/2)),
+ * reduced over a contiguous d_state axis by rotate-and-add with steps
+ * d_state/2, ..., 1 (slot e*d_state then holds the sum over the axis), and
+ * split by one conjugation:
+ *     out[2l]   = Xi + conj(Xi)        = 2 Sigma(t_2l)
+ *     out[2l+1] = -i (Xi - conj(Xi))   = 2 Sigma(t_2l+1)
+ * (the factor 2 belongs to the caller's scale bookkeeping).  An odd last
+ * chunk is reduced alone.  h, decay, cfac, out: host arrays of `chunks`
+ * device pointers; outputs are [level-2][2][N] and must not alias inputs.
+ * Needs the relinearisation key, the rotation keys of the reduction steps
+ * and (chunks >= 2) the conjugation key; FESC_ERR_NO_KEY otherwise. */
+int fesc_scan_contract(fesc_ctx* ctx, const uint64_t* const* h, const uint64_t* const* decay,
+                       const uint64_t* const* cfac, uint32_t chunks, uint32_t d_state,
+                       uint64_t* const* out, uint32_t level, void* stream);
+
 /* Host helper: CKKS encoding of n = N/2 complex slots (re, im host arrays;
  * im may be NULL) at scale Delta into int64 coefficients, rounded half away
  * from zero; slot j is the evaluation at exp(i pi 5^j / N).  FESC_ERR_ARG if

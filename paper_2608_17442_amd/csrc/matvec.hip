@@ -26,6 +26,7 @@ struct fesc_matvec_plan {
   const uint64_t** d_baby = nullptr;  // device table of baby pointers
   uint64_t** d_ct = nullptr;          // device table of c~ pointers
   size_t ct_words = 0;
+  hipEvent_t ev[4] = {};               // phase marks of the last run
 };
 
 namespace fesc {
@@ -144,6 +145,7 @@ int matvec_plan_create(Context* c, const fesc_matvec_desc* d, const uint64_t* co
     delete p;
     return fail(FESC_ERR_OOM, "matvec workspace allocation failed");
   }
+  for (auto& e : p->ev) hipEventCreate(&e);
   *out = p;
   return FESC_OK;
 }
@@ -155,6 +157,8 @@ void matvec_plan_destroy(fesc_matvec_plan* p) {
   hipFree(p->d_diag);
   hipFree(p->d_baby);
   hipFree(p->d_ct);
+  for (auto& e : p->ev)
+    if (e) hipEventDestroy(e);
   delete p;
 }
 
@@ -167,6 +171,7 @@ int ptct_matvec(Context* c, fesc_matvec_plan* p, const uint64_t* const* in,
   uint64_t* ct = p->work + n_baby * W;
   uint64_t* tmp = ct + (size_t)d.n_out * d.n2 * W;
   int err;
+  HIPCK(hipEventRecord(p->ev[0], s));
   // baby steps, hoisted per input
   std::vector<int32_t> steps(d.n1);
   std::vector<uint64_t*> bouts(d.n1);
@@ -175,12 +180,14 @@ int ptct_matvec(Context* c, fesc_matvec_plan* p, const uint64_t* const* in,
     for (uint32_t q = 0; q < d.n1; ++q) bouts[q] = baby + ((size_t)u * d.n1 + q) * W;
     if ((err = op_rotate_many(c, in[u], d.n1, steps.data(), bouts.data(), level, s))) return err;
   }
+  HIPCK(hipEventRecord(p->ev[1], s));
   // pt-MAC over all (b, p)
   const uint32_t n_outputs = d.n_out * d.n2;
   dim3 grid((c->n + kThreads - 1) / kThreads, level, (n_outputs + kGroup - 1) / kGroup);
   hipLaunchKernelGGL(k_ptmac<kGroup>, grid, dim3(kThreads), 0, s, p->d_baby, p->d_diag, p->d_ct,
                      n_outputs, (uint32_t)n_baby, c->n, c->d_pk);
   HIPCK(hipGetLastError());
+  HIPCK(hipEventRecord(p->ev[2], s));
   // giant steps, real extraction, rescale
   for (uint32_t b = 0; b < d.n_out; ++b) {
     uint64_t* y = ct + (size_t)b * d.n2 * W;
@@ -201,6 +208,7 @@ int ptct_matvec(Context* c, fesc_matvec_plan* p, const uint64_t* const* in,
       HIPCK(hipMemcpyAsync(out[b], y, W * 8, hipMemcpyDeviceToDevice, s));
     }
   }
+  HIPCK(hipEventRecord(p->ev[3], s));
   return FESC_OK;
 }
 
@@ -224,6 +232,17 @@ int fesc_ptct_matvec(fesc_ctx* ctx, fesc_matvec_plan* plan, const uint64_t* cons
   for (uint32_t b = 0; b < plan->d.n_out; ++b)
     if (!out[b]) return fesc::fail(FESC_ERR_ARG, "null output");
   return fesc::ptct_matvec(ctx, plan, in, out, reinterpret_cast<hipStream_t>(stream));
+}
+
+int fesc_matvec_phase_ms(const fesc_matvec_plan* plan, float* baby_ms, float* ptmac_ms,
+                         float* tail_ms) {
+  if (!plan || !baby_ms || !ptmac_ms || !tail_ms) return fesc::fail(FESC_ERR_ARG, "null argument");
+  float* dst[3] = {baby_ms, ptmac_ms, tail_ms};
+  for (int i = 0; i < 3; ++i) {
+    hipError_t e = hipEventElapsedTime(dst[i], plan->ev[i], plan->ev[i + 1]);
+    if (e != hipSuccess) return fesc::hip_check(e, "matvec phase timing");
+  }
+  return FESC_OK;
 }
 
 }  // extern "C"

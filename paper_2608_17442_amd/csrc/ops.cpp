@@ -105,19 +105,21 @@ struct Scratch {
   uint64_t* d2;   // [L][N]           tensor d2
   uint64_t* v;    // [2][N]           rescale: last limb
   uint64_t* w;    // [2][L][N]        rescale: lifted last limb
+  uint64_t* ws;   // [3][L][2][N]     ciphertexts of composite operations
 };
 
 int scratch(Context* c, Scratch* s) {
   const size_t n = c->n, L = c->L, E = c->L + c->alpha;
-  const size_t sizes[9] = {2 * L * n, L * n, c->dnum * E * n, 2 * E * n, 2 * L * n,
-                           2 * L * n, L * n, 2 * n, 2 * L * n};
+  const size_t sizes[10] = {2 * L * n, L * n, c->dnum * E * n, 2 * E * n, 2 * L * n,
+                            2 * L * n, L * n, 2 * n, 2 * L * n, 6 * L * n};
   size_t total = 0;
   for (size_t x : sizes) total += x;
   int err;
   uint64_t* base = static_cast<uint64_t*>(scratch_get(c, total * sizeof(uint64_t), &err));
   if (!base) return err;
-  uint64_t** dst[9] = {&s->cin, &s->cc, &s->ext, &s->acc, &s->y, &s->d01, &s->d2, &s->v, &s->w};
-  for (int i = 0; i < 9; ++i) {
+  uint64_t** dst[10] = {&s->cin, &s->cc,  &s->ext, &s->acc, &s->y,
+                        &s->d01, &s->d2,  &s->v,   &s->w,   &s->ws};
+  for (int i = 0; i < 10; ++i) {
     *dst[i] = base;
     base += sizes[i];
   }
@@ -309,6 +311,56 @@ int op_plain_from_coeffs(Context* c, const int64_t* m, uint64_t* pt, uint32_t le
                          hipStream_t s) {
   HIPCK(k_lift_launch(c, m, nullptr, pt, level, 0, level, 0, s));
   HIPCK(ntt_rows(c, pt, 1, 0, level, 0, false, s));
+  return FESC_OK;
+}
+
+}  // namespace fesc
+
+namespace fesc {
+
+// Scan-contract slice of one token (see fesc.h): per chunk k,
+//   t2_k = RS(relin(RS(relin(decay_k * h_k)) * c_k)),
+// chunk pairs packed as chi = t2_2l + i t2_2l+1, reduced over the d_s axis by
+// rotate-and-add, and split by one conjugation into 2 Sigma(t2_2l) and
+// 2 Sigma(t2_2l+1).
+int op_scan_contract(Context* c, const uint64_t* const* h, const uint64_t* const* decay,
+                     const uint64_t* const* cfac, uint32_t K, uint32_t d_s,
+                     uint64_t* const* out, uint32_t level, hipStream_t s) {
+  Scratch S;
+  int err;
+  if ((err = scratch(c, &S))) return err;
+  const size_t n = c->n, W = (size_t)2 * c->L * n;
+  uint64_t* t1 = S.ws;
+  uint64_t* chi = S.ws + W;
+  uint64_t* tmp = S.ws + 2 * W;
+  const uint32_t lo = level - 2;
+  for (uint32_t k = 0; k < K; ++k) {
+    if ((err = op_mul_relin(c, decay[k], h[k], t1, level, s))) return err;
+    if ((err = op_rescale(c, t1, t1, level, s))) return err;
+    if ((err = op_mul_relin(c, t1, cfac[k], t1, level - 1, s))) return err;
+    if ((err = op_rescale(c, t1, out[k], level - 1, s))) return err;
+  }
+  auto reduce = [&](uint64_t* x) -> int {
+    for (uint32_t st = d_s / 2; st >= 1; st /= 2) {
+      const int32_t step = (int32_t)st;
+      int e;
+      if ((e = op_rotate_many(c, x, 1, &step, &tmp, lo, s))) return e;
+      HIPCK(k_binary_launch(c, x, tmp, x, 2 * lo, 1, 0, s));
+    }
+    return FESC_OK;
+  };
+  for (uint32_t l = 0; l + 1 < K; l += 2) {
+    HIPCK(k_monomial_launch(c, out[l + 1], chi, lo, c->n / 2, s));
+    HIPCK(k_binary_launch(c, out[l], chi, chi, 2 * lo, 1, 0, s));
+    if ((err = reduce(chi))) return err;
+    const int32_t cj = INT32_MIN;
+    if ((err = op_rotate_many(c, chi, 1, &cj, &tmp, lo, s))) return err;
+    HIPCK(k_binary_launch(c, chi, tmp, out[l], 2 * lo, 1, 0, s));
+    HIPCK(k_binary_launch(c, chi, tmp, tmp, 2 * lo, 1, 1, s));
+    HIPCK(k_monomial_launch(c, tmp, out[l + 1], lo, 3 * c->n / 2, s));
+  }
+  if (K % 2 && (err = reduce(out[K - 1]))) return err;
+  (void)n;
   return FESC_OK;
 }
 

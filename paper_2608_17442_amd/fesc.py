@@ -56,6 +56,8 @@ _SIGS = {
     "fesc_encrypt_sk": [_vp, _vp, _vp, _vp, _vp, _vp, _u32, _vp],
     "fesc_plain_from_coeffs": [_vp, _vp, _vp, _u32, _vp],
     "fesc_encode": [_u32, _vp, _vp, ctypes.c_double, _vp],
+    "fesc_scan_contract": [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp), ctypes.POINTER(_vp),
+                           _u32, _u32, ctypes.POINTER(_vp), _u32, _vp],
 }
 
 CONJ = -(2 ** 31)
@@ -203,6 +205,12 @@ class Context:
     def plain_from_coeffs(self, m, pt, level, stream=None):
         _check(_lib.fesc_plain_from_coeffs(self._h, _ptr(m), _ptr(pt), level, _stream(stream)))
 
+    def scan_contract(self, h, decay, cfac, d_state, outs, level, stream=None):
+        K = len(h)
+        arr = lambda ts: (_vp * K)(*[_ptr(t) for t in ts])
+        _check(_lib.fesc_scan_contract(self._h, arr(h), arr(decay), arr(cfac), K, d_state,
+                                       arr(outs), level, _stream(stream)))
+
     def key_words(self) -> int:
         return self.dnum * (self.L + self.alpha) * 2 * self.n
 
@@ -231,6 +239,8 @@ _lib.fesc_matvec_plan_destroy.argtypes = [_vp]
 _lib.fesc_matvec_plan_destroy.restype = None
 _lib.fesc_ptct_matvec.argtypes = [_vp, _vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp), _vp]
 _lib.fesc_ptct_matvec.restype = ctypes.c_int
+_lib.fesc_matvec_phase_ms.argtypes = [_vp] + [ctypes.POINTER(ctypes.c_float)] * 3
+_lib.fesc_matvec_phase_ms.restype = ctypes.c_int
 
 
 class MatvecPlan:
@@ -253,6 +263,12 @@ class MatvecPlan:
         a = (_vp * len(ins))(*[_ptr(t) for t in ins])
         b = (_vp * len(outs))(*[_ptr(t) for t in outs])
         _check(_lib.fesc_ptct_matvec(self.ctx._h, self._h, a, b, _stream(stream)))
+
+    def phase_ms(self):
+        """(baby steps, pt-MAC, tail) durations of the last completed run."""
+        v = [ctypes.c_float() for _ in range(3)]
+        _check(_lib.fesc_matvec_phase_ms(self._h, *[ctypes.byref(x) for x in v]))
+        return tuple(float(x.value) for x in v)
 
     def close(self):
         if getattr(self, "_h", None):

@@ -1,0 +1,105 @@
+"""GPU parity of the scan-contract slice against the oracle: a small ring with
+four chunks, and one full-size Mamba-2-base token (N = 2^16, 12 state chunks
+of 128 channels x d_state 128, level 20 -> 18)."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+import synth.workloads as WL
+from oracle import ckks as C
+from oracle import workloads as OW
+from tests.gpu_helpers import first_mismatch, need_gpu, step, to_host
+from tests.test_gpu_ckks import Setup
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    need_gpu()
+
+
+def chunk_slots(z, cvec, H, K, n_slots, d_s, head_dim, s_state=None):
+    """Slot vectors of the state-chunk packing: chunk k holds channels
+    [k*c, (k+1)*c), c = s_state / d_s, channel e at slots (e - k*c)*d_s + i;
+    slots from s_state on are zero.  Returns per chunk (h, decay, C)."""
+    s_state = s_state or n_slots
+    c_state = s_state // d_s
+    j = np.arange(n_slots)
+    out = []
+    decay = 1.0 / (1.0 + np.exp(z))          # exp(-softplus(z))
+    for k in range(K):
+        e = k * c_state + j // d_s
+        i = j % d_s
+        ok = (e < H.shape[0]) & (j < s_state)
+        hv = np.where(ok, H[np.minimum(e, H.shape[0] - 1), i], 0.0)
+        dv = np.where(ok, decay[np.minimum(e, H.shape[0] - 1) // head_dim], 0.0)
+        cv = np.where(ok, cvec[i], 0.0)
+        out.append((hv, dv, cv))
+    return out
+
+
+def _run(P, S, chunks, level, d_s, tag):
+    hs_o, ds_o, cs_o, hs_d, ds_d, cs_d = [], [], [], [], [], []
+    for k, (hv, dv, cv) in enumerate(chunks):
+        for vals, scale, lo, ld, role in [(hv, 2.0 ** 40, hs_o, hs_d, 0),
+                                          (dv, float(P.q[level - 1]), ds_o, ds_d, 1),
+                                          (cv, float(P.q[level - 2]), cs_o, cs_d, 2)]:
+            co, cd = S.encrypt(vals.astype(complex), scale, level, 10 * k + role)
+            lo.append(co)
+            ld.append(cd)
+    outs_d = [torch.zeros((level - 2) * 2 * P.n, dtype=torch.int64, device="cuda")
+              for _ in chunks]
+    step(f"scan_contract {tag} chunks={len(chunks)}")
+    S.ctx.scan_contract(hs_d, ds_d, cs_d, d_s, outs_d, level)
+    outs_o = OW.scan_contract_token(P, hs_o, ds_o, cs_o, S.keys[0], S.keys, d_s)
+    for k, (od, oo) in enumerate(zip(outs_d, outs_o)):
+        got = to_host(od).reshape(oo.shape)
+        assert np.array_equal(got, oo), f"{tag} output {k}: {first_mismatch(got, oo)}"
+    return outs_o
+
+
+def test_scan_contract_small():
+    P = C.params_small(12, 50, 5, 2)
+    d_s, head_dim, K, level = 8, 16, 5, 4       # odd K exercises the lone last chunk
+    n_slots = P.n // 2
+    S = Setup(P, 31, rot_steps=[1, 2, 4], relin=True, conj=True)
+    E = K * (n_slots // d_s) - 40               # ragged: last chunk partly empty
+    z = synth.normal(31, "z", -(-E // head_dim))
+    cvec = synth.normal(31, "C", d_s)
+    H = synth.normal(31, "h", (E, d_s))
+    outs = _run(P, S, chunk_slots(z, cvec, H, K, n_slots, d_s, head_dim), level, d_s, "small")
+    decay = 1.0 / (1.0 + np.exp(z))
+    want = (decay[np.arange(E) // head_dim][:, None] * H * cvec[None, :]).sum(axis=1)
+    c_state = n_slots // d_s
+    for l in range(K // 2):
+        for half in range(2):
+            k = 2 * l + half
+            dec = C.decrypt(P, S.sk, outs[k], 2.0 * 2.0 ** 40).real[::d_s]
+            ref = np.zeros(c_state)
+            seg = want[k * c_state:(k + 1) * c_state]
+            ref[:len(seg)] = seg
+            assert np.max(np.abs(dec - ref)) <= 2.0 ** -15
+
+
+def test_cfg5_one_token_full_size():
+    P = C.params_p16(24)
+    cfg = WL.CFG5
+    d_s, head_dim, level = cfg["d_state"], cfg["head_dim"], cfg["level"]
+    n_slots = P.n // 2
+    s_state = 16384
+    K = cfg["heads"] * head_dim * d_s // s_state          # 12 chunks
+    steps = [d_s >> k for k in range(1, 8)]               # 64 .. 1
+    S = Setup(P, cfg["seed"], rot_steps=steps, relin=True, conj=True)
+    z, cvec, H = WL.cfg5_token(0)
+    chunks = chunk_slots(z, cvec, H, K, n_slots, d_s, head_dim, s_state)
+    outs = _run(P, S, chunks, level, d_s, "cfg5")
+    decay = 1.0 / (1.0 + np.exp(z))
+    want = (decay[np.arange(H.shape[0]) // head_dim][:, None] * H * cvec[None, :]).sum(axis=1)
+    c_state = s_state // d_s
+    for k in [0, 1, K - 1]:
+        dec = C.decrypt(P, S.sk, outs[k], 2.0 * 2.0 ** 40).real[:s_state:d_s]
+        err = np.max(np.abs(dec - want[k * c_state:(k + 1) * c_state]))
+        print(f"cfg5 chunk {k}: max |decoded - fp64| = {err:.3e}")
+        assert err <= 2.0 ** -15
