@@ -117,8 +117,7 @@ class Workloads:
 
     def run_ks(self, ev):
         ev[0].record()
-        for c, o, st in zip(self.ks_in, self.ks_out, self.ks_steps):
-            self.ctx.rotate(c, o, 24, st)
+        self.ctx.rotate_batch(self.ks_in, self.ks_steps, self.ks_out, 24)
         ev[1].record()
 
     # ---- BSGS projection

@@ -154,6 +154,16 @@ int fesc_rotate(fesc_ctx* ctx, const uint64_t* in, uint64_t* out, uint32_t level
 int fesc_rotate_hoisted(fesc_ctx* ctx, const uint64_t* in, uint32_t count, const int32_t* steps,
                         uint64_t* const* outs, uint32_t level, void* stream);
 
+/* Batched rotations of `count` independent ciphertexts: outs[i] =
+ * rho(ins[i]; steps[i]) (FESC_CONJ allowed).  Up to 32 key switches run in
+ * each launch of the pipeline, so the device is filled by the batch rather
+ * than by one ciphertext.  ins / outs / steps are host arrays; outputs must
+ * not alias inputs (FESC_ERR_ARG).  Results equal fesc_rotate residue for
+ * residue. */
+int fesc_rotate_batch(fesc_ctx* ctx, uint32_t count, const uint64_t* const* ins,
+                      const int32_t* steps, uint64_t* const* outs, uint32_t level,
+                      void* stream);
+
 /* Switching-key generation on the device from caller-drawn randomness:
  * s: int8[N] ternary secret coefficients; a: uint64[dnum][L+alpha][N] uniform
  * residues (evaluation form); e: int64[dnum][N] error coefficients.  For

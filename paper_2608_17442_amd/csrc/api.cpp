@@ -198,6 +198,25 @@ int fesc_rotate_hoisted(fesc_ctx* ctx, const uint64_t* in, uint32_t count, const
   return op_rotate_many(ctx, in, count, steps, outs, level, S(stream));
 }
 
+int fesc_rotate_batch(fesc_ctx* ctx, uint32_t count, const uint64_t* const* ins,
+                      const int32_t* steps, uint64_t* const* outs, uint32_t level,
+                      void* stream) {
+  int rc = check_level(ctx, level);
+  if (rc) return rc;
+  if (!ins || !steps || !outs || count == 0) return fail(FESC_ERR_ARG, "bad batch arguments");
+  for (uint32_t i = 0; i < count; ++i) {
+    if (!ins[i] || !outs[i]) return fail(FESC_ERR_ARG, "null buffer");
+    for (uint32_t j = 0; j < count; ++j)
+      if (outs[i] == ins[j]) return fail(FESC_ERR_ARG, "batched outputs must not alias inputs");
+  }
+  for (uint32_t i = 0; i < count; ++i) {
+    const uint32_t g = galois_of_step(ctx, steps[i]);
+    if (g != 1 && !ctx->keys.count(g))
+      return fail(FESC_ERR_NO_KEY, "no switching key for Galois element " + std::to_string(g));
+  }
+  return op_rotate_batch(ctx, count, ins, steps, outs, nullptr, level, S(stream));
+}
+
 int fesc_keygen(fesc_ctx* ctx, uint32_t galois_elt, const int8_t* s, const uint64_t* a,
                 const int64_t* e, void* stream) {
   if (!ctx || !s || !a || !e) return fail(FESC_ERR_ARG, "null argument");

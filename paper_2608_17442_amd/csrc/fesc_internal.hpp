@@ -135,7 +135,7 @@ struct RowSel {
   uint64_t* base;
   size_t batch_stride, limb_stride;
   uint32_t prime0, split, prime1;
-  uint32_t skip_alpha, skip_limit;
+  uint32_t skip_alpha, skip_limit, skip_mod;
   __device__ uint64_t* row() const;
   __device__ uint32_t prime() const;
   __device__ bool skip() const;

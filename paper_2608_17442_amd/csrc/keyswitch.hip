@@ -9,6 +9,10 @@
 // sigma_g to the extended digits (evaluation-form index permutation) for any
 // number of rotations of the same ciphertext.
 //
+// Every kernel here is batched: up to kMaxBatch ModUp sources and key-switch
+// jobs run in one launch (tables passed by value in the kernel arguments), so
+// independent key switches fill the GPU together instead of one at a time.
+//
 // Extended basis at level l: rows 0..l-1 are q_0..q_{l-1}, rows l..l+alpha-1
 // are p_0..p_{alpha-1} (extended prime index L + k).
 #include "fesc_internal.hpp"
@@ -31,20 +35,34 @@ __device__ __forceinline__ uint32_t galois_src(uint32_t jp, uint32_t g, uint32_t
   return __builtin_bitreverse32((e - 1u) >> 1) >> (32 - log_n);
 }
 
-// ModUp: coefficient-form input rows cc[0..level) -> ext[j][row] for every row
-// outside digit j (coefficient form; the caller transforms them).
+// cc[s][i][k] = src s row i (evaluation form, rows at in + i*stride).
+__global__ __launch_bounds__(kThreads) void k_gather(KsTable tab, uint64_t* __restrict__ cc,
+                                                     uint32_t level, uint32_t n) {
+  const uint32_t i = blockIdx.y, s = blockIdx.z;
+  const uint32_t k = 2 * (blockIdx.x * kThreads + threadIdx.x);
+  if (k >= n) return;
+  const ulonglong2 v =
+      *reinterpret_cast<const ulonglong2*>(tab.src_in[s] + (size_t)i * tab.src_stride[s] + k);
+  *reinterpret_cast<ulonglong2*>(cc + ((size_t)s * level + i) * n + k) = v;
+}
+
+// ModUp: coefficient-form rows cc[s][0..level) -> ext[s][j][row] for every
+// row outside digit j (coefficient form; transformed afterwards).
+// blockIdx.y = s * dnum_l + j.
 template <int MAXA>
 __global__ __launch_bounds__(kThreads) void k_modup(const uint64_t* __restrict__ cc,
                                                     uint64_t* __restrict__ ext, uint32_t level,
-                                                    uint32_t L, uint32_t alpha, uint32_t n,
-                                                    const PrimeK* __restrict__ pk,
+                                                    uint32_t L, uint32_t alpha, uint32_t dnum_l,
+                                                    uint32_t n, const PrimeK* __restrict__ pk,
                                                     const double2* __restrict__ mu_inv,
                                                     const double2* __restrict__ mu_hat) {
-  const uint32_t j = blockIdx.y;
+  const uint32_t s = blockIdx.y / dnum_l, j = blockIdx.y % dnum_l;
   const uint32_t lo = j * alpha, hi = min(lo + alpha, level), aj = hi - lo;
   const uint32_t E = level + alpha;
   const uint32_t k = 2 * (blockIdx.x * kThreads + threadIdx.x);
   if (k >= n) return;
+  const uint64_t* src = cc + (size_t)s * level * n;
+  uint64_t* dst = ext + ((size_t)s * dnum_l + j) * E * n;
   double x0[MAXA], x1[MAXA];
 #pragma unroll
   for (int a = 0; a < MAXA; ++a) {
@@ -52,7 +70,7 @@ __global__ __launch_bounds__(kThreads) void k_modup(const uint64_t* __restrict__
     if (a < (int)aj) {
       const PrimeK P = pk[lo + a];
       const double2 f = mu_inv[j * alpha + a];
-      const ulonglong2 v = *reinterpret_cast<const ulonglong2*>(cc + (size_t)(lo + a) * n + k);
+      const ulonglong2 v = *reinterpret_cast<const ulonglong2*>(src + (size_t)(lo + a) * n + k);
       x0[a] = center(red_full(mm_shoup(u2d(v.x), f.x, f.y, P.q), P.q, P.qinv), P.q);
       x1[a] = center(red_full(mm_shoup(u2d(v.y), f.x, f.y, P.q), P.q, P.qinv), P.q);
     }
@@ -78,27 +96,27 @@ __global__ __launch_bounds__(kThreads) void k_modup(const uint64_t* __restrict__
     ulonglong2 o;
     o.x = d2u(red_full(acc0, M.q, M.qinv));
     o.y = d2u(red_full(acc1, M.q, M.qinv));
-    *reinterpret_cast<ulonglong2*>(ext + ((size_t)j * E + row) * n + k) = o;
+    *reinterpret_cast<ulonglong2*>(dst + (size_t)row * n + k) = o;
   }
 }
 
 // Inner product with the key, sigma_g applied to the extended digits on the
-// fly: acc[t][row][k] = sum_j d_j[row][src(k)] * key[j][prime(row)][t][k].
-// Own-digit rows of d_j are the input polynomial itself (row i at
-// in + i*in_stride, evaluation form).
-__global__ __launch_bounds__(kThreads) void k_ip(const uint64_t* __restrict__ ext,
-                                                 const uint64_t* __restrict__ in,
-                                                 size_t in_stride,
-                                                 const uint64_t* __restrict__ key,
+// fly: acc[job][t][row][k] = sum_j d_j[row][src(k)] * key[j][prime(row)][t][k].
+// Own-digit rows of d_j are the source polynomial itself.  blockIdx.z = job.
+__global__ __launch_bounds__(kThreads) void k_ip(KsTable tab, const uint64_t* __restrict__ ext,
                                                  uint64_t* __restrict__ acc, uint32_t level,
                                                  uint32_t L, uint32_t alpha, uint32_t dnum_l,
-                                                 uint32_t log_n, uint32_t galois,
-                                                 const PrimeK* __restrict__ pk) {
+                                                 uint32_t log_n, const PrimeK* __restrict__ pk) {
   const uint32_t n = 1u << log_n;
-  const uint32_t row = blockIdx.y;
+  const uint32_t row = blockIdx.y, job = blockIdx.z;
   const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
   if (k >= n) return;
   const uint32_t E = level + alpha, KE = L + alpha;
+  const uint32_t s = tab.job_src[job], galois = tab.galois[job];
+  const uint64_t* key = tab.key[job];
+  const uint64_t* in = tab.src_in[s];
+  const size_t in_stride = tab.src_stride[s];
+  const uint64_t* ex = ext + (size_t)s * dnum_l * E * n;
   const uint32_t prime = ext_prime(row, level, L);
   const PrimeK M = pk[prime];
   const uint32_t src = galois ? galois_src(k, galois, log_n) : k;
@@ -106,7 +124,7 @@ __global__ __launch_bounds__(kThreads) void k_ip(const uint64_t* __restrict__ ex
   for (uint32_t j = 0; j < dnum_l; ++j) {
     const uint32_t lo = j * alpha, hi = min(lo + alpha, level);
     const uint64_t dv = (row >= lo && row < hi) ? in[(size_t)row * in_stride + src]
-                                                : ext[((size_t)j * E + row) * n + src];
+                                                : ex[((size_t)j * E + row) * n + src];
     const double d = u2d(dv);
     const size_t ko = (((size_t)j * KE + prime) * 2) * n + k;
     ab += mm_var(d, u2d(key[ko]), M.q, M.qinv);
@@ -116,11 +134,13 @@ __global__ __launch_bounds__(kThreads) void k_ip(const uint64_t* __restrict__ ex
       aa = red_bal(aa, M.q, M.qinv);
     }
   }
-  acc[(size_t)row * n + k] = d2u(red_full(ab, M.q, M.qinv));
-  acc[((size_t)E + row) * n + k] = d2u(red_full(aa, M.q, M.qinv));
+  uint64_t* out = acc + (size_t)job * 2 * E * n;
+  out[(size_t)row * n + k] = d2u(red_full(ab, M.q, M.qinv));
+  out[((size_t)E + row) * n + k] = d2u(red_full(aa, M.q, M.qinv));
 }
 
-// ModDown conversion: P-rows of acc[t] (coefficient form) -> y[t][i], i < level.
+// ModDown conversion: for u = 2*job + t (blockIdx.y), the P-rows of acc[u]
+// (coefficient form) -> y[u][i], i < level.
 template <int MAXA>
 __global__ __launch_bounds__(kThreads) void k_moddown_bconv(const uint64_t* __restrict__ acc,
                                                             uint64_t* __restrict__ y,
@@ -129,7 +149,7 @@ __global__ __launch_bounds__(kThreads) void k_moddown_bconv(const uint64_t* __re
                                                             const PrimeK* __restrict__ pk,
                                                             const double2* __restrict__ md_inv,
                                                             const double2* __restrict__ md_hat) {
-  const uint32_t t = blockIdx.y;
+  const uint32_t u = blockIdx.y;
   const uint32_t E = level + alpha;
   const uint32_t k = 2 * (blockIdx.x * kThreads + threadIdx.x);
   if (k >= n) return;
@@ -141,7 +161,7 @@ __global__ __launch_bounds__(kThreads) void k_moddown_bconv(const uint64_t* __re
       const PrimeK P = pk[L + a];
       const double2 f = md_inv[a];
       const ulonglong2 v =
-          *reinterpret_cast<const ulonglong2*>(acc + ((size_t)t * E + level + a) * n + k);
+          *reinterpret_cast<const ulonglong2*>(acc + ((size_t)u * E + level + a) * n + k);
       x0[a] = center(red_full(mm_shoup(u2d(v.x), f.x, f.y, P.q), P.q, P.qinv), P.q);
       x1[a] = center(red_full(mm_shoup(u2d(v.y), f.x, f.y, P.q), P.q, P.qinv), P.q);
     }
@@ -166,65 +186,74 @@ __global__ __launch_bounds__(kThreads) void k_moddown_bconv(const uint64_t* __re
     ulonglong2 o;
     o.x = d2u(red_full(s0, M.q, M.qinv));
     o.y = d2u(red_full(s1, M.q, M.qinv));
-    *reinterpret_cast<ulonglong2*>(y + ((size_t)t * level + i) * n + k) = o;
+    *reinterpret_cast<ulonglong2*>(y + ((size_t)u * level + i) * n + k) = o;
   }
 }
 
-// out[i][t] = (acc[t][i] - y[t][i]) * P^-1 (+ add[i][t][src(k)] when bit t of
-// add_mask is set; add row i component t at add + i*2N + t*N).
-__global__ __launch_bounds__(kThreads) void k_ks_combine(const uint64_t* __restrict__ acc,
+// out_job[i][t] = (acc[u][i] - y[u][i]) * P^-1
+//               + add_job[i][t][src(k)]   if bit t of add_mask_job
+//               + add2_job[i][t][k]       if add2_job != null
+// u = 2*job + t = blockIdx.z.
+__global__ __launch_bounds__(kThreads) void k_ks_combine(KsTable tab,
+                                                         const uint64_t* __restrict__ acc,
                                                          const uint64_t* __restrict__ y,
-                                                         const uint64_t* add,
-                                                         uint32_t add_mask, uint32_t add_galois,
-                                                         uint64_t* out, uint32_t level,
-                                                         uint32_t alpha, uint32_t log_n,
+                                                         uint32_t level, uint32_t alpha,
+                                                         uint32_t log_n,
                                                          const PrimeK* __restrict__ pk,
                                                          const double2* __restrict__ pinv) {
   const uint32_t n = 1u << log_n;
-  const uint32_t i = blockIdx.y, t = blockIdx.z;
+  const uint32_t i = blockIdx.y, u = blockIdx.z, job = u >> 1, t = u & 1;
   const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
   if (k >= n) return;
   const uint32_t E = level + alpha;
   const PrimeK M = pk[i];
   const double2 f = pinv[i];
-  const double d = u2d(acc[((size_t)t * E + i) * n + k]) - u2d(y[((size_t)t * level + i) * n + k]);
+  const double d = u2d(acc[((size_t)u * E + i) * n + k]) - u2d(y[((size_t)u * level + i) * n + k]);
   double v = mm_shoup(d, f.x, f.y, M.q);
-  if ((add_mask >> t) & 1u) {
-    const uint32_t src = add_galois ? galois_src(k, add_galois, log_n) : k;
-    v += u2d(add[((size_t)2 * i + t) * n + src]);
+  const size_t o = ((size_t)2 * i + t) * n;
+  if ((tab.add_mask[job] >> t) & 1u) {
+    const uint32_t g = tab.add_galois[job];
+    v += u2d(tab.add[job][o + (g ? galois_src(k, g, log_n) : k)]);
   }
-  out[((size_t)2 * i + t) * n + k] = d2u(red_full(v, M.q, M.qinv));
+  if (tab.add2[job]) v += u2d(tab.add2[job][o + k]);
+  tab.out[job][o + k] = d2u(red_full(v, M.q, M.qinv));
 }
 
 }  // namespace
 
-hipError_t k_modup_launch(const Context* c, const LevelTables& T, const uint64_t* cc,
-                          uint64_t* ext, uint32_t level, hipStream_t s) {
-  const uint32_t dnum_l = (level + c->alpha - 1) / c->alpha;
-  const uint32_t E = level + c->alpha;
-  dim3 grid((c->n / 2 + kThreads - 1) / kThreads, dnum_l, (E + kRowsPerZ - 1) / kRowsPerZ);
-  if (c->alpha <= 8)
-    hipLaunchKernelGGL(k_modup<8>, grid, dim3(kThreads), 0, s, cc, ext, level, c->L, c->alpha,
-                       c->n, c->d_pk, T.mu_inv, T.mu_hat);
-  else
-    hipLaunchKernelGGL(k_modup<16>, grid, dim3(kThreads), 0, s, cc, ext, level, c->L, c->alpha,
-                       c->n, c->d_pk, T.mu_inv, T.mu_hat);
+hipError_t k_gather_launch(const Context* c, const KsTable& tab, uint32_t nsrc, uint64_t* cc,
+                           uint32_t level, hipStream_t s) {
+  dim3 grid((c->n / 2 + kThreads - 1) / kThreads, level, nsrc);
+  hipLaunchKernelGGL(k_gather, grid, dim3(kThreads), 0, s, tab, cc, level, c->n);
   return hipGetLastError();
 }
 
-hipError_t k_ip_launch(const Context* c, const uint64_t* ext, const uint64_t* in,
-                       size_t in_stride, const uint64_t* key, uint64_t* acc, uint32_t level,
-                       uint32_t galois, hipStream_t s) {
+hipError_t k_modup_launch(const Context* c, const LevelTables& T, const uint64_t* cc,
+                          uint64_t* ext, uint32_t nsrc, uint32_t level, hipStream_t s) {
   const uint32_t dnum_l = (level + c->alpha - 1) / c->alpha;
-  dim3 grid((c->n + kThreads - 1) / kThreads, level + c->alpha);
-  hipLaunchKernelGGL(k_ip, grid, dim3(kThreads), 0, s, ext, in, in_stride, key, acc, level, c->L,
-                     c->alpha, dnum_l, c->log_n, galois, c->d_pk);
+  const uint32_t E = level + c->alpha;
+  dim3 grid((c->n / 2 + kThreads - 1) / kThreads, nsrc * dnum_l, (E + kRowsPerZ - 1) / kRowsPerZ);
+  if (c->alpha <= 8)
+    hipLaunchKernelGGL(k_modup<8>, grid, dim3(kThreads), 0, s, cc, ext, level, c->L, c->alpha,
+                       dnum_l, c->n, c->d_pk, T.mu_inv, T.mu_hat);
+  else
+    hipLaunchKernelGGL(k_modup<16>, grid, dim3(kThreads), 0, s, cc, ext, level, c->L, c->alpha,
+                       dnum_l, c->n, c->d_pk, T.mu_inv, T.mu_hat);
+  return hipGetLastError();
+}
+
+hipError_t k_ip_launch(const Context* c, const KsTable& tab, uint32_t njobs, const uint64_t* ext,
+                       uint64_t* acc, uint32_t level, hipStream_t s) {
+  const uint32_t dnum_l = (level + c->alpha - 1) / c->alpha;
+  dim3 grid((c->n + kThreads - 1) / kThreads, level + c->alpha, njobs);
+  hipLaunchKernelGGL(k_ip, grid, dim3(kThreads), 0, s, tab, ext, acc, level, c->L, c->alpha,
+                     dnum_l, c->log_n, c->d_pk);
   return hipGetLastError();
 }
 
 hipError_t k_moddown_bconv_launch(const Context* c, const LevelTables& T, const uint64_t* acc,
-                                  uint64_t* y, uint32_t level, hipStream_t s) {
-  dim3 grid((c->n / 2 + kThreads - 1) / kThreads, 2, (level + kRowsPerZ - 1) / kRowsPerZ);
+                                  uint64_t* y, uint32_t njobs, uint32_t level, hipStream_t s) {
+  dim3 grid((c->n / 2 + kThreads - 1) / kThreads, 2 * njobs, (level + kRowsPerZ - 1) / kRowsPerZ);
   if (c->alpha <= 8)
     hipLaunchKernelGGL(k_moddown_bconv<8>, grid, dim3(kThreads), 0, s, acc, y, level, c->L,
                        c->alpha, c->n, c->d_pk, T.md_inv, T.md_hat);
@@ -234,13 +263,12 @@ hipError_t k_moddown_bconv_launch(const Context* c, const LevelTables& T, const 
   return hipGetLastError();
 }
 
-hipError_t k_ks_combine_launch(const Context* c, const LevelTables& T, const uint64_t* acc,
-                               const uint64_t* y, const uint64_t* add, uint32_t add_mask,
-                               uint32_t add_galois, uint64_t* out, uint32_t level,
-                               hipStream_t s) {
-  dim3 grid((c->n + kThreads - 1) / kThreads, level, 2);
-  hipLaunchKernelGGL(k_ks_combine, grid, dim3(kThreads), 0, s, acc, y, add, add_mask, add_galois,
-                     out, level, c->alpha, c->log_n, c->d_pk, T.md_pinv);
+hipError_t k_ks_combine_launch(const Context* c, const LevelTables& T, const KsTable& tab,
+                               uint32_t njobs, const uint64_t* acc, const uint64_t* y,
+                               uint32_t level, hipStream_t s) {
+  dim3 grid((c->n + kThreads - 1) / kThreads, level, 2 * njobs);
+  hipLaunchKernelGGL(k_ks_combine, grid, dim3(kThreads), 0, s, tab, acc, y, level, c->alpha,
+                     c->log_n, c->d_pk, T.md_pinv);
   return hipGetLastError();
 }
 

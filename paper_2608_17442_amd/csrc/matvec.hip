@@ -22,7 +22,7 @@ struct fesc_matvec_plan {
   fesc_matvec_desc d;
   std::vector<const uint64_t*> diag;  // host copy of the table [n_out][n2][n_in][n1]
   const uint64_t** d_diag = nullptr;  // device copy
-  uint64_t* work = nullptr;           // baby [n_in][n1] cts, then c~ [n_out][n2] cts
+  uint64_t* work = nullptr;           // baby [n_in][n1], c~ [n_out][n2], extraction [n_out] cts
   const uint64_t** d_baby = nullptr;  // device table of baby pointers
   uint64_t** d_ct = nullptr;          // device table of c~ pointers
   size_t ct_words = 0;
@@ -124,7 +124,7 @@ int matvec_plan_create(Context* c, const fesc_matvec_desc* d, const uint64_t* co
   const size_t n_baby = (size_t)d->n_in * d->n1, n_ct = (size_t)d->n_out * d->n2;
   std::vector<const uint64_t*> baby(n_baby);
   std::vector<uint64_t*> cts(n_ct);
-  bool ok = hipMalloc(&p->work, (n_baby + n_ct + 1) * p->ct_words * 8) == hipSuccess &&
+  bool ok = hipMalloc(&p->work, (n_baby + n_ct + d->n_out) * p->ct_words * 8) == hipSuccess &&
             hipMalloc(&p->d_diag, n_diag * sizeof(void*)) == hipSuccess &&
             hipMalloc(&p->d_baby, n_baby * sizeof(void*)) == hipSuccess &&
             hipMalloc(&p->d_ct, n_ct * sizeof(void*)) == hipSuccess;
@@ -170,15 +170,28 @@ int ptct_matvec(Context* c, fesc_matvec_plan* p, const uint64_t* const* in,
   uint64_t* baby = p->work;
   uint64_t* ct = p->work + n_baby * W;
   uint64_t* tmp = ct + (size_t)d.n_out * d.n2 * W;
+  const size_t n = c->n;
   int err;
   HIPCK(hipEventRecord(p->ev[0], s));
-  // baby steps, hoisted per input
-  std::vector<int32_t> steps(d.n1);
-  std::vector<uint64_t*> bouts(d.n1);
-  for (uint32_t q = 0; q < d.n1; ++q) steps[q] = (int32_t)(((int64_t)q * d.unit) % (c->n / 2));
+  // baby steps: one ModUp per input, all (u, q) key switches batched
+  std::vector<KsSource> srcs;
+  std::vector<KsJob> jobs;
   for (uint32_t u = 0; u < d.n_in; ++u) {
-    for (uint32_t q = 0; q < d.n1; ++q) bouts[q] = baby + ((size_t)u * d.n1 + q) * W;
-    if ((err = op_rotate_many(c, in[u], d.n1, steps.data(), bouts.data(), level, s))) return err;
+    for (uint32_t q = 0; q < d.n1; ++q) {
+      uint64_t* o = baby + ((size_t)u * d.n1 + q) * W;
+      const uint32_t g = galois_of_step(c, (int32_t)(((int64_t)q * d.unit) % (c->n / 2)));
+      if (g == 1) {
+        HIPCK(hipMemcpyAsync(o, in[u], W * 8, hipMemcpyDeviceToDevice, s));
+        continue;
+      }
+      jobs.push_back(KsJob{(uint32_t)srcs.size(), c->keys.at(g), g, in[u], 1u, g, nullptr, o});
+    }
+    srcs.push_back(KsSource{in[u] + n, 2 * n});
+    if (srcs.size() == kMaxBatch || u + 1 == d.n_in) {
+      if ((err = key_switch_batch(c, level, srcs, jobs, s))) return err;
+      srcs.clear();
+      jobs.clear();
+    }
   }
   HIPCK(hipEventRecord(p->ev[1], s));
   // pt-MAC over all (b, p)
@@ -188,24 +201,39 @@ int ptct_matvec(Context* c, fesc_matvec_plan* p, const uint64_t* const* in,
                      n_outputs, (uint32_t)n_baby, c->n, c->d_pk);
   HIPCK(hipGetLastError());
   HIPCK(hipEventRecord(p->ev[2], s));
-  // giant steps, real extraction, rescale
+  // giant steps: y_b += Phi^(p n1)(c~_{b,p}), one batch over b per p
+  std::vector<const uint64_t*> gin(d.n_out);
+  std::vector<uint64_t*> gout(d.n_out);
+  std::vector<int32_t> gst(d.n_out);
+  for (uint32_t g = 1; g < d.n2; ++g) {
+    for (uint32_t b = 0; b < d.n_out; ++b) {
+      gin[b] = ct + ((size_t)b * d.n2 + g) * W;
+      gout[b] = ct + (size_t)b * d.n2 * W;
+      gst[b] = (int32_t)(((int64_t)g * d.n1 * d.unit) % (c->n / 2));
+    }
+    if ((err = op_rotate_batch(c, d.n_out, gin.data(), gst.data(), gout.data(),
+                               (const uint64_t* const*)gout.data(), level, s)))
+      return err;
+  }
+  // real extraction: t_b = conj(y_b) + y_b, one batch
+  std::vector<uint64_t*> res(d.n_out);
+  for (uint32_t b = 0; b < d.n_out; ++b) res[b] = ct + (size_t)b * d.n2 * W;
+  if (d.real_extract) {
+    for (uint32_t b = 0; b < d.n_out; ++b) {
+      gin[b] = res[b];
+      gout[b] = tmp + (size_t)b * W;
+      gst[b] = INT32_MIN;
+    }
+    if ((err = op_rotate_batch(c, d.n_out, gin.data(), gst.data(), gout.data(), gin.data(),
+                               level, s)))
+      return err;
+    for (uint32_t b = 0; b < d.n_out; ++b) res[b] = gout[b];
+  }
   for (uint32_t b = 0; b < d.n_out; ++b) {
-    uint64_t* y = ct + (size_t)b * d.n2 * W;
-    for (uint32_t g = 1; g < d.n2; ++g) {
-      uint64_t* cp = y + (size_t)g * W;
-      const int32_t st = (int32_t)(((int64_t)g * d.n1 * d.unit) % (c->n / 2));
-      if ((err = op_rotate_many(c, cp, 1, &st, &cp, level, s))) return err;
-      HIPCK(k_binary_launch(c, y, cp, y, 2 * level, 1, 0, s));
-    }
-    if (d.real_extract) {
-      const int32_t cj = INT32_MIN;
-      if ((err = op_rotate_many(c, y, 1, &cj, &tmp, level, s))) return err;
-      HIPCK(k_binary_launch(c, y, tmp, y, 2 * level, 1, 0, s));
-    }
     if (d.rescale) {
-      if ((err = op_rescale(c, y, out[b], level, s))) return err;
+      if ((err = op_rescale(c, res[b], out[b], level, s))) return err;
     } else {
-      HIPCK(hipMemcpyAsync(out[b], y, W * 8, hipMemcpyDeviceToDevice, s));
+      HIPCK(hipMemcpyAsync(out[b], res[b], W * 8, hipMemcpyDeviceToDevice, s));
     }
   }
   HIPCK(hipEventRecord(p->ev[3], s));

@@ -96,8 +96,9 @@ __device__ __forceinline__ void gs_head(double (&x)[16], const double2* tw, uint
 // blockIdx.z = limb index i (the batch varies fastest between workgroups, so
 // the twiddle table of one prime stays resident in L2 across the batch).
 // Limb i < split uses prime prime0 + i, limb i >= split prime1 + (i - split).
-// If skip_alpha != 0, limbs [b*skip_alpha, min((b+1)*skip_alpha, skip_limit))
-// of batch element b are left untouched (the own-digit rows of a ModUp).
+// If skip_alpha != 0, limbs [d*skip_alpha, min((d+1)*skip_alpha, skip_limit))
+// of batch element b, d = b mod skip_mod, are left untouched (the own-digit
+// rows of digit d in a batch of ModUp outputs).
 __device__ __forceinline__ uint64_t* RowSel::row() const {
   return base + (size_t)blockIdx.y * batch_stride + (size_t)blockIdx.z * limb_stride;
 }
@@ -107,7 +108,7 @@ __device__ __forceinline__ uint32_t RowSel::prime() const {
 }
 __device__ __forceinline__ bool RowSel::skip() const {
   if (!skip_alpha) return false;
-  const uint32_t lo = blockIdx.y * skip_alpha;
+  const uint32_t lo = (blockIdx.y % skip_mod) * skip_alpha;
   const uint32_t hi = min(lo + skip_alpha, skip_limit);
   return blockIdx.z >= lo && blockIdx.z < hi;
 }
@@ -155,12 +156,61 @@ __global__ __launch_bounds__(kThreads) void k_fwd_outer(RowSel rs, uint32_t log_
   }
 }
 
+// Inner-pass twiddles.  For half-distance t = 2^lt inside block `blk` the
+// butterfly group r (< 128/t) uses psi_rev[N/2t + blk*128/t + r]; the two
+// parts of that index have disjoint bits, so the twiddle factors as
+//     F_lt * psi_rev[r],   F_lt = psi_rev[N/2t + blk*128/t],
+// i.e. eight per-block values and the first 128 table entries (kept in LDS).
+// Each twiddle costs one modular product instead of a global load.
+__device__ __forceinline__ double2 tw_prod(double F, const double2* small, uint32_t r, double q,
+                                           double qinv) {
+  const double2 c = small[r];
+  const double w = mm_shoup(F, c.x, c.y, q);  // |w| < q
+  return double2{w, w * qinv};
+}
+
+// Forward stage with register distance H on a tile whose group g has twiddle
+// index r = rbase + g / 2H.
+template <int H, bool RB0>
+__device__ __forceinline__ void ct_stage_f(double (&x)[16], double F, const double2* small,
+                                           uint32_t rbase, double q, double qinv) {
+#pragma unroll
+  for (int g = 0; g < 16; g += 2 * H) {
+    const double2 w = (RB0 && g == 0) ? double2{F, F * qinv}
+                                      : tw_prod(F, small, rbase + g / (2 * H), q, qinv);
+#pragma unroll
+    for (int r = g; r < g + H; ++r) {
+      double u = red_bal(x[r], q, qinv);
+      double v = mm_shoup(x[r + H], w.x, w.y, q);
+      x[r] = u + v;
+      x[r + H] = u - v;
+    }
+  }
+}
+
+template <int H, bool RB0>
+__device__ __forceinline__ void gs_stage_f(double (&x)[16], double F, const double2* small,
+                                           uint32_t rbase, double q, double qinv) {
+#pragma unroll
+  for (int g = 0; g < 16; g += 2 * H) {
+    const double2 w = (RB0 && g == 0) ? double2{F, F * qinv}
+                                      : tw_prod(F, small, rbase + g / (2 * H), q, qinv);
+#pragma unroll
+    for (int r = g; r < g + H; ++r) {
+      double u = x[r], v = x[r + H];
+      x[r] = red_bal(u + v, q, qinv);
+      x[r + H] = mm_shoup(u - v, w.x, w.y, q);
+    }
+  }
+}
+
 // Inner pass: 256-point blocks, 16 threads per block, 16 blocks per workgroup.
 // Reads fp64 (outer-pass output), writes canonical uint64 residues.
 __global__ __launch_bounds__(kThreads) void k_fwd_inner(RowSel rs, uint32_t log_n,
                                                         const PrimeK* __restrict__ pk,
                                                         const double2* __restrict__ twf) {
   __shared__ double lds[16 * 16 * kPadRow];
+  __shared__ double2 small[128];
   if (rs.skip()) return;
   const uint32_t n = 1u << log_n;
   const uint32_t prime = rs.prime();
@@ -169,18 +219,31 @@ __global__ __launch_bounds__(kThreads) void k_fwd_inner(RowSel rs, uint32_t log_
   uint64_t* row = rs.row();
   const uint32_t tid = threadIdx.x, sp = tid >> 4, s0 = tid & 15;
   const uint32_t base = (blockIdx.x * 16 + sp) * 256;
+  if (tid < 128) small[tid] = tw[tid];
+  double F[8];
+#pragma unroll
+  for (int lt = 0; lt < 8; ++lt) F[lt] = tw[(n + base) >> (lt + 1)].x;
   const double* src = reinterpret_cast<const double*>(row) + base;
   double x[16];
 #pragma unroll
   for (int r = 0; r < 16; ++r) x[r] = src[s0 + 16 * r];
-  ct_tail<4>(x, tw, n, base + s0, 4, q, qinv);
+  __syncthreads();
+  // t = 128, 64, 32, 16: value r at s0 + 16r, group index g / 2H
+  ct_stage_f<8, true>(x, F[7], small, 0, q, qinv);
+  ct_stage_f<4, true>(x, F[6], small, 0, q, qinv);
+  ct_stage_f<2, true>(x, F[5], small, 0, q, qinv);
+  ct_stage_f<1, true>(x, F[4], small, 0, q, qinv);
   double* my = lds + sp * (16 * kPadRow);
 #pragma unroll
   for (int r = 0; r < 16; ++r) my[pad16(s0 + 16 * r)] = x[r];
   __syncthreads();
 #pragma unroll
   for (int r = 0; r < 16; ++r) x[r] = my[pad16(16 * s0 + r)];
-  ct_tail<4>(x, tw, n, base + 16 * s0, 0, q, qinv);
+  // t = 8, 4, 2, 1: value r at 16 s0 + r, group index 8 s0 / H + g / 2H
+  ct_stage_f<8, false>(x, F[3], small, s0, q, qinv);
+  ct_stage_f<4, false>(x, F[2], small, 2 * s0, q, qinv);
+  ct_stage_f<2, false>(x, F[1], small, 4 * s0, q, qinv);
+  ct_stage_f<1, false>(x, F[0], small, 8 * s0, q, qinv);
   ulonglong2* dst = reinterpret_cast<ulonglong2*>(row + base + 16 * s0);
 #pragma unroll
   for (int r = 0; r < 16; r += 2) {
@@ -198,6 +261,7 @@ __global__ __launch_bounds__(kThreads) void k_inv_inner(RowSel rs, uint32_t log_
                                                         const PrimeK* __restrict__ pk,
                                                         const double2* __restrict__ twi) {
   __shared__ double lds[16 * 16 * kPadRow];
+  __shared__ double2 small[128];
   if (rs.skip()) return;
   const uint32_t n = 1u << log_n;
   const uint32_t prime = rs.prime();
@@ -206,6 +270,10 @@ __global__ __launch_bounds__(kThreads) void k_inv_inner(RowSel rs, uint32_t log_
   uint64_t* row = rs.row();
   const uint32_t tid = threadIdx.x, sp = tid >> 4, s0 = tid & 15;
   const uint32_t base = (blockIdx.x * 16 + sp) * 256;
+  if (tid < 128) small[tid] = tw[tid];
+  double F[8];
+#pragma unroll
+  for (int lt = 0; lt < 8; ++lt) F[lt] = tw[(n + base) >> (lt + 1)].x;
   const ulonglong2* src = reinterpret_cast<const ulonglong2*>(row + base + 16 * s0);
   double x[16];
 #pragma unroll
@@ -214,14 +282,23 @@ __global__ __launch_bounds__(kThreads) void k_inv_inner(RowSel rs, uint32_t log_
     x[r] = u2d(v.x);
     x[r + 1] = u2d(v.y);
   }
-  gs_head<4>(x, tw, n, base + 16 * s0, 0, q, qinv);
+  __syncthreads();
+  // t = 1, 2, 4, 8 on 16 consecutive values
+  gs_stage_f<1, false>(x, F[0], small, 8 * s0, q, qinv);
+  gs_stage_f<2, false>(x, F[1], small, 4 * s0, q, qinv);
+  gs_stage_f<4, false>(x, F[2], small, 2 * s0, q, qinv);
+  gs_stage_f<8, false>(x, F[3], small, s0, q, qinv);
   double* my = lds + sp * (16 * kPadRow);
 #pragma unroll
   for (int r = 0; r < 16; ++r) my[pad16(16 * s0 + r)] = x[r];
   __syncthreads();
 #pragma unroll
   for (int r = 0; r < 16; ++r) x[r] = my[pad16(s0 + 16 * r)];
-  gs_head<4>(x, tw, n, base + s0, 4, q, qinv);
+  // t = 16, 32, 64, 128 on values s0 + 16 r
+  gs_stage_f<1, true>(x, F[4], small, 0, q, qinv);
+  gs_stage_f<2, true>(x, F[5], small, 0, q, qinv);
+  gs_stage_f<4, true>(x, F[6], small, 0, q, qinv);
+  gs_stage_f<8, true>(x, F[7], small, 0, q, qinv);
   double* dst = reinterpret_cast<double*>(row) + base;
 #pragma unroll
   for (int r = 0; r < 16; ++r) dst[s0 + 16 * r] = x[r];
@@ -278,8 +355,9 @@ void launch_outer(bool inverse, dim3 grid, hipStream_t s, RowSel rs, uint32_t lo
 
 }  // namespace
 
-hipError_t launch_ntt_rows(const Context* c, const RowSel& rs, uint32_t batch, uint32_t limbs,
-                           bool inverse, hipStream_t s) {
+// Both passes of one batch chunk.
+static hipError_t launch_chunk(const Context* c, const RowSel& rs, uint32_t batch, uint32_t limbs,
+                               bool inverse, hipStream_t s) {
   const uint32_t log_n = c->log_n;
   const double2* tw = inverse ? c->d_tw_inv : c->d_tw_fwd;
   dim3 inner(c->n / 4096, batch, limbs);
@@ -297,6 +375,14 @@ hipError_t launch_ntt_rows(const Context* c, const RowSel& rs, uint32_t batch, u
   if (!inverse)
     hipLaunchKernelGGL(k_fwd_inner, inner, dim3(kThreads), 0, s, rs, log_n, c->d_pk, tw);
   return hipGetLastError();
+}
+
+// (Splitting a large batch into cache-sized chunks, so that the second pass
+// would read the first pass's output back from the 256 MB Infinity Cache,
+// measured slower on MI355X than one launch per pass over the whole batch.)
+hipError_t launch_ntt_rows(const Context* c, const RowSel& rs, uint32_t batch, uint32_t limbs,
+                           bool inverse, hipStream_t s) {
+  return launch_chunk(c, rs, batch, limbs, inverse, s);
 }
 
 hipError_t launch_ntt(const Context* c, uint64_t* d, uint32_t batch, size_t batch_stride,

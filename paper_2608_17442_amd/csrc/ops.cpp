@@ -2,6 +2,7 @@
 // scratch layout, and the launch sequences of key switching, rotation,
 // relinearisation, rescaling, key generation and encryption.  Every launch is
 // asynchronous on the caller's stream; nothing here synchronises.
+#include <algorithm>
 #include <string>
 #include <vector>
 
@@ -56,7 +57,8 @@ const LevelTables* level_tables(Context* c, uint32_t level, int* err) {
     pmod[i] = entry(P, q);
     if (i < level) {
       md_pinv[i] = entry(h_inv(P, q), q);
-      for (uint32_t a = 0; a < alpha; ++a) md_hat[(size_t)i * alpha + a] = entry(prod_mod_except(ps, a, q), q);
+      for (uint32_t a = 0; a < alpha; ++a)
+        md_hat[(size_t)i * alpha + a] = entry(prod_mod_except(ps, a, q), q);
       if (i + 1 < level) rs_inv[i] = entry(h_inv(c->primes[level - 1] % q, q), q);
     }
   }
@@ -64,7 +66,8 @@ const LevelTables* level_tables(Context* c, uint32_t level, int* err) {
   LevelTables T;
   T.level = level;
   size_t off[7];
-  const std::vector<double2>* parts[7] = {&mu_inv, &mu_hat, &md_inv, &md_hat, &md_pinv, &pmod, &rs_inv};
+  const std::vector<double2>* parts[7] = {&mu_inv, &mu_hat, &md_inv, &md_hat,
+                                          &md_pinv, &pmod,   &rs_inv};
   for (int p = 0; p < 7; ++p) {
     off[p] = all.size();
     all.insert(all.end(), parts[p]->begin(), parts[p]->end());
@@ -94,31 +97,42 @@ const LevelTables* level_tables(Context* c, uint32_t level, int* err) {
 
 namespace {
 
-// One scratch layout, sized for the top level, shared by every operation.
+// One scratch layout, sized for the top level and a batch capacity B (1, or
+// kMaxBatch once a batched key switch is requested), shared by every
+// operation of the context.
 struct Scratch {
-  uint64_t* cin;  // [L][2][N]        private copy of an aliased input
-  uint64_t* cc;   // [L][N]           coefficient form of the switched polynomial
-  uint64_t* ext;  // [dnum][L+a][N]   ModUp output
-  uint64_t* acc;  // [2][L+a][N]      key inner products
-  uint64_t* y;    // [2][L][N]        ModDown conversion
-  uint64_t* d01;  // [L][2][N]        tensor (d0, d1)
-  uint64_t* d2;   // [L][N]           tensor d2
-  uint64_t* v;    // [2][N]           rescale: last limb
-  uint64_t* w;    // [2][L][N]        rescale: lifted last limb
-  uint64_t* ws;   // [3][L][2][N]     ciphertexts of composite operations
+  uint32_t cap;
+  uint64_t* cin;  // [L][2][N]          private copy of an aliased input
+  uint64_t* cc;   // [B][L][N]          coefficient form of switched polynomials
+  uint64_t* ext;  // [B][dnum][L+a][N]  ModUp outputs
+  uint64_t* acc;  // [B][2][L+a][N]     key inner products
+  uint64_t* y;    // [B][2][L][N]       ModDown conversions
+  uint64_t* d01;  // [L][2][N]          tensor (d0, d1)
+  uint64_t* d2;   // [L][N]             tensor d2
+  uint64_t* v;    // [2][N]             rescale: last limb
+  uint64_t* w;    // [2][L][N]          rescale: lifted last limb
+  uint64_t* ws;   // [3][L][2][N]       ciphertexts of composite operations
 };
 
-int scratch(Context* c, Scratch* s) {
+int scratch(Context* c, Scratch* s, uint32_t batch = 1) {
   const size_t n = c->n, L = c->L, E = c->L + c->alpha;
-  const size_t sizes[10] = {2 * L * n, L * n, c->dnum * E * n, 2 * E * n, 2 * L * n,
-                            2 * L * n, L * n, 2 * n, 2 * L * n, 6 * L * n};
+  size_t B = batch <= 1 ? 1 : kMaxBatch;
+  if (c->scratch_bytes) {  // keep the larger capacity once allocated
+    const size_t per_b = (L + c->dnum * E + 2 * E + 2 * L) * n * 8;
+    const size_t fixed = (2 * L + 2 * L + L + 2 + 2 * L + 6 * L) * n * 8;
+    if (c->scratch_bytes >= fixed + kMaxBatch * per_b) B = kMaxBatch;
+  }
+  const size_t sizes[10] = {2 * L * n,     B * L * n, B * c->dnum * E * n, B * 2 * E * n,
+                            B * 2 * L * n, 2 * L * n, L * n,               2 * n,
+                            2 * L * n,     6 * L * n};
   size_t total = 0;
   for (size_t x : sizes) total += x;
   int err;
   uint64_t* base = static_cast<uint64_t*>(scratch_get(c, total * sizeof(uint64_t), &err));
   if (!base) return err;
-  uint64_t** dst[10] = {&s->cin, &s->cc,  &s->ext, &s->acc, &s->y,
-                        &s->d01, &s->d2,  &s->v,   &s->w,   &s->ws};
+  s->cap = (uint32_t)B;
+  uint64_t** dst[10] = {&s->cin, &s->cc, &s->ext, &s->acc, &s->y,
+                        &s->d01, &s->d2, &s->v,   &s->w,   &s->ws};
   for (int i = 0; i < 10; ++i) {
     *dst[i] = base;
     base += sizes[i];
@@ -126,50 +140,69 @@ int scratch(Context* c, Scratch* s) {
   return FESC_OK;
 }
 
-#define HIPCK(expr)                                   \
-  do {                                                \
-    hipError_t e_ = (expr);                           \
+#define HIPCK(expr)                                    \
+  do {                                                 \
+    hipError_t e_ = (expr);                            \
     if (e_ != hipSuccess) return hip_check(e_, #expr); \
   } while (0)
 
 hipError_t ntt_rows(const Context* c, uint64_t* d, uint32_t batch, size_t batch_stride,
                     uint32_t limbs, uint32_t prime0, bool inverse, hipStream_t s) {
-  RowSel rs{d, batch_stride, (size_t)c->n, prime0, limbs, 0, 0, 0};
+  RowSel rs{d, batch_stride, (size_t)c->n, prime0, limbs, 0, 0, 0, 0};
   return launch_ntt_rows(c, rs, batch, limbs, inverse, s);
 }
 
-// ModUp of the polynomial whose row i is at in + i*in_stride (evaluation
-// form): cc <- inverse transform of a copy, ext <- converted digits, forward
-// transformed (own-digit rows are left to the inner product).
-int modup(Context* c, const LevelTables& T, const Scratch& S, const uint64_t* in,
-          size_t in_stride, uint32_t level, hipStream_t s) {
-  const size_t n = c->n;
-  HIPCK(hipMemcpy2DAsync(S.cc, n * 8, in, in_stride * 8, n * 8, level, hipMemcpyDeviceToDevice, s));
-  HIPCK(ntt_rows(c, S.cc, 1, 0, level, 0, true, s));
-  HIPCK(k_modup_launch(c, T, S.cc, S.ext, level, s));
-  const uint32_t E = level + c->alpha, dnum_l = (level + c->alpha - 1) / c->alpha;
-  RowSel rs{S.ext, (size_t)E * n, n, 0, level, c->L, c->alpha, level};
-  HIPCK(launch_ntt_rows(c, rs, dnum_l, E, false, s));
-  return FESC_OK;
-}
-
-// Inner product with `key` (sigma_g on the digits when galois != 0), ModDown,
-// and the combine into `out` (ciphertext layout).
-int ip_moddown(Context* c, const LevelTables& T, const Scratch& S, const uint64_t* in,
-               size_t in_stride, const uint64_t* key, uint32_t galois, const uint64_t* add,
-               uint32_t add_mask, uint32_t add_galois, uint64_t* out, uint32_t level,
-               hipStream_t s) {
-  const size_t n = c->n;
-  const uint32_t E = level + c->alpha;
-  HIPCK(k_ip_launch(c, S.ext, in, in_stride, key, S.acc, level, galois, s));
-  HIPCK(ntt_rows(c, S.acc + (size_t)level * n, 2, (size_t)E * n, c->alpha, c->L, true, s));
-  HIPCK(k_moddown_bconv_launch(c, T, S.acc, S.y, level, s));
-  HIPCK(ntt_rows(c, S.y, 2, (size_t)level * n, level, 0, false, s));
-  HIPCK(k_ks_combine_launch(c, T, S.acc, S.y, add, add_mask, add_galois, out, level, s));
-  return FESC_OK;
-}
-
 }  // namespace
+
+// --------------------------------------------------------- key switch engine
+
+int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& srcs,
+                     const std::vector<KsJob>& jobs, hipStream_t s) {
+  if (jobs.empty()) return FESC_OK;
+  if (srcs.size() > kMaxBatch) return fail(FESC_ERR_ARG, "too many key-switch sources");
+  int err;
+  const LevelTables* T = level_tables(c, level, &err);
+  if (!T) return err;
+  Scratch S;
+  if ((err = scratch(c, &S, (uint32_t)std::max(srcs.size(), jobs.size())))) return err;
+  const size_t n = c->n;
+  const uint32_t E = level + c->alpha, dnum_l = (level + c->alpha - 1) / c->alpha;
+  KsTable tab{};
+  for (size_t i = 0; i < srcs.size(); ++i) {
+    tab.src_in[i] = srcs[i].in;
+    tab.src_stride[i] = srcs[i].stride;
+  }
+  // ModUp of every source (the scratch capacity covers all of them)
+  const uint32_t ns = (uint32_t)srcs.size();
+  if (ns > S.cap) return fail(FESC_ERR_ARG, "key-switch sources exceed the scratch capacity");
+  HIPCK(k_gather_launch(c, tab, ns, S.cc, level, s));
+  HIPCK(ntt_rows(c, S.cc, ns, (size_t)level * n, level, 0, true, s));
+  HIPCK(k_modup_launch(c, *T, S.cc, S.ext, ns, level, s));
+  RowSel rs{S.ext, (size_t)E * n, n, 0, level, c->L, c->alpha, level, dnum_l};
+  HIPCK(launch_ntt_rows(c, rs, ns * dnum_l, E, false, s));
+  // jobs
+  for (size_t j0 = 0; j0 < jobs.size(); j0 += S.cap) {
+    const uint32_t nj = std::min<uint32_t>(S.cap, (uint32_t)(jobs.size() - j0));
+    KsTable t = tab;
+    for (uint32_t j = 0; j < nj; ++j) {
+      const KsJob& J = jobs[j0 + j];
+      t.job_src[j] = J.src;
+      t.key[j] = J.key;
+      t.galois[j] = J.galois;
+      t.add[j] = J.add;
+      t.add_mask[j] = J.add ? J.add_mask : 0;
+      t.add_galois[j] = J.add_galois;
+      t.add2[j] = J.add2;
+      t.out[j] = J.out;
+    }
+    HIPCK(k_ip_launch(c, t, nj, S.ext, S.acc, level, s));
+    HIPCK(ntt_rows(c, S.acc + (size_t)level * n, 2 * nj, (size_t)E * n, c->alpha, c->L, true, s));
+    HIPCK(k_moddown_bconv_launch(c, *T, S.acc, S.y, nj, level, s));
+    HIPCK(ntt_rows(c, S.y, 2 * nj, (size_t)level * n, level, 0, false, s));
+    HIPCK(k_ks_combine_launch(c, *T, t, nj, S.acc, S.y, level, s));
+  }
+  return FESC_OK;
+}
 
 // ------------------------------------------------------------------- drivers
 
@@ -182,26 +215,31 @@ uint32_t galois_of_step(const Context* c, int32_t step) {
   return (uint32_t)h_powmod(5, (uint64_t)r, two_n);
 }
 
+static int key_of(Context* c, uint32_t g, const uint64_t** key) {
+  auto it = c->keys.find(g);
+  if (it == c->keys.end())
+    return fail(FESC_ERR_NO_KEY, g == 0 ? std::string("no relinearisation key")
+                                        : "no switching key for Galois element " +
+                                              std::to_string(g));
+  *key = it->second;
+  return FESC_OK;
+}
+
+// Rotations of one ciphertext sharing one ModUp.
 int op_rotate_many(Context* c, const uint64_t* in, uint32_t count, const int32_t* steps,
                    uint64_t* const* outs, uint32_t level, hipStream_t s) {
   const size_t n = c->n, ct_words = (size_t)2 * level * n;
   std::vector<uint32_t> gal(count);
-  bool any = false;
+  std::vector<const uint64_t*> keys(count, nullptr);
+  int err;
   for (uint32_t r = 0; r < count; ++r) {
     gal[r] = galois_of_step(c, steps[r]);
-    if (gal[r] != 1) {
-      if (!c->keys.count(gal[r]))
-        return fail(FESC_ERR_NO_KEY, "no switching key for Galois element " + std::to_string(gal[r]));
-      any = true;
-    }
+    if (gal[r] != 1 && (err = key_of(c, gal[r], &keys[r]))) return err;
   }
-  int err;
-  const LevelTables* T = level_tables(c, level, &err);
-  if (!T) return err;
   Scratch S;
-  if ((err = scratch(c, &S))) return err;
+  if ((err = scratch(c, &S, count))) return err;
   // an output that aliases the input would be overwritten while later
-  // rotations still read the input: work from a private copy then
+  // rotations still read it: work from a private copy then
   const uint64_t* src = in;
   for (uint32_t r = 0; r < count; ++r)
     if (outs[r] == in) {
@@ -209,32 +247,59 @@ int op_rotate_many(Context* c, const uint64_t* in, uint32_t count, const int32_t
       src = S.cin;
       break;
     }
-  if (any && (err = modup(c, *T, S, src + n, 2 * n, level, s))) return err;
+  std::vector<KsJob> jobs;
   for (uint32_t r = 0; r < count; ++r) {
     if (gal[r] == 1) {
       if (outs[r] != src)
         HIPCK(hipMemcpyAsync(outs[r], src, ct_words * 8, hipMemcpyDeviceToDevice, s));
       continue;
     }
-    if ((err = ip_moddown(c, *T, S, src + n, 2 * n, c->keys[gal[r]], gal[r], src, 1u, gal[r],
-                          outs[r], level, s)))
-      return err;
+    jobs.push_back(KsJob{0, keys[r], gal[r], src, 1u, gal[r], nullptr, outs[r]});
+  }
+  return key_switch_batch(c, level, {KsSource{src + n, 2 * n}}, jobs, s);
+}
+
+// Rotation of `count` different ciphertexts, ins[i] by steps[i] into outs[i]
+// (+ add2[i] when given).  Outputs must not alias inputs.
+int op_rotate_batch(Context* c, uint32_t count, const uint64_t* const* ins,
+                    const int32_t* steps, uint64_t* const* outs, const uint64_t* const* add2,
+                    uint32_t level, hipStream_t s) {
+  const size_t n = c->n, ct_words = (size_t)2 * level * n;
+  int err;
+  for (uint32_t b0 = 0; b0 < count; b0 += kMaxBatch) {
+    const uint32_t nb = std::min(kMaxBatch, count - b0);
+    std::vector<KsSource> srcs;
+    std::vector<KsJob> jobs;
+    for (uint32_t i = b0; i < b0 + nb; ++i) {
+      const uint32_t g = galois_of_step(c, steps[i]);
+      const uint64_t* a2 = add2 ? add2[i] : nullptr;
+      if (g == 1) {
+        if (a2)
+          HIPCK(k_binary_launch(c, ins[i], a2, outs[i], 2 * level, 1, 0, s));
+        else if (outs[i] != ins[i])
+          HIPCK(hipMemcpyAsync(outs[i], ins[i], ct_words * 8, hipMemcpyDeviceToDevice, s));
+        continue;
+      }
+      const uint64_t* key;
+      if ((err = key_of(c, g, &key))) return err;
+      jobs.push_back(KsJob{(uint32_t)srcs.size(), key, g, ins[i], 1u, g, a2, outs[i]});
+      srcs.push_back(KsSource{ins[i] + n, 2 * n});
+    }
+    if ((err = key_switch_batch(c, level, srcs, jobs, s))) return err;
   }
   return FESC_OK;
 }
 
 int op_mul_relin(Context* c, const uint64_t* a, const uint64_t* b, uint64_t* out,
                  uint32_t level, hipStream_t s) {
-  auto it = c->keys.find(0);
-  if (it == c->keys.end()) return fail(FESC_ERR_NO_KEY, "no relinearisation key");
+  const uint64_t* key;
   int err;
-  const LevelTables* T = level_tables(c, level, &err);
-  if (!T) return err;
+  if ((err = key_of(c, 0, &key))) return err;
   Scratch S;
   if ((err = scratch(c, &S))) return err;
   HIPCK(k_tensor_launch(c, a, b, S.d01, S.d2, level, s));
-  if ((err = modup(c, *T, S, S.d2, c->n, level, s))) return err;
-  return ip_moddown(c, *T, S, S.d2, c->n, it->second, 0, S.d01, 3u, 0, out, level, s);
+  return key_switch_batch(c, level, {KsSource{S.d2, c->n}},
+                          {KsJob{0, key, 0, S.d01, 3u, 0, nullptr, out}}, s);
 }
 
 int op_rescale(Context* c, const uint64_t* in, uint64_t* out, uint32_t level, hipStream_t s) {
@@ -292,7 +357,6 @@ int op_encrypt(Context* c, const int8_t* sk, const int64_t* m, const uint64_t* a
   Scratch S;
   int err;
   if ((err = scratch(c, &S))) return err;
-  const size_t n = c->n;
   uint64_t* me = S.cc;
   uint64_t* et = S.y;
   uint64_t* sl = S.d2;
@@ -303,7 +367,6 @@ int op_encrypt(Context* c, const int8_t* sk, const int64_t* m, const uint64_t* a
   HIPCK(k_lift_launch(c, nullptr, sk, sl, level, 0, level, 0, s));
   HIPCK(ntt_rows(c, sl, 1, 0, level, 0, false, s));
   HIPCK(k_encrypt_launch(c, a, sl, me, ct, level, s));
-  (void)n;
   return FESC_OK;
 }
 
@@ -313,10 +376,6 @@ int op_plain_from_coeffs(Context* c, const int64_t* m, uint64_t* pt, uint32_t le
   HIPCK(ntt_rows(c, pt, 1, 0, level, 0, false, s));
   return FESC_OK;
 }
-
-}  // namespace fesc
-
-namespace fesc {
 
 // Scan-contract slice of one token (see fesc.h): per chunk k,
 //   t2_k = RS(relin(RS(relin(decay_k * h_k)) * c_k)),
@@ -344,7 +403,7 @@ int op_scan_contract(Context* c, const uint64_t* const* h, const uint64_t* const
     for (uint32_t st = d_s / 2; st >= 1; st /= 2) {
       const int32_t step = (int32_t)st;
       int e;
-      if ((e = op_rotate_many(c, x, 1, &step, &tmp, lo, s))) return e;
+      if ((e = op_rotate_batch(c, 1, &x, &step, &tmp, nullptr, lo, s))) return e;
       HIPCK(k_binary_launch(c, x, tmp, x, 2 * lo, 1, 0, s));
     }
     return FESC_OK;
@@ -354,13 +413,12 @@ int op_scan_contract(Context* c, const uint64_t* const* h, const uint64_t* const
     HIPCK(k_binary_launch(c, out[l], chi, chi, 2 * lo, 1, 0, s));
     if ((err = reduce(chi))) return err;
     const int32_t cj = INT32_MIN;
-    if ((err = op_rotate_many(c, chi, 1, &cj, &tmp, lo, s))) return err;
+    if ((err = op_rotate_batch(c, 1, &chi, &cj, &tmp, nullptr, lo, s))) return err;
     HIPCK(k_binary_launch(c, chi, tmp, out[l], 2 * lo, 1, 0, s));
     HIPCK(k_binary_launch(c, chi, tmp, tmp, 2 * lo, 1, 1, s));
     HIPCK(k_monomial_launch(c, tmp, out[l + 1], lo, 3 * c->n / 2, s));
   }
   if (K % 2 && (err = reduce(out[K - 1]))) return err;
-  (void)n;
   return FESC_OK;
 }
 

@@ -2,6 +2,8 @@
 // drivers of ops.cpp.
 #pragma once
 
+#include <vector>
+
 #include "fesc_internal.hpp"
 
 namespace fesc {
@@ -33,27 +35,68 @@ hipError_t k_rescale_combine_launch(const Context* c, const uint64_t* in, const 
 
 // ----------------------------------------------------------- keyswitch.hip
 
-// Scratch buffers of one key switch at `level` (all uint64, device).
-struct KsBuffers {
-  uint64_t* cc;   // [level][N]                 coefficient form of the input
-  uint64_t* ext;  // [dnum][level+alpha][N]     ModUp output, evaluation form
-  uint64_t* acc;  // [2][level+alpha][N]        inner products
-  uint64_t* y;    // [2][level][N]              ModDown conversion
+// Up to kMaxBatch ModUp sources and key-switch jobs per launch.  Passed by
+// value as a kernel argument (2 KB).
+constexpr uint32_t kMaxBatch = 32;
+
+struct KsTable {
+  const uint64_t* src_in[kMaxBatch];  // source s: row i at src_in[s] + i*src_stride[s]
+  uint64_t src_stride[kMaxBatch];
+  const uint64_t* key[kMaxBatch];     // job: switching key
+  const uint64_t* add[kMaxBatch];     // job: ciphertext added after sigma_g (or null)
+  const uint64_t* add2[kMaxBatch];    // job: ciphertext added as is (or null)
+  uint64_t* out[kMaxBatch];           // job: output ciphertext
+  uint32_t job_src[kMaxBatch];        // job: its ModUp source
+  uint32_t galois[kMaxBatch];         // job: Galois element on the digits (0: none)
+  uint32_t add_mask[kMaxBatch];       // job: components of `add` used (bit t)
+  uint32_t add_galois[kMaxBatch];     // job: permutation of `add` (0: none)
 };
 
+hipError_t k_gather_launch(const Context* c, const KsTable& tab, uint32_t nsrc, uint64_t* cc,
+                           uint32_t level, hipStream_t s);
 hipError_t k_modup_launch(const Context* c, const LevelTables& T, const uint64_t* cc,
-                          uint64_t* ext, uint32_t level, hipStream_t s);
-hipError_t k_ip_launch(const Context* c, const uint64_t* ext, const uint64_t* in,
-                       size_t in_stride, const uint64_t* key, uint64_t* acc, uint32_t level,
-                       uint32_t galois, hipStream_t s);
+                          uint64_t* ext, uint32_t nsrc, uint32_t level, hipStream_t s);
+hipError_t k_ip_launch(const Context* c, const KsTable& tab, uint32_t njobs, const uint64_t* ext,
+                       uint64_t* acc, uint32_t level, hipStream_t s);
 hipError_t k_moddown_bconv_launch(const Context* c, const LevelTables& T, const uint64_t* acc,
-                                  uint64_t* y, uint32_t level, hipStream_t s);
-hipError_t k_ks_combine_launch(const Context* c, const LevelTables& T, const uint64_t* acc,
-                               const uint64_t* y, const uint64_t* add, uint32_t add_mask,
-                               uint32_t add_galois, uint64_t* out, uint32_t level,
-                               hipStream_t s);
+                                  uint64_t* y, uint32_t njobs, uint32_t level, hipStream_t s);
+hipError_t k_ks_combine_launch(const Context* c, const LevelTables& T, const KsTable& tab,
+                               uint32_t njobs, const uint64_t* acc, const uint64_t* y,
+                               uint32_t level, hipStream_t s);
 
 // ------------------------------------------------------------------ ops.cpp
 const LevelTables* level_tables(Context* c, uint32_t level, int* err);
+
+// One key switch: polynomial of source `src` switched with `key` under
+// Galois element `galois`, combined into `out` (see KsTable).
+struct KsJob {
+  uint32_t src;
+  const uint64_t* key;
+  uint32_t galois;
+  const uint64_t* add;
+  uint32_t add_mask;
+  uint32_t add_galois;
+  const uint64_t* add2;
+  uint64_t* out;
+};
+struct KsSource {
+  const uint64_t* in;
+  size_t stride;
+};
+
+// Runs any number of key switches at one level: ModUp of every source (in
+// groups of kMaxBatch), then inner product, ModDown and combine of the jobs
+// in groups of kMaxBatch.  Sources must stay unmodified until all jobs have
+// read them; outputs must not alias sources or adds of later groups.
+int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& srcs,
+                     const std::vector<KsJob>& jobs, hipStream_t s);
+
+int op_rotate_many(Context* c, const uint64_t* in, uint32_t count, const int32_t* steps,
+                   uint64_t* const* outs, uint32_t level, hipStream_t s);
+int op_rotate_batch(Context* c, uint32_t count, const uint64_t* const* ins,
+                    const int32_t* steps, uint64_t* const* outs, const uint64_t* const* add2,
+                    uint32_t level, hipStream_t s);
+int op_rescale(Context* c, const uint64_t* in, uint64_t* out, uint32_t level, hipStream_t s);
+uint32_t galois_of_step(const Context* c, int32_t step);
 
 }  // namespace fesc

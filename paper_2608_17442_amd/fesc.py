@@ -50,6 +50,8 @@ _SIGS = {
     "fesc_rotate": [_vp, _vp, _vp, _u32, _i32, _vp],
     "fesc_rotate_hoisted": [_vp, _vp, _u32, ctypes.POINTER(_i32), ctypes.POINTER(_vp), _u32,
                             _vp],
+    "fesc_rotate_batch": [_vp, _u32, ctypes.POINTER(_vp), ctypes.POINTER(_i32),
+                          ctypes.POINTER(_vp), _u32, _vp],
     "fesc_keygen": [_vp, _u32, _vp, _vp, _vp, _vp],
     "fesc_key_load": [_vp, _u32, _vp, _vp],
     "fesc_key_store": [_vp, _u32, _vp, _vp],
@@ -188,6 +190,13 @@ class Context:
         ptrs = (_vp * len(outs))(*[_ptr(o) for o in outs])
         _check(_lib.fesc_rotate_hoisted(self._h, _ptr(ct), len(steps), st, ptrs, level,
                                         _stream(stream)))
+
+    def rotate_batch(self, cts, steps, outs, level, stream=None):
+        n = len(cts)
+        a = (_vp * n)(*[_ptr(t) for t in cts])
+        st = (_i32 * n)(*steps)
+        b = (_vp * n)(*[_ptr(t) for t in outs])
+        _check(_lib.fesc_rotate_batch(self._h, n, a, st, b, level, _stream(stream)))
 
     def keygen(self, galois_elt, s, a, e, stream=None):
         _check(_lib.fesc_keygen(self._h, galois_elt, _ptr(s), _ptr(a), _ptr(e), _stream(stream)))

@@ -164,6 +164,27 @@ def test_mul_relin(log_n, bits, L, alpha):
         np.testing.assert_allclose(C.decrypt(P, S.sk, want, 2.0 ** 40), z1 * z2, atol=2.0 ** -7)
 
 
+@pytest.mark.parametrize("log_n,bits,L,alpha", SMALL)
+def test_rotate_batch(log_n, bits, L, alpha):
+    """Independent ciphertexts rotated in one batch (more than one launch
+    group of 32, identity and conjugation steps mixed in) equal the oracle's
+    single rotations."""
+    from paper_2608_17442_amd.fesc import CONJ
+    P = C.params_small(log_n, bits, L, alpha)
+    base = [1, 2, 3, -1, 7, 0]
+    S = Setup(P, 14, rot_steps=base, conj=True)
+    level = L - 1
+    count = 37
+    steps = [base[i % len(base)] if i % 9 else CONJ for i in range(count)]
+    cts = [S.encrypt(_z(400 + i, P.n // 2), 2.0 ** 30, level, 400 + i) for i in range(count)]
+    outs = [torch.zeros_like(cts[0][1]) for _ in range(count)]
+    step(f"rotate_batch count={count}")
+    S.ctx.rotate_batch([d for _, d in cts], steps, outs, level)
+    for i, ((co, _), st, o) in enumerate(zip(cts, steps, outs)):
+        want = C.conjugate(P, co, S.keys) if st == CONJ else C.rotate(P, co, st, S.keys)
+        _eq(o, want, f"batch item {i} step {st}")
+
+
 def test_error_codes():
     from paper_2608_17442_amd import fesc as F
     P = C.params_small(12, 50, 3, 1)
