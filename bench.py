@@ -139,7 +139,10 @@ class Workloads:
                                    seed, "cfg4", u) for u in range(n_in)]
         n_diag = n_out * n2 * n_in * n1
         log(f"encoding {n_diag} diagonals ({n_diag * level * self.n * 8 / 1e9:.1f} GB)")
-        self.diags = torch.empty((n_diag, level * self.n), dtype=torch.int64, device="cuda")
+        desc = self.F.matvec_desc(level, n_in, n_out, n1, n2, seg, True, True)
+        self.bank = torch.empty(self.F.matvec_bank_words(self.ctx, desc), dtype=torch.int64,
+                                device="cuda")
+        stage = [torch.empty(level * self.n, dtype=torch.int64, device="cuda") for _ in range(8)]
         scale = float(self.q[level - 1])
         index = [(b, p, u, q) for b in range(n_out) for p in range(n2) for u in range(n_in)
                  for q in range(n1)]
@@ -157,11 +160,13 @@ class Workloads:
                 ids = list(range(c0, min(c0 + chunk, n_diag)))
                 coeffs = torch.from_numpy(np.stack(list(ex.map(enc_one, ids)))).cuda()
                 for j, t in enumerate(ids):
-                    self.ctx.plain_from_coeffs(coeffs[j], self.diags[t], level)
+                    pt = stage[t % len(stage)]
+                    self.ctx.plain_from_coeffs(coeffs[j], pt, level)
+                    self.F.matvec_bank_pack(self.ctx, desc, self.bank, t, pt)
         torch.cuda.synchronize()
         log(f"diagonals ready in {time.perf_counter() - t0:.1f} s")
         self.mv_plan = self.F.MatvecPlan(self.ctx, level, n_in, n_out, n1, n2, seg, True, True,
-                                         [self.diags[t] for t in range(n_diag)])
+                                         bank=self.bank)
         self.mv_out = [torch.empty((level - 1) * 2 * self.n, dtype=torch.int64, device="cuda")
                        for _ in range(n_out)]
         self.mv_shape = dict(n_in=n_in, n_out=n_out, n1=n1, n2=n2, n_diag=n_diag)

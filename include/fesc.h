@@ -228,6 +228,20 @@ void fesc_matvec_plan_destroy(fesc_matvec_plan* plan);
 int fesc_ptct_matvec(fesc_ctx* ctx, fesc_matvec_plan* plan, const uint64_t* const* in,
                      uint64_t* const* out, void* stream);
 
+/* Diagonal bank: the same diagonals in one device buffer tiled for
+ * streaming, [limb][N/256][n_out*n2][n_in*n1][256] (256-coefficient tiles;
+ * one workgroup of the plaintext MAC then reads a contiguous region).
+ * fesc_matvec_bank_words gives its size in uint64 words (level*N per
+ * diagonal); fesc_matvec_bank_pack copies plaintext `pt` ([level][N]) into
+ * slot `index` = ((b*n2 + p)*n_in + u)*n1 + q of the bank; a plan created
+ * from a bank reads it instead of a pointer table (results are identical).
+ * The bank must stay valid for the plan's lifetime. */
+int fesc_matvec_bank_words(const fesc_ctx* ctx, const fesc_matvec_desc* desc, size_t* words);
+int fesc_matvec_bank_pack(fesc_ctx* ctx, const fesc_matvec_desc* desc, uint64_t* bank,
+                          uint32_t index, const uint64_t* pt, void* stream);
+int fesc_matvec_plan_create_bank(fesc_ctx* ctx, const fesc_matvec_desc* desc,
+                                 const uint64_t* bank, fesc_matvec_plan** plan);
+
 /* Phase durations of the plan's last completed run, from HIP events recorded
  * on its stream: baby steps, pt-MAC (one kernel), giant steps + extraction +
  * rescale.  The caller synchronises first; FESC_ERR_HIP if not complete. */

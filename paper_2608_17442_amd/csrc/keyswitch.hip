@@ -23,7 +23,17 @@ namespace fesc {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr uint32_t kRowsPerZ = 8;
+// Basis-conversion launches split the target rows over gridDim.z only as far
+// as needed to reach about kTargetBlocks workgroups: every split recomputes
+// the centred digits of its coefficients.
+constexpr uint32_t kTargetBlocks = 4096;
+constexpr uint32_t kMinRowsPerZ = 4;
+
+uint32_t row_splits(uint32_t xy_blocks, uint32_t rows) {
+  uint32_t z = (kTargetBlocks + xy_blocks - 1) / xy_blocks;
+  const uint32_t zmax = (rows + kMinRowsPerZ - 1) / kMinRowsPerZ;
+  return z < 1 ? 1 : (z > zmax ? zmax : z);
+}
 
 __device__ __forceinline__ uint32_t ext_prime(uint32_t row, uint32_t level, uint32_t L) {
   return row < level ? row : L + (row - level);
@@ -75,7 +85,8 @@ __global__ __launch_bounds__(kThreads) void k_modup(const uint64_t* __restrict__
       x1[a] = center(red_full(mm_shoup(u2d(v.y), f.x, f.y, P.q), P.q, P.qinv), P.q);
     }
   }
-  const uint32_t r0 = blockIdx.z * kRowsPerZ, r1 = min(r0 + kRowsPerZ, E);
+  const uint32_t per = (E + gridDim.z - 1) / gridDim.z;
+  const uint32_t r0 = blockIdx.z * per, r1 = min(r0 + per, E);
   for (uint32_t row = r0; row < r1; ++row) {
     if (row >= lo && row < hi) continue;
     const PrimeK M = pk[ext_prime(row, level, L)];
@@ -166,7 +177,8 @@ __global__ __launch_bounds__(kThreads) void k_moddown_bconv(const uint64_t* __re
       x1[a] = center(red_full(mm_shoup(u2d(v.y), f.x, f.y, P.q), P.q, P.qinv), P.q);
     }
   }
-  const uint32_t i0 = blockIdx.z * kRowsPerZ, i1 = min(i0 + kRowsPerZ, level);
+  const uint32_t per = (level + gridDim.z - 1) / gridDim.z;
+  const uint32_t i0 = blockIdx.z * per, i1 = min(i0 + per, level);
   for (uint32_t i = i0; i < i1; ++i) {
     const PrimeK M = pk[i];
     const double2* h = md_hat + (size_t)i * alpha;
@@ -232,7 +244,8 @@ hipError_t k_modup_launch(const Context* c, const LevelTables& T, const uint64_t
                           uint64_t* ext, uint32_t nsrc, uint32_t level, hipStream_t s) {
   const uint32_t dnum_l = (level + c->alpha - 1) / c->alpha;
   const uint32_t E = level + c->alpha;
-  dim3 grid((c->n / 2 + kThreads - 1) / kThreads, nsrc * dnum_l, (E + kRowsPerZ - 1) / kRowsPerZ);
+  const uint32_t xb = (c->n / 2 + kThreads - 1) / kThreads;
+  dim3 grid(xb, nsrc * dnum_l, row_splits(xb * nsrc * dnum_l, E));
   if (c->alpha <= 8)
     hipLaunchKernelGGL(k_modup<8>, grid, dim3(kThreads), 0, s, cc, ext, level, c->L, c->alpha,
                        dnum_l, c->n, c->d_pk, T.mu_inv, T.mu_hat);
@@ -253,7 +266,8 @@ hipError_t k_ip_launch(const Context* c, const KsTable& tab, uint32_t njobs, con
 
 hipError_t k_moddown_bconv_launch(const Context* c, const LevelTables& T, const uint64_t* acc,
                                   uint64_t* y, uint32_t njobs, uint32_t level, hipStream_t s) {
-  dim3 grid((c->n / 2 + kThreads - 1) / kThreads, 2 * njobs, (level + kRowsPerZ - 1) / kRowsPerZ);
+  const uint32_t xb = (c->n / 2 + kThreads - 1) / kThreads;
+  dim3 grid(xb, 2 * njobs, row_splits(xb * 2 * njobs, level));
   if (c->alpha <= 8)
     hipLaunchKernelGGL(k_moddown_bconv<8>, grid, dim3(kThreads), 0, s, acc, y, level, c->L,
                        c->alpha, c->n, c->d_pk, T.md_inv, T.md_hat);

@@ -26,6 +26,7 @@ struct fesc_matvec_plan {
   const uint64_t** d_baby = nullptr;  // device table of baby pointers
   uint64_t** d_ct = nullptr;          // device table of c~ pointers
   size_t ct_words = 0;
+  const uint64_t* bank = nullptr;     // tiled diagonal bank (instead of the table), or null
   hipEvent_t ev[4] = {};               // phase marks of the last run
 };
 
@@ -38,35 +39,71 @@ uint32_t galois_of_step(const Context* c, int32_t step);
 
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kGroup = 16;  // outputs accumulated per thread
+constexpr int kThreads = 256;  // also the coefficient tile of the diagonal bank
+constexpr int kGroup = 16;     // outputs accumulated per thread
 
-template <int G>
+// Diagonal (o, t) of a bank: tiles of kThreads coefficients, ordered
+// [limb][tile][output][term][coefficient], so that one workgroup streams a
+// contiguous G * terms * 2 KB region.
+__host__ __device__ __forceinline__ size_t bank_offset(uint32_t i, uint32_t tile, uint32_t o,
+                                                       uint32_t t, uint32_t n,
+                                                       uint32_t n_outputs, uint32_t terms) {
+  const size_t tiles = n / kThreads;
+  return ((((size_t)i * tiles + tile) * n_outputs + o) * terms + t) * kThreads;
+}
+
+// BANK: diagonals from a tiled bank; otherwise from the table of plaintexts.
+template <int G, bool BANK>
 __global__ __launch_bounds__(kThreads) void k_ptmac(const uint64_t* const* __restrict__ baby,
                                                     const uint64_t* const* __restrict__ diag,
+                                                    const uint64_t* __restrict__ bank,
                                                     uint64_t* const* __restrict__ outs,
                                                     uint32_t n_outputs, uint32_t terms,
-                                                    uint32_t n, const PrimeK* __restrict__ pk) {
-  const uint32_t i = blockIdx.y;
-  const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
-  const uint32_t o0 = blockIdx.z * G;
-  if (k >= n) return;
+                                                    uint32_t n, uint32_t limbs,
+                                                    const PrimeK* __restrict__ pk) {
+  // 1-D grid over (coefficient tile, limb, output group).  Workgroups are
+  // dealt to the 8 XCDs round-robin; the decode keeps all output groups of one
+  // tile on the same XCD and adjacent in time, so the tile's baby-step values
+  // (read once per group) come from that XCD's L2 instead of HBM.
+  const uint32_t tiles = n / kThreads, n_groups = (n_outputs + G - 1) / G;
+  const uint32_t total_tiles = tiles * limbs;
+  uint32_t tile_lin, grp;
+  if ((total_tiles & 7u) == 0) {
+    const uint32_t L = blockIdx.x, xcd = L & 7u, slot = L >> 3;
+    grp = slot % n_groups;
+    tile_lin = (slot / n_groups) * 8u + xcd;
+  } else {
+    grp = blockIdx.x % n_groups;
+    tile_lin = blockIdx.x / n_groups;
+  }
+  const uint32_t i = tile_lin / tiles, tile = tile_lin % tiles;
+  const uint32_t k = tile * kThreads + threadIdx.x;
+  const uint32_t o0 = grp * G;
+  if (i >= limbs) return;
   const PrimeK P = pk[i];
   const uint32_t g_end = min((uint32_t)G, n_outputs - o0);
   double a0[G], a1[G];
 #pragma unroll
   for (int g = 0; g < G; ++g) a0[g] = a1[g] = 0.0;
   const size_t pi = (size_t)i * n + k, c0 = (size_t)2 * i * n + k, c1 = c0 + n;
+  const uint64_t* bk =
+      BANK ? bank + bank_offset(i, tile, o0, 0, n, n_outputs, terms) + threadIdx.x : nullptr;
+  const size_t o_stride = (size_t)terms * kThreads;
+  // Outputs past the end of a partial group re-read the group's last valid
+  // diagonal (results discarded at the store), which keeps the loop body free
+  // of branches so the G loads of a term are issued together.
+  uint32_t og[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) og[g] = min((uint32_t)g, g_end - 1);
   for (uint32_t t = 0; t < terms; ++t) {
     const uint64_t* bp = baby[t];
     const double x0 = u2d(bp[c0]), x1 = u2d(bp[c1]);
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      if ((uint32_t)g < g_end) {
-        const double w = u2d(diag[(size_t)(o0 + g) * terms + t][pi]);
-        a0[g] += mm_var(x0, w, P.q, P.qinv);
-        a1[g] += mm_var(x1, w, P.q, P.qinv);
-      }
+      const double w = BANK ? u2d(bk[og[g] * o_stride + (size_t)t * kThreads])
+                            : u2d(diag[(size_t)(o0 + og[g]) * terms + t][pi]);
+      a0[g] += mm_var(x0, w, P.q, P.qinv);
+      a1[g] += mm_var(x1, w, P.q, P.qinv);
     }
     if ((t & 3) == 3) {
 #pragma unroll
@@ -86,6 +123,16 @@ __global__ __launch_bounds__(kThreads) void k_ptmac(const uint64_t* const* __res
   }
 }
 
+// bank tile (i, tile, o, t) <- plaintext limb i, coefficients of the tile
+__global__ __launch_bounds__(kThreads) void k_bank_pack(const uint64_t* __restrict__ pt,
+                                                        uint64_t* __restrict__ bank, uint32_t o,
+                                                        uint32_t t, uint32_t n,
+                                                        uint32_t n_outputs, uint32_t terms) {
+  const uint32_t i = blockIdx.y, tile = blockIdx.x;
+  bank[bank_offset(i, tile, o, t, n, n_outputs, terms) + threadIdx.x] =
+      pt[(size_t)i * n + (size_t)tile * kThreads + threadIdx.x];
+}
+
 #define HIPCK(expr)                                   \
   do {                                                \
     hipError_t e_ = (expr);                           \
@@ -94,17 +141,25 @@ __global__ __launch_bounds__(kThreads) void k_ptmac(const uint64_t* const* __res
 
 }  // namespace
 
-int matvec_plan_create(Context* c, const fesc_matvec_desc* d, const uint64_t* const* diags,
-                       fesc_matvec_plan** out) {
-  if (!d || !diags || !out) return fail(FESC_ERR_ARG, "null argument");
-  *out = nullptr;
+int check_desc(const Context* c, const fesc_matvec_desc* d) {
+  if (!d) return fail(FESC_ERR_ARG, "null descriptor");
   if (d->level < 1 || d->level > c->L) return fail(FESC_ERR_LEVEL, "matvec level out of range");
   if (d->rescale && d->level < 2) return fail(FESC_ERR_LEVEL, "rescale needs level >= 2");
   if (!d->n_in || !d->n_out || !d->n1 || !d->n2 || !d->unit)
     return fail(FESC_ERR_ARG, "matvec sizes must be positive");
+  return FESC_OK;
+}
+
+int matvec_plan_create(Context* c, const fesc_matvec_desc* d, const uint64_t* const* diags,
+                       const uint64_t* bank, fesc_matvec_plan** out) {
+  if (!out || (!diags && !bank)) return fail(FESC_ERR_ARG, "null argument");
+  *out = nullptr;
+  int rc = check_desc(c, d);
+  if (rc) return rc;
   const size_t n_diag = (size_t)d->n_out * d->n2 * d->n_in * d->n1;
-  for (size_t t = 0; t < n_diag; ++t)
-    if (!diags[t]) return fail(FESC_ERR_ARG, "null diagonal " + std::to_string(t));
+  if (!bank)
+    for (size_t t = 0; t < n_diag; ++t)
+      if (!diags[t]) return fail(FESC_ERR_ARG, "null diagonal " + std::to_string(t));
   // every Galois key the schedule needs must be present
   std::vector<int64_t> steps;
   for (uint32_t q = 1; q < d->n1; ++q) steps.push_back((int64_t)q * d->unit);
@@ -119,20 +174,21 @@ int matvec_plan_create(Context* c, const fesc_matvec_desc* d, const uint64_t* co
 
   fesc_matvec_plan* p = new fesc_matvec_plan();
   p->d = *d;
-  p->diag.assign(diags, diags + n_diag);
+  p->bank = bank;
+  if (!bank) p->diag.assign(diags, diags + n_diag);
   p->ct_words = (size_t)2 * d->level * c->n;
   const size_t n_baby = (size_t)d->n_in * d->n1, n_ct = (size_t)d->n_out * d->n2;
   std::vector<const uint64_t*> baby(n_baby);
   std::vector<uint64_t*> cts(n_ct);
   bool ok = hipMalloc(&p->work, (n_baby + n_ct + d->n_out) * p->ct_words * 8) == hipSuccess &&
-            hipMalloc(&p->d_diag, n_diag * sizeof(void*)) == hipSuccess &&
+            (bank || hipMalloc(&p->d_diag, n_diag * sizeof(void*)) == hipSuccess) &&
             hipMalloc(&p->d_baby, n_baby * sizeof(void*)) == hipSuccess &&
             hipMalloc(&p->d_ct, n_ct * sizeof(void*)) == hipSuccess;
   if (ok) {
     for (size_t t = 0; t < n_baby; ++t) baby[t] = p->work + t * p->ct_words;
     for (size_t t = 0; t < n_ct; ++t) cts[t] = p->work + (n_baby + t) * p->ct_words;
-    ok = hipMemcpy(p->d_diag, p->diag.data(), n_diag * sizeof(void*), hipMemcpyHostToDevice) ==
-             hipSuccess &&
+    ok = (bank || hipMemcpy(p->d_diag, p->diag.data(), n_diag * sizeof(void*),
+                            hipMemcpyHostToDevice) == hipSuccess) &&
          hipMemcpy(p->d_baby, baby.data(), n_baby * sizeof(void*), hipMemcpyHostToDevice) ==
              hipSuccess &&
          hipMemcpy(p->d_ct, cts.data(), n_ct * sizeof(void*), hipMemcpyHostToDevice) == hipSuccess;
@@ -196,9 +252,15 @@ int ptct_matvec(Context* c, fesc_matvec_plan* p, const uint64_t* const* in,
   HIPCK(hipEventRecord(p->ev[1], s));
   // pt-MAC over all (b, p)
   const uint32_t n_outputs = d.n_out * d.n2;
-  dim3 grid((c->n + kThreads - 1) / kThreads, level, (n_outputs + kGroup - 1) / kGroup);
-  hipLaunchKernelGGL(k_ptmac<kGroup>, grid, dim3(kThreads), 0, s, p->d_baby, p->d_diag, p->d_ct,
-                     n_outputs, (uint32_t)n_baby, c->n, c->d_pk);
+  dim3 grid((c->n / kThreads) * level * ((n_outputs + kGroup - 1) / kGroup));
+  if (p->bank)
+    hipLaunchKernelGGL((k_ptmac<kGroup, true>), grid, dim3(kThreads), 0, s, p->d_baby,
+                       (const uint64_t* const*)nullptr, p->bank, p->d_ct, n_outputs,
+                       (uint32_t)n_baby, c->n, level, c->d_pk);
+  else
+    hipLaunchKernelGGL((k_ptmac<kGroup, false>), grid, dim3(kThreads), 0, s, p->d_baby,
+                       p->d_diag, (const uint64_t*)nullptr, p->d_ct, n_outputs,
+                       (uint32_t)n_baby, c->n, level, c->d_pk);
   HIPCK(hipGetLastError());
   HIPCK(hipEventRecord(p->ev[2], s));
   // giant steps: y_b += Phi^(p n1)(c~_{b,p}), one batch over b per p
@@ -247,7 +309,37 @@ extern "C" {
 int fesc_matvec_plan_create(fesc_ctx* ctx, const fesc_matvec_desc* desc,
                             const uint64_t* const* diags, fesc_matvec_plan** plan) {
   if (!ctx) return fesc::fail(FESC_ERR_ARG, "null context");
-  return fesc::matvec_plan_create(ctx, desc, diags, plan);
+  if (!diags) return fesc::fail(FESC_ERR_ARG, "null diagonal table");
+  return fesc::matvec_plan_create(ctx, desc, diags, nullptr, plan);
+}
+
+int fesc_matvec_bank_words(const fesc_ctx* ctx, const fesc_matvec_desc* desc, size_t* words) {
+  if (!ctx || !words) return fesc::fail(FESC_ERR_ARG, "null argument");
+  int rc = fesc::check_desc(ctx, desc);
+  if (rc) return rc;
+  *words = (size_t)desc->n_out * desc->n2 * desc->n_in * desc->n1 * desc->level * ctx->n;
+  return FESC_OK;
+}
+
+int fesc_matvec_bank_pack(fesc_ctx* ctx, const fesc_matvec_desc* desc, uint64_t* bank,
+                          uint32_t index, const uint64_t* pt, void* stream) {
+  if (!ctx || !bank || !pt) return fesc::fail(FESC_ERR_ARG, "null argument");
+  int rc = fesc::check_desc(ctx, desc);
+  if (rc) return rc;
+  const uint32_t terms = desc->n_in * desc->n1, outputs = desc->n_out * desc->n2;
+  if ((uint64_t)index >= (uint64_t)terms * outputs)
+    return fesc::fail(FESC_ERR_ARG, "diagonal index out of range");
+  hipLaunchKernelGGL(fesc::k_bank_pack, dim3(ctx->n / fesc::kThreads, desc->level),
+                     dim3(fesc::kThreads), 0, reinterpret_cast<hipStream_t>(stream), pt, bank,
+                     index / terms, index % terms, ctx->n, outputs, terms);
+  return fesc::hip_check(hipGetLastError(), "bank_pack");
+}
+
+int fesc_matvec_plan_create_bank(fesc_ctx* ctx, const fesc_matvec_desc* desc,
+                                 const uint64_t* bank, fesc_matvec_plan** plan) {
+  if (!ctx) return fesc::fail(FESC_ERR_ARG, "null context");
+  if (!bank) return fesc::fail(FESC_ERR_ARG, "null bank");
+  return fesc::matvec_plan_create(ctx, desc, nullptr, bank, plan);
 }
 
 void fesc_matvec_plan_destroy(fesc_matvec_plan* plan) { fesc::matvec_plan_destroy(plan); }

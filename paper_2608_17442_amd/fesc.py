@@ -252,20 +252,50 @@ _lib.fesc_matvec_phase_ms.argtypes = [_vp] + [ctypes.POINTER(ctypes.c_float)] * 
 _lib.fesc_matvec_phase_ms.restype = ctypes.c_int
 
 
+_lib.fesc_matvec_bank_words.argtypes = [_vp, ctypes.POINTER(_MatvecDesc),
+                                        ctypes.POINTER(ctypes.c_size_t)]
+_lib.fesc_matvec_bank_words.restype = ctypes.c_int
+_lib.fesc_matvec_bank_pack.argtypes = [_vp, ctypes.POINTER(_MatvecDesc), _vp, _u32, _vp, _vp]
+_lib.fesc_matvec_bank_pack.restype = ctypes.c_int
+_lib.fesc_matvec_plan_create_bank.argtypes = [_vp, ctypes.POINTER(_MatvecDesc), _vp,
+                                              ctypes.POINTER(_vp)]
+_lib.fesc_matvec_plan_create_bank.restype = ctypes.c_int
+
+
+def matvec_desc(level, n_in, n_out, n1, n2, unit, real_extract, rescale) -> _MatvecDesc:
+    return _MatvecDesc(level, n_in, n_out, n1, n2, unit, int(real_extract), int(rescale))
+
+
+def matvec_bank_words(ctx: Context, desc: _MatvecDesc) -> int:
+    w = ctypes.c_size_t()
+    _check(_lib.fesc_matvec_bank_words(ctx._h, ctypes.byref(desc), ctypes.byref(w)))
+    return int(w.value)
+
+
+def matvec_bank_pack(ctx: Context, desc: _MatvecDesc, bank, index: int, pt, stream=None):
+    _check(_lib.fesc_matvec_bank_pack(ctx._h, ctypes.byref(desc), _ptr(bank), index, _ptr(pt),
+                                      _stream(stream)))
+
+
 class MatvecPlan:
-    """BSGS projection plan over pre-encoded diagonals ``diags[b][p][u][q]``
-    (a flat list in that order of device plaintexts, kept alive here)."""
+    """BSGS projection plan over pre-encoded diagonals: either ``diags``, a
+    flat list of device plaintexts in [b][p][u][q] order, or ``bank``, one
+    tiled device buffer (see fesc_matvec_bank_pack).  Inputs are kept alive."""
 
     def __init__(self, ctx: Context, level, n_in, n_out, n1, n2, unit, real_extract, rescale,
-                 diags):
+                 diags=None, bank=None):
         self.ctx = ctx
-        self.desc = _MatvecDesc(level, n_in, n_out, n1, n2, unit, int(real_extract),
-                                int(rescale))
-        self._diags = list(diags)
-        arr = (_vp * len(self._diags))(*[_ptr(t) for t in self._diags])
+        self.desc = matvec_desc(level, n_in, n_out, n1, n2, unit, real_extract, rescale)
         h = _vp()
-        _check(_lib.fesc_matvec_plan_create(ctx._h, ctypes.byref(self.desc), arr,
-                                            ctypes.byref(h)))
+        if bank is not None:
+            self._bank = bank
+            _check(_lib.fesc_matvec_plan_create_bank(ctx._h, ctypes.byref(self.desc), _ptr(bank),
+                                                     ctypes.byref(h)))
+        else:
+            self._diags = list(diags)
+            arr = (_vp * len(self._diags))(*[_ptr(t) for t in self._diags])
+            _check(_lib.fesc_matvec_plan_create(ctx._h, ctypes.byref(self.desc), arr,
+                                                ctypes.byref(h)))
         self._h = h
 
     def __call__(self, ins, outs, stream=None):

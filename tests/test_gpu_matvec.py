@@ -42,13 +42,25 @@ def _run(P, S, desc, X_slots, scale_x, diag_slots, scale_d, seed_tag):
                     diag_pt[(b, p, u, q)] = pt
                     flat.append(to_dev(pt))
     step(f"matvec plan n_in={desc.n_in} n_out={desc.n_out} n1={desc.n1} n2={desc.n2}")
-    plan = F.MatvecPlan(S.ctx, desc.level, desc.n_in, desc.n_out, desc.n1, desc.n2, desc.unit,
-                        desc.real_extract, desc.rescale, flat)
+    args = (desc.level, desc.n_in, desc.n_out, desc.n1, desc.n2, desc.unit, desc.real_extract,
+            desc.rescale)
+    plan = F.MatvecPlan(S.ctx, *args, diags=flat)
     out_level = level - 1 if desc.rescale else level
     outs_d = [torch.zeros(out_level * 2 * P.n, dtype=torch.int64, device="cuda")
               for _ in range(desc.n_out)]
     step("matvec run")
     plan(ins_d, outs_d)
+    # the same diagonals through a tiled bank give the same residues
+    fd = F.matvec_desc(*args)
+    bank = torch.zeros(F.matvec_bank_words(S.ctx, fd), dtype=torch.int64, device="cuda")
+    for t, pt in enumerate(flat):
+        F.matvec_bank_pack(S.ctx, fd, bank, t, pt)
+    plan_b = F.MatvecPlan(S.ctx, *args, bank=bank)
+    outs_b = [torch.zeros_like(o) for o in outs_d]
+    step("matvec run (bank)")
+    plan_b(ins_d, outs_b)
+    for ob, od in zip(outs_b, outs_d):
+        assert torch.equal(ob, od)
     outs_o = OW.bsgs_matvec(P, desc, ins_o, lambda b, p, u, q: diag_pt[(b, p, u, q)], S.keys)
     assert keys_needed <= {r for r in range(P.n // 2)}
     return outs_o, outs_d
