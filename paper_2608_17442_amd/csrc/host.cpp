@@ -167,6 +167,7 @@ int create(const fesc_params* p, fesc_ctx** out) {
   const uint32_t dnum = (p->num_q + p->num_p - 1) / p->num_p;
   if (p->dnum != dnum)
     return fail(FESC_ERR_ARG, "dnum must equal ceil(num_q / num_p) = " + std::to_string(dnum));
+  if (dnum > 16) return fail(FESC_ERR_ARG, "at most 16 digits (dnum <= 16)");
   const uint64_t two_n = 2ull << p->log_n;
   std::vector<uint64_t> primes(p->q, p->q + p->num_q);
   primes.insert(primes.end(), p->p, p->p + p->num_p);
