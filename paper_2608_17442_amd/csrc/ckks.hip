@@ -19,14 +19,6 @@ __device__ __forceinline__ void st(uint64_t* p, double v, double q, double qinv)
   *p = d2u(red_full(v, q, qinv));
 }
 
-// index of the evaluation point whose g-th power is the point of index jp:
-// sigma_g(a)[jp] = a[galois_src(jp)]  (g odd, < 2N)
-__device__ __forceinline__ uint32_t galois_src(uint32_t jp, uint32_t g, uint32_t log_n) {
-  const uint32_t b = __builtin_bitreverse32(jp) >> (32 - log_n);
-  const uint32_t e = (g * (2u * b + 1u)) & ((2u << log_n) - 1u);  // wraps mod 2^32 first
-  return __builtin_bitreverse32((e - 1u) >> 1) >> (32 - log_n);
-}
-
 // ---------------------------------------------------------------- binary
 
 // op 0: a + b, op 1: a - b, op 2: a * b (all rows), prime of row r = r >> shift

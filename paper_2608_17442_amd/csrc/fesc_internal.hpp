@@ -66,6 +66,15 @@ __device__ __forceinline__ double center(double x, double q) {
   return x > 0.5 * q ? x - q : x;
 }
 
+// Galois automorphism X -> X^g (g odd, < 2N) in evaluation form: the value at
+// index jp of sigma_g(a) is a[galois_src(jp)], the index whose evaluation
+// point psi^(2 brv(j) + 1) is the g-th power of jp's point.
+__device__ __forceinline__ uint32_t galois_src(uint32_t jp, uint32_t g, uint32_t log_n) {
+  const uint32_t b = __builtin_bitreverse32(jp) >> (32 - log_n);
+  const uint32_t e = (g * (2u * b + 1u)) & ((2u << log_n) - 1u);  // wraps mod 2^32 first
+  return __builtin_bitreverse32((e - 1u) >> 1) >> (32 - log_n);
+}
+
 __device__ __forceinline__ double u2d(uint64_t x) {
   return __builtin_fma((double)(uint32_t)(x >> 32), 4294967296.0, (double)(uint32_t)x);
 }
@@ -105,6 +114,10 @@ struct Context {
   PrimeK* d_pk = nullptr;         // [L+alpha]
   double2* d_tw_fwd = nullptr;    // [L+alpha][N] {psi^brv(i), /q}
   double2* d_tw_inv = nullptr;    // [L+alpha][N] {psi^-brv(i), /q}
+  // the powers used by the radix-16 step on index bits 3..0 of the 4096-point
+  // inner NTT blocks, re-ordered [L+alpha][N/4096][15][256] (see ntt.hip)
+  double* d_tw3_fwd = nullptr;
+  double* d_tw3_inv = nullptr;
   // keys: Galois element (0 = relinearisation) -> device [dnum][L+alpha][2][N]
   std::map<uint32_t, uint64_t*> keys;
   // basis-conversion / rescale constants, built on first use per level

@@ -112,6 +112,8 @@ static int build_tables(Context* c) {
   const uint32_t n = c->n, np = (uint32_t)c->ext_count();
   std::vector<PrimeK> pk(np);
   std::vector<double2> fwd((size_t)np * n), inv((size_t)np * n);
+  const uint32_t nblk = n / 4096;
+  std::vector<double> fwd3((size_t)np * nblk * 15 * 256), inv3(fwd3.size());
   std::vector<uint64_t> pw(n);
   for (uint32_t i = 0; i < np; ++i) {
     const uint64_t q = c->primes[i];
@@ -127,18 +129,35 @@ static int build_tables(Context* c) {
         const double w = (double)pw[bitrev(k, c->log_n)];
         t[k] = double2{w, w / qd};
       }
+      // Block blk, slot k (register distance H, group gi), thread e: the
+      // twiddle psi_rev[(N + 4096 blk) / 2H + e * 8/H + gi].
+      double* t3 = (dir == 0 ? fwd3.data() : inv3.data()) + (size_t)i * nblk * 15 * 256;
+      for (uint32_t blk = 0; blk < nblk; ++blk)
+        for (uint32_t k = 0; k < 15; ++k) {
+          const uint32_t lh = k == 0 ? 3 : k < 3 ? 2 : k < 7 ? 1 : 0;
+          const uint32_t gi = k - ((1u << (3 - lh)) - 1);
+          const uint32_t base = (n + 4096 * blk) >> (lh + 1);
+          for (uint32_t e = 0; e < 256; ++e)
+            t3[((size_t)blk * 15 + k) * 256 + e] = t[base + e * (8u >> lh) + gi].x;
+        }
     }
   }
   int rc;
   if ((rc = hip_check(hipMalloc(&c->d_pk, sizeof(PrimeK) * np), "hipMalloc")) ||
       (rc = hip_check(hipMalloc(&c->d_tw_fwd, sizeof(double2) * fwd.size()), "hipMalloc")) ||
-      (rc = hip_check(hipMalloc(&c->d_tw_inv, sizeof(double2) * inv.size()), "hipMalloc")))
+      (rc = hip_check(hipMalloc(&c->d_tw_inv, sizeof(double2) * inv.size()), "hipMalloc")) ||
+      (rc = hip_check(hipMalloc(&c->d_tw3_fwd, sizeof(double) * fwd3.size()), "hipMalloc")) ||
+      (rc = hip_check(hipMalloc(&c->d_tw3_inv, sizeof(double) * inv3.size()), "hipMalloc")))
     return rc == FESC_ERR_HIP ? fail(FESC_ERR_OOM, "table allocation failed") : rc;
   if ((rc = hip_check(hipMemcpy(c->d_pk, pk.data(), sizeof(PrimeK) * np, hipMemcpyHostToDevice),
                       "hipMemcpy")) ||
       (rc = hip_check(hipMemcpy(c->d_tw_fwd, fwd.data(), sizeof(double2) * fwd.size(),
                                 hipMemcpyHostToDevice), "hipMemcpy")) ||
       (rc = hip_check(hipMemcpy(c->d_tw_inv, inv.data(), sizeof(double2) * inv.size(),
+                                hipMemcpyHostToDevice), "hipMemcpy")) ||
+      (rc = hip_check(hipMemcpy(c->d_tw3_fwd, fwd3.data(), sizeof(double) * fwd3.size(),
+                                hipMemcpyHostToDevice), "hipMemcpy")) ||
+      (rc = hip_check(hipMemcpy(c->d_tw3_inv, inv3.data(), sizeof(double) * inv3.size(),
                                 hipMemcpyHostToDevice), "hipMemcpy")))
     return rc;
   return FESC_OK;
@@ -152,6 +171,8 @@ void destroy(Context* c) {
   hipFree(c->d_pk);
   hipFree(c->d_tw_fwd);
   hipFree(c->d_tw_inv);
+  hipFree(c->d_tw3_fwd);
+  hipFree(c->d_tw3_inv);
   hipFree(c->scratch);
   delete static_cast<fesc_ctx*>(c);
 }

@@ -43,12 +43,6 @@ __device__ __forceinline__ uint32_t ext_prime(uint32_t row, uint32_t level, uint
   return row < level ? row : L + (row - level);
 }
 
-__device__ __forceinline__ uint32_t galois_src(uint32_t jp, uint32_t g, uint32_t log_n) {
-  const uint32_t b = __builtin_bitreverse32(jp) >> (32 - log_n);
-  const uint32_t e = (g * (2u * b + 1u)) & ((2u << log_n) - 1u);
-  return __builtin_bitreverse32((e - 1u) >> 1) >> (32 - log_n);
-}
-
 // centred [v * f]_q of a canonical residue pair
 __device__ __forceinline__ void centred_digit(const ulonglong2 v, const double2 f, const PrimeK& P,
                                               double& y0, double& y1) {

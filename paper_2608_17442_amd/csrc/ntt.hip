@@ -7,94 +7,99 @@
 // twiddle psi^brv((N + j) / 2t); the inverse is the Gentleman-Sande network
 // with psi^-1 and a final scaling by N^-1.
 //
-// gfx950 mapping.  N = N1 * 256 with N1 = 2^(log N - 8) in [16, 256].  Two
-// passes, each over independent sub-transforms held entirely on chip:
-//   outer pass: the first log N1 stages couple only indices that agree mod
-//               256, i.e. N1-point "columns" at stride 256;
-//   inner pass: the last 8 stages couple only indices inside a contiguous
-//               256-element block.
-// Every sub-transform is split over 16-value register tiles: a thread runs
-// four radix-2 stages on its 16 values (a radix-16 step), the tiles are
-// transposed through LDS, and the thread runs the remaining stages.  Between
-// the passes the row holds the signed fp64 intermediate in place of the
-// uint64 residues (same 8 bytes per value), so no conversion or full
-// reduction is spent on it.
+// gfx950 mapping.  N = M * 4096 with M = 2^(log N - 12) in [1, 16].  At most
+// two passes over HBM, each over independent sub-transforms held on chip:
+//   outer pass (M > 1): the first log M stages couple only indices that agree
+//               mod 4096, i.e. M-point "columns" at stride 4096.  A thread
+//               keeps whole columns in registers; a wavefront reads and writes
+//               64 adjacent columns, so every access is a contiguous 512-byte
+//               run (2 KB per workgroup) and no LDS is needed.  The twiddles of
+//               these stages do not depend on the column (M - 1 values).
+//   inner pass: the last 12 stages couple only indices inside a contiguous
+//               4096-element block, one block per 256-thread workgroup.  The
+//               block is processed as three radix-16 register steps on index
+//               bits 11..8, 7..4 and 3..0, with LDS transposes in between, so
+//               loads and stores of the forward pass are fully coalesced.
+// Between the passes the row holds the signed fp64 intermediate in place of
+// the uint64 residues (same 8 bytes per value), so no conversion or full
+// reduction is spent on it.  For N = 4096 the inner pass alone is the whole
+// transform.
+//
+// Twiddles: stages on bits 11..4 read the bit-reversed power table (few
+// distinct values per wavefront); stages on bits 3..0 read a per-block
+// re-ordering of the same powers (Context::d_tw3_*), laid out so that these
+// loads are coalesced too.
 #include "fesc_internal.hpp"
+#include "ops.hpp"
 
 namespace fesc {
 
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kPadRow = 17;  // LDS: one pad word per 16 values
+constexpr uint32_t kBlock = 4096;
 
+// LDS index with one pad word per 16 values
 __device__ __forceinline__ uint32_t pad16(uint32_t k) { return k + (k >> 4); }
+constexpr int kLds = kBlock + kBlock / 16;
 
-template <int H>
-struct Log2H { static constexpr int v = H == 8 ? 3 : H == 4 ? 2 : H == 2 ? 1 : 0; };
-
-// One forward stage on the 16-value tile x: pairs (r, r + H), r & H == 0.
-// Value r sits at global index jb + (r << js_log).
-template <int H>
-__device__ __forceinline__ void ct_stage(double (&x)[16], const double2* __restrict__ tw,
-                                         uint32_t n, uint32_t jb, uint32_t js_log, double q,
-                                         double qinv) {
-  const uint32_t sh = Log2H<H>::v + js_log + 1;
+// Radix-2 stages on a 16-value register tile, pairs (r, r + H) with r & H == 0.
+// tw(gi) gives the twiddle {w, w/q} of group gi = r / 2H.
+template <int H, class TW>
+__device__ __forceinline__ void ct_st(double (&x)[16], TW tw, double q, double qinv) {
 #pragma unroll
   for (int g = 0; g < 16; g += 2 * H) {
-    const double2 w = tw[(n + jb + ((uint32_t)g << js_log)) >> sh];
+    const double2 w = tw(g / (2 * H));
 #pragma unroll
     for (int r = g; r < g + H; ++r) {
-      double u = red_bal(x[r], q, qinv);
-      double v = mm_shoup(x[r + H], w.x, w.y, q);
+      const double u = red_bal(x[r], q, qinv);
+      const double v = mm_shoup(x[r + H], w.x, w.y, q);
       x[r] = u + v;
       x[r + H] = u - v;
     }
   }
 }
 
-template <int H>
-__device__ __forceinline__ void gs_stage(double (&x)[16], const double2* __restrict__ tw,
-                                         uint32_t n, uint32_t jb, uint32_t js_log, double q,
-                                         double qinv) {
-  const uint32_t sh = Log2H<H>::v + js_log + 1;
+template <int H, class TW>
+__device__ __forceinline__ void gs_st(double (&x)[16], TW tw, double q, double qinv) {
 #pragma unroll
   for (int g = 0; g < 16; g += 2 * H) {
-    const double2 w = tw[(n + jb + ((uint32_t)g << js_log)) >> sh];
+    const double2 w = tw(g / (2 * H));
 #pragma unroll
     for (int r = g; r < g + H; ++r) {
-      double u = x[r], v = x[r + H];
+      const double u = x[r], v = x[r + H];
       x[r] = red_bal(u + v, q, qinv);
       x[r + H] = mm_shoup(u - v, w.x, w.y, q);
     }
   }
 }
 
-// Forward stages with register distances 2^(nst-1), ..., 1.
-template <int NST>
-__device__ __forceinline__ void ct_tail(double (&x)[16], const double2* tw, uint32_t n,
-                                        uint32_t jb, uint32_t js_log, double q, double qinv) {
-  if constexpr (NST >= 4) ct_stage<8>(x, tw, n, jb, js_log, q, qinv);
-  if constexpr (NST >= 3) ct_stage<4>(x, tw, n, jb, js_log, q, qinv);
-  if constexpr (NST >= 2) ct_stage<2>(x, tw, n, jb, js_log, q, qinv);
-  if constexpr (NST >= 1) ct_stage<1>(x, tw, n, jb, js_log, q, qinv);
-}
-
-// Inverse stages with register distances 1, ..., 2^(nst-1).
-template <int NST>
-__device__ __forceinline__ void gs_head(double (&x)[16], const double2* tw, uint32_t n,
-                                        uint32_t jb, uint32_t js_log, double q, double qinv) {
-  if constexpr (NST >= 1) gs_stage<1>(x, tw, n, jb, js_log, q, qinv);
-  if constexpr (NST >= 2) gs_stage<2>(x, tw, n, jb, js_log, q, qinv);
-  if constexpr (NST >= 3) gs_stage<4>(x, tw, n, jb, js_log, q, qinv);
-  if constexpr (NST >= 4) gs_stage<8>(x, tw, n, jb, js_log, q, qinv);
-}
+// Table reads of the twiddles.  For index bits 11..8 (register distance H,
+// distance 256 H) the group twiddle is psi_rev[(N + B) / 512H + gi]; for bits
+// 7..4 (distance 16 H) with a = bits 11..8 of the thread's values it is
+// psi_rev[(N + B) / 32H + a * 8/H + gi]; B is the block offset in the row.
+struct TwHi {
+  const double2* tw;
+  uint32_t base;
+  __device__ __forceinline__ double2 operator()(int gi) const { return tw[base + gi]; }
+};
+// Bits 3..0: re-ordered table s3[k][e] (k = H-group slot, e = thread).
+template <int H>
+struct TwLo {
+  const double* s3;
+  double qinv;
+  __device__ __forceinline__ double2 operator()(int gi) const {
+    constexpr int k0 = H == 8 ? 0 : H == 4 ? 1 : H == 2 ? 3 : 7;
+    const double w = s3[(k0 + gi) * kThreads];
+    return double2{w, w * qinv};
+  }
+};
 
 }  // namespace
 
 // Row selection of a batched transform launch.  blockIdx.y = batch index b,
 // blockIdx.z = limb index i (the batch varies fastest between workgroups, so
-// the twiddle table of one prime stays resident in L2 across the batch).
+// the twiddle tables of one prime stay resident in L2 across the batch).
 // Limb i < split uses prime prime0 + i, limb i >= split prime1 + (i - split).
 // If skip_alpha != 0, limbs [d*skip_alpha, min((d+1)*skip_alpha, skip_limit))
 // of batch element b, d = b mod skip_mod, are left untouched (the own-digit
@@ -115,203 +120,57 @@ __device__ __forceinline__ bool RowSel::skip() const {
 
 namespace {
 
-// ---------------------------------------------------------------- forward
+// ------------------------------------------------------------- outer pass
 
-// Outer pass, M = 2^LOGM point columns at stride 256.  TPS threads per column,
-// SPW columns per workgroup.  Reads uint64 residues, writes fp64.
+// M = 2^LOGM point columns at stride 4096; a thread holds C = 16/M columns,
+// c0 + 256 j (j < C), value m of column j in x[j*M + m].  Grid x = M.
+// Stage s (distance 4096 * M/2^(s+1)) uses psi_rev[2^s + m / 2^(LOGM-s)].
 template <int LOGM>
 __global__ __launch_bounds__(kThreads) void k_fwd_outer(RowSel rs, uint32_t log_n,
                                                         const PrimeK* __restrict__ pk,
                                                         const double2* __restrict__ twf) {
-  constexpr int TPS = (1 << LOGM) / 16;
-  constexpr int SPW = kThreads / TPS;
-  __shared__ double lds[SPW * TPS * 16 + SPW * TPS];
+  constexpr int M = 1 << LOGM, C = 16 / M;
   if (rs.skip()) return;
   const uint32_t n = 1u << log_n;
   const uint32_t prime = rs.prime();
   const double q = pk[prime].q, qinv = pk[prime].qinv;
   const double2* tw = twf + (size_t)prime * n;
   uint64_t* row = rs.row();
-  const uint32_t tid = threadIdx.x, sp = tid % SPW, k0 = tid / SPW;
-  const uint32_t c = blockIdx.x * SPW + sp;
+  const uint32_t c0 = blockIdx.x * (kThreads * C) + threadIdx.x;
   double x[16];
 #pragma unroll
-  for (int r = 0; r < 16; ++r) x[r] = u2d(row[c + 256u * (k0 + TPS * r)]);
-  // first four stages: value r is at global index c + 256 * (k0 + TPS * r)
-  ct_tail<4>(x, tw, n, c + 256u * k0, 8 + (LOGM - 4), q, qinv);
+  for (int j = 0; j < C; ++j)
+#pragma unroll
+    for (int m = 0; m < M; ++m) x[j * M + m] = u2d(row[c0 + kThreads * j + kBlock * m]);
+#pragma unroll
+  for (int s = 0; s < LOGM; ++s) {
+    const int H = M >> (s + 1);
+#pragma unroll
+    for (int m = 0; m < M; ++m) {
+      if (m & H) continue;
+      const double2 w = tw[(1 << s) + (m >> (LOGM - s))];
+#pragma unroll
+      for (int j = 0; j < C; ++j) {
+        const double u = red_bal(x[j * M + m], q, qinv);
+        const double v = mm_shoup(x[j * M + m + H], w.x, w.y, q);
+        x[j * M + m] = u + v;
+        x[j * M + m + H] = u - v;
+      }
+    }
+  }
   double* rowd = reinterpret_cast<double*>(row);
-  if constexpr (LOGM > 4) {
-    double* my = lds + sp * (TPS * kPadRow);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) my[pad16(k0 + TPS * r)] = x[r];
-    __syncthreads();
+  for (int j = 0; j < C; ++j)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) x[r] = my[pad16(16 * k0 + r)];
-    ct_tail<LOGM - 4>(x, tw, n, c + 256u * 16u * k0, 8, q, qinv);
-#pragma unroll
-    for (int r = 0; r < 16; ++r) rowd[c + 256u * (16 * k0 + r)] = x[r];
-  } else {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) rowd[c + 256u * r] = x[r];
-  }
+    for (int m = 0; m < M; ++m) rowd[c0 + kThreads * j + kBlock * m] = x[j * M + m];
 }
 
-// Inner-pass twiddles.  For half-distance t = 2^lt inside block `blk` the
-// butterfly group r (< 128/t) uses psi_rev[N/2t + blk*128/t + r]; the two
-// parts of that index have disjoint bits, so the twiddle factors as
-//     F_lt * psi_rev[r],   F_lt = psi_rev[N/2t + blk*128/t],
-// i.e. eight per-block values and the first 128 table entries (kept in LDS).
-// Each twiddle costs one modular product instead of a global load.
-__device__ __forceinline__ double2 tw_prod(double F, const double2* small, uint32_t r, double q,
-                                           double qinv) {
-  const double2 c = small[r];
-  const double w = mm_shoup(F, c.x, c.y, q);  // |w| < q
-  return double2{w, w * qinv};
-}
-
-// Forward stage with register distance H on a tile whose group g has twiddle
-// index r = rbase + g / 2H.
-template <int H, bool RB0>
-__device__ __forceinline__ void ct_stage_f(double (&x)[16], double F, const double2* small,
-                                           uint32_t rbase, double q, double qinv) {
-#pragma unroll
-  for (int g = 0; g < 16; g += 2 * H) {
-    const double2 w = (RB0 && g == 0) ? double2{F, F * qinv}
-                                      : tw_prod(F, small, rbase + g / (2 * H), q, qinv);
-#pragma unroll
-    for (int r = g; r < g + H; ++r) {
-      double u = red_bal(x[r], q, qinv);
-      double v = mm_shoup(x[r + H], w.x, w.y, q);
-      x[r] = u + v;
-      x[r + H] = u - v;
-    }
-  }
-}
-
-template <int H, bool RB0>
-__device__ __forceinline__ void gs_stage_f(double (&x)[16], double F, const double2* small,
-                                           uint32_t rbase, double q, double qinv) {
-#pragma unroll
-  for (int g = 0; g < 16; g += 2 * H) {
-    const double2 w = (RB0 && g == 0) ? double2{F, F * qinv}
-                                      : tw_prod(F, small, rbase + g / (2 * H), q, qinv);
-#pragma unroll
-    for (int r = g; r < g + H; ++r) {
-      double u = x[r], v = x[r + H];
-      x[r] = red_bal(u + v, q, qinv);
-      x[r + H] = mm_shoup(u - v, w.x, w.y, q);
-    }
-  }
-}
-
-// Inner pass: 256-point blocks, 16 threads per block, 16 blocks per workgroup.
-// Reads fp64 (outer-pass output), writes canonical uint64 residues.
-__global__ __launch_bounds__(kThreads) void k_fwd_inner(RowSel rs, uint32_t log_n,
-                                                        const PrimeK* __restrict__ pk,
-                                                        const double2* __restrict__ twf) {
-  __shared__ double lds[16 * 16 * kPadRow];
-  __shared__ double2 small[128];
-  if (rs.skip()) return;
-  const uint32_t n = 1u << log_n;
-  const uint32_t prime = rs.prime();
-  const double q = pk[prime].q, qinv = pk[prime].qinv;
-  const double2* tw = twf + (size_t)prime * n;
-  uint64_t* row = rs.row();
-  const uint32_t tid = threadIdx.x, sp = tid >> 4, s0 = tid & 15;
-  const uint32_t base = (blockIdx.x * 16 + sp) * 256;
-  if (tid < 128) small[tid] = tw[tid];
-  double F[8];
-#pragma unroll
-  for (int lt = 0; lt < 8; ++lt) F[lt] = tw[(n + base) >> (lt + 1)].x;
-  const double* src = reinterpret_cast<const double*>(row) + base;
-  double x[16];
-#pragma unroll
-  for (int r = 0; r < 16; ++r) x[r] = src[s0 + 16 * r];
-  __syncthreads();
-  // t = 128, 64, 32, 16: value r at s0 + 16r, group index g / 2H
-  ct_stage_f<8, true>(x, F[7], small, 0, q, qinv);
-  ct_stage_f<4, true>(x, F[6], small, 0, q, qinv);
-  ct_stage_f<2, true>(x, F[5], small, 0, q, qinv);
-  ct_stage_f<1, true>(x, F[4], small, 0, q, qinv);
-  double* my = lds + sp * (16 * kPadRow);
-#pragma unroll
-  for (int r = 0; r < 16; ++r) my[pad16(s0 + 16 * r)] = x[r];
-  __syncthreads();
-#pragma unroll
-  for (int r = 0; r < 16; ++r) x[r] = my[pad16(16 * s0 + r)];
-  // t = 8, 4, 2, 1: value r at 16 s0 + r, group index 8 s0 / H + g / 2H
-  ct_stage_f<8, false>(x, F[3], small, s0, q, qinv);
-  ct_stage_f<4, false>(x, F[2], small, 2 * s0, q, qinv);
-  ct_stage_f<2, false>(x, F[1], small, 4 * s0, q, qinv);
-  ct_stage_f<1, false>(x, F[0], small, 8 * s0, q, qinv);
-  ulonglong2* dst = reinterpret_cast<ulonglong2*>(row + base + 16 * s0);
-#pragma unroll
-  for (int r = 0; r < 16; r += 2) {
-    ulonglong2 v;
-    v.x = d2u(red_full(x[r], q, qinv));
-    v.y = d2u(red_full(x[r + 1], q, qinv));
-    dst[r / 2] = v;
-  }
-}
-
-// ---------------------------------------------------------------- inverse
-
-// Inner pass first: reads uint64 residues, writes fp64.
-__global__ __launch_bounds__(kThreads) void k_inv_inner(RowSel rs, uint32_t log_n,
-                                                        const PrimeK* __restrict__ pk,
-                                                        const double2* __restrict__ twi) {
-  __shared__ double lds[16 * 16 * kPadRow];
-  __shared__ double2 small[128];
-  if (rs.skip()) return;
-  const uint32_t n = 1u << log_n;
-  const uint32_t prime = rs.prime();
-  const double q = pk[prime].q, qinv = pk[prime].qinv;
-  const double2* tw = twi + (size_t)prime * n;
-  uint64_t* row = rs.row();
-  const uint32_t tid = threadIdx.x, sp = tid >> 4, s0 = tid & 15;
-  const uint32_t base = (blockIdx.x * 16 + sp) * 256;
-  if (tid < 128) small[tid] = tw[tid];
-  double F[8];
-#pragma unroll
-  for (int lt = 0; lt < 8; ++lt) F[lt] = tw[(n + base) >> (lt + 1)].x;
-  const ulonglong2* src = reinterpret_cast<const ulonglong2*>(row + base + 16 * s0);
-  double x[16];
-#pragma unroll
-  for (int r = 0; r < 16; r += 2) {
-    ulonglong2 v = src[r / 2];
-    x[r] = u2d(v.x);
-    x[r + 1] = u2d(v.y);
-  }
-  __syncthreads();
-  // t = 1, 2, 4, 8 on 16 consecutive values
-  gs_stage_f<1, false>(x, F[0], small, 8 * s0, q, qinv);
-  gs_stage_f<2, false>(x, F[1], small, 4 * s0, q, qinv);
-  gs_stage_f<4, false>(x, F[2], small, 2 * s0, q, qinv);
-  gs_stage_f<8, false>(x, F[3], small, s0, q, qinv);
-  double* my = lds + sp * (16 * kPadRow);
-#pragma unroll
-  for (int r = 0; r < 16; ++r) my[pad16(16 * s0 + r)] = x[r];
-  __syncthreads();
-#pragma unroll
-  for (int r = 0; r < 16; ++r) x[r] = my[pad16(s0 + 16 * r)];
-  // t = 16, 32, 64, 128 on values s0 + 16 r
-  gs_stage_f<1, true>(x, F[4], small, 0, q, qinv);
-  gs_stage_f<2, true>(x, F[5], small, 0, q, qinv);
-  gs_stage_f<4, true>(x, F[6], small, 0, q, qinv);
-  gs_stage_f<8, true>(x, F[7], small, 0, q, qinv);
-  double* dst = reinterpret_cast<double*>(row) + base;
-#pragma unroll
-  for (int r = 0; r < 16; ++r) dst[s0 + 16 * r] = x[r];
-}
-
-// Outer pass last: reads fp64, scales by N^-1, writes canonical uint64.
+// Inverse: stages in reverse order, then N^-1 and canonical uint64 residues.
 template <int LOGM>
 __global__ __launch_bounds__(kThreads) void k_inv_outer(RowSel rs, uint32_t log_n,
                                                         const PrimeK* __restrict__ pk,
                                                         const double2* __restrict__ twi) {
-  constexpr int TPS = (1 << LOGM) / 16;
-  constexpr int SPW = kThreads / TPS;
-  __shared__ double lds[SPW * TPS * 16 + SPW * TPS];
+  constexpr int M = 1 << LOGM, C = 16 / M;
   if (rs.skip()) return;
   const uint32_t n = 1u << log_n;
   const uint32_t prime = rs.prime();
@@ -319,61 +178,294 @@ __global__ __launch_bounds__(kThreads) void k_inv_outer(RowSel rs, uint32_t log_
   const double2* tw = twi + (size_t)prime * n;
   uint64_t* row = rs.row();
   const double* rowd = reinterpret_cast<const double*>(row);
-  const uint32_t tid = threadIdx.x, sp = tid % SPW, k0 = tid / SPW;
-  const uint32_t c = blockIdx.x * SPW + sp;
+  const uint32_t c0 = blockIdx.x * (kThreads * C) + threadIdx.x;
   double x[16];
-  if constexpr (LOGM > 4) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) x[r] = rowd[c + 256u * (16 * k0 + r)];
-    gs_head<LOGM - 4>(x, tw, n, c + 256u * 16u * k0, 8, P.q, P.qinv);
-    double* my = lds + sp * (TPS * kPadRow);
+  for (int j = 0; j < C; ++j)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) my[pad16(16 * k0 + r)] = x[r];
-    __syncthreads();
+    for (int m = 0; m < M; ++m) x[j * M + m] = rowd[c0 + kThreads * j + kBlock * m];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) x[r] = my[pad16(k0 + TPS * r)];
-  } else {
+  for (int s = LOGM - 1; s >= 0; --s) {
+    const int H = M >> (s + 1);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) x[r] = rowd[c + 256u * r];
+    for (int m = 0; m < M; ++m) {
+      if (m & H) continue;
+      const double2 w = tw[(1 << s) + (m >> (LOGM - s))];
+#pragma unroll
+      for (int j = 0; j < C; ++j) {
+        const double u = x[j * M + m], v = x[j * M + m + H];
+        x[j * M + m] = red_bal(u + v, P.q, P.qinv);
+        x[j * M + m + H] = mm_shoup(u - v, w.x, w.y, P.q);
+      }
+    }
   }
-  gs_head<4>(x, tw, n, c + 256u * k0, 8 + (LOGM - 4), P.q, P.qinv);
 #pragma unroll
-  for (int r = 0; r < 16; ++r)
-    row[c + 256u * (k0 + TPS * r)] =
-        d2u(red_full(mm_shoup(x[r], P.ninv, P.ninvp, P.q), P.q, P.qinv));
+  for (int j = 0; j < C; ++j)
+#pragma unroll
+    for (int m = 0; m < M; ++m)
+      row[c0 + kThreads * j + kBlock * m] =
+          d2u(red_full(mm_shoup(x[j * M + m], P.ninv, P.ninvp, P.q), P.q, P.qinv));
 }
 
-template <int LOGM>
-void launch_outer(bool inverse, dim3 grid, hipStream_t s, RowSel rs, uint32_t log_n,
-                  const PrimeK* pk, const double2* tw) {
-  grid.x = (1u << LOGM) / 16;  // 256 / SPW
-  if (inverse)
-    hipLaunchKernelGGL(k_inv_outer<LOGM>, grid, dim3(kThreads), 0, s, rs, log_n, pk, tw);
-  else
-    hipLaunchKernelGGL(k_fwd_outer<LOGM>, grid, dim3(kThreads), 0, s, rs, log_n, pk, tw);
+// ------------------------------------------------------------- inner pass
+
+// Forward 4096-point blocks.  Thread t starts with values t + 256 r (bits
+// 11..8 in registers), moves to a*256 + 16 r + b (a = t/16, b = t%16; bits
+// 7..4) and to 16 t + r (bits 3..0), and is handed back values t + 256 r for
+// the epilogue.  Each transpose writes exactly the LDS words the thread read
+// in the previous one, so only the reads need a barrier.
+//
+// SINGLE: N = 4096, the pass reads uint64 residues; otherwise it reads the
+// outer pass's fp64 intermediate.
+template <bool SINGLE, class Epi>
+__global__ __launch_bounds__(kThreads) void k_fwd_inner(RowSel rs, uint32_t log_n,
+                                                        const PrimeK* __restrict__ pk,
+                                                        const double2* __restrict__ twf,
+                                                        const double* __restrict__ tw3, Epi epi) {
+  __shared__ double lds[kLds];
+  if (rs.skip()) return;
+  const uint32_t n = 1u << log_n;
+  const uint32_t prime = rs.prime();
+  const double q = pk[prime].q, qinv = pk[prime].qinv;
+  const double2* tw = twf + (size_t)prime * n;
+  uint64_t* row = rs.row();
+  const uint32_t t = threadIdx.x, a = t >> 4, b = t & 15;
+  const uint32_t B = blockIdx.x * kBlock, nb = n + B;
+  double x[16];
+  if constexpr (SINGLE) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) x[r] = u2d(row[B + t + 256 * r]);
+  } else {
+    const double* src = reinterpret_cast<const double*>(row) + B + t;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) x[r] = src[256 * r];
+  }
+  // bits 11..8
+  ct_st<8>(x, TwHi{tw, nb >> 12}, q, qinv);
+  ct_st<4>(x, TwHi{tw, nb >> 11}, q, qinv);
+  ct_st<2>(x, TwHi{tw, nb >> 10}, q, qinv);
+  ct_st<1>(x, TwHi{tw, nb >> 9}, q, qinv);
+#pragma unroll
+  for (int r = 0; r < 16; ++r) lds[pad16(t + 256 * r)] = x[r];
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < 16; ++r) x[r] = lds[pad16(256 * a + 16 * r + b)];
+  // bits 7..4
+  ct_st<8>(x, TwHi{tw, (nb >> 8) + a}, q, qinv);
+  ct_st<4>(x, TwHi{tw, (nb >> 7) + 2 * a}, q, qinv);
+  ct_st<2>(x, TwHi{tw, (nb >> 6) + 4 * a}, q, qinv);
+  ct_st<1>(x, TwHi{tw, (nb >> 5) + 8 * a}, q, qinv);
+#pragma unroll
+  for (int r = 0; r < 16; ++r) lds[pad16(256 * a + 16 * r + b)] = x[r];
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < 16; ++r) x[r] = lds[pad16(16 * t + r)];
+  // bits 3..0
+  const double* s3 = tw3 + ((size_t)prime * (n / kBlock) + blockIdx.x) * (15 * kThreads) + t;
+  ct_st<8>(x, TwLo<8>{s3, qinv}, q, qinv);
+  ct_st<4>(x, TwLo<4>{s3, qinv}, q, qinv);
+  ct_st<2>(x, TwLo<2>{s3, qinv}, q, qinv);
+  ct_st<1>(x, TwLo<1>{s3, qinv}, q, qinv);
+#pragma unroll
+  for (int r = 0; r < 16; ++r) lds[pad16(16 * t + r)] = x[r];
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < 16; ++r) x[r] = lds[pad16(t + 256 * r)];
+  epi(row, B + t, x, q, qinv, n);
+}
+
+// Epilogue of the forward transform: canonical residues, value r at k0 + 256 r.
+struct StoreResidues {
+  __device__ __forceinline__ void operator()(uint64_t* row, uint32_t k0, const double (&x)[16],
+                                             double q, double qinv, uint32_t) const {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) row[k0 + 256 * r] = d2u(red_full(x[r], q, qinv));
+  }
+};
+
+// Source of the inverse inner pass: the row itself (in place).
+struct LoadRow {
+  __device__ __forceinline__ const uint64_t* operator()(uint64_t* row) const { return row; }
+};
+
+// Source of the inverse inner pass: row blockIdx.z of source blockIdx.y of a
+// key-switch table (out of place; the row receives the result).
+struct LoadSources {
+  KsTable tab;
+  __device__ __forceinline__ const uint64_t* operator()(uint64_t*) const {
+    return tab.src_in[blockIdx.y] + (size_t)blockIdx.z * tab.src_stride[blockIdx.y];
+  }
+};
+
+// Inverse 4096-point blocks: the mirror image of k_fwd_inner.  Reads uint64
+// residues (16 consecutive values per thread), writes fp64 for the outer pass
+// or, if SINGLE, the scaled canonical residues.
+template <bool SINGLE, class Ld>
+__global__ __launch_bounds__(kThreads) void k_inv_inner(RowSel rs, uint32_t log_n,
+                                                        const PrimeK* __restrict__ pk,
+                                                        const double2* __restrict__ twi,
+                                                        const double* __restrict__ tw3, Ld ld) {
+  __shared__ double lds[kLds];
+  if (rs.skip()) return;
+  const uint32_t n = 1u << log_n;
+  const uint32_t prime = rs.prime();
+  const PrimeK P = pk[prime];
+  const double q = P.q, qinv = P.qinv;
+  const double2* tw = twi + (size_t)prime * n;
+  uint64_t* row = rs.row();
+  const uint32_t t = threadIdx.x, a = t >> 4, b = t & 15;
+  const uint32_t B = blockIdx.x * kBlock, nb = n + B;
+  const ulonglong2* src = reinterpret_cast<const ulonglong2*>(ld(row) + B + 16 * t);
+  double x[16];
+#pragma unroll
+  for (int r = 0; r < 16; r += 2) {
+    const ulonglong2 v = src[r / 2];
+    x[r] = u2d(v.x);
+    x[r + 1] = u2d(v.y);
+  }
+  // bits 3..0
+  const double* s3 = tw3 + ((size_t)prime * (n / kBlock) + blockIdx.x) * (15 * kThreads) + t;
+  gs_st<1>(x, TwLo<1>{s3, qinv}, q, qinv);
+  gs_st<2>(x, TwLo<2>{s3, qinv}, q, qinv);
+  gs_st<4>(x, TwLo<4>{s3, qinv}, q, qinv);
+  gs_st<8>(x, TwLo<8>{s3, qinv}, q, qinv);
+#pragma unroll
+  for (int r = 0; r < 16; ++r) lds[pad16(16 * t + r)] = x[r];
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < 16; ++r) x[r] = lds[pad16(256 * a + 16 * r + b)];
+  // bits 7..4
+  gs_st<1>(x, TwHi{tw, (nb >> 5) + 8 * a}, q, qinv);
+  gs_st<2>(x, TwHi{tw, (nb >> 6) + 4 * a}, q, qinv);
+  gs_st<4>(x, TwHi{tw, (nb >> 7) + 2 * a}, q, qinv);
+  gs_st<8>(x, TwHi{tw, (nb >> 8) + a}, q, qinv);
+#pragma unroll
+  for (int r = 0; r < 16; ++r) lds[pad16(256 * a + 16 * r + b)] = x[r];
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < 16; ++r) x[r] = lds[pad16(t + 256 * r)];
+  // bits 11..8
+  gs_st<1>(x, TwHi{tw, nb >> 9}, q, qinv);
+  gs_st<2>(x, TwHi{tw, nb >> 10}, q, qinv);
+  gs_st<4>(x, TwHi{tw, nb >> 11}, q, qinv);
+  gs_st<8>(x, TwHi{tw, nb >> 12}, q, qinv);
+  if constexpr (SINGLE) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      row[B + t + 256 * r] = d2u(red_full(mm_shoup(x[r], P.ninv, P.ninvp, q), q, qinv));
+  } else {
+    double* dst = reinterpret_cast<double*>(row) + B + t;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) dst[256 * r] = x[r];
+  }
 }
 
 }  // namespace
 
-// Both passes of one batch chunk.
-static hipError_t launch_chunk(const Context* c, const RowSel& rs, uint32_t batch, uint32_t limbs,
-                               bool inverse, hipStream_t s) {
-  const uint32_t log_n = c->log_n;
+// Epilogue fusing the key-switch combine into the forward transform of the
+// ModDown conversion y: for u = 2*job + t (blockIdx.y) and limb i
+// (blockIdx.z), out_job[i][t] = (acc[u][i] - NTT(y)[u][i]) * P^-1 + adds,
+// with the adds of the job table (sigma_g-permuted `add`, plain `add2`).
+struct KsCombine {
+  KsTable tab;
+  const uint64_t* acc;
+  const double2* pinv;
+  uint32_t level, alpha, log_n;
+  __device__ __forceinline__ void operator()(uint64_t*, uint32_t k0, const double (&x)[16],
+                                             double q, double qinv, uint32_t n) const {
+    const uint32_t u = blockIdx.y, i = blockIdx.z, job = u >> 1, t = u & 1;
+    const uint32_t E = level + alpha;
+    const double2 f = pinv[i];
+    const uint64_t* a = acc + ((size_t)u * E + i) * n;
+    const size_t o = ((size_t)2 * i + t) * n;
+    const bool use_add = (tab.add_mask[job] >> t) & 1u;
+    const uint32_t g = tab.add_galois[job];
+    const uint64_t* add = use_add ? tab.add[job] + o : nullptr;
+    const uint64_t* add2 = tab.add2[job];
+    uint64_t* out = tab.out[job] + o;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const uint32_t k = k0 + 256 * r;
+      double v = mm_shoup(u2d(a[k]) - x[r], f.x, f.y, q);
+      if (use_add) v += u2d(add[g ? galois_src(k, g, log_n) : k]);
+      if (add2) v += u2d(add2[o + k]);
+      out[k] = d2u(red_full(v, q, qinv));
+    }
+  }
+};
+
+namespace {
+
+static hipError_t launch_outer_pass(const Context* c, const RowSel& rs, uint32_t batch,
+                                    uint32_t limbs, bool inverse, hipStream_t s) {
+  if (c->log_n == 12) return hipSuccess;
   const double2* tw = inverse ? c->d_tw_inv : c->d_tw_fwd;
-  dim3 inner(c->n / 4096, batch, limbs);
-  dim3 outer(1, batch, limbs);
-  if (inverse)
-    hipLaunchKernelGGL(k_inv_inner, inner, dim3(kThreads), 0, s, rs, log_n, c->d_pk, tw);
-  switch (log_n) {
-    case 12: launch_outer<4>(inverse, outer, s, rs, log_n, c->d_pk, tw); break;
-    case 13: launch_outer<5>(inverse, outer, s, rs, log_n, c->d_pk, tw); break;
-    case 14: launch_outer<6>(inverse, outer, s, rs, log_n, c->d_pk, tw); break;
-    case 15: launch_outer<7>(inverse, outer, s, rs, log_n, c->d_pk, tw); break;
-    case 16: launch_outer<8>(inverse, outer, s, rs, log_n, c->d_pk, tw); break;
+  const dim3 grid(c->n / kBlock, batch, limbs), blk(kThreads);
+#define FESC_OUTER(L)                                                                \
+  if (inverse)                                                                       \
+    hipLaunchKernelGGL(k_inv_outer<L>, grid, blk, 0, s, rs, c->log_n, c->d_pk, tw);  \
+  else                                                                               \
+    hipLaunchKernelGGL(k_fwd_outer<L>, grid, blk, 0, s, rs, c->log_n, c->d_pk, tw);  \
+  break;
+  switch (c->log_n) {
+    case 13: FESC_OUTER(1)
+    case 14: FESC_OUTER(2)
+    case 15: FESC_OUTER(3)
+    case 16: FESC_OUTER(4)
     default: return hipErrorInvalidValue;
   }
-  if (!inverse)
-    hipLaunchKernelGGL(k_fwd_inner, inner, dim3(kThreads), 0, s, rs, log_n, c->d_pk, tw);
+#undef FESC_OUTER
+  return hipGetLastError();
+}
+
+template <class Epi>
+void launch_fwd_inner(const Context* c, const RowSel& rs, uint32_t batch, uint32_t limbs,
+                      const Epi& epi, hipStream_t s) {
+  const dim3 grid(c->n / kBlock, batch, limbs), blk(kThreads);
+  if (c->log_n == 12)
+    k_fwd_inner<true, Epi><<<grid, blk, 0, s>>>(rs, c->log_n, c->d_pk,
+                       c->d_tw_fwd, c->d_tw3_fwd, epi);
+  else
+    k_fwd_inner<false, Epi><<<grid, blk, 0, s>>>(rs, c->log_n, c->d_pk,
+                       c->d_tw_fwd, c->d_tw3_fwd, epi);
+}
+
+template <class Ld>
+void launch_inv_inner(const Context* c, const RowSel& rs, uint32_t batch, uint32_t limbs,
+                      const Ld& ld, hipStream_t s) {
+  const dim3 grid(c->n / kBlock, batch, limbs), blk(kThreads);
+  if (c->log_n == 12)
+    k_inv_inner<true, Ld><<<grid, blk, 0, s>>>(rs, c->log_n, c->d_pk,
+                       c->d_tw_inv, c->d_tw3_inv, ld);
+  else
+    k_inv_inner<false, Ld><<<grid, blk, 0, s>>>(rs, c->log_n, c->d_pk,
+                       c->d_tw_inv, c->d_tw3_inv, ld);
+}
+
+}  // namespace
+
+// Inverse transform of the first `level` rows of each key-switch source into
+// cc[s][level][N] (out of place: the first pass reads the sources directly).
+hipError_t launch_ntt_inv_sources(const Context* c, const KsTable& tab, uint32_t nsrc,
+                                  uint64_t* cc, uint32_t level, hipStream_t s) {
+  RowSel rs{cc, (size_t)level * c->n, (size_t)c->n, 0, level, 0, 0, 0, 0};
+  launch_inv_inner(c, rs, nsrc, level, LoadSources{tab}, s);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_outer_pass(c, rs, nsrc, level, true, s);
+}
+
+// Forward transform of the ModDown conversions y[2*njobs][level][N] with the
+// key-switch combine as the epilogue (writes the jobs' outputs; y keeps the
+// first pass's intermediate only).
+hipError_t launch_ntt_fwd_ks_combine(const Context* c, uint64_t* y, uint32_t njobs,
+                                     uint32_t level, const KsTable& tab, const uint64_t* acc,
+                                     const double2* pinv, hipStream_t s) {
+  RowSel rs{y, (size_t)level * c->n, (size_t)c->n, 0, level, 0, 0, 0, 0};
+  hipError_t e = launch_outer_pass(c, rs, 2 * njobs, level, false, s);
+  if (e != hipSuccess) return e;
+  launch_fwd_inner(c, rs, 2 * njobs, level, KsCombine{tab, acc, pinv, level, c->alpha, c->log_n},
+                   s);
   return hipGetLastError();
 }
 
@@ -382,7 +474,16 @@ static hipError_t launch_chunk(const Context* c, const RowSel& rs, uint32_t batc
 // measured slower on MI355X than one launch per pass over the whole batch.)
 hipError_t launch_ntt_rows(const Context* c, const RowSel& rs, uint32_t batch, uint32_t limbs,
                            bool inverse, hipStream_t s) {
-  return launch_chunk(c, rs, batch, limbs, inverse, s);
+  if (inverse) {
+    launch_inv_inner(c, rs, batch, limbs, LoadRow{}, s);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_outer_pass(c, rs, batch, limbs, true, s);
+  }
+  hipError_t e = launch_outer_pass(c, rs, batch, limbs, false, s);
+  if (e != hipSuccess) return e;
+  launch_fwd_inner(c, rs, batch, limbs, StoreResidues{}, s);
+  return hipGetLastError();
 }
 
 hipError_t launch_ntt(const Context* c, uint64_t* d, uint32_t batch, size_t batch_stride,

@@ -175,8 +175,7 @@ int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& sr
   // ModUp of every source (the scratch capacity covers all of them)
   const uint32_t ns = (uint32_t)srcs.size();
   if (ns > S.cap) return fail(FESC_ERR_ARG, "key-switch sources exceed the scratch capacity");
-  HIPCK(k_gather_launch(c, tab, ns, S.cc, level, s));
-  HIPCK(ntt_rows(c, S.cc, ns, (size_t)level * n, level, 0, true, s));
+  HIPCK(launch_ntt_inv_sources(c, tab, ns, S.cc, level, s));
   HIPCK(k_modup_launch(c, *T, S.cc, S.ext, ns, level, s));
   RowSel rs{S.ext, (size_t)E * n, n, 0, level, c->L, c->alpha, level, dnum_l};
   HIPCK(launch_ntt_rows(c, rs, ns * dnum_l, E, false, s));
@@ -198,8 +197,7 @@ int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& sr
     HIPCK(k_ip_launch(c, t, nj, S.ext, S.acc, level, s));
     HIPCK(ntt_rows(c, S.acc + (size_t)level * n, 2 * nj, (size_t)E * n, c->alpha, c->L, true, s));
     HIPCK(k_moddown_bconv_launch(c, *T, S.acc, S.y, nj, level, s));
-    HIPCK(ntt_rows(c, S.y, 2 * nj, (size_t)level * n, level, 0, false, s));
-    HIPCK(k_ks_combine_launch(c, *T, t, nj, S.acc, S.y, level, s));
+    HIPCK(launch_ntt_fwd_ks_combine(c, S.y, nj, level, t, S.acc, T->md_pinv, s));
   }
   return FESC_OK;
 }

@@ -54,6 +54,13 @@ struct KsTable {
 
 hipError_t k_gather_launch(const Context* c, const KsTable& tab, uint32_t nsrc, uint64_t* cc,
                            uint32_t level, hipStream_t s);
+
+// ntt.hip: fused transforms of the key-switch pipeline
+hipError_t launch_ntt_inv_sources(const Context* c, const KsTable& tab, uint32_t nsrc,
+                                  uint64_t* cc, uint32_t level, hipStream_t s);
+hipError_t launch_ntt_fwd_ks_combine(const Context* c, uint64_t* y, uint32_t njobs,
+                                     uint32_t level, const KsTable& tab, const uint64_t* acc,
+                                     const double2* pinv, hipStream_t s);
 hipError_t k_modup_launch(const Context* c, const LevelTables& T, const uint64_t* cc,
                           uint64_t* ext, uint32_t nsrc, uint32_t level, hipStream_t s);
 hipError_t k_ip_launch(const Context* c, const KsTable& tab, uint32_t njobs, const uint64_t* ext,
