@@ -16,7 +16,7 @@ constexpr int kThreads = 256;
 
 __device__ __forceinline__ double ld(const uint64_t* p) { return u2d(*p); }
 __device__ __forceinline__ void st(uint64_t* p, double v, double q, double qinv) {
-  *p = d2u(red_full(v, q, qinv));
+  *p = to_res(v, q, qinv);
 }
 
 // ---------------------------------------------------------------- binary

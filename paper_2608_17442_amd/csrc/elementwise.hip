@@ -29,8 +29,8 @@ __global__ __launch_bounds__(kThreads) void k_mac(const uint64_t* __restrict__ a
     acc1 = red_bal(acc1 + mm_var(u2d(va.y), u2d(vb.y), q, qinv), q, qinv);
   }
   ulonglong2 r;
-  r.x = d2u(red_full(acc0, q, qinv));
-  r.y = d2u(red_full(acc1, q, qinv));
+  r.x = to_res(acc0, q, qinv);
+  r.y = to_res(acc1, q, qinv);
   *reinterpret_cast<ulonglong2*>(out + off) = r;
 }
 

@@ -75,15 +75,21 @@ __device__ __forceinline__ uint32_t galois_src(uint32_t jp, uint32_t g, uint32_t
   return __builtin_bitreverse32((e - 1u) >> 1) >> (32 - log_n);
 }
 
+// Integer <-> double for values below 2^52: the double 2^52 + x has exactly
+// x in its 52 mantissa bits, so each direction is one bit operation and one
+// fp64 add.
+constexpr double kTwo52 = 4503599627370496.0;
+
+// x: residue (below 2^52)
 __device__ __forceinline__ double u2d(uint64_t x) {
-  return __builtin_fma((double)(uint32_t)(x >> 32), 4294967296.0, (double)(uint32_t)x);
+  return __longlong_as_double((long long)(x | 0x4330000000000000ull)) - kTwo52;
 }
 
-// r: non-negative integer below 2^53
-__device__ __forceinline__ uint64_t d2u(double r) {
-  double hi = __builtin_floor(r * (1.0 / 4294967296.0));
-  double lo = __builtin_fma(-hi, 4294967296.0, r);
-  return ((uint64_t)(uint32_t)hi << 32) | (uint64_t)(uint32_t)lo;
+// Canonical residue in [0, q) of an integer-valued x, |x| < 2^52, as uint64.
+__device__ __forceinline__ uint64_t to_res(double x, double q, double qinv) {
+  const double r = red_bal(x, q, qinv);
+  const double v = r + (r < 0.0 ? q + kTwo52 : kTwo52);
+  return (uint64_t)__double_as_longlong(v) & 0x000FFFFFFFFFFFFFull;
 }
 
 // ------------------------------------------------------------- host side
@@ -112,8 +118,10 @@ struct Context {
   std::vector<uint64_t> primes;   // ext order: q_0..q_{L-1}, p_0..p_{alpha-1}
   std::vector<uint64_t> psi;      // smallest primitive 2N-th root per prime
   PrimeK* d_pk = nullptr;         // [L+alpha]
-  double2* d_tw_fwd = nullptr;    // [L+alpha][N] {psi^brv(i), /q}
-  double2* d_tw_inv = nullptr;    // [L+alpha][N] {psi^-brv(i), /q}
+  // [L+alpha][N] {w, w/q}, w = psi^brv(i) (inverse: psi^-brv(i)) as the
+  // balanced representative in [-q/2, q/2]
+  double2* d_tw_fwd = nullptr;
+  double2* d_tw_inv = nullptr;
   // the powers used by the radix-16 step on index bits 3..0 of the 4096-point
   // inner NTT blocks, re-ordered [L+alpha][N/4096][15][256] (see ntt.hip)
   double* d_tw3_fwd = nullptr;

@@ -125,8 +125,11 @@ static int build_tables(Context* c) {
       pw[0] = 1;
       for (uint32_t e = 1; e < n; ++e) pw[e] = h_mulmod(pw[e - 1], root, q);
       double2* t = (dir == 0 ? fwd.data() : inv.data()) + (size_t)i * n;
+      // balanced representative, |w| <= q/2 (halves the error term of the
+      // Shoup products, which the lazy butterflies rely on)
       for (uint32_t k = 0; k < n; ++k) {
-        const double w = (double)pw[bitrev(k, c->log_n)];
+        const uint64_t e = pw[bitrev(k, c->log_n)];
+        const double w = e > q / 2 ? -(double)(q - e) : (double)e;
         t[k] = double2{w, w / qd};
       }
       // Block blk, slot k (register distance H, group gi), thread e: the

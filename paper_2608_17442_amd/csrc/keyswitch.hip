@@ -67,8 +67,8 @@ __device__ __forceinline__ void conv_row(const double (&x0)[A], const double (&x
     }
   }
   ulonglong2 o;
-  o.x = d2u(red_full(s0, M.q, M.qinv));
-  o.y = d2u(red_full(s1, M.q, M.qinv));
+  o.x = to_res(s0, M.q, M.qinv);
+  o.y = to_res(s1, M.q, M.qinv);
   *reinterpret_cast<ulonglong2*>(dst) = o;
 }
 
@@ -165,8 +165,8 @@ __global__ __launch_bounds__(kThreads) void k_ip(KsTable tab, const uint64_t* __
     }
   }
   uint64_t* out = acc + (size_t)job * 2 * E * n;
-  out[(size_t)row * n + k] = d2u(red_full(ab, M.q, M.qinv));
-  out[((size_t)E + row) * n + k] = d2u(red_full(aa, M.q, M.qinv));
+  out[(size_t)row * n + k] = to_res(ab, M.q, M.qinv);
+  out[((size_t)E + row) * n + k] = to_res(aa, M.q, M.qinv);
 }
 
 // ModDown conversion: for u = 2*job + t (blockIdx.y), the P-rows of acc[u]
@@ -222,7 +222,7 @@ __global__ __launch_bounds__(kThreads) void k_ks_combine(KsTable tab,
     v += u2d(tab.add[job][o + (g ? galois_src(k, g, log_n) : k)]);
   }
   if (tab.add2[job]) v += u2d(tab.add2[job][o + k]);
-  tab.out[job][o + k] = d2u(red_full(v, M.q, M.qinv));
+  tab.out[job][o + k] = to_res(v, M.q, M.qinv);
 }
 
 // Dispatch on a runtime value to a template instantiation 1..16.

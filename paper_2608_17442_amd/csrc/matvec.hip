@@ -117,8 +117,8 @@ __global__ __launch_bounds__(kThreads) void k_ptmac(const uint64_t* const* __res
   for (int g = 0; g < G; ++g) {
     if ((uint32_t)g < g_end) {
       uint64_t* o = outs[o0 + g];
-      o[c0] = d2u(red_full(a0[g], P.q, P.qinv));
-      o[c1] = d2u(red_full(a1[g], P.q, P.qinv));
+      o[c0] = to_res(a0[g], P.q, P.qinv);
+      o[c1] = to_res(a1[g], P.q, P.qinv);
     }
   }
 }

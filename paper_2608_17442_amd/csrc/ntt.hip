@@ -39,20 +39,43 @@ namespace {
 constexpr int kThreads = 256;
 constexpr uint32_t kBlock = 4096;
 
-// LDS index with one pad word per 16 values
-__device__ __forceinline__ uint32_t pad16(uint32_t k) { return k + (k >> 4); }
+// LDS layout of a 4096-value block: one pad word after every 16 values, so
+// value k sits at k + k/16.  All three access patterns below then reduce to a
+// per-thread base plus a compile-time offset (no address arithmetic per
+// access), and 16 consecutive lanes always hit 16 distinct 8-byte bank slots.
+//   lds_row(t, r):    value t + 256 r        (bits 11..8 in registers)
+//   lds_mid(a, b, r): value 256 a + 16 r + b (bits 7..4 in registers)
+//   lds_col(t, r):    value 16 t + r         (bits 3..0 in registers)
+__device__ __forceinline__ uint32_t lds_row(uint32_t t, uint32_t r) {
+  return (t + (t >> 4)) + 272 * r;
+}
+__device__ __forceinline__ uint32_t lds_mid(uint32_t a, uint32_t b, uint32_t r) {
+  return (272 * a + b) + 17 * r;
+}
+__device__ __forceinline__ uint32_t lds_col(uint32_t t, uint32_t r) { return 17 * t + r; }
 constexpr int kLds = kBlock + kBlock / 16;
 
 // Radix-2 stages on a 16-value register tile, pairs (r, r + H) with r & H == 0.
 // tw(gi) gives the twiddle {w, w/q} of group gi = r / 2H.
-template <int H, class TW>
+//
+// Twiddles are stored balanced, |w| <= q/2, so the Shoup product of
+// |x| <= X q lands within (0.5 + X/8) q for q < 2^50 (its quotient estimate is
+// off by at most |x w/q| 2^-52).  Butterflies therefore reduce lazily:
+//   forward (CT): only every other stage (RED) reduces the pass-through
+//     operand u; a reducing stage maps the bound X to 1 + X/8, a lazy one to
+//     0.5 + 1.125 X, so from any input below 2.6 q values stay below 2.6 q;
+//   inverse (GS): only every other stage reduces the sum u + v; the
+//     difference goes through a Shoup product, so a (reducing, lazy) pair maps
+//     X to 1 + X/2 and inputs below 2 q stay below 2 q.
+// Both are far inside the 2^53 range of exact fp64 integers.
+template <int H, bool RED, class TW>
 __device__ __forceinline__ void ct_st(double (&x)[16], TW tw, double q, double qinv) {
 #pragma unroll
   for (int g = 0; g < 16; g += 2 * H) {
     const double2 w = tw(g / (2 * H));
 #pragma unroll
     for (int r = g; r < g + H; ++r) {
-      const double u = red_bal(x[r], q, qinv);
+      const double u = RED ? red_bal(x[r], q, qinv) : x[r];
       const double v = mm_shoup(x[r + H], w.x, w.y, q);
       x[r] = u + v;
       x[r + H] = u - v;
@@ -60,7 +83,7 @@ __device__ __forceinline__ void ct_st(double (&x)[16], TW tw, double q, double q
   }
 }
 
-template <int H, class TW>
+template <int H, bool RED, class TW>
 __device__ __forceinline__ void gs_st(double (&x)[16], TW tw, double q, double qinv) {
 #pragma unroll
   for (int g = 0; g < 16; g += 2 * H) {
@@ -68,7 +91,7 @@ __device__ __forceinline__ void gs_st(double (&x)[16], TW tw, double q, double q
 #pragma unroll
     for (int r = g; r < g + H; ++r) {
       const double u = x[r], v = x[r + H];
-      x[r] = red_bal(u + v, q, qinv);
+      x[r] = RED ? red_bal(u + v, q, qinv) : u + v;
       x[r + H] = mm_shoup(u - v, w.x, w.y, q);
     }
   }
@@ -125,6 +148,7 @@ namespace {
 // M = 2^LOGM point columns at stride 4096; a thread holds C = 16/M columns,
 // c0 + 256 j (j < C), value m of column j in x[j*M + m].  Grid x = M.
 // Stage s (distance 4096 * M/2^(s+1)) uses psi_rev[2^s + m / 2^(LOGM-s)].
+// Forward stages reduce lazily as in ct_st (even s reduce).
 template <int LOGM>
 __global__ __launch_bounds__(kThreads) void k_fwd_outer(RowSel rs, uint32_t log_n,
                                                         const PrimeK* __restrict__ pk,
@@ -151,7 +175,7 @@ __global__ __launch_bounds__(kThreads) void k_fwd_outer(RowSel rs, uint32_t log_
       const double2 w = tw[(1 << s) + (m >> (LOGM - s))];
 #pragma unroll
       for (int j = 0; j < C; ++j) {
-        const double u = red_bal(x[j * M + m], q, qinv);
+        const double u = (s % 2 == 0) ? red_bal(x[j * M + m], q, qinv) : x[j * M + m];
         const double v = mm_shoup(x[j * M + m + H], w.x, w.y, q);
         x[j * M + m] = u + v;
         x[j * M + m + H] = u - v;
@@ -165,7 +189,8 @@ __global__ __launch_bounds__(kThreads) void k_fwd_outer(RowSel rs, uint32_t log_
     for (int m = 0; m < M; ++m) rowd[c0 + kThreads * j + kBlock * m] = x[j * M + m];
 }
 
-// Inverse: stages in reverse order, then N^-1 and canonical uint64 residues.
+// Inverse: stages in reverse order (every other one reducing, as in gs_st),
+// then N^-1 and canonical uint64 residues.
 template <int LOGM>
 __global__ __launch_bounds__(kThreads) void k_inv_outer(RowSel rs, uint32_t log_n,
                                                         const PrimeK* __restrict__ pk,
@@ -194,7 +219,7 @@ __global__ __launch_bounds__(kThreads) void k_inv_outer(RowSel rs, uint32_t log_
 #pragma unroll
       for (int j = 0; j < C; ++j) {
         const double u = x[j * M + m], v = x[j * M + m + H];
-        x[j * M + m] = red_bal(u + v, P.q, P.qinv);
+        x[j * M + m] = ((LOGM - 1 - s) % 2 == 0) ? red_bal(u + v, P.q, P.qinv) : u + v;
         x[j * M + m + H] = mm_shoup(u - v, w.x, w.y, P.q);
       }
     }
@@ -204,7 +229,7 @@ __global__ __launch_bounds__(kThreads) void k_inv_outer(RowSel rs, uint32_t log_
 #pragma unroll
     for (int m = 0; m < M; ++m)
       row[c0 + kThreads * j + kBlock * m] =
-          d2u(red_full(mm_shoup(x[j * M + m], P.ninv, P.ninvp, P.q), P.q, P.qinv));
+          to_res(mm_shoup(x[j * M + m], P.ninv, P.ninvp, P.q), P.q, P.qinv);
 }
 
 // ------------------------------------------------------------- inner pass
@@ -241,36 +266,36 @@ __global__ __launch_bounds__(kThreads) void k_fwd_inner(RowSel rs, uint32_t log_
     for (int r = 0; r < 16; ++r) x[r] = src[256 * r];
   }
   // bits 11..8
-  ct_st<8>(x, TwHi{tw, nb >> 12}, q, qinv);
-  ct_st<4>(x, TwHi{tw, nb >> 11}, q, qinv);
-  ct_st<2>(x, TwHi{tw, nb >> 10}, q, qinv);
-  ct_st<1>(x, TwHi{tw, nb >> 9}, q, qinv);
+  ct_st<8, true>(x, TwHi{tw, nb >> 12}, q, qinv);
+  ct_st<4, false>(x, TwHi{tw, nb >> 11}, q, qinv);
+  ct_st<2, true>(x, TwHi{tw, nb >> 10}, q, qinv);
+  ct_st<1, false>(x, TwHi{tw, nb >> 9}, q, qinv);
 #pragma unroll
-  for (int r = 0; r < 16; ++r) lds[pad16(t + 256 * r)] = x[r];
+  for (int r = 0; r < 16; ++r) lds[lds_row(t, r)] = x[r];
   __syncthreads();
 #pragma unroll
-  for (int r = 0; r < 16; ++r) x[r] = lds[pad16(256 * a + 16 * r + b)];
+  for (int r = 0; r < 16; ++r) x[r] = lds[lds_mid(a, b, r)];
   // bits 7..4
-  ct_st<8>(x, TwHi{tw, (nb >> 8) + a}, q, qinv);
-  ct_st<4>(x, TwHi{tw, (nb >> 7) + 2 * a}, q, qinv);
-  ct_st<2>(x, TwHi{tw, (nb >> 6) + 4 * a}, q, qinv);
-  ct_st<1>(x, TwHi{tw, (nb >> 5) + 8 * a}, q, qinv);
+  ct_st<8, true>(x, TwHi{tw, (nb >> 8) + a}, q, qinv);
+  ct_st<4, false>(x, TwHi{tw, (nb >> 7) + 2 * a}, q, qinv);
+  ct_st<2, true>(x, TwHi{tw, (nb >> 6) + 4 * a}, q, qinv);
+  ct_st<1, false>(x, TwHi{tw, (nb >> 5) + 8 * a}, q, qinv);
 #pragma unroll
-  for (int r = 0; r < 16; ++r) lds[pad16(256 * a + 16 * r + b)] = x[r];
+  for (int r = 0; r < 16; ++r) lds[lds_mid(a, b, r)] = x[r];
   __syncthreads();
 #pragma unroll
-  for (int r = 0; r < 16; ++r) x[r] = lds[pad16(16 * t + r)];
+  for (int r = 0; r < 16; ++r) x[r] = lds[lds_col(t, r)];
   // bits 3..0
   const double* s3 = tw3 + ((size_t)prime * (n / kBlock) + blockIdx.x) * (15 * kThreads) + t;
-  ct_st<8>(x, TwLo<8>{s3, qinv}, q, qinv);
-  ct_st<4>(x, TwLo<4>{s3, qinv}, q, qinv);
-  ct_st<2>(x, TwLo<2>{s3, qinv}, q, qinv);
-  ct_st<1>(x, TwLo<1>{s3, qinv}, q, qinv);
+  ct_st<8, true>(x, TwLo<8>{s3, qinv}, q, qinv);
+  ct_st<4, false>(x, TwLo<4>{s3, qinv}, q, qinv);
+  ct_st<2, true>(x, TwLo<2>{s3, qinv}, q, qinv);
+  ct_st<1, false>(x, TwLo<1>{s3, qinv}, q, qinv);
 #pragma unroll
-  for (int r = 0; r < 16; ++r) lds[pad16(16 * t + r)] = x[r];
+  for (int r = 0; r < 16; ++r) lds[lds_col(t, r)] = x[r];
   __syncthreads();
 #pragma unroll
-  for (int r = 0; r < 16; ++r) x[r] = lds[pad16(t + 256 * r)];
+  for (int r = 0; r < 16; ++r) x[r] = lds[lds_row(t, r)];
   epi(row, B + t, x, q, qinv, n);
 }
 
@@ -279,7 +304,7 @@ struct StoreResidues {
   __device__ __forceinline__ void operator()(uint64_t* row, uint32_t k0, const double (&x)[16],
                                              double q, double qinv, uint32_t) const {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) row[k0 + 256 * r] = d2u(red_full(x[r], q, qinv));
+    for (int r = 0; r < 16; ++r) row[k0 + 256 * r] = to_res(x[r], q, qinv);
   }
 };
 
@@ -325,34 +350,34 @@ __global__ __launch_bounds__(kThreads) void k_inv_inner(RowSel rs, uint32_t log_
   }
   // bits 3..0
   const double* s3 = tw3 + ((size_t)prime * (n / kBlock) + blockIdx.x) * (15 * kThreads) + t;
-  gs_st<1>(x, TwLo<1>{s3, qinv}, q, qinv);
-  gs_st<2>(x, TwLo<2>{s3, qinv}, q, qinv);
-  gs_st<4>(x, TwLo<4>{s3, qinv}, q, qinv);
-  gs_st<8>(x, TwLo<8>{s3, qinv}, q, qinv);
+  gs_st<1, true>(x, TwLo<1>{s3, qinv}, q, qinv);
+  gs_st<2, false>(x, TwLo<2>{s3, qinv}, q, qinv);
+  gs_st<4, true>(x, TwLo<4>{s3, qinv}, q, qinv);
+  gs_st<8, false>(x, TwLo<8>{s3, qinv}, q, qinv);
 #pragma unroll
-  for (int r = 0; r < 16; ++r) lds[pad16(16 * t + r)] = x[r];
+  for (int r = 0; r < 16; ++r) lds[lds_col(t, r)] = x[r];
   __syncthreads();
 #pragma unroll
-  for (int r = 0; r < 16; ++r) x[r] = lds[pad16(256 * a + 16 * r + b)];
+  for (int r = 0; r < 16; ++r) x[r] = lds[lds_mid(a, b, r)];
   // bits 7..4
-  gs_st<1>(x, TwHi{tw, (nb >> 5) + 8 * a}, q, qinv);
-  gs_st<2>(x, TwHi{tw, (nb >> 6) + 4 * a}, q, qinv);
-  gs_st<4>(x, TwHi{tw, (nb >> 7) + 2 * a}, q, qinv);
-  gs_st<8>(x, TwHi{tw, (nb >> 8) + a}, q, qinv);
+  gs_st<1, true>(x, TwHi{tw, (nb >> 5) + 8 * a}, q, qinv);
+  gs_st<2, false>(x, TwHi{tw, (nb >> 6) + 4 * a}, q, qinv);
+  gs_st<4, true>(x, TwHi{tw, (nb >> 7) + 2 * a}, q, qinv);
+  gs_st<8, false>(x, TwHi{tw, (nb >> 8) + a}, q, qinv);
 #pragma unroll
-  for (int r = 0; r < 16; ++r) lds[pad16(256 * a + 16 * r + b)] = x[r];
+  for (int r = 0; r < 16; ++r) lds[lds_mid(a, b, r)] = x[r];
   __syncthreads();
 #pragma unroll
-  for (int r = 0; r < 16; ++r) x[r] = lds[pad16(t + 256 * r)];
+  for (int r = 0; r < 16; ++r) x[r] = lds[lds_row(t, r)];
   // bits 11..8
-  gs_st<1>(x, TwHi{tw, nb >> 9}, q, qinv);
-  gs_st<2>(x, TwHi{tw, nb >> 10}, q, qinv);
-  gs_st<4>(x, TwHi{tw, nb >> 11}, q, qinv);
-  gs_st<8>(x, TwHi{tw, nb >> 12}, q, qinv);
+  gs_st<1, true>(x, TwHi{tw, nb >> 9}, q, qinv);
+  gs_st<2, false>(x, TwHi{tw, nb >> 10}, q, qinv);
+  gs_st<4, true>(x, TwHi{tw, nb >> 11}, q, qinv);
+  gs_st<8, false>(x, TwHi{tw, nb >> 12}, q, qinv);
   if constexpr (SINGLE) {
 #pragma unroll
     for (int r = 0; r < 16; ++r)
-      row[B + t + 256 * r] = d2u(red_full(mm_shoup(x[r], P.ninv, P.ninvp, q), q, qinv));
+      row[B + t + 256 * r] = to_res(mm_shoup(x[r], P.ninv, P.ninvp, q), q, qinv);
   } else {
     double* dst = reinterpret_cast<double*>(row) + B + t;
 #pragma unroll
@@ -389,7 +414,7 @@ struct KsCombine {
       double v = mm_shoup(u2d(a[k]) - x[r], f.x, f.y, q);
       if (use_add) v += u2d(add[g ? galois_src(k, g, log_n) : k]);
       if (add2) v += u2d(add2[o + k]);
-      out[k] = d2u(red_full(v, q, qinv));
+      out[k] = to_res(v, q, qinv);
     }
   }
 };

@@ -52,3 +52,32 @@ def test_host_helpers_reject_bad_input():
     with pytest.raises(F.FescError) as e:
         F.root_of_unity(12, 1000003)   # prime, but not 1 mod 2N
     assert e.value.code == -1
+
+
+@pytest.mark.parametrize("log_n,scale_bits,kind", [(12, 30, "pm1"), (16, 40, "pm1"),
+                                                   (16, 49, "normal")])
+def test_host_encoder_matches_oracle_encoding(log_n, scale_bits, kind):
+    """fesc_encode (host slot encoder, Sec. 2.1 packing) against the oracle's
+    encoding.  Both round Delta * m_k half away from zero after an FFT of their
+    own, so the integers agree except where Delta * m_k lies within the two
+    FFTs' rounding error of a half-integer; there they may differ by one."""
+    import numpy as np
+
+    import synth
+    from oracle import encoding as E
+    from paper_2608_17442_amd import fesc as F
+    n = 1 << log_n
+    if kind == "pm1":
+        z = synth.uniform_pm1(50 + log_n, "enc-re", n // 2) \
+            + 1j * synth.uniform_pm1(50 + log_n, "enc-im", n // 2)
+    else:
+        z = synth.normal(51, "enc-n", n // 2, 0.02).astype(complex)
+    scale = 2.0 ** scale_bits
+    got = F.encode(log_n, z, scale)
+    raw = E.encode_real_coeffs(z, scale, n)
+    want = E.encode(z, scale, n)
+    diff = got - want
+    near_tie = np.abs(np.abs(raw - np.trunc(raw)) - 0.5) < 1e-2
+    assert np.all(np.abs(diff) <= 1)
+    assert not np.any(diff[~near_tie]), np.flatnonzero(diff[~near_tie])[:8]
+    assert np.count_nonzero(diff) <= np.count_nonzero(near_tie)
