@@ -107,3 +107,86 @@ def test_paired_bsgs_small():
         assert np.array_equal(got, outs_o[b]), f"block {b}: {first_mismatch(got, outs_o[b])}"
         dec = C.decrypt(P, S.sk, outs_o[b], 2.0 ** 40)
         assert np.max(np.abs(dec.real - Y[r, b * Cc + s])) <= 2.0 ** -15
+
+
+def test_cfg4_full_size_projection():
+    """The 768 x 1536 projection at full size (N = 2^16, 16 limbs at input,
+    12 paired input ciphertexts of 1024 tokens, 48 output ciphertexts, BSGS
+    n1 = 16, n2 = 2) in the launch configuration the benchmark times: all
+    18,432 diagonals in one tiled bank.  Output blocks 0 and 47 (47 lies in
+    the second, partial group of 32 batched giant-step key switches) are
+    compared residue by residue with the oracle; every output block is
+    decrypted and compared with X W in fp64 within 2^-15."""
+    import concurrent.futures as cf
+    import os
+
+    from paper_2608_17442_amd import fesc as F
+    from paper_2608_17442_amd import packing as PK
+    cfg = WL.CFG4
+    P = C.params_p16()
+    level, seg = cfg["level"], cfg["tokens"]
+    n_slots = P.n // 2
+    Cc = n_slots // seg
+    n1, n2 = cfg["n1"], cfg["n2"]
+    n_in, n_out = cfg["d_in"] // Cc // 2, cfg["d_out"] // Cc
+    desc = OW.MatvecDesc(level, n_in, n_out, n1, n2, seg, True, True)
+    S = Setup(P, cfg["seed"], rot_steps=sorted(OW.required_rotations(desc, n_slots)), conj=True)
+    X, Wm = WL.cfg4_values()
+    ins_o, ins_d = [], []
+    for u in range(n_in):
+        z = OW.pack_input(X, n_slots, seg, Cc, 2 * u) + 1j * OW.pack_input(X, n_slots, seg, Cc,
+                                                                            2 * u + 1)
+        co, cd = S.encrypt(z, 2.0 ** 40, level, 3000 + u)
+        ins_o.append(co)
+        ins_d.append(cd)
+    check = (0, n_out - 1)
+    scale = float(P.q[level - 1])
+    index = [(b, p, u, q) for b in range(n_out) for p in range(n2) for u in range(n_in)
+             for q in range(n1)]
+    fd = F.matvec_desc(level, n_in, n_out, n1, n2, seg, True, True)
+    bank = torch.zeros(F.matvec_bank_words(S.ctx, fd), dtype=torch.int64, device="cuda")
+    stage = torch.empty(level * P.n, dtype=torch.int64, device="cuda")
+    oracle_pt = {}
+
+    def prepare(t):
+        b, p, u, q = index[t]
+        if b in check:   # oracle encoding of the diagonals of the compared blocks
+            v = OW.bsgs_diagonal_slots(Wm, n_slots, seg, Cc, n1, b, p, u, q, True)
+            oracle_pt[index[t]] = C.encode_plain(P, v, scale, level)
+            return None
+        return F.encode(P.log_n, PK.diagonal_slots(Wm, b, p, u, q, n1, n_slots, seg, Cc, True),
+                        scale)
+
+    step(f"cfg4 bank: {len(index)} diagonals")
+    with cf.ThreadPoolExecutor(min(16, os.cpu_count() or 1)) as ex:
+        for c0 in range(0, len(index), 512):
+            ids = list(range(c0, min(c0 + 512, len(index))))
+            for t, coeffs in zip(ids, ex.map(prepare, ids)):
+                if coeffs is None:
+                    F.matvec_bank_pack(S.ctx, fd, bank, t, to_dev(oracle_pt[index[t]]))
+                else:
+                    S.ctx.plain_from_coeffs(torch.from_numpy(coeffs).cuda(), stage, level)
+                    F.matvec_bank_pack(S.ctx, fd, bank, t, stage)
+    torch.cuda.synchronize()
+    plan = F.MatvecPlan(S.ctx, level, n_in, n_out, n1, n2, seg, True, True, bank=bank)
+    outs_d = [torch.zeros((level - 1) * 2 * P.n, dtype=torch.int64, device="cuda")
+              for _ in range(n_out)]
+    step("cfg4 matvec run")
+    plan(ins_d, outs_d)
+    torch.cuda.synchronize()
+    del bank
+    step("cfg4 oracle blocks")
+    outs_o = OW.bsgs_matvec(P, desc, ins_o, lambda b, p, u, q: oracle_pt[(b, p, u, q)], S.keys,
+                            blocks=check)
+    for b, want in zip(check, outs_o):
+        got = to_host(outs_d[b]).reshape(want.shape)
+        assert np.array_equal(got, want), f"block {b}: {first_mismatch(got, want)}"
+    Y = X @ Wm
+    r, s = OW.segment_indices(n_slots, seg, Cc)
+    worst = 0.0
+    for b in range(n_out):
+        ct = to_host(outs_d[b]).reshape(level - 1, 2, P.n)
+        dec = C.decrypt(P, S.sk, ct, 2.0 ** 40)
+        worst = max(worst, float(np.max(np.abs(dec.real - Y[r, b * Cc + s]))))
+    print(f"cfg4 max |decoded - fp64| over 48 blocks = {worst:.3e} (2^{np.log2(worst):.1f})")
+    assert worst <= 2.0 ** -15
