@@ -36,6 +36,41 @@ METRIC = "keyswitch/s + NTT GB/s at N=2^16, 24 limbs; encrypted 768×1536 matvec
 HBM_PEAK_GBS = 8000.0
 
 
+# HBM traffic of the roofline kernel (k_ptmac) per launch, from the committed
+# rocprofv3 FETCH_SIZE / WRITE_SIZE summary; valid only while the kernel's
+# sources are byte-identical to those the counters were taken on.
+PTMAC_PROFILE = os.path.join(ROOT, "profiles", "k_ptmac_projection_768x1536_n65536_l16.txt")
+PTMAC_SOURCES = [os.path.join(ROOT, "paper_2608_17442_amd", "csrc", f)
+                 for f in ("matvec.hip", "fesc_internal.hpp")]
+
+
+def kernel_sources_sha256(paths) -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for p in paths:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def profiled_traffic(profile: str, sources) -> int | None:
+    """Bytes per launch recorded in `profile`, or None if the file is missing
+    or the kernel sources changed since the counters were taken."""
+    if not os.path.exists(profile):
+        return None
+    fields = {}
+    for line in open(profile):
+        if ":" in line and line.startswith("# ") and not line.startswith("#   "):
+            k, v = line[2:].split(":", 1)
+            fields[k.strip()] = v.strip()
+    if fields.get("kernel_sources_sha256") != kernel_sources_sha256(sources):
+        return None
+    try:
+        return int(fields["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -324,7 +359,8 @@ def main():
         "roofline": {
             "bound": "hbm", "kernel": "k_ptmac (projection plaintext-diagonal MAC)",
             "achieved": round(ptmac_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(ptmac_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+            "frac": round(ptmac_gbs / HBM_PEAK_GBS, 4),
+            "traffic": profiled_traffic(PTMAC_PROFILE, PTMAC_SOURCES),
             "algorithmic_bytes": ptmac_bytes,
         },
         "rooflines_other": {

@@ -16,6 +16,11 @@
 // (alpha, dnum) with clamped indices instead of bounds branches, so that all
 // loads of a loop are issued together.
 //
+// The transforms around these kernels carry two more steps of the pipeline
+// (ntt.hip): the inverse NTT of the sources reads the callers' ciphertexts
+// directly (no gather copy), and the forward NTT of the ModDown conversion y
+// ends in the combine (acc - y) * P^-1 + sigma_g(c0) that writes the outputs.
+//
 // Extended basis at level l: rows 0..l-1 are q_0..q_{l-1}, rows l..l+alpha-1
 // are p_0..p_{alpha-1} (extended prime index L + k).
 #include "fesc_internal.hpp"
@@ -70,17 +75,6 @@ __device__ __forceinline__ void conv_row(const double (&x0)[A], const double (&x
   o.x = to_res(s0, M.q, M.qinv);
   o.y = to_res(s1, M.q, M.qinv);
   *reinterpret_cast<ulonglong2*>(dst) = o;
-}
-
-// cc[s][i][k] = src s row i (evaluation form, rows at in + i*stride).
-__global__ __launch_bounds__(kThreads) void k_gather(KsTable tab, uint64_t* __restrict__ cc,
-                                                     uint32_t level, uint32_t n) {
-  const uint32_t i = blockIdx.y, s = blockIdx.z;
-  const uint32_t k = 2 * (blockIdx.x * kThreads + threadIdx.x);
-  if (k >= n) return;
-  const ulonglong2 v =
-      *reinterpret_cast<const ulonglong2*>(tab.src_in[s] + (size_t)i * tab.src_stride[s] + k);
-  *reinterpret_cast<ulonglong2*>(cc + ((size_t)s * level + i) * n + k) = v;
 }
 
 // ModUp: coefficient-form rows cc[s][0..level) -> ext[s][j][row] for every
@@ -196,35 +190,6 @@ __global__ __launch_bounds__(kThreads) void k_moddown_bconv(const uint64_t* __re
     conv_row<A>(x0, x1, md_hat + (size_t)i * A, pk[i], y + ((size_t)u * level + i) * n + k);
 }
 
-// out_job[i][t] = (acc[u][i] - y[u][i]) * P^-1
-//               + add_job[i][t][src(k)]   if bit t of add_mask_job
-//               + add2_job[i][t][k]       if add2_job != null
-// u = 2*job + t = blockIdx.z.
-__global__ __launch_bounds__(kThreads) void k_ks_combine(KsTable tab,
-                                                         const uint64_t* __restrict__ acc,
-                                                         const uint64_t* __restrict__ y,
-                                                         uint32_t level, uint32_t alpha,
-                                                         uint32_t log_n,
-                                                         const PrimeK* __restrict__ pk,
-                                                         const double2* __restrict__ pinv) {
-  const uint32_t n = 1u << log_n;
-  const uint32_t i = blockIdx.y, u = blockIdx.z, job = u >> 1, t = u & 1;
-  const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
-  if (k >= n) return;
-  const uint32_t E = level + alpha;
-  const PrimeK M = pk[i];
-  const double2 f = pinv[i];
-  const double d = u2d(acc[((size_t)u * E + i) * n + k]) - u2d(y[((size_t)u * level + i) * n + k]);
-  double v = mm_shoup(d, f.x, f.y, M.q);
-  const size_t o = ((size_t)2 * i + t) * n;
-  if ((tab.add_mask[job] >> t) & 1u) {
-    const uint32_t g = tab.add_galois[job];
-    v += u2d(tab.add[job][o + (g ? galois_src(k, g, log_n) : k)]);
-  }
-  if (tab.add2[job]) v += u2d(tab.add2[job][o + k]);
-  tab.out[job][o + k] = to_res(v, M.q, M.qinv);
-}
-
 // Dispatch on a runtime value to a template instantiation 1..16.
 template <template <int> class K, typename... Args>
 void dispatch16(uint32_t a, Args&&... args) {
@@ -270,13 +235,6 @@ struct IpL {
 
 }  // namespace
 
-hipError_t k_gather_launch(const Context* c, const KsTable& tab, uint32_t nsrc, uint64_t* cc,
-                           uint32_t level, hipStream_t s) {
-  dim3 grid((c->n / 2 + kThreads - 1) / kThreads, level, nsrc);
-  hipLaunchKernelGGL(k_gather, grid, dim3(kThreads), 0, s, tab, cc, level, c->n);
-  return hipGetLastError();
-}
-
 hipError_t k_modup_launch(const Context* c, const LevelTables& T, const uint64_t* cc,
                           uint64_t* ext, uint32_t nsrc, uint32_t level, hipStream_t s) {
   const uint32_t dnum_l = (level + c->alpha - 1) / c->alpha;
@@ -303,15 +261,6 @@ hipError_t k_moddown_bconv_launch(const Context* c, const LevelTables& T, const 
   dim3 grid(xb, 2 * njobs, row_splits(xb * 2 * njobs, level));
   dispatch16<ModdownL>(c->alpha, grid, s, acc, y, level, c->L, c->n, c->d_pk, T.md_inv,
                        T.md_hat);
-  return hipGetLastError();
-}
-
-hipError_t k_ks_combine_launch(const Context* c, const LevelTables& T, const KsTable& tab,
-                               uint32_t njobs, const uint64_t* acc, const uint64_t* y,
-                               uint32_t level, hipStream_t s) {
-  dim3 grid((c->n + kThreads - 1) / kThreads, level, 2 * njobs);
-  hipLaunchKernelGGL(k_ks_combine, grid, dim3(kThreads), 0, s, tab, acc, y, level, c->alpha,
-                     c->log_n, c->d_pk, T.md_pinv);
   return hipGetLastError();
 }
 

@@ -52,9 +52,6 @@ struct KsTable {
   uint32_t add_galois[kMaxBatch];     // job: permutation of `add` (0: none)
 };
 
-hipError_t k_gather_launch(const Context* c, const KsTable& tab, uint32_t nsrc, uint64_t* cc,
-                           uint32_t level, hipStream_t s);
-
 // ntt.hip: fused transforms of the key-switch pipeline
 hipError_t launch_ntt_inv_sources(const Context* c, const KsTable& tab, uint32_t nsrc,
                                   uint64_t* cc, uint32_t level, hipStream_t s);
@@ -67,9 +64,6 @@ hipError_t k_ip_launch(const Context* c, const KsTable& tab, uint32_t njobs, con
                        uint64_t* acc, uint32_t level, hipStream_t s);
 hipError_t k_moddown_bconv_launch(const Context* c, const LevelTables& T, const uint64_t* acc,
                                   uint64_t* y, uint32_t njobs, uint32_t level, hipStream_t s);
-hipError_t k_ks_combine_launch(const Context* c, const LevelTables& T, const KsTable& tab,
-                               uint32_t njobs, const uint64_t* acc, const uint64_t* y,
-                               uint32_t level, hipStream_t s);
 
 // ------------------------------------------------------------------ ops.cpp
 const LevelTables* level_tables(Context* c, uint32_t level, int* err);
