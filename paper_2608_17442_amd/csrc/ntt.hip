@@ -234,29 +234,16 @@ __global__ __launch_bounds__(kThreads) void k_inv_outer(RowSel rs, uint32_t log_
 
 // ------------------------------------------------------------- inner pass
 
-// Forward 4096-point blocks.  Thread t starts with values t + 256 r (bits
-// 11..8 in registers), moves to a*256 + 16 r + b (a = t/16, b = t%16; bits
-// 7..4) and to 16 t + r (bits 3..0), and is handed back values t + 256 r for
-// the epilogue.  Each transpose writes exactly the LDS words the thread read
-// in the previous one, so only the reads need a barrier.
-//
-// SINGLE: N = 4096, the pass reads uint64 residues; otherwise it reads the
-// outer pass's fp64 intermediate.
-template <bool SINGLE, class Epi>
-__global__ __launch_bounds__(kThreads) void k_fwd_inner(RowSel rs, uint32_t log_n,
-                                                        const PrimeK* __restrict__ pk,
-                                                        const double2* __restrict__ twf,
-                                                        const double* __restrict__ tw3, Epi epi) {
-  __shared__ double lds[kLds];
-  if (rs.skip()) return;
-  const uint32_t n = 1u << log_n;
-  const uint32_t prime = rs.prime();
-  const double q = pk[prime].q, qinv = pk[prime].qinv;
-  const double2* tw = twf + (size_t)prime * n;
-  uint64_t* row = rs.row();
+// The last 12 forward stages on block B (offset of its first value) of
+// `row`: on return thread t holds the values at block positions 16 t + r in
+// x[r].  Uses all of `lds`; the caller needs a barrier before touching it
+// again unless it only writes the words it is handed (positions 16 t + r).
+template <bool SINGLE>
+__device__ __forceinline__ void fwd_block(const uint64_t* row, uint32_t B, uint32_t n,
+                                          const double2* tw, const double* s3, double q,
+                                          double qinv, double* lds, double (&x)[16]) {
   const uint32_t t = threadIdx.x, a = t >> 4, b = t & 15;
-  const uint32_t B = blockIdx.x * kBlock, nb = n + B;
-  double x[16];
+  const uint32_t nb = n + B;
   if constexpr (SINGLE) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) x[r] = u2d(row[B + t + 256 * r]);
@@ -286,11 +273,37 @@ __global__ __launch_bounds__(kThreads) void k_fwd_inner(RowSel rs, uint32_t log_
 #pragma unroll
   for (int r = 0; r < 16; ++r) x[r] = lds[lds_col(t, r)];
   // bits 3..0
-  const double* s3 = tw3 + ((size_t)prime * (n / kBlock) + blockIdx.x) * (15 * kThreads) + t;
   ct_st<8, true>(x, TwLo<8>{s3, qinv}, q, qinv);
   ct_st<4, false>(x, TwLo<4>{s3, qinv}, q, qinv);
   ct_st<2, true>(x, TwLo<2>{s3, qinv}, q, qinv);
   ct_st<1, false>(x, TwLo<1>{s3, qinv}, q, qinv);
+}
+
+// Forward 4096-point blocks.  Thread t starts with values t + 256 r (bits
+// 11..8 in registers), moves to a*256 + 16 r + b (a = t/16, b = t%16; bits
+// 7..4) and to 16 t + r (bits 3..0); fwd_block ends there.  Each transpose
+// writes exactly the LDS words the thread read in the previous one, so only
+// the reads need a barrier.  The kernel hands values t + 256 r to the
+// epilogue.
+//
+// SINGLE: N = 4096, the pass reads uint64 residues; otherwise it reads the
+// outer pass's fp64 intermediate.
+template <bool SINGLE, class Epi>
+__global__ __launch_bounds__(kThreads) void k_fwd_inner(RowSel rs, uint32_t log_n,
+                                                        const PrimeK* __restrict__ pk,
+                                                        const double2* __restrict__ twf,
+                                                        const double* __restrict__ tw3, Epi epi) {
+  __shared__ double lds[kLds];
+  if (rs.skip()) return;
+  const uint32_t n = 1u << log_n;
+  const uint32_t prime = rs.prime();
+  const double q = pk[prime].q, qinv = pk[prime].qinv;
+  uint64_t* row = rs.row();
+  const uint32_t t = threadIdx.x;
+  const uint32_t B = blockIdx.x * kBlock;
+  const double* s3 = tw3 + ((size_t)prime * (n / kBlock) + blockIdx.x) * (15 * kThreads) + t;
+  double x[16];
+  fwd_block<SINGLE>(row, B, n, twf + (size_t)prime * n, s3, q, qinv, lds, x);
 #pragma unroll
   for (int r = 0; r < 16; ++r) lds[lds_col(t, r)] = x[r];
   __syncthreads();

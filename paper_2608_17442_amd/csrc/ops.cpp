@@ -175,6 +175,8 @@ int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& sr
   // ModUp of every source (the scratch capacity covers all of them)
   const uint32_t ns = (uint32_t)srcs.size();
   if (ns > S.cap) return fail(FESC_ERR_ARG, "key-switch sources exceed the scratch capacity");
+  for (const KsJob& J : jobs)
+    if (J.src >= ns) return fail(FESC_ERR_ARG, "key-switch job names a missing source");
   HIPCK(launch_ntt_inv_sources(c, tab, ns, S.cc, level, s));
   HIPCK(k_modup_launch(c, *T, S.cc, S.ext, ns, level, s));
   RowSel rs{S.ext, (size_t)E * n, n, 0, level, c->L, c->alpha, level, dnum_l};
