@@ -276,6 +276,21 @@ int fesc_scan_contract(fesc_ctx* ctx, const uint64_t* const* h, const uint64_t* 
 int fesc_encode(uint32_t log_n, const double* re, const double* im, double scale,
                 int64_t* coeffs);
 
+/* Measurement helper, not part of the method: runs the register-resident
+ * arithmetic of the library's inner loops on every compute unit of the
+ * context's device with no memory traffic and stores the measured rate in
+ * *rate (operations per second).  kind FESC_CALIB_CT: forward NTT
+ * butterflies (radix-2 Cooley-Tukey with the transform's lazy reduction);
+ * FESC_CALIB_GS: inverse NTT butterflies (Gentleman-Sande); FESC_CALIB_MAC:
+ * modular multiply-accumulates as in basis conversion and the key inner
+ * product (reduced after every four terms).  Each thread runs `iters`
+ * iterations (1 .. 2^20) of 32 butterflies or 8 MACs.  Synchronises `stream`;
+ * uses context scratch; FESC_ERR_ARG for a bad kind or count. */
+#define FESC_CALIB_CT 0
+#define FESC_CALIB_GS 1
+#define FESC_CALIB_MAC 2
+int fesc_calib_valu(fesc_ctx* ctx, int kind, uint32_t iters, double* rate, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

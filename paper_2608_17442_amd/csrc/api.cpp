@@ -106,6 +106,7 @@ int op_scan_contract(Context* c, const uint64_t* const* h, const uint64_t* const
                      const uint64_t* const* cfac, uint32_t K, uint32_t d_s,
                      uint64_t* const* out, uint32_t level, hipStream_t s);
 int encode(uint32_t log_n, const double* re, const double* im, double scale, int64_t* out);
+int calib_valu(Context* c, int kind, uint32_t iters, double* rate, hipStream_t s);
 }  // namespace fesc
 
 #include "ops.hpp"
@@ -284,6 +285,11 @@ int fesc_scan_contract(fesc_ctx* ctx, const uint64_t* const* h, const uint64_t* 
   if (chunks >= 2 && !ctx->keys.count(2 * ctx->n - 1))
     return fail(FESC_ERR_NO_KEY, "no conjugation key");
   return op_scan_contract(ctx, h, decay, cfac, chunks, d_state, out, level, S(stream));
+}
+
+int fesc_calib_valu(fesc_ctx* ctx, int kind, uint32_t iters, double* rate, void* stream) {
+  if (!ctx || !rate) return fail(FESC_ERR_ARG, "null argument");
+  return calib_valu(ctx, kind, iters, rate, S(stream));
 }
 
 }  // extern "C"

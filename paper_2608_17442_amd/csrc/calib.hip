@@ -1,0 +1,135 @@
+// VALU calibration: the register-resident arithmetic of the NTT stages and of
+// the modular multiply-accumulate sums (basis conversion, key inner product),
+// run on every compute unit with no memory traffic.  The measured rates are
+// the compute roof against which the transforms and key switching are
+// reported; they are not part of the method.
+#include <cmath>
+
+#include "butterfly.hpp"
+#include "fesc_internal.hpp"
+
+namespace fesc {
+
+namespace {
+
+constexpr int kThreads = 256;
+
+// The 15 twiddles of one radix-16 step (1 + 2 + 4 + 8 groups), uniform.
+struct Tw15 {
+  double2 w[15];
+};
+template <int OFF>
+struct TwArg {
+  const Tw15* t;
+  __device__ __forceinline__ double2 operator()(int gi) const { return t->w[OFF + gi]; }
+};
+
+// One radix-16 step (four radix-2 stages, 32 butterflies per thread) per
+// iteration, forward (CT) or inverse (GS), with the kernels' lazy reduction
+// pattern.
+template <bool INV>
+__global__ __launch_bounds__(kThreads) void k_calib_bfly(Tw15 tw, double q, double qinv,
+                                                         uint32_t iters, double* out) {
+  const uint32_t t = blockIdx.x * kThreads + threadIdx.x;
+  double x[16];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) x[r] = (double)((t * 16u + r) % 1000003u);
+  for (uint32_t i = 0; i < iters; ++i) {
+    if constexpr (INV) {
+      gs_st<1, true>(x, TwArg<7>{&tw}, q, qinv);
+      gs_st<2, false>(x, TwArg<3>{&tw}, q, qinv);
+      gs_st<4, true>(x, TwArg<1>{&tw}, q, qinv);
+      gs_st<8, false>(x, TwArg<0>{&tw}, q, qinv);
+    } else {
+      ct_st<8, true>(x, TwArg<0>{&tw}, q, qinv);
+      ct_st<4, false>(x, TwArg<1>{&tw}, q, qinv);
+      ct_st<2, true>(x, TwArg<3>{&tw}, q, qinv);
+      ct_st<1, false>(x, TwArg<7>{&tw}, q, qinv);
+    }
+  }
+  double s = 0.0;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) s += x[r];
+  out[t] = s;
+}
+
+// Eight independent sums of products x_j * y_j mod q (per-lane operands),
+// reduced after every four terms as the basis-conversion and inner-product
+// kernels do: 8 MACs per thread per iteration.
+__global__ __launch_bounds__(kThreads) void k_calib_mac(double q, double qinv, uint32_t iters,
+                                                        double* out) {
+  const uint32_t t = blockIdx.x * kThreads + threadIdx.x;
+  double x[8], y[8], acc[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    x[j] = (double)((t * 8u + j) % 1000003u);
+    y[j] = (double)((t * 131u + 7u * j) % 999983u);
+    acc[j] = 0.0;
+  }
+  for (uint32_t i = 0; i < iters; ++i) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] += mm_var(x[j], y[j], q, qinv);
+    if ((i & 3) == 3) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[j] = red_bal(acc[j], q, qinv);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) x[j] = acc[j];  // carry a dependency into the next term
+  }
+  double s = 0.0;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) s += acc[j];
+  out[t] = s;
+}
+
+}  // namespace
+
+int calib_valu(Context* c, int kind, uint32_t iters, double* rate, hipStream_t s) {
+  if (kind < FESC_CALIB_CT || kind > FESC_CALIB_MAC || iters == 0 || iters > (1u << 20))
+    return fail(FESC_ERR_ARG, "bad calibration arguments");
+  int cus = 0;
+  if (int rc = hip_check(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount,
+                                               c->device), "hipDeviceGetAttribute"))
+    return rc;
+  const uint32_t blocks = (uint32_t)cus * 8;
+  int err;
+  double* out = static_cast<double*>(scratch_get(c, sizeof(double) * blocks * kThreads, &err));
+  if (!out) return err;
+  const double q = (double)c->primes[0], qinv = 1.0 / q;
+  Tw15 tw;
+  for (int i = 0; i < 15; ++i) {
+    const double w = std::floor(q / (3.0 + i));
+    tw.w[i] = double2{w, w / q};
+  }
+  hipEvent_t e0, e1;
+  if (int rc = hip_check(hipEventCreate(&e0), "hipEventCreate")) return rc;
+  if (int rc = hip_check(hipEventCreate(&e1), "hipEventCreate")) {
+    hipEventDestroy(e0);
+    return rc;
+  }
+  auto launch = [&]() {
+    if (kind == FESC_CALIB_CT)
+      hipLaunchKernelGGL(k_calib_bfly<false>, dim3(blocks), dim3(kThreads), 0, s, tw, q, qinv,
+                         iters, out);
+    else if (kind == FESC_CALIB_GS)
+      hipLaunchKernelGGL(k_calib_bfly<true>, dim3(blocks), dim3(kThreads), 0, s, tw, q, qinv,
+                         iters, out);
+    else
+      hipLaunchKernelGGL(k_calib_mac, dim3(blocks), dim3(kThreads), 0, s, q, qinv, iters, out);
+  };
+  launch();  // warm-up
+  hipEventRecord(e0, s);
+  launch();
+  hipEventRecord(e1, s);
+  int rc = hip_check(hipEventSynchronize(e1), "hipEventSynchronize");
+  float ms = 0.f;
+  if (!rc) rc = hip_check(hipEventElapsedTime(&ms, e0, e1), "hipEventElapsedTime");
+  hipEventDestroy(e0);
+  hipEventDestroy(e1);
+  if (rc) return rc;
+  const double per_thread = kind == FESC_CALIB_MAC ? 8.0 * iters : 32.0 * iters;
+  *rate = (double)blocks * kThreads * per_thread / (ms * 1e-3);
+  return FESC_OK;
+}
+
+}  // namespace fesc

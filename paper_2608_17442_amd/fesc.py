@@ -60,9 +60,11 @@ _SIGS = {
     "fesc_encode": [_u32, _vp, _vp, ctypes.c_double, _vp],
     "fesc_scan_contract": [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp), ctypes.POINTER(_vp),
                            _u32, _u32, ctypes.POINTER(_vp), _u32, _vp],
+    "fesc_calib_valu": [_vp, ctypes.c_int, _u32, ctypes.POINTER(ctypes.c_double), _vp],
 }
 
 CONJ = -(2 ** 31)
+CALIB_CT, CALIB_GS, CALIB_MAC = 0, 1, 2
 
 for _name, _args in _SIGS.items():
     _f = getattr(_lib, _name)
@@ -222,6 +224,13 @@ class Context:
 
     def key_words(self) -> int:
         return self.dnum * (self.L + self.alpha) * 2 * self.n
+
+    def calib_valu(self, kind: int, iters: int = 4096, stream=None) -> float:
+        """Measured register-resident rate (operations/s) of NTT butterflies
+        (CALIB_CT, CALIB_GS) or modular multiply-accumulates (CALIB_MAC)."""
+        r = ctypes.c_double()
+        _check(_lib.fesc_calib_valu(self._h, kind, iters, ctypes.byref(r), _stream(stream)))
+        return float(r.value)
 
 
 def encode(log_n: int, z, scale: float):

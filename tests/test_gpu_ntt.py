@@ -145,3 +145,20 @@ def test_cfg2_full_size():
     ctx.ntt_inv(d, B, Lm * n, Lm, n, 0)
     back = to_host(d)
     assert np.array_equal(back, A), first_mismatch(back, A)
+
+
+def test_calib_valu_rates_are_positive_and_ordered():
+    """The VALU calibration helper runs all three kernels and reports finite
+    rates; a radix-2 butterfly (one modular product, lazily reduced sum and
+    difference) cannot be cheaper than about a third of a multiply-accumulate
+    and both stay below the device's fp64 instruction rate."""
+    from paper_2608_17442_amd import fesc as F
+    P = C.params_small(12, 36, 3, 1)
+    ctx = F.Context(P.log_n, P.q, P.p)
+    step("calib valu")
+    r = {k: ctx.calib_valu(k, 256) for k in (F.CALIB_CT, F.CALIB_GS, F.CALIB_MAC)}
+    print({k: f"{v / 1e12:.3f} T/s" for k, v in r.items()})
+    for v in r.values():
+        assert np.isfinite(v) and 1e9 < v < 1e14
+    with pytest.raises(F.FescError):
+        ctx.calib_valu(7, 16)
