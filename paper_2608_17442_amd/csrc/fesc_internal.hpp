@@ -109,6 +109,8 @@ struct LevelTables {
   double2* md_pinv = nullptr;  // [level]                   P^-1 mod q_i
   double2* pmod = nullptr;     // [L]                       P mod q_i
   double2* rs_inv = nullptr;   // [level]                   q_{level-1}^-1 mod q_i
+  double2* mu_inv_n = nullptr; // [level]  N^-1 (Q_D/q_i)^-1 mod q_i (q_i in digit D)
+  double2* md_inv_n = nullptr; // [alpha]  N^-1 (P/p_k)^-1 mod p_k
 };
 
 struct Context {

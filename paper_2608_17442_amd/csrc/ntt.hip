@@ -148,12 +148,34 @@ __global__ __launch_bounds__(kThreads) void k_fwd_outer(RowSel rs, uint32_t log_
     for (int m = 0; m < M; ++m) rowd[c0 + kThreads * j + kBlock * m] = x[j * M + m];
 }
 
+// Final store of an inverse transform: N^-1 x as a canonical uint64 residue.
+struct InvCanon {
+  __device__ __forceinline__ void operator()(uint64_t* row, uint32_t k, double x,
+                                             const PrimeK& P) const {
+    row[k] = to_res(mm_shoup(x, P.ninv, P.ninvp, P.q), P.q, P.qinv);
+  }
+};
+
+// Final store of an inverse transform that feeds a fast basis conversion: the
+// centred digit [N^-1 f_i x]_q in (-q/2, q/2), stored as fp64 in place of the
+// residue.  f holds {N^-1 f_i mod q_i, /q_i} per limb i (blockIdx.z), where
+// f_i is the conversion's (Q_D/q_i)^-1.
+struct InvDigit {
+  const double2* f;
+  __device__ __forceinline__ void operator()(uint64_t* row, uint32_t k, double x,
+                                             const PrimeK& P) const {
+    const double2 c = f[blockIdx.z];
+    reinterpret_cast<double*>(row)[k] =
+        center(red_full(mm_shoup(x, c.x, c.y, P.q), P.q, P.qinv), P.q);
+  }
+};
+
 // Inverse: stages in reverse order (every other one reducing, as in gs_st),
-// then N^-1 and canonical uint64 residues.
-template <int LOGM>
+// then the final store (N^-1 scaling included).
+template <int LOGM, class St>
 __global__ __launch_bounds__(kThreads) void k_inv_outer(RowSel rs, uint32_t log_n,
                                                         const PrimeK* __restrict__ pk,
-                                                        const double2* __restrict__ twi) {
+                                                        const double2* __restrict__ twi, St st) {
   constexpr int M = 1 << LOGM, C = 16 / M;
   if (rs.skip()) return;
   const uint32_t n = 1u << log_n;
@@ -186,10 +208,157 @@ __global__ __launch_bounds__(kThreads) void k_inv_outer(RowSel rs, uint32_t log_
 #pragma unroll
   for (int j = 0; j < C; ++j)
 #pragma unroll
-    for (int m = 0; m < M; ++m)
-      row[c0 + kThreads * j + kBlock * m] =
-          to_res(mm_shoup(x[j * M + m], P.ninv, P.ninvp, P.q), P.q, P.qinv);
+    for (int m = 0; m < M; ++m) st(row, c0 + kThreads * j + kBlock * m, x[j * M + m], P);
 }
+
+// ------------------------------------------ basis conversion + outer pass
+
+// Fused fast basis conversion and first forward pass.  For group g
+// (blockIdx.z) and targets t = T blockIdx.y .. T blockIdx.y + T - 1 of the
+// map, value k of target row t (prime m) is
+//     y_k = sum_{a < aj} x_a[k] * hat_a  mod m,
+// x_a the centred digits stored by the inverse transform (InvDigit, fp64).
+// The first log M forward stages then run on the thread's columns exactly as
+// in k_fwd_outer and the fp64 intermediate is stored; for M = 1 (no outer
+// pass) the canonical residue is stored instead.  Targets vary fastest after
+// the column block, so all targets of a column block run together and read
+// its digit rows from L2; with M a multiple of 8 a column block also stays on
+// one XCD (workgroups are dealt to the 8 XCDs round-robin).
+template <int LOGM, int T, class Map>
+__global__ __launch_bounds__(kThreads) void k_bconv_outer(Map map, uint32_t log_n,
+                                                          const PrimeK* __restrict__ pk,
+                                                          const double2* __restrict__ twf) {
+  constexpr int M = 1 << LOGM, C = 16 / M;
+  const uint32_t g = blockIdx.z, t0 = blockIdx.y * T;
+  const uint32_t nt = map.targets(g);
+  if (t0 >= nt) return;
+  const uint32_t n = 1u << log_n;
+  const uint32_t aj = map.aj(g);
+  uint32_t prime[T];
+  const double2* hat[T];
+#pragma unroll
+  for (int i = 0; i < T; ++i) {
+    const uint32_t row = map.row(g, min(t0 + i, nt - 1));
+    prime[i] = map.prime(row);
+    hat[i] = map.hat(g, row);
+  }
+  const double* dig = map.digits(g);
+  const uint32_t c0 = blockIdx.x * (kThreads * C) + threadIdx.x;
+  double y[T][16];
+#pragma unroll
+  for (int i = 0; i < T; ++i)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) y[i][v] = 0.0;
+  // |x_a| < 2^49 and hat_a < m: each Shoup product lies within 0.625 m, so
+  // eight terms and a carried reduced sum stay below 2^53
+  for (uint32_t a = 0; a < map.alpha; ++a) {
+    const uint32_t ac = a < aj ? a : aj - 1;
+    const double* da = dig + (size_t)ac * n + c0;
+    double x[16];
+#pragma unroll
+    for (int j = 0; j < C; ++j)
+#pragma unroll
+      for (int m = 0; m < M; ++m) x[j * M + m] = da[kThreads * j + kBlock * m];
+#pragma unroll
+    for (int i = 0; i < T; ++i) {
+      const double q = pk[prime[i]].q;
+      const double2 h = a < aj ? hat[i][ac] : double2{0.0, 0.0};
+#pragma unroll
+      for (int v = 0; v < 16; ++v) y[i][v] += mm_shoup(x[v], h.x, h.y, q);
+    }
+    if ((a & 7) == 7) {
+#pragma unroll
+      for (int i = 0; i < T; ++i) {
+        const double q = pk[prime[i]].q, qinv = pk[prime[i]].qinv;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) y[i][v] = red_bal(y[i][v], q, qinv);
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < T; ++i) {
+    if (t0 + i >= nt) break;
+    const uint32_t row = map.row(g, t0 + i);
+    const double q = pk[prime[i]].q, qinv = pk[prime[i]].qinv;
+    uint64_t* out = map.out(g, row);
+    double (&x)[16] = y[i];
+    if constexpr (LOGM == 0) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) out[c0 + kThreads * v] = to_res(x[v], q, qinv);
+    } else {
+      const double2* tw = twf + (size_t)prime[i] * n;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) x[v] = red_bal(x[v], q, qinv);
+#pragma unroll
+      for (int s = 0; s < LOGM; ++s) {
+        const int H = M >> (s + 1);
+#pragma unroll
+        for (int m = 0; m < M; ++m) {
+          if (m & H) continue;
+          const double2 w = tw[(1 << s) + (m >> (LOGM - s))];
+#pragma unroll
+          for (int j = 0; j < C; ++j) {
+            const double u = (s % 2 == 0) ? red_bal(x[j * M + m], q, qinv) : x[j * M + m];
+            const double v = mm_shoup(x[j * M + m + H], w.x, w.y, q);
+            x[j * M + m] = u + v;
+            x[j * M + m + H] = u - v;
+          }
+        }
+      }
+      double* outd = reinterpret_cast<double*>(out);
+#pragma unroll
+      for (int j = 0; j < C; ++j)
+#pragma unroll
+        for (int m = 0; m < M; ++m) outd[c0 + kThreads * j + kBlock * m] = x[j * M + m];
+    }
+  }
+}
+
+// ModUp: group g = s * dnum + j (source s, digit j = primes [lo, lo + aj)),
+// targets = the extended rows outside the digit, digits = cc[s][lo ..].
+struct ModupMap {
+  const double* cc;
+  uint64_t* ext;
+  const double2* mu_hat;
+  uint32_t level, L, alpha, dnum_l, n;
+  __device__ uint32_t lo(uint32_t g) const { return (g % dnum_l) * alpha; }
+  __device__ uint32_t aj(uint32_t g) const { return min(alpha, level - lo(g)); }
+  __device__ uint32_t targets(uint32_t g) const { return level + alpha - aj(g); }
+  __device__ uint32_t row(uint32_t g, uint32_t t) const {
+    const uint32_t l = lo(g);
+    return t < l ? t : t + aj(g);
+  }
+  __device__ uint32_t prime(uint32_t r) const { return r < level ? r : L + (r - level); }
+  __device__ const double* digits(uint32_t g) const {
+    return cc + ((size_t)(g / dnum_l) * level + lo(g)) * n;
+  }
+  __device__ const double2* hat(uint32_t g, uint32_t r) const {
+    return mu_hat + ((size_t)(g % dnum_l) * (level + alpha) + r) * alpha;
+  }
+  __device__ uint64_t* out(uint32_t g, uint32_t r) const {
+    return ext + ((size_t)g * (level + alpha) + r) * n;
+  }
+};
+
+// ModDown: group g = 2 * job + component, digits = the alpha special-prime
+// rows of acc[g], targets = the level rows of y[g].
+struct ModdownMap {
+  const uint64_t* acc;
+  uint64_t* y;
+  const double2* md_hat;
+  uint32_t level, alpha, n;
+  __device__ uint32_t aj(uint32_t) const { return alpha; }
+  __device__ uint32_t targets(uint32_t) const { return level; }
+  __device__ uint32_t row(uint32_t, uint32_t t) const { return t; }
+  __device__ uint32_t prime(uint32_t r) const { return r; }
+  __device__ const double* digits(uint32_t g) const {
+    return reinterpret_cast<const double*>(acc + ((size_t)g * (level + alpha) + level) * n);
+  }
+  __device__ const double2* hat(uint32_t, uint32_t r) const { return md_hat + (size_t)r * alpha; }
+  __device__ uint64_t* out(uint32_t g, uint32_t r) const {
+    return y + ((size_t)g * level + r) * n;
+  }
+};
 
 // ------------------------------------------------------------- inner pass
 
@@ -296,12 +465,13 @@ struct LoadSources {
 
 // Inverse 4096-point blocks: the mirror image of k_fwd_inner.  Reads uint64
 // residues (16 consecutive values per thread), writes fp64 for the outer pass
-// or, if SINGLE, the scaled canonical residues.
-template <bool SINGLE, class Ld>
+// or, if SINGLE, applies the final store St.
+template <bool SINGLE, class Ld, class St>
 __global__ __launch_bounds__(kThreads) void k_inv_inner(RowSel rs, uint32_t log_n,
                                                         const PrimeK* __restrict__ pk,
                                                         const double2* __restrict__ twi,
-                                                        const double* __restrict__ tw3, Ld ld) {
+                                                        const double* __restrict__ tw3, Ld ld,
+                                                        St st) {
   __shared__ double lds[kLds];
   if (rs.skip()) return;
   const uint32_t n = 1u << log_n;
@@ -348,8 +518,7 @@ __global__ __launch_bounds__(kThreads) void k_inv_inner(RowSel rs, uint32_t log_
   gs_st<8, false>(x, TwHi{tw, nb >> 12}, q, qinv);
   if constexpr (SINGLE) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r)
-      row[B + t + 256 * r] = to_res(mm_shoup(x[r], P.ninv, P.ninvp, q), q, qinv);
+    for (int r = 0; r < 16; ++r) st(row, B + t + 256 * r, x[r], P);
   } else {
     double* dst = reinterpret_cast<double*>(row) + B + t;
 #pragma unroll
@@ -393,94 +562,150 @@ struct KsCombine {
 
 namespace {
 
-static hipError_t launch_outer_pass(const Context* c, const RowSel& rs, uint32_t batch,
-                                    uint32_t limbs, bool inverse, hipStream_t s) {
-  if (c->log_n == 12) return hipSuccess;
-  const double2* tw = inverse ? c->d_tw_inv : c->d_tw_fwd;
+hipError_t launch_fwd_outer(const Context* c, const RowSel& rs, uint32_t batch, uint32_t limbs,
+                            hipStream_t s) {
   const dim3 grid(c->n / kBlock, batch, limbs), blk(kThreads);
-#define FESC_OUTER(L)                                                                \
-  if (inverse)                                                                       \
-    hipLaunchKernelGGL(k_inv_outer<L>, grid, blk, 0, s, rs, c->log_n, c->d_pk, tw);  \
-  else                                                                               \
-    hipLaunchKernelGGL(k_fwd_outer<L>, grid, blk, 0, s, rs, c->log_n, c->d_pk, tw);  \
-  break;
+  const double2* tw = c->d_tw_fwd;
   switch (c->log_n) {
-    case 13: FESC_OUTER(1)
-    case 14: FESC_OUTER(2)
-    case 15: FESC_OUTER(3)
-    case 16: FESC_OUTER(4)
+    case 12: return hipSuccess;
+    case 13: hipLaunchKernelGGL(k_fwd_outer<1>, grid, blk, 0, s, rs, c->log_n, c->d_pk, tw); break;
+    case 14: hipLaunchKernelGGL(k_fwd_outer<2>, grid, blk, 0, s, rs, c->log_n, c->d_pk, tw); break;
+    case 15: hipLaunchKernelGGL(k_fwd_outer<3>, grid, blk, 0, s, rs, c->log_n, c->d_pk, tw); break;
+    case 16: hipLaunchKernelGGL(k_fwd_outer<4>, grid, blk, 0, s, rs, c->log_n, c->d_pk, tw); break;
     default: return hipErrorInvalidValue;
   }
-#undef FESC_OUTER
+  return hipGetLastError();
+}
+
+template <class St>
+hipError_t launch_inv_outer(const Context* c, const RowSel& rs, uint32_t batch, uint32_t limbs,
+                            const St& st, hipStream_t s) {
+  const dim3 grid(c->n / kBlock, batch, limbs), blk(kThreads);
+  const double2* tw = c->d_tw_inv;
+  switch (c->log_n) {
+    case 12: return hipSuccess;
+    case 13: k_inv_outer<1, St><<<grid, blk, 0, s>>>(rs, c->log_n, c->d_pk, tw, st); break;
+    case 14: k_inv_outer<2, St><<<grid, blk, 0, s>>>(rs, c->log_n, c->d_pk, tw, st); break;
+    case 15: k_inv_outer<3, St><<<grid, blk, 0, s>>>(rs, c->log_n, c->d_pk, tw, st); break;
+    case 16: k_inv_outer<4, St><<<grid, blk, 0, s>>>(rs, c->log_n, c->d_pk, tw, st); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
 template <class Epi>
-void launch_fwd_inner(const Context* c, const RowSel& rs, uint32_t batch, uint32_t limbs,
-                      const Epi& epi, hipStream_t s) {
+hipError_t launch_fwd_inner(const Context* c, const RowSel& rs, uint32_t batch, uint32_t limbs,
+                            const Epi& epi, hipStream_t s) {
   const dim3 grid(c->n / kBlock, batch, limbs), blk(kThreads);
   if (c->log_n == 12)
-    k_fwd_inner<true, Epi><<<grid, blk, 0, s>>>(rs, c->log_n, c->d_pk,
-                       c->d_tw_fwd, c->d_tw3_fwd, epi);
+    k_fwd_inner<true, Epi><<<grid, blk, 0, s>>>(rs, c->log_n, c->d_pk, c->d_tw_fwd,
+                                                 c->d_tw3_fwd, epi);
   else
-    k_fwd_inner<false, Epi><<<grid, blk, 0, s>>>(rs, c->log_n, c->d_pk,
-                       c->d_tw_fwd, c->d_tw3_fwd, epi);
+    k_fwd_inner<false, Epi><<<grid, blk, 0, s>>>(rs, c->log_n, c->d_pk, c->d_tw_fwd,
+                                                  c->d_tw3_fwd, epi);
+  return hipGetLastError();
 }
 
-template <class Ld>
-void launch_inv_inner(const Context* c, const RowSel& rs, uint32_t batch, uint32_t limbs,
-                      const Ld& ld, hipStream_t s) {
+// Inverse transform: inner pass (reading through Ld), then the outer pass; St
+// is the final store of whichever pass is last.
+template <class Ld, class St>
+hipError_t launch_inverse(const Context* c, const RowSel& rs, uint32_t batch, uint32_t limbs,
+                          const Ld& ld, const St& st, hipStream_t s) {
   const dim3 grid(c->n / kBlock, batch, limbs), blk(kThreads);
   if (c->log_n == 12)
-    k_inv_inner<true, Ld><<<grid, blk, 0, s>>>(rs, c->log_n, c->d_pk,
-                       c->d_tw_inv, c->d_tw3_inv, ld);
+    k_inv_inner<true, Ld, St><<<grid, blk, 0, s>>>(rs, c->log_n, c->d_pk, c->d_tw_inv,
+                                                    c->d_tw3_inv, ld, st);
   else
-    k_inv_inner<false, Ld><<<grid, blk, 0, s>>>(rs, c->log_n, c->d_pk,
-                       c->d_tw_inv, c->d_tw3_inv, ld);
+    k_inv_inner<false, Ld, St><<<grid, blk, 0, s>>>(rs, c->log_n, c->d_pk, c->d_tw_inv,
+                                                     c->d_tw3_inv, ld, st);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_inv_outer(c, rs, batch, limbs, st, s);
+}
+
+constexpr int kBconvTargets = 3;
+
+template <class Map>
+hipError_t launch_bconv_outer(const Context* c, const Map& map, uint32_t targets, uint32_t groups,
+                              hipStream_t s) {
+  constexpr int T = kBconvTargets;
+  const dim3 grid(c->n / kBlock, (targets + T - 1) / T, groups), blk(kThreads);
+  const double2* tw = c->d_tw_fwd;
+  switch (c->log_n) {
+    case 12: k_bconv_outer<0, T, Map><<<grid, blk, 0, s>>>(map, c->log_n, c->d_pk, tw); break;
+    case 13: k_bconv_outer<1, T, Map><<<grid, blk, 0, s>>>(map, c->log_n, c->d_pk, tw); break;
+    case 14: k_bconv_outer<2, T, Map><<<grid, blk, 0, s>>>(map, c->log_n, c->d_pk, tw); break;
+    case 15: k_bconv_outer<3, T, Map><<<grid, blk, 0, s>>>(map, c->log_n, c->d_pk, tw); break;
+    case 16: k_bconv_outer<4, T, Map><<<grid, blk, 0, s>>>(map, c->log_n, c->d_pk, tw); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 }  // namespace
 
 // Inverse transform of the first `level` rows of each key-switch source into
-// cc[s][level][N] (out of place: the first pass reads the sources directly).
+// cc[s][level][N] (out of place: the first pass reads the sources directly),
+// stored as the centred ModUp digits [N^-1 (Q_D/q_i)^-1 x]_{q_i} (fp64);
+// f = LevelTables::mu_inv_n.
 hipError_t launch_ntt_inv_sources(const Context* c, const KsTable& tab, uint32_t nsrc,
-                                  uint64_t* cc, uint32_t level, hipStream_t s) {
+                                  uint64_t* cc, uint32_t level, const double2* f, hipStream_t s) {
   RowSel rs{cc, (size_t)level * c->n, (size_t)c->n, 0, level, 0, 0, 0, 0};
-  launch_inv_inner(c, rs, nsrc, level, LoadSources{tab}, s);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  return launch_outer_pass(c, rs, nsrc, level, true, s);
+  return launch_inverse(c, rs, nsrc, level, LoadSources{tab}, InvDigit{f}, s);
 }
 
-// Forward transform of the ModDown conversions y[2*njobs][level][N] with the
-// key-switch combine as the epilogue (writes the jobs' outputs; y keeps the
-// first pass's intermediate only).
+// Inverse transform of the rows rs selects (in place), stored as centred
+// digits [N^-1 f_i x]_{q_i} (fp64), f per limb.
+hipError_t launch_ntt_inv_digits(const Context* c, const RowSel& rs, uint32_t batch,
+                                 uint32_t limbs, const double2* f, hipStream_t s) {
+  return launch_inverse(c, rs, batch, limbs, LoadRow{}, InvDigit{f}, s);
+}
+
+// ModUp of every source (digits from launch_ntt_inv_sources) fused with the
+// first forward pass of the extended rows (own-digit rows are not written).
+hipError_t launch_modup_outer(const Context* c, const LevelTables& T, const uint64_t* cc,
+                              uint64_t* ext, uint32_t nsrc, uint32_t level, hipStream_t s) {
+  const uint32_t dnum_l = (level + c->alpha - 1) / c->alpha;
+  const uint32_t aj_min = level - (dnum_l - 1) * c->alpha;
+  const ModupMap map{reinterpret_cast<const double*>(cc), ext, T.mu_hat, level, c->L, c->alpha,
+                     dnum_l, c->n};
+  return launch_bconv_outer(c, map, level + c->alpha - aj_min, nsrc * dnum_l, s);
+}
+
+// ModDown conversion of the special-prime rows of acc (digits from
+// launch_ntt_inv_digits) fused with the first forward pass of y.
+hipError_t launch_moddown_outer(const Context* c, const LevelTables& T, const uint64_t* acc,
+                                uint64_t* y, uint32_t njobs, uint32_t level, hipStream_t s) {
+  const ModdownMap map{acc, y, T.md_hat, level, c->alpha, c->n};
+  return launch_bconv_outer(c, map, level, 2 * njobs, s);
+}
+
+// Second forward pass of rows whose first pass has run (launch_modup_outer).
+hipError_t launch_ntt_fwd_inner_rows(const Context* c, const RowSel& rs, uint32_t batch,
+                                     uint32_t limbs, hipStream_t s) {
+  return launch_fwd_inner(c, rs, batch, limbs, StoreResidues{}, s);
+}
+
+// Second forward pass of the ModDown conversions y[2*njobs][level][N]
+// (first pass: launch_moddown_outer) with the key-switch combine as the
+// epilogue; writes the jobs' outputs.
 hipError_t launch_ntt_fwd_ks_combine(const Context* c, uint64_t* y, uint32_t njobs,
                                      uint32_t level, const KsTable& tab, const uint64_t* acc,
                                      const double2* pinv, hipStream_t s) {
   RowSel rs{y, (size_t)level * c->n, (size_t)c->n, 0, level, 0, 0, 0, 0};
-  hipError_t e = launch_outer_pass(c, rs, 2 * njobs, level, false, s);
-  if (e != hipSuccess) return e;
-  launch_fwd_inner(c, rs, 2 * njobs, level, KsCombine{tab, acc, pinv, level, c->alpha, c->log_n},
-                   s);
-  return hipGetLastError();
+  return launch_fwd_inner(c, rs, 2 * njobs, level,
+                          KsCombine{tab, acc, pinv, level, c->alpha, c->log_n}, s);
 }
 
 // (Splitting a large batch into cache-sized chunks, so that the second pass
 // would read the first pass's output back from the 256 MB Infinity Cache,
-// measured slower on MI355X than one launch per pass over the whole batch.)
+// measured no faster on MI355X than one launch per pass over the whole batch.)
 hipError_t launch_ntt_rows(const Context* c, const RowSel& rs, uint32_t batch, uint32_t limbs,
                            bool inverse, hipStream_t s) {
-  if (inverse) {
-    launch_inv_inner(c, rs, batch, limbs, LoadRow{}, s);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    return launch_outer_pass(c, rs, batch, limbs, true, s);
-  }
-  hipError_t e = launch_outer_pass(c, rs, batch, limbs, false, s);
+  if (inverse) return launch_inverse(c, rs, batch, limbs, LoadRow{}, InvCanon{}, s);
+  hipError_t e = launch_fwd_outer(c, rs, batch, limbs, s);
   if (e != hipSuccess) return e;
-  launch_fwd_inner(c, rs, batch, limbs, StoreResidues{}, s);
-  return hipGetLastError();
+  return launch_fwd_inner(c, rs, batch, limbs, StoreResidues{}, s);
 }
 
 hipError_t launch_ntt(const Context* c, uint64_t* d, uint32_t batch, size_t batch_stride,

@@ -35,12 +35,15 @@ const LevelTables* level_tables(Context* c, uint32_t level, int* err) {
   auto ext_prime = [&](uint32_t row) { return c->primes[row < level ? row : L + (row - level)]; };
   std::vector<uint64_t> ps(c->primes.begin() + L, c->primes.end());
 
-  std::vector<double2> mu_inv((size_t)dnum_l * alpha), mu_hat((size_t)dnum_l * E * alpha);
+  std::vector<double2> mu_inv((size_t)dnum_l * alpha), mu_hat((size_t)dnum_l * E * alpha),
+      mu_inv_n(level);
   for (uint32_t j = 0; j < dnum_l; ++j) {
     const uint32_t lo = j * alpha, hi = std::min(lo + alpha, level);
     std::vector<uint64_t> dq(c->primes.begin() + lo, c->primes.begin() + hi);
     for (uint32_t a = 0; a < hi - lo; ++a) {
-      mu_inv[j * alpha + a] = entry(h_inv(prod_mod_except(dq, a, dq[a]), dq[a]), dq[a]);
+      const uint64_t inv = h_inv(prod_mod_except(dq, a, dq[a]), dq[a]);
+      mu_inv[j * alpha + a] = entry(inv, dq[a]);
+      mu_inv_n[lo + a] = entry(h_mulmod(inv, h_inv(c->n % dq[a], dq[a]), dq[a]), dq[a]);
       for (uint32_t row = 0; row < E; ++row) {
         const uint64_t m = ext_prime(row);
         mu_hat[((size_t)j * E + row) * alpha + a] = entry(prod_mod_except(dq, a, m), m);
@@ -48,9 +51,12 @@ const LevelTables* level_tables(Context* c, uint32_t level, int* err) {
     }
   }
   std::vector<double2> md_inv(alpha), md_hat((size_t)level * alpha), md_pinv(level), pmod(L),
-      rs_inv(level);
-  for (uint32_t a = 0; a < alpha; ++a)
-    md_inv[a] = entry(h_inv(prod_mod_except(ps, a, ps[a]), ps[a]), ps[a]);
+      rs_inv(level), md_inv_n(alpha);
+  for (uint32_t a = 0; a < alpha; ++a) {
+    const uint64_t inv = h_inv(prod_mod_except(ps, a, ps[a]), ps[a]);
+    md_inv[a] = entry(inv, ps[a]);
+    md_inv_n[a] = entry(h_mulmod(inv, h_inv(c->n % ps[a], ps[a]), ps[a]), ps[a]);
+  }
   for (uint32_t i = 0; i < L; ++i) {
     const uint64_t q = c->primes[i];
     const uint64_t P = prod_mod_except(ps, ps.size(), q);
@@ -65,10 +71,10 @@ const LevelTables* level_tables(Context* c, uint32_t level, int* err) {
   std::vector<double2> all;
   LevelTables T;
   T.level = level;
-  size_t off[7];
-  const std::vector<double2>* parts[7] = {&mu_inv, &mu_hat, &md_inv, &md_hat,
-                                          &md_pinv, &pmod,   &rs_inv};
-  for (int p = 0; p < 7; ++p) {
+  size_t off[9];
+  const std::vector<double2>* parts[9] = {&mu_inv,  &mu_hat, &md_inv, &md_hat,  &md_pinv,
+                                          &pmod,    &rs_inv, &mu_inv_n, &md_inv_n};
+  for (int p = 0; p < 9; ++p) {
     off[p] = all.size();
     all.insert(all.end(), parts[p]->begin(), parts[p]->end());
   }
@@ -90,6 +96,8 @@ const LevelTables* level_tables(Context* c, uint32_t level, int* err) {
   T.md_pinv = d + off[4];
   T.pmod = d + off[5];
   T.rs_inv = d + off[6];
+  T.mu_inv_n = d + off[7];
+  T.md_inv_n = d + off[8];
   return &(c->level_tabs[level] = T);
 }
 
@@ -103,10 +111,10 @@ namespace {
 struct Scratch {
   uint32_t cap;
   uint64_t* cin;  // [L][2][N]          private copy of an aliased input
-  uint64_t* cc;   // [B][L][N]          coefficient form of switched polynomials
-  uint64_t* ext;  // [B][dnum][L+a][N]  ModUp outputs
+  uint64_t* cc;   // [B][L][N]          centred ModUp digits of the switched polynomials (fp64)
+  uint64_t* ext;  // [B][dnum][L+a][N]  ModUp outputs (evaluation form)
   uint64_t* acc;  // [B][2][L+a][N]     key inner products
-  uint64_t* y;    // [B][2][L][N]       ModDown conversions
+  uint64_t* y;    // [B][2][L][N]       ModDown conversions (first-pass fp64)
   uint64_t* d01;  // [L][2][N]          tensor (d0, d1)
   uint64_t* d2;   // [L][N]             tensor d2
   uint64_t* v;    // [2][N]             rescale: last limb
@@ -177,10 +185,13 @@ int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& sr
   if (ns > S.cap) return fail(FESC_ERR_ARG, "key-switch sources exceed the scratch capacity");
   for (const KsJob& J : jobs)
     if (J.src >= ns) return fail(FESC_ERR_ARG, "key-switch job names a missing source");
-  HIPCK(launch_ntt_inv_sources(c, tab, ns, S.cc, level, s));
-  HIPCK(k_modup_launch(c, *T, S.cc, S.ext, ns, level, s));
+  // iNTT of the sources, stored as centred ModUp digits; ModUp fused with the
+  // first forward pass of the extended rows; second pass (own-digit rows are
+  // never written: the inner product reads them from the source)
+  HIPCK(launch_ntt_inv_sources(c, tab, ns, S.cc, level, T->mu_inv_n, s));
+  HIPCK(launch_modup_outer(c, *T, S.cc, S.ext, ns, level, s));
   RowSel rs{S.ext, (size_t)E * n, n, 0, level, c->L, c->alpha, level, dnum_l};
-  HIPCK(launch_ntt_rows(c, rs, ns * dnum_l, E, false, s));
+  HIPCK(launch_ntt_fwd_inner_rows(c, rs, ns * dnum_l, E, s));
   // jobs
   for (size_t j0 = 0; j0 < jobs.size(); j0 += S.cap) {
     const uint32_t nj = std::min<uint32_t>(S.cap, (uint32_t)(jobs.size() - j0));
@@ -197,8 +208,11 @@ int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& sr
       t.out[j] = J.out;
     }
     HIPCK(k_ip_launch(c, t, nj, S.ext, S.acc, level, s));
-    HIPCK(ntt_rows(c, S.acc + (size_t)level * n, 2 * nj, (size_t)E * n, c->alpha, c->L, true, s));
-    HIPCK(k_moddown_bconv_launch(c, *T, S.acc, S.y, nj, level, s));
+    // special-prime rows: iNTT to centred ModDown digits, conversion fused
+    // with the first forward pass of y, second pass ending in the combine
+    const RowSel rp{S.acc + (size_t)level * n, (size_t)E * n, n, c->L, c->alpha, 0, 0, 0, 0};
+    HIPCK(launch_ntt_inv_digits(c, rp, 2 * nj, c->alpha, T->md_inv_n, s));
+    HIPCK(launch_moddown_outer(c, *T, S.acc, S.y, nj, level, s));
     HIPCK(launch_ntt_fwd_ks_combine(c, S.y, nj, level, t, S.acc, T->md_pinv, s));
   }
   return FESC_OK;

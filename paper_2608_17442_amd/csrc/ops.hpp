@@ -52,18 +52,23 @@ struct KsTable {
   uint32_t add_galois[kMaxBatch];     // job: permutation of `add` (0: none)
 };
 
-// ntt.hip: fused transforms of the key-switch pipeline
+// ntt.hip: transforms of the key-switch pipeline (inverse transforms store
+// centred conversion digits; conversions are fused with the first forward pass)
 hipError_t launch_ntt_inv_sources(const Context* c, const KsTable& tab, uint32_t nsrc,
-                                  uint64_t* cc, uint32_t level, hipStream_t s);
+                                  uint64_t* cc, uint32_t level, const double2* f, hipStream_t s);
+hipError_t launch_ntt_inv_digits(const Context* c, const RowSel& rs, uint32_t batch,
+                                 uint32_t limbs, const double2* f, hipStream_t s);
+hipError_t launch_modup_outer(const Context* c, const LevelTables& T, const uint64_t* cc,
+                              uint64_t* ext, uint32_t nsrc, uint32_t level, hipStream_t s);
+hipError_t launch_moddown_outer(const Context* c, const LevelTables& T, const uint64_t* acc,
+                                uint64_t* y, uint32_t njobs, uint32_t level, hipStream_t s);
+hipError_t launch_ntt_fwd_inner_rows(const Context* c, const RowSel& rs, uint32_t batch,
+                                     uint32_t limbs, hipStream_t s);
 hipError_t launch_ntt_fwd_ks_combine(const Context* c, uint64_t* y, uint32_t njobs,
                                      uint32_t level, const KsTable& tab, const uint64_t* acc,
                                      const double2* pinv, hipStream_t s);
-hipError_t k_modup_launch(const Context* c, const LevelTables& T, const uint64_t* cc,
-                          uint64_t* ext, uint32_t nsrc, uint32_t level, hipStream_t s);
 hipError_t k_ip_launch(const Context* c, const KsTable& tab, uint32_t njobs, const uint64_t* ext,
                        uint64_t* acc, uint32_t level, hipStream_t s);
-hipError_t k_moddown_bconv_launch(const Context* c, const LevelTables& T, const uint64_t* acc,
-                                  uint64_t* y, uint32_t njobs, uint32_t level, hipStream_t s);
 
 // ------------------------------------------------------------------ ops.cpp
 const LevelTables* level_tables(Context* c, uint32_t level, int* err);
