@@ -175,10 +175,10 @@ class Workloads:
         self.mv_in = [self.encrypt(PK.paired_input(X, u, n_slots, seg, Cc), 2.0 ** 40, level,
                                    seed, "cfg4", u) for u in range(n_in)]
         n_diag = n_out * n2 * n_in * n1
-        log(f"encoding {n_diag} diagonals ({n_diag * level * self.n * 8 / 1e9:.1f} GB)")
         desc = self.F.matvec_desc(level, n_in, n_out, n1, n2, seg, True, True)
-        self.bank = torch.empty(self.F.matvec_bank_words(self.ctx, desc), dtype=torch.int64,
-                                device="cuda")
+        self.bank_bytes = 8 * self.F.matvec_bank_words(self.ctx, desc)
+        log(f"encoding {n_diag} diagonals ({self.bank_bytes / 1e9:.1f} GB bank)")
+        self.bank = torch.empty(self.bank_bytes // 8, dtype=torch.int64, device="cuda")
         stage = [torch.empty(level * self.n, dtype=torch.int64, device="cuda") for _ in range(8)]
         scale = float(self.q[level - 1])
         index = [(b, p, u, q) for b in range(n_out) for p in range(n2) for u in range(n_in)
@@ -339,7 +339,7 @@ def main():
     s = W.mv_shape
     lv = W.mv_level
     ct_bytes = 2 * lv * n * 8
-    ptmac_bytes = s["n_diag"] * lv * n * 8 + s["n_in"] * s["n1"] * ct_bytes \
+    ptmac_bytes = W.bank_bytes + s["n_in"] * s["n1"] * ct_bytes \
         + s["n_out"] * s["n2"] * ct_bytes
     ptmac_gbs = ptmac_bytes / (ptmac_ms * 1e-3) / 1e9
     # VALU work: a limb transform is (N/2) log N butterflies; a key switch at
