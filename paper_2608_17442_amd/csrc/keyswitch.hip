@@ -37,53 +37,60 @@ __device__ __forceinline__ uint32_t ext_prime(uint32_t row, uint32_t level, uint
   return row < level ? row : L + (row - level);
 }
 
-// Inner product with the key, sigma_g applied to the extended digits on the
-// fly: acc[job][t][row][k] = sum_j d_j[row][src(k)] * key[j][prime(row)][t][k].
-// Own-digit rows of d_j are the source polynomial itself.  blockIdx.z = job.
-// D = number of digits at this level (compile time), A = alpha.
+// Key-stationary inner product with sigma_g applied to the extended digits on
+// the fly: for every job j of key group blockIdx.z (jobs sharing one switching
+// key and Galois element g),
+//     acc[j][t][row][k] = sum_d D_d(src_j)[row][gsrc(k)] * key[d][prime(row)][t][k],
+// D_d(src) the ModUp digit d of the job's source, whose own-digit rows are the
+// source polynomial itself.  The key values of a coefficient are loaded once
+// and reused by every job of the group.  D = number of digits at this level
+// (compile time).
 template <int D>
 __global__ __launch_bounds__(kThreads) void k_ip(KsTable tab, const uint64_t* __restrict__ ext,
                                                  uint64_t* __restrict__ acc, uint32_t level,
                                                  uint32_t L, uint32_t alpha, uint32_t log_n,
                                                  const PrimeK* __restrict__ pk) {
   const uint32_t n = 1u << log_n;
-  const uint32_t row = blockIdx.y, job = blockIdx.z;
+  const uint32_t row = blockIdx.y, kg = blockIdx.z;
   const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
   if (k >= n) return;
   const uint32_t E = level + alpha, KE = L + alpha;
-  const uint32_t s = tab.job_src[job], galois = tab.galois[job];
-  const uint64_t* key = tab.key[job];
-  const uint64_t* in = tab.src_in[s];
-  const size_t in_stride = tab.src_stride[s];
-  const uint64_t* ex = ext + (size_t)s * D * E * n;
+  const uint32_t j0 = tab.kg_first[kg], j1 = j0 + tab.kg_count[kg];
+  const uint32_t galois = tab.galois[j0];
+  const uint64_t* key = tab.key[j0];
   const uint32_t prime = ext_prime(row, level, L);
   const PrimeK M = pk[prime];
   const uint32_t src = galois ? galois_src(k, galois, log_n) : k;
   const uint32_t own = row < level ? row / alpha : D;  // digit whose rows hold `row`
-  uint64_t dv[D], kb[D], ka[D];
+  double kb[D], ka[D];
 #pragma unroll
   for (int j = 0; j < D; ++j) {
-    const uint64_t* p = (uint32_t)j == own ? in + (size_t)row * in_stride
-                                           : ex + ((size_t)j * E + row) * n;
-    dv[j] = p[src];
     const size_t ko = (((size_t)j * KE + prime) * 2) * n + k;
-    kb[j] = key[ko];
-    ka[j] = key[ko + n];
+    kb[j] = u2d(key[ko]);
+    ka[j] = u2d(key[ko + n]);
   }
-  double ab = 0.0, aa = 0.0;
+  for (uint32_t job = j0; job < j1; ++job) {
+    const uint32_t s = tab.job_src[job];
+    const uint64_t* in = tab.src_in[s] + (size_t)row * tab.src_stride[s];
+    const uint64_t* ex = ext + ((size_t)s * D * E + row) * n;
+    uint64_t dv[D];
 #pragma unroll
-  for (int j = 0; j < D; ++j) {
-    const double d = u2d(dv[j]);
-    ab += mm_var(d, u2d(kb[j]), M.q, M.qinv);
-    aa += mm_var(d, u2d(ka[j]), M.q, M.qinv);
-    if ((j & 3) == 3 && j + 1 < D) {
-      ab = red_bal(ab, M.q, M.qinv);
-      aa = red_bal(aa, M.q, M.qinv);
+    for (int j = 0; j < D; ++j) dv[j] = ((uint32_t)j == own ? in : ex + (size_t)j * E * n)[src];
+    double ab = 0.0, aa = 0.0;
+#pragma unroll
+    for (int j = 0; j < D; ++j) {
+      const double d = u2d(dv[j]);
+      ab += mm_var(d, kb[j], M.q, M.qinv);
+      aa += mm_var(d, ka[j], M.q, M.qinv);
+      if ((j & 3) == 3 && j + 1 < D) {
+        ab = red_bal(ab, M.q, M.qinv);
+        aa = red_bal(aa, M.q, M.qinv);
+      }
     }
+    uint64_t* out = acc + (size_t)job * 2 * E * n;
+    out[(size_t)row * n + k] = to_res(ab, M.q, M.qinv);
+    out[((size_t)E + row) * n + k] = to_res(aa, M.q, M.qinv);
   }
-  uint64_t* out = acc + (size_t)job * 2 * E * n;
-  out[(size_t)row * n + k] = to_res(ab, M.q, M.qinv);
-  out[((size_t)E + row) * n + k] = to_res(aa, M.q, M.qinv);
 }
 
 // Dispatch on a runtime value to a template instantiation 1..16.
@@ -111,11 +118,11 @@ struct IpL {
 
 }  // namespace
 
-hipError_t k_ip_launch(const Context* c, const KsTable& tab, uint32_t njobs, const uint64_t* ext,
+hipError_t k_ip_launch(const Context* c, const KsTable& tab, uint32_t nkeys, const uint64_t* ext,
                        uint64_t* acc, uint32_t level, hipStream_t s) {
   const uint32_t dnum_l = (level + c->alpha - 1) / c->alpha;
   if (dnum_l > 16) return hipErrorInvalidValue;
-  dim3 grid((c->n + kThreads - 1) / kThreads, level + c->alpha, njobs);
+  dim3 grid((c->n + kThreads - 1) / kThreads, level + c->alpha, nkeys);
   dispatch16<IpL>(dnum_l, grid, s, tab, ext, acc, level, c->L, c->alpha, c->log_n, c->d_pk);
   return hipGetLastError();
 }

@@ -3,6 +3,7 @@
 // relinearisation, rescaling, key generation and encryption.  Every launch is
 // asynchronous on the caller's stream; nothing here synchronises.
 #include <algorithm>
+#include <functional>
 #include <string>
 #include <vector>
 
@@ -193,11 +194,25 @@ int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& sr
   RowSel rs{S.ext, (size_t)E * n, n, 0, level, c->L, c->alpha, level, dnum_l};
   HIPCK(launch_ntt_fwd_inner_rows(c, rs, ns * dnum_l, E, s));
   // jobs
+  // jobs ordered by (key, Galois element): each group of kMaxBatch jobs then
+  // holds few distinct keys, and the inner product reads each key once
+  std::vector<uint32_t> order(jobs.size());
+  for (uint32_t j = 0; j < order.size(); ++j) order[j] = j;
+  std::stable_sort(order.begin(), order.end(), [&](uint32_t x, uint32_t y) {
+    const KsJob &a = jobs[x], &b = jobs[y];
+    return a.key != b.key ? std::less<const uint64_t*>()(a.key, b.key) : a.galois < b.galois;
+  });
   for (size_t j0 = 0; j0 < jobs.size(); j0 += S.cap) {
     const uint32_t nj = std::min<uint32_t>(S.cap, (uint32_t)(jobs.size() - j0));
     KsTable t = tab;
+    uint32_t nkeys = 0;
     for (uint32_t j = 0; j < nj; ++j) {
-      const KsJob& J = jobs[j0 + j];
+      const KsJob& J = jobs[order[j0 + j]];
+      if (j == 0 || J.key != t.key[j - 1] || J.galois != t.galois[j - 1]) {
+        t.kg_first[nkeys] = j;
+        t.kg_count[nkeys++] = 0;
+      }
+      ++t.kg_count[nkeys - 1];
       t.job_src[j] = J.src;
       t.key[j] = J.key;
       t.galois[j] = J.galois;
@@ -207,7 +222,7 @@ int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& sr
       t.add2[j] = J.add2;
       t.out[j] = J.out;
     }
-    HIPCK(k_ip_launch(c, t, nj, S.ext, S.acc, level, s));
+    HIPCK(k_ip_launch(c, t, nkeys, S.ext, S.acc, level, s));
     // special-prime rows: iNTT to centred ModDown digits, conversion fused
     // with the first forward pass of y, second pass ending in the combine
     const RowSel rp{S.acc + (size_t)level * n, (size_t)E * n, n, c->L, c->alpha, 0, 0, 0, 0};

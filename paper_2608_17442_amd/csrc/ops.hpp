@@ -50,6 +50,10 @@ struct KsTable {
   uint32_t galois[kMaxBatch];         // job: Galois element on the digits (0: none)
   uint32_t add_mask[kMaxBatch];       // job: components of `add` used (bit t)
   uint32_t add_galois[kMaxBatch];     // job: permutation of `add` (0: none)
+  // jobs sharing a switching key (and Galois element) are consecutive: key
+  // group g holds jobs kg_first[g] .. kg_first[g] + kg_count[g] - 1
+  uint32_t kg_first[kMaxBatch];
+  uint32_t kg_count[kMaxBatch];
 };
 
 // ntt.hip: transforms of the key-switch pipeline (inverse transforms store
@@ -67,7 +71,7 @@ hipError_t launch_ntt_fwd_inner_rows(const Context* c, const RowSel& rs, uint32_
 hipError_t launch_ntt_fwd_ks_combine(const Context* c, uint64_t* y, uint32_t njobs,
                                      uint32_t level, const KsTable& tab, const uint64_t* acc,
                                      const double2* pinv, hipStream_t s);
-hipError_t k_ip_launch(const Context* c, const KsTable& tab, uint32_t njobs, const uint64_t* ext,
+hipError_t k_ip_launch(const Context* c, const KsTable& tab, uint32_t nkeys, const uint64_t* ext,
                        uint64_t* acc, uint32_t level, hipStream_t s);
 
 // ------------------------------------------------------------------ ops.cpp
@@ -90,10 +94,12 @@ struct KsSource {
   size_t stride;
 };
 
-// Runs any number of key switches at one level: ModUp of every source (in
-// groups of kMaxBatch), then inner product, ModDown and combine of the jobs
-// in groups of kMaxBatch.  Sources must stay unmodified until all jobs have
-// read them; outputs must not alias sources or adds of later groups.
+// Runs any number of key switches at one level: ModUp of every source (at
+// most kMaxBatch), then inner product, ModDown and combine of the jobs in
+// groups of kMaxBatch, jobs ordered by switching key so that each key is read
+// once per group (key-stationary inner product).  Sources must stay
+// unmodified until all jobs have read them; a job's output must not alias a
+// source or addend of another job.
 int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& srcs,
                      const std::vector<KsJob>& jobs, hipStream_t s);
 
