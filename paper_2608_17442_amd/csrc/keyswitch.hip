@@ -43,13 +43,17 @@ __device__ __forceinline__ uint32_t ext_prime(uint32_t row, uint32_t level, uint
 //     acc[j][t][row][k] = sum_d D_d(src_j)[row][gsrc(k)] * key[d][prime(row)][t][k],
 // D_d(src) the ModUp digit d of the job's source, whose own-digit rows are the
 // source polynomial itself.  The key values of a coefficient are loaded once
-// and reused by every job of the group.  D = number of digits at this level
-// (compile time).
+// and reused by every job of the group.  With tab.fold the level rows
+// (row < level) store acc * P^-1 plus the job's addend components instead
+// (the addend read through the same permutation), so that the combine only
+// has to subtract y * P^-1.  D = number of digits at this level (compile
+// time).
 template <int D>
 __global__ __launch_bounds__(kThreads) void k_ip(KsTable tab, const uint64_t* __restrict__ ext,
                                                  uint64_t* __restrict__ acc, uint32_t level,
                                                  uint32_t L, uint32_t alpha, uint32_t log_n,
-                                                 const PrimeK* __restrict__ pk) {
+                                                 const PrimeK* __restrict__ pk,
+                                                 const double2* __restrict__ pinv) {
   const uint32_t n = 1u << log_n;
   const uint32_t row = blockIdx.y, kg = blockIdx.z;
   const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
@@ -87,6 +91,15 @@ __global__ __launch_bounds__(kThreads) void k_ip(KsTable tab, const uint64_t* __
         aa = red_bal(aa, M.q, M.qinv);
       }
     }
+    if (tab.fold && row < level) {
+      const double2 f = pinv[row];
+      ab = mm_shoup(ab, f.x, f.y, M.q);
+      aa = mm_shoup(aa, f.x, f.y, M.q);
+      const uint64_t* add = tab.add[job];
+      const uint32_t mask = tab.add_mask[job];
+      if (add && (mask & 1u)) ab += u2d(add[(size_t)2 * row * n + src]);
+      if (add && (mask & 2u)) aa += u2d(add[((size_t)2 * row + 1) * n + src]);
+    }
     uint64_t* out = acc + (size_t)job * 2 * E * n;
     out[(size_t)row * n + k] = to_res(ab, M.q, M.qinv);
     out[((size_t)E + row) * n + k] = to_res(aa, M.q, M.qinv);
@@ -110,20 +123,22 @@ void dispatch16(uint32_t a, Args&&... args) {
 template <int D>
 struct IpL {
   static void run(dim3 g, hipStream_t s, const KsTable& tab, const uint64_t* ext, uint64_t* acc,
-                  uint32_t level, uint32_t L, uint32_t alpha, uint32_t log_n, const PrimeK* pk) {
+                  uint32_t level, uint32_t L, uint32_t alpha, uint32_t log_n, const PrimeK* pk,
+                  const double2* pinv) {
     hipLaunchKernelGGL(k_ip<D>, g, dim3(kThreads), 0, s, tab, ext, acc, level, L, alpha, log_n,
-                       pk);
+                       pk, pinv);
   }
 };
 
 }  // namespace
 
 hipError_t k_ip_launch(const Context* c, const KsTable& tab, uint32_t nkeys, const uint64_t* ext,
-                       uint64_t* acc, uint32_t level, hipStream_t s) {
+                       uint64_t* acc, uint32_t level, const double2* pinv, hipStream_t s) {
   const uint32_t dnum_l = (level + c->alpha - 1) / c->alpha;
   if (dnum_l > 16) return hipErrorInvalidValue;
   dim3 grid((c->n + kThreads - 1) / kThreads, level + c->alpha, nkeys);
-  dispatch16<IpL>(dnum_l, grid, s, tab, ext, acc, level, c->L, c->alpha, c->log_n, c->d_pk);
+  dispatch16<IpL>(dnum_l, grid, s, tab, ext, acc, level, c->L, c->alpha, c->log_n, c->d_pk,
+                  pinv);
   return hipGetLastError();
 }
 

@@ -531,7 +531,9 @@ __global__ __launch_bounds__(kThreads) void k_inv_inner(RowSel rs, uint32_t log_
 // Epilogue fusing the key-switch combine into the forward transform of the
 // ModDown conversion y: for u = 2*job + t (blockIdx.y) and limb i
 // (blockIdx.z), out_job[i][t] = (acc[u][i] - NTT(y)[u][i]) * P^-1 + adds,
-// with the adds of the job table (sigma_g-permuted `add`, plain `add2`).
+// with the adds of the job table (sigma_g-permuted `add`, plain `add2`).  If
+// tab.fold the inner product has already stored acc * P^-1 + add, and only
+// NTT(y) * P^-1 is subtracted here.
 struct KsCombine {
   KsTable tab;
   const uint64_t* acc;
@@ -549,6 +551,16 @@ struct KsCombine {
     const uint64_t* add = use_add ? tab.add[job] + o : nullptr;
     const uint64_t* add2 = tab.add2[job];
     uint64_t* out = tab.out[job] + o;
+    if (tab.fold) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const uint32_t k = k0 + 256 * r;
+        double v = u2d(a[k]) - mm_shoup(x[r], f.x, f.y, q);
+        if (add2) v += u2d(add2[o + k]);
+        out[k] = to_res(v, q, qinv);
+      }
+      return;
+    }
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const uint32_t k = k0 + 256 * r;

@@ -205,6 +205,7 @@ int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& sr
   for (size_t j0 = 0; j0 < jobs.size(); j0 += S.cap) {
     const uint32_t nj = std::min<uint32_t>(S.cap, (uint32_t)(jobs.size() - j0));
     KsTable t = tab;
+    t.fold = 1;
     uint32_t nkeys = 0;
     for (uint32_t j = 0; j < nj; ++j) {
       const KsJob& J = jobs[order[j0 + j]];
@@ -219,10 +220,11 @@ int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& sr
       t.add[j] = J.add;
       t.add_mask[j] = J.add ? J.add_mask : 0;
       t.add_galois[j] = J.add_galois;
+      if (J.add && J.add_galois != J.galois) t.fold = 0;
       t.add2[j] = J.add2;
       t.out[j] = J.out;
     }
-    HIPCK(k_ip_launch(c, t, nkeys, S.ext, S.acc, level, s));
+    HIPCK(k_ip_launch(c, t, nkeys, S.ext, S.acc, level, T->md_pinv, s));
     // special-prime rows: iNTT to centred ModDown digits, conversion fused
     // with the first forward pass of y, second pass ending in the combine
     const RowSel rp{S.acc + (size_t)level * n, (size_t)E * n, n, c->L, c->alpha, 0, 0, 0, 0};

@@ -54,6 +54,10 @@ struct KsTable {
   // group g holds jobs kg_first[g] .. kg_first[g] + kg_count[g] - 1
   uint32_t kg_first[kMaxBatch];
   uint32_t kg_count[kMaxBatch];
+  // 1 when every job's addend uses the job's own Galois element (or there is
+  // none): the inner product then stores acc * P^-1 + add on the level rows
+  // and the combine only subtracts y * P^-1
+  uint32_t fold;
 };
 
 // ntt.hip: transforms of the key-switch pipeline (inverse transforms store
@@ -72,7 +76,7 @@ hipError_t launch_ntt_fwd_ks_combine(const Context* c, uint64_t* y, uint32_t njo
                                      uint32_t level, const KsTable& tab, const uint64_t* acc,
                                      const double2* pinv, hipStream_t s);
 hipError_t k_ip_launch(const Context* c, const KsTable& tab, uint32_t nkeys, const uint64_t* ext,
-                       uint64_t* acc, uint32_t level, hipStream_t s);
+                       uint64_t* acc, uint32_t level, const double2* pinv, hipStream_t s);
 
 // ------------------------------------------------------------------ ops.cpp
 const LevelTables* level_tables(Context* c, uint32_t level, int* err);
