@@ -167,9 +167,9 @@ __global__ __launch_bounds__(kThreads) void k_encrypt(const uint64_t* __restrict
   ct[(2 * (size_t)i + 1) * n + k] = a[o];
 }
 
-// Rescale, step 1: v = centred coefficients (mod q_last) of the last limb of
-// both components (rows 0, 1 of `v`, coefficient form); write [v]_{q_i} into
-// w[t][i] for i < l - 1.
+// Rescale, step 1: v = the last limb of every component to rescale (row
+// t = blockIdx.z of `v`, coefficient form); write its centred value mod q_i
+// into w[t][i] for i < l - 1.
 __global__ __launch_bounds__(kThreads) void k_rescale_lift(const uint64_t* __restrict__ v,
                                                            uint64_t* __restrict__ w,
                                                            uint32_t n, uint32_t last,
@@ -183,22 +183,24 @@ __global__ __launch_bounds__(kThreads) void k_rescale_lift(const uint64_t* __res
   st(w + ((size_t)t * last + i) * n + k, x, P.q, P.qinv);
 }
 
-// Rescale, step 2: out[i][t] = (c[i][t] - w[t][i]) * q_last^-1 mod q_i.
-__global__ __launch_bounds__(kThreads) void k_rescale_combine(const uint64_t* c,
+// Rescale, step 2, for ciphertext b = blockIdx.z of the table:
+// out_b[i][t] = (c_b[i][t] - w[2b + t][i]) * q_last^-1 mod q_i.
+__global__ __launch_bounds__(kThreads) void k_rescale_combine(RsTable tab,
                                                               const uint64_t* __restrict__ w,
-                                                              uint64_t* out, uint32_t n,
-                                                              uint32_t last,
+                                                              uint32_t n, uint32_t last,
                                                               const double2* __restrict__ qlinv,
                                                               const PrimeK* __restrict__ pk) {
-  const uint32_t i = blockIdx.y;
+  const uint32_t i = blockIdx.y, b = blockIdx.z;
   const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
   if (k >= n) return;
+  const uint64_t* c = tab.in[b];
+  uint64_t* out = tab.out[b];
   const PrimeK P = pk[i];
   const double2 f = qlinv[i];
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
     const size_t o = ((size_t)2 * i + t) * n + k;
-    const double d = ld(c + o) - ld(w + ((size_t)t * last + i) * n + k);
+    const double d = ld(c + o) - ld(w + ((size_t)(2 * b + t) * last + i) * n + k);
     st(out + o, mm_shoup(d, f.x, f.y, P.q), P.q, P.qinv);
   }
 }
@@ -268,17 +270,17 @@ hipError_t k_encrypt_launch(const Context* c, const uint64_t* a, const uint64_t*
 }
 
 hipError_t k_rescale_lift_launch(const Context* c, const uint64_t* v, uint64_t* w,
-                                 uint32_t level, hipStream_t s) {
-  hipLaunchKernelGGL(k_rescale_lift, grid_rows(c->n, level - 1, 2), dim3(kThreads), 0, s, v, w,
-                     c->n, level - 1, c->d_pk);
+                                 uint32_t level, uint32_t rows, hipStream_t s) {
+  hipLaunchKernelGGL(k_rescale_lift, grid_rows(c->n, level - 1, rows), dim3(kThreads), 0, s, v,
+                     w, c->n, level - 1, c->d_pk);
   return hipGetLastError();
 }
 
-hipError_t k_rescale_combine_launch(const Context* c, const uint64_t* in, const uint64_t* w,
-                                    uint64_t* out, uint32_t level, const double2* qlinv,
+hipError_t k_rescale_combine_launch(const Context* c, const RsTable& tab, uint32_t count,
+                                    const uint64_t* w, uint32_t level, const double2* qlinv,
                                     hipStream_t s) {
-  hipLaunchKernelGGL(k_rescale_combine, grid_rows(c->n, level - 1), dim3(kThreads), 0, s, in, w,
-                     out, c->n, level - 1, qlinv, c->d_pk);
+  hipLaunchKernelGGL(k_rescale_combine, grid_rows(c->n, level - 1, count), dim3(kThreads), 0, s,
+                     tab, w, c->n, level - 1, qlinv, c->d_pk);
   return hipGetLastError();
 }
 

@@ -35,6 +35,8 @@ namespace fesc {
 int op_rotate_many(Context* c, const uint64_t* in, uint32_t count, const int32_t* steps,
                    uint64_t* const* outs, uint32_t level, hipStream_t s);
 int op_rescale(Context* c, const uint64_t* in, uint64_t* out, uint32_t level, hipStream_t s);
+int op_rescale_many(Context* c, uint32_t count, const uint64_t* const* ins, uint64_t* const* outs,
+                    uint32_t level, hipStream_t s);
 uint32_t galois_of_step(const Context* c, int32_t step);
 
 namespace {
@@ -291,12 +293,11 @@ int ptct_matvec(Context* c, fesc_matvec_plan* p, const uint64_t* const* in,
       return err;
     for (uint32_t b = 0; b < d.n_out; ++b) res[b] = gout[b];
   }
-  for (uint32_t b = 0; b < d.n_out; ++b) {
-    if (d.rescale) {
-      if ((err = op_rescale(c, res[b], out[b], level, s))) return err;
-    } else {
+  if (d.rescale) {
+    if ((err = op_rescale_many(c, d.n_out, res.data(), out, level, s))) return err;
+  } else {
+    for (uint32_t b = 0; b < d.n_out; ++b)
       HIPCK(hipMemcpyAsync(out[b], res[b], W * 8, hipMemcpyDeviceToDevice, s));
-    }
   }
   HIPCK(hipEventRecord(p->ev[3], s));
   return FESC_OK;

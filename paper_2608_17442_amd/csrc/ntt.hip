@@ -666,6 +666,14 @@ hipError_t launch_ntt_inv_sources(const Context* c, const KsTable& tab, uint32_t
   return launch_inverse(c, rs, nsrc, level, LoadSources{tab}, InvDigit{f}, s);
 }
 
+// Inverse transform (canonical output) of nrows single rows, row r read from
+// tab.src_in[r], all under prime `prime`, into out[r][N].
+hipError_t launch_ntt_inv_gather(const Context* c, const KsTable& tab, uint32_t nrows,
+                                 uint64_t* out, uint32_t prime, hipStream_t s) {
+  RowSel rs{out, (size_t)c->n, (size_t)c->n, prime, 1, 0, 0, 0, 0};
+  return launch_inverse(c, rs, nrows, 1, LoadSources{tab}, InvCanon{}, s);
+}
+
 // Inverse transform of the rows rs selects (in place), stored as centred
 // digits [N^-1 f_i x]_{q_i} (fp64), f per limb.
 hipError_t launch_ntt_inv_digits(const Context* c, const RowSel& rs, uint32_t batch,

@@ -333,20 +333,42 @@ int op_mul_relin(Context* c, const uint64_t* a, const uint64_t* b, uint64_t* out
                           {KsJob{0, key, 0, S.d01, 3u, 0, nullptr, out}}, s);
 }
 
-int op_rescale(Context* c, const uint64_t* in, uint64_t* out, uint32_t level, hipStream_t s) {
+// Rescale (c - [c mod q_last]) / q_last of up to kRescaleBatch ciphertexts
+// per launch sequence: inverse NTT of every last limb (read in place), lift
+// of the centred coefficients to the other primes, forward NTT, combine.
+int op_rescale_many(Context* c, uint32_t count, const uint64_t* const* ins, uint64_t* const* outs,
+                    uint32_t level, hipStream_t s) {
   int err;
   const LevelTables* T = level_tables(c, level, &err);
   if (!T) return err;
   Scratch S;
-  if ((err = scratch(c, &S))) return err;
+  if ((err = scratch(c, &S, count))) return err;
+  if (count > 1 && S.cap < kMaxBatch) return fail(FESC_ERR_ARG, "rescale batch needs scratch");
   const size_t n = c->n;
-  HIPCK(hipMemcpyAsync(S.v, in + (size_t)2 * (level - 1) * n, 2 * n * 8,
-                       hipMemcpyDeviceToDevice, s));
-  HIPCK(ntt_rows(c, S.v, 2, n, 1, level - 1, true, s));
-  HIPCK(k_rescale_lift_launch(c, S.v, S.w, level, s));
-  HIPCK(ntt_rows(c, S.w, 2, (size_t)(level - 1) * n, level - 1, 0, false, s));
-  HIPCK(k_rescale_combine_launch(c, in, S.w, out, level, T->rs_inv, s));
+  const uint32_t last = level - 1;
+  // the key-switch regions are idle here: last limbs in cc, lifted rows in ext
+  uint64_t* v = count > 1 ? S.cc : S.v;
+  uint64_t* w = count > 1 ? S.ext : S.w;
+  for (uint32_t b0 = 0; b0 < count; b0 += kRescaleBatch) {
+    const uint32_t m = std::min(kRescaleBatch, count - b0);
+    KsTable tab{};
+    RsTable rt{};
+    for (uint32_t b = 0; b < m; ++b) {
+      tab.src_in[2 * b] = ins[b0 + b] + (size_t)2 * last * n;
+      tab.src_in[2 * b + 1] = ins[b0 + b] + ((size_t)2 * last + 1) * n;
+      rt.in[b] = ins[b0 + b];
+      rt.out[b] = outs[b0 + b];
+    }
+    HIPCK(launch_ntt_inv_gather(c, tab, 2 * m, v, last, s));
+    HIPCK(k_rescale_lift_launch(c, v, w, level, 2 * m, s));
+    HIPCK(ntt_rows(c, w, 2 * m, (size_t)last * n, last, 0, false, s));
+    HIPCK(k_rescale_combine_launch(c, rt, m, w, level, T->rs_inv, s));
+  }
   return FESC_OK;
+}
+
+int op_rescale(Context* c, const uint64_t* in, uint64_t* out, uint32_t level, hipStream_t s) {
+  return op_rescale_many(c, 1, &in, &out, level, s);
 }
 
 int op_keygen(Context* c, uint32_t galois, const int8_t* sk, const uint64_t* a, const int64_t* e,

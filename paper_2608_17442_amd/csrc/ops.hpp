@@ -28,9 +28,16 @@ hipError_t k_keygen_launch(const Context* c, const uint64_t* a, const uint64_t* 
 hipError_t k_encrypt_launch(const Context* c, const uint64_t* a, const uint64_t* s,
                             const uint64_t* me, uint64_t* ct, uint32_t level, hipStream_t st);
 hipError_t k_rescale_lift_launch(const Context* c, const uint64_t* v, uint64_t* w,
-                                 uint32_t level, hipStream_t s);
-hipError_t k_rescale_combine_launch(const Context* c, const uint64_t* in, const uint64_t* w,
-                                    uint64_t* out, uint32_t level, const double2* qlinv,
+                                 uint32_t level, uint32_t rows, hipStream_t s);
+
+// Up to kRescaleBatch ciphertexts per batched rescale launch.
+constexpr uint32_t kRescaleBatch = 16;
+struct RsTable {
+  const uint64_t* in[kRescaleBatch];
+  uint64_t* out[kRescaleBatch];
+};
+hipError_t k_rescale_combine_launch(const Context* c, const RsTable& tab, uint32_t count,
+                                    const uint64_t* w, uint32_t level, const double2* qlinv,
                                     hipStream_t s);
 
 // ----------------------------------------------------------- keyswitch.hip
@@ -64,6 +71,8 @@ struct KsTable {
 // centred conversion digits; conversions are fused with the first forward pass)
 hipError_t launch_ntt_inv_sources(const Context* c, const KsTable& tab, uint32_t nsrc,
                                   uint64_t* cc, uint32_t level, const double2* f, hipStream_t s);
+hipError_t launch_ntt_inv_gather(const Context* c, const KsTable& tab, uint32_t nrows,
+                                 uint64_t* out, uint32_t prime, hipStream_t s);
 hipError_t launch_ntt_inv_digits(const Context* c, const RowSel& rs, uint32_t batch,
                                  uint32_t limbs, const double2* f, hipStream_t s);
 hipError_t launch_modup_outer(const Context* c, const LevelTables& T, const uint64_t* cc,
@@ -113,6 +122,9 @@ int op_rotate_batch(Context* c, uint32_t count, const uint64_t* const* ins,
                     const int32_t* steps, uint64_t* const* outs, const uint64_t* const* add2,
                     uint32_t level, hipStream_t s);
 int op_rescale(Context* c, const uint64_t* in, uint64_t* out, uint32_t level, hipStream_t s);
+// Rescale of `count` ciphertexts (batched launches); out[i] may alias in[i].
+int op_rescale_many(Context* c, uint32_t count, const uint64_t* const* ins, uint64_t* const* outs,
+                    uint32_t level, hipStream_t s);
 uint32_t galois_of_step(const Context* c, int32_t step);
 
 }  // namespace fesc
