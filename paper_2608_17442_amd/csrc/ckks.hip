@@ -55,7 +55,7 @@ __global__ __launch_bounds__(kThreads) void k_mul_plain(const uint64_t* ct,
 
 // (d0, d1) into ct layout `d01`, d2 into poly layout `d2`
 __global__ __launch_bounds__(kThreads) void k_tensor(const uint64_t* a, const uint64_t* b,
-                                                     uint64_t* __restrict__ d01,
+                                                     uint64_t* d01,  // may alias a or b
                                                      uint64_t* __restrict__ d2, uint32_t n,
                                                      const PrimeK* __restrict__ pk) {
   const uint32_t i = blockIdx.y;

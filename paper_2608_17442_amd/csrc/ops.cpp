@@ -121,28 +121,30 @@ struct Scratch {
   uint64_t* v;    // [2][N]             rescale: last limb
   uint64_t* w;    // [2][L][N]          rescale: lifted last limb
   uint64_t* ws;   // [3][L][2][N]       ciphertexts of composite operations
+  uint64_t* d2s;  // [B][L][N]          batched products: relinearised parts d2
+  uint64_t* cts;  // [B][L][2][N]       batched composite operations: ciphertexts
 };
 
 int scratch(Context* c, Scratch* s, uint32_t batch = 1) {
   const size_t n = c->n, L = c->L, E = c->L + c->alpha;
   size_t B = batch <= 1 ? 1 : kMaxBatch;
   if (c->scratch_bytes) {  // keep the larger capacity once allocated
-    const size_t per_b = (L + c->dnum * E + 2 * E + 2 * L) * n * 8;
+    const size_t per_b = (L + c->dnum * E + 2 * E + 2 * L + L + 2 * L) * n * 8;
     const size_t fixed = (2 * L + 2 * L + L + 2 + 2 * L + 6 * L) * n * 8;
     if (c->scratch_bytes >= fixed + kMaxBatch * per_b) B = kMaxBatch;
   }
-  const size_t sizes[10] = {2 * L * n,     B * L * n, B * c->dnum * E * n, B * 2 * E * n,
+  const size_t sizes[12] = {2 * L * n,     B * L * n, B * c->dnum * E * n, B * 2 * E * n,
                             B * 2 * L * n, 2 * L * n, L * n,               2 * n,
-                            2 * L * n,     6 * L * n};
+                            2 * L * n,     6 * L * n, B * L * n,           B * 2 * L * n};
   size_t total = 0;
   for (size_t x : sizes) total += x;
   int err;
   uint64_t* base = static_cast<uint64_t*>(scratch_get(c, total * sizeof(uint64_t), &err));
   if (!base) return err;
   s->cap = (uint32_t)B;
-  uint64_t** dst[10] = {&s->cin, &s->cc, &s->ext, &s->acc, &s->y,
-                        &s->d01, &s->d2, &s->v,   &s->w,   &s->ws};
-  for (int i = 0; i < 10; ++i) {
+  uint64_t** dst[12] = {&s->cin, &s->cc, &s->ext, &s->acc, &s->y,   &s->d01,
+                        &s->d2,  &s->v,  &s->w,   &s->ws,  &s->d2s, &s->cts};
+  for (int i = 0; i < 12; ++i) {
     *dst[i] = base;
     base += sizes[i];
   }
@@ -321,16 +323,38 @@ int op_rotate_batch(Context* c, uint32_t count, const uint64_t* const* ins,
   return FESC_OK;
 }
 
-int op_mul_relin(Context* c, const uint64_t* a, const uint64_t* b, uint64_t* out,
-                 uint32_t level, hipStream_t s) {
+// Products a_i * b_i relinearised, in groups of up to kMaxBatch: the tensor
+// writes (d0, d1) straight into out_i and d2 into scratch, and one batched key
+// switch (all jobs share the relinearisation key) adds relin(d2) to out_i.
+// out_i may alias a_i or b_i (the tensor is elementwise).
+int op_mul_relin_many(Context* c, uint32_t count, const uint64_t* const* as,
+                      const uint64_t* const* bs, uint64_t* const* outs, uint32_t level,
+                      hipStream_t s) {
   const uint64_t* key;
   int err;
   if ((err = key_of(c, 0, &key))) return err;
   Scratch S;
-  if ((err = scratch(c, &S))) return err;
-  HIPCK(k_tensor_launch(c, a, b, S.d01, S.d2, level, s));
-  return key_switch_batch(c, level, {KsSource{S.d2, c->n}},
-                          {KsJob{0, key, 0, S.d01, 3u, 0, nullptr, out}}, s);
+  if ((err = scratch(c, &S, count))) return err;
+  const size_t n = c->n;
+  for (uint32_t b0 = 0; b0 < count; b0 += S.cap) {
+    const uint32_t m = std::min(S.cap, count - b0);
+    std::vector<KsSource> srcs;
+    std::vector<KsJob> jobs;
+    for (uint32_t b = 0; b < m; ++b) {
+      uint64_t* d2 = S.d2s + (size_t)b * c->L * n;
+      uint64_t* o = outs[b0 + b];
+      HIPCK(k_tensor_launch(c, as[b0 + b], bs[b0 + b], o, d2, level, s));
+      srcs.push_back(KsSource{d2, n});
+      jobs.push_back(KsJob{b, key, 0, o, 3u, 0, nullptr, o});
+    }
+    if ((err = key_switch_batch(c, level, srcs, jobs, s))) return err;
+  }
+  return FESC_OK;
+}
+
+int op_mul_relin(Context* c, const uint64_t* a, const uint64_t* b, uint64_t* out,
+                 uint32_t level, hipStream_t s) {
+  return op_mul_relin_many(c, 1, &a, &b, &out, level, s);
 }
 
 // Rescale (c - [c mod q_last]) / q_last of up to kRescaleBatch ciphertexts
@@ -438,40 +462,66 @@ int op_plain_from_coeffs(Context* c, const int64_t* m, uint64_t* pt, uint32_t le
 int op_scan_contract(Context* c, const uint64_t* const* h, const uint64_t* const* decay,
                      const uint64_t* const* cfac, uint32_t K, uint32_t d_s,
                      uint64_t* const* out, uint32_t level, hipStream_t s) {
-  Scratch S;
   int err;
-  if ((err = scratch(c, &S))) return err;
-  const size_t n = c->n, W = (size_t)2 * c->L * n;
-  uint64_t* t1 = S.ws;
-  uint64_t* chi = S.ws + W;
-  uint64_t* tmp = S.ws + 2 * W;
   const uint32_t lo = level - 2;
-  for (uint32_t k = 0; k < K; ++k) {
-    if ((err = op_mul_relin(c, decay[k], h[k], t1, level, s))) return err;
-    if ((err = op_rescale(c, t1, t1, level, s))) return err;
-    if ((err = op_mul_relin(c, t1, cfac[k], t1, level - 1, s))) return err;
-    if ((err = op_rescale(c, t1, out[k], level - 1, s))) return err;
-  }
-  auto reduce = [&](uint64_t* x) -> int {
-    for (uint32_t st = d_s / 2; st >= 1; st /= 2) {
-      const int32_t step = (int32_t)st;
-      int e;
-      if ((e = op_rotate_batch(c, 1, &x, &step, &tmp, nullptr, lo, s))) return e;
-      HIPCK(k_binary_launch(c, x, tmp, x, 2 * lo, 1, 0, s));
+  // The batched layout is taken first: the calls below request no more, so
+  // the ciphertext region S.cts stays in place while it is in use.
+  Scratch S;
+  if ((err = scratch(c, &S, 2))) return err;
+  if (S.cap < 2) return fail(FESC_ERR_OOM, "scan-contract needs batched scratch");
+  const size_t W = (size_t)2 * c->L * c->n;
+  const uint32_t G = S.cap & ~1u;  // chunks per group (even, so pairs stay together)
+  for (uint32_t k0 = 0; k0 < K; k0 += G) {
+    const uint32_t m = std::min(G, K - k0);
+    // t_k = RS(relin(RS(relin(a_k * h_k)) * C_k)), each step batched over the
+    // group; the level and level-1 intermediates live in S.cts, only the
+    // final rescale writes out_k (level - 2 limbs)
+    std::vector<uint64_t*> t(m);
+    for (uint32_t k = 0; k < m; ++k) t[k] = S.cts + (size_t)k * W;
+    if ((err = op_mul_relin_many(c, m, decay + k0, h + k0, t.data(), level, s))) return err;
+    if ((err = op_rescale_many(c, m, t.data(), t.data(), level, s))) return err;
+    if ((err = op_mul_relin_many(c, m, t.data(), cfac + k0, t.data(), level - 1, s))) return err;
+    if ((err = op_rescale_many(c, m, t.data(), out + k0, level - 1, s))) return err;
+    uint64_t* const* o = out + k0;
+    const uint32_t P = m / 2;  // complex pairs (2l, 2l+1); an odd last chunk is reduced alone
+    const uint32_t R = P + (m % 2);
+    // x[r]: value being reduced (chi_l = t_2l + i t_2l+1, or the odd chunk);
+    // y[r]: its partner buffer (rotate-and-add ping-pongs between the two).
+    // 2R <= G buffers; the t_k above are dead once out_k is written.
+    std::vector<uint64_t*> x(R), y(R);
+    for (uint32_t r = 0; r < R; ++r) {
+      x[r] = S.cts + (size_t)(2 * r) * W;
+      y[r] = S.cts + (size_t)(2 * r + 1) * W;
     }
-    return FESC_OK;
-  };
-  for (uint32_t l = 0; l + 1 < K; l += 2) {
-    HIPCK(k_monomial_launch(c, out[l + 1], chi, lo, c->n / 2, s));
-    HIPCK(k_binary_launch(c, out[l], chi, chi, 2 * lo, 1, 0, s));
-    if ((err = reduce(chi))) return err;
-    const int32_t cj = INT32_MIN;
-    if ((err = op_rotate_batch(c, 1, &chi, &cj, &tmp, nullptr, lo, s))) return err;
-    HIPCK(k_binary_launch(c, chi, tmp, out[l], 2 * lo, 1, 0, s));
-    HIPCK(k_binary_launch(c, chi, tmp, tmp, 2 * lo, 1, 1, s));
-    HIPCK(k_monomial_launch(c, tmp, out[l + 1], lo, 3 * c->n / 2, s));
+    for (uint32_t l = 0; l < P; ++l) {
+      HIPCK(k_monomial_launch(c, o[2 * l + 1], x[l], lo, c->n / 2, s));
+      HIPCK(k_binary_launch(c, o[2 * l], x[l], x[l], 2 * lo, 1, 0, s));
+    }
+    if (m % 2)
+      HIPCK(hipMemcpyAsync(x[P], o[m - 1], (size_t)2 * lo * c->n * 8, hipMemcpyDeviceToDevice,
+                           s));
+    for (uint32_t st = d_s / 2; st >= 1; st /= 2) {
+      const std::vector<int32_t> steps(R, (int32_t)st);
+      // y = x + rot(x, st)
+      if ((err = op_rotate_batch(c, R, x.data(), steps.data(), y.data(), x.data(), lo, s)))
+        return err;
+      std::swap(x, y);
+    }
+    if (P > 0) {
+      const std::vector<int32_t> cj(P, INT32_MIN);
+      if ((err = op_rotate_batch(c, P, x.data(), cj.data(), y.data(), nullptr, lo, s)))
+        return err;
+      for (uint32_t l = 0; l < P; ++l) {
+        // out_2l = chi + conj(chi);  out_2l+1 = -i (chi - conj(chi)) = X^(3N/2) (chi - conj(chi))
+        HIPCK(k_binary_launch(c, x[l], y[l], o[2 * l], 2 * lo, 1, 0, s));
+        HIPCK(k_binary_launch(c, x[l], y[l], y[l], 2 * lo, 1, 1, s));
+        HIPCK(k_monomial_launch(c, y[l], o[2 * l + 1], lo, 3 * c->n / 2, s));
+      }
+    }
+    if (m % 2)
+      HIPCK(hipMemcpyAsync(o[m - 1], x[P], (size_t)2 * lo * c->n * 8, hipMemcpyDeviceToDevice,
+                           s));
   }
-  if (K % 2 && (err = reduce(out[K - 1]))) return err;
   return FESC_OK;
 }
 

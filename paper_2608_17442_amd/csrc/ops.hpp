@@ -122,6 +122,10 @@ int op_rotate_batch(Context* c, uint32_t count, const uint64_t* const* ins,
                     const int32_t* steps, uint64_t* const* outs, const uint64_t* const* add2,
                     uint32_t level, hipStream_t s);
 int op_rescale(Context* c, const uint64_t* in, uint64_t* out, uint32_t level, hipStream_t s);
+// Relinearised products out_i = a_i * b_i (batched); out_i may alias a_i or b_i.
+int op_mul_relin_many(Context* c, uint32_t count, const uint64_t* const* as,
+                      const uint64_t* const* bs, uint64_t* const* outs, uint32_t level,
+                      hipStream_t s);
 // Rescale of `count` ciphertexts (batched launches); out[i] may alias in[i].
 int op_rescale_many(Context* c, uint32_t count, const uint64_t* const* ins, uint64_t* const* outs,
                     uint32_t level, hipStream_t s);
