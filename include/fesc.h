@@ -269,6 +269,51 @@ int fesc_scan_contract(fesc_ctx* ctx, const uint64_t* const* h, const uint64_t* 
                        const uint64_t* const* cfac, uint32_t chunks, uint32_t d_state,
                        uint64_t* const* out, uint32_t level, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Encrypted affine prefix scan (Sec. "Parallel Prefix Scans", paragraph
+ * "Affine Prefix Composition", Eq. "compact_affine_compose"; Brent-Kung
+ * network of Appendix "Prefix-Network Selection").  `chunks` independent
+ * sequences (state chunks) of L token maps F_k(z) = a_k z + s_k: a[c*L + k]
+ * and s[c*L + k] are device pointers to [level][2][N] ciphertexts, all at
+ * `level` (a: decay broadcast into the chunk's packing; s: additive update).
+ * When R follows E the composition is
+ *     (RS(relin(a_R a_E)),  RS(relin(a_R s_E)) + s_R)
+ * taken at the lower level of the two operands (a higher operand enters
+ * through its leading limbs; s_R through its first level - 1 limbs).  The
+ * Brent-Kung network (up-sweep over the 2^s-aligned positions; down-sweep
+ * from every multiple k of 2^s to k + 2^(s-1); positions past L not computed)
+ * runs in place: on return buffer (c, k) holds in its leading *out_level limbs
+ * ([out_level][2][N]) the inclusive prefix T_1 o ... o T_k, a = product of the
+ * decays and s = the state h_k (the prefix applied to the zero state).
+ * out_level = level - D, D the largest composition depth (2m - 2 for
+ * L = 2^m >= 4, 1 for L = 2, 0 for L = 1).  Two relinearisations per
+ * composition: 2 (2(L - 1) - log2 L) key switches per chunk for L a power of
+ * two.  All 2 L chunks buffers must be distinct.  FESC_ERR_NO_KEY without the
+ * relinearisation key; FESC_ERR_LEVEL if a composition would fall below
+ * level 2. */
+int fesc_affine_scan(fesc_ctx* ctx, uint64_t* const* a, uint64_t* const* s, uint32_t L,
+                     uint32_t chunks, uint32_t level, uint32_t* out_level, void* stream);
+
+/* The same scan by the two-pass resident block schedule (Sec. "Resident
+ * Block Schedule", Eq. "resident-block-schedule"), returning states only.
+ * Blocks of `block` tokens (the last may be partial).  Pass 1 keeps the
+ * summary (last local prefix) of every block but the last; the same network
+ * over the summaries gives the carries G_j = S_{j-1} o ... o S_0; pass 2
+ * replays each block's local prefixes P_{j,t} and writes the state of
+ * P_{j,t} o G_j, i.e. a_P s_G + s_P (one relinearised product; block 0: s_P).
+ * a, s: as for fesc_affine_scan, not modified.  h[c*L + k]: distinct output
+ * buffers of [out_level][2][N], not aliasing inputs.  `workspace`: device
+ * memory of at least the size fesc_affine_scan_resident_info reports (per
+ * chunk one block of tuples and the summaries, at `level`); the info call also
+ * gives out_level (no device work).  Errors as for fesc_affine_scan, and
+ * FESC_ERR_ARG for a short workspace. */
+int fesc_affine_scan_resident_info(fesc_ctx* ctx, uint32_t L, uint32_t chunks, uint32_t block,
+                                   uint32_t level, uint32_t* out_level, size_t* workspace_bytes);
+int fesc_affine_scan_resident(fesc_ctx* ctx, const uint64_t* const* a, const uint64_t* const* s,
+                              uint32_t L, uint32_t chunks, uint32_t block, uint64_t* const* h,
+                              uint32_t level, void* workspace, size_t workspace_bytes,
+                              void* stream);
+
 /* Host helper: CKKS encoding of n = N/2 complex slots (re, im host arrays;
  * im may be NULL) at scale Delta into int64 coefficients, rounded half away
  * from zero; slot j is the evaluation at exp(i pi 5^j / N).  FESC_ERR_ARG if

@@ -1,6 +1,8 @@
 // extern "C" entry points: argument validation, then dispatch to the
 // launchers.  No allocation happens here except through scratch_get().
+#include <algorithm>
 #include <string>
+#include <vector>
 
 #include "fesc_internal.hpp"
 
@@ -107,6 +109,15 @@ int op_scan_contract(Context* c, const uint64_t* const* h, const uint64_t* const
                      uint64_t* const* out, uint32_t level, hipStream_t s);
 int encode(uint32_t log_n, const double* re, const double* im, double scale, int64_t* out);
 int calib_valu(Context* c, int kind, uint32_t iters, double* rate, hipStream_t s);
+int op_affine_scan(Context* c, uint64_t* const* a, uint64_t* const* s, uint32_t L,
+                   uint32_t chunks, uint32_t level, uint32_t* out_level, hipStream_t st);
+size_t affine_scan_resident_words(const Context* c, uint32_t L, uint32_t chunks, uint32_t block,
+                                  uint32_t level);
+int op_affine_scan_resident_level(Context* c, uint32_t L, uint32_t block, uint32_t level,
+                                  uint32_t* out_level);
+int op_affine_scan_resident(Context* c, const uint64_t* const* a, const uint64_t* const* s,
+                            uint32_t L, uint32_t chunks, uint32_t block, uint64_t* const* h,
+                            uint32_t level, uint64_t* ws, uint32_t* out_level, hipStream_t st);
 }  // namespace fesc
 
 #include "ops.hpp"
@@ -285,6 +296,69 @@ int fesc_scan_contract(fesc_ctx* ctx, const uint64_t* const* h, const uint64_t* 
   if (chunks >= 2 && !ctx->keys.count(2 * ctx->n - 1))
     return fail(FESC_ERR_NO_KEY, "no conjugation key");
   return op_scan_contract(ctx, h, decay, cfac, chunks, d_state, out, level, S(stream));
+}
+
+static int scan_args(fesc_ctx* ctx, uint32_t L, uint32_t chunks, uint32_t level) {
+  int rc = check_level(ctx, level);
+  if (rc) return rc;
+  if (L == 0 || chunks == 0 || (uint64_t)L * chunks > (1u << 24))
+    return fail(FESC_ERR_ARG, "need L >= 1, chunks >= 1 and L * chunks <= 2^24");
+  if (!ctx->keys.count(0)) return fail(FESC_ERR_NO_KEY, "no relinearisation key");
+  return FESC_OK;
+}
+
+static bool distinct(std::vector<const void*> p) {
+  std::sort(p.begin(), p.end());
+  return std::adjacent_find(p.begin(), p.end()) == p.end();
+}
+
+int fesc_affine_scan(fesc_ctx* ctx, uint64_t* const* a, uint64_t* const* s, uint32_t L,
+                     uint32_t chunks, uint32_t level, uint32_t* out_level, void* stream) {
+  int rc = scan_args(ctx, L, chunks, level);
+  if (rc) return rc;
+  if (!a || !s || !out_level) return fail(FESC_ERR_ARG, "null argument");
+  std::vector<const void*> all;
+  for (size_t i = 0; i < (size_t)L * chunks; ++i) {
+    if (!a[i] || !s[i]) return fail(FESC_ERR_ARG, "null buffer");
+    all.push_back(a[i]);
+    all.push_back(s[i]);
+  }
+  if (!distinct(all)) return fail(FESC_ERR_ARG, "scan buffers must be distinct");
+  return op_affine_scan(ctx, a, s, L, chunks, level, out_level, S(stream));
+}
+
+int fesc_affine_scan_resident_info(fesc_ctx* ctx, uint32_t L, uint32_t chunks, uint32_t block,
+                                   uint32_t level, uint32_t* out_level, size_t* workspace_bytes) {
+  int rc = scan_args(ctx, L, chunks, level);
+  if (rc) return rc;
+  if (block == 0 || !out_level || !workspace_bytes) return fail(FESC_ERR_ARG, "bad argument");
+  if ((rc = op_affine_scan_resident_level(ctx, L, block, level, out_level))) return rc;
+  *workspace_bytes = affine_scan_resident_words(ctx, L, chunks, block, level) * 8;
+  return FESC_OK;
+}
+
+int fesc_affine_scan_resident(fesc_ctx* ctx, const uint64_t* const* a, const uint64_t* const* s,
+                              uint32_t L, uint32_t chunks, uint32_t block, uint64_t* const* h,
+                              uint32_t level, void* workspace, size_t workspace_bytes,
+                              void* stream) {
+  uint32_t lo;
+  size_t need;
+  int rc = fesc_affine_scan_resident_info(ctx, L, chunks, block, level, &lo, &need);
+  if (rc) return rc;
+  if (!a || !s || !h) return fail(FESC_ERR_ARG, "null argument");
+  if (need && (!workspace || workspace_bytes < need))
+    return fail(FESC_ERR_ARG, "workspace of " + std::to_string(need) + " bytes needed");
+  std::vector<const void*> all;
+  for (size_t i = 0; i < (size_t)L * chunks; ++i) {
+    if (!a[i] || !s[i] || !h[i]) return fail(FESC_ERR_ARG, "null buffer");
+    all.push_back(a[i]);
+    all.push_back(s[i]);
+    all.push_back(h[i]);
+  }
+  if (!distinct(all)) return fail(FESC_ERR_ARG, "scan buffers must be distinct");
+  uint32_t got;
+  return op_affine_scan_resident(ctx, a, s, L, chunks, block, h, level,
+                                 static_cast<uint64_t*>(workspace), &got, S(stream));
 }
 
 int fesc_calib_valu(fesc_ctx* ctx, int kind, uint32_t iters, double* rate, void* stream) {

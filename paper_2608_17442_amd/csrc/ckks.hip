@@ -184,7 +184,8 @@ __global__ __launch_bounds__(kThreads) void k_rescale_lift(const uint64_t* __res
 }
 
 // Rescale, step 2, for ciphertext b = blockIdx.z of the table:
-// out_b[i][t] = (c_b[i][t] - w[2b + t][i]) * q_last^-1 mod q_i.
+// out_b[i][t] = (c_b[i][t] - w[2b + t][i]) * q_last^-1 (+ add_b[i][t]) mod q_i,
+// for the limbs i < gridDim.y.
 __global__ __launch_bounds__(kThreads) void k_rescale_combine(RsTable tab,
                                                               const uint64_t* __restrict__ w,
                                                               uint32_t n, uint32_t last,
@@ -195,13 +196,15 @@ __global__ __launch_bounds__(kThreads) void k_rescale_combine(RsTable tab,
   if (k >= n) return;
   const uint64_t* c = tab.in[b];
   uint64_t* out = tab.out[b];
+  const uint64_t* add = tab.add[b];
   const PrimeK P = pk[i];
   const double2 f = qlinv[i];
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
     const size_t o = ((size_t)2 * i + t) * n + k;
     const double d = ld(c + o) - ld(w + ((size_t)(2 * b + t) * last + i) * n + k);
-    st(out + o, mm_shoup(d, f.x, f.y, P.q), P.q, P.qinv);
+    const double r = mm_shoup(d, f.x, f.y, P.q);  // |r| < 1.5q
+    st(out + o, add ? r + ld(add + o) : r, P.q, P.qinv);
   }
 }
 
@@ -277,9 +280,9 @@ hipError_t k_rescale_lift_launch(const Context* c, const uint64_t* v, uint64_t* 
 }
 
 hipError_t k_rescale_combine_launch(const Context* c, const RsTable& tab, uint32_t count,
-                                    const uint64_t* w, uint32_t level, const double2* qlinv,
-                                    hipStream_t s) {
-  hipLaunchKernelGGL(k_rescale_combine, grid_rows(c->n, level - 1, count), dim3(kThreads), 0, s,
+                                    const uint64_t* w, uint32_t level, uint32_t rows,
+                                    const double2* qlinv, hipStream_t s) {
+  hipLaunchKernelGGL(k_rescale_combine, grid_rows(c->n, rows, count), dim3(kThreads), 0, s,
                      tab, w, c->n, level - 1, qlinv, c->d_pk);
   return hipGetLastError();
 }

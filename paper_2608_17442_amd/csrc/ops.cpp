@@ -360,8 +360,11 @@ int op_mul_relin(Context* c, const uint64_t* a, const uint64_t* b, uint64_t* out
 // Rescale (c - [c mod q_last]) / q_last of up to kRescaleBatch ciphertexts
 // per launch sequence: inverse NTT of every last limb (read in place), lift
 // of the centred coefficients to the other primes, forward NTT, combine.
-int op_rescale_many(Context* c, uint32_t count, const uint64_t* const* ins, uint64_t* const* outs,
-                    uint32_t level, hipStream_t s) {
+int op_rescale_add_many(Context* c, uint32_t count, const uint64_t* const* ins,
+                        uint64_t* const* outs, const uint64_t* const* adds, uint32_t level,
+                        uint32_t out_rows, hipStream_t s) {
+  if (level < 2 || out_rows < 1 || out_rows > level - 1)
+    return fail(FESC_ERR_LEVEL, "rescale needs level >= 2 and 1 <= rows <= level - 1");
   int err;
   const LevelTables* T = level_tables(c, level, &err);
   if (!T) return err;
@@ -382,11 +385,59 @@ int op_rescale_many(Context* c, uint32_t count, const uint64_t* const* ins, uint
       tab.src_in[2 * b + 1] = ins[b0 + b] + ((size_t)2 * last + 1) * n;
       rt.in[b] = ins[b0 + b];
       rt.out[b] = outs[b0 + b];
+      rt.add[b] = adds ? adds[b0 + b] : nullptr;
     }
     HIPCK(launch_ntt_inv_gather(c, tab, 2 * m, v, last, s));
     HIPCK(k_rescale_lift_launch(c, v, w, level, 2 * m, s));
     HIPCK(ntt_rows(c, w, 2 * m, (size_t)last * n, last, 0, false, s));
-    HIPCK(k_rescale_combine_launch(c, rt, m, w, level, T->rs_inv, s));
+    HIPCK(k_rescale_combine_launch(c, rt, m, w, level, out_rows, T->rs_inv, s));
+  }
+  return FESC_OK;
+}
+
+int op_rescale_many(Context* c, uint32_t count, const uint64_t* const* ins, uint64_t* const* outs,
+                    uint32_t level, hipStream_t s) {
+  return op_rescale_add_many(c, count, ins, outs, nullptr, level, level - 1, s);
+}
+
+uint32_t prod_group(Context* c, int* err) {
+  Scratch S;
+  if ((*err = scratch(c, &S, 2))) return 0;
+  return S.cap & ~1u;
+}
+
+int op_prod_rescale_many(Context* c, uint32_t count, const uint64_t* const* xs,
+                         const uint64_t* const* ys, uint64_t* const* outs,
+                         const uint64_t* const* adds, uint32_t level, uint32_t out_rows,
+                         hipStream_t s) {
+  if (level < 2 || out_rows < 1 || out_rows > level - 1)
+    return fail(FESC_ERR_LEVEL, "product needs level >= 2 and 1 <= rows <= level - 1");
+  const uint64_t* key;
+  int err;
+  if ((err = key_of(c, 0, &key))) return err;
+  // the batched layout first: the calls below keep it, so S.cts and S.d2s
+  // stay in place
+  Scratch S;
+  if ((err = scratch(c, &S, 2))) return err;
+  const uint32_t G = S.cap & ~1u;
+  if (G < 2) return fail(FESC_ERR_OOM, "batched products need batched scratch");
+  const size_t n = c->n, W = (size_t)2 * c->L * n;
+  std::vector<uint64_t*> t(G);
+  for (uint32_t b = 0; b < G; ++b) t[b] = S.cts + (size_t)b * W;
+  for (uint32_t g0 = 0; g0 < count; g0 += G) {
+    const uint32_t m = std::min(G, count - g0);
+    std::vector<KsSource> srcs;
+    std::vector<KsJob> jobs;
+    for (uint32_t b = 0; b < m; ++b) {
+      uint64_t* d2 = S.d2s + (size_t)b * c->L * n;
+      HIPCK(k_tensor_launch(c, xs[g0 + b], ys[g0 + b], t[b], d2, level, s));
+      srcs.push_back(KsSource{d2, n});
+      jobs.push_back(KsJob{b, key, 0, t[b], 3u, 0, nullptr, t[b]});
+    }
+    if ((err = key_switch_batch(c, level, srcs, jobs, s))) return err;
+    if ((err = op_rescale_add_many(c, m, t.data(), outs + g0, adds ? adds + g0 : nullptr, level,
+                                   out_rows, s)))
+      return err;
   }
   return FESC_OK;
 }

@@ -35,10 +35,12 @@ constexpr uint32_t kRescaleBatch = 16;
 struct RsTable {
   const uint64_t* in[kRescaleBatch];
   uint64_t* out[kRescaleBatch];
+  const uint64_t* add[kRescaleBatch];  // added after the division (or null)
 };
+// Writes the first `rows` (<= level - 1) limbs of each output.
 hipError_t k_rescale_combine_launch(const Context* c, const RsTable& tab, uint32_t count,
-                                    const uint64_t* w, uint32_t level, const double2* qlinv,
-                                    hipStream_t s);
+                                    const uint64_t* w, uint32_t level, uint32_t rows,
+                                    const double2* qlinv, hipStream_t s);
 
 // ----------------------------------------------------------- keyswitch.hip
 
@@ -129,6 +131,23 @@ int op_mul_relin_many(Context* c, uint32_t count, const uint64_t* const* as,
 // Rescale of `count` ciphertexts (batched launches); out[i] may alias in[i].
 int op_rescale_many(Context* c, uint32_t count, const uint64_t* const* ins, uint64_t* const* outs,
                     uint32_t level, hipStream_t s);
+// out_i = RS(in_i) + add_i (adds null, or add_i null: no addend), only the
+// first out_rows limbs (1 <= out_rows <= level - 1) written.  out_i may alias
+// in_i or add_i.
+int op_rescale_add_many(Context* c, uint32_t count, const uint64_t* const* ins,
+                        uint64_t* const* outs, const uint64_t* const* adds, uint32_t level,
+                        uint32_t out_rows, hipStream_t s);
+// Products out_i = RS(relin(x_i * y_i)) + add_i at `level`, first out_rows
+// limbs written.  Runs in groups of the scratch capacity (an even number):
+// every tensor of a group is formed before any output of the group is
+// written, so an output may alias an input of a product in its own group;
+// it must not alias an input of a product in a later group.
+int op_prod_rescale_many(Context* c, uint32_t count, const uint64_t* const* xs,
+                         const uint64_t* const* ys, uint64_t* const* outs,
+                         const uint64_t* const* adds, uint32_t level, uint32_t out_rows,
+                         hipStream_t s);
+// Scratch capacity (products per group of op_prod_rescale_many).
+uint32_t prod_group(Context* c, int* err);
 uint32_t galois_of_step(const Context* c, int32_t step);
 
 }  // namespace fesc

@@ -1,0 +1,286 @@
+// Host driver of the encrypted affine prefix scan of HEScan (Sec. "Parallel
+// Prefix Scans", paragraph "Affine Prefix Composition", Eq.
+// "compact_affine_compose"; Brent-Kung network of Appendix "Prefix-Network
+// Selection"; Sec. "Resident Block Schedule", Eq. "resident-block-schedule").
+//
+// A token map is the ciphertext pair (a, s) for F(z) = a z + s; R after L
+// composes to (a_R a_L, a_R s_L + s_R).  One composition is two products at
+// the lower level l of its operands, each relinearised and rescaled:
+//     a' = RS(relin(a_R a_L)),   s' = RS(relin(a_R s_L)) + s_R   (level l - 1)
+// where s_R enters through its first l - 1 limbs.  Ciphertexts are
+// [level][2][N] limb-major, so dropping to a lower level is taking a prefix of
+// the buffer: no copies are made for it.
+//
+// Every stage of the network is one batch: its nodes are independent (no
+// node reads a position another node of the stage writes), so the nodes of a
+// stage, over all chunks, are grouped by level and run as batched products
+// (tensors, one batched key switch sharing the relinearisation key, batched
+// rescales with the addend fused into the final combine).  The two products
+// of a node always fall in the same product group, so the node may write in
+// place over the operands it reads.
+#include <algorithm>
+#include <map>
+#include <vector>
+
+#include "fesc_internal.hpp"
+#include "ops.hpp"
+
+namespace fesc {
+
+namespace {
+
+#define HIPCK_RET(expr)                                \
+  do {                                                 \
+    hipError_t e_ = (expr);                            \
+    if (e_ != hipSuccess) return hip_check(e_, #expr); \
+  } while (0)
+
+struct Node {
+  uint32_t dst, src;  // 0-based positions; dst takes src o dst
+};
+using Stages = std::vector<std::vector<Node>>;
+
+// Brent-Kung network over L positions (padded to L' = 2^ceil(log2 L); nodes
+// whose destination lies past L are left out: no node reads a position above
+// its destination, so valid prefixes do not depend on them).  Up-sweep stage
+// s: each 2^s-aligned position takes the one 2^(s-1) to its left; down-sweep
+// stage s: each multiple k of 2^s passes its prefix to k + 2^(s-1).
+Stages bk_network(uint32_t L) {
+  Stages st;
+  if (L < 2) return st;
+  uint32_t m = 0;
+  while ((1u << m) < L) ++m;
+  const uint32_t Lp = 1u << m;
+  for (uint32_t s = 1; s <= m; ++s) {
+    std::vector<Node> v;
+    for (uint32_t k = 1u << s; k <= Lp; k += 1u << s)
+      if (k <= L) v.push_back(Node{k - 1, k - 1 - (1u << (s - 1))});
+    st.push_back(v);
+  }
+  for (uint32_t s = m - 1; s >= 1; --s) {
+    std::vector<Node> v;
+    for (uint32_t k = 1u << s; k <= Lp; k += 1u << s) {
+      const uint32_t j = k + (1u << (s - 1));
+      if (j <= L) v.push_back(Node{j - 1, k - 1});
+    }
+    st.push_back(v);
+  }
+  return st;
+}
+
+// Only the nodes the last position depends on (a block summary).
+Stages prune_to_last(const Stages& st, uint32_t L) {
+  std::vector<char> need(L, 0);
+  need[L - 1] = 1;
+  Stages out(st.size());
+  for (size_t i = st.size(); i-- > 0;)
+    for (const Node& nd : st[i])
+      if (need[nd.dst]) {
+        out[i].push_back(nd);
+        need[nd.src] = 1;
+      }
+  return out;
+}
+
+// One chunk's positions: the buffers holding their current values and the
+// buffers a composition writes to.
+struct Seq {
+  std::vector<const uint64_t*> cur_a, cur_s;
+  std::vector<uint64_t*> home_a, home_s;
+};
+
+// Runs the stages over all chunks; lvl[] (shared by the chunks, which have
+// the same structure) tracks each position's level.  dry: levels only.
+int run_stages(Context* c, const Stages& st, std::vector<Seq>& seqs, std::vector<uint32_t>& lvl,
+               bool dry, hipStream_t s) {
+  for (const auto& stage : st) {
+    std::map<uint32_t, std::vector<Node>> by_level;
+    for (const Node& nd : stage) by_level[std::min(lvl[nd.dst], lvl[nd.src])].push_back(nd);
+    for (const auto& kv : by_level) {
+      const uint32_t l = kv.first;
+      if (l < 2) return fail(FESC_ERR_LEVEL, "affine scan needs more levels than the input has");
+      if (!dry) {
+        std::vector<const uint64_t*> xs, ys, adds;
+        std::vector<uint64_t*> outs;
+        for (Seq& q : seqs)
+          for (const Node& nd : kv.second) {
+            // state part first, then the decay part (both read a_dst)
+            xs.push_back(q.cur_a[nd.dst]);
+            ys.push_back(q.cur_s[nd.src]);
+            outs.push_back(q.home_s[nd.dst]);
+            adds.push_back(q.cur_s[nd.dst]);
+            xs.push_back(q.cur_a[nd.dst]);
+            ys.push_back(q.cur_a[nd.src]);
+            outs.push_back(q.home_a[nd.dst]);
+            adds.push_back(nullptr);
+          }
+        int err = op_prod_rescale_many(c, (uint32_t)xs.size(), xs.data(), ys.data(), outs.data(),
+                                       adds.data(), l, l - 1, s);
+        if (err) return err;
+      }
+      for (const Node& nd : kv.second) {
+        for (Seq& q : seqs) {
+          q.cur_a[nd.dst] = q.home_a[nd.dst];
+          q.cur_s[nd.dst] = q.home_s[nd.dst];
+        }
+        lvl[nd.dst] = l - 1;
+      }
+    }
+  }
+  return FESC_OK;
+}
+
+uint32_t min_level(const std::vector<uint32_t>& lvl) {
+  return *std::min_element(lvl.begin(), lvl.end());
+}
+
+}  // namespace
+
+int op_affine_scan(Context* c, uint64_t* const* a, uint64_t* const* s, uint32_t L,
+                   uint32_t chunks, uint32_t level, uint32_t* out_level, hipStream_t st) {
+  const Stages net = bk_network(L);
+  std::vector<uint32_t> lvl(L, level);
+  std::vector<Seq> none;
+  int err;
+  if ((err = run_stages(c, net, none, lvl, true, st))) return err;
+  std::vector<Seq> seqs(chunks);
+  for (uint32_t ch = 0; ch < chunks; ++ch) {
+    Seq& q = seqs[ch];
+    for (uint32_t k = 0; k < L; ++k) {
+      q.cur_a.push_back(a[(size_t)ch * L + k]);
+      q.cur_s.push_back(s[(size_t)ch * L + k]);
+      q.home_a.push_back(a[(size_t)ch * L + k]);
+      q.home_s.push_back(s[(size_t)ch * L + k]);
+    }
+  }
+  lvl.assign(L, level);
+  if ((err = run_stages(c, net, seqs, lvl, false, st))) return err;
+  *out_level = min_level(lvl);
+  return FESC_OK;
+}
+
+size_t affine_scan_resident_words(const Context* c, uint32_t L, uint32_t chunks, uint32_t block,
+                                  uint32_t level) {
+  const size_t K = (L + block - 1) / block;
+  return (size_t)chunks * (2 * block + 2 * (K - 1)) * 2 * level * c->n;
+}
+
+// Two passes over blocks of `block` tokens: pass 1 builds the summary (last
+// local prefix) of every block but the last, an exclusive scan over the
+// summaries (the same network) gives the carries G_j, pass 2 replays each
+// block and writes the states of its corrected prefixes P_{j,t} o G_j:
+//     h = a_P G_s + s_P  (j >= 1),   h = s_P  (j = 0).
+// The workspace holds, per chunk, one block of tuples and the summaries:
+// [chunk][2 block + 2 (K - 1)][level][2][N].
+static int resident(Context* c, const uint64_t* const* a, const uint64_t* const* s, uint32_t L,
+                    uint32_t chunks, uint32_t block, uint64_t* const* h, uint32_t level,
+                    uint32_t out_level, uint64_t* ws, bool dry, uint32_t* min_out,
+                    hipStream_t st) {
+  const uint32_t K = (L + block - 1) / block;
+  const size_t W = (size_t)2 * level * c->n;
+  const size_t per_chunk = (size_t)(2 * block + 2 * (K - 1)) * W;
+  auto blk_a = [&](uint32_t ch, uint32_t t) { return ws + ch * per_chunk + (size_t)t * W; };
+  auto blk_s = [&](uint32_t ch, uint32_t t) {
+    return ws + ch * per_chunk + (size_t)(block + t) * W;
+  };
+  auto sum_a = [&](uint32_t ch, uint32_t j) {
+    return ws + ch * per_chunk + (size_t)(2 * block + j) * W;
+  };
+  auto sum_s = [&](uint32_t ch, uint32_t j) {
+    return ws + ch * per_chunk + (size_t)(2 * block + (K - 1) + j) * W;
+  };
+  auto in_seq = [&](uint32_t ch, uint32_t j, uint32_t Bj, bool summary) {
+    Seq q;
+    for (uint32_t t = 0; t < Bj; ++t) {
+      const size_t idx = (size_t)ch * L + (size_t)j * block + t;
+      q.cur_a.push_back(dry ? nullptr : a[idx]);
+      q.cur_s.push_back(dry ? nullptr : s[idx]);
+      const bool last = summary && t == Bj - 1;
+      q.home_a.push_back(dry ? nullptr : last ? sum_a(ch, j) : blk_a(ch, t));
+      q.home_s.push_back(dry ? nullptr : last ? sum_s(ch, j) : blk_s(ch, t));
+    }
+    return q;
+  };
+  const uint32_t nseq = dry ? 1 : chunks;
+  int err;
+  // pass 1: summaries of blocks 0 .. K-2
+  const Stages summary_net = prune_to_last(bk_network(block), block);
+  std::vector<Seq> carry(nseq);
+  std::vector<uint32_t> lvl_sum;
+  for (uint32_t j = 0; j + 1 < K; ++j) {
+    std::vector<Seq> seqs;
+    for (uint32_t ch = 0; ch < nseq; ++ch) seqs.push_back(in_seq(ch, j, block, true));
+    std::vector<uint32_t> lvl(block, level);
+    if ((err = run_stages(c, summary_net, seqs, lvl, dry, st))) return err;
+    lvl_sum.push_back(lvl[block - 1]);
+    for (uint32_t ch = 0; ch < nseq; ++ch) {
+      carry[ch].cur_a.push_back(seqs[ch].cur_a[block - 1]);
+      carry[ch].cur_s.push_back(seqs[ch].cur_s[block - 1]);
+      carry[ch].home_a.push_back(dry ? nullptr : sum_a(ch, j));
+      carry[ch].home_s.push_back(dry ? nullptr : sum_s(ch, j));
+    }
+  }
+  // exclusive scan over the summaries: G_j = carry position j - 1
+  if (K > 1 && (err = run_stages(c, bk_network(K - 1), carry, lvl_sum, dry, st))) return err;
+  // pass 2: replay and carry injection
+  uint32_t lo = level;
+  for (uint32_t j = 0; j < K; ++j) {
+    const uint32_t Bj = std::min(block, L - j * block);
+    std::vector<Seq> seqs;
+    for (uint32_t ch = 0; ch < nseq; ++ch) seqs.push_back(in_seq(ch, j, Bj, false));
+    std::vector<uint32_t> lvl(Bj, level);
+    if ((err = run_stages(c, bk_network(Bj), seqs, lvl, dry, st))) return err;
+    if (j == 0) {
+      lo = std::min(lo, min_level(lvl));
+      if (!dry)
+        for (uint32_t ch = 0; ch < chunks; ++ch)
+          for (uint32_t t = 0; t < Bj; ++t)
+            HIPCK_RET(hipMemcpyAsync(h[(size_t)ch * L + t], seqs[ch].cur_s[t],
+                                     (size_t)2 * out_level * c->n * 8, hipMemcpyDeviceToDevice,
+                                     st));
+      continue;
+    }
+    std::map<uint32_t, std::vector<uint32_t>> by_level;
+    for (uint32_t t = 0; t < Bj; ++t) by_level[std::min(lvl[t], lvl_sum[j - 1])].push_back(t);
+    for (const auto& kv : by_level) {
+      const uint32_t l = kv.first;
+      if (l < 2) return fail(FESC_ERR_LEVEL, "affine scan needs more levels than the input has");
+      lo = std::min(lo, l - 1);
+      if (dry) continue;
+      std::vector<const uint64_t*> xs, ys, adds;
+      std::vector<uint64_t*> outs;
+      for (uint32_t ch = 0; ch < chunks; ++ch)
+        for (uint32_t t : kv.second) {
+          xs.push_back(seqs[ch].cur_a[t]);
+          ys.push_back(carry[ch].cur_s[j - 1]);
+          adds.push_back(seqs[ch].cur_s[t]);
+          outs.push_back(h[(size_t)ch * L + (size_t)j * block + t]);
+        }
+      if ((err = op_prod_rescale_many(c, (uint32_t)xs.size(), xs.data(), ys.data(), outs.data(),
+                                      adds.data(), l, out_level, st)))
+        return err;
+    }
+  }
+  *min_out = lo;
+  return FESC_OK;
+}
+
+int op_affine_scan_resident_level(Context* c, uint32_t L, uint32_t block, uint32_t level,
+                                  uint32_t* out_level) {
+  return resident(c, nullptr, nullptr, L, 1, block, nullptr, level, 0, nullptr, true, out_level,
+                  nullptr);
+}
+
+int op_affine_scan_resident(Context* c, const uint64_t* const* a, const uint64_t* const* s,
+                            uint32_t L, uint32_t chunks, uint32_t block, uint64_t* const* h,
+                            uint32_t level, uint64_t* ws, uint32_t* out_level, hipStream_t st) {
+  uint32_t lo;
+  int err;
+  if ((err = op_affine_scan_resident_level(c, L, block, level, &lo))) return err;
+  uint32_t got;
+  if ((err = resident(c, a, s, L, chunks, block, h, level, lo, ws, false, &got, st))) return err;
+  *out_level = lo;
+  return FESC_OK;
+}
+
+}  // namespace fesc

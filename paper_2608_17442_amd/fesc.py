@@ -61,6 +61,12 @@ _SIGS = {
     "fesc_scan_contract": [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp), ctypes.POINTER(_vp),
                            _u32, _u32, ctypes.POINTER(_vp), _u32, _vp],
     "fesc_calib_valu": [_vp, ctypes.c_int, _u32, ctypes.POINTER(ctypes.c_double), _vp],
+    "fesc_affine_scan": [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp), _u32, _u32, _u32,
+                         ctypes.POINTER(_u32), _vp],
+    "fesc_affine_scan_resident_info": [_vp, _u32, _u32, _u32, _u32, ctypes.POINTER(_u32),
+                                       ctypes.POINTER(_sz)],
+    "fesc_affine_scan_resident": [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp), _u32, _u32,
+                                  _u32, ctypes.POINTER(_vp), _u32, _vp, _sz, _vp],
 }
 
 CONJ = -(2 ** 31)
@@ -221,6 +227,32 @@ class Context:
         arr = lambda ts: (_vp * K)(*[_ptr(t) for t in ts])
         _check(_lib.fesc_scan_contract(self._h, arr(h), arr(decay), arr(cfac), K, d_state,
                                        arr(outs), level, _stream(stream)))
+
+    def affine_scan(self, a, s, chunks, level, stream=None) -> int:
+        """In-place Brent-Kung scan of `chunks` sequences of len(a) // chunks
+        token maps (a[c*L + k], s[c*L + k]); returns the output level."""
+        n = len(a)
+        arr = lambda ts: (_vp * n)(*[_ptr(t) for t in ts])
+        out = _u32()
+        _check(_lib.fesc_affine_scan(self._h, arr(a), arr(s), n // chunks, chunks, level,
+                                     ctypes.byref(out), _stream(stream)))
+        return int(out.value)
+
+    def affine_scan_resident_info(self, L, chunks, block, level):
+        """(output level, workspace bytes) of the resident schedule."""
+        lo, ws = _u32(), _sz()
+        _check(_lib.fesc_affine_scan_resident_info(self._h, L, chunks, block, level,
+                                                   ctypes.byref(lo), ctypes.byref(ws)))
+        return int(lo.value), int(ws.value)
+
+    def affine_scan_resident(self, a, s, chunks, block, h, level, workspace, stream=None):
+        """States of the resident block schedule into h (see the C header)."""
+        n = len(a)
+        arr = lambda ts: (_vp * n)(*[_ptr(t) for t in ts])
+        ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+        _check(_lib.fesc_affine_scan_resident(self._h, arr(a), arr(s), n // chunks, chunks, block,
+                                              arr(h), level, _ptr(workspace) if ws_bytes else None,
+                                              ws_bytes, _stream(stream)))
 
     def key_words(self) -> int:
         return self.dnum * (self.L + self.alpha) * 2 * self.n
