@@ -16,8 +16,16 @@ Metric (three workloads, all N = 2^16 with ~50-bit primes = 1 mod 2N; the
          and rescale -> 48 ciphertexts (seed 3); 18,432 pre-encoded diagonals
          (154.6 GB) resident in HBM.
 
-One step runs all three.  `value` is the NTT GB/s (the headline
-configuration); keyswitch/s and matvec ms are reported in `components`.
+  SCAN   scan-contract slice of one Mamba-base token (24 heads x 64 channels
+         x d_state 128 in 12 state chunks of 16,384 slots, level 20 -> 18,
+         seed 4): products with decay and C, rotate-and-add over d_state,
+         complex-paired conjugation split.
+
+One step runs all four.  `value` is the NTT GB/s (the headline
+configuration); keyswitch/s, matvec ms and scan-contract ms are reported in
+`components`.  After the steps, the HEScan affine prefix scan (Brent-Kung,
+128 tokens x 12 state chunks at 16 limbs, uniform residues: the arithmetic
+is data-oblivious) is timed on its own as `components.affine_scan`.
 Prints ONE JSON line on stdout.  --gpus > 1 is refused (single-GPU build).
 """
 from __future__ import annotations
@@ -97,6 +105,7 @@ class Workloads:
         self.skip_matvec = skip_matvec
         if not skip_matvec:
             self.setup_matvec()
+        self.setup_scan_contract()
 
     def dev(self, a):
         a = self.np.ascontiguousarray(a)
@@ -213,6 +222,66 @@ class Workloads:
         self.mv_plan(self.mv_in, self.mv_out)
         ev[1].record()
 
+    # ---- scan-contract slice: one Mamba-base token, 12 state chunks
+    def setup_scan_contract(self):
+        np, WL = self.np, self.WL
+        cfg = WL.CFG5
+        seed, level, d_s, hd = cfg["seed"], cfg["level"], cfg["d_state"], cfg["head_dim"]
+        n_slots, s_state = self.n // 2, 16384
+        log("scan-contract keys and ciphertexts")
+        for st in [d_s >> k for k in range(1, 8)]:
+            self.keygen(self.ctx.galois_element(st), seed)
+        self.keygen(2 * self.n - 1, seed)
+        self.keygen(0, seed)
+        z, cvec, H = WL.cfg5_token(0)
+        K = cfg["heads"] * hd * d_s // s_state
+        decay = 1.0 / (1.0 + np.exp(z))
+        c_state = s_state // d_s
+        j = np.arange(n_slots)
+        self.sc_in = ([], [], [])
+        for k in range(K):
+            # chunk k: channel e = k c_state + j // d_s at slots (j // d_s) d_s + j % d_s
+            e, i = k * c_state + j // d_s, j % d_s
+            ok = j < s_state
+            e = np.minimum(e, H.shape[0] - 1)
+            vals = (np.where(ok, H[e, i], 0.0), np.where(ok, decay[e // hd], 0.0),
+                    np.where(ok, cvec[i], 0.0))
+            scales = (2.0 ** 40, float(self.q[level - 1]), float(self.q[level - 2]))
+            for r in range(3):
+                self.sc_in[r].append(self.encrypt(vals[r].astype(complex), scales[r], level, seed,
+                                                  "cfg5", 3 * k + r))
+        self.sc_out = [self.torch.empty((level - 2) * 2 * self.n, dtype=self.torch.int64,
+                                        device="cuda") for _ in range(K)]
+        self.sc_shape = dict(chunks=K, d_state=d_s, level=level)
+
+    def run_scan_contract(self, ev):
+        ev[0].record()
+        h, dec, cf_ = self.sc_in
+        self.ctx.scan_contract(h, dec, cf_, self.sc_shape["d_state"], self.sc_out,
+                               self.sc_shape["level"])
+        ev[1].record()
+
+    # ---- affine prefix scan (HEScan): Brent-Kung over 128 tokens x 12 chunks
+    def setup_affine(self, L=128, chunks=12, level=16):
+        torch = self.torch
+        self.keygen(0, self.WL.CFG5["seed"])
+        words = level * 2 * self.n
+        log(f"affine-scan inputs ({2 * L * chunks * words * 8 / 1e9:.1f} GB)")
+        # residues below 2^49 are valid for every prime here (all exceed 2^49);
+        # the modular arithmetic is data-oblivious, so timing needs no encryption
+        self.af_buf = torch.randint(0, 1 << 49, (2 * L * chunks, words), dtype=torch.int64,
+                                    device="cuda")
+        self.af_a = [self.af_buf[i] for i in range(L * chunks)]
+        self.af_s = [self.af_buf[L * chunks + i] for i in range(L * chunks)]
+        self.af_shape = dict(L=L, chunks=chunks, level=level)
+
+    def run_affine(self, ev):
+        sh = self.af_shape
+        ev[0].record()
+        lo = self.ctx.affine_scan(self.af_a, self.af_s, sh["chunks"], sh["level"])
+        ev[1].record()
+        return lo
+
 
 # ---------------------------------------------------------------- baseline
 
@@ -274,6 +343,8 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-affine", action="store_true",
+                    help="skip the affine prefix scan component (timed after the steps)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run one 1 GiB device-to-device copy, the reference kernel for "
                          "scaling hardware traffic counters")
@@ -308,12 +379,16 @@ def main():
         W.run_ntt(ev["ntt"])
         W.run_ks(ev["ks"])
         W.run_matvec(ev["mv"])
+        W.run_scan_contract(ev["sc"])
+
+    def step_events():
+        return {"ntt": new_events(4), "ks": new_events(2), "mv": new_events(2),
+                "sc": new_events(2)}
 
     for _ in range(args.warmup):
-        step({"ntt": new_events(4), "ks": new_events(2), "mv": new_events(2)})
+        step(step_events())
     torch.cuda.synchronize()
-    evs = [{"ntt": new_events(4), "ks": new_events(2), "mv": new_events(2)}
-           for _ in range(args.steps)]
+    evs = [step_events() for _ in range(args.steps)]
     phases = []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -331,7 +406,28 @@ def main():
     inv = float(np.mean([el(e["ntt"], 2, 3) for e in evs]))
     ks = float(np.mean([el(e["ks"], 0, 1) for e in evs]))
     mv = float(np.median([el(e["mv"], 0, 1) for e in evs]))
+    sc = float(np.median([el(e["sc"], 0, 1) for e in evs]))
     baby_ms, ptmac_ms, tail_ms = phases[-1]
+    # HEScan affine prefix scan, timed after the steps with the projection's
+    # diagonal bank released (its 128 x 12 x 2 ciphertexts take 51.5 GB)
+    affine = None
+    if not args.no_affine:
+        del W.mv_plan, W.bank
+        torch.cuda.empty_cache()
+        W.setup_affine()
+        W.run_affine(new_events(2))          # warm-up (in place; the arithmetic is
+        torch.cuda.synchronize()             # data-oblivious, so reruns are timed alike)
+        aev = [new_events(2) for _ in range(2)]
+        lo = [W.run_affine(e) for e in aev]
+        torch.cuda.synchronize()
+        af_ms = float(np.mean([el(e, 0, 1) for e in aev]))
+        sh = W.af_shape
+        Lp, m = sh["L"], sh["L"].bit_length() - 1
+        n_ks = 2 * sh["chunks"] * (2 * (Lp - 1) - m)
+        affine = {"tokens": sh["L"], "chunks": sh["chunks"], "level_in": sh["level"],
+                  "level_out": lo[-1], "ms": round(af_ms, 2), "key_switches": n_ks,
+                  "keyswitch_per_s": round(n_ks / (af_ms * 1e-3), 1),
+                  "network": "Brent-Kung, in place, stages batched over chunks"}
     n, rows = W.n, W.limbs * W.batch
     bytes_dir = 2 * 8 * n * rows
     ntt_gbs = 2 * bytes_dir / ((fwd + inv) * 1e-3) / 1e9
@@ -372,11 +468,13 @@ def main():
         "vs_baseline": None,
         "dtype": "u64 residues, fp64 modular arithmetic",
         "data": "synthetic (uniform residues seed 1; U[-1,1] slots seed 2; N(0,1) x N(0,0.02^2) "
-                "projection seed 3)",
+                "projection seed 3; N(0,1) Mamba-base token seed 4; uniform residues for the "
+                "affine scan)",
         "config": {"workload": "N=2^16, 24 limbs: NTT microbench (64 polys fwd + 64-pair MAC + "
                                "inv) + 32-ciphertext rotation set (30 key switches, dnum 3, 8 "
                                "special primes) + 768x1536 BSGS projection (12 -> 48 cts, "
-                               "16 limbs)",
+                               "16 limbs) + scan-contract slice of one Mamba-base token "
+                               "(12 state chunks, 20 -> 18 limbs)",
                    "log_n": 16, "limbs": 24, "special_primes": 8, "parallelism": "single GPU"},
         "components": {
             "ntt_gbs": round(ntt_gbs, 2),
@@ -387,6 +485,8 @@ def main():
             "matvec_ms": round(mv, 3),
             "matvec_phases_ms": {"baby_steps": round(baby_ms, 3), "pt_mac": round(ptmac_ms, 3),
                                  "giant_conj_rescale": round(tail_ms, 3)},
+            "scan_contract_ms": round(sc, 3),
+            "affine_scan": affine,
         },
         "roofline": {
             "bound": "hbm", "kernel": "k_ptmac (projection plaintext-diagonal MAC)",
