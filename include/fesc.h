@@ -288,11 +288,20 @@ int fesc_scan_contract(fesc_ctx* ctx, const uint64_t* const* h, const uint64_t* 
  * out_level = level - D, D the largest composition depth (2m - 2 for
  * L = 2^m >= 4, 1 for L = 2, 0 for L = 1).  Two relinearisations per
  * composition: 2 (2(L - 1) - log2 L) key switches per chunk for L a power of
- * two.  All 2 L chunks buffers must be distinct.  FESC_ERR_NO_KEY without the
- * relinearisation key; FESC_ERR_LEVEL if a composition would fall below
- * level 2. */
+ * two.  flags FESC_SCAN_STATES_ONLY: only the states are wanted; decay
+ * products no later product reads are skipped (about a quarter of all
+ * products; the a buffers then hold no defined result).  All 2 L chunks
+ * buffers must be distinct.  FESC_ERR_NO_KEY without the relinearisation key;
+ * FESC_ERR_LEVEL if a composition would fall below level 2. */
+#define FESC_SCAN_STATES_ONLY 1u
 int fesc_affine_scan(fesc_ctx* ctx, uint64_t* const* a, uint64_t* const* s, uint32_t L,
-                     uint32_t chunks, uint32_t level, uint32_t* out_level, void* stream);
+                     uint32_t chunks, uint32_t level, uint32_t flags, uint32_t* out_level,
+                     void* stream);
+
+/* Output level and number of relinearised products (= key switches) per
+ * chunk of fesc_affine_scan with these arguments; no device work. */
+int fesc_affine_scan_info(fesc_ctx* ctx, uint32_t L, uint32_t level, uint32_t flags,
+                          uint32_t* out_level, uint64_t* key_switches);
 
 /* The same scan by the two-pass resident block schedule (Sec. "Resident
  * Block Schedule", Eq. "resident-block-schedule"), returning states only.
@@ -305,10 +314,13 @@ int fesc_affine_scan(fesc_ctx* ctx, uint64_t* const* a, uint64_t* const* s, uint
  * buffers of [out_level][2][N], not aliasing inputs.  `workspace`: device
  * memory of at least the size fesc_affine_scan_resident_info reports (per
  * chunk one block of tuples and the summaries, at `level`); the info call also
- * gives out_level (no device work).  Errors as for fesc_affine_scan, and
- * FESC_ERR_ARG for a short workspace. */
+ * gives out_level and the relinearised products per chunk (no device work).
+ * Block 0 and the carries are used through their states only, so dead decay
+ * products are skipped there as in FESC_SCAN_STATES_ONLY.  Errors as for
+ * fesc_affine_scan, and FESC_ERR_ARG for a short workspace. */
 int fesc_affine_scan_resident_info(fesc_ctx* ctx, uint32_t L, uint32_t chunks, uint32_t block,
-                                   uint32_t level, uint32_t* out_level, size_t* workspace_bytes);
+                                   uint32_t level, uint32_t* out_level, size_t* workspace_bytes,
+                                   uint64_t* key_switches);
 int fesc_affine_scan_resident(fesc_ctx* ctx, const uint64_t* const* a, const uint64_t* const* s,
                               uint32_t L, uint32_t chunks, uint32_t block, uint64_t* const* h,
                               uint32_t level, void* workspace, size_t workspace_bytes,

@@ -110,11 +110,14 @@ int op_scan_contract(Context* c, const uint64_t* const* h, const uint64_t* const
 int encode(uint32_t log_n, const double* re, const double* im, double scale, int64_t* out);
 int calib_valu(Context* c, int kind, uint32_t iters, double* rate, hipStream_t s);
 int op_affine_scan(Context* c, uint64_t* const* a, uint64_t* const* s, uint32_t L,
-                   uint32_t chunks, uint32_t level, uint32_t* out_level, hipStream_t st);
+                   uint32_t chunks, uint32_t level, bool states_only, uint32_t* out_level,
+                   hipStream_t st);
+int op_affine_scan_level(Context* c, uint32_t L, uint32_t level, bool states_only,
+                         uint32_t* out_level, uint64_t* products);
 size_t affine_scan_resident_words(const Context* c, uint32_t L, uint32_t chunks, uint32_t block,
                                   uint32_t level);
 int op_affine_scan_resident_level(Context* c, uint32_t L, uint32_t block, uint32_t level,
-                                  uint32_t* out_level);
+                                  uint32_t* out_level, uint64_t* products);
 int op_affine_scan_resident(Context* c, const uint64_t* const* a, const uint64_t* const* s,
                             uint32_t L, uint32_t chunks, uint32_t block, uint64_t* const* h,
                             uint32_t level, uint64_t* ws, uint32_t* out_level, hipStream_t st);
@@ -312,11 +315,23 @@ static bool distinct(std::vector<const void*> p) {
   return std::adjacent_find(p.begin(), p.end()) == p.end();
 }
 
+int fesc_affine_scan_info(fesc_ctx* ctx, uint32_t L, uint32_t level, uint32_t flags,
+                          uint32_t* out_level, uint64_t* key_switches) {
+  int rc = scan_args(ctx, L, 1, level);
+  if (rc) return rc;
+  if (!out_level || !key_switches || (flags & ~FESC_SCAN_STATES_ONLY))
+    return fail(FESC_ERR_ARG, "bad argument");
+  return op_affine_scan_level(ctx, L, level, flags & FESC_SCAN_STATES_ONLY, out_level,
+                              key_switches);
+}
+
 int fesc_affine_scan(fesc_ctx* ctx, uint64_t* const* a, uint64_t* const* s, uint32_t L,
-                     uint32_t chunks, uint32_t level, uint32_t* out_level, void* stream) {
+                     uint32_t chunks, uint32_t level, uint32_t flags, uint32_t* out_level,
+                     void* stream) {
   int rc = scan_args(ctx, L, chunks, level);
   if (rc) return rc;
   if (!a || !s || !out_level) return fail(FESC_ERR_ARG, "null argument");
+  if (flags & ~FESC_SCAN_STATES_ONLY) return fail(FESC_ERR_ARG, "unknown flags");
   std::vector<const void*> all;
   for (size_t i = 0; i < (size_t)L * chunks; ++i) {
     if (!a[i] || !s[i]) return fail(FESC_ERR_ARG, "null buffer");
@@ -324,15 +339,18 @@ int fesc_affine_scan(fesc_ctx* ctx, uint64_t* const* a, uint64_t* const* s, uint
     all.push_back(s[i]);
   }
   if (!distinct(all)) return fail(FESC_ERR_ARG, "scan buffers must be distinct");
-  return op_affine_scan(ctx, a, s, L, chunks, level, out_level, S(stream));
+  return op_affine_scan(ctx, a, s, L, chunks, level, flags & FESC_SCAN_STATES_ONLY, out_level,
+                        S(stream));
 }
 
 int fesc_affine_scan_resident_info(fesc_ctx* ctx, uint32_t L, uint32_t chunks, uint32_t block,
-                                   uint32_t level, uint32_t* out_level, size_t* workspace_bytes) {
+                                   uint32_t level, uint32_t* out_level, size_t* workspace_bytes,
+                                   uint64_t* key_switches) {
   int rc = scan_args(ctx, L, chunks, level);
   if (rc) return rc;
   if (block == 0 || !out_level || !workspace_bytes) return fail(FESC_ERR_ARG, "bad argument");
-  if ((rc = op_affine_scan_resident_level(ctx, L, block, level, out_level))) return rc;
+  if ((rc = op_affine_scan_resident_level(ctx, L, block, level, out_level, key_switches)))
+    return rc;
   *workspace_bytes = affine_scan_resident_words(ctx, L, chunks, block, level) * 8;
   return FESC_OK;
 }
@@ -343,7 +361,7 @@ int fesc_affine_scan_resident(fesc_ctx* ctx, const uint64_t* const* a, const uin
                               void* stream) {
   uint32_t lo;
   size_t need;
-  int rc = fesc_affine_scan_resident_info(ctx, L, chunks, block, level, &lo, &need);
+  int rc = fesc_affine_scan_resident_info(ctx, L, chunks, block, level, &lo, &need, nullptr);
   if (rc) return rc;
   if (!a || !s || !h) return fail(FESC_ERR_ARG, "null argument");
   if (need && (!workspace || workspace_bytes < need))

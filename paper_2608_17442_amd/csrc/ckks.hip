@@ -53,20 +53,23 @@ __global__ __launch_bounds__(kThreads) void k_mul_plain(const uint64_t* ct,
   }
 }
 
-// (d0, d1) into ct layout `d01`, d2 into poly layout `d2`
-__global__ __launch_bounds__(kThreads) void k_tensor(const uint64_t* a, const uint64_t* b,
-                                                     uint64_t* d01,  // may alias a or b
-                                                     uint64_t* __restrict__ d2, uint32_t n,
+// Tensor of product b = blockIdx.z of the table: (d0, d1) into ct layout
+// d01[b], d2 into poly layout d2[b].  d01[b] may alias x[b] or y[b] (each
+// thread reads its four operands before writing).
+__global__ __launch_bounds__(kThreads) void k_tensor(TsTable tab, uint32_t n,
                                                      const PrimeK* __restrict__ pk) {
-  const uint32_t i = blockIdx.y;
+  const uint32_t i = blockIdx.y, p = blockIdx.z;
   const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
   if (k >= n) return;
   const PrimeK P = pk[i];
+  const uint64_t* a = tab.x[p];
+  const uint64_t* b = tab.y[p];
+  uint64_t* d01 = tab.d01[p];
   const size_t o0 = (size_t)2 * i * n + k, o1 = o0 + n;
   const double a0 = ld(a + o0), a1 = ld(a + o1), b0 = ld(b + o0), b1 = ld(b + o1);
   st(d01 + o0, mm_var(a0, b0, P.q, P.qinv), P.q, P.qinv);
   st(d01 + o1, mm_var(a0, b1, P.q, P.qinv) + mm_var(a1, b0, P.q, P.qinv), P.q, P.qinv);
-  st(d2 + (size_t)i * n + k, mm_var(a1, b1, P.q, P.qinv), P.q, P.qinv);
+  st(tab.d2[p] + (size_t)i * n + k, mm_var(a1, b1, P.q, P.qinv), P.q, P.qinv);
 }
 
 // multiplication by X^m: the evaluation at psi^(2 brv(j) + 1) scales by
@@ -167,47 +170,6 @@ __global__ __launch_bounds__(kThreads) void k_encrypt(const uint64_t* __restrict
   ct[(2 * (size_t)i + 1) * n + k] = a[o];
 }
 
-// Rescale, step 1: v = the last limb of every component to rescale (row
-// t = blockIdx.z of `v`, coefficient form); write its centred value mod q_i
-// into w[t][i] for i < l - 1.
-__global__ __launch_bounds__(kThreads) void k_rescale_lift(const uint64_t* __restrict__ v,
-                                                           uint64_t* __restrict__ w,
-                                                           uint32_t n, uint32_t last,
-                                                           const PrimeK* __restrict__ pk) {
-  const uint32_t i = blockIdx.y, t = blockIdx.z;
-  const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
-  if (k >= n) return;
-  const double ql = pk[last].q;
-  const double x = center(ld(v + (size_t)t * n + k), ql);
-  const PrimeK P = pk[i];
-  st(w + ((size_t)t * last + i) * n + k, x, P.q, P.qinv);
-}
-
-// Rescale, step 2, for ciphertext b = blockIdx.z of the table:
-// out_b[i][t] = (c_b[i][t] - w[2b + t][i]) * q_last^-1 (+ add_b[i][t]) mod q_i,
-// for the limbs i < gridDim.y.
-__global__ __launch_bounds__(kThreads) void k_rescale_combine(RsTable tab,
-                                                              const uint64_t* __restrict__ w,
-                                                              uint32_t n, uint32_t last,
-                                                              const double2* __restrict__ qlinv,
-                                                              const PrimeK* __restrict__ pk) {
-  const uint32_t i = blockIdx.y, b = blockIdx.z;
-  const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
-  if (k >= n) return;
-  const uint64_t* c = tab.in[b];
-  uint64_t* out = tab.out[b];
-  const uint64_t* add = tab.add[b];
-  const PrimeK P = pk[i];
-  const double2 f = qlinv[i];
-#pragma unroll
-  for (int t = 0; t < 2; ++t) {
-    const size_t o = ((size_t)2 * i + t) * n + k;
-    const double d = ld(c + o) - ld(w + ((size_t)(2 * b + t) * last + i) * n + k);
-    const double r = mm_shoup(d, f.x, f.y, P.q);  // |r| < 1.5q
-    st(out + o, add ? r + ld(add + o) : r, P.q, P.qinv);
-  }
-}
-
 inline dim3 grid_rows(uint32_t n, uint32_t rows, uint32_t z = 1) {
   return dim3((n + kThreads - 1) / kThreads, rows, z);
 }
@@ -228,10 +190,10 @@ hipError_t k_mul_plain_launch(const Context* c, const uint64_t* ct, const uint64
   return hipGetLastError();
 }
 
-hipError_t k_tensor_launch(const Context* c, const uint64_t* a, const uint64_t* b,
-                           uint64_t* d01, uint64_t* d2, uint32_t level, hipStream_t s) {
-  hipLaunchKernelGGL(k_tensor, grid_rows(c->n, level), dim3(kThreads), 0, s, a, b, d01, d2,
-                     c->n, c->d_pk);
+hipError_t k_tensor_launch(const Context* c, const TsTable& tab, uint32_t count, uint32_t level,
+                           hipStream_t s) {
+  hipLaunchKernelGGL(k_tensor, grid_rows(c->n, level, count), dim3(kThreads), 0, s, tab, c->n,
+                     c->d_pk);
   return hipGetLastError();
 }
 
@@ -269,21 +231,6 @@ hipError_t k_encrypt_launch(const Context* c, const uint64_t* a, const uint64_t*
                             const uint64_t* me, uint64_t* ct, uint32_t level, hipStream_t st) {
   hipLaunchKernelGGL(k_encrypt, grid_rows(c->n, level), dim3(kThreads), 0, st, a, s, me, ct,
                      c->n, c->d_pk);
-  return hipGetLastError();
-}
-
-hipError_t k_rescale_lift_launch(const Context* c, const uint64_t* v, uint64_t* w,
-                                 uint32_t level, uint32_t rows, hipStream_t s) {
-  hipLaunchKernelGGL(k_rescale_lift, grid_rows(c->n, level - 1, rows), dim3(kThreads), 0, s, v,
-                     w, c->n, level - 1, c->d_pk);
-  return hipGetLastError();
-}
-
-hipError_t k_rescale_combine_launch(const Context* c, const RsTable& tab, uint32_t count,
-                                    const uint64_t* w, uint32_t level, uint32_t rows,
-                                    const double2* qlinv, hipStream_t s) {
-  hipLaunchKernelGGL(k_rescale_combine, grid_rows(c->n, rows, count), dim3(kThreads), 0, s,
-                     tab, w, c->n, level - 1, qlinv, c->d_pk);
   return hipGetLastError();
 }
 

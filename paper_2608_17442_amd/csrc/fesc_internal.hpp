@@ -111,6 +111,8 @@ struct LevelTables {
   double2* rs_inv = nullptr;   // [level]                   q_{level-1}^-1 mod q_i
   double2* mu_inv_n = nullptr; // [level]  N^-1 (Q_D/q_i)^-1 mod q_i (q_i in digit D)
   double2* md_inv_n = nullptr; // [alpha]  N^-1 (P/p_k)^-1 mod p_k
+  double2* rs_ninv = nullptr;  // [1]      N^-1 mod q_{level-1}
+  double2* one = nullptr;      // [level]  1 (with 1/q_i)
 };
 
 struct Context {

@@ -360,6 +360,24 @@ struct ModdownMap {
   }
 };
 
+// Rescale lift: group g = 2 b + t (component t of ciphertext b), one digit =
+// the centred last limb v[g] (|v| < q_last / 2), weight 1 for every target,
+// targets = rows 0 .. rows-1 of w[g]: each target row gets v mod q_i.
+struct RescaleMap {
+  const double* v;
+  uint64_t* w;
+  const double2* one;  // {1, 1/q_i}
+  uint32_t last, rows, n;
+  static constexpr uint32_t alpha = 1;
+  __device__ uint32_t aj(uint32_t) const { return 1; }
+  __device__ uint32_t targets(uint32_t) const { return rows; }
+  __device__ uint32_t row(uint32_t, uint32_t t) const { return t; }
+  __device__ uint32_t prime(uint32_t r) const { return r; }
+  __device__ const double* digits(uint32_t g) const { return v + (size_t)g * n; }
+  __device__ const double2* hat(uint32_t, uint32_t r) const { return one + r; }
+  __device__ uint64_t* out(uint32_t g, uint32_t r) const { return w + ((size_t)g * last + r) * n; }
+};
+
 // ------------------------------------------------------------- inner pass
 
 // The last 12 forward stages on block B (offset of its first value) of
@@ -572,6 +590,31 @@ struct KsCombine {
   }
 };
 
+// Epilogue fusing the rescale combine into the forward transform of the
+// lifted last limbs: for u = 2 b + t (blockIdx.y) and limb i (blockIdx.z),
+// out_b[i][t] = (in_b[i][t] - NTT(w)[u][i]) * q_last^-1 (+ add_b[i][t]).
+// out_b may alias in_b or add_b (same element, same thread).
+struct RsCombine {
+  RsTable tab;
+  const double2* qlinv;
+  __device__ __forceinline__ void operator()(uint64_t*, uint32_t k0, const double (&x)[16],
+                                             double q, double qinv, uint32_t n) const {
+    const uint32_t u = blockIdx.y, i = blockIdx.z, b = u >> 1, t = u & 1;
+    const double2 f = qlinv[i];
+    const size_t o = ((size_t)2 * i + t) * n;
+    const uint64_t* in = tab.in[b] + o;
+    const uint64_t* add = tab.add[b];
+    uint64_t* out = tab.out[b] + o;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const uint32_t k = k0 + 256 * r;
+      double v = mm_shoup(u2d(in[k]) - x[r], f.x, f.y, q);
+      if (add) v += u2d(add[o + k]);
+      out[k] = to_res(v, q, qinv);
+    }
+  }
+};
+
 namespace {
 
 hipError_t launch_fwd_outer(const Context* c, const RowSel& rs, uint32_t batch, uint32_t limbs,
@@ -666,12 +709,32 @@ hipError_t launch_ntt_inv_sources(const Context* c, const KsTable& tab, uint32_t
   return launch_inverse(c, rs, nsrc, level, LoadSources{tab}, InvDigit{f}, s);
 }
 
-// Inverse transform (canonical output) of nrows single rows, row r read from
-// tab.src_in[r], all under prime `prime`, into out[r][N].
-hipError_t launch_ntt_inv_gather(const Context* c, const KsTable& tab, uint32_t nrows,
-                                 uint64_t* out, uint32_t prime, hipStream_t s) {
-  RowSel rs{out, (size_t)c->n, (size_t)c->n, prime, 1, 0, 0, 0, 0};
-  return launch_inverse(c, rs, nrows, 1, LoadSources{tab}, InvCanon{}, s);
+// Rescale, step 1: inverse transform of nrows single rows under prime
+// `last`, row r read from tab.src_in[r], stored into v[r][N] as the centred
+// coefficients [N^-1 x]_{q_last} (fp64; ninv = {N^-1 mod q_last, /q_last}).
+hipError_t launch_ntt_inv_rescale_last(const Context* c, const KsTable& tab, uint32_t nrows,
+                                       uint64_t* v, uint32_t last, const double2* ninv,
+                                       hipStream_t s) {
+  RowSel rs{v, (size_t)c->n, (size_t)c->n, last, 1, 0, 0, 0, 0};
+  return launch_inverse(c, rs, nrows, 1, LoadSources{tab}, InvDigit{ninv}, s);
+}
+
+// Rescale, step 2: each centred last limb lifted to rows 0 .. rows-1 (a
+// conversion with one digit and weight 1) fused with their first forward
+// pass, into w[g][last][N].
+hipError_t launch_rescale_outer(const Context* c, const uint64_t* v, uint64_t* w, uint32_t groups,
+                                uint32_t last, uint32_t rows, const double2* one, hipStream_t s) {
+  const RescaleMap map{reinterpret_cast<const double*>(v), w, one, last, rows, c->n};
+  return launch_bconv_outer(c, map, rows, groups, s);
+}
+
+// Rescale, step 3: second forward pass of w with the combine
+// out_b = (in_b - w) * q_last^-1 (+ add_b) as the epilogue, first `rows` limbs.
+hipError_t launch_ntt_fwd_rs_combine(const Context* c, uint64_t* w, uint32_t count, uint32_t last,
+                                     uint32_t rows, const RsTable& tab, const double2* qlinv,
+                                     hipStream_t s) {
+  RowSel rs{w, (size_t)last * c->n, (size_t)c->n, 0, rows, 0, 0, 0, 0};
+  return launch_fwd_inner(c, rs, 2 * count, rows, RsCombine{tab, qlinv}, s);
 }
 
 // Inverse transform of the rows rs selects (in place), stored as centred

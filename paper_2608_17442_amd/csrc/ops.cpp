@@ -69,13 +69,20 @@ const LevelTables* level_tables(Context* c, uint32_t level, int* err) {
       if (i + 1 < level) rs_inv[i] = entry(h_inv(c->primes[level - 1] % q, q), q);
     }
   }
+  std::vector<double2> rs_ninv(1), one(level);
+  {
+    const uint64_t ql = c->primes[level - 1];
+    rs_ninv[0] = entry(h_inv(c->n % ql, ql), ql);
+    for (uint32_t i = 0; i < level; ++i) one[i] = entry(1, c->primes[i]);
+  }
   std::vector<double2> all;
   LevelTables T;
   T.level = level;
-  size_t off[9];
-  const std::vector<double2>* parts[9] = {&mu_inv,  &mu_hat, &md_inv, &md_hat,  &md_pinv,
-                                          &pmod,    &rs_inv, &mu_inv_n, &md_inv_n};
-  for (int p = 0; p < 9; ++p) {
+  size_t off[11];
+  const std::vector<double2>* parts[11] = {&mu_inv,   &mu_hat,   &md_inv,  &md_hat,
+                                           &md_pinv,  &pmod,     &rs_inv,  &mu_inv_n,
+                                           &md_inv_n, &rs_ninv,  &one};
+  for (int p = 0; p < 11; ++p) {
     off[p] = all.size();
     all.insert(all.end(), parts[p]->begin(), parts[p]->end());
   }
@@ -99,6 +106,8 @@ const LevelTables* level_tables(Context* c, uint32_t level, int* err) {
   T.rs_inv = d + off[6];
   T.mu_inv_n = d + off[7];
   T.md_inv_n = d + off[8];
+  T.rs_ninv = d + off[9];
+  T.one = d + off[10];
   return &(c->level_tabs[level] = T);
 }
 
@@ -340,13 +349,18 @@ int op_mul_relin_many(Context* c, uint32_t count, const uint64_t* const* as,
     const uint32_t m = std::min(S.cap, count - b0);
     std::vector<KsSource> srcs;
     std::vector<KsJob> jobs;
+    TsTable tt{};
     for (uint32_t b = 0; b < m; ++b) {
       uint64_t* d2 = S.d2s + (size_t)b * c->L * n;
       uint64_t* o = outs[b0 + b];
-      HIPCK(k_tensor_launch(c, as[b0 + b], bs[b0 + b], o, d2, level, s));
+      tt.x[b] = as[b0 + b];
+      tt.y[b] = bs[b0 + b];
+      tt.d01[b] = o;
+      tt.d2[b] = d2;
       srcs.push_back(KsSource{d2, n});
       jobs.push_back(KsJob{b, key, 0, o, 3u, 0, nullptr, o});
     }
+    HIPCK(k_tensor_launch(c, tt, m, level, s));
     if ((err = key_switch_batch(c, level, srcs, jobs, s))) return err;
   }
   return FESC_OK;
@@ -387,10 +401,11 @@ int op_rescale_add_many(Context* c, uint32_t count, const uint64_t* const* ins,
       rt.out[b] = outs[b0 + b];
       rt.add[b] = adds ? adds[b0 + b] : nullptr;
     }
-    HIPCK(launch_ntt_inv_gather(c, tab, 2 * m, v, last, s));
-    HIPCK(k_rescale_lift_launch(c, v, w, level, 2 * m, s));
-    HIPCK(ntt_rows(c, w, 2 * m, (size_t)last * n, last, 0, false, s));
-    HIPCK(k_rescale_combine_launch(c, rt, m, w, level, out_rows, T->rs_inv, s));
+    // last limbs to centred coefficients (fp64), lifted to the kept rows
+    // inside the first forward pass, combined in the second pass's epilogue
+    HIPCK(launch_ntt_inv_rescale_last(c, tab, 2 * m, v, last, T->rs_ninv, s));
+    HIPCK(launch_rescale_outer(c, v, w, 2 * m, last, out_rows, T->one, s));
+    HIPCK(launch_ntt_fwd_rs_combine(c, w, m, last, out_rows, rt, T->rs_inv, s));
   }
   return FESC_OK;
 }
@@ -428,12 +443,17 @@ int op_prod_rescale_many(Context* c, uint32_t count, const uint64_t* const* xs,
     const uint32_t m = std::min(G, count - g0);
     std::vector<KsSource> srcs;
     std::vector<KsJob> jobs;
+    TsTable tt{};
     for (uint32_t b = 0; b < m; ++b) {
       uint64_t* d2 = S.d2s + (size_t)b * c->L * n;
-      HIPCK(k_tensor_launch(c, xs[g0 + b], ys[g0 + b], t[b], d2, level, s));
+      tt.x[b] = xs[g0 + b];
+      tt.y[b] = ys[g0 + b];
+      tt.d01[b] = t[b];
+      tt.d2[b] = d2;
       srcs.push_back(KsSource{d2, n});
       jobs.push_back(KsJob{b, key, 0, t[b], 3u, 0, nullptr, t[b]});
     }
+    HIPCK(k_tensor_launch(c, tt, m, level, s));
     if ((err = key_switch_batch(c, level, srcs, jobs, s))) return err;
     if ((err = op_rescale_add_many(c, m, t.data(), outs + g0, adds ? adds + g0 : nullptr, level,
                                    out_rows, s)))

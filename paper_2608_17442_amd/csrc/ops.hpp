@@ -13,8 +13,16 @@ hipError_t k_binary_launch(const Context* c, const uint64_t* a, const uint64_t* 
                            uint32_t rows, uint32_t shift, int op, hipStream_t s);
 hipError_t k_mul_plain_launch(const Context* c, const uint64_t* ct, const uint64_t* pt,
                               uint64_t* out, uint32_t level, hipStream_t s);
-hipError_t k_tensor_launch(const Context* c, const uint64_t* a, const uint64_t* b,
-                           uint64_t* d01, uint64_t* d2, uint32_t level, hipStream_t s);
+// Tensors of up to kMaxBatch products (blockIdx.z = product): d01[b] may
+// alias x[b] or y[b], but no operand of another product of the launch.
+struct TsTable {
+  const uint64_t* x[32];
+  const uint64_t* y[32];
+  uint64_t* d01[32];
+  uint64_t* d2[32];
+};
+hipError_t k_tensor_launch(const Context* c, const TsTable& tab, uint32_t count, uint32_t level,
+                           hipStream_t s);
 hipError_t k_monomial_launch(const Context* c, const uint64_t* in, uint64_t* out,
                              uint32_t level, uint32_t m, hipStream_t s);
 hipError_t k_galois_launch(const Context* c, const uint64_t* in, uint64_t* out, uint32_t rows,
@@ -27,8 +35,6 @@ hipError_t k_keygen_launch(const Context* c, const uint64_t* a, const uint64_t* 
                            const double2* pmod, hipStream_t st);
 hipError_t k_encrypt_launch(const Context* c, const uint64_t* a, const uint64_t* s,
                             const uint64_t* me, uint64_t* ct, uint32_t level, hipStream_t st);
-hipError_t k_rescale_lift_launch(const Context* c, const uint64_t* v, uint64_t* w,
-                                 uint32_t level, uint32_t rows, hipStream_t s);
 
 // Up to kRescaleBatch ciphertexts per batched rescale launch.
 constexpr uint32_t kRescaleBatch = 16;
@@ -37,10 +43,7 @@ struct RsTable {
   uint64_t* out[kRescaleBatch];
   const uint64_t* add[kRescaleBatch];  // added after the division (or null)
 };
-// Writes the first `rows` (<= level - 1) limbs of each output.
-hipError_t k_rescale_combine_launch(const Context* c, const RsTable& tab, uint32_t count,
-                                    const uint64_t* w, uint32_t level, uint32_t rows,
-                                    const double2* qlinv, hipStream_t s);
+
 
 // ----------------------------------------------------------- keyswitch.hip
 
@@ -73,8 +76,14 @@ struct KsTable {
 // centred conversion digits; conversions are fused with the first forward pass)
 hipError_t launch_ntt_inv_sources(const Context* c, const KsTable& tab, uint32_t nsrc,
                                   uint64_t* cc, uint32_t level, const double2* f, hipStream_t s);
-hipError_t launch_ntt_inv_gather(const Context* c, const KsTable& tab, uint32_t nrows,
-                                 uint64_t* out, uint32_t prime, hipStream_t s);
+hipError_t launch_ntt_inv_rescale_last(const Context* c, const KsTable& tab, uint32_t nrows,
+                                       uint64_t* v, uint32_t last, const double2* ninv,
+                                       hipStream_t s);
+hipError_t launch_rescale_outer(const Context* c, const uint64_t* v, uint64_t* w, uint32_t groups,
+                                uint32_t last, uint32_t rows, const double2* one, hipStream_t s);
+hipError_t launch_ntt_fwd_rs_combine(const Context* c, uint64_t* w, uint32_t count, uint32_t last,
+                                     uint32_t rows, const RsTable& tab, const double2* qlinv,
+                                     hipStream_t s);
 hipError_t launch_ntt_inv_digits(const Context* c, const RowSel& rs, uint32_t batch,
                                  uint32_t limbs, const double2* f, hipStream_t s);
 hipError_t launch_modup_outer(const Context* c, const LevelTables& T, const uint64_t* cc,

@@ -82,6 +82,38 @@ Stages prune_to_last(const Stages& st, uint32_t L) {
   return out;
 }
 
+// Which decay products are needed.  A node (dst <- src o dst) always forms
+// its state product a_dst s_src (every state is an output or feeds one); its
+// decay product a_dst a_src only if a later product reads the new a_dst.
+// need[p]: the final decay of position p is wanted by the caller.  Walking
+// the nodes backwards: the decay product of a node is live iff its dst's
+// decay is needed afterwards; a node's products read the old a_dst (always)
+// and a_src (if the decay product is live).  Returns per stage, per node.
+std::vector<std::vector<char>> live_decay(const Stages& st, std::vector<char> need) {
+  std::vector<std::vector<char>> live(st.size());
+  for (size_t i = 0; i < st.size(); ++i) live[i].assign(st[i].size(), 0);
+  for (size_t i = st.size(); i-- > 0;)
+    for (size_t j = st[i].size(); j-- > 0;) {
+      const Node& nd = st[i][j];
+      live[i][j] = need[nd.dst];
+      if (live[i][j]) need[nd.src] = 1;
+      need[nd.dst] = 1;
+    }
+  return live;
+}
+
+// Decay needs at the start of a network (before any node), given the final
+// needs: which input decays the network reads.
+std::vector<char> decay_needed_at_start(const Stages& st, std::vector<char> need) {
+  for (size_t i = st.size(); i-- > 0;)
+    for (size_t j = st[i].size(); j-- > 0;) {
+      const Node& nd = st[i][j];
+      if (need[nd.dst]) need[nd.src] = 1;
+      need[nd.dst] = 1;
+    }
+  return need;
+}
+
 // One chunk's positions: the buffers holding their current values and the
 // buffers a composition writes to.
 struct Seq {
@@ -90,12 +122,25 @@ struct Seq {
 };
 
 // Runs the stages over all chunks; lvl[] (shared by the chunks, which have
-// the same structure) tracks each position's level.  dry: levels only.
+// the same structure) tracks each position's level.  need_final[p]: the
+// caller wants position p's final decay (dead decay products are skipped).
+// dry: levels only.  Each node's state product is issued before its decay
+// product: the state product reads the old a_dst and writes only s_dst,
+// which the decay product does not read, so the two may fall in different
+// product groups.
 int run_stages(Context* c, const Stages& st, std::vector<Seq>& seqs, std::vector<uint32_t>& lvl,
-               bool dry, hipStream_t s) {
-  for (const auto& stage : st) {
-    std::map<uint32_t, std::vector<Node>> by_level;
-    for (const Node& nd : stage) by_level[std::min(lvl[nd.dst], lvl[nd.src])].push_back(nd);
+               const std::vector<char>& need_final, bool dry, hipStream_t s,
+               uint64_t* nprod = nullptr) {
+  const std::vector<std::vector<char>> live = live_decay(st, need_final);
+  if (nprod)
+    for (size_t i = 0; i < st.size(); ++i)
+      for (size_t j = 0; j < st[i].size(); ++j) *nprod += 1 + live[i][j];
+  for (size_t si = 0; si < st.size(); ++si) {
+    std::map<uint32_t, std::vector<uint32_t>> by_level;  // node indices of the stage
+    for (uint32_t j = 0; j < st[si].size(); ++j) {
+      const Node& nd = st[si][j];
+      by_level[std::min(lvl[nd.dst], lvl[nd.src])].push_back(j);
+    }
     for (const auto& kv : by_level) {
       const uint32_t l = kv.first;
       if (l < 2) return fail(FESC_ERR_LEVEL, "affine scan needs more levels than the input has");
@@ -103,12 +148,13 @@ int run_stages(Context* c, const Stages& st, std::vector<Seq>& seqs, std::vector
         std::vector<const uint64_t*> xs, ys, adds;
         std::vector<uint64_t*> outs;
         for (Seq& q : seqs)
-          for (const Node& nd : kv.second) {
-            // state part first, then the decay part (both read a_dst)
+          for (uint32_t j : kv.second) {
+            const Node& nd = st[si][j];
             xs.push_back(q.cur_a[nd.dst]);
             ys.push_back(q.cur_s[nd.src]);
             outs.push_back(q.home_s[nd.dst]);
             adds.push_back(q.cur_s[nd.dst]);
+            if (!live[si][j]) continue;
             xs.push_back(q.cur_a[nd.dst]);
             ys.push_back(q.cur_a[nd.src]);
             outs.push_back(q.home_a[nd.dst]);
@@ -118,9 +164,10 @@ int run_stages(Context* c, const Stages& st, std::vector<Seq>& seqs, std::vector
                                        adds.data(), l, l - 1, s);
         if (err) return err;
       }
-      for (const Node& nd : kv.second) {
+      for (uint32_t j : kv.second) {
+        const Node& nd = st[si][j];
         for (Seq& q : seqs) {
-          q.cur_a[nd.dst] = q.home_a[nd.dst];
+          q.cur_a[nd.dst] = live[si][j] ? q.home_a[nd.dst] : nullptr;  // dead: never read
           q.cur_s[nd.dst] = q.home_s[nd.dst];
         }
         lvl[nd.dst] = l - 1;
@@ -130,19 +177,35 @@ int run_stages(Context* c, const Stages& st, std::vector<Seq>& seqs, std::vector
   return FESC_OK;
 }
 
+
 uint32_t min_level(const std::vector<uint32_t>& lvl) {
   return *std::min_element(lvl.begin(), lvl.end());
 }
 
 }  // namespace
 
-int op_affine_scan(Context* c, uint64_t* const* a, uint64_t* const* s, uint32_t L,
-                   uint32_t chunks, uint32_t level, uint32_t* out_level, hipStream_t st) {
+int op_affine_scan_level(Context* c, uint32_t L, uint32_t level, bool states_only,
+                         uint32_t* out_level, uint64_t* products) {
   const Stages net = bk_network(L);
   std::vector<uint32_t> lvl(L, level);
   std::vector<Seq> none;
+  *products = 0;
+  int err = run_stages(c, net, none, lvl, std::vector<char>(L, states_only ? 0 : 1), true,
+                       nullptr, products);
+  if (err) return err;
+  *out_level = min_level(lvl);
+  return FESC_OK;
+}
+
+int op_affine_scan(Context* c, uint64_t* const* a, uint64_t* const* s, uint32_t L,
+                   uint32_t chunks, uint32_t level, bool states_only, uint32_t* out_level,
+                   hipStream_t st) {
+  const Stages net = bk_network(L);
+  const std::vector<char> need(L, states_only ? 0 : 1);
+  std::vector<uint32_t> lvl(L, level);
+  std::vector<Seq> none;
   int err;
-  if ((err = run_stages(c, net, none, lvl, true, st))) return err;
+  if ((err = run_stages(c, net, none, lvl, need, true, st))) return err;
   std::vector<Seq> seqs(chunks);
   for (uint32_t ch = 0; ch < chunks; ++ch) {
     Seq& q = seqs[ch];
@@ -154,10 +217,11 @@ int op_affine_scan(Context* c, uint64_t* const* a, uint64_t* const* s, uint32_t 
     }
   }
   lvl.assign(L, level);
-  if ((err = run_stages(c, net, seqs, lvl, false, st))) return err;
+  if ((err = run_stages(c, net, seqs, lvl, need, false, st))) return err;
   *out_level = min_level(lvl);
   return FESC_OK;
 }
+
 
 size_t affine_scan_resident_words(const Context* c, uint32_t L, uint32_t chunks, uint32_t block,
                                   uint32_t level) {
@@ -175,7 +239,7 @@ size_t affine_scan_resident_words(const Context* c, uint32_t L, uint32_t chunks,
 static int resident(Context* c, const uint64_t* const* a, const uint64_t* const* s, uint32_t L,
                     uint32_t chunks, uint32_t block, uint64_t* const* h, uint32_t level,
                     uint32_t out_level, uint64_t* ws, bool dry, uint32_t* min_out,
-                    hipStream_t st) {
+                    hipStream_t st, uint64_t* nprod = nullptr) {
   const uint32_t K = (L + block - 1) / block;
   const size_t W = (size_t)2 * level * c->n;
   const size_t per_chunk = (size_t)(2 * block + 2 * (K - 1)) * W;
@@ -203,6 +267,11 @@ static int resident(Context* c, const uint64_t* const* a, const uint64_t* const*
   };
   const uint32_t nseq = dry ? 1 : chunks;
   int err;
+  // decays needed: the carries are used through their states only; the
+  // carry network then says which summary decays it reads
+  const Stages carry_net = K > 1 ? bk_network(K - 1) : Stages{};
+  const std::vector<char> carry_need(K > 1 ? K - 1 : 0, 0);
+  const std::vector<char> sum_need = decay_needed_at_start(carry_net, carry_need);
   // pass 1: summaries of blocks 0 .. K-2
   const Stages summary_net = prune_to_last(bk_network(block), block);
   std::vector<Seq> carry(nseq);
@@ -211,7 +280,9 @@ static int resident(Context* c, const uint64_t* const* a, const uint64_t* const*
     std::vector<Seq> seqs;
     for (uint32_t ch = 0; ch < nseq; ++ch) seqs.push_back(in_seq(ch, j, block, true));
     std::vector<uint32_t> lvl(block, level);
-    if ((err = run_stages(c, summary_net, seqs, lvl, dry, st))) return err;
+    std::vector<char> need(block, 0);
+    need[block - 1] = sum_need[j];
+    if ((err = run_stages(c, summary_net, seqs, lvl, need, dry, st, nprod))) return err;
     lvl_sum.push_back(lvl[block - 1]);
     for (uint32_t ch = 0; ch < nseq; ++ch) {
       carry[ch].cur_a.push_back(seqs[ch].cur_a[block - 1]);
@@ -221,7 +292,8 @@ static int resident(Context* c, const uint64_t* const* a, const uint64_t* const*
     }
   }
   // exclusive scan over the summaries: G_j = carry position j - 1
-  if (K > 1 && (err = run_stages(c, bk_network(K - 1), carry, lvl_sum, dry, st))) return err;
+  if (K > 1 && (err = run_stages(c, carry_net, carry, lvl_sum, carry_need, dry, st, nprod)))
+    return err;
   // pass 2: replay and carry injection
   uint32_t lo = level;
   for (uint32_t j = 0; j < K; ++j) {
@@ -229,7 +301,9 @@ static int resident(Context* c, const uint64_t* const* a, const uint64_t* const*
     std::vector<Seq> seqs;
     for (uint32_t ch = 0; ch < nseq; ++ch) seqs.push_back(in_seq(ch, j, Bj, false));
     std::vector<uint32_t> lvl(Bj, level);
-    if ((err = run_stages(c, bk_network(Bj), seqs, lvl, dry, st))) return err;
+    // block 0 gives states; later blocks' decays enter the carry injection
+    const std::vector<char> need(Bj, j == 0 ? 0 : 1);
+    if ((err = run_stages(c, bk_network(Bj), seqs, lvl, need, dry, st, nprod))) return err;
     if (j == 0) {
       lo = std::min(lo, min_level(lvl));
       if (!dry)
@@ -246,6 +320,7 @@ static int resident(Context* c, const uint64_t* const* a, const uint64_t* const*
       const uint32_t l = kv.first;
       if (l < 2) return fail(FESC_ERR_LEVEL, "affine scan needs more levels than the input has");
       lo = std::min(lo, l - 1);
+      if (nprod) *nprod += kv.second.size();
       if (dry) continue;
       std::vector<const uint64_t*> xs, ys, adds;
       std::vector<uint64_t*> outs;
@@ -266,9 +341,12 @@ static int resident(Context* c, const uint64_t* const* a, const uint64_t* const*
 }
 
 int op_affine_scan_resident_level(Context* c, uint32_t L, uint32_t block, uint32_t level,
-                                  uint32_t* out_level) {
-  return resident(c, nullptr, nullptr, L, 1, block, nullptr, level, 0, nullptr, true, out_level,
-                  nullptr);
+                                  uint32_t* out_level, uint64_t* products) {
+  uint64_t k = 0;
+  int err = resident(c, nullptr, nullptr, L, 1, block, nullptr, level, 0, nullptr, true,
+                     out_level, nullptr, &k);
+  if (products) *products = k;
+  return err;
 }
 
 int op_affine_scan_resident(Context* c, const uint64_t* const* a, const uint64_t* const* s,
@@ -276,7 +354,7 @@ int op_affine_scan_resident(Context* c, const uint64_t* const* a, const uint64_t
                             uint32_t level, uint64_t* ws, uint32_t* out_level, hipStream_t st) {
   uint32_t lo;
   int err;
-  if ((err = op_affine_scan_resident_level(c, L, block, level, &lo))) return err;
+  if ((err = op_affine_scan_resident_level(c, L, block, level, &lo, nullptr))) return err;
   uint32_t got;
   if ((err = resident(c, a, s, L, chunks, block, h, level, lo, ws, false, &got, st))) return err;
   *out_level = lo;

@@ -61,16 +61,18 @@ _SIGS = {
     "fesc_scan_contract": [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp), ctypes.POINTER(_vp),
                            _u32, _u32, ctypes.POINTER(_vp), _u32, _vp],
     "fesc_calib_valu": [_vp, ctypes.c_int, _u32, ctypes.POINTER(ctypes.c_double), _vp],
-    "fesc_affine_scan": [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp), _u32, _u32, _u32,
+    "fesc_affine_scan": [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp), _u32, _u32, _u32, _u32,
                          ctypes.POINTER(_u32), _vp],
+    "fesc_affine_scan_info": [_vp, _u32, _u32, _u32, ctypes.POINTER(_u32), ctypes.POINTER(_u64)],
     "fesc_affine_scan_resident_info": [_vp, _u32, _u32, _u32, _u32, ctypes.POINTER(_u32),
-                                       ctypes.POINTER(_sz)],
+                                       ctypes.POINTER(_sz), ctypes.POINTER(_u64)],
     "fesc_affine_scan_resident": [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp), _u32, _u32,
                                   _u32, ctypes.POINTER(_vp), _u32, _vp, _sz, _vp],
 }
 
 CONJ = -(2 ** 31)
 CALIB_CT, CALIB_GS, CALIB_MAC = 0, 1, 2
+SCAN_STATES_ONLY = 1
 
 for _name, _args in _SIGS.items():
     _f = getattr(_lib, _name)
@@ -228,22 +230,32 @@ class Context:
         _check(_lib.fesc_scan_contract(self._h, arr(h), arr(decay), arr(cfac), K, d_state,
                                        arr(outs), level, _stream(stream)))
 
-    def affine_scan(self, a, s, chunks, level, stream=None) -> int:
+    def affine_scan(self, a, s, chunks, level, states_only=False, stream=None) -> int:
         """In-place Brent-Kung scan of `chunks` sequences of len(a) // chunks
         token maps (a[c*L + k], s[c*L + k]); returns the output level."""
         n = len(a)
         arr = lambda ts: (_vp * n)(*[_ptr(t) for t in ts])
         out = _u32()
         _check(_lib.fesc_affine_scan(self._h, arr(a), arr(s), n // chunks, chunks, level,
-                                     ctypes.byref(out), _stream(stream)))
+                                     SCAN_STATES_ONLY if states_only else 0, ctypes.byref(out),
+                                     _stream(stream)))
         return int(out.value)
 
+    def affine_scan_info(self, L, level, states_only=False):
+        """(output level, key switches per chunk) of affine_scan."""
+        lo, ks = _u32(), _u64()
+        _check(_lib.fesc_affine_scan_info(self._h, L, level, SCAN_STATES_ONLY if states_only else 0,
+                                          ctypes.byref(lo), ctypes.byref(ks)))
+        return int(lo.value), int(ks.value)
+
     def affine_scan_resident_info(self, L, chunks, block, level):
-        """(output level, workspace bytes) of the resident schedule."""
-        lo, ws = _u32(), _sz()
+        """(output level, workspace bytes, key switches per chunk) of the
+        resident schedule."""
+        lo, ws, ks = _u32(), _sz(), _u64()
         _check(_lib.fesc_affine_scan_resident_info(self._h, L, chunks, block, level,
-                                                   ctypes.byref(lo), ctypes.byref(ws)))
-        return int(lo.value), int(ws.value)
+                                                   ctypes.byref(lo), ctypes.byref(ws),
+                                                   ctypes.byref(ks)))
+        return int(lo.value), int(ws.value), int(ks.value)
 
     def affine_scan_resident(self, a, s, chunks, block, h, level, workspace, stream=None):
         """States of the resident block schedule into h (see the C header)."""

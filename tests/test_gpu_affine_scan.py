@@ -61,6 +61,8 @@ def test_affine_scan_small(small, L, chunks):
     lo = S.ctx.affine_scan(ad, sd, chunks, level)
     depth = {1: 0, 2: 1, 7: 4, 8: 4, 13: 5}[L]
     assert lo == level - depth
+    lo_i, ks = S.ctx.affine_scan_info(L, level)
+    assert lo_i == lo and ks == 2 * OS.brent_kung(list(range(L)), lambda x, y: x)[1]
     for c in range(chunks):
         A, H = OS.affine_scan(S.P, ao[c * L:(c + 1) * L], so[c * L:(c + 1) * L], S.keys[0])
         for k in range(L):
@@ -68,11 +70,29 @@ def test_affine_scan_small(small, L, chunks):
             _eq_prefix(sd[c * L + k], H[k], f"chunk {c} state {k}")
 
 
+@pytest.mark.parametrize("L,chunks", [(7, 2), (16, 1)])
+def test_affine_scan_states_only(small, L, chunks):
+    """Dead decay products skipped: the states are unchanged, with
+    2 (2(L-1) - log2 L) - (dead decay products) key switches."""
+    S, level = small, 8
+    ao, so, ad, sd = _inputs(S, L, chunks, level, f"so{L}")
+    lo_i, ks = S.ctx.affine_scan_info(L, level, states_only=True)
+    step(f"affine_scan states-only L={L} chunks={chunks} level={level}")
+    lo = S.ctx.affine_scan(ad, sd, chunks, level, states_only=True)
+    assert lo == lo_i
+    if L == 16:
+        assert ks == 37          # 26 state products + 11 live decay products
+    for c in range(chunks):
+        _, H = OS.affine_scan(S.P, ao[c * L:(c + 1) * L], so[c * L:(c + 1) * L], S.keys[0])
+        for k in range(L):
+            _eq_prefix(sd[c * L + k], H[k], f"chunk {c} state {k}")
+
+
 @pytest.mark.parametrize("L,chunks,block", [(11, 2, 4), (9, 1, 3), (5, 1, 8), (6, 2, 1)])
 def test_affine_scan_resident_small(small, L, chunks, block):
     S, level = small, 8
     ao, so, ad, sd = _inputs(S, L, chunks, level, f"res{L}-{block}")
-    lo, ws_bytes = S.ctx.affine_scan_resident_info(L, chunks, block, level)
+    lo, ws_bytes, _ = S.ctx.affine_scan_resident_info(L, chunks, block, level)
     h = [torch.zeros(lo * 2 * S.P.n, dtype=torch.int64, device="cuda") for _ in range(L * chunks)]
     ws = torch.empty(max(ws_bytes // 8, 1), dtype=torch.int64, device="cuda")
     keep = [x.clone() for x in ad + sd]
@@ -96,7 +116,7 @@ def test_affine_scan_errors(small):
     _, _, ad16, sd16 = _inputs(S, 16, 1, 4, "deep")
     with pytest.raises(F.FescError, match="levels"):
         S.ctx.affine_scan(ad16, sd16, 1, 4)
-    lo, ws_bytes = S.ctx.affine_scan_resident_info(4, 1, 2, level)
+    lo, ws_bytes, _ = S.ctx.affine_scan_resident_info(4, 1, 2, level)
     h = [torch.zeros(lo * 2 * S.P.n, dtype=torch.int64, device="cuda") for _ in range(4)]
     short = torch.empty(ws_bytes // 8 - 1, dtype=torch.int64, device="cuda")
     with pytest.raises(F.FescError, match="workspace"):
