@@ -86,7 +86,7 @@ def log(msg):
 # --------------------------------------------------------------- workloads
 
 class Workloads:
-    def __init__(self, F, torch, np, skip_matvec=False):
+    def __init__(self, F, torch, np, skip_matvec=False, affine_only=False):
         import synth
         import synth.workloads as WL
         self.F, self.torch, self.np, self.WL, self.synth = F, torch, np, WL, synth
@@ -100,6 +100,8 @@ class Workloads:
         self.s = synth.secret(WL.CFG3["seed"], self.n)
         self.s_dev = torch.from_numpy(self.s).cuda()
         self._keys = set()
+        if affine_only:
+            return
         self.setup_ntt()
         self.setup_ks()
         self.skip_matvec = skip_matvec
@@ -284,6 +286,29 @@ class Workloads:
         return lo
 
 
+def time_affine(W, F, torch, np):
+    """HEScan affine prefix scan: one warm-up, mean of two timed runs (in
+    place; the arithmetic is data-oblivious, so reruns are timed alike)."""
+    W.setup_affine()
+    ev = lambda: [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    W.run_affine(ev())
+    torch.cuda.synchronize()
+    aev = [ev() for _ in range(2)]
+    lo = [W.run_affine(e) for e in aev]
+    torch.cuda.synchronize()
+    af_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in aev]))
+    sh = W.af_shape
+    Lp, m = sh["L"], sh["L"].bit_length() - 1
+    n_paper = 2 * sh["chunks"] * (2 * (Lp - 1) - m)     # two per composition node
+    n_ks = sh["chunks"] * W.ctx.affine_scan_info(sh["L"], sh["level"], states_only=True)[1]
+    return {"tokens": sh["L"], "chunks": sh["chunks"], "level_in": sh["level"],
+            "level_out": lo[-1], "ms": round(af_ms, 2), "key_switches": n_ks,
+            "key_switches_all_nodes": n_paper,
+            "keyswitch_per_s": round(n_ks / (af_ms * 1e-3), 1),
+            "network": "Brent-Kung, in place, states only (dead decay products skipped), "
+                       "stages batched over chunks"}
+
+
 # ---------------------------------------------------------------- baseline
 
 def cpu_baseline(ntt_reps: int = 16):
@@ -346,6 +371,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-affine", action="store_true",
                     help="skip the affine prefix scan component (timed after the steps)")
+    ap.add_argument("--affine-only", action="store_true",
+                    help="set up and time only the affine prefix scan component (profiling)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run one 1 GiB device-to-device copy, the reference kernel for "
                          "scaling hardware traffic counters")
@@ -367,6 +394,11 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if args.affine_only:
+        W = Workloads(F, torch, np, affine_only=True)
+        print(json.dumps({"components": {"affine_scan": time_affine(W, F, torch, np)}}),
+              flush=True)
+        return
     W = Workloads(F, torch, np)
     torch.cuda.synchronize()
     # register-resident arithmetic peaks of this device (VALU roof)
@@ -415,23 +447,7 @@ def main():
     if not args.no_affine:
         del W.mv_plan, W.bank
         torch.cuda.empty_cache()
-        W.setup_affine()
-        W.run_affine(new_events(2))          # warm-up (in place; the arithmetic is
-        torch.cuda.synchronize()             # data-oblivious, so reruns are timed alike)
-        aev = [new_events(2) for _ in range(2)]
-        lo = [W.run_affine(e) for e in aev]
-        torch.cuda.synchronize()
-        af_ms = float(np.mean([el(e, 0, 1) for e in aev]))
-        sh = W.af_shape
-        Lp, m = sh["L"], sh["L"].bit_length() - 1
-        n_paper = 2 * sh["chunks"] * (2 * (Lp - 1) - m)     # two per composition node
-        n_ks = sh["chunks"] * W.ctx.affine_scan_info(sh["L"], sh["level"], states_only=True)[1]
-        affine = {"tokens": sh["L"], "chunks": sh["chunks"], "level_in": sh["level"],
-                  "level_out": lo[-1], "ms": round(af_ms, 2), "key_switches": n_ks,
-                  "key_switches_all_nodes": n_paper,
-                  "keyswitch_per_s": round(n_ks / (af_ms * 1e-3), 1),
-                  "network": "Brent-Kung, in place, states only (dead decay products "
-                             "skipped), stages batched over chunks"}
+        affine = time_affine(W, F, torch, np)
     n, rows = W.n, W.limbs * W.batch
     bytes_dir = 2 * 8 * n * rows
     ntt_gbs = 2 * bytes_dir / ((fwd + inv) * 1e-3) / 1e9
