@@ -53,25 +53,6 @@ __global__ __launch_bounds__(kThreads) void k_mul_plain(const uint64_t* ct,
   }
 }
 
-// Tensor of product b = blockIdx.z of the table: (d0, d1) into ct layout
-// d01[b], d2 into poly layout d2[b].  d01[b] may alias x[b] or y[b] (each
-// thread reads its four operands before writing).
-__global__ __launch_bounds__(kThreads) void k_tensor(TsTable tab, uint32_t n,
-                                                     const PrimeK* __restrict__ pk) {
-  const uint32_t i = blockIdx.y, p = blockIdx.z;
-  const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
-  if (k >= n) return;
-  const PrimeK P = pk[i];
-  const uint64_t* a = tab.x[p];
-  const uint64_t* b = tab.y[p];
-  uint64_t* d01 = tab.d01[p];
-  const size_t o0 = (size_t)2 * i * n + k, o1 = o0 + n;
-  const double a0 = ld(a + o0), a1 = ld(a + o1), b0 = ld(b + o0), b1 = ld(b + o1);
-  st(d01 + o0, mm_var(a0, b0, P.q, P.qinv), P.q, P.qinv);
-  st(d01 + o1, mm_var(a0, b1, P.q, P.qinv) + mm_var(a1, b0, P.q, P.qinv), P.q, P.qinv);
-  st(tab.d2[p] + (size_t)i * n + k, mm_var(a1, b1, P.q, P.qinv), P.q, P.qinv);
-}
-
 // multiplication by X^m: the evaluation at psi^(2 brv(j) + 1) scales by
 // psi^e, e = (2 brv(j) + 1) m mod 2N; psi^e = tw[brv(e)] for e < N and
 // -tw[brv(e - N)] otherwise (tw = forward twiddle table).
@@ -187,13 +168,6 @@ hipError_t k_mul_plain_launch(const Context* c, const uint64_t* ct, const uint64
                               uint64_t* out, uint32_t level, hipStream_t s) {
   hipLaunchKernelGGL(k_mul_plain, grid_rows(c->n, level), dim3(kThreads), 0, s, ct, pt, out,
                      c->n, c->d_pk);
-  return hipGetLastError();
-}
-
-hipError_t k_tensor_launch(const Context* c, const TsTable& tab, uint32_t count, uint32_t level,
-                           hipStream_t s) {
-  hipLaunchKernelGGL(k_tensor, grid_rows(c->n, level, count), dim3(kThreads), 0, s, tab, c->n,
-                     c->d_pk);
   return hipGetLastError();
 }
 

@@ -75,17 +75,24 @@ __global__ __launch_bounds__(kThreads) void k_ip(KsTable tab, const uint64_t* __
   }
   for (uint32_t job = j0; job < j1; ++job) {
     const uint32_t s = tab.job_src[job];
-    const uint64_t* in = tab.src_in[s] + (size_t)row * tab.src_stride[s];
-    const uint64_t* ex = ext + ((size_t)s * D * E + row) * n;
-    uint64_t dv[D];
+    const size_t so = (size_t)row * tab.src_stride[s] + src;
+    const uint64_t* ex = ext + ((size_t)s * D * E + row) * n + src;
+    const uint64_t* y = tab.src_y[s];
+    double dv[D];
 #pragma unroll
-    for (int j = 0; j < D; ++j) dv[j] = ((uint32_t)j == own ? in : ex + (size_t)j * E * n)[src];
+    for (int j = 0; j < D; ++j) {
+      if ((uint32_t)j != own) {
+        dv[j] = u2d(ex[(size_t)j * E * n]);
+      } else {  // own digit: the source row itself (a product source formed here)
+        dv[j] = u2d(tab.src_in[s][so]);
+        if (y) dv[j] = mm_var(dv[j], u2d(y[so]), M.q, M.qinv);
+      }
+    }
     double ab = 0.0, aa = 0.0;
 #pragma unroll
     for (int j = 0; j < D; ++j) {
-      const double d = u2d(dv[j]);
-      ab += mm_var(d, kb[j], M.q, M.qinv);
-      aa += mm_var(d, ka[j], M.q, M.qinv);
+      ab += mm_var(dv[j], kb[j], M.q, M.qinv);
+      aa += mm_var(dv[j], ka[j], M.q, M.qinv);
       if ((j & 3) == 3 && j + 1 < D) {
         ab = red_bal(ab, M.q, M.qinv);
         aa = red_bal(aa, M.q, M.qinv);
@@ -97,8 +104,17 @@ __global__ __launch_bounds__(kThreads) void k_ip(KsTable tab, const uint64_t* __
       aa = mm_shoup(aa, f.x, f.y, M.q);
       const uint64_t* add = tab.add[job];
       const uint32_t mask = tab.add_mask[job];
-      if (add && (mask & 1u)) ab += u2d(add[(size_t)2 * row * n + src]);
-      if (add && (mask & 2u)) aa += u2d(add[((size_t)2 * row + 1) * n + src]);
+      const size_t o0 = (size_t)2 * row * n + src, o1 = o0 + n;
+      if (const uint64_t* ay = tab.add_y[job]) {
+        // tensor addend (d0, d1) = (x0 y0, x0 y1 + x1 y0), |each| < q
+        const double x0 = u2d(add[o0]), x1 = u2d(add[o1]);
+        const double y0 = u2d(ay[o0]), y1 = u2d(ay[o1]);
+        if (mask & 1u) ab += mm_var(x0, y0, M.q, M.qinv);
+        if (mask & 2u) aa += mm_var(x0, y1, M.q, M.qinv) + mm_var(x1, y0, M.q, M.qinv);
+      } else {
+        if (add && (mask & 1u)) ab += u2d(add[o0]);
+        if (add && (mask & 2u)) aa += u2d(add[o1]);
+      }
     }
     uint64_t* out = acc + (size_t)job * 2 * E * n;
     out[(size_t)row * n + k] = to_res(ab, M.q, M.qinv);

@@ -467,17 +467,41 @@ struct StoreResidues {
   }
 };
 
+// 16 consecutive residues at p (two 16-byte loads per pair).
+__device__ __forceinline__ void load16(const uint64_t* p, double (&x)[16]) {
+  const ulonglong2* v = reinterpret_cast<const ulonglong2*>(p);
+#pragma unroll
+  for (int r = 0; r < 16; r += 2) {
+    const ulonglong2 w = v[r / 2];
+    x[r] = u2d(w.x);
+    x[r + 1] = u2d(w.y);
+  }
+}
+
 // Source of the inverse inner pass: the row itself (in place).
 struct LoadRow {
-  __device__ __forceinline__ const uint64_t* operator()(uint64_t* row) const { return row; }
+  __device__ __forceinline__ void operator()(const uint64_t* row, uint32_t off, double (&x)[16],
+                                             double, double) const {
+    load16(row + off, x);
+  }
 };
 
 // Source of the inverse inner pass: row blockIdx.z of source blockIdx.y of a
-// key-switch table (out of place; the row receives the result).
+// key-switch table (out of place; the row receives the result).  A product
+// source (src_y set) is formed here, x y mod q in (-q/2, q/2] (balanced
+// values sit inside the inverse butterflies' input bound).
 struct LoadSources {
   KsTable tab;
-  __device__ __forceinline__ const uint64_t* operator()(uint64_t*) const {
-    return tab.src_in[blockIdx.y] + (size_t)blockIdx.z * tab.src_stride[blockIdx.y];
+  __device__ __forceinline__ void operator()(const uint64_t*, uint32_t off, double (&x)[16],
+                                             double q, double qinv) const {
+    const size_t o = (size_t)blockIdx.z * tab.src_stride[blockIdx.y] + off;
+    load16(tab.src_in[blockIdx.y] + o, x);
+    if (const uint64_t* y = tab.src_y[blockIdx.y]) {
+      double z[16];
+      load16(y + o, z);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) x[r] = mm_var(x[r], z[r], q, qinv);
+    }
   }
 };
 
@@ -500,14 +524,8 @@ __global__ __launch_bounds__(kThreads) void k_inv_inner(RowSel rs, uint32_t log_
   uint64_t* row = rs.row();
   const uint32_t t = threadIdx.x, a = t >> 4, b = t & 15;
   const uint32_t B = blockIdx.x * kBlock, nb = n + B;
-  const ulonglong2* src = reinterpret_cast<const ulonglong2*>(ld(row) + B + 16 * t);
   double x[16];
-#pragma unroll
-  for (int r = 0; r < 16; r += 2) {
-    const ulonglong2 v = src[r / 2];
-    x[r] = u2d(v.x);
-    x[r + 1] = u2d(v.y);
-  }
+  ld(row, B + 16 * t, x, q, qinv);
   // bits 3..0
   const double* s3 = tw3 + ((size_t)prime * (n / kBlock) + blockIdx.x) * (15 * kThreads) + t;
   gs_st<1, true>(x, TwLo<1>{s3, qinv}, q, qinv);

@@ -125,12 +125,9 @@ struct Scratch {
   uint64_t* ext;  // [B][dnum][L+a][N]  ModUp outputs (evaluation form)
   uint64_t* acc;  // [B][2][L+a][N]     key inner products
   uint64_t* y;    // [B][2][L][N]       ModDown conversions (first-pass fp64)
-  uint64_t* d01;  // [L][2][N]          tensor (d0, d1)
-  uint64_t* d2;   // [L][N]             tensor d2
+  uint64_t* d2;   // [L][N]             one polynomial (encryption: the secret)
   uint64_t* v;    // [2][N]             rescale: last limb
   uint64_t* w;    // [2][L][N]          rescale: lifted last limb
-  uint64_t* ws;   // [3][L][2][N]       ciphertexts of composite operations
-  uint64_t* d2s;  // [B][L][N]          batched products: relinearised parts d2
   uint64_t* cts;  // [B][L][2][N]       batched composite operations: ciphertexts
 };
 
@@ -138,22 +135,21 @@ int scratch(Context* c, Scratch* s, uint32_t batch = 1) {
   const size_t n = c->n, L = c->L, E = c->L + c->alpha;
   size_t B = batch <= 1 ? 1 : kMaxBatch;
   if (c->scratch_bytes) {  // keep the larger capacity once allocated
-    const size_t per_b = (L + c->dnum * E + 2 * E + 2 * L + L + 2 * L) * n * 8;
-    const size_t fixed = (2 * L + 2 * L + L + 2 + 2 * L + 6 * L) * n * 8;
+    const size_t per_b = (L + c->dnum * E + 2 * E + 2 * L + 2 * L) * n * 8;
+    const size_t fixed = (2 * L + L + 2 + 2 * L) * n * 8;
     if (c->scratch_bytes >= fixed + kMaxBatch * per_b) B = kMaxBatch;
   }
-  const size_t sizes[12] = {2 * L * n,     B * L * n, B * c->dnum * E * n, B * 2 * E * n,
-                            B * 2 * L * n, 2 * L * n, L * n,               2 * n,
-                            2 * L * n,     6 * L * n, B * L * n,           B * 2 * L * n};
+  const size_t sizes[9] = {2 * L * n,     B * L * n, B * c->dnum * E * n, B * 2 * E * n,
+                           B * 2 * L * n, L * n,     2 * n,               2 * L * n,
+                           B * 2 * L * n};
   size_t total = 0;
   for (size_t x : sizes) total += x;
   int err;
   uint64_t* base = static_cast<uint64_t*>(scratch_get(c, total * sizeof(uint64_t), &err));
   if (!base) return err;
   s->cap = (uint32_t)B;
-  uint64_t** dst[12] = {&s->cin, &s->cc, &s->ext, &s->acc, &s->y,   &s->d01,
-                        &s->d2,  &s->v,  &s->w,   &s->ws,  &s->d2s, &s->cts};
-  for (int i = 0; i < 12; ++i) {
+  uint64_t** dst[9] = {&s->cin, &s->cc, &s->ext, &s->acc, &s->y, &s->d2, &s->v, &s->w, &s->cts};
+  for (int i = 0; i < 9; ++i) {
     *dst[i] = base;
     base += sizes[i];
   }
@@ -191,6 +187,7 @@ int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& sr
   for (size_t i = 0; i < srcs.size(); ++i) {
     tab.src_in[i] = srcs[i].in;
     tab.src_stride[i] = srcs[i].stride;
+    tab.src_y[i] = srcs[i].y;
   }
   // ModUp of every source (the scratch capacity covers all of them)
   const uint32_t ns = (uint32_t)srcs.size();
@@ -234,7 +231,10 @@ int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& sr
       if (J.add && J.add_galois != J.galois) t.fold = 0;
       t.add2[j] = J.add2;
       t.out[j] = J.out;
+      t.add_y[j] = J.add_y;
     }
+    for (uint32_t j = 0; j < nj && !t.fold; ++j)
+      if (t.add_y[j]) return fail(FESC_ERR_ARG, "a tensor addend needs the folded combine");
     HIPCK(k_ip_launch(c, t, nkeys, S.ext, S.acc, level, T->md_pinv, s));
     // special-prime rows: iNTT to centred ModDown digits, conversion fused
     // with the first forward pass of y, second pass ending in the combine
@@ -332,10 +332,12 @@ int op_rotate_batch(Context* c, uint32_t count, const uint64_t* const* ins,
   return FESC_OK;
 }
 
-// Products a_i * b_i relinearised, in groups of up to kMaxBatch: the tensor
-// writes (d0, d1) straight into out_i and d2 into scratch, and one batched key
-// switch (all jobs share the relinearisation key) adds relin(d2) to out_i.
-// out_i may alias a_i or b_i (the tensor is elementwise).
+// Products a_i * b_i relinearised, in groups of up to kMaxBatch, each group
+// one batched key switch (all jobs share the relinearisation key) whose
+// source is d2 = a1 b1 and whose addend is (d0, d1) = (a0 b0, a0 b1 + a1 b0),
+// both formed from the operands where they are read: the tensor is never
+// stored.  out_i may alias a_i or b_i (all operands of a group are read
+// before its combine writes).
 int op_mul_relin_many(Context* c, uint32_t count, const uint64_t* const* as,
                       const uint64_t* const* bs, uint64_t* const* outs, uint32_t level,
                       hipStream_t s) {
@@ -347,20 +349,15 @@ int op_mul_relin_many(Context* c, uint32_t count, const uint64_t* const* as,
   const size_t n = c->n;
   for (uint32_t b0 = 0; b0 < count; b0 += S.cap) {
     const uint32_t m = std::min(S.cap, count - b0);
+    // the tensor is never stored: the source d2 = a1 b1 is formed by the
+    // inverse transform and the inner product, (d0, d1) by the fold
     std::vector<KsSource> srcs;
     std::vector<KsJob> jobs;
-    TsTable tt{};
     for (uint32_t b = 0; b < m; ++b) {
-      uint64_t* d2 = S.d2s + (size_t)b * c->L * n;
-      uint64_t* o = outs[b0 + b];
-      tt.x[b] = as[b0 + b];
-      tt.y[b] = bs[b0 + b];
-      tt.d01[b] = o;
-      tt.d2[b] = d2;
-      srcs.push_back(KsSource{d2, n});
-      jobs.push_back(KsJob{b, key, 0, o, 3u, 0, nullptr, o});
+      const uint64_t *x = as[b0 + b], *y = bs[b0 + b];
+      srcs.push_back(KsSource{x + n, 2 * n, y + n});
+      jobs.push_back(KsJob{b, key, 0, x, 3u, 0, nullptr, outs[b0 + b], y});
     }
-    HIPCK(k_tensor_launch(c, tt, m, level, s));
     if ((err = key_switch_batch(c, level, srcs, jobs, s))) return err;
   }
   return FESC_OK;
@@ -430,8 +427,8 @@ int op_prod_rescale_many(Context* c, uint32_t count, const uint64_t* const* xs,
   const uint64_t* key;
   int err;
   if ((err = key_of(c, 0, &key))) return err;
-  // the batched layout first: the calls below keep it, so S.cts and S.d2s
-  // stay in place
+  // the batched layout first: the calls below keep it, so S.cts stays in
+  // place
   Scratch S;
   if ((err = scratch(c, &S, 2))) return err;
   const uint32_t G = S.cap & ~1u;
@@ -443,17 +440,11 @@ int op_prod_rescale_many(Context* c, uint32_t count, const uint64_t* const* xs,
     const uint32_t m = std::min(G, count - g0);
     std::vector<KsSource> srcs;
     std::vector<KsJob> jobs;
-    TsTable tt{};
     for (uint32_t b = 0; b < m; ++b) {
-      uint64_t* d2 = S.d2s + (size_t)b * c->L * n;
-      tt.x[b] = xs[g0 + b];
-      tt.y[b] = ys[g0 + b];
-      tt.d01[b] = t[b];
-      tt.d2[b] = d2;
-      srcs.push_back(KsSource{d2, n});
-      jobs.push_back(KsJob{b, key, 0, t[b], 3u, 0, nullptr, t[b]});
+      const uint64_t *x = xs[g0 + b], *y = ys[g0 + b];
+      srcs.push_back(KsSource{x + n, 2 * n, y + n});
+      jobs.push_back(KsJob{b, key, 0, x, 3u, 0, nullptr, t[b], y});
     }
-    HIPCK(k_tensor_launch(c, tt, m, level, s));
     if ((err = key_switch_batch(c, level, srcs, jobs, s))) return err;
     if ((err = op_rescale_add_many(c, m, t.data(), outs + g0, adds ? adds + g0 : nullptr, level,
                                    out_rows, s)))

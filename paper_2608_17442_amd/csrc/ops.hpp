@@ -13,16 +13,6 @@ hipError_t k_binary_launch(const Context* c, const uint64_t* a, const uint64_t* 
                            uint32_t rows, uint32_t shift, int op, hipStream_t s);
 hipError_t k_mul_plain_launch(const Context* c, const uint64_t* ct, const uint64_t* pt,
                               uint64_t* out, uint32_t level, hipStream_t s);
-// Tensors of up to kMaxBatch products (blockIdx.z = product): d01[b] may
-// alias x[b] or y[b], but no operand of another product of the launch.
-struct TsTable {
-  const uint64_t* x[32];
-  const uint64_t* y[32];
-  uint64_t* d01[32];
-  uint64_t* d2[32];
-};
-hipError_t k_tensor_launch(const Context* c, const TsTable& tab, uint32_t count, uint32_t level,
-                           hipStream_t s);
 hipError_t k_monomial_launch(const Context* c, const uint64_t* in, uint64_t* out,
                              uint32_t level, uint32_t m, hipStream_t s);
 hipError_t k_galois_launch(const Context* c, const uint64_t* in, uint64_t* out, uint32_t rows,
@@ -48,12 +38,18 @@ struct RsTable {
 // ----------------------------------------------------------- keyswitch.hip
 
 // Up to kMaxBatch ModUp sources and key-switch jobs per launch.  Passed by
-// value as a kernel argument (2 KB).
+// value as a kernel argument (under 3 KB).
 constexpr uint32_t kMaxBatch = 32;
 
 struct KsTable {
   const uint64_t* src_in[kMaxBatch];  // source s: row i at src_in[s] + i*src_stride[s]
   uint64_t src_stride[kMaxBatch];
+  // source s a product (relinearisation): row i is src_in[s] row i times
+  // src_y[s] row i (same stride), formed where it is read; null: plain
+  const uint64_t* src_y[kMaxBatch];
+  // job addend a tensor: with x = add, y = add_y (ciphertexts), the addend
+  // components are (x0 y0, x0 y1 + x1 y0); needs fold; null: plain addend
+  const uint64_t* add_y[kMaxBatch];
   const uint64_t* key[kMaxBatch];     // job: switching key
   const uint64_t* add[kMaxBatch];     // job: ciphertext added after sigma_g (or null)
   const uint64_t* add2[kMaxBatch];    // job: ciphertext added as is (or null)
@@ -112,11 +108,14 @@ struct KsJob {
   uint32_t add_galois;
   const uint64_t* add2;
   uint64_t* out;
+  const uint64_t* add_y = nullptr;  // addend is the tensor (add, add_y): components 0, 1
 };
 struct KsSource {
   const uint64_t* in;
   size_t stride;
+  const uint64_t* y = nullptr;  // source is the product in * y (row by row)
 };
+static_assert(sizeof(KsTable) < 3072, "key-switch table must stay a small kernel argument");
 
 // Runs any number of key switches at one level: ModUp of every source (at
 // most kMaxBatch), then inner product, ModDown and combine of the jobs in
@@ -148,9 +147,9 @@ int op_rescale_add_many(Context* c, uint32_t count, const uint64_t* const* ins,
                         uint32_t out_rows, hipStream_t s);
 // Products out_i = RS(relin(x_i * y_i)) + add_i at `level`, first out_rows
 // limbs written.  Runs in groups of the scratch capacity (an even number):
-// every tensor of a group is formed before any output of the group is
-// written, so an output may alias an input of a product in its own group;
-// it must not alias an input of a product in a later group.
+// every operand of a group is read (by its key switch) before any output of
+// the group is written, so an output may alias an input of a product in its
+// own group; it must not alias an input of a product in a later group.
 int op_prod_rescale_many(Context* c, uint32_t count, const uint64_t* const* xs,
                          const uint64_t* const* ys, uint64_t* const* outs,
                          const uint64_t* const* adds, uint32_t level, uint32_t out_rows,
