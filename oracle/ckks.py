@@ -381,6 +381,42 @@ def moddown(P: Params, acc: np.ndarray, level: int) -> np.ndarray:
     return pscalar(psub(acc[:level], y, qs), pinv, qs)
 
 
+def moddown_rescale(P: Params, x: np.ndarray, level: int) -> np.ndarray:
+    """ModDown and rescale as one division by M = P q_{level-1}: x over
+    ext(level) (evaluation form) -> (x - FastBConv_{M->Q}([x]_M)) * M^-1 on
+    q_0..q_{level-2}, the conversion digits coming from the q_{level-1} row and
+    the special-prime rows (the floor variant of ModDown with q_{level-1}
+    joined to the special primes)."""
+    assert level >= 2
+    ql = P.q[level - 1]
+    src = [ql] + list(P.p)
+    coef = intt(P, np.concatenate([x[level - 1:level], x[level:]]), src)
+    qs = P.qs(level - 1)
+    y = ntt(P, fast_bconv(coef, src, qs), qs)
+    M = P.P * ql
+    return pscalar(psub(x[:level - 1], y, qs), [pow(M % q, -1, q) for q in qs], qs)
+
+
+def mul_relin_rescale(P: Params, a, b, rlk):
+    """Relinearised product divided by P q_{level-1} in one step: acc = key
+    product of d2 over ext(level); x_t = acc_t + P d_t on the Q rows (P d_t
+    vanishes modulo every special prime); out_t = moddown_rescale(x_t).  The
+    result is at level - 1; it differs from rescale(mul_relin(a, b)) only in
+    the rounding (one conversion error of at most (alpha + 1) / 2 units)."""
+    level = a.shape[0]
+    d0, d1, d2 = tensor(P, a, b)
+    qs, ext = P.qs(level), P.ext(level)
+    digits = [ntt(P, d, ext) for d in modup(P, intt(P, d2, qs), level)]
+    acc = key_inner_product(P, digits, rlk, level)
+    pm = [P.P % q for q in qs]
+    out = np.empty((level - 1, 2, P.n), dtype=np.uint64)
+    for t, d in enumerate((d0, d1)):
+        x = acc[t].copy()
+        x[:level] = padd(acc[t][:level], pscalar(d, pm, qs), qs)
+        out[:, t] = moddown_rescale(P, x, level)
+    return out
+
+
 def key_switch(P: Params, c: np.ndarray, key: np.ndarray, level: int):
     """Hybrid key switch of one evaluation-form polynomial ``u64[level][N]``;
     returns (out_b, out_a), each ``u64[level][N]``."""

@@ -20,9 +20,11 @@ Readings taken where the paper is silent or inconsistent:
   independent scan over (a^(kappa), s^(kappa)), two relinearised products per
   composition, which is the per-chunk count 2 K_s BK(L) of Table
   "real-phantom-scan".
-* A ciphertext product is relinearised and rescaled; the addend s_R is
-  brought to the product's level by dropping its trailing limbs (modulus
-  switching without division: message and scale unchanged).
+* A ciphertext product is relinearised and rescaled in one division by
+  P q_{l-1} (ckks.mul_relin_rescale: the ModDown conversion takes q_{l-1}
+  together with the special primes; the paper fixes neither operation); the
+  addend s_R is brought to the product's level by dropping its trailing limbs
+  (modulus switching without division: message and scale unchanged).
 * Operands at different levels (the down-sweep combines prefixes of unequal
   depth) are composed at the lower level, the higher one dropped to it.
 * Down-sweep: at stage s every multiple k of 2^s passes its prefix to
@@ -100,8 +102,8 @@ def compose(P: C.Params, left: tuple, right: tuple, rlk) -> tuple:
     aR, sR = right
     lvl = min(aL.shape[0], aR.shape[0])
     aL, sL, aR, sR = (_drop(x, lvl) for x in (aL, sL, aR, sR))
-    a = C.rescale(P, C.mul_relin(P, aR, aL, rlk))
-    s = C.ct_add(P, C.rescale(P, C.mul_relin(P, aR, sL, rlk)), _drop(sR, lvl - 1))
+    a = C.mul_relin_rescale(P, aR, aL, rlk)
+    s = C.ct_add(P, C.mul_relin_rescale(P, aR, sL, rlk), _drop(sR, lvl - 1))
     return a, s
 
 
@@ -110,7 +112,7 @@ def apply_to_state(P: C.Params, prefix: tuple, carry_s, rlk):
     prefix(G(0)) = a_P * s_G + s_P."""
     aP, sP = prefix
     lvl = min(aP.shape[0], carry_s.shape[0])
-    prod = C.rescale(P, C.mul_relin(P, _drop(aP, lvl), _drop(carry_s, lvl), rlk))
+    prod = C.mul_relin_rescale(P, _drop(aP, lvl), _drop(carry_s, lvl), rlk)
     return C.ct_add(P, prod, _drop(sP, lvl - 1))
 
 

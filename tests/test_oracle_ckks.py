@@ -155,6 +155,54 @@ def test_moddown_is_exact_division_of_acc_minus_bconv(small):
         assert abs(y) < P.alpha * P.P // 2
 
 
+def test_moddown_rescale_is_exact_division(small):
+    """(X - y) / M with M = P q_{l-1} and y the centred conversion of X mod M
+    from the digits of q_{l-1} and the special primes, big-integer arithmetic."""
+    P, sk = small
+    level = 4
+    ext = P.ext(level)
+    rnd = np.random.default_rng(6)
+    x = np.stack([rnd.integers(0, m, size=P.n, dtype=np.uint64) for m in ext])
+    out = C.moddown_rescale(P, C.ntt(P, x, ext), level)
+    assert out.shape == (level - 1, P.n)
+    QP = 1
+    for m in ext:
+        QP *= m
+    ql = P.q[level - 1]
+    M = P.P * ql
+    Qo = QP // M
+    A = [int(v) % QP for v in E.crt_centered(x, ext)]
+    got = [int(v) % Qo for v in E.crt_centered(C.intt(P, out, P.qs(level - 1)),
+                                                P.qs(level - 1))]
+    for k in range(P.n):
+        y = 0
+        for m in [ql] + list(P.p):
+            mh = M // m
+            xi = A[k] % m * pow(mh, -1, m) % m
+            if xi > m // 2:
+                xi -= m
+            y += xi * mh
+        assert (A[k] - y) % M == 0
+        assert got[k] == ((A[k] - y) // M) % Qo
+        assert abs(y) < (P.alpha + 1) * M // 2
+
+
+def test_mul_relin_rescale_decrypts_like_the_two_steps(small):
+    P, sk = small
+    rlk = C.keygen_from_seed(P, sk, 3, 0)
+    level = 5
+    z1, z2 = _z(50, P.n // 2), _z(51, P.n // 2)
+    ql = P.q[level - 1]
+    c1 = _enc(P, sk, z1, 2.0 ** 40, level, "mrr1")
+    c2 = _enc(P, sk, z2, float(ql), level, "mrr2")
+    fused = C.mul_relin_rescale(P, c1, c2, rlk)
+    seq = C.rescale(P, C.mul_relin(P, c1, c2, rlk))
+    assert fused.shape == seq.shape == (level - 1, 2, P.n)
+    df = C.decrypt(P, sk, fused, 2.0 ** 40)
+    np.testing.assert_allclose(df, z1 * z2, atol=2.0 ** -15)
+    np.testing.assert_allclose(df, C.decrypt(P, sk, seq, 2.0 ** 40), atol=2.0 ** -28)
+
+
 # --------------------------------------------- decrypt-based operation pins
 
 
