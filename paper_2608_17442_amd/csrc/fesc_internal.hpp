@@ -113,6 +113,10 @@ struct LevelTables {
   double2* md_inv_n = nullptr; // [alpha]  N^-1 (P/p_k)^-1 mod p_k
   double2* rs_ninv = nullptr;  // [1]      N^-1 mod q_{level-1}
   double2* one = nullptr;      // [level]  1 (with 1/q_i)
+  // ModDown merged with the rescale (division by M = P q_{level-1}); digit
+  // sources m_0 = q_{level-1}, m_{1+k} = p_k
+  double2* mr_inv_n = nullptr; // [alpha+1]  N^-1 (M/m_j)^-1 mod m_j (m_0: N^-1, the row holding x P^-1)
+  double2* mr_hat = nullptr;   // [level-1][alpha+1]  (M/m_j) mod q_i
 };
 
 struct Context {

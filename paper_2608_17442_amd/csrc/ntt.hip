@@ -360,6 +360,28 @@ struct ModdownMap {
   }
 };
 
+// ModDown merged with the rescale: group g = 2 * job + component, digits =
+// the alpha + 1 rows level-1 .. level+alpha-1 of acc[g] (q_{level-1}, then the
+// special primes), targets = rows 0 .. rows-1 (< level - 1) of y[g], stored
+// [g][level-1][N].
+struct ModdownRescaleMap {
+  const uint64_t* acc;
+  uint64_t* y;
+  const double2* mr_hat;
+  uint32_t level, E, alpha, rows, n;  // alpha = number of digits (special primes + 1)
+  __device__ uint32_t aj(uint32_t) const { return alpha; }
+  __device__ uint32_t targets(uint32_t) const { return rows; }
+  __device__ uint32_t row(uint32_t, uint32_t t) const { return t; }
+  __device__ uint32_t prime(uint32_t r) const { return r; }
+  __device__ const double* digits(uint32_t g) const {
+    return reinterpret_cast<const double*>(acc + ((size_t)g * E + level - 1) * n);
+  }
+  __device__ const double2* hat(uint32_t, uint32_t r) const { return mr_hat + (size_t)r * alpha; }
+  __device__ uint64_t* out(uint32_t g, uint32_t r) const {
+    return y + ((size_t)g * (level - 1) + r) * n;
+  }
+};
+
 // Rescale lift: group g = 2 b + t (component t of ciphertext b), one digit =
 // the centred last limb v[g] (|v| < q_last / 2), weight 1 for every target,
 // targets = rows 0 .. rows-1 of w[g]: each target row gets v mod q_i.
@@ -569,11 +591,14 @@ __global__ __launch_bounds__(kThreads) void k_inv_inner(RowSel rs, uint32_t log_
 // (blockIdx.z), out_job[i][t] = (acc[u][i] - NTT(y)[u][i]) * P^-1 + adds,
 // with the adds of the job table (sigma_g-permuted `add`, plain `add2`).  If
 // tab.fold the inner product has already stored acc * P^-1 + add, and only
-// NTT(y) * P^-1 is subtracted here.
+// NTT(y) * P^-1 is subtracted here.  With qlinv (ModDown merged with the
+// rescale, fold only) the difference is also multiplied by q_{level-1}^-1
+// before add2 is added.
 struct KsCombine {
   KsTable tab;
   const uint64_t* acc;
   const double2* pinv;
+  const double2* qlinv;
   uint32_t level, alpha, log_n;
   __device__ __forceinline__ void operator()(uint64_t*, uint32_t k0, const double (&x)[16],
                                              double q, double qinv, uint32_t n) const {
@@ -588,10 +613,12 @@ struct KsCombine {
     const uint64_t* add2 = tab.add2[job];
     uint64_t* out = tab.out[job] + o;
     if (tab.fold) {
+      const double2 h = qlinv ? qlinv[i] : double2{0.0, 0.0};
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const uint32_t k = k0 + 256 * r;
-        double v = u2d(a[k]) - mm_shoup(x[r], f.x, f.y, q);
+        double v = u2d(a[k]) - mm_shoup(x[r], f.x, f.y, q);  // |v| < 2.5 q
+        if (qlinv) v = mm_shoup(v, h.x, h.y, q);
         if (add2) v += u2d(add2[o + k]);
         out[k] = to_res(v, q, qinv);
       }
@@ -787,15 +814,28 @@ hipError_t launch_ntt_fwd_inner_rows(const Context* c, const RowSel& rs, uint32_
   return launch_fwd_inner(c, rs, batch, limbs, StoreResidues{}, s);
 }
 
-// Second forward pass of the ModDown conversions y[2*njobs][level][N]
-// (first pass: launch_moddown_outer) with the key-switch combine as the
-// epilogue; writes the jobs' outputs.
+// ModDown merged with the rescale: conversion of the alpha + 1 digit rows of
+// acc (launch_ntt_inv_digits with mr_inv_n) to rows 0 .. rows-1, fused with
+// the first forward pass of y[2*njobs][level-1][N].
+hipError_t launch_moddown_rescale_outer(const Context* c, const LevelTables& T,
+                                        const uint64_t* acc, uint64_t* y, uint32_t njobs,
+                                        uint32_t level, uint32_t rows, hipStream_t s) {
+  const ModdownRescaleMap map{acc, y, T.mr_hat, level, level + c->alpha, c->alpha + 1, rows,
+                              c->n};
+  return launch_bconv_outer(c, map, rows, 2 * njobs, s);
+}
+
+// Second forward pass of the ModDown conversions y[2*njobs][ystride][N]
+// (first pass: launch_moddown_outer or launch_moddown_rescale_outer) with the
+// key-switch combine as the epilogue; writes rows 0 .. rows-1 of the jobs'
+// outputs.  qlinv: null, or q_{level-1}^-1 per row (merged rescale).
 hipError_t launch_ntt_fwd_ks_combine(const Context* c, uint64_t* y, uint32_t njobs,
-                                     uint32_t level, const KsTable& tab, const uint64_t* acc,
-                                     const double2* pinv, hipStream_t s) {
-  RowSel rs{y, (size_t)level * c->n, (size_t)c->n, 0, level, 0, 0, 0, 0};
-  return launch_fwd_inner(c, rs, 2 * njobs, level,
-                          KsCombine{tab, acc, pinv, level, c->alpha, c->log_n}, s);
+                                     uint32_t level, uint32_t rows, uint32_t ystride,
+                                     const KsTable& tab, const uint64_t* acc,
+                                     const double2* pinv, const double2* qlinv, hipStream_t s) {
+  RowSel rs{y, (size_t)ystride * c->n, (size_t)c->n, 0, rows, 0, 0, 0, 0};
+  return launch_fwd_inner(c, rs, 2 * njobs, rows,
+                          KsCombine{tab, acc, pinv, qlinv, level, c->alpha, c->log_n}, s);
 }
 
 // (Splitting a large batch into cache-sized chunks, so that the second pass

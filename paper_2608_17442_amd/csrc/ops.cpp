@@ -69,20 +69,36 @@ const LevelTables* level_tables(Context* c, uint32_t level, int* err) {
       if (i + 1 < level) rs_inv[i] = entry(h_inv(c->primes[level - 1] % q, q), q);
     }
   }
-  std::vector<double2> rs_ninv(1), one(level);
+  std::vector<double2> rs_ninv(1), one(level), mr_inv_n(alpha + 1),
+      mr_hat((size_t)(level - 1) * (alpha + 1));
   {
     const uint64_t ql = c->primes[level - 1];
     rs_ninv[0] = entry(h_inv(c->n % ql, ql), ql);
     for (uint32_t i = 0; i < level; ++i) one[i] = entry(1, c->primes[i]);
+    // m_0 = q_{level-1}: the inner product stores x P^-1 on that row, which is
+    // already x (M/m_0)^-1, so its constant is N^-1 alone
+    mr_inv_n[0] = entry(h_inv(c->n % ql, ql), ql);
+    for (uint32_t a = 0; a < alpha; ++a) {
+      const uint64_t pa = ps[a];
+      const uint64_t mh = h_mulmod(prod_mod_except(ps, a, pa), ql % pa, pa);  // M/p_a mod p_a
+      mr_inv_n[1 + a] = entry(h_mulmod(h_inv(mh, pa), h_inv(c->n % pa, pa), pa), pa);
+    }
+    for (uint32_t i = 0; i + 1 < level; ++i) {
+      const uint64_t q = c->primes[i];
+      mr_hat[(size_t)i * (alpha + 1)] = entry(prod_mod_except(ps, ps.size(), q), q);  // P
+      for (uint32_t a = 0; a < alpha; ++a)
+        mr_hat[(size_t)i * (alpha + 1) + 1 + a] =
+            entry(h_mulmod(prod_mod_except(ps, a, q), ql % q, q), q);  // (P/p_a) q_{l-1}
+    }
   }
   std::vector<double2> all;
   LevelTables T;
   T.level = level;
-  size_t off[11];
-  const std::vector<double2>* parts[11] = {&mu_inv,   &mu_hat,   &md_inv,  &md_hat,
-                                           &md_pinv,  &pmod,     &rs_inv,  &mu_inv_n,
-                                           &md_inv_n, &rs_ninv,  &one};
-  for (int p = 0; p < 11; ++p) {
+  size_t off[13];
+  const std::vector<double2>* parts[13] = {&mu_inv,   &mu_hat,  &md_inv,   &md_hat, &md_pinv,
+                                           &pmod,     &rs_inv,  &mu_inv_n, &md_inv_n,
+                                           &rs_ninv,  &one,     &mr_inv_n, &mr_hat};
+  for (int p = 0; p < 13; ++p) {
     off[p] = all.size();
     all.insert(all.end(), parts[p]->begin(), parts[p]->end());
   }
@@ -108,6 +124,8 @@ const LevelTables* level_tables(Context* c, uint32_t level, int* err) {
   T.md_inv_n = d + off[8];
   T.rs_ninv = d + off[9];
   T.one = d + off[10];
+  T.mr_inv_n = d + off[11];
+  T.mr_hat = d + off[12];
   return &(c->level_tabs[level] = T);
 }
 
@@ -173,8 +191,10 @@ hipError_t ntt_rows(const Context* c, uint64_t* d, uint32_t batch, size_t batch_
 // --------------------------------------------------------- key switch engine
 
 int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& srcs,
-                     const std::vector<KsJob>& jobs, hipStream_t s) {
+                     const std::vector<KsJob>& jobs, hipStream_t s, uint32_t rescale_rows) {
   if (jobs.empty()) return FESC_OK;
+  if (rescale_rows && (level < 2 || rescale_rows > level - 1))
+    return fail(FESC_ERR_LEVEL, "merged rescale needs level >= 2 and rows <= level - 1");
   if (srcs.size() > kMaxBatch) return fail(FESC_ERR_ARG, "too many key-switch sources");
   int err;
   const LevelTables* T = level_tables(c, level, &err);
@@ -235,13 +255,27 @@ int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& sr
     }
     for (uint32_t j = 0; j < nj && !t.fold; ++j)
       if (t.add_y[j]) return fail(FESC_ERR_ARG, "a tensor addend needs the folded combine");
+    if (rescale_rows && !t.fold) return fail(FESC_ERR_ARG, "merged rescale needs folded addends");
     HIPCK(k_ip_launch(c, t, nkeys, S.ext, S.acc, level, T->md_pinv, s));
+    if (rescale_rows) {
+      // rows q_{level-1}, p_0 .. p_{alpha-1} (adjacent in acc): iNTT to the
+      // centred digits of M = P q_{level-1}; conversion to the kept rows fused
+      // with the first forward pass; combine times q_{level-1}^-1
+      const RowSel rp{S.acc + (size_t)(level - 1) * n, (size_t)E * n, n, level - 1, 1, c->L,
+                      0, 0, 0};
+      HIPCK(launch_ntt_inv_digits(c, rp, 2 * nj, c->alpha + 1, T->mr_inv_n, s));
+      HIPCK(launch_moddown_rescale_outer(c, *T, S.acc, S.y, nj, level, rescale_rows, s));
+      HIPCK(launch_ntt_fwd_ks_combine(c, S.y, nj, level, rescale_rows, level - 1, t, S.acc,
+                                      T->md_pinv, T->rs_inv, s));
+      continue;
+    }
     // special-prime rows: iNTT to centred ModDown digits, conversion fused
     // with the first forward pass of y, second pass ending in the combine
     const RowSel rp{S.acc + (size_t)level * n, (size_t)E * n, n, c->L, c->alpha, 0, 0, 0, 0};
     HIPCK(launch_ntt_inv_digits(c, rp, 2 * nj, c->alpha, T->md_inv_n, s));
     HIPCK(launch_moddown_outer(c, *T, S.acc, S.y, nj, level, s));
-    HIPCK(launch_ntt_fwd_ks_combine(c, S.y, nj, level, t, S.acc, T->md_pinv, s));
+    HIPCK(launch_ntt_fwd_ks_combine(c, S.y, nj, level, level, level, t, S.acc, T->md_pinv,
+                                    nullptr, s));
   }
   return FESC_OK;
 }
@@ -427,15 +461,14 @@ int op_prod_rescale_many(Context* c, uint32_t count, const uint64_t* const* xs,
   const uint64_t* key;
   int err;
   if ((err = key_of(c, 0, &key))) return err;
-  // the batched layout first: the calls below keep it, so S.cts stays in
-  // place
   Scratch S;
   if ((err = scratch(c, &S, 2))) return err;
   const uint32_t G = S.cap & ~1u;
   if (G < 2) return fail(FESC_ERR_OOM, "batched products need batched scratch");
-  const size_t n = c->n, W = (size_t)2 * c->L * n;
-  std::vector<uint64_t*> t(G);
-  for (uint32_t b = 0; b < G; ++b) t[b] = S.cts + (size_t)b * W;
+  const size_t n = c->n;
+  // one key switch per group: tensor formed inside (source x1 y1, folded
+  // addend (x0 y0, x0 y1 + x1 y0)), ModDown merged with the rescale, add_i
+  // added in the combine
   for (uint32_t g0 = 0; g0 < count; g0 += G) {
     const uint32_t m = std::min(G, count - g0);
     std::vector<KsSource> srcs;
@@ -443,12 +476,10 @@ int op_prod_rescale_many(Context* c, uint32_t count, const uint64_t* const* xs,
     for (uint32_t b = 0; b < m; ++b) {
       const uint64_t *x = xs[g0 + b], *y = ys[g0 + b];
       srcs.push_back(KsSource{x + n, 2 * n, y + n});
-      jobs.push_back(KsJob{b, key, 0, x, 3u, 0, nullptr, t[b], y});
+      jobs.push_back(
+          KsJob{b, key, 0, x, 3u, 0, adds ? adds[g0 + b] : nullptr, outs[g0 + b], y});
     }
-    if ((err = key_switch_batch(c, level, srcs, jobs, s))) return err;
-    if ((err = op_rescale_add_many(c, m, t.data(), outs + g0, adds ? adds + g0 : nullptr, level,
-                                   out_rows, s)))
-      return err;
+    if ((err = key_switch_batch(c, level, srcs, jobs, s, out_rows))) return err;
   }
   return FESC_OK;
 }

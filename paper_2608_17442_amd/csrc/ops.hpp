@@ -88,9 +88,13 @@ hipError_t launch_moddown_outer(const Context* c, const LevelTables& T, const ui
                                 uint64_t* y, uint32_t njobs, uint32_t level, hipStream_t s);
 hipError_t launch_ntt_fwd_inner_rows(const Context* c, const RowSel& rs, uint32_t batch,
                                      uint32_t limbs, hipStream_t s);
+hipError_t launch_moddown_rescale_outer(const Context* c, const LevelTables& T,
+                                        const uint64_t* acc, uint64_t* y, uint32_t njobs,
+                                        uint32_t level, uint32_t rows, hipStream_t s);
 hipError_t launch_ntt_fwd_ks_combine(const Context* c, uint64_t* y, uint32_t njobs,
-                                     uint32_t level, const KsTable& tab, const uint64_t* acc,
-                                     const double2* pinv, hipStream_t s);
+                                     uint32_t level, uint32_t rows, uint32_t ystride,
+                                     const KsTable& tab, const uint64_t* acc,
+                                     const double2* pinv, const double2* qlinv, hipStream_t s);
 hipError_t k_ip_launch(const Context* c, const KsTable& tab, uint32_t nkeys, const uint64_t* ext,
                        uint64_t* acc, uint32_t level, const double2* pinv, hipStream_t s);
 
@@ -122,9 +126,11 @@ static_assert(sizeof(KsTable) < 3072, "key-switch table must stay a small kernel
 // groups of kMaxBatch, jobs ordered by switching key so that each key is read
 // once per group (key-stationary inner product).  Sources must stay
 // unmodified until all jobs have read them; a job's output must not alias a
-// source or addend of another job.
+// source or addend of another job.  rescale_rows > 0: ModDown is merged with
+// the rescale (one division by P q_{level-1}, every addend folded) and the
+// outputs are the first rescale_rows (<= level - 1) limbs at level - 1.
 int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& srcs,
-                     const std::vector<KsJob>& jobs, hipStream_t s);
+                     const std::vector<KsJob>& jobs, hipStream_t s, uint32_t rescale_rows = 0);
 
 int op_rotate_many(Context* c, const uint64_t* in, uint32_t count, const int32_t* steps,
                    uint64_t* const* outs, uint32_t level, hipStream_t s);
@@ -145,11 +151,12 @@ int op_rescale_many(Context* c, uint32_t count, const uint64_t* const* ins, uint
 int op_rescale_add_many(Context* c, uint32_t count, const uint64_t* const* ins,
                         uint64_t* const* outs, const uint64_t* const* adds, uint32_t level,
                         uint32_t out_rows, hipStream_t s);
-// Products out_i = RS(relin(x_i * y_i)) + add_i at `level`, first out_rows
-// limbs written.  Runs in groups of the scratch capacity (an even number):
-// every operand of a group is read (by its key switch) before any output of
-// the group is written, so an output may alias an input of a product in its
-// own group; it must not alias an input of a product in a later group.
+// Products out_i = relin(x_i * y_i) / (P q_{level-1}) + add_i (ModDown merged
+// with the rescale) at `level`, first out_rows limbs written.  Runs in groups
+// of the scratch capacity (an even number), one key switch per group: every
+// operand of a group is read before any output of the group is written, so an
+// output may alias an input of a product in its own group (add_i only its own
+// product's); it must not alias an input of a product in a later group.
 int op_prod_rescale_many(Context* c, uint32_t count, const uint64_t* const* xs,
                          const uint64_t* const* ys, uint64_t* const* outs,
                          const uint64_t* const* adds, uint32_t level, uint32_t out_rows,
