@@ -61,9 +61,19 @@ def kernel_sources_sha256(paths) -> str:
     return h.hexdigest()
 
 
-def profiled_traffic(profile: str, sources) -> int | None:
-    """Bytes per launch recorded in `profile`, or None if the file is missing
-    or the kernel sources changed since the counters were taken."""
+# Per-kernel roofline of the key switch (each kernel's time at its own binding
+# resource, HBM from the rocprofv3 counters or VALU from its work and the
+# calibrated rates), from the committed profile of the rotation set; valid
+# only while the pipeline's sources are unchanged.
+KS_PROFILE = os.path.join(ROOT, "profiles", "keyswitch_rotation_set_n65536_l24_dnum3.txt")
+KS_SOURCES = [os.path.join(ROOT, "paper_2608_17442_amd", "csrc", f)
+              for f in ("ntt.hip", "keyswitch.hip", "butterfly.hpp", "fesc_internal.hpp",
+                        "ops.cpp", "ops.hpp")]
+
+
+def profiled_fields(profile: str, sources) -> dict | None:
+    """The '# key: value' lines of `profile`, or None if the file is missing
+    or the kernel sources changed since it was taken."""
     if not os.path.exists(profile):
         return None
     fields = {}
@@ -72,6 +82,15 @@ def profiled_traffic(profile: str, sources) -> int | None:
             k, v = line[2:].split(":", 1)
             fields[k.strip()] = v.strip()
     if fields.get("kernel_sources_sha256") != kernel_sources_sha256(sources):
+        return None
+    return fields
+
+
+def profiled_traffic(profile: str, sources) -> int | None:
+    """Bytes per launch recorded in `profile`, or None if the file is missing
+    or the kernel sources changed since the counters were taken."""
+    fields = profiled_fields(profile, sources)
+    if fields is None:
         return None
     try:
         return int(fields["traffic_bytes_per_launch"])
@@ -284,6 +303,17 @@ class Workloads:
                                   states_only=True)
         ev[1].record()
         return lo
+
+
+def keyswitch_per_kernel():
+    f = profiled_fields(KS_PROFILE, KS_SOURCES)
+    if f is None or "keyswitch_bound_fraction" not in f:
+        return None
+    return {"bound": "hbm or alu per kernel",
+            "frac": float(f["keyswitch_bound_fraction"].split()[0]),
+            "source": os.path.relpath(KS_PROFILE, ROOT),
+            "note": "sum over the key switch's kernels of max(HBM bytes / 8 TB/s, VALU work / "
+                    "calibrated VALU rate), over the sum of their measured times"}
 
 
 def time_affine(W, F, torch, np):
@@ -525,6 +555,7 @@ def main():
                                  "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                  "frac": round(2 * ntt_gbs / HBM_PEAK_GBS, 4),
                                  "note": "two passes each read and write the data once"},
+            "keyswitch_per_kernel": keyswitch_per_kernel(),
             "keyswitch_valu": {"bound": "alu", "frac": round(ks_valu_frac, 4),
                                "per_key_switch": {"butterflies": ks_bfly, "mod_macs": ks_macs},
                                "peak_butterflies_per_s": round(peak["ct"], -9),
