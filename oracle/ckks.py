@@ -304,6 +304,14 @@ def ct_sub(P, a, b):
     return out
 
 
+def add_plain(P: Params, ct: np.ndarray, pt: np.ndarray) -> np.ndarray:
+    """(c0 + p, c1): adds the plaintext p to the message."""
+    level = ct.shape[0]
+    out = ct.copy()
+    out[:, 0] = padd(ct[:, 0], pt[:level], P.qs(level))
+    return out
+
+
 def mul_plain(P: Params, ct: np.ndarray, pt: np.ndarray) -> np.ndarray:
     """ptmul: (c0 * p, c1 * p) limb-wise."""
     level = ct.shape[0]

@@ -23,6 +23,12 @@ When the slot count exceeds the packed width (n_slots > C * seg_len) the
 segment index is taken modulo C, i.e. the vector is replicated, which is how a
 short vector is made rotation-periodic.
 
+Small kernels on the same primitives: HEConv (Sec. "Causal Depthwise
+Convolution"), the fused post-SSM path (Appendix "Fused Post-SSM Path"),
+modulus trimming before the CKKS-to-MPC conversion (Appendix "Adopted Modulus
+Trimming") and the server's conversion mask (Algorithm "Complex CKKS-to-MPC
+conversion", first two steps).
+
 Scan-contract slice (Eq. "hescan-contract-output" and Appendix "Complex-Packed
 Reduction Accounting"): per token and state chunk, t1 = RS(relin(a * h)),
 t2 = RS(relin(t1 * C)); chunks (2l, 2l+1) are packed as chi = t2^(2l) + i
@@ -171,3 +177,53 @@ def scan_contract_token(P: C.Params, h: list, decay: list, cfac: list, rlk, keys
     if K % 2:
         outs.append(reduce_axis(P, t2[-1], d_s, keys))
     return outs
+
+
+# ------------------------------------------ small kernels on the same primitives
+
+
+def heconv(P: C.Params, q: np.ndarray, deltas, masks, bias, keys: dict) -> np.ndarray:
+    """HEConv: eta = RS(sum_r M_r (.) rho(q; delta_r)) + b.  q: ciphertext at
+    level l; masks: plaintexts (tap weights fused with the causal boundary
+    mask), encoded at the scale of q_{l-1} so that the rescale returns q's
+    scale; bias: plaintext at that output scale (>= l - 1 limbs), or None;
+    deltas: public rotation offsets (negative: rotation to the right).  Output
+    at level l - 1."""
+    acc = None
+    for d, m in zip(deltas, masks):
+        t = C.mul_plain(P, C.rotate(P, q, d, keys), m)
+        acc = t if acc is None else C.ct_add(P, acc, t)
+    out = C.rescale(P, acc)
+    if bias is not None:
+        out = C.add_plain(P, out, bias)
+    return out
+
+
+def post_ssm(P: C.Params, m: np.ndarray, x_skip: np.ndarray, d_skip: np.ndarray,
+             g: np.ndarray, rlk) -> np.ndarray:
+    """Fused post-SSM path: y = m + D (.) x_skip, then y (.) g.  m, x_skip, g
+    at level l; D a plaintext (at the scale of q_{l-1}); g at the scale of
+    q_{l-2}.  y = RS(D (.) x_skip) + m at level l - 1; the gate product is
+    relinearised and rescaled in one division (as in the scan) -> level l - 2."""
+    level = m.shape[0]
+    y = C.ct_add(P, C.rescale(P, C.mul_plain(P, x_skip, d_skip)), m[:level - 1])
+    return C.mul_relin_rescale(P, y, g[:level - 1], rlk)
+
+
+def c2m_level(P: C.Params, level: int, ell: int, sigma: int, delta: float, bmax: float):
+    """Modulus trimming before CKKS-to-MPC conversion: the smallest level
+    l' <= level whose modulus Q = q_0 ... q_{l'-1} has log2 Q >= ell + sigma + 1
+    and Q / 2 > delta * bmax (the ciphertext is then its first l' limbs); None
+    if no level qualifies."""
+    Q = 1
+    for lp in range(1, level + 1):
+        Q *= P.q[lp - 1]
+        if Q >= 1 << (ell + sigma + 1) and Q / 2 > delta * bmax:
+            return lp
+    return None
+
+
+def c2m_mask(P: C.Params, ct: np.ndarray, rhat: np.ndarray) -> np.ndarray:
+    """The server's conversion mask: <d> = <m> + r_hat, r_hat a uniform
+    polynomial (evaluation form, drawn by the caller) added to the message."""
+    return C.add_plain(P, ct, rhat)

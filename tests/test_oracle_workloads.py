@@ -134,3 +134,103 @@ def test_scan_contract_slice_small():
             assert outs[2 * l + half].shape[0] == 2
             got = dec.real[:: d_s]
             np.testing.assert_allclose(got, want[k * c_state:(k + 1) * c_state], atol=2.0 ** -15)
+
+
+# ------------------------------------------------- small kernels (HEConv etc.)
+
+
+def _enc_ct(P, sk, vals, scale, level, tag, idx=0):
+    return C.encrypt(P, sk, C.encode_plain(P, np.asarray(vals, dtype=complex), scale, level),
+                     level, *synth.encrypt_draws(6, P.qs(level), P.n, tag, idx))
+
+
+def conv_inputs(P, T, d_conv, seed=6):
+    """Channels on segments of T token slots (slot c*T + k); taps r = 0..d-1 at
+    offset -r with the causal boundary (k >= r) in the mask."""
+    n_slots = P.n // 2
+    Cn = n_slots // T
+    qv = synth.normal(seed, "conv-q", (Cn, T))
+    w = synth.normal(seed, "conv-w", (Cn, d_conv), 0.5)
+    b = synth.normal(seed, "conv-b", Cn)
+    k = np.arange(T)
+    masks = [np.where(k[None, :] >= r, w[:, r:r + 1], 0.0).reshape(-1) for r in range(d_conv)]
+    return qv, w, b, masks
+
+
+def test_heconv_decodes_to_the_depthwise_causal_convolution():
+    P = C.params_small(12, 50, 4, 2)
+    sk = C.secret_key(P, synth.secret(6, P.n))
+    T, d_conv, level = 64, 4, 3
+    deltas = [-r for r in range(d_conv)]
+    keys = _keys(P, sk, 6, deltas)
+    qv, w, b, masks = conv_inputs(P, T, d_conv)
+    Cn = qv.shape[0]
+    ql = float(P.q[level - 1])
+    q = _enc_ct(P, sk, qv.reshape(-1), 2.0 ** 40, level, "q")
+    pts = [C.encode_plain(P, m.astype(complex), ql, level) for m in masks]
+    bias = C.encode_plain(P, np.repeat(b, T).astype(complex), 2.0 ** 40, level)
+    out = W.heconv(P, q, deltas, pts, bias, keys)
+    assert out.shape[0] == level - 1
+    got = C.decrypt(P, sk, out, 2.0 ** 40).real.reshape(Cn, T)
+    # Eq. "conv1d_depthwise": eta_k[c] = b_c + sum_r w_{c,r} q_{k-r}[c], q_t = 0 for t < 0
+    want = np.tile(b[:, None], (1, T))
+    for r in range(d_conv):
+        shifted = np.zeros_like(qv)
+        shifted[:, r:] = qv[:, :T - r]
+        want += w[:, r:r + 1] * shifted
+    np.testing.assert_allclose(got, want, atol=2.0 ** -15)
+
+
+def test_post_ssm_decodes_to_gated_skip():
+    P = C.params_small(12, 50, 5, 2)
+    sk = C.secret_key(P, synth.secret(6, P.n))
+    rlk = C.keygen_from_seed(P, sk, 6, 0)
+    level, n_slots = 4, P.n // 2
+    mv = synth.normal(6, "ps-m", n_slots)
+    xv = synth.normal(6, "ps-x", n_slots)
+    dv = synth.normal(6, "ps-D", n_slots)
+    gv = synth.uniform_pm1(6, "ps-g", n_slots)
+    m = _enc_ct(P, sk, mv, 2.0 ** 40, level, "m")
+    x = _enc_ct(P, sk, xv, 2.0 ** 40, level, "x")
+    g = _enc_ct(P, sk, gv, float(P.q[level - 2]), level, "g")
+    D = C.encode_plain(P, dv.astype(complex), float(P.q[level - 1]), level)
+    out = W.post_ssm(P, m, x, D, g, rlk)
+    assert out.shape[0] == level - 2
+    got = C.decrypt(P, sk, out, 2.0 ** 40).real
+    np.testing.assert_allclose(got, (mv + dv * xv) * gv, atol=2.0 ** -15)
+
+
+def test_c2m_level_is_the_shortest_admissible_modulus():
+    P = C.params_p16(24)
+    # 50-bit primes: ell + sigma + 1 = 64 + 40 + 1 = 105 bits need three primes
+    assert W.c2m_level(P, 24, 64, 40, 2.0 ** 40, 2.0 ** 10) == 3
+    # a large boundary magnitude: Q / 2 > 2^40 * 2^70 = 2^110 needs three primes too,
+    # 2^160 needs four
+    assert W.c2m_level(P, 24, 16, 40, 2.0 ** 40, 2.0 ** 120) == 4
+    # below the requirement at the available level: none
+    assert W.c2m_level(P, 2, 64, 40, 2.0 ** 40, 1.0) is None
+    # brute force over every level
+    for ell, sig, bm in [(32, 40, 2.0 ** 8), (48, 40, 2.0 ** 60), (20, 20, 1.0)]:
+        want = None
+        for lp in range(1, 25):
+            Q = int(np.prod([P.q[i] for i in range(lp)], dtype=object))
+            if Q.bit_length() - 1 >= ell + sig + 1 and Q / 2 > 2.0 ** 40 * bm:
+                want = lp
+                break
+        assert W.c2m_level(P, 24, ell, sig, 2.0 ** 40, bm) == want
+
+
+def test_c2m_mask_shares_reconstruct_the_message():
+    """Dec(<m> + r_hat) - r_hat = Dec(<m>) exactly on the coefficients (the two
+    shares of Algorithm "Complex CKKS-to-MPC conversion" reconstruct)."""
+    P = C.params_small(12, 50, 3, 1)
+    sk = C.secret_key(P, synth.secret(6, P.n))
+    level = 2
+    ct = _enc_ct(P, sk, synth.normal(6, "c2m", P.n // 2), 2.0 ** 40, level, "c2m")
+    rhat = synth.uniform_residues(6, "rhat", P.qs(level), P.n)
+    d = W.c2m_mask(P, ct, rhat)
+    qs = P.qs(level)
+    share0 = C.intt(P, C.padd(d[:, 0], C.pmul(d[:, 1], sk.ntt_ext[:level], qs), qs), qs)
+    share1 = C.intt(P, C.psub(np.zeros_like(rhat), rhat, qs), qs)
+    dec = C.intt(P, C.padd(ct[:, 0], C.pmul(ct[:, 1], sk.ntt_ext[:level], qs), qs), qs)
+    assert np.array_equal(C.padd(share0, share1, qs), dec)
