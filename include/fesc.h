@@ -326,6 +326,48 @@ int fesc_affine_scan_resident(fesc_ctx* ctx, const uint64_t* const* a, const uin
                               uint32_t level, void* workspace, size_t workspace_bytes,
                               void* stream);
 
+/* ------------------------------------------------------------------------
+ * Small kernels on the same primitives.
+ *
+ * HEConv (Sec. "Causal Depthwise Convolution"): causal depthwise convolution
+ * over token slots, eta = RS(sum_r M_r (.) rho(q; delta_r)) + b.  q: device
+ * ciphertext [level][2][N] (level >= 2); taps (1 .. 16) rotation offsets
+ * deltas (host array; rho(v; d)_j = v_{j+d}, so -r brings token k - r to
+ * slot k; FESC_CONJ not allowed) and masks (host array of device plaintexts
+ * [level][N], tap weights fused with the causal boundary mask, encoded at the
+ * scale of q_{level-1}); bias: device plaintext at the output scale with at
+ * least level limbs, or NULL.  The rotations share one ModUp.  out: device
+ * ciphertext [level-1][2][N], not aliasing q.  FESC_ERR_NO_KEY without a
+ * tap's rotation key. */
+int fesc_heconv(fesc_ctx* ctx, const uint64_t* q, uint32_t taps, const int32_t* deltas,
+                const uint64_t* const* masks, const uint64_t* bias, uint64_t* out,
+                uint32_t level, void* stream);
+
+/* Fused post-SSM path (Appendix "Fused Post-SSM Path"), all inputs at `level`
+ * (>= 3): y = RS(D (.) x_skip) + m (level - 1), out = y (.) g relinearised
+ * and divided by P q_{level-2} in one step (level - 2).  D: device plaintext
+ * [level][N] at the scale of q_{level-1}; g at the scale of q_{level-2}; m,
+ * x_skip, g: device ciphertexts [level][2][N]; out [level-2][2][N].  Needs the
+ * relinearisation key. */
+int fesc_post_ssm(fesc_ctx* ctx, const uint64_t* m, const uint64_t* x_skip,
+                  const uint64_t* d_skip, const uint64_t* g, uint64_t* out, uint32_t level,
+                  void* stream);
+
+/* Plaintext addition out = (c0 + pt, c1) (pt: [level][N], evaluation form);
+ * out may alias ct.  With pt a uniform polynomial r_hat this is the server's
+ * mask <m> + r_hat of the CKKS-to-MPC conversion (Algorithm "Complex
+ * CKKS-to-MPC conversion"); r_hat is drawn by the caller. */
+int fesc_add_plain(fesc_ctx* ctx, const uint64_t* ct, const uint64_t* pt, uint64_t* out,
+                   uint32_t level, void* stream);
+
+/* Host helper, modulus trimming before conversion (Appendix "Adopted Modulus
+ * Trimming"): the smallest l' in 1 .. level whose modulus Q = q[0] ... q[l'-1]
+ * has log2 Q >= ell + sigma + 1 and Q / 2 > delta * bmax (exact integer
+ * comparisons), or 0 if none; the trimmed ciphertext is the first l' limbs of
+ * the buffer.  q: host array of the ciphertext primes. */
+int fesc_c2m_level(const uint64_t* q, uint32_t level, uint32_t ell, uint32_t sigma, double delta,
+                   double bmax, uint32_t* out_level);
+
 /* Host helper: CKKS encoding of n = N/2 complex slots (re, im host arrays;
  * im may be NULL) at scale Delta into int64 coefficients, rounded half away
  * from zero; slot j is the evaluation at exp(i pi 5^j / N).  FESC_ERR_ARG if

@@ -218,7 +218,7 @@ def c2m_level(P: C.Params, level: int, ell: int, sigma: int, delta: float, bmax:
     Q = 1
     for lp in range(1, level + 1):
         Q *= P.q[lp - 1]
-        if Q >= 1 << (ell + sigma + 1) and Q / 2 > delta * bmax:
+        if Q >= 1 << (ell + sigma + 1) and Q > 2 * delta * bmax:  # exact int/float compare
             return lp
     return None
 

@@ -109,6 +109,15 @@ int op_scan_contract(Context* c, const uint64_t* const* h, const uint64_t* const
                      uint64_t* const* out, uint32_t level, hipStream_t s);
 int encode(uint32_t log_n, const double* re, const double* im, double scale, int64_t* out);
 int calib_valu(Context* c, int kind, uint32_t iters, double* rate, hipStream_t s);
+int op_heconv(Context* c, const uint64_t* q, uint32_t taps, const int32_t* deltas,
+              const uint64_t* const* masks, const uint64_t* bias, uint64_t* out, uint32_t level,
+              hipStream_t s);
+int op_post_ssm(Context* c, const uint64_t* m, const uint64_t* x_skip, const uint64_t* d_skip,
+                const uint64_t* g, uint64_t* out, uint32_t level, hipStream_t s);
+int op_add_plain(Context* c, const uint64_t* ct, const uint64_t* pt, uint64_t* out,
+                 uint32_t level, hipStream_t s);
+int c2m_level(const uint64_t* q, uint32_t level, uint32_t ell, uint32_t sigma, double delta,
+              double bmax, uint32_t* out);
 int op_affine_scan(Context* c, uint64_t* const* a, uint64_t* const* s, uint32_t L,
                    uint32_t chunks, uint32_t level, bool states_only, uint32_t* out_level,
                    hipStream_t st);
@@ -377,6 +386,47 @@ int fesc_affine_scan_resident(fesc_ctx* ctx, const uint64_t* const* a, const uin
   uint32_t got;
   return op_affine_scan_resident(ctx, a, s, L, chunks, block, h, level,
                                  static_cast<uint64_t*>(workspace), &got, S(stream));
+}
+
+int fesc_heconv(fesc_ctx* ctx, const uint64_t* q, uint32_t taps, const int32_t* deltas,
+                const uint64_t* const* masks, const uint64_t* bias, uint64_t* out,
+                uint32_t level, void* stream) {
+  int rc = check_level(ctx, level, 2);
+  if (rc) return rc;
+  if (!q || !deltas || !masks || !out || taps == 0 || taps > kMaxConvTaps)
+    return fail(FESC_ERR_ARG, "bad HEConv arguments (1 <= taps <= 16)");
+  if (out == q) return fail(FESC_ERR_ARG, "HEConv output must not alias its input");
+  for (uint32_t r = 0; r < taps; ++r) {
+    if (!masks[r]) return fail(FESC_ERR_ARG, "null mask");
+    if (deltas[r] == FESC_CONJ) return fail(FESC_ERR_ARG, "HEConv offsets are rotations");
+    const uint32_t g = galois_of_step(ctx, deltas[r]);
+    if (g != 1 && !ctx->keys.count(g))
+      return fail(FESC_ERR_NO_KEY, "no key for rotation " + std::to_string(deltas[r]));
+  }
+  return op_heconv(ctx, q, taps, deltas, masks, bias, out, level, S(stream));
+}
+
+int fesc_post_ssm(fesc_ctx* ctx, const uint64_t* m, const uint64_t* x_skip,
+                  const uint64_t* d_skip, const uint64_t* g, uint64_t* out, uint32_t level,
+                  void* stream) {
+  int rc = check_level(ctx, level, 3);
+  if (rc) return rc;
+  if (!m || !x_skip || !d_skip || !g || !out) return fail(FESC_ERR_ARG, "null buffer");
+  if (!ctx->keys.count(0)) return fail(FESC_ERR_NO_KEY, "no relinearisation key");
+  return op_post_ssm(ctx, m, x_skip, d_skip, g, out, level, S(stream));
+}
+
+int fesc_add_plain(fesc_ctx* ctx, const uint64_t* ct, const uint64_t* pt, uint64_t* out,
+                   uint32_t level, void* stream) {
+  int rc = check_level(ctx, level);
+  if (rc) return rc;
+  if (!ct || !pt || !out) return fail(FESC_ERR_ARG, "null buffer");
+  return op_add_plain(ctx, ct, pt, out, level, S(stream));
+}
+
+int fesc_c2m_level(const uint64_t* q, uint32_t level, uint32_t ell, uint32_t sigma, double delta,
+                   double bmax, uint32_t* out_level) {
+  return c2m_level(q, level, ell, sigma, delta, bmax, out_level);
 }
 
 int fesc_calib_valu(fesc_ctx* ctx, int kind, uint32_t iters, double* rate, void* stream) {

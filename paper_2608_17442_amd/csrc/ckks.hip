@@ -53,6 +53,50 @@ __global__ __launch_bounds__(kThreads) void k_mul_plain(const uint64_t* ct,
   }
 }
 
+// out = (c0 + pt, c1); out may alias ct.
+__global__ __launch_bounds__(kThreads) void k_add_plain(const uint64_t* ct,
+                                                        const uint64_t* __restrict__ pt,
+                                                        uint64_t* out, uint32_t n,
+                                                        const PrimeK* __restrict__ pk) {
+  const uint32_t i = blockIdx.y;
+  const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
+  if (k >= n) return;
+  const PrimeK P = pk[i];
+  const size_t o = (size_t)2 * i * n + k;
+  st(out + o, ld(ct + o) + ld(pt + (size_t)i * n + k), P.q, P.qinv);
+  out[o + n] = ct[o + n];
+}
+
+// HEConv accumulation: acc[i][t] = sum_r mask_r[i] rot_r[i][t] (+ for t = 0:
+// (q_{l-1} mod q_i) bias[i], so that the following rescale adds the bias
+// exactly).  Partial sums are reduced every four terms.
+__global__ __launch_bounds__(kThreads) void k_conv_acc(ConvTable tab, const uint64_t* bias,
+                                                       uint64_t* acc, uint32_t n, uint32_t level,
+                                                       const PrimeK* __restrict__ pk) {
+  const uint32_t i = blockIdx.y;
+  const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
+  if (k >= n) return;
+  const PrimeK P = pk[i];
+  const size_t o0 = (size_t)2 * i * n + k, o1 = o0 + n, op = (size_t)i * n + k;
+  double a0 = 0.0, a1 = 0.0;
+  for (uint32_t r = 0; r < tab.taps; ++r) {
+    const double w = ld(tab.mask[r] + op);
+    a0 += mm_var(ld(tab.rot[r] + o0), w, P.q, P.qinv);
+    a1 += mm_var(ld(tab.rot[r] + o1), w, P.q, P.qinv);
+    if ((r & 3) == 3) {
+      a0 = red_bal(a0, P.q, P.qinv);
+      a1 = red_bal(a1, P.q, P.qinv);
+    }
+  }
+  if (bias) {
+    const double ql = pk[level - 1].q;
+    const double qlm = ql >= P.q ? ql - P.q : ql;  // all primes within a factor 2
+    a0 += mm_var(ld(bias + op), qlm, P.q, P.qinv);
+  }
+  st(acc + o0, a0, P.q, P.qinv);
+  st(acc + o1, a1, P.q, P.qinv);
+}
+
 // multiplication by X^m: the evaluation at psi^(2 brv(j) + 1) scales by
 // psi^e, e = (2 brv(j) + 1) m mod 2N; psi^e = tw[brv(e)] for e < N and
 // -tw[brv(e - N)] otherwise (tw = forward twiddle table).
@@ -168,6 +212,20 @@ hipError_t k_mul_plain_launch(const Context* c, const uint64_t* ct, const uint64
                               uint64_t* out, uint32_t level, hipStream_t s) {
   hipLaunchKernelGGL(k_mul_plain, grid_rows(c->n, level), dim3(kThreads), 0, s, ct, pt, out,
                      c->n, c->d_pk);
+  return hipGetLastError();
+}
+
+hipError_t k_add_plain_launch(const Context* c, const uint64_t* ct, const uint64_t* pt,
+                              uint64_t* out, uint32_t level, hipStream_t s) {
+  hipLaunchKernelGGL(k_add_plain, grid_rows(c->n, level), dim3(kThreads), 0, s, ct, pt, out,
+                     c->n, c->d_pk);
+  return hipGetLastError();
+}
+
+hipError_t k_conv_acc_launch(const Context* c, const ConvTable& tab, const uint64_t* bias,
+                             uint64_t* acc, uint32_t level, hipStream_t s) {
+  hipLaunchKernelGGL(k_conv_acc, grid_rows(c->n, level), dim3(kThreads), 0, s, tab, bias, acc,
+                     c->n, level, c->d_pk);
   return hipGetLastError();
 }
 

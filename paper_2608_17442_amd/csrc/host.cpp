@@ -2,6 +2,7 @@
 // parameter set, twiddle tables and scratch memory.
 #include <hip/hip_runtime.h>
 
+#include <cmath>
 #include <cstdio>
 #include <cstring>
 #include <string>
@@ -83,6 +84,80 @@ uint64_t h_min_root(uint64_t q, uint32_t log_n) {
 
 static uint32_t bitrev(uint32_t x, uint32_t bits) {
   return __builtin_bitreverse32(x) >> (32 - bits);
+}
+
+// ------------------------------------------------- modulus trimming (host)
+
+namespace {
+
+using Big = std::vector<uint32_t>;  // little-endian 32-bit limbs, no leading zeros
+
+void big_mul(Big& a, uint64_t m) {
+  unsigned __int128 carry = 0;
+  for (uint32_t& w : a) {
+    const unsigned __int128 cur = (unsigned __int128)w * m + carry;
+    w = (uint32_t)cur;
+    carry = cur >> 32;
+  }
+  while (carry) {
+    a.push_back((uint32_t)carry);
+    carry >>= 32;
+  }
+}
+
+uint32_t big_bits(const Big& a) {
+  return a.empty() ? 0 : 32 * (uint32_t)(a.size() - 1) + (32 - __builtin_clz(a.back()));
+}
+
+// a > floor(d) for a finite d >= 1 (equivalently a > d, a being an integer)
+bool big_gt(const Big& a, double d) {
+  int e;
+  const double m = std::frexp(d, &e);  // d = m 2^e, 0.5 <= m < 1
+  uint64_t mant = (uint64_t)std::ldexp(m, 53);
+  int sh = e - 53;
+  if (sh < 0) {
+    mant >>= -sh;
+    sh = 0;
+  }
+  Big b;
+  for (uint64_t x = mant; x; x >>= 32) b.push_back((uint32_t)x);
+  if (sh) {  // b <<= sh
+    const uint32_t words = sh / 32, bits = sh % 32;
+    Big t(words, 0);
+    uint32_t carry = 0;
+    for (uint32_t w : b) {
+      t.push_back(bits ? (w << bits) | carry : w);
+      carry = bits ? w >> (32 - bits) : 0;
+    }
+    if (carry) t.push_back(carry);
+    b.swap(t);
+  }
+  while (!b.empty() && !b.back()) b.pop_back();
+  if (a.size() != b.size()) return a.size() > b.size();
+  for (size_t i = a.size(); i-- > 0;)
+    if (a[i] != b[i]) return a[i] > b[i];
+  return false;
+}
+
+}  // namespace
+
+int c2m_level(const uint64_t* q, uint32_t level, uint32_t ell, uint32_t sigma, double delta,
+              double bmax, uint32_t* out) {
+  if (!q || !out || level == 0) return fail(FESC_ERR_ARG, "bad modulus-trimming arguments");
+  const double bound = 2.0 * delta * bmax;
+  if (!(bound >= 0.0)) return fail(FESC_ERR_ARG, "delta * bmax must be a non-negative number");
+  Big Q{1};
+  *out = 0;
+  for (uint32_t lp = 1; lp <= level; ++lp) {
+    big_mul(Q, q[lp - 1]);
+    const bool enough_bits = big_bits(Q) >= ell + sigma + 2;  // Q >= 2^(ell + sigma + 1)
+    const bool no_wrap = std::isinf(bound) ? false : bound < 1.0 || big_gt(Q, bound);
+    if (enough_bits && no_wrap) {
+      *out = lp;
+      return FESC_OK;
+    }
+  }
+  return FESC_OK;
 }
 
 // ------------------------------------------------------------------ scratch

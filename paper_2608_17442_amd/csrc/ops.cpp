@@ -619,3 +619,58 @@ int op_scan_contract(Context* c, const uint64_t* const* h, const uint64_t* const
 }
 
 }  // namespace fesc
+
+namespace fesc {
+
+// HEConv (Sec. "Causal Depthwise Convolution"): the taps' rotations share one
+// ModUp (hoisted), one pass accumulates sum_r M_r (.) rho(q; delta_r) with the
+// bias folded in as q_{l-1} b, and a rescale divides by q_{l-1}:
+//     out = RS(sum_r M_r (.) rho(q; delta_r)) + b            (level - 1)
+int op_heconv(Context* c, const uint64_t* q, uint32_t taps, const int32_t* deltas,
+              const uint64_t* const* masks, const uint64_t* bias, uint64_t* out, uint32_t level,
+              hipStream_t s) {
+  Scratch S;
+  int err;
+  if ((err = scratch(c, &S, 2))) return err;  // batched layout: S.cts stays in place
+  if (taps + 1 > S.cap) return fail(FESC_ERR_ARG, "too many taps");
+  const size_t W = (size_t)2 * c->L * c->n;
+  std::vector<uint64_t*> rot(taps);
+  for (uint32_t r = 0; r < taps; ++r) rot[r] = S.cts + (size_t)r * W;
+  uint64_t* acc = S.cts + (size_t)taps * W;
+  if ((err = op_rotate_many(c, q, taps, deltas, rot.data(), level, s))) return err;
+  ConvTable tab{};
+  for (uint32_t r = 0; r < taps; ++r) {
+    tab.rot[r] = rot[r];
+    tab.mask[r] = masks[r];
+  }
+  tab.taps = taps;
+  HIPCK(k_conv_acc_launch(c, tab, bias, acc, level, s));
+  const uint64_t* in = acc;
+  return op_rescale_many(c, 1, &in, &out, level, s);
+}
+
+// Fused post-SSM path (Appendix "Fused Post-SSM Path"):
+//     y = RS(D (.) x_skip) + m          (level - 1; m through its leading limbs)
+//     out = y (.) g / (P q_{level-2})   (level - 2; one merged key switch)
+int op_post_ssm(Context* c, const uint64_t* m, const uint64_t* x_skip, const uint64_t* d_skip,
+                const uint64_t* g, uint64_t* out, uint32_t level, hipStream_t s) {
+  Scratch S;
+  int err;
+  if ((err = scratch(c, &S, 2))) return err;
+  const size_t W = (size_t)2 * c->L * c->n;
+  uint64_t* t = S.cts;
+  uint64_t* y = S.cts + W;
+  HIPCK(k_mul_plain_launch(c, x_skip, d_skip, t, level, s));
+  const uint64_t* tin = t;
+  if ((err = op_rescale_add_many(c, 1, &tin, &y, &m, level, level - 1, s))) return err;
+  const uint64_t* yin = y;
+  return op_prod_rescale_many(c, 1, &yin, &g, &out, nullptr, level - 1, level - 2, s);
+}
+
+int op_add_plain(Context* c, const uint64_t* ct, const uint64_t* pt, uint64_t* out,
+                 uint32_t level, hipStream_t s) {
+  HIPCK(k_add_plain_launch(c, ct, pt, out, level, s));
+  return FESC_OK;
+}
+
+}  // namespace fesc

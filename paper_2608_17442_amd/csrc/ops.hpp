@@ -13,6 +13,17 @@ hipError_t k_binary_launch(const Context* c, const uint64_t* a, const uint64_t* 
                            uint32_t rows, uint32_t shift, int op, hipStream_t s);
 hipError_t k_mul_plain_launch(const Context* c, const uint64_t* ct, const uint64_t* pt,
                               uint64_t* out, uint32_t level, hipStream_t s);
+hipError_t k_add_plain_launch(const Context* c, const uint64_t* ct, const uint64_t* pt,
+                              uint64_t* out, uint32_t level, hipStream_t s);
+// HEConv taps (at most kMaxConvTaps)
+constexpr uint32_t kMaxConvTaps = 16;
+struct ConvTable {
+  const uint64_t* rot[kMaxConvTaps];   // rotated ciphertexts
+  const uint64_t* mask[kMaxConvTaps];  // plaintext masks
+  uint32_t taps;
+};
+hipError_t k_conv_acc_launch(const Context* c, const ConvTable& tab, const uint64_t* bias,
+                             uint64_t* acc, uint32_t level, hipStream_t s);
 hipError_t k_monomial_launch(const Context* c, const uint64_t* in, uint64_t* out,
                              uint32_t level, uint32_t m, hipStream_t s);
 hipError_t k_galois_launch(const Context* c, const uint64_t* in, uint64_t* out, uint32_t rows,

@@ -66,6 +66,12 @@ _SIGS = {
     "fesc_affine_scan_info": [_vp, _u32, _u32, _u32, ctypes.POINTER(_u32), ctypes.POINTER(_u64)],
     "fesc_affine_scan_resident_info": [_vp, _u32, _u32, _u32, _u32, ctypes.POINTER(_u32),
                                        ctypes.POINTER(_sz), ctypes.POINTER(_u64)],
+    "fesc_heconv": [_vp, _vp, _u32, ctypes.POINTER(_i32), ctypes.POINTER(_vp), _vp, _vp, _u32,
+                    _vp],
+    "fesc_post_ssm": [_vp, _vp, _vp, _vp, _vp, _vp, _u32, _vp],
+    "fesc_add_plain": [_vp, _vp, _vp, _vp, _u32, _vp],
+    "fesc_c2m_level": [ctypes.POINTER(_u64), _u32, _u32, _u32, ctypes.c_double, ctypes.c_double,
+                       ctypes.POINTER(_u32)],
     "fesc_affine_scan_resident": [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp), _u32, _u32,
                                   _u32, ctypes.POINTER(_vp), _u32, _vp, _sz, _vp],
 }
@@ -266,6 +272,21 @@ class Context:
                                               arr(h), level, _ptr(workspace) if ws_bytes else None,
                                               ws_bytes, _stream(stream)))
 
+    def heconv(self, q, deltas, masks, bias, out, level, stream=None):
+        """out = RS(sum_r masks[r] (.) rho(q; deltas[r])) + bias (see the C header)."""
+        t = len(deltas)
+        _check(_lib.fesc_heconv(self._h, _ptr(q), t, (_i32 * t)(*deltas),
+                                (_vp * t)(*[_ptr(m) for m in masks]), _ptr(bias), _ptr(out),
+                                level, _stream(stream)))
+
+    def post_ssm(self, m, x_skip, d_skip, g, out, level, stream=None):
+        _check(_lib.fesc_post_ssm(self._h, _ptr(m), _ptr(x_skip), _ptr(d_skip), _ptr(g),
+                                  _ptr(out), level, _stream(stream)))
+
+    def add_plain(self, ct, pt, out, level, stream=None):
+        _check(_lib.fesc_add_plain(self._h, _ptr(ct), _ptr(pt), _ptr(out), level,
+                                   _stream(stream)))
+
     def key_words(self) -> int:
         return self.dnum * (self.L + self.alpha) * 2 * self.n
 
@@ -275,6 +296,15 @@ class Context:
         r = ctypes.c_double()
         _check(_lib.fesc_calib_valu(self._h, kind, iters, ctypes.byref(r), _stream(stream)))
         return float(r.value)
+
+
+def c2m_level(q, level: int, ell: int, sigma: int, delta: float, bmax: float) -> int:
+    """Smallest admissible conversion level (0: none); host-only."""
+    qs = (_u64 * len(q))(*q)
+    out = _u32()
+    _check(_lib.fesc_c2m_level(qs, level, ell, sigma, float(delta), float(bmax),
+                               ctypes.byref(out)))
+    return int(out.value)
 
 
 def encode(log_n: int, z, scale: float):

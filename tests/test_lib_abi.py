@@ -81,3 +81,26 @@ def test_host_encoder_matches_oracle_encoding(log_n, scale_bits, kind):
     assert np.all(np.abs(diff) <= 1)
     assert not np.any(diff[~near_tie]), np.flatnonzero(diff[~near_tie])[:8]
     assert np.count_nonzero(diff) <= np.count_nonzero(near_tie)
+
+
+def test_c2m_level_matches_oracle():
+    """Host modulus trimming (exact big-integer comparisons) against the
+    oracle's, over boundary-adjacent and out-of-range bounds."""
+    from oracle import ckks as C
+    from oracle import workloads as W
+    from paper_2608_17442_amd import fesc as F
+    P = C.params_p16(24)
+    cases = [(64, 40, 2.0 ** 40, 2.0 ** 10), (16, 40, 2.0 ** 40, 2.0 ** 120), (64, 40, 2.0 ** 40, 1.0),
+             (0, 0, 0.0, 0.0), (200, 40, 1.0, 1.0), (1100, 40, 1.0, 1.0), (20, 20, 2.0 ** 40, 2.0 ** 900),
+             (20, 20, 2.0 ** 40, 1e300), (32, 40, 3.5, 7.25)]
+    # bounds placed exactly at the product of the first primes
+    for lp in (1, 2, 3, 5):
+        Q = 1
+        for i in range(lp):
+            Q *= P.q[i]
+        cases += [(8, 8, float(Q) / 2, 0.5), (8, 8, float(Q) / 2, 0.5 * (1 + 2.0 ** -52)),
+                  (Q.bit_length() - 10, 9, 1.0, 1.0), (Q.bit_length() - 10, 8, 1.0, 1.0)]
+    for level in (1, 2, 5, 24):
+        for ell, sig, d, b in cases:
+            want = W.c2m_level(P, level, ell, sig, d, b)
+            assert F.c2m_level(P.q, level, ell, sig, d, b) == (want or 0), (level, ell, sig, d, b)

@@ -214,7 +214,7 @@ def test_c2m_level_is_the_shortest_admissible_modulus():
         want = None
         for lp in range(1, 25):
             Q = int(np.prod([P.q[i] for i in range(lp)], dtype=object))
-            if Q.bit_length() - 1 >= ell + sig + 1 and Q / 2 > 2.0 ** 40 * bm:
+            if Q.bit_length() - 1 >= ell + sig + 1 and Q > 2 * 2.0 ** 40 * bm:
                 want = lp
                 break
         assert W.c2m_level(P, 24, ell, sig, 2.0 ** 40, bm) == want
