@@ -25,7 +25,10 @@ One step runs all four.  `value` is the NTT GB/s (the headline
 configuration); keyswitch/s, matvec ms and scan-contract ms are reported in
 `components`.  After the steps, the HEScan affine prefix scan (Brent-Kung,
 128 tokens x 12 state chunks at 16 limbs, uniform residues: the arithmetic
-is data-oblivious) is timed on its own as `components.affine_scan`.
+is data-oblivious) is timed on its own as `components.affine_scan`, and the
+HEScan scan of one layer at the paper's long-sequence shape (L = 2048, resident
+schedule with blocks of 1024, 12 state chunks in turn, 22 limbs) as
+`components.hescan_layer`.
 Prints ONE JSON line on stdout.  --gpus > 1 is refused (single-GPU build).
 """
 from __future__ import annotations
@@ -305,6 +308,76 @@ class Workloads:
         return lo
 
 
+def time_hescan(W, F, torch, np, L=2048, block=1024, level=22, chunks=12):
+    """HEScan scan of one layer at the paper's long-sequence shape (L tokens,
+    `chunks` state chunks, inputs at `level`), two schedules:
+      full_length: the whole sequence as one Brent-Kung network, in place and
+        states only, two chunks per launch sequence (2 x 94.5 GB of tuples);
+      two_pass: the resident schedule with blocks of `block` tokens (block
+        summaries, carries, replay), one chunk at a time (the paper's choice
+        on a 40 GB device).
+    Tuples are uniform residues (the arithmetic is data-oblivious); every round
+    reuses the same buffers; one warm-up round each."""
+    if hasattr(W, "af_buf"):
+        del W.af_buf, W.af_a, W.af_s
+    torch.cuda.empty_cache()
+    W.keygen(0, W.WL.CFG5["seed"])
+    ctx, n = W.ctx, W.n
+    words = level * 2 * n
+    ev = lambda: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+    out = {"tokens": L, "chunks": chunks, "level_in": level,
+           "paper_context": "HEScan 284.2 s/layer on one A100-40GB at this shape (two-pass, "
+                            "blocks of 1024; includes update construction and contraction; "
+                            "372K key switches; the full-length schedule did not fit in 40 GB)"}
+    # full length, in place, two chunks per round
+    per = 2
+    lo, ks = ctx.affine_scan_info(L, level, states_only=True)
+    log(f"HEScan full-length inputs: {2 * L * per * words * 8 / 1e9:.1f} GB")
+    buf = torch.randint(0, 1 << 49, (2 * L * per, words), dtype=torch.int64, device="cuda")
+    a = [buf[i] for i in range(L * per)]
+    s = [buf[L * per + i] for i in range(L * per)]
+    ctx.affine_scan(a, s, per, level, states_only=True)
+    torch.cuda.synchronize()
+    e0, e1 = ev()
+    e0.record()
+    for _ in range(chunks // per):
+        ctx.affine_scan(a, s, per, level, states_only=True)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    out["full_length"] = {"level_out": lo, "s_per_layer": round(ms / 1e3, 3),
+                          "key_switches": ks * chunks,
+                          "keyswitch_per_s": round(ks * chunks / (ms * 1e-3), 1),
+                          "chunks_per_launch": per}
+    del buf, a, s
+    torch.cuda.empty_cache()
+    # two-pass resident schedule, one chunk at a time
+    lo, ws_bytes, ks = ctx.affine_scan_resident_info(L, 1, block, level)
+    log(f"HEScan two-pass inputs: {2 * L * words * 8 / 1e9:.1f} GB per chunk, "
+        f"workspace {ws_bytes / 1e9:.1f} GB")
+    buf = torch.randint(0, 1 << 49, (2 * L, words), dtype=torch.int64, device="cuda")
+    a = [buf[i] for i in range(L)]
+    s = [buf[L + i] for i in range(L)]
+    hb = torch.empty((L, lo * 2 * n), dtype=torch.int64, device="cuda")
+    h = [hb[i] for i in range(L)]
+    ws = torch.empty(ws_bytes // 8 + 1, dtype=torch.int64, device="cuda")
+    ctx.affine_scan_resident(a, s, 1, block, h, level, ws)
+    torch.cuda.synchronize()
+    e0, e1 = ev()
+    e0.record()
+    for _ in range(chunks):
+        ctx.affine_scan_resident(a, s, 1, block, h, level, ws)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    out["two_pass"] = {"block": block, "level_out": lo, "s_per_layer": round(ms / 1e3, 3),
+                       "key_switches": ks * chunks,
+                       "keyswitch_per_s": round(ks * chunks / (ms * 1e-3), 1)}
+    del buf, a, s, hb, h, ws
+    torch.cuda.empty_cache()
+    return out
+
+
 def keyswitch_per_kernel():
     f = profiled_fields(KS_PROFILE, KS_SOURCES)
     if f is None or "keyswitch_bound_fraction" not in f:
@@ -401,6 +474,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-affine", action="store_true",
                     help="skip the affine prefix scan component (timed after the steps)")
+    ap.add_argument("--no-hescan", action="store_true",
+                    help="skip the HEScan layer component (L=2048, resident schedule)")
     ap.add_argument("--affine-only", action="store_true",
                     help="set up and time only the affine prefix scan component (profiling)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -426,8 +501,10 @@ def main():
         del src, dst
     if args.affine_only:
         W = Workloads(F, torch, np, affine_only=True)
-        print(json.dumps({"components": {"affine_scan": time_affine(W, F, torch, np)}}),
-              flush=True)
+        comp = {"affine_scan": time_affine(W, F, torch, np)}
+        if not args.no_hescan:
+            comp["hescan_layer"] = time_hescan(W, F, torch, np)
+        print(json.dumps({"components": comp}), flush=True)
         return
     W = Workloads(F, torch, np)
     torch.cuda.synchronize()
@@ -473,11 +550,13 @@ def main():
     baby_ms, ptmac_ms, tail_ms = phases[-1]
     # HEScan affine prefix scan, timed after the steps with the projection's
     # diagonal bank released (its 128 x 12 x 2 ciphertexts take 51.5 GB)
-    affine = None
+    affine = hescan = None
     if not args.no_affine:
         del W.mv_plan, W.bank
         torch.cuda.empty_cache()
         affine = time_affine(W, F, torch, np)
+        if not args.no_hescan:
+            hescan = time_hescan(W, F, torch, np)
     n, rows = W.n, W.limbs * W.batch
     bytes_dir = 2 * 8 * n * rows
     ntt_gbs = 2 * bytes_dir / ((fwd + inv) * 1e-3) / 1e9
@@ -537,6 +616,7 @@ def main():
                                  "giant_conj_rescale": round(tail_ms, 3)},
             "scan_contract_ms": round(sc, 3),
             "affine_scan": affine,
+            "hescan_layer": hescan,
         },
         "roofline": {
             "bound": "hbm", "kernel": "k_ptmac (projection plaintext-diagonal MAC)",
