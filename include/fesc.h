@@ -368,6 +368,19 @@ int fesc_add_plain(fesc_ctx* ctx, const uint64_t* ct, const uint64_t* pt, uint64
 int fesc_c2m_level(const uint64_t* q, uint32_t level, uint32_t ell, uint32_t sigma, double delta,
                    double bmax, uint32_t* out_level);
 
+/* Device CKKS encoding (offline plaintext preparation; slot convention and
+ * rounding of fesc_encode): `count` slot vectors z ([count][N/2] complex,
+ * interleaved re/im fp64, device) at scale `scale` into evaluation-form
+ * plaintexts pt ([count][level][N], device): m_k = round half away from zero
+ * of (scale / N) Re(zeta^-k Y_k), Y the length-N DFT of the slots placed at
+ * the odd exponents 5^j (and their conjugates at -5^j), computed by a two-pass
+ * fp64 FFT on the device, then reduced into q_0 .. q_{level-1} and transformed.
+ * The coefficients equal fesc_encode's except within the FFTs' rounding of a
+ * half-integer (+-1 there).  |scale * z| must stay below 2^62 (not checked on
+ * the device).  Uses context scratch; asynchronous on `stream`. */
+int fesc_encode_plain(fesc_ctx* ctx, const double* z, uint32_t count, double scale, uint64_t* pt,
+                      uint32_t level, void* stream);
+
 /* Host helper: CKKS encoding of n = N/2 complex slots (re, im host arrays;
  * im may be NULL) at scale Delta into int64 coefficients, rounded half away
  * from zero; slot j is the evaluation at exp(i pi 5^j / N).  FESC_ERR_ARG if

@@ -1,6 +1,7 @@
 // extern "C" entry points: argument validation, then dispatch to the
 // launchers.  No allocation happens here except through scratch_get().
 #include <algorithm>
+#include <cmath>
 #include <string>
 #include <vector>
 
@@ -118,6 +119,9 @@ int op_add_plain(Context* c, const uint64_t* ct, const uint64_t* pt, uint64_t* o
                  uint32_t level, hipStream_t s);
 int c2m_level(const uint64_t* q, uint32_t level, uint32_t ell, uint32_t sigma, double delta,
               double bmax, uint32_t* out);
+int scratch_slots(Context* c, uint64_t** cts, uint32_t* cap);
+int op_encode_plain(Context* c, const double2* z, uint32_t count, double scale, uint64_t* pt,
+                    uint32_t level, uint64_t* slots, uint32_t nslots, hipStream_t s);
 int op_affine_scan(Context* c, uint64_t* const* a, uint64_t* const* s, uint32_t L,
                    uint32_t chunks, uint32_t level, bool states_only, uint32_t* out_level,
                    hipStream_t st);
@@ -422,6 +426,20 @@ int fesc_add_plain(fesc_ctx* ctx, const uint64_t* ct, const uint64_t* pt, uint64
   if (rc) return rc;
   if (!ct || !pt || !out) return fail(FESC_ERR_ARG, "null buffer");
   return op_add_plain(ctx, ct, pt, out, level, S(stream));
+}
+
+int fesc_encode_plain(fesc_ctx* ctx, const double* z, uint32_t count, double scale, uint64_t* pt,
+                      uint32_t level, void* stream) {
+  int rc = check_level(ctx, level);
+  if (rc) return rc;
+  if (!(std::fabs(scale) < 4611686018427387904.0)) return fail(FESC_ERR_ARG, "bad scale");
+  if (count == 0) return FESC_OK;
+  if (!z || !pt) return fail(FESC_ERR_ARG, "null buffer");
+  uint64_t* slots;
+  uint32_t cap;
+  if ((rc = scratch_slots(ctx, &slots, &cap))) return rc;
+  return op_encode_plain(ctx, reinterpret_cast<const double2*>(z), count, scale, pt, level, slots,
+                         cap, S(stream));
 }
 
 int fesc_c2m_level(const uint64_t* q, uint32_t level, uint32_t ell, uint32_t sigma, double delta,

@@ -134,6 +134,11 @@ struct Context {
   // inner NTT blocks, re-ordered [L+alpha][N/4096][15][256] (see ntt.hip)
   double* d_tw3_fwd = nullptr;
   double* d_tw3_inv = nullptr;
+  // device encoding: T[k] = exp(-i pi k / N) for k < 2N, and the inverse slot
+  // map (position p of the length-N transform input holds z_j if inv[p] = j,
+  // conj(z_j) if inv[p] = ~j)
+  double2* d_enc_tw = nullptr;
+  int32_t* d_enc_inv = nullptr;
   // keys: Galois element (0 = relinearisation) -> device [dnum][L+alpha][2][N]
   std::map<uint32_t, uint64_t*> keys;
   // basis-conversion / rescale constants, built on first use per level

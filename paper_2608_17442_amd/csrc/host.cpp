@@ -220,7 +220,29 @@ static int build_tables(Context* c) {
         }
     }
   }
+  // device encoding tables
+  std::vector<double2> enc_tw(2 * (size_t)n);
+  for (uint32_t k = 0; k < 2 * n; ++k) {
+    const double ang = -M_PI * (double)k / (double)n;
+    enc_tw[k] = double2{std::cos(ang), std::sin(ang)};
+  }
+  std::vector<int32_t> enc_inv(n);
+  {
+    uint64_t e = 1;
+    for (uint32_t j = 0; j < n / 2; ++j) {
+      enc_inv[(e - 1) / 2] = (int32_t)j;
+      enc_inv[n - 1 - (e - 1) / 2] = ~(int32_t)j;
+      e = e * 5 % (2ull * n);
+    }
+  }
   int rc;
+  if ((rc = hip_check(hipMalloc(&c->d_enc_tw, sizeof(double2) * enc_tw.size()), "hipMalloc")) ||
+      (rc = hip_check(hipMalloc(&c->d_enc_inv, sizeof(int32_t) * enc_inv.size()), "hipMalloc")) ||
+      (rc = hip_check(hipMemcpy(c->d_enc_tw, enc_tw.data(), sizeof(double2) * enc_tw.size(),
+                                hipMemcpyHostToDevice), "hipMemcpy")) ||
+      (rc = hip_check(hipMemcpy(c->d_enc_inv, enc_inv.data(), sizeof(int32_t) * enc_inv.size(),
+                                hipMemcpyHostToDevice), "hipMemcpy")))
+    return rc == FESC_ERR_HIP ? fail(FESC_ERR_OOM, "encoding table allocation failed") : rc;
   if ((rc = hip_check(hipMalloc(&c->d_pk, sizeof(PrimeK) * np), "hipMalloc")) ||
       (rc = hip_check(hipMalloc(&c->d_tw_fwd, sizeof(double2) * fwd.size()), "hipMalloc")) ||
       (rc = hip_check(hipMalloc(&c->d_tw_inv, sizeof(double2) * inv.size()), "hipMalloc")) ||
@@ -251,6 +273,8 @@ void destroy(Context* c) {
   hipFree(c->d_tw_inv);
   hipFree(c->d_tw3_fwd);
   hipFree(c->d_tw3_inv);
+  hipFree(c->d_enc_tw);
+  hipFree(c->d_enc_inv);
   hipFree(c->scratch);
   delete static_cast<fesc_ctx*>(c);
 }

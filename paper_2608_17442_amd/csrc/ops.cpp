@@ -674,3 +674,18 @@ int op_add_plain(Context* c, const uint64_t* ct, const uint64_t* pt, uint64_t* o
 }
 
 }  // namespace fesc
+
+namespace fesc {
+
+// The batched scratch ciphertext slots ([cap][L][2][N] words) for callers
+// outside this file (device encoding).
+int scratch_slots(Context* c, uint64_t** cts, uint32_t* cap) {
+  Scratch S;
+  int err;
+  if ((err = scratch(c, &S, 2))) return err;
+  *cts = S.cts;
+  *cap = S.cap;
+  return FESC_OK;
+}
+
+}  // namespace fesc

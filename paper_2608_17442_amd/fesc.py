@@ -70,6 +70,7 @@ _SIGS = {
                     _vp],
     "fesc_post_ssm": [_vp, _vp, _vp, _vp, _vp, _vp, _u32, _vp],
     "fesc_add_plain": [_vp, _vp, _vp, _vp, _u32, _vp],
+    "fesc_encode_plain": [_vp, _vp, _u32, ctypes.c_double, _vp, _u32, _vp],
     "fesc_c2m_level": [ctypes.POINTER(_u64), _u32, _u32, _u32, ctypes.c_double, ctypes.c_double,
                        ctypes.POINTER(_u32)],
     "fesc_affine_scan_resident": [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp), _u32, _u32,
@@ -286,6 +287,15 @@ class Context:
     def add_plain(self, ct, pt, out, level, stream=None):
         _check(_lib.fesc_add_plain(self._h, _ptr(ct), _ptr(pt), _ptr(out), level,
                                    _stream(stream)))
+
+    def encode_plain(self, z, scale, pt, level, stream=None):
+        """Device encoding: z a complex128 CUDA tensor [count][N/2] (or [N/2])
+        -> evaluation-form plaintexts pt (int64 tensor, [count][level][N])."""
+        zr = torch.view_as_real(z.reshape(-1, self.n // 2)).contiguous()
+        assert zr.is_cuda and zr.dtype == torch.float64
+        count = zr.shape[0]
+        _check(_lib.fesc_encode_plain(self._h, zr.data_ptr(), count, float(scale), _ptr(pt),
+                                      level, _stream(stream)))
 
     def key_words(self) -> int:
         return self.dnum * (self.L + self.alpha) * 2 * self.n
