@@ -85,7 +85,8 @@ int fesc_get_psi(const fesc_ctx* ctx, uint32_t idx, uint64_t* psi);
  * order above; inverse: the exact inverse).  Row (b, i), b < batch, i < limbs,
  * starts at d + b*batch_stride + i*limb_stride (strides in uint64 words) and
  * uses extended prime prime0 + i.  Inputs must be canonical residues; outputs
- * are canonical.  Rows must not overlap.  FESC_ERR_ARG on bad indices. */
+ * are canonical.  Rows must not overlap.  FESC_ERR_ARG on bad indices or an
+ * empty batch (batch 0). */
 int fesc_ntt_fwd(fesc_ctx* ctx, uint64_t* d, uint32_t batch, size_t batch_stride,
                  uint32_t limbs, size_t limb_stride, uint32_t prime0, void* stream);
 int fesc_ntt_inv(fesc_ctx* ctx, uint64_t* d, uint32_t batch, size_t batch_stride,

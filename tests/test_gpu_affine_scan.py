@@ -138,3 +138,20 @@ def test_affine_scan_full_size():
     for k in range(L):
         _eq_prefix(ad[k], A[k], f"a-prefix {k}")
         _eq_prefix(sd[k], H[k], f"state {k}")
+
+
+@pytest.mark.parametrize("L,level,states_only", [(2, 2, False), (4, 3, False), (4, 3, True),
+                                                 (3, 4, True)])
+def test_affine_scan_down_to_level_one(small, L, level, states_only):
+    """The last compositions at level 2 (one q prime left with the special
+    primes in the merged division): outputs at level 1."""
+    S = small
+    ao, so, ad, sd = _inputs(S, L, 1, level, f"low{L}-{level}")
+    step(f"affine_scan low L={L} level={level} states_only={states_only}")
+    lo = S.ctx.affine_scan(ad, sd, 1, level, states_only=states_only)
+    assert lo == {(2, 2): 1, (4, 3): 1, (3, 4): 2}[(L, level)]
+    A, H = OS.affine_scan(S.P, ao, so, S.keys[0])
+    for k in range(L):
+        _eq_prefix(sd[k], H[k], f"state {k}")
+        if not states_only:
+            _eq_prefix(ad[k], A[k], f"a-prefix {k}")

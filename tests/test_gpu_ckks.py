@@ -148,7 +148,9 @@ def test_rotations_conjugation_hoisted(log_n, bits, L, alpha):
 def test_mul_relin(log_n, bits, L, alpha):
     P = C.params_small(log_n, bits, L, alpha)
     S = Setup(P, 13, relin=True)
-    for level in [L, 1]:
+    # the top level, full-digit levels (every digit alpha primes), level 2, level 1
+    levels = sorted({L, alpha * (L // alpha), alpha, 2, 1} & set(range(1, L + 1)), reverse=True)
+    for level in levels:
         z1, z2 = _z(20 + level, P.n // 2), _z(30 + level, P.n // 2)
         ao, ad = S.encrypt(z1, 2.0 ** 20, level, 200 + level)
         bo, bd = S.encrypt(z2, 2.0 ** 20, level, 300 + level)
@@ -224,3 +226,19 @@ def test_cfg3_full_size_rotations():
         _eq(out, want, f"cfg3 rotate {r}")
         got = C.decrypt(P, S.sk, want, 2.0 ** 40)
         assert np.max(np.abs(got - np.roll(z, -r))) < 2.0 ** -15
+
+
+def test_empty_batches_are_rejected():
+    """A zero batch is an argument error (nothing launched), for the NTT and
+    for batched rotations."""
+    from paper_2608_17442_amd import fesc as F
+    P = C.params_small(12, 50, 3, 1)
+    ctx = F.Context(P.log_n, P.q, P.p)
+    d = torch.zeros(3 * P.n, dtype=torch.int64, device="cuda")
+    for fn in (ctx.ntt_fwd, ctx.ntt_inv):
+        with pytest.raises(F.FescError) as e:
+            fn(d, 0, 3 * P.n, 3, P.n, 0)
+        assert e.value.code == -1
+    with pytest.raises(F.FescError) as e:
+        ctx.rotate_batch([], [], [], 3)
+    assert e.value.code == -1

@@ -47,9 +47,9 @@ def _heconv(P, seed, T, d_conv, level, with_bias):
     _eq(out, want, "heconv")
 
 
-@pytest.mark.parametrize("with_bias", [True, False])
-def test_heconv_small(with_bias):
-    _heconv(C.params_small(12, 50, 4, 2), 61, 64, 4, 3, with_bias)
+@pytest.mark.parametrize("with_bias,level", [(True, 3), (False, 3), (True, 2)])
+def test_heconv_small(with_bias, level):
+    _heconv(C.params_small(12, 50, 4, 2), 61, 64, 4, level, with_bias)
 
 
 def test_heconv_full_size():
@@ -74,8 +74,9 @@ def _post_ssm(P, seed, level):
     _eq(out, want, "post_ssm")
 
 
-def test_post_ssm_small():
-    _post_ssm(C.params_small(12, 50, 5, 2), 63, 4)
+@pytest.mark.parametrize("level", [4, 3])
+def test_post_ssm_small(level):
+    _post_ssm(C.params_small(12, 50, 5, 2), 63, level)
 
 
 def test_post_ssm_full_size():
