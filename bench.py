@@ -383,6 +383,53 @@ def time_hescan(W, F, torch, np, L=2048, block=1024, level=22, chunks=12):
     return out
 
 
+def scan_block_sweep(W, F, torch, np, L=2048, level=22, blocks=(64, 128, 256, 512, 1024, 2048)):
+    """Resident-schedule block sizes at L tokens, one state chunk, inputs at
+    `level` (the paper's sweep at L = 2048): output level (the depth the
+    schedule needs), key switches, resident bytes and time per chunk.  A block
+    of L is the full-length network (in place, states only)."""
+    W.keygen(0, W.WL.CFG5["seed"])
+    ctx, n = W.ctx, W.n
+    words = level * 2 * n
+    buf = torch.randint(0, 1 << 49, (2 * L, words), dtype=torch.int64, device="cuda")
+    a = [buf[i] for i in range(L)]
+    s = [buf[L + i] for i in range(L)]
+    rows = []
+    for B in blocks:
+        ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+        if B >= L:
+            lo, ks = ctx.affine_scan_info(L, level, states_only=True)
+            ctx.affine_scan(a, s, 1, level, states_only=True)          # warm-up
+            torch.cuda.synchronize()
+            ev[0].record()
+            ctx.affine_scan(a, s, 1, level, states_only=True)
+            ev[1].record()
+            resident = 2 * L * words * 8
+        else:
+            lo, ws_bytes, ks = ctx.affine_scan_resident_info(L, 1, B, level)
+            hb = torch.empty((L, lo * 2 * n), dtype=torch.int64, device="cuda")
+            h = [hb[i] for i in range(L)]
+            ws = torch.empty(ws_bytes // 8 + 1, dtype=torch.int64, device="cuda")
+            ctx.affine_scan_resident(a, s, 1, B, h, level, ws)
+            torch.cuda.synchronize()
+            ev[0].record()
+            ctx.affine_scan_resident(a, s, 1, B, h, level, ws)
+            ev[1].record()
+            resident = 2 * L * words * 8 + ws_bytes + L * lo * 2 * n * 8
+        torch.cuda.synchronize()
+        rows.append({"block": B, "level_out": lo, "depth": level - lo, "key_switches": ks,
+                     "resident_gb": round(resident / 1e9, 1),
+                     "ms_per_chunk": round(ev[0].elapsed_time(ev[1]), 1)})
+        log(f"block {B}: {rows[-1]}")
+        if B < L:
+            del hb, h, ws
+            torch.cuda.empty_cache()
+    del buf, a, s
+    torch.cuda.empty_cache()
+    return {"tokens": L, "level_in": level, "chunk": "one state chunk (N=2^16, 12 per layer)",
+            "rows": rows}
+
+
 def keyswitch_per_kernel():
     f = profiled_fields(KS_PROFILE, KS_SOURCES)
     if f is None or "keyswitch_bound_fraction" not in f:
@@ -481,6 +528,8 @@ def main():
                     help="skip the affine prefix scan component (timed after the steps)")
     ap.add_argument("--no-hescan", action="store_true",
                     help="skip the HEScan layer component (L=2048, resident schedule)")
+    ap.add_argument("--scan-sweep", action="store_true",
+                    help="only the resident-schedule block-size sweep at L=2048 (one chunk)")
     ap.add_argument("--affine-only", action="store_true",
                     help="set up and time only the affine prefix scan component (profiling)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -504,6 +553,10 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if args.scan_sweep:
+        W = Workloads(F, torch, np, affine_only=True)
+        print(json.dumps({"scan_block_sweep": scan_block_sweep(W, F, torch, np)}), flush=True)
+        return
     if args.affine_only:
         W = Workloads(F, torch, np, affine_only=True)
         comp = {"affine_scan": time_affine(W, F, torch, np)}
