@@ -1,7 +1,9 @@
 // Ciphertext-level elementwise kernels (evaluation form): add / sub, plaintext
-// product, tensor product, monomial product, Galois permutation, lifting of
-// signed integer coefficients, and the combine steps of key generation,
-// encryption and rescaling.
+// product and addition, monomial product, Galois permutation (key
+// generation), lifting of signed integer coefficients, the HEConv
+// accumulation, and the combine steps of key generation and encryption.  (The
+// tensor of a relinearised product is formed inside the key switch; the
+// rescale runs in the transforms' passes.)
 //
 // Ciphertext layout [l][2][N]: row r = 2*i + t holds component t of limb i,
 // so the prime of row r is r >> 1.

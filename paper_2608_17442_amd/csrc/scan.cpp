@@ -5,8 +5,9 @@
 //
 // A token map is the ciphertext pair (a, s) for F(z) = a z + s; R after L
 // composes to (a_R a_L, a_R s_L + s_R).  One composition is two products at
-// the lower level l of its operands, each relinearised and rescaled:
-//     a' = RS(relin(a_R a_L)),   s' = RS(relin(a_R s_L)) + s_R   (level l - 1)
+// the lower level l of its operands, each relinearised and divided by
+// P q_{l-1} in one step (ModDown merged with the rescale):
+//     a' = a_R a_L / (P q_{l-1}),   s' = a_R s_L / (P q_{l-1}) + s_R   (level l - 1)
 // where s_R enters through its first l - 1 limbs.  Ciphertexts are
 // [level][2][N] limb-major, so dropping to a lower level is taking a prefix of
 // the buffer: no copies are made for it.
@@ -14,10 +15,10 @@
 // Every stage of the network is one batch: its nodes are independent (no
 // node reads a position another node of the stage writes), so the nodes of a
 // stage, over all chunks, are grouped by level and run as batched products
-// (tensors, one batched key switch sharing the relinearisation key, batched
-// rescales with the addend fused into the final combine).  The two products
-// of a node always fall in the same product group, so the node may write in
-// place over the operands it reads.
+// (op_prod_rescale_many: one key switch per 32 products, sharing the
+// relinearisation key, with the tensor formed inside and s_R added in the
+// final combine).  A node's state product is issued before its decay product,
+// so the node may write in place over the operands it reads.
 #include <algorithm>
 #include <map>
 #include <vector>
