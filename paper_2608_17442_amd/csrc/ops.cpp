@@ -1,7 +1,10 @@
 // Host drivers of the ciphertext operations: per-level constant tables,
 // scratch layout, and the launch sequences of key switching, rotation,
-// relinearisation, rescaling, key generation and encryption.  Every launch is
-// asynchronous on the caller's stream; nothing here synchronises.
+// relinearisation, rescaling (separate, or merged with ModDown), key
+// generation and encryption, and of the compositions built on them (the
+// scan-contract slice, HEConv, the post-SSM path).  Every launch is
+// asynchronous on the caller's stream; only a growth of the context scratch
+// synchronises the device (before the old allocation is freed).
 #include <algorithm>
 #include <functional>
 #include <string>
