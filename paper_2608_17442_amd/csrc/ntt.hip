@@ -447,6 +447,9 @@ __device__ __forceinline__ void fwd_block(const uint64_t* row, uint32_t B, uint3
   ct_st<1, false>(x, TwLo<1>{s3, qinv}, q, qinv);
 }
 
+// An epilogue with nothing to load ahead of the transform.
+struct NoPre {};
+
 // Forward 4096-point blocks.  Thread t starts with values t + 256 r (bits
 // 11..8 in registers), moves to a*256 + 16 r + b (a = t/16, b = t%16; bits
 // 7..4) and to 16 t + r (bits 3..0); fwd_block ends there.  Each transpose
@@ -470,6 +473,9 @@ __global__ __launch_bounds__(kThreads) void k_fwd_inner(RowSel rs, uint32_t log_
   const uint32_t t = threadIdx.x;
   const uint32_t B = blockIdx.x * kBlock;
   const double* s3 = tw3 + ((size_t)prime * (n / kBlock) + blockIdx.x) * (15 * kThreads) + t;
+  // operands of the epilogue loaded before the transform, so that their
+  // latency overlaps the butterflies
+  const typename Epi::Pre pv = epi.pre(B + t, n);
   double x[16];
   fwd_block<SINGLE>(row, B, n, twf + (size_t)prime * n, s3, q, qinv, lds, x);
 #pragma unroll
@@ -477,13 +483,15 @@ __global__ __launch_bounds__(kThreads) void k_fwd_inner(RowSel rs, uint32_t log_
   __syncthreads();
 #pragma unroll
   for (int r = 0; r < 16; ++r) x[r] = lds[lds_row(t, r)];
-  epi(row, B + t, x, q, qinv, n);
+  epi(row, B + t, x, q, qinv, n, pv);
 }
 
 // Epilogue of the forward transform: canonical residues, value r at k0 + 256 r.
 struct StoreResidues {
+  using Pre = NoPre;
+  __device__ __forceinline__ Pre pre(uint32_t, uint32_t) const { return {}; }
   __device__ __forceinline__ void operator()(uint64_t* row, uint32_t k0, const double (&x)[16],
-                                             double q, double qinv, uint32_t) const {
+                                             double q, double qinv, uint32_t, Pre) const {
 #pragma unroll
     for (int r = 0; r < 16; ++r) row[k0 + 256 * r] = to_res(x[r], q, qinv);
   }
@@ -600,12 +608,21 @@ struct KsCombine {
   const double2* pinv;
   const double2* qlinv;
   uint32_t level, alpha, log_n;
+  struct Pre {
+    uint64_t a[16];  // acc[u][i] at k0 + 256 r
+  };
+  __device__ __forceinline__ Pre pre(uint32_t k0, uint32_t n) const {
+    const uint64_t* a = acc + ((size_t)blockIdx.y * (level + alpha) + blockIdx.z) * n + k0;
+    Pre p;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) p.a[r] = a[256 * r];
+    return p;
+  }
   __device__ __forceinline__ void operator()(uint64_t*, uint32_t k0, const double (&x)[16],
-                                             double q, double qinv, uint32_t n) const {
+                                             double q, double qinv, uint32_t n,
+                                             const Pre& pa) const {
     const uint32_t u = blockIdx.y, i = blockIdx.z, job = u >> 1, t = u & 1;
-    const uint32_t E = level + alpha;
     const double2 f = pinv[i];
-    const uint64_t* a = acc + ((size_t)u * E + i) * n;
     const size_t o = ((size_t)2 * i + t) * n;
     const bool use_add = (tab.add_mask[job] >> t) & 1u;
     const uint32_t g = tab.add_galois[job];
@@ -617,7 +634,7 @@ struct KsCombine {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const uint32_t k = k0 + 256 * r;
-        double v = u2d(a[k]) - mm_shoup(x[r], f.x, f.y, q);  // |v| < 2.5 q
+        double v = u2d(pa.a[r]) - mm_shoup(x[r], f.x, f.y, q);  // |v| < 2.5 q
         if (qlinv) v = mm_shoup(v, h.x, h.y, q);
         if (add2) v += u2d(add2[o + k]);
         out[k] = to_res(v, q, qinv);
@@ -627,7 +644,7 @@ struct KsCombine {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const uint32_t k = k0 + 256 * r;
-      double v = mm_shoup(u2d(a[k]) - x[r], f.x, f.y, q);
+      double v = mm_shoup(u2d(pa.a[r]) - x[r], f.x, f.y, q);
       if (use_add) v += u2d(add[g ? galois_src(k, g, log_n) : k]);
       if (add2) v += u2d(add2[o + k]);
       out[k] = to_res(v, q, qinv);
@@ -642,8 +659,10 @@ struct KsCombine {
 struct RsCombine {
   RsTable tab;
   const double2* qlinv;
+  using Pre = NoPre;
+  __device__ __forceinline__ Pre pre(uint32_t, uint32_t) const { return {}; }
   __device__ __forceinline__ void operator()(uint64_t*, uint32_t k0, const double (&x)[16],
-                                             double q, double qinv, uint32_t n) const {
+                                             double q, double qinv, uint32_t n, Pre) const {
     const uint32_t u = blockIdx.y, i = blockIdx.z, b = u >> 1, t = u & 1;
     const double2 f = qlinv[i];
     const size_t o = ((size_t)2 * i + t) * n;
