@@ -250,11 +250,11 @@ int fesc_matvec_phase_ms(const fesc_matvec_plan* plan, float* baby_ms, float* pt
                          float* tail_ms);
 
 /* ------------------------------------------------------------------------
- * Scan-contract slice of one token (paper Eq. "hescan-contract-output" and
- * Appendix "Complex-Packed Reduction Accounting").  For each state chunk k
- * (inputs at `level` >= 3: state h_k, broadcast decay a_k, broadcast output
- * factor C_k, each [level][2][N]):
- *     t_k = RS(relin(RS(relin(a_k * h_k)) * C_k))              (level - 2)
+ * Scan-contract slice of a block of tokens (paper Eq. "hescan-contract-output"
+ * and Appendix "Complex-Packed Reduction Accounting").  For each token u and
+ * state chunk k (inputs at `level` >= 3: state h, broadcast decay a,
+ * broadcast output factor C, each [level][2][N], indexed u*chunks + k):
+ *     t = RS(relin(RS(relin(a * h)) * C))                        (level - 2)
  * Chunks are paired (2l, 2l+1) as chi = t_2l + i t_2l+1 (i = X^(N/2)),
  * reduced over a contiguous d_state axis by rotate-and-add with steps
  * d_state/2, ..., 1 (slot e*d_state then holds the sum over the axis), and
@@ -262,13 +262,17 @@ int fesc_matvec_phase_ms(const fesc_matvec_plan* plan, float* baby_ms, float* pt
  *     out[2l]   = Xi + conj(Xi)        = 2 Sigma(t_2l)
  *     out[2l+1] = -i (Xi - conj(Xi))   = 2 Sigma(t_2l+1)
  * (the factor 2 belongs to the caller's scale bookkeeping).  An odd last
- * chunk is reduced alone.  h, decay, cfac, out: host arrays of `chunks`
- * device pointers; outputs are [level-2][2][N] and must not alias inputs.
- * Needs the relinearisation key, the rotation keys of the reduction steps
- * and (chunks >= 2) the conjugation key; FESC_ERR_NO_KEY otherwise. */
+ * chunk is reduced alone.  The products of all (token, chunk) pairs run in
+ * groups of 32, every rotation step as one batch over all tokens; each
+ * token's result equals that of a one-token call.  h, decay, cfac, out: host
+ * arrays of tokens*chunks device pointers; outputs are [level-2][2][N],
+ * distinct, not aliasing inputs (they also serve as the reduction's
+ * workspace).  At most 32 tokens when chunks is odd.  Needs the
+ * relinearisation key, the rotation keys of the reduction steps and
+ * (chunks >= 2) the conjugation key; FESC_ERR_NO_KEY otherwise. */
 int fesc_scan_contract(fesc_ctx* ctx, const uint64_t* const* h, const uint64_t* const* decay,
-                       const uint64_t* const* cfac, uint32_t chunks, uint32_t d_state,
-                       uint64_t* const* out, uint32_t level, void* stream);
+                       const uint64_t* const* cfac, uint32_t chunks, uint32_t tokens,
+                       uint32_t d_state, uint64_t* const* out, uint32_t level, void* stream);
 
 /* ------------------------------------------------------------------------
  * Encrypted affine prefix scan (Sec. "Parallel Prefix Scans", paragraph

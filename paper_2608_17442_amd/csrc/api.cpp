@@ -106,7 +106,7 @@ int op_plain_from_coeffs(Context* c, const int64_t* m, uint64_t* pt, uint32_t le
                          hipStream_t s);
 uint32_t galois_of_step(const Context* c, int32_t step);
 int op_scan_contract(Context* c, const uint64_t* const* h, const uint64_t* const* decay,
-                     const uint64_t* const* cfac, uint32_t K, uint32_t d_s,
+                     const uint64_t* const* cfac, uint32_t K, uint32_t T, uint32_t d_s,
                      uint64_t* const* out, uint32_t level, hipStream_t s);
 int encode(uint32_t log_n, const double* re, const double* im, double scale, int64_t* out);
 int calib_valu(Context* c, int kind, uint32_t iters, double* rate, hipStream_t s);
@@ -296,22 +296,34 @@ int fesc_encode(uint32_t log_n, const double* re, const double* im, double scale
 }
 
 int fesc_scan_contract(fesc_ctx* ctx, const uint64_t* const* h, const uint64_t* const* decay,
-                       const uint64_t* const* cfac, uint32_t chunks, uint32_t d_state,
-                       uint64_t* const* out, uint32_t level, void* stream) {
+                       const uint64_t* const* cfac, uint32_t chunks, uint32_t tokens,
+                       uint32_t d_state, uint64_t* const* out, uint32_t level, void* stream) {
   int rc = check_level(ctx, level, 3);
   if (rc) return rc;
-  if (!h || !decay || !cfac || !out || chunks == 0 || d_state == 0 ||
-      (d_state & (d_state - 1)) || d_state > ctx->n / 2)
+  if (!h || !decay || !cfac || !out || chunks == 0 || tokens == 0 || d_state == 0 ||
+      (d_state & (d_state - 1)) || d_state > ctx->n / 2 || (uint64_t)chunks * tokens > (1u << 20))
     return fail(FESC_ERR_ARG, "bad scan-contract arguments");
-  for (uint32_t k = 0; k < chunks; ++k)
+  const size_t KT = (size_t)chunks * tokens;
+  std::vector<const void*> outs;
+  for (size_t k = 0; k < KT; ++k) {
     if (!h[k] || !decay[k] || !cfac[k] || !out[k]) return fail(FESC_ERR_ARG, "null buffer");
+    outs.push_back(out[k]);
+  }
+  // the outputs are also the reduction's workspace
+  std::sort(outs.begin(), outs.end());
+  if (std::adjacent_find(outs.begin(), outs.end()) != outs.end())
+    return fail(FESC_ERR_ARG, "scan-contract outputs must be distinct");
+  for (size_t k = 0; k < KT; ++k)
+    for (const void* p : {(const void*)h[k], (const void*)decay[k], (const void*)cfac[k]})
+      if (std::binary_search(outs.begin(), outs.end(), p))
+        return fail(FESC_ERR_ARG, "scan-contract outputs must not alias inputs");
   if (!ctx->keys.count(0)) return fail(FESC_ERR_NO_KEY, "no relinearisation key");
   for (uint32_t st = d_state / 2; st >= 1; st /= 2)
     if (!ctx->keys.count(galois_of_step(ctx, (int32_t)st)))
       return fail(FESC_ERR_NO_KEY, "no key for rotation " + std::to_string(st));
   if (chunks >= 2 && !ctx->keys.count(2 * ctx->n - 1))
     return fail(FESC_ERR_NO_KEY, "no conjugation key");
-  return op_scan_contract(ctx, h, decay, cfac, chunks, d_state, out, level, S(stream));
+  return op_scan_contract(ctx, h, decay, cfac, chunks, tokens, d_state, out, level, S(stream));
 }
 
 static int scan_args(fesc_ctx* ctx, uint32_t L, uint32_t chunks, uint32_t level) {

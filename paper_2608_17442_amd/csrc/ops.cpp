@@ -556,68 +556,99 @@ int op_plain_from_coeffs(Context* c, const int64_t* m, uint64_t* pt, uint32_t le
 // rotate-and-add, and split by one conjugation into 2 Sigma(t2_2l) and
 // 2 Sigma(t2_2l+1).
 int op_scan_contract(Context* c, const uint64_t* const* h, const uint64_t* const* decay,
-                     const uint64_t* const* cfac, uint32_t K, uint32_t d_s,
+                     const uint64_t* const* cfac, uint32_t K, uint32_t T, uint32_t d_s,
                      uint64_t* const* out, uint32_t level, hipStream_t s) {
   int err;
   const uint32_t lo = level - 2;
+  const size_t n = c->n;
   // The batched layout is taken first: the calls below request no more, so
   // the ciphertext region S.cts stays in place while it is in use.
   Scratch S;
   if ((err = scratch(c, &S, 2))) return err;
   if (S.cap < 2) return fail(FESC_ERR_OOM, "scan-contract needs batched scratch");
-  const size_t W = (size_t)2 * c->L * c->n;
-  const uint32_t G = S.cap & ~1u;  // chunks per group (even, so pairs stay together)
-  for (uint32_t k0 = 0; k0 < K; k0 += G) {
-    const uint32_t m = std::min(G, K - k0);
-    // t_k = RS(relin(RS(relin(a_k * h_k)) * C_k)), each step batched over the
-    // group; the level and level-1 intermediates live in S.cts, only the
-    // final rescale writes out_k (level - 2 limbs)
+  const size_t W = (size_t)2 * c->L * n;
+  const uint32_t G = S.cap & ~1u;
+  const uint32_t KT = K * T;
+  if (K % 2 && T > S.cap) return fail(FESC_ERR_ARG, "at most 32 tokens with an odd chunk count");
+  // t = RS(relin(RS(relin(a h)) C)) for every (token, chunk), in groups of G;
+  // the level and level-1 intermediates live in S.cts, the final rescale
+  // writes out (level - 2 limbs)
+  for (uint32_t g0 = 0; g0 < KT; g0 += G) {
+    const uint32_t m = std::min(G, KT - g0);
     std::vector<uint64_t*> t(m);
     for (uint32_t k = 0; k < m; ++k) t[k] = S.cts + (size_t)k * W;
-    if ((err = op_mul_relin_many(c, m, decay + k0, h + k0, t.data(), level, s))) return err;
+    if ((err = op_mul_relin_many(c, m, decay + g0, h + g0, t.data(), level, s))) return err;
     if ((err = op_rescale_many(c, m, t.data(), t.data(), level, s))) return err;
-    if ((err = op_mul_relin_many(c, m, t.data(), cfac + k0, t.data(), level - 1, s))) return err;
-    if ((err = op_rescale_many(c, m, t.data(), out + k0, level - 1, s))) return err;
-    uint64_t* const* o = out + k0;
-    const uint32_t P = m / 2;  // complex pairs (2l, 2l+1); an odd last chunk is reduced alone
-    const uint32_t R = P + (m % 2);
-    // x[r]: value being reduced (chi_l = t_2l + i t_2l+1, or the odd chunk);
-    // y[r]: its partner buffer (rotate-and-add ping-pongs between the two).
-    // 2R <= G buffers; the t_k above are dead once out_k is written.
-    std::vector<uint64_t*> x(R), y(R);
-    for (uint32_t r = 0; r < R; ++r) {
-      x[r] = S.cts + (size_t)(2 * r) * W;
-      y[r] = S.cts + (size_t)(2 * r + 1) * W;
-    }
+    if ((err = op_mul_relin_many(c, m, t.data(), cfac + g0, t.data(), level - 1, s))) return err;
+    if ((err = op_rescale_many(c, m, t.data(), out + g0, level - 1, s))) return err;
+  }
+  const uint32_t P = K / 2;  // complex pairs (2l, 2l+1); an odd last chunk is reduced alone
+  const uint32_t R = P + (K % 2);
+  if (R == 0) return FESC_OK;
+  // Reduction of every token at once.  Pair l of token u is reduced in its own
+  // two output buffers (x: the value, y: the partner; rotate-and-add
+  // ping-pongs between them); an odd chunk's partner is a scratch slot.
+  std::vector<uint64_t*> x, y;
+  for (uint32_t u = 0; u < T; ++u) {
+    uint64_t* const* o = out + (size_t)u * K;
     for (uint32_t l = 0; l < P; ++l) {
-      HIPCK(k_monomial_launch(c, o[2 * l + 1], x[l], lo, c->n / 2, s));
-      HIPCK(k_binary_launch(c, o[2 * l], x[l], x[l], 2 * lo, 1, 0, s));
+      x.push_back(o[2 * l]);
+      y.push_back(o[2 * l + 1]);
     }
-    if (m % 2)
-      HIPCK(hipMemcpyAsync(x[P], o[m - 1], (size_t)2 * lo * c->n * 8, hipMemcpyDeviceToDevice,
-                           s));
-    for (uint32_t st = d_s / 2; st >= 1; st /= 2) {
-      const std::vector<int32_t> steps(R, (int32_t)st);
-      // y = x + rot(x, st)
-      if ((err = op_rotate_batch(c, R, x.data(), steps.data(), y.data(), x.data(), lo, s)))
-        return err;
-      std::swap(x, y);
+    if (K % 2) {
+      x.push_back(o[K - 1]);
+      y.push_back(S.cts + (size_t)u * W);
     }
-    if (P > 0) {
-      const std::vector<int32_t> cj(P, INT32_MIN);
-      if ((err = op_rotate_batch(c, P, x.data(), cj.data(), y.data(), nullptr, lo, s)))
-        return err;
-      for (uint32_t l = 0; l < P; ++l) {
-        // out_2l = chi + conj(chi);  out_2l+1 = -i (chi - conj(chi)) = X^(3N/2) (chi - conj(chi))
-        HIPCK(k_binary_launch(c, x[l], y[l], o[2 * l], 2 * lo, 1, 0, s));
-        HIPCK(k_binary_launch(c, x[l], y[l], y[l], 2 * lo, 1, 1, s));
-        HIPCK(k_monomial_launch(c, y[l], o[2 * l + 1], lo, 3 * c->n / 2, s));
+  }
+  const std::vector<uint64_t*> first = x;  // where out_2l (or the odd output) lives
+  // chi_l = t_2l + i t_2l+1 (i = X^(N/2)), formed in x
+  for (uint32_t r = 0; r < R * T; ++r) {
+    if (K % 2 && r % R == P) continue;
+    HIPCK(k_monomial_launch(c, y[r], y[r], lo, c->n / 2, s));
+    HIPCK(k_binary_launch(c, x[r], y[r], x[r], 2 * lo, 1, 0, s));
+  }
+  for (uint32_t st = d_s / 2; st >= 1; st /= 2) {
+    const std::vector<int32_t> steps(R * T, (int32_t)st);
+    // y = x + rot(x, st)
+    if ((err = op_rotate_batch(c, R * T, x.data(), steps.data(), y.data(), x.data(), lo, s)))
+      return err;
+    std::swap(x, y);
+  }
+  if (P > 0) {
+    std::vector<uint64_t*> xp, yp;
+    for (uint32_t r = 0; r < R * T; ++r)
+      if (!(K % 2 && r % R == P)) {
+        xp.push_back(x[r]);
+        yp.push_back(y[r]);
+      }
+    const std::vector<int32_t> cj(xp.size(), INT32_MIN);
+    if ((err = op_rotate_batch(c, (uint32_t)xp.size(), xp.data(), cj.data(), yp.data(), nullptr,
+                               lo, s)))
+      return err;
+    // out_2l = chi + conj(chi);  out_2l+1 = -i (chi - conj(chi)) = X^(3N/2) (chi - conj(chi)),
+    // in place in the pair's two buffers (A = chi, B = conj(chi))
+    for (uint32_t r = 0; r < R * T; ++r) {
+      if (K % 2 && r % R == P) continue;
+      uint64_t *A = x[r], *B = y[r];
+      if (A == first[r]) {                                    // A -> out_2l, B -> out_2l+1
+        HIPCK(k_binary_launch(c, A, B, B, 2 * lo, 1, 1, s));  // B = chi - cj
+        HIPCK(k_binary_launch(c, A, A, A, 2 * lo, 1, 0, s));  // A = 2 chi
+        HIPCK(k_binary_launch(c, A, B, A, 2 * lo, 1, 1, s));  // A = chi + cj
+        HIPCK(k_monomial_launch(c, B, B, lo, 3 * c->n / 2, s));
+      } else {                                                // B -> out_2l, A -> out_2l+1
+        HIPCK(k_binary_launch(c, A, B, A, 2 * lo, 1, 1, s));  // A = chi - cj
+        HIPCK(k_binary_launch(c, B, B, B, 2 * lo, 1, 0, s));  // B = 2 cj
+        HIPCK(k_binary_launch(c, B, A, B, 2 * lo, 1, 0, s));  // B = chi + cj
+        HIPCK(k_monomial_launch(c, A, A, lo, 3 * c->n / 2, s));
       }
     }
-    if (m % 2)
-      HIPCK(hipMemcpyAsync(o[m - 1], x[P], (size_t)2 * lo * c->n * 8, hipMemcpyDeviceToDevice,
-                           s));
   }
+  if (K % 2)
+    for (uint32_t u = 0; u < T; ++u) {
+      const uint32_t r = u * R + P;
+      if (x[r] != first[r])
+        HIPCK(hipMemcpyAsync(first[r], x[r], (size_t)2 * lo * n * 8, hipMemcpyDeviceToDevice, s));
+    }
   return FESC_OK;
 }
 

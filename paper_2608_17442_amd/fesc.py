@@ -59,7 +59,7 @@ _SIGS = {
     "fesc_plain_from_coeffs": [_vp, _vp, _vp, _u32, _vp],
     "fesc_encode": [_u32, _vp, _vp, ctypes.c_double, _vp],
     "fesc_scan_contract": [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp), ctypes.POINTER(_vp),
-                           _u32, _u32, ctypes.POINTER(_vp), _u32, _vp],
+                           _u32, _u32, _u32, ctypes.POINTER(_vp), _u32, _vp],
     "fesc_calib_valu": [_vp, ctypes.c_int, _u32, ctypes.POINTER(ctypes.c_double), _vp],
     "fesc_affine_scan": [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp), _u32, _u32, _u32, _u32,
                          ctypes.POINTER(_u32), _vp],
@@ -231,11 +231,12 @@ class Context:
     def plain_from_coeffs(self, m, pt, level, stream=None):
         _check(_lib.fesc_plain_from_coeffs(self._h, _ptr(m), _ptr(pt), level, _stream(stream)))
 
-    def scan_contract(self, h, decay, cfac, d_state, outs, level, stream=None):
-        K = len(h)
-        arr = lambda ts: (_vp * K)(*[_ptr(t) for t in ts])
-        _check(_lib.fesc_scan_contract(self._h, arr(h), arr(decay), arr(cfac), K, d_state,
-                                       arr(outs), level, _stream(stream)))
+    def scan_contract(self, h, decay, cfac, d_state, outs, level, tokens=1, stream=None):
+        """Lists of tokens * chunks ciphertexts, token-major."""
+        m = len(h)
+        arr = lambda ts: (_vp * m)(*[_ptr(t) for t in ts])
+        _check(_lib.fesc_scan_contract(self._h, arr(h), arr(decay), arr(cfac), m // tokens, tokens,
+                                       d_state, arr(outs), level, _stream(stream)))
 
     def affine_scan(self, a, s, chunks, level, states_only=False, stream=None) -> int:
         """In-place Brent-Kung scan of `chunks` sequences of len(a) // chunks

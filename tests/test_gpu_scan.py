@@ -103,3 +103,38 @@ def test_cfg5_one_token_full_size():
         err = np.max(np.abs(dec - want[k * c_state:(k + 1) * c_state]))
         print(f"cfg5 chunk {k}: max |decoded - fp64| = {err:.3e}")
         assert err <= 2.0 ** -15
+
+
+@pytest.mark.parametrize("K,T", [(4, 3), (5, 2), (2, 17)])
+def test_scan_contract_token_block(K, T):
+    """Several tokens per call (the reduction batched over all of them, the
+    outputs used as its workspace): every token equals the oracle's
+    one-token slice.  K = 2, T = 17 puts 17 pairs in each rotation batch."""
+    P = C.params_small(12, 50, 5, 2)
+    d_s, head_dim, level = 8, 16, 4
+    n_slots = P.n // 2
+    S = Setup(P, 37, rot_steps=[1, 2, 4], relin=True, conj=True)
+    E = K * (n_slots // d_s)
+    hs_o, ds_o, cs_o, hs_d, ds_d, cs_d = [], [], [], [], [], []
+    for u in range(T):
+        z = synth.normal(37 + u, "z", -(-E // head_dim))
+        cvec = synth.normal(37 + u, "C", d_s)
+        H = synth.normal(37 + u, "h", (E, d_s))
+        for k, (hv, dv, cv) in enumerate(chunk_slots(z, cvec, H, K, n_slots, d_s, head_dim)):
+            i = 3 * (u * K + k)
+            for vals, scale, lo, ld, j in [(hv, 2.0 ** 40, hs_o, hs_d, 0),
+                                           (dv, float(P.q[level - 1]), ds_o, ds_d, 1),
+                                           (cv, float(P.q[level - 2]), cs_o, cs_d, 2)]:
+                co, cd = S.encrypt(vals.astype(complex), scale, level, 5000 + i + j)
+                lo.append(co)
+                ld.append(cd)
+    outs_d = [torch.zeros((level - 2) * 2 * P.n, dtype=torch.int64, device="cuda")
+              for _ in range(K * T)]
+    step(f"scan_contract token block K={K} T={T}")
+    S.ctx.scan_contract(hs_d, ds_d, cs_d, d_s, outs_d, level, tokens=T)
+    for u in range(T):
+        sl = slice(u * K, (u + 1) * K)
+        want = OW.scan_contract_token(P, hs_o[sl], ds_o[sl], cs_o[sl], S.keys[0], S.keys, d_s)
+        for k, (od, oo) in enumerate(zip(outs_d[sl], want)):
+            got = to_host(od).reshape(oo.shape)
+            assert np.array_equal(got, oo), f"token {u} output {k}: {first_mismatch(got, oo)}"
