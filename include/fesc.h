@@ -130,6 +130,24 @@ int fesc_mul_monomial(fesc_ctx* ctx, const uint64_t* in, uint64_t* out, uint32_t
 int fesc_mul_relin(fesc_ctx* ctx, const uint64_t* a, const uint64_t* b, uint64_t* out,
                    uint32_t level, void* stream);
 
+/* Batched relinearised product with the rescale merged into the key switch
+ * (the ciphertext products of HEScan: update construction
+ * s = br(x) * br(B), affine composition and contraction, Sec. "On-Demand
+ * Construction and Contraction"): for i < count,
+ *     out_i = (P d_i + KS(d2_i) - FastBConv_{M->Q}(...)) * M^-1,  M = P q_{l-1}
+ * i.e. relin(a_i * b_i) divided by P q_{l-1} in one ModDown whose conversion
+ * takes q_{l-1} together with the special primes; the result is at level
+ * l - 1 ([l-1][2][N]) and differs from rescale(mul_relin(a_i, b_i)) only in
+ * the rounding (at most (alpha + 1) / 2 units of one conversion).  a, b, out:
+ * host arrays of `count` device pointers; a_i and b_i at `level` >= 2 (a
+ * longer operand enters through its leading limbs).  out_i may be a_i or
+ * b_i; otherwise outputs are distinct and alias no operand (FESC_ERR_ARG).
+ * 32 products share one key-switch launch sequence.  count = 0 is a no-op.
+ * FESC_ERR_NO_KEY without the relinearisation key. */
+int fesc_mul_relin_rescale(fesc_ctx* ctx, uint32_t count, const uint64_t* const* a,
+                           const uint64_t* const* b, uint64_t* const* out, uint32_t level,
+                           void* stream);
+
 /* Rescale: out = round(in / q_{l-1}) at level l-1 (written as [l-1][2][N]);
  * l >= 2.  Computed as (c_i - [c mod q_{l-1}]_centred) * q_{l-1}^-1 mod q_i. */
 int fesc_rescale(fesc_ctx* ctx, const uint64_t* in, uint64_t* out, uint32_t level,
@@ -252,9 +270,14 @@ int fesc_matvec_phase_ms(const fesc_matvec_plan* plan, float* baby_ms, float* pt
 /* ------------------------------------------------------------------------
  * Scan-contract slice of a block of tokens (paper Eq. "hescan-contract-output"
  * and Appendix "Complex-Packed Reduction Accounting").  For each token u and
- * state chunk k (inputs at `level` >= 3: state h, broadcast decay a,
- * broadcast output factor C, each [level][2][N], indexed u*chunks + k):
- *     t = RS(relin(RS(relin(a * h)) * C))                        (level - 2)
+ * state chunk k (inputs at `level`: state h, broadcast decay a, broadcast
+ * output factor C, each [level][2][N], indexed u*chunks + k):
+ *     t = RS(relin(RS(relin(a * h)) * C))     (level >= 3; out at level - 2)
+ * or, with decay = NULL (the contraction of states the scan already formed,
+ * Eq. "hescan-contract-output"),
+ *     t = RS(relin(h * C))                    (level >= 2; out at level - 1)
+ * each RS(relin(.)) one merged division by P q_{l-1} as in
+ * fesc_mul_relin_rescale.
  * Chunks are paired (2l, 2l+1) as chi = t_2l + i t_2l+1 (i = X^(N/2)),
  * reduced over a contiguous d_state axis by rotate-and-add with steps
  * d_state/2, ..., 1 (slot e*d_state then holds the sum over the axis), and
@@ -265,7 +288,8 @@ int fesc_matvec_phase_ms(const fesc_matvec_plan* plan, float* baby_ms, float* pt
  * chunk is reduced alone.  The products of all (token, chunk) pairs run in
  * groups of 32, every rotation step as one batch over all tokens; each
  * token's result equals that of a one-token call.  h, decay, cfac, out: host
- * arrays of tokens*chunks device pointers; outputs are [level-2][2][N],
+ * arrays of tokens*chunks device pointers; outputs are [lo][2][N] (lo the
+ * output level above),
  * distinct, not aliasing inputs (they also serve as the reduction's
  * workspace).  At most 32 tokens when chunks is odd.  Needs the
  * relinearisation key, the rotation keys of the reduction steps and

@@ -154,3 +154,29 @@ def resident_scan(P: C.Params, a: list, s: list, block: int, rlk) -> list:
                                lambda pre: pre[1],
                                lambda pre, g: apply_to_state(P, pre, g[1], rlk))
     return _to_one_level(states)
+
+
+def hescan(P: C.Params, x: list, B: list, a: list, cfac: list, rlk, keys: dict, d_s: int,
+           block: int | None = None) -> list:
+    """HEScan of one sequence over K state chunks (Sec. "On-Demand
+    Construction and Contraction", Eqs. "fesc_recurrence", "fesc_contract" and
+    "hescan-contract-output").  x, B, a, cfac: [K][L] ciphertexts, broadcast
+    into each chunk's packing; x and B at one level l, a at >= l - 1 limbs,
+    cfac at >= the states' level.  Per chunk: the update s_k = RS(relin(x_k B_k))
+    (level l - 1), the states h_k by the Brent-Kung scan (block None) or the
+    resident schedule, at one common level; then per token the contraction
+    (the scan-contract slice without the decay product).  Returns per token
+    the slice's outputs."""
+    from . import workloads as W
+    K, L = len(x), len(x[0])
+    H = []
+    for k in range(K):
+        s = [C.mul_relin_rescale(P, x[k][t], B[k][t], rlk) for t in range(L)]
+        lvl = s[0].shape[0]
+        ak = [_drop(a[k][t], lvl) for t in range(L)]
+        H.append(affine_scan(P, ak, s, rlk)[1] if block is None
+                 else resident_scan(P, ak, s, block, rlk))
+    return [W.scan_contract_token(P, [H[k][t] for k in range(K)], None,
+                                  [cfac[k][t] for k in range(K)], rlk, keys, d_s)
+            for t in range(L)]
+

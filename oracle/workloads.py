@@ -157,16 +157,20 @@ def reduce_axis(P: C.Params, ct: np.ndarray, d: int, keys: dict) -> np.ndarray:
     return ct
 
 
-def scan_contract_token(P: C.Params, h: list, decay: list, cfac: list, rlk, keys: dict,
+def scan_contract_token(P: C.Params, h: list, decay, cfac: list, rlk, keys: dict,
                         d_s: int) -> list:
     """One token of the scan-contract slice.  h, decay, cfac: per-chunk
-    ciphertexts at the same level.  Returns [Re_0, Im_0, Re_1, Im_1, ...]."""
+    ciphertexts at the same level (decay None: the contraction alone,
+    t = h * C).  Every relinearised product is rescaled in the same division
+    (ckks.mul_relin_rescale, the reading the scan takes).  Returns
+    [Re_0, Im_0, Re_1, Im_1, ...] (each twice the reduced sum of its chunk;
+    an odd last chunk reduced alone)."""
     K = len(h)
     t2 = []
     for k in range(K):
-        t1 = C.rescale(P, C.mul_relin(P, decay[k], h[k], rlk))
+        t1 = h[k] if decay is None else C.mul_relin_rescale(P, decay[k], h[k], rlk)
         c = cfac[k][: t1.shape[0]]
-        t2.append(C.rescale(P, C.mul_relin(P, t1, c, rlk)))
+        t2.append(C.mul_relin_rescale(P, t1, c, rlk))
     outs = []
     for l in range(K // 2):
         chi = C.ct_add(P, t2[2 * l], C.mul_monomial(P, t2[2 * l + 1], P.n // 2))

@@ -193,6 +193,33 @@ int fesc_mul_relin(fesc_ctx* ctx, const uint64_t* a, const uint64_t* b, uint64_t
   return op_mul_relin(ctx, a, b, out, level, S(stream));
 }
 
+int fesc_mul_relin_rescale(fesc_ctx* ctx, uint32_t count, const uint64_t* const* a,
+                           const uint64_t* const* b, uint64_t* const* out, uint32_t level,
+                           void* stream) {
+  int rc = check_level(ctx, level, 2);
+  if (rc) return rc;
+  if (count == 0) return FESC_OK;
+  if (!a || !b || !out || count > (1u << 20)) return fail(FESC_ERR_ARG, "bad product arguments");
+  // out_i may be a_i or b_i; no output may be another product's operand or output
+  std::vector<std::pair<const void*, uint32_t>> outs;
+  for (uint32_t i = 0; i < count; ++i) {
+    if (!a[i] || !b[i] || !out[i]) return fail(FESC_ERR_ARG, "null buffer");
+    outs.emplace_back(out[i], i);
+  }
+  std::sort(outs.begin(), outs.end());
+  for (uint32_t i = 1; i < count; ++i)
+    if (outs[i].first == outs[i - 1].first)
+      return fail(FESC_ERR_ARG, "product outputs must be distinct");
+  for (uint32_t i = 0; i < count; ++i)
+    for (const void* p : {(const void*)a[i], (const void*)b[i]}) {
+      auto it = std::lower_bound(outs.begin(), outs.end(), std::make_pair(p, 0u));
+      if (it != outs.end() && it->first == p && it->second != i)
+        return fail(FESC_ERR_ARG, "an output aliases another product's operand");
+    }
+  if (!ctx->keys.count(0)) return fail(FESC_ERR_NO_KEY, "no relinearisation key");
+  return op_prod_rescale_many(ctx, count, a, b, out, nullptr, level, level - 1, S(stream));
+}
+
 int fesc_rescale(fesc_ctx* ctx, const uint64_t* in, uint64_t* out, uint32_t level,
                  void* stream) {
   int rc = check_level(ctx, level, 2);
@@ -298,15 +325,16 @@ int fesc_encode(uint32_t log_n, const double* re, const double* im, double scale
 int fesc_scan_contract(fesc_ctx* ctx, const uint64_t* const* h, const uint64_t* const* decay,
                        const uint64_t* const* cfac, uint32_t chunks, uint32_t tokens,
                        uint32_t d_state, uint64_t* const* out, uint32_t level, void* stream) {
-  int rc = check_level(ctx, level, 3);
+  int rc = check_level(ctx, level, decay ? 3 : 2);
   if (rc) return rc;
-  if (!h || !decay || !cfac || !out || chunks == 0 || tokens == 0 || d_state == 0 ||
+  if (!h || !cfac || !out || chunks == 0 || tokens == 0 || d_state == 0 ||
       (d_state & (d_state - 1)) || d_state > ctx->n / 2 || (uint64_t)chunks * tokens > (1u << 20))
     return fail(FESC_ERR_ARG, "bad scan-contract arguments");
   const size_t KT = (size_t)chunks * tokens;
   std::vector<const void*> outs;
   for (size_t k = 0; k < KT; ++k) {
-    if (!h[k] || !decay[k] || !cfac[k] || !out[k]) return fail(FESC_ERR_ARG, "null buffer");
+    if (!h[k] || (decay && !decay[k]) || !cfac[k] || !out[k])
+      return fail(FESC_ERR_ARG, "null buffer");
     outs.push_back(out[k]);
   }
   // the outputs are also the reduction's workspace
@@ -314,8 +342,9 @@ int fesc_scan_contract(fesc_ctx* ctx, const uint64_t* const* h, const uint64_t* 
   if (std::adjacent_find(outs.begin(), outs.end()) != outs.end())
     return fail(FESC_ERR_ARG, "scan-contract outputs must be distinct");
   for (size_t k = 0; k < KT; ++k)
-    for (const void* p : {(const void*)h[k], (const void*)decay[k], (const void*)cfac[k]})
-      if (std::binary_search(outs.begin(), outs.end(), p))
+    for (const void* p : {(const void*)h[k], decay ? (const void*)decay[k] : nullptr,
+                          (const void*)cfac[k]})
+      if (p && std::binary_search(outs.begin(), outs.end(), p))
         return fail(FESC_ERR_ARG, "scan-contract outputs must not alias inputs");
   if (!ctx->keys.count(0)) return fail(FESC_ERR_NO_KEY, "no relinearisation key");
   for (uint32_t st = d_state / 2; st >= 1; st /= 2)

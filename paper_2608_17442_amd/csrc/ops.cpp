@@ -550,16 +550,18 @@ int op_plain_from_coeffs(Context* c, const int64_t* m, uint64_t* pt, uint32_t le
   return FESC_OK;
 }
 
-// Scan-contract slice of one token (see fesc.h): per chunk k,
-//   t2_k = RS(relin(RS(relin(decay_k * h_k)) * c_k)),
-// chunk pairs packed as chi = t2_2l + i t2_2l+1, reduced over the d_s axis by
-// rotate-and-add, and split by one conjugation into 2 Sigma(t2_2l) and
-// 2 Sigma(t2_2l+1).
+// Scan-contract slice (see fesc.h): per (token, chunk),
+//   t = RS(relin(RS(relin(decay * h)) * c))     (decay given; level - 2)
+//   t = RS(relin(h * c))                        (contraction only; level - 1)
+// each relinearised product divided by P q_{l-1} in one merged key switch;
+// chunk pairs packed as chi = t_2l + i t_2l+1, reduced over the d_s axis by
+// rotate-and-add, and split by one conjugation into 2 Sigma(t_2l) and
+// 2 Sigma(t_2l+1).
 int op_scan_contract(Context* c, const uint64_t* const* h, const uint64_t* const* decay,
                      const uint64_t* const* cfac, uint32_t K, uint32_t T, uint32_t d_s,
                      uint64_t* const* out, uint32_t level, hipStream_t s) {
   int err;
-  const uint32_t lo = level - 2;
+  const uint32_t lo = decay ? level - 2 : level - 1;
   const size_t n = c->n;
   // The batched layout is taken first: the calls below request no more, so
   // the ciphertext region S.cts stays in place while it is in use.
@@ -570,17 +572,25 @@ int op_scan_contract(Context* c, const uint64_t* const* h, const uint64_t* const
   const uint32_t G = S.cap & ~1u;
   const uint32_t KT = K * T;
   if (K % 2 && T > S.cap) return fail(FESC_ERR_ARG, "at most 32 tokens with an odd chunk count");
-  // t = RS(relin(RS(relin(a h)) C)) for every (token, chunk), in groups of G;
-  // the level and level-1 intermediates live in S.cts, the final rescale
-  // writes out (level - 2 limbs)
+  // the products of every (token, chunk) in groups of G; the decay product's
+  // level - 1 intermediates live in S.cts, the last product writes out
   for (uint32_t g0 = 0; g0 < KT; g0 += G) {
     const uint32_t m = std::min(G, KT - g0);
+    if (!decay) {
+      if ((err = op_prod_rescale_many(c, m, h + g0, cfac + g0, out + g0, nullptr, level,
+                                      level - 1, s)))
+        return err;
+      continue;
+    }
     std::vector<uint64_t*> t(m);
     for (uint32_t k = 0; k < m; ++k) t[k] = S.cts + (size_t)k * W;
-    if ((err = op_mul_relin_many(c, m, decay + g0, h + g0, t.data(), level, s))) return err;
-    if ((err = op_rescale_many(c, m, t.data(), t.data(), level, s))) return err;
-    if ((err = op_mul_relin_many(c, m, t.data(), cfac + g0, t.data(), level - 1, s))) return err;
-    if ((err = op_rescale_many(c, m, t.data(), out + g0, level - 1, s))) return err;
+    if ((err = op_prod_rescale_many(c, m, decay + g0, h + g0, t.data(), nullptr, level,
+                                    level - 1, s)))
+      return err;
+    const std::vector<const uint64_t*> tc(t.begin(), t.end());
+    if ((err = op_prod_rescale_many(c, m, tc.data(), cfac + g0, out + g0, nullptr, level - 1,
+                                    level - 2, s)))
+      return err;
   }
   const uint32_t P = K / 2;  // complex pairs (2l, 2l+1); an odd last chunk is reduced alone
   const uint32_t R = P + (K % 2);

@@ -46,6 +46,8 @@ _SIGS = {
     "fesc_mul_monomial": [_vp, _vp, _vp, _u32, _u32, _vp],
     "fesc_mul_relin": [_vp, _vp, _vp, _vp, _u32, _vp],
     "fesc_rescale": [_vp, _vp, _vp, _u32, _vp],
+    "fesc_mul_relin_rescale": [_vp, _u32, ctypes.POINTER(_vp), ctypes.POINTER(_vp),
+                               ctypes.POINTER(_vp), _u32, _vp],
     "fesc_galois_element": [_vp, _i32, ctypes.POINTER(_u32)],
     "fesc_rotate": [_vp, _vp, _vp, _u32, _i32, _vp],
     "fesc_rotate_hoisted": [_vp, _vp, _u32, ctypes.POINTER(_i32), ctypes.POINTER(_vp), _u32,
@@ -191,6 +193,13 @@ class Context:
         _check(_lib.fesc_mul_relin(self._h, _ptr(a), _ptr(b), _ptr(out), level,
                                    _stream(stream)))
 
+    def mul_relin_rescale(self, a, b, outs, level, stream=None):
+        """out_i = relin(a_i * b_i) / (P q_{level-1}), batched (level - 1)."""
+        m = len(a)
+        arr = lambda ts: (_vp * m)(*[_ptr(t) for t in ts])
+        _check(_lib.fesc_mul_relin_rescale(self._h, m, arr(a), arr(b), arr(outs), level,
+                                           _stream(stream)))
+
     def rescale(self, ct, out, level, stream=None):
         _check(_lib.fesc_rescale(self._h, _ptr(ct), _ptr(out), level, _stream(stream)))
 
@@ -232,10 +241,12 @@ class Context:
         _check(_lib.fesc_plain_from_coeffs(self._h, _ptr(m), _ptr(pt), level, _stream(stream)))
 
     def scan_contract(self, h, decay, cfac, d_state, outs, level, tokens=1, stream=None):
-        """Lists of tokens * chunks ciphertexts, token-major."""
+        """Lists of tokens * chunks ciphertexts, token-major; decay None for
+        the contraction alone."""
         m = len(h)
         arr = lambda ts: (_vp * m)(*[_ptr(t) for t in ts])
-        _check(_lib.fesc_scan_contract(self._h, arr(h), arr(decay), arr(cfac), m // tokens, tokens,
+        dec = None if decay is None else arr(decay)
+        _check(_lib.fesc_scan_contract(self._h, arr(h), dec, arr(cfac), m // tokens, tokens,
                                        d_state, arr(outs), level, _stream(stream)))
 
     def affine_scan(self, a, s, chunks, level, states_only=False, stream=None) -> int:

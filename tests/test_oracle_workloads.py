@@ -136,6 +136,106 @@ def test_scan_contract_slice_small():
             np.testing.assert_allclose(got, want[k * c_state:(k + 1) * c_state], atol=2.0 ** -15)
 
 
+def test_scan_contract_contraction_only_odd_chunks():
+    """decay None: t = h * C alone (one level), three chunks: one complex
+    pair (outputs 2 Sigma) and an odd chunk reduced alone (Sigma)."""
+    P = C.params_small(10, 50, 4, 2)
+    sk = C.secret_key(P, synth.secret(5, P.n))
+    n_slots, d_s, K, level = P.n // 2, 8, 3, 3
+    c_state = n_slots // d_s
+    Cv = synth.normal(5, "C", d_s)
+    H = synth.normal(5, "h", (K * c_state, d_s))
+    want = (H * Cv[None, :]).sum(axis=1)
+    rlk = C.keygen_from_seed(P, sk, 5, 0)
+    keys = _keys(P, sk, 5, [1, 2, 4], conj=True)
+    j = np.arange(n_slots)
+    hs, cs = [], []
+    for k in range(K):
+        enc = lambda vals, scale, tag: C.encrypt(
+            P, sk, C.encode_plain(P, vals.astype(complex), scale, level), level,
+            *synth.encrypt_draws(5, P.qs(level), P.n, tag, k))
+        hs.append(enc(H[k * c_state + j // d_s, j % d_s], 2.0 ** 40, "h"))
+        cs.append(enc(Cv[j % d_s], float(P.q[level - 1]), "C"))
+    outs = W.scan_contract_token(P, hs, None, cs, rlk, keys, d_s)
+    assert len(outs) == K and all(o.shape[0] == level - 1 for o in outs)
+    for k in range(K):
+        factor = 2.0 if k < K - 1 else 1.0
+        got = C.decrypt(P, sk, outs[k], factor * 2.0 ** 40).real[::d_s]
+        np.testing.assert_allclose(got, want[k * c_state:(k + 1) * c_state], atol=2.0 ** -15)
+
+
+def hescan_packets(P, seed, L, K, d_s, head_dim):
+    """Mamba-2 factor packets of L tokens (Sec. "HEScan": x_k over E = HP
+    channels, a_k over heads, B_k and C_k over d_state, one group), the
+    decay exp(-softplus(z)) and the rest N(0, 1), and their broadcasts into K
+    chunks of c_state = n_slots / d_s channels (chunk slot j holds channel
+    kappa c_state + j // d_s and state index j % d_s)."""
+    n_slots = P.n // 2
+    c_state = n_slots // d_s
+    E = K * c_state
+    x = synth.normal(seed, "hx", (L, E))
+    z = synth.normal(seed, "hz", (L, E // head_dim))
+    a = 1.0 / (1.0 + np.exp(z))
+    Bv = synth.normal(seed, "hB", (L, d_s))
+    Cv = synth.normal(seed, "hC", (L, d_s))
+    j = np.arange(n_slots)
+
+    def br(k, t):
+        e, i = k * c_state + j // d_s, j % d_s
+        return x[t, e], a[t, e // head_dim], Bv[t, i], Cv[t, i]
+    return (x, a, Bv, Cv), br
+
+
+def hescan_reference(vals, head_dim):
+    """Eqs. "fesc_recurrence" and "fesc_contract" in fp64: h_k = a_k h_{k-1}
+    + x_k (x) B_k, m_k = sum_i h_k[., i] C_k[i]; returns m [L][E]."""
+    x, a, Bv, Cv = vals
+    L, E = x.shape
+    h = np.zeros((E, Bv.shape[1]))
+    out = []
+    for t in range(L):
+        h = a[t][np.arange(E) // head_dim][:, None] * h + x[t][:, None] * Bv[t][None, :]
+        out.append(h @ Cv[t])
+    return np.array(out)
+
+
+@pytest.mark.parametrize("L,block", [(4, None), (5, 2)])
+def test_hescan_layer_follows_the_recurrence(L, block):
+    """Update construction, the encrypted scan (Brent-Kung or resident) and
+    the contraction of every token decode to the fp64 recurrence."""
+    from oracle import scan as OS
+    P = C.params_small(10, 50, 8, 2)
+    seed, d_s, head_dim, K, level = 6, 8, 16, 2, 8
+    sk = C.secret_key(P, synth.secret(seed, P.n))
+    rlk = C.keygen_from_seed(P, sk, seed, 0)
+    keys = _keys(P, sk, seed, [1, 2, 4], conj=True)
+    vals, br = hescan_packets(P, seed, L, K, d_s, head_dim)
+    lo = {(4, None): 5, (5, 2): 4}[(L, block)]      # states' level: 8 - 1 - depth
+
+    def enc(v, scale, lvl, tag, idx):
+        return C.encrypt(P, sk, C.encode_plain(P, v.astype(complex), scale, lvl), lvl,
+                         *synth.encrypt_draws(seed, P.qs(lvl), P.n, tag, idx))
+    X, Bc, A, Cc = [], [], [], []
+    for k in range(K):
+        cols = [br(k, t) for t in range(L)]
+        X.append([enc(c[0], 2.0 ** 40, level, "hx", k * L + t) for t, c in enumerate(cols)])
+        A.append([enc(c[1], float(P.q[level - 2]), level - 1, "ha", k * L + t)
+                  for t, c in enumerate(cols)])
+        Bc.append([enc(c[2], float(P.q[level - 1]), level, "hB", k * L + t)
+                   for t, c in enumerate(cols)])
+        Cc.append([enc(c[3], float(P.q[lo - 1]), lo, "hC", k * L + t)
+                   for t, c in enumerate(cols)])
+    outs = OS.hescan(P, X, Bc, A, Cc, rlk, keys, d_s, block)
+    want = hescan_reference(vals, head_dim)
+    c_state = P.n // 2 // d_s
+    for t in range(L):
+        assert [o.shape[0] for o in outs[t]] == [lo - 1] * K
+        for k in range(K):
+            got = C.decrypt(P, sk, outs[t][k], 2.0 * 2.0 ** 40).real[::d_s]
+            np.testing.assert_allclose(got, want[t, k * c_state:(k + 1) * c_state],
+                                       atol=2.0 ** -15, err_msg=f"token {t} chunk {k}")
+
+
 # ------------------------------------------------- small kernels (HEConv etc.)
 
 
