@@ -26,10 +26,10 @@ One step runs all four.  `value` is the NTT GB/s (the headline
 configuration); keyswitch/s, matvec ms and scan-contract ms are reported in
 `components`.  After the steps, the HEScan affine prefix scan (Brent-Kung,
 128 tokens x 12 state chunks at 16 limbs, uniform residues: the arithmetic
-is data-oblivious) is timed on its own as `components.affine_scan`, and the
-HEScan scan of one layer at the paper's long-sequence shape (L = 2048, resident
-schedule with blocks of 1024, 12 state chunks in turn, 22 limbs) as
-`components.hescan_layer`.
+is data-oblivious) is timed on its own as `components.affine_scan`, and one
+whole HEScan layer at the paper's long-sequence shape (L = 2048, 12 state
+chunks, 23 limbs in: update construction, scan, contraction of every token;
+full-length and two-pass schedules) as `components.hescan_layer`.
 Prints ONE JSON line on stdout.  --gpus > 1 is refused (single-GPU build).
 """
 from __future__ import annotations
@@ -320,72 +320,108 @@ class Workloads:
         return lo
 
 
-def time_hescan(W, F, torch, np, L=2048, block=1024, level=22, chunks=12):
-    """HEScan scan of one layer at the paper's long-sequence shape (L tokens,
-    `chunks` state chunks, inputs at `level`), two schedules:
+def time_hescan(W, F, torch, np, L=2048, block=1024, level=23, chunks=12, d_s=128, pool=64):
+    """One HEScan layer at the paper's long-sequence shape (L tokens, `chunks`
+    state chunks of 128 channels x d_state 128, N = 2^16), chunk pair by chunk
+    pair (2l, 2l+1): the on-demand update construction s = RS(relin(x B)) from
+    `level` (23 limbs, the paper's chain of 23 ciphertext primes), the scan of
+    the states from level - 1, and the contraction of every token
+    (RS(relin(h C)), complex-paired rotate-and-add over d_state, one
+    conjugation), in two schedules:
       full_length: the whole sequence as one Brent-Kung network, in place and
-        states only, two chunks per launch sequence (2 x 94.5 GB of tuples);
-      two_pass: the resident schedule with blocks of `block` tokens (block
-        summaries, carries, replay), one chunk at a time (the paper's choice
-        on a 40 GB device).
-    Tuples are uniform residues (the arithmetic is data-oblivious); every round
-    reuses the same buffers; one warm-up round each."""
-    if hasattr(W, "af_buf"):
-        del W.af_buf, W.af_a, W.af_s
+        states only, both chunks of the pair in one launch sequence;
+      two_pass: the resident schedule with blocks of `block` tokens, one chunk
+        at a time (the paper's schedule on a 40 GB device).
+    Ciphertexts are uniform residues (the arithmetic is data-oblivious): x, a
+    and C per (token, chunk) of the pair, B from a pool of `pool` (B is as
+    large as x: holding both for 4,096 tuples next to a would exceed HBM);
+    every pair reuses the buffers; one warm-up pair per schedule."""
+    for name in ("af_buf", "af_a", "af_s"):
+        if hasattr(W, name):
+            delattr(W, name)
     torch.cuda.empty_cache()
-    W.keygen(0, W.WL.CFG5["seed"])
+    seed = W.WL.CFG5["seed"]
+    W.keygen(0, seed)
+    for st in [d_s >> k for k in range(1, d_s.bit_length())]:
+        W.keygen(W.ctx.galois_element(st), seed)
+    W.keygen(2 * W.n - 1, seed)
     ctx, n = W.ctx, W.n
-    words = level * 2 * n
-    ev = lambda: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-    out = {"tokens": L, "chunks": chunks, "level_in": level,
+    words = lambda lvl: lvl * 2 * n
+    rnd = lambda rows, lvl: torch.randint(0, 1 << 49, (rows, words(lvl)), dtype=torch.int64,
+                                          device="cuda")
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    out = {"tokens": L, "chunks": chunks, "d_state": d_s, "level_in": level,
            "paper_context": "HEScan 284.2 s/layer on one A100-40GB at this shape (two-pass, "
-                            "blocks of 1024; includes update construction and contraction; "
-                            "372K key switches; the full-length schedule did not fit in 40 GB)"}
-    # full length, in place, two chunks per round
-    per = 2
-    lo, ks = ctx.affine_scan_info(L, level, states_only=True)
-    log(f"HEScan full-length inputs: {2 * L * per * words * 8 / 1e9:.1f} GB")
-    buf = torch.randint(0, 1 << 49, (2 * L * per, words), dtype=torch.int64, device="cuda")
-    a = [buf[i] for i in range(L * per)]
-    s = [buf[L * per + i] for i in range(L * per)]
-    ctx.affine_scan(a, s, per, level, states_only=True)
-    torch.cuda.synchronize()
-    e0, e1 = ev()
-    e0.record()
-    for _ in range(chunks // per):
-        ctx.affine_scan(a, s, per, level, states_only=True)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1)
-    out["full_length"] = {"level_out": lo, "s_per_layer": round(ms / 1e3, 3),
-                          "key_switches": ks * chunks,
-                          "keyswitch_per_s": round(ks * chunks / (ms * 1e-3), 1),
-                          "chunks_per_launch": per}
-    del buf, a, s
+                            "blocks of 1024, chain of 23 ciphertext primes; construction, scan "
+                            "and contraction; 372K key switches)"}
+    pairs = chunks // 2
+    red_ks = L * (d_s.bit_length() - 1) + L            # rotations + conjugations per pair
+
+    def span(spans, key, fn):
+        a, b = ev(), ev()
+        a.record()
+        fn()
+        b.record()
+        spans.append((key, a, b))
+
+    def run(one_pair):
+        one_pair([])                                    # warm-up
+        torch.cuda.synchronize()
+        spans = []
+        for _ in range(pairs):
+            one_pair(spans)
+        torch.cuda.synchronize()
+        r = {k: 0.0 for k in ("construct_s", "scan_s", "contract_s")}
+        for k, a, b in spans:
+            r[k] += a.elapsed_time(b) / 1e3
+        r = {k: round(v, 3) for k, v in r.items()}
+        r["s_per_layer"] = round(spans[0][1].elapsed_time(spans[-1][2]) / 1e3, 3)
+        return r
+
+    tm = lambda v, K: [v[k * L + t] for t in range(L) for k in range(K)]
+    # full length: both chunks of a pair in place
+    lo, ks = ctx.affine_scan_info(L, level - 1, states_only=True)
+    gb = (2 * L * (2 * level - 1 + 2 * lo - 1) + pool * level) * 16 * n / 1e9
+    log(f"HEScan layer, full length: {gb:.1f} GB of ciphertexts")
+    X, A, Cc, O, Bp = rnd(2 * L, level), rnd(2 * L, level - 1), rnd(2 * L, lo), \
+        rnd(2 * L, lo - 1), rnd(pool, level)
+    xs, as_, cs, os_ = list(X), list(A), list(Cc), list(O)
+    bs = [Bp[i % pool] for i in range(2 * L)]
+
+    def full_pair(spans):
+        span(spans, "construct_s", lambda: ctx.mul_relin_rescale(xs, bs, xs, level))
+        span(spans, "scan_s", lambda: ctx.affine_scan(as_, xs, 2, level - 1, states_only=True))
+        span(spans, "contract_s", lambda: ctx.scan_contract(tm(xs, 2), None, tm(cs, 2), d_s,
+                                                            tm(os_, 2), lo, tokens=L))
+    r = run(full_pair)
+    total_ks = pairs * (2 * L + 2 * ks + 2 * L + red_ks)
+    r.update({"level_states": lo, "level_out": lo - 1, "key_switches": total_ks,
+              "keyswitch_per_s": round(total_ks / r["s_per_layer"], 1)})
+    out["full_length"] = r
+    del X, A, Cc, O, Bp, xs, as_, cs, os_, bs
     torch.cuda.empty_cache()
-    # two-pass resident schedule, one chunk at a time
-    lo, ws_bytes, ks = ctx.affine_scan_resident_info(L, 1, block, level)
-    log(f"HEScan two-pass inputs: {2 * L * words * 8 / 1e9:.1f} GB per chunk, "
-        f"workspace {ws_bytes / 1e9:.1f} GB")
-    buf = torch.randint(0, 1 << 49, (2 * L, words), dtype=torch.int64, device="cuda")
-    a = [buf[i] for i in range(L)]
-    s = [buf[L + i] for i in range(L)]
-    hb = torch.empty((L, lo * 2 * n), dtype=torch.int64, device="cuda")
-    h = [hb[i] for i in range(L)]
+    # two-pass resident schedule: one chunk at a time, the pair contracted together
+    lo, ws_bytes, ks = ctx.affine_scan_resident_info(L, 1, block, level - 1)
+    log(f"HEScan layer, two-pass: workspace {ws_bytes / 1e9:.1f} GB")
+    X, A, H, Cc, O, Bp = rnd(L, level), rnd(L, level - 1), rnd(2 * L, lo), rnd(2 * L, lo), \
+        rnd(2 * L, lo - 1), rnd(pool, level)
     ws = torch.empty(ws_bytes // 8 + 1, dtype=torch.int64, device="cuda")
-    ctx.affine_scan_resident(a, s, 1, block, h, level, ws)
-    torch.cuda.synchronize()
-    e0, e1 = ev()
-    e0.record()
-    for _ in range(chunks):
-        ctx.affine_scan_resident(a, s, 1, block, h, level, ws)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1)
-    out["two_pass"] = {"block": block, "level_out": lo, "s_per_layer": round(ms / 1e3, 3),
-                       "key_switches": ks * chunks,
-                       "keyswitch_per_s": round(ks * chunks / (ms * 1e-3), 1)}
-    del buf, a, s, hb, h, ws
+    xs, as_, hs, cs, os_ = list(X), list(A), list(H), list(Cc), list(O)
+    bs = [Bp[i % pool] for i in range(L)]
+
+    def two_pass_pair(spans):
+        for c in range(2):
+            span(spans, "construct_s", lambda: ctx.mul_relin_rescale(xs, bs, xs, level))
+            span(spans, "scan_s", lambda: ctx.affine_scan_resident(
+                as_, xs, 1, block, hs[c * L:(c + 1) * L], level - 1, ws))
+        span(spans, "contract_s", lambda: ctx.scan_contract(tm(hs, 2), None, tm(cs, 2), d_s,
+                                                            tm(os_, 2), lo, tokens=L))
+    r = run(two_pass_pair)
+    total_ks = pairs * (2 * L + 2 * ks + 2 * L + red_ks)
+    r.update({"block": block, "level_states": lo, "level_out": lo - 1,
+              "key_switches": total_ks, "keyswitch_per_s": round(total_ks / r["s_per_layer"], 1)})
+    out["two_pass"] = r
+    del X, A, H, Cc, O, Bp, ws, xs, as_, hs, cs, os_, bs
     torch.cuda.empty_cache()
     return out
 
@@ -617,7 +653,7 @@ def main():
     # diagonal bank released (its 128 x 12 x 2 ciphertexts take 51.5 GB)
     affine = hescan = None
     if not args.no_affine:
-        del W.mv_plan, W.bank
+        del W.mv_plan, W.bank, W.sc_in, W.sc_out
         torch.cuda.empty_cache()
         affine = time_affine(W, F, torch, np)
         if not args.no_hescan:
