@@ -72,7 +72,7 @@ def kernel_sources_sha256(paths) -> str:
 KS_PROFILE = os.path.join(ROOT, "profiles", "keyswitch_rotation_set_n65536_l24_dnum3.txt")
 KS_SOURCES = [os.path.join(ROOT, "paper_2608_17442_amd", "csrc", f)
               for f in ("ntt.hip", "keyswitch.hip", "butterfly.hpp", "fesc_internal.hpp",
-                        "ops.cpp", "ops.hpp")]
+                        "ops.cpp", "ops.hpp", "scratch.hpp")]
 
 
 def profiled_fields(profile: str, sources) -> dict | None:
