@@ -162,3 +162,41 @@ def test_hescan_layer(small, L, K, block):
             factor = 1.0 if (K % 2 and k == K - 1) else 2.0
             dec = C.decrypt(P, S.sk, want[t][k], factor * 2.0 ** 40).real[::d_s]
             assert np.max(np.abs(dec - ref[t, k * c_state:(k + 1) * c_state])) <= 2.0 ** -15
+
+
+def test_hescan_layer_full_size():
+    """The layer at the bench's ring and chain (N = 2^16, x and B at 23
+    limbs, d_state 128, Brent-Kung scan in place, contraction of every token
+    in one call), four tokens of one chunk pair: bit-exact against the oracle
+    and within 2^-15 of the fp64 recurrence."""
+    P = C.params_p16(24)
+    d_s, head_dim, level, L, K = 128, 64, 23, 4, 2
+    S = Setup(P, 64, rot_steps=[d_s >> k for k in range(1, 8)], relin=True, conj=True)
+    vals, br = hescan_packets(P, 64, L, K, d_s, head_dim)
+    lo = level - 1 - 2                                  # Brent-Kung depth 2 for 4 tokens
+    Xo, Bo, Ao, Co = ([[] for _ in range(K)] for _ in range(4))
+    Xd, Bd, Ad, Cd = [], [], [], []
+    for k in range(K):
+        for t in range(L):
+            xv, av, bv, cv = br(k, t)
+            i = 4 * (k * L + t)
+            for v, sc, lvl, o, d, r in [(xv, 2.0 ** 40, level, Xo, Xd, 0),
+                                        (bv, float(P.q[level - 1]), level, Bo, Bd, 1),
+                                        (av, float(P.q[level - 2]), level - 1, Ao, Ad, 2),
+                                        (cv, float(P.q[lo - 1]), lo, Co, Cd, 3)]:
+                co, cd = S.encrypt(v, sc, lvl, 700 + i + r)
+                o[k].append(co)
+                d.append(cd)
+    step(f"hescan layer full size L={L} K={K} level={level}")
+    outs, lo_out = hescan_gpu(S.ctx, Xd, Bd, Ad, Cd, K, L, d_s, level, None)
+    assert lo_out == lo - 1
+    want = OS.hescan(P, Xo, Bo, Ao, Co, S.keys[0], S.keys, d_s, None)
+    ref = hescan_reference(vals, head_dim)
+    c_state = P.n // 2 // d_s
+    for t in range(L):
+        for k in range(K):
+            _eq(outs[t * K + k], want[t][k], f"token {t} chunk {k}")
+            dec = C.decrypt(P, S.sk, want[t][k], 2.0 * 2.0 ** 40).real[::d_s]
+            err = np.max(np.abs(dec - ref[t, k * c_state:(k + 1) * c_state]))
+            print(f"full-size layer token {t} chunk {k}: max |decoded - fp64| = {err:.3e}")
+            assert err <= 2.0 ** -15
