@@ -16,11 +16,13 @@ Metric (three workloads, all N = 2^16 with ~50-bit primes = 1 mod 2N; the
          and rescale -> 48 ciphertexts (seed 3); 18,432 pre-encoded diagonals
          (154.6 GB) resident in HBM.
 
-  SCAN   scan-contract slice of a block of 16 Mamba-base tokens (24 heads x
-         64 channels x d_state 128 in 12 state chunks of 16,384 slots, level
-         20 -> 18, seed 4; the block repeats token 0's ciphertexts): products
-         with decay and C, rotate-and-add over d_state, complex-paired
-         conjugation split, every step batched over the block.
+  SCAN   scan-contract slice of a block of 16 distinct Mamba-base tokens (24
+         heads x 64 channels x d_state 128 in 12 state chunks of 16,384 slots,
+         level 20 -> 18, seed 4): products with decay and C, rotate-and-add
+         over d_state, complex-paired conjugation split, every step batched
+         over the block.  After the steps the whole 2048-token sequence (the
+         16-token pool cycled, 128 calls) is timed as
+         `components.scan_contract_sequence`.
 
 One step runs all four.  `value` is the NTT GB/s (the headline
 configuration); keyswitch/s, matvec ms and scan-contract ms are reported in
@@ -252,9 +254,7 @@ class Workloads:
         self.mv_plan(self.mv_in, self.mv_out)
         ev[1].record()
 
-    # ---- scan-contract slice: one Mamba-base token, 12 state chunks
-    sc_tokens = 16
-
+    # ---- scan-contract slice: a block of 16 Mamba-base tokens, 12 state chunks each
     def setup_scan_contract(self):
         np, WL = self.np, self.WL
         cfg = WL.CFG5
@@ -265,37 +265,57 @@ class Workloads:
             self.keygen(self.ctx.galois_element(st), seed)
         self.keygen(2 * self.n - 1, seed)
         self.keygen(0, seed)
-        z, cvec, H = WL.cfg5_token(0)
         K = cfg["heads"] * hd * d_s // s_state
-        decay = 1.0 / (1.0 + np.exp(z))
         c_state = s_state // d_s
         j = np.arange(n_slots)
+        T = cfg["pool"]
+        # a pool of 16 distinct tokens (token k of the sequence uses entry k mod 16),
+        # token-major: index u*K + k
         self.sc_in = ([], [], [])
-        for k in range(K):
-            # chunk k: channel e = k c_state + j // d_s at slots (j // d_s) d_s + j % d_s
-            e, i = k * c_state + j // d_s, j % d_s
-            ok = j < s_state
-            e = np.minimum(e, H.shape[0] - 1)
-            vals = (np.where(ok, H[e, i], 0.0), np.where(ok, decay[e // hd], 0.0),
-                    np.where(ok, cvec[i], 0.0))
-            scales = (2.0 ** 40, float(self.q[level - 1]), float(self.q[level - 2]))
-            for r in range(3):
-                self.sc_in[r].append(self.encrypt(vals[r].astype(complex), scales[r], level, seed,
-                                                  "cfg5", 3 * k + r))
-        # a block of tokens per call (token 0's ciphertexts copied: the
-        # arithmetic is data-oblivious)
-        T = self.sc_tokens
-        self.sc_in = tuple([x.clone() for _ in range(T) for x in part] for part in self.sc_in)
-        self.sc_out = [self.torch.empty((level - 2) * 2 * self.n, dtype=self.torch.int64,
-                                        device="cuda") for _ in range(K * T)]
+        for u in range(T):
+            z, cvec, H = WL.cfg5_token(u)
+            decay = 1.0 / (1.0 + np.exp(z))
+            for k in range(K):
+                # chunk k: channel e = k c_state + j // d_s at slots (j // d_s) d_s + j % d_s
+                e, i = k * c_state + j // d_s, j % d_s
+                ok = j < s_state
+                e = np.minimum(e, H.shape[0] - 1)
+                vals = (np.where(ok, H[e, i], 0.0), np.where(ok, decay[e // hd], 0.0),
+                        np.where(ok, cvec[i], 0.0))
+                scales = (2.0 ** 40, float(self.q[level - 1]), float(self.q[level - 2]))
+                for r in range(3):
+                    self.sc_in[r].append(self.encrypt(vals[r].astype(complex), scales[r], level,
+                                                      seed, "cfg5", 3 * (u * K + k) + r))
+        # two output sets: tokens 0-15 kept, the rest of a sequence to a ring
+        self.sc_out = [[self.torch.empty((level - 2) * 2 * self.n, dtype=self.torch.int64,
+                                         device="cuda") for _ in range(K * T)] for _ in range(2)]
         self.sc_shape = dict(chunks=K, tokens=T, d_state=d_s, level=level)
 
-    def run_scan_contract(self, ev):
-        ev[0].record()
+    def run_scan_contract(self, ev, ring=0):
+        ev and ev[0].record()
         h, dec, cf_ = self.sc_in
-        self.ctx.scan_contract(h, dec, cf_, self.sc_shape["d_state"], self.sc_out,
+        self.ctx.scan_contract(h, dec, cf_, self.sc_shape["d_state"], self.sc_out[ring],
                                self.sc_shape["level"], tokens=self.sc_shape["tokens"])
+        ev and ev[1].record()
+
+    def time_scan_contract_sequence(self):
+        """The slice over a whole cfg5 sequence (2048 tokens: 128 calls over the
+        16-token pool, outputs of tokens 0-15 kept, the rest to a ring)."""
+        torch = self.torch
+        L, T = self.WL.CFG5["L"], self.sc_shape["tokens"]
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        ev[0].record()
+        for b in range(L // T):
+            self.run_scan_contract(None, ring=min(b, 1))
         ev[1].record()
+        torch.cuda.synchronize()
+        t = ev[0].elapsed_time(ev[1]) / 1e3
+        ks = L * (2 * self.sc_shape["chunks"] + (self.sc_shape["chunks"] // 2)
+                  * (self.sc_shape["d_state"].bit_length() - 1 + 1))
+        return {"tokens": L, "tokens_per_call": T, "s": round(t, 3),
+                "ms_per_token": round(t * 1e3 / L, 3), "key_switches": ks,
+                "keyswitch_per_s": round(ks / t, 1)}
 
     # ---- affine prefix scan (HEScan): Brent-Kung over 128 tokens x 12 chunks
     def setup_affine(self, L=128, chunks=12, level=16):
@@ -568,9 +588,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-affine", action="store_true",
-                    help="skip the affine prefix scan component (timed after the steps)")
+                    help="skip the components timed after the steps (whole-sequence "
+                         "scan-contract, affine prefix scan, HEScan layer)")
     ap.add_argument("--no-hescan", action="store_true",
-                    help="skip the HEScan layer component (L=2048, resident schedule)")
+                    help="skip the HEScan layer component (L=2048: construction, scan, "
+                         "contraction)")
     ap.add_argument("--scan-sweep", action="store_true",
                     help="only the resident-schedule block-size sweep at L=2048 (one chunk)")
     ap.add_argument("--affine-only", action="store_true",
@@ -651,8 +673,9 @@ def main():
     baby_ms, ptmac_ms, tail_ms = phases[-1]
     # HEScan affine prefix scan, timed after the steps with the projection's
     # diagonal bank released (its 128 x 12 x 2 ciphertexts take 51.5 GB)
-    affine = hescan = None
+    affine = hescan = sc_seq = None
     if not args.no_affine:
+        sc_seq = W.time_scan_contract_sequence()
         del W.mv_plan, W.bank, W.sc_in, W.sc_out
         torch.cuda.empty_cache()
         affine = time_affine(W, F, torch, np)
@@ -717,6 +740,7 @@ def main():
                                  "giant_conj_rescale": round(tail_ms, 3)},
             "scan_contract_ms_per_token": round(sc / W.sc_shape["tokens"], 3),
             "scan_contract_tokens_per_call": W.sc_shape["tokens"],
+            "scan_contract_sequence": sc_seq,
             "diagonal_bank_build_s": {"total": round(W.bank_build_s, 2),
                                       "host_slot_values": round(W.bank_slots_s, 2),
                                       "diagonals": W.mv_shape["n_diag"],
