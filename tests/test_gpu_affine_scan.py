@@ -155,3 +155,42 @@ def test_affine_scan_down_to_level_one(small, L, level, states_only):
         _eq_prefix(sd[k], H[k], f"state {k}")
         if not states_only:
             _eq_prefix(ad[k], A[k], f"a-prefix {k}")
+
+
+def test_affine_scan_bench_configuration():
+    """The benchmark's launch: 128 tokens x 12 chunks at 16 limbs (N = 2^16),
+    states only, in place.  Prefix k depends only on tokens 0..k and the
+    network forms positions below 2^m exactly as a 2^m-token network does, so
+    the oracle checks sampled prefixes from the first tokens: chunk 0 through
+    32 tokens, chunk 11 through 8; every other tuple is uniform residues.
+    Compared on the leading limbs of the common output level."""
+    P = C.params_p16(24)
+    S = Setup(P, 54, relin=True)
+    L, chunks, level = 128, 12, 16
+    real = {0: 32, chunks - 1: 8}
+    words = level * 2 * P.n
+    ad, sd, ao, so = [], [], {}, {}
+    for c in range(chunks):
+        for k in range(L):
+            if k < real.get(c, 0):
+                i = c * L + k
+                dec = 0.5 + 0.5 * synth.uniform_pm1(S.seed, "bench-a", P.n // 2, i) ** 2
+                upd = synth.normal(S.seed, "bench-s", P.n // 2, 1.0, i)
+                x, y = S.encrypt(dec, float(P.q[level - 1]), level, 3000 + 2 * i)
+                ao.setdefault(c, []).append(x)
+                ad.append(y)
+                x, y = S.encrypt(upd, 2.0 ** 40, level, 3001 + 2 * i)
+                so.setdefault(c, []).append(x)
+                sd.append(y)
+            else:
+                ad.append(torch.randint(0, 1 << 49, (words,), dtype=torch.int64, device="cuda"))
+                sd.append(torch.randint(0, 1 << 49, (words,), dtype=torch.int64, device="cuda"))
+    lo_i, _ = S.ctx.affine_scan_info(L, level, states_only=True)
+    step(f"affine_scan bench configuration L={L} chunks={chunks} level={level}")
+    lo = S.ctx.affine_scan(ad, sd, chunks, level, states_only=True)
+    assert lo == lo_i == level - 12
+    for c, m in real.items():
+        _, H = OS.affine_scan(S.P, ao[c], so[c], S.keys[0])
+        for k in range(m):
+            want = H[k][:lo]
+            _eq_prefix(sd[c * L + k], want, f"chunk {c} state {k}")

@@ -1,6 +1,8 @@
 """GPU parity of the scan-contract slice against the oracle: a small ring with
-four chunks, and one full-size Mamba-2-base token (N = 2^16, 12 state chunks
-of 128 channels x d_state 128, level 20 -> 18)."""
+five chunks, blocks of tokens, and one full-size Mamba-2-base token (N = 2^16,
+12 state chunks of 128 channels x d_state 128, level 20 -> 18), also run as a
+16-token block (the benchmark's launch configuration) of copies that must all
+equal it."""
 import numpy as np
 import pytest
 import torch
@@ -40,7 +42,7 @@ def chunk_slots(z, cvec, H, K, n_slots, d_s, head_dim, s_state=None):
     return out
 
 
-def _run(P, S, chunks, level, d_s, tag):
+def _run(P, S, chunks, level, d_s, tag, block=0):
     hs_o, ds_o, cs_o, hs_d, ds_d, cs_d = [], [], [], [], [], []
     for k, (hv, dv, cv) in enumerate(chunks):
         for vals, scale, lo, ld, role in [(hv, 2.0 ** 40, hs_o, hs_d, 0),
@@ -57,6 +59,20 @@ def _run(P, S, chunks, level, d_s, tag):
     for k, (od, oo) in enumerate(zip(outs_d, outs_o)):
         got = to_host(od).reshape(oo.shape)
         assert np.array_equal(got, oo), f"{tag} output {k}: {first_mismatch(got, oo)}"
+    if block:
+        # the launch configuration of a token block: `block` tokens per call
+        # (copies of this token's inputs), every token equal to the one above
+        K = len(chunks)
+        outs_b = [torch.zeros((level - 2) * 2 * P.n, dtype=torch.int64, device="cuda")
+                  for _ in range(K * block)]
+        step(f"scan_contract {tag} block of {block} tokens")
+        S.ctx.scan_contract(hs_d * block, ds_d * block, cs_d * block, d_s, outs_b, level,
+                            tokens=block)
+        for u in range(block):
+            for k in range(K):
+                got = to_host(outs_b[u * K + k]).reshape(outs_o[k].shape)
+                assert np.array_equal(got, outs_o[k]), \
+                    f"{tag} block token {u} output {k}: {first_mismatch(got, outs_o[k])}"
     return outs_o
 
 
@@ -94,7 +110,7 @@ def test_cfg5_one_token_full_size():
     S = Setup(P, cfg["seed"], rot_steps=steps, relin=True, conj=True)
     z, cvec, H = WL.cfg5_token(0)
     chunks = chunk_slots(z, cvec, H, K, n_slots, d_s, head_dim, s_state)
-    outs = _run(P, S, chunks, level, d_s, "cfg5")
+    outs = _run(P, S, chunks, level, d_s, "cfg5", block=cfg["pool"])
     decay = 1.0 / (1.0 + np.exp(z))
     want = (decay[np.arange(H.shape[0]) // head_dim][:, None] * H * cvec[None, :]).sum(axis=1)
     c_state = s_state // d_s
