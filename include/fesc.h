@@ -332,6 +332,17 @@ int fesc_affine_scan(fesc_ctx* ctx, uint64_t* const* a, uint64_t* const* s, uint
 int fesc_affine_scan_info(fesc_ctx* ctx, uint32_t L, uint32_t level, uint32_t flags,
                           uint32_t* out_level, uint64_t* key_switches);
 
+/* Host only (no context, no device): the network fesc_affine_scan runs for L
+ * positions, one node per composition in execution order, 4 words each:
+ * (stage, dst, src, decay) -- position dst takes T_src o T_dst (0-based
+ * positions), and decay = 1 if the node forms its decay product (always, unless
+ * flags has FESC_SCAN_STATES_ONLY and no later product reads it).  Nodes of
+ * one stage are independent.  With nodes = NULL only *count is set; otherwise
+ * cap nodes are available and FESC_ERR_ARG is returned (after *count is set)
+ * if the network has more.  1 <= L <= 2^20. */
+int fesc_affine_scan_network(uint32_t L, uint32_t flags, uint32_t* nodes, size_t cap,
+                             size_t* count);
+
 /* The same scan by the two-pass resident block schedule (Sec. "Resident
  * Block Schedule", Eq. "resident-block-schedule"), returning states only.
  * Blocks of `block` tokens (the last may be partial).  Pass 1 keeps the

@@ -127,6 +127,7 @@ int op_affine_scan(Context* c, uint64_t* const* a, uint64_t* const* s, uint32_t 
                    hipStream_t st);
 int op_affine_scan_level(Context* c, uint32_t L, uint32_t level, bool states_only,
                          uint32_t* out_level, uint64_t* products);
+size_t affine_scan_network(uint32_t L, bool states_only, uint32_t* nodes, size_t cap);
 size_t affine_scan_resident_words(const Context* c, uint32_t L, uint32_t chunks, uint32_t block,
                                   uint32_t level);
 int op_affine_scan_resident_level(Context* c, uint32_t L, uint32_t block, uint32_t level,
@@ -377,6 +378,15 @@ int fesc_affine_scan_info(fesc_ctx* ctx, uint32_t L, uint32_t level, uint32_t fl
     return fail(FESC_ERR_ARG, "bad argument");
   return op_affine_scan_level(ctx, L, level, flags & FESC_SCAN_STATES_ONLY, out_level,
                               key_switches);
+}
+
+int fesc_affine_scan_network(uint32_t L, uint32_t flags, uint32_t* nodes, size_t cap,
+                             size_t* count) {
+  if (!count || L == 0 || L > (1u << 20) || (flags & ~FESC_SCAN_STATES_ONLY))
+    return fail(FESC_ERR_ARG, "bad scan-network arguments");
+  *count = affine_scan_network(L, flags & FESC_SCAN_STATES_ONLY, nodes, cap);
+  if (nodes && *count > cap) return fail(FESC_ERR_ARG, "node array too small");
+  return FESC_OK;
 }
 
 int fesc_affine_scan(fesc_ctx* ctx, uint64_t* const* a, uint64_t* const* s, uint32_t L,

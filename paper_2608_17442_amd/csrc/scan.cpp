@@ -185,6 +185,23 @@ uint32_t min_level(const std::vector<uint32_t>& lvl) {
 
 }  // namespace
 
+size_t affine_scan_network(uint32_t L, bool states_only, uint32_t* nodes, size_t cap) {
+  const Stages net = bk_network(L);
+  const std::vector<std::vector<char>> live =
+      live_decay(net, std::vector<char>(L, states_only ? 0 : 1));
+  size_t k = 0;
+  for (size_t i = 0; i < net.size(); ++i)
+    for (size_t j = 0; j < net[i].size(); ++j, ++k)
+      if (nodes && k < cap) {
+        uint32_t* o = nodes + 4 * k;
+        o[0] = (uint32_t)i;
+        o[1] = net[i][j].dst;
+        o[2] = net[i][j].src;
+        o[3] = (uint32_t)live[i][j];
+      }
+  return k;
+}
+
 int op_affine_scan_level(Context* c, uint32_t L, uint32_t level, bool states_only,
                          uint32_t* out_level, uint64_t* products) {
   const Stages net = bk_network(L);

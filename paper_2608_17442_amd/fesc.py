@@ -66,6 +66,7 @@ _SIGS = {
     "fesc_affine_scan": [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp), _u32, _u32, _u32, _u32,
                          ctypes.POINTER(_u32), _vp],
     "fesc_affine_scan_info": [_vp, _u32, _u32, _u32, ctypes.POINTER(_u32), ctypes.POINTER(_u64)],
+    "fesc_affine_scan_network": [_u32, _u32, ctypes.POINTER(_u32), _sz, ctypes.POINTER(_sz)],
     "fesc_affine_scan_resident_info": [_vp, _u32, _u32, _u32, _u32, ctypes.POINTER(_u32),
                                        ctypes.POINTER(_sz), ctypes.POINTER(_u64)],
     "fesc_heconv": [_vp, _vp, _u32, ctypes.POINTER(_i32), ctypes.POINTER(_vp), _vp, _vp, _u32,
@@ -327,6 +328,16 @@ def c2m_level(q, level: int, ell: int, sigma: int, delta: float, bmax: float) ->
     _check(_lib.fesc_c2m_level(qs, level, ell, sigma, float(delta), float(bmax),
                                ctypes.byref(out)))
     return int(out.value)
+
+
+def affine_scan_network(L: int, states_only: bool = False):
+    """Nodes (stage, dst, src, decay) of the affine scan's network; host-only."""
+    flags = SCAN_STATES_ONLY if states_only else 0
+    cnt = _sz()
+    _check(_lib.fesc_affine_scan_network(L, flags, None, 0, ctypes.byref(cnt)))
+    buf = (_u32 * (4 * max(cnt.value, 1)))()
+    _check(_lib.fesc_affine_scan_network(L, flags, buf, cnt.value, ctypes.byref(cnt)))
+    return [tuple(buf[4 * i:4 * i + 4]) for i in range(cnt.value)]
 
 
 def encode(log_n: int, z, scale: float):

@@ -5,6 +5,7 @@ import ctypes
 import os
 import re
 
+import numpy as np
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -104,3 +105,62 @@ def test_c2m_level_matches_oracle():
         for ell, sig, d, b in cases:
             want = W.c2m_level(P, level, ell, sig, d, b)
             assert F.c2m_level(P.q, level, ell, sig, d, b) == (want or 0), (level, ell, sig, d, b)
+
+
+SCAN_LENGTHS = list(range(1, 70)) + [127, 128, 129, 255, 256, 1000, 1024, 2047, 2048, 4096]
+
+
+@pytest.mark.parametrize("states_only", [False, True])
+def test_affine_scan_network_matches_oracle(states_only):
+    """The library's scan network (host export) against the oracle's
+    Brent-Kung network: the same compositions (dst <- src o dst), independent
+    nodes within a stage, adjacent intervals composed so that every position
+    ends with its full prefix, the same composition depth; every decay product
+    formed without states_only, and with it the pruned network still gives the
+    recurrence's states (affine maps mod a prime, skipped decay products left
+    stale)."""
+    from oracle import scan as OS
+    from paper_2608_17442_amd import fesc as F
+    prime = (1 << 61) - 1
+    for L in SCAN_LENGTHS:
+        nodes = F.affine_scan_network(L, states_only)
+        ops = []
+        OS.brent_kung([(k, k) for k in range(L)],
+                      lambda l, r: ops.append((r[1], l[1])) or (l[0], r[1]))
+        assert sorted((d, s) for _, d, s, _ in nodes) == sorted(ops), L
+        # stages: non-decreasing; within a stage no node reads another's destination
+        stages = {}
+        for st, d, s, _ in nodes:
+            stages.setdefault(st, []).append((d, s))
+        assert [n[0] for n in nodes] == sorted(n[0] for n in nodes)
+        for st, v in stages.items():
+            dsts = {d for d, _ in v}
+            assert len(dsts) == len(v) and not any(s in dsts for _, s in v), (L, st)
+        # interval semantics and depth
+        iv = [(k, k) for k in range(L)]
+        depth = [0] * L
+        for _, d, s, _ in nodes:
+            assert iv[s][1] + 1 == iv[d][0], (L, d, s)
+            iv[d] = (iv[s][0], iv[d][1])
+            depth[d] = max(depth[d], depth[s]) + 1
+        assert iv == [(0, k) for k in range(L)]
+        want_depth = OS.brent_kung([0] * L, lambda l, r: max(l, r) + 1)[0] if L > 1 else [0]
+        assert max(depth) == max(want_depth), L
+        if not states_only:
+            assert all(n[3] == 1 for n in nodes)
+            continue
+        # pruned network: states equal the sequential recurrence
+        rng = np.random.default_rng(L)
+        a0 = [int(x) for x in rng.integers(1, prime, L)]
+        s0 = [int(x) for x in rng.integers(0, prime, L)]
+        a, s = list(a0), list(s0)
+        for _, d, src, live in nodes:
+            s[d] = (a[d] * s[src] + s[d]) % prime
+            if live:
+                a[d] = a[d] * a[src] % prime
+            else:
+                a[d] = None                      # a product nothing may read
+        h = 0
+        for k in range(L):
+            h = (a0[k] * h + s0[k]) % prime
+            assert s[k] == h, (L, k)
