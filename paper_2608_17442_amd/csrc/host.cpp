@@ -188,7 +188,7 @@ static int build_tables(Context* c) {
   std::vector<PrimeK> pk(np);
   std::vector<double2> fwd((size_t)np * n), inv((size_t)np * n);
   const uint32_t nblk = n / 4096;
-  std::vector<double> fwd3((size_t)np * nblk * 15 * 256), inv3(fwd3.size());
+  std::vector<double> fwd3((size_t)np * nblk * 256), inv3(fwd3.size());
   std::vector<uint64_t> pw(n);
   for (uint32_t i = 0; i < np; ++i) {
     const uint64_t q = c->primes[i];
@@ -207,17 +207,13 @@ static int build_tables(Context* c) {
         const double w = e > q / 2 ? -(double)(q - e) : (double)e;
         t[k] = double2{w, w / qd};
       }
-      // Block blk, slot k (register distance H, group gi), thread e: the
-      // twiddle psi_rev[(N + 4096 blk) / 2H + e * 8/H + gi].
-      double* t3 = (dir == 0 ? fwd3.data() : inv3.data()) + (size_t)i * nblk * 15 * 256;
+      // Block blk, thread e: psi_rev[(N + 4096 blk) / 2 + 8 e], the power from
+      // which an inner pass generates the twiddles of index bits 3..0 of its
+      // 16 consecutive values.
+      double* t3 = (dir == 0 ? fwd3.data() : inv3.data()) + (size_t)i * nblk * 256;
       for (uint32_t blk = 0; blk < nblk; ++blk)
-        for (uint32_t k = 0; k < 15; ++k) {
-          const uint32_t lh = k == 0 ? 3 : k < 3 ? 2 : k < 7 ? 1 : 0;
-          const uint32_t gi = k - ((1u << (3 - lh)) - 1);
-          const uint32_t base = (n + 4096 * blk) >> (lh + 1);
-          for (uint32_t e = 0; e < 256; ++e)
-            t3[((size_t)blk * 15 + k) * 256 + e] = t[base + e * (8u >> lh) + gi].x;
-        }
+        for (uint32_t e = 0; e < 256; ++e)
+          t3[(size_t)blk * 256 + e] = t[((n + 4096 * blk) >> 1) + 8 * e].x;
     }
   }
   // device encoding tables

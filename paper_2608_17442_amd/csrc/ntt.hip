@@ -25,10 +25,11 @@
 // reduction is spent on it.  For N = 4096 the inner pass alone is the whole
 // transform.
 //
-// Twiddles: stages on bits 11..4 read the bit-reversed power table (few
-// distinct values per wavefront); stages on bits 3..0 read a per-block
-// re-ordering of the same powers (Context::d_tw3_*), laid out so that these
-// loads are coalesced too.
+// Twiddles: the outer passes read the bit-reversed power table (uniform per
+// stage); an inner pass stages its block's 255 twiddles of bits 11..4 in LDS
+// next to the data and generates those of bits 3..0 from one power per
+// thread (Context::d_tw3_*), so that no global load is waited on
+// between its butterflies.
 #include "butterfly.hpp"
 #include "fesc_internal.hpp"
 #include "ops.hpp"
@@ -56,26 +57,47 @@ __device__ __forceinline__ uint32_t lds_mid(uint32_t a, uint32_t b, uint32_t r) 
 __device__ __forceinline__ uint32_t lds_col(uint32_t t, uint32_t r) { return 17 * t + r; }
 constexpr int kLds = kBlock + kBlock / 16;
 
-// Table reads of the twiddles.  For index bits 11..8 (register distance H,
-// distance 256 H) the group twiddle is psi_rev[(N + B) / 512H + gi]; for bits
-// 7..4 (distance 16 H) with a = bits 11..8 of the thread's values it is
-// psi_rev[(N + B) / 32H + a * 8/H + gi]; B is the block offset in the row.
-struct TwHi {
-  const double2* tw;
-  uint32_t base;
-  __device__ __forceinline__ double2 operator()(int gi) const { return tw[base + gi]; }
+// Inner passes: the twiddles of bits 11..4 staged in LDS per block.  For
+// index bits 11..8 (register distance H, distance 256 H) the group twiddle is
+// psi_rev[(N + B) / 512H + gi]; for bits 7..4 (distance 16 H) with a = bits
+// 11..8 of the thread's values it is psi_rev[(N + B) / 32H + a * 8/H + gi]
+// (B the block offset in the row): eight contiguous runs of the table, 255
+// values.  Entry t < 255 of the staging array lies in segment k = floor(log2(t + 1))
+// (the 2^k group twiddles of one stage) at index t + 1 - 2^k, i.e.
+// psi_rev[(N + B) / 2^(12 - k) + t + 1 - 2^k]; entries 255..261 are
+// psi_rev[1..7].  For bits 11..8 (distance 256 H) the stage of H uses
+// segment log2(8/H); for bits 7..4 (distance 16 H) segment 4 + log2(8/H), at
+// a * 8/H + gi.
+constexpr int kTwL = 262;
+__device__ __forceinline__ double2 block_twiddle(const double2* tw, uint32_t nb, uint32_t t) {
+  const uint32_t k = 31 - __builtin_clz(t + 1);  // t < 255
+  return tw[(nb >> (12 - k)) + t + 1 - (1u << k)];
+}
+struct TwL {
+  const double2* lt;
+  uint32_t off;
+  __device__ __forceinline__ double2 operator()(int gi) const { return lt[off + gi]; }
 };
-// Bits 3..0: re-ordered table s3[k][e] (k = H-group slot, e = thread).
-template <int H>
-struct TwLo {
-  const double* s3;
-  double qinv;
+
+// Bits 3..0, generated instead of loaded: thread t's 16 consecutive values
+// are positions 16 j + r with j = (N + B) / 16 + t; brv(j) has its three low
+// bits clear, so psi_rev[j 8/H + gi] = psi_rev[j 8/H] psi_rev[gi] and
+// psi_rev[j 8/H] = b^(8/H) with b = psi_rev[8 j].  Each twiddle is formed as
+// the balanced representative (the table's value) and w' = w / q as w qinv
+// (as for the loaded ones).
+struct TwGen {
+  double base;         // psi_rev[j 8/H], balanced
+  const double2* c;    // psi_rev[1..7] (LDS)
+  double q, qinv;
   __device__ __forceinline__ double2 operator()(int gi) const {
-    constexpr int k0 = H == 8 ? 0 : H == 4 ? 1 : H == 2 ? 3 : 7;
-    const double w = s3[(k0 + gi) * kThreads];
+    const double w =
+        gi == 0 ? base : red_bal(mm_shoup(base, c[gi - 1].x, c[gi - 1].y, q), q, qinv);
     return double2{w, w * qinv};
   }
 };
+__device__ __forceinline__ double sq_bal(double b, double q, double qinv) {
+  return red_bal(mm_shoup(b, b, b * qinv, q), q, qinv);
+}
 
 }  // namespace
 
@@ -406,12 +428,11 @@ struct RescaleMap {
 // `row`: on return thread t holds the values at block positions 16 t + r in
 // x[r].  Uses all of `lds`; the caller needs a barrier before touching it
 // again unless it only writes the words it is handed (positions 16 t + r).
+// Thread t's values t + 256 r of block B: uint64 residues (SINGLE) or the
+// outer pass's fp64 intermediate.
 template <bool SINGLE>
-__device__ __forceinline__ void fwd_block(const uint64_t* row, uint32_t B, uint32_t n,
-                                          const double2* tw, const double* s3, double q,
-                                          double qinv, double* lds, double (&x)[16]) {
-  const uint32_t t = threadIdx.x, a = t >> 4, b = t & 15;
-  const uint32_t nb = n + B;
+__device__ __forceinline__ void fwd_load(const uint64_t* row, uint32_t B, double (&x)[16]) {
+  const uint32_t t = threadIdx.x;
   if constexpr (SINGLE) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) x[r] = u2d(row[B + t + 256 * r]);
@@ -420,31 +441,39 @@ __device__ __forceinline__ void fwd_block(const uint64_t* row, uint32_t B, uint3
 #pragma unroll
     for (int r = 0; r < 16; ++r) x[r] = src[256 * r];
   }
+}
+
+// The 12 stages on values already loaded by fwd_load; lt: the block's
+// staged twiddles (visible to every thread), b: psi_rev[(N + B) / 2 + 8 t].
+__device__ __forceinline__ void fwd_transform(const double2* lt, double b, double q, double qinv,
+                                              double* lds, double (&x)[16]) {
+  const uint32_t t = threadIdx.x, a = t >> 4, bb = t & 15;
   // bits 11..8
-  ct_st<8, true>(x, TwHi{tw, nb >> 12}, q, qinv);
-  ct_st<4, false>(x, TwHi{tw, nb >> 11}, q, qinv);
-  ct_st<2, true>(x, TwHi{tw, nb >> 10}, q, qinv);
-  ct_st<1, false>(x, TwHi{tw, nb >> 9}, q, qinv);
+  ct_st<8, true>(x, TwL{lt, 0}, q, qinv);
+  ct_st<4, false>(x, TwL{lt, 1}, q, qinv);
+  ct_st<2, true>(x, TwL{lt, 3}, q, qinv);
+  ct_st<1, false>(x, TwL{lt, 7}, q, qinv);
 #pragma unroll
   for (int r = 0; r < 16; ++r) lds[lds_row(t, r)] = x[r];
   __syncthreads();
 #pragma unroll
-  for (int r = 0; r < 16; ++r) x[r] = lds[lds_mid(a, b, r)];
+  for (int r = 0; r < 16; ++r) x[r] = lds[lds_mid(a, bb, r)];
   // bits 7..4
-  ct_st<8, true>(x, TwHi{tw, (nb >> 8) + a}, q, qinv);
-  ct_st<4, false>(x, TwHi{tw, (nb >> 7) + 2 * a}, q, qinv);
-  ct_st<2, true>(x, TwHi{tw, (nb >> 6) + 4 * a}, q, qinv);
-  ct_st<1, false>(x, TwHi{tw, (nb >> 5) + 8 * a}, q, qinv);
+  ct_st<8, true>(x, TwL{lt, 15 + a}, q, qinv);
+  ct_st<4, false>(x, TwL{lt, 31 + 2 * a}, q, qinv);
+  ct_st<2, true>(x, TwL{lt, 63 + 4 * a}, q, qinv);
+  ct_st<1, false>(x, TwL{lt, 127 + 8 * a}, q, qinv);
 #pragma unroll
-  for (int r = 0; r < 16; ++r) lds[lds_mid(a, b, r)] = x[r];
+  for (int r = 0; r < 16; ++r) lds[lds_mid(a, bb, r)] = x[r];
   __syncthreads();
 #pragma unroll
   for (int r = 0; r < 16; ++r) x[r] = lds[lds_col(t, r)];
   // bits 3..0
-  ct_st<8, true>(x, TwLo<8>{s3, qinv}, q, qinv);
-  ct_st<4, false>(x, TwLo<4>{s3, qinv}, q, qinv);
-  ct_st<2, true>(x, TwLo<2>{s3, qinv}, q, qinv);
-  ct_st<1, false>(x, TwLo<1>{s3, qinv}, q, qinv);
+  const double b2 = sq_bal(b, q, qinv), b4 = sq_bal(b2, q, qinv);
+  ct_st<8, true>(x, TwGen{sq_bal(b4, q, qinv), lt + 255, q, qinv}, q, qinv);
+  ct_st<4, false>(x, TwGen{b4, lt + 255, q, qinv}, q, qinv);
+  ct_st<2, true>(x, TwGen{b2, lt + 255, q, qinv}, q, qinv);
+  ct_st<1, false>(x, TwGen{b, lt + 255, q, qinv}, q, qinv);
 }
 
 // An epilogue with nothing to load ahead of the transform.
@@ -452,19 +481,22 @@ struct NoPre {};
 
 // Forward 4096-point blocks.  Thread t starts with values t + 256 r (bits
 // 11..8 in registers), moves to a*256 + 16 r + b (a = t/16, b = t%16; bits
-// 7..4) and to 16 t + r (bits 3..0); fwd_block ends there.  Each transpose
+// 7..4) and to 16 t + r (bits 3..0); fwd_transform ends there.  Each transpose
 // writes exactly the LDS words the thread read in the previous one, so only
 // the reads need a barrier.  The kernel hands values t + 256 r to the
 // epilogue.
 //
 // SINGLE: N = 4096, the pass reads uint64 residues; otherwise it reads the
-// outer pass's fp64 intermediate.
+// outer pass's fp64 intermediate.  No global load is waited on inside the
+// transform: the block's twiddles of bits 11..4 are staged in LDS with the
+// data loads, those of bits 3..0 generated from one loaded power.
 template <bool SINGLE, class Epi>
 __global__ __launch_bounds__(kThreads) void k_fwd_inner(RowSel rs, uint32_t log_n,
                                                         const PrimeK* __restrict__ pk,
                                                         const double2* __restrict__ twf,
                                                         const double* __restrict__ tw3, Epi epi) {
   __shared__ double lds[kLds];
+  __shared__ double2 lt[kTwL];
   if (rs.skip()) return;
   const uint32_t n = 1u << log_n;
   const uint32_t prime = rs.prime();
@@ -472,12 +504,18 @@ __global__ __launch_bounds__(kThreads) void k_fwd_inner(RowSel rs, uint32_t log_
   uint64_t* row = rs.row();
   const uint32_t t = threadIdx.x;
   const uint32_t B = blockIdx.x * kBlock;
-  const double* s3 = tw3 + ((size_t)prime * (n / kBlock) + blockIdx.x) * (15 * kThreads) + t;
+  const double2* tw = twf + (size_t)prime * n;
+  if (t < 255) lt[t] = block_twiddle(tw, n + B, t);
+  if (t < 7) lt[255 + t] = tw[t + 1];
+  // psi_rev[(N + B) / 2 + 8 t]
+  const double b = tw3[((size_t)prime * (n / kBlock) + blockIdx.x) * kThreads + t];
   // operands of the epilogue loaded before the transform, so that their
   // latency overlaps the butterflies
   const typename Epi::Pre pv = epi.pre(B + t, n);
   double x[16];
-  fwd_block<SINGLE>(row, B, n, twf + (size_t)prime * n, s3, q, qinv, lds, x);
+  fwd_load<SINGLE>(row, B, x);
+  __syncthreads();
+  fwd_transform(lt, b, q, qinv, lds, x);
 #pragma unroll
   for (int r = 0; r < 16; ++r) lds[lds_col(t, r)] = x[r];
   __syncthreads();
@@ -535,7 +573,8 @@ struct LoadSources {
   }
 };
 
-// Inverse 4096-point blocks: the mirror image of k_fwd_inner.  Reads uint64
+// Inverse 4096-point blocks: the mirror image of k_fwd_inner (twiddles of
+// bits 11..4 staged in LDS, those of bits 3..0 generated).  Reads uint64
 // residues (16 consecutive values per thread), writes fp64 for the outer pass
 // or, if SINGLE, applies the final store St.
 template <bool SINGLE, class Ld, class St>
@@ -545,6 +584,7 @@ __global__ __launch_bounds__(kThreads) void k_inv_inner(RowSel rs, uint32_t log_
                                                         const double* __restrict__ tw3, Ld ld,
                                                         St st) {
   __shared__ double lds[kLds];
+  __shared__ double2 lt[kTwL];
   if (rs.skip()) return;
   const uint32_t n = 1u << log_n;
   const uint32_t prime = rs.prime();
@@ -553,35 +593,40 @@ __global__ __launch_bounds__(kThreads) void k_inv_inner(RowSel rs, uint32_t log_
   const double2* tw = twi + (size_t)prime * n;
   uint64_t* row = rs.row();
   const uint32_t t = threadIdx.x, a = t >> 4, b = t & 15;
-  const uint32_t B = blockIdx.x * kBlock, nb = n + B;
+  const uint32_t B = blockIdx.x * kBlock;
+  if (t < 255) lt[t] = block_twiddle(tw, n + B, t);
+  if (t < 7) lt[255 + t] = tw[t + 1];
+  // psi_rev[(N + B) / 2 + 8 t] (inverse powers)
+  const double b1 = tw3[((size_t)prime * (n / kBlock) + blockIdx.x) * kThreads + t];
   double x[16];
   ld(row, B + 16 * t, x, q, qinv);
+  __syncthreads();
   // bits 3..0
-  const double* s3 = tw3 + ((size_t)prime * (n / kBlock) + blockIdx.x) * (15 * kThreads) + t;
-  gs_st<1, true>(x, TwLo<1>{s3, qinv}, q, qinv);
-  gs_st<2, false>(x, TwLo<2>{s3, qinv}, q, qinv);
-  gs_st<4, true>(x, TwLo<4>{s3, qinv}, q, qinv);
-  gs_st<8, false>(x, TwLo<8>{s3, qinv}, q, qinv);
+  const double b2 = sq_bal(b1, q, qinv), b4 = sq_bal(b2, q, qinv);
+  gs_st<1, true>(x, TwGen{b1, lt + 255, q, qinv}, q, qinv);
+  gs_st<2, false>(x, TwGen{b2, lt + 255, q, qinv}, q, qinv);
+  gs_st<4, true>(x, TwGen{b4, lt + 255, q, qinv}, q, qinv);
+  gs_st<8, false>(x, TwGen{sq_bal(b4, q, qinv), lt + 255, q, qinv}, q, qinv);
 #pragma unroll
   for (int r = 0; r < 16; ++r) lds[lds_col(t, r)] = x[r];
   __syncthreads();
 #pragma unroll
   for (int r = 0; r < 16; ++r) x[r] = lds[lds_mid(a, b, r)];
   // bits 7..4
-  gs_st<1, true>(x, TwHi{tw, (nb >> 5) + 8 * a}, q, qinv);
-  gs_st<2, false>(x, TwHi{tw, (nb >> 6) + 4 * a}, q, qinv);
-  gs_st<4, true>(x, TwHi{tw, (nb >> 7) + 2 * a}, q, qinv);
-  gs_st<8, false>(x, TwHi{tw, (nb >> 8) + a}, q, qinv);
+  gs_st<1, true>(x, TwL{lt, 127 + 8 * a}, q, qinv);
+  gs_st<2, false>(x, TwL{lt, 63 + 4 * a}, q, qinv);
+  gs_st<4, true>(x, TwL{lt, 31 + 2 * a}, q, qinv);
+  gs_st<8, false>(x, TwL{lt, 15 + a}, q, qinv);
 #pragma unroll
   for (int r = 0; r < 16; ++r) lds[lds_mid(a, b, r)] = x[r];
   __syncthreads();
 #pragma unroll
   for (int r = 0; r < 16; ++r) x[r] = lds[lds_row(t, r)];
   // bits 11..8
-  gs_st<1, true>(x, TwHi{tw, nb >> 9}, q, qinv);
-  gs_st<2, false>(x, TwHi{tw, nb >> 10}, q, qinv);
-  gs_st<4, true>(x, TwHi{tw, nb >> 11}, q, qinv);
-  gs_st<8, false>(x, TwHi{tw, nb >> 12}, q, qinv);
+  gs_st<1, true>(x, TwL{lt, 7}, q, qinv);
+  gs_st<2, false>(x, TwL{lt, 3}, q, qinv);
+  gs_st<4, true>(x, TwL{lt, 1}, q, qinv);
+  gs_st<8, false>(x, TwL{lt, 0}, q, qinv);
   if constexpr (SINGLE) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) st(row, B + t + 256 * r, x[r], P);
@@ -715,13 +760,15 @@ hipError_t launch_inv_outer(const Context* c, const RowSel& rs, uint32_t batch, 
 template <class Epi>
 hipError_t launch_fwd_inner(const Context* c, const RowSel& rs, uint32_t batch, uint32_t limbs,
                             const Epi& epi, hipStream_t s) {
-  const dim3 grid(c->n / kBlock, batch, limbs), blk(kThreads);
-  if (c->log_n == 12)
-    k_fwd_inner<true, Epi><<<grid, blk, 0, s>>>(rs, c->log_n, c->d_pk, c->d_tw_fwd,
-                                                 c->d_tw3_fwd, epi);
-  else
-    k_fwd_inner<false, Epi><<<grid, blk, 0, s>>>(rs, c->log_n, c->d_pk, c->d_tw_fwd,
-                                                  c->d_tw3_fwd, epi);
+  const uint32_t nblk = c->n / kBlock;
+  const dim3 blk(kThreads);
+  if (c->log_n == 12) {
+    k_fwd_inner<true, Epi><<<dim3(nblk, batch, limbs), blk, 0, s>>>(
+        rs, c->log_n, c->d_pk, c->d_tw_fwd, c->d_tw3_fwd, epi);
+  } else {
+    k_fwd_inner<false, Epi><<<dim3(nblk, batch, limbs), blk, 0, s>>>(
+        rs, c->log_n, c->d_pk, c->d_tw_fwd, c->d_tw3_fwd, epi);
+  }
   return hipGetLastError();
 }
 
