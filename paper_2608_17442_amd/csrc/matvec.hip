@@ -45,13 +45,15 @@ constexpr int kThreads = 256;  // also the coefficient tile of the diagonal bank
 constexpr int kGroup = 16;     // outputs accumulated per thread
 
 // Diagonal (o, t) of a bank: tiles of kThreads coefficients, ordered
-// [limb][tile][output][term][coefficient], so that one workgroup streams a
-// contiguous G * terms * 2 KB region.
+// [limb][tile][term][output][coefficient]: for each term a workgroup reads
+// its G outputs' tiles as one contiguous G * 2 KB run, and the output groups
+// of one tile (kept on one XCD, adjacent in time) sweep one contiguous
+// terms * outputs * 2 KB region together.
 __host__ __device__ __forceinline__ size_t bank_offset(uint32_t i, uint32_t tile, uint32_t o,
                                                        uint32_t t, uint32_t n,
                                                        uint32_t n_outputs, uint32_t terms) {
   const size_t tiles = n / kThreads;
-  return ((((size_t)i * tiles + tile) * n_outputs + o) * terms + t) * kThreads;
+  return ((((size_t)i * tiles + tile) * terms + t) * n_outputs + o) * kThreads;
 }
 
 // BANK: diagonals from a tiled bank; otherwise from the table of plaintexts.
@@ -90,7 +92,7 @@ __global__ __launch_bounds__(kThreads) void k_ptmac(const uint64_t* const* __res
   const size_t pi = (size_t)i * n + k, c0 = (size_t)2 * i * n + k, c1 = c0 + n;
   const uint64_t* bk =
       BANK ? bank + bank_offset(i, tile, o0, 0, n, n_outputs, terms) + threadIdx.x : nullptr;
-  const size_t o_stride = (size_t)terms * kThreads;
+  const size_t t_stride = (size_t)n_outputs * kThreads;
   // Outputs past the end of a partial group re-read the group's last valid
   // diagonal (results discarded at the store), which keeps the loop body free
   // of branches so the G loads of a term are issued together.
@@ -102,7 +104,7 @@ __global__ __launch_bounds__(kThreads) void k_ptmac(const uint64_t* const* __res
     const double x0 = u2d(bp[c0]), x1 = u2d(bp[c1]);
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      const double w = BANK ? u2d(bk[og[g] * o_stride + (size_t)t * kThreads])
+      const double w = BANK ? u2d(bk[(size_t)t * t_stride + og[g] * kThreads])
                             : u2d(diag[(size_t)(o0 + og[g]) * terms + t][pi]);
       a0[g] += mm_var(x0, w, P.q, P.qinv);
       a1[g] += mm_var(x1, w, P.q, P.qinv);
