@@ -195,7 +195,7 @@ struct InvDigit {
 // Inverse: stages in reverse order (every other one reducing, as in gs_st),
 // then the final store (N^-1 scaling included).
 template <int LOGM, class St>
-__global__ __launch_bounds__(kThreads) void k_inv_outer(RowSel rs, uint32_t log_n,
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(5))) void k_inv_outer(RowSel rs, uint32_t log_n,
                                                         const PrimeK* __restrict__ pk,
                                                         const double2* __restrict__ twi, St st) {
   constexpr int M = 1 << LOGM, C = 16 / M;
