@@ -102,6 +102,18 @@ __global__ __launch_bounds__(kThreads) void k_conv_acc(ConvTable tab, const uint
 // multiplication by X^m: the evaluation at psi^(2 brv(j) + 1) scales by
 // psi^e, e = (2 brv(j) + 1) m mod 2N; psi^e = tw[brv(e)] for e < N and
 // -tw[brv(e - N)] otherwise (tw = forward twiddle table).
+// Evaluation of X^m at the point of index k (prime i): the value psi^e,
+// e = (2 brv(k) + 1) m mod 2N, as a table twiddle and a sign (psi^N = -1).
+__device__ __forceinline__ double2 monomial_w(uint32_t k, uint32_t m, uint32_t log_n, uint32_t i,
+                                              const double2* __restrict__ twf, bool* neg) {
+  const uint32_t n = 1u << log_n;
+  const uint32_t b = __builtin_bitreverse32(k) >> (32 - log_n);
+  const uint32_t e = ((2u * b + 1u) * m) & (2u * n - 1u);
+  *neg = e >= n;
+  const uint32_t eb = __builtin_bitreverse32(*neg ? e - n : e) >> (32 - log_n);
+  return twf[(size_t)i * n + eb];
+}
+
 __global__ __launch_bounds__(kThreads) void k_monomial(const uint64_t* in, uint64_t* out,
                                                        uint32_t log_n, uint32_t m,
                                                        const PrimeK* __restrict__ pk,
@@ -111,14 +123,37 @@ __global__ __launch_bounds__(kThreads) void k_monomial(const uint64_t* in, uint6
   const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
   if (k >= n) return;
   const PrimeK P = pk[i];
-  const uint32_t b = __builtin_bitreverse32(k) >> (32 - log_n);
-  const uint32_t e = ((2u * b + 1u) * m) & (2u * n - 1u);
-  const bool neg = e >= n;
-  const uint32_t eb = __builtin_bitreverse32(neg ? e - n : e) >> (32 - log_n);
-  const double2 w = twf[(size_t)i * n + eb];
+  bool neg;
+  const double2 w = monomial_w(k, m, log_n, i, twf, &neg);
   const size_t o = (size_t)r * n + k;
   double v = mm_shoup(ld(in + o), w.x, w.y, P.q);
   st(out + o, neg ? -v : v, P.q, P.qinv);
+}
+
+// Pair blockIdx.z of the table, row blockIdx.y (limb r / 2, component r % 2).
+// X^(N/2) and X^(3N/2) evaluate to -+ psi^(N/2) at every point, so the
+// monomial is one Shoup product and a sign.
+__global__ __launch_bounds__(kThreads) void k_pair(PairTable tab, bool split, uint32_t log_n,
+                                                   const PrimeK* __restrict__ pk,
+                                                   const double2* __restrict__ twf) {
+  const uint32_t n = 1u << log_n;
+  const uint32_t r = blockIdx.y, i = r >> 1, j = blockIdx.z;
+  const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
+  if (k >= n) return;
+  const PrimeK P = pk[i];
+  const size_t o = (size_t)r * n + k;
+  bool neg;
+  if (!split) {
+    const double2 w = monomial_w(k, n / 2, log_n, i, twf, &neg);
+    const double v = mm_shoup(ld(tab.y[j] + o), w.x, w.y, P.q);
+    st(tab.x[j] + o, ld(tab.x[j] + o) + (neg ? -v : v), P.q, P.qinv);
+  } else {
+    const double a = ld(tab.x[j] + o), b = ld(tab.y[j] + o);
+    const double2 w = monomial_w(k, 3 * n / 2, log_n, i, twf, &neg);
+    const double v = mm_shoup(a - b, w.x, w.y, P.q);
+    st(tab.first[j] + o, a + b, P.q, P.qinv);
+    st(tab.second[j] + o, neg ? -v : v, P.q, P.qinv);
+  }
 }
 
 // out[row][k] = in[row][galois_src(k)]; rows share one prime list (prime of
@@ -235,6 +270,15 @@ hipError_t k_monomial_launch(const Context* c, const uint64_t* in, uint64_t* out
                              uint32_t level, uint32_t m, hipStream_t s) {
   hipLaunchKernelGGL(k_monomial, grid_rows(c->n, 2 * level), dim3(kThreads), 0, s, in, out,
                      c->log_n, m, c->d_pk, c->d_tw_fwd);
+  return hipGetLastError();
+}
+
+hipError_t k_pair_launch(const Context* c, const PairTable& tab, uint32_t count, bool split,
+                         uint32_t level, hipStream_t s) {
+  if (count == 0) return hipSuccess;
+  if (count > kPairBatch) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_pair, grid_rows(c->n, 2 * level, count), dim3(kThreads), 0, s, tab, split,
+                     c->log_n, c->d_pk, c->d_tw_fwd);
   return hipGetLastError();
 }
 

@@ -78,12 +78,27 @@ int op_scan_contract(Context* c, const uint64_t* const* h, const uint64_t* const
     }
   }
   const std::vector<uint64_t*> first = x;  // where out_2l (or the odd output) lives
+  // pair entries (an odd chunk has none), kPairBatch per launch
+  auto pairs = [&](bool split) -> int {
+    PairTable tab{};
+    uint32_t m = 0;
+    for (uint32_t r = 0; r < R * T; ++r) {
+      if (K % 2 && r % R == P) continue;
+      tab.x[m] = x[r];
+      tab.y[m] = y[r];
+      // out_2l goes to the buffer it started in, out_2l+1 to the other
+      tab.first[m] = first[r];
+      tab.second[m] = first[r] == x[r] ? y[r] : x[r];
+      if (++m == kPairBatch) {
+        HIPCK(k_pair_launch(c, tab, m, split, lo, s));
+        m = 0;
+      }
+    }
+    if (m) HIPCK(k_pair_launch(c, tab, m, split, lo, s));
+    return FESC_OK;
+  };
   // chi_l = t_2l + i t_2l+1 (i = X^(N/2)), formed in x
-  for (uint32_t r = 0; r < R * T; ++r) {
-    if (K % 2 && r % R == P) continue;
-    HIPCK(k_monomial_launch(c, y[r], y[r], lo, c->n / 2, s));
-    HIPCK(k_binary_launch(c, x[r], y[r], x[r], 2 * lo, 1, 0, s));
-  }
+  if ((err = pairs(false))) return err;
   for (uint32_t st = d_s / 2; st >= 1; st /= 2) {
     const std::vector<int32_t> steps(R * T, (int32_t)st);
     // y = x + rot(x, st)
@@ -103,22 +118,8 @@ int op_scan_contract(Context* c, const uint64_t* const* h, const uint64_t* const
                                lo, s)))
       return err;
     // out_2l = chi + conj(chi);  out_2l+1 = -i (chi - conj(chi)) = X^(3N/2) (chi - conj(chi)),
-    // in place in the pair's two buffers (A = chi, B = conj(chi))
-    for (uint32_t r = 0; r < R * T; ++r) {
-      if (K % 2 && r % R == P) continue;
-      uint64_t *A = x[r], *B = y[r];
-      if (A == first[r]) {                                    // A -> out_2l, B -> out_2l+1
-        HIPCK(k_binary_launch(c, A, B, B, 2 * lo, 1, 1, s));  // B = chi - cj
-        HIPCK(k_binary_launch(c, A, A, A, 2 * lo, 1, 0, s));  // A = 2 chi
-        HIPCK(k_binary_launch(c, A, B, A, 2 * lo, 1, 1, s));  // A = chi + cj
-        HIPCK(k_monomial_launch(c, B, B, lo, 3 * c->n / 2, s));
-      } else {                                                // B -> out_2l, A -> out_2l+1
-        HIPCK(k_binary_launch(c, A, B, A, 2 * lo, 1, 1, s));  // A = chi - cj
-        HIPCK(k_binary_launch(c, B, B, B, 2 * lo, 1, 0, s));  // B = 2 cj
-        HIPCK(k_binary_launch(c, B, A, B, 2 * lo, 1, 0, s));  // B = chi + cj
-        HIPCK(k_monomial_launch(c, A, A, lo, 3 * c->n / 2, s));
-      }
-    }
+    // in place in the pair's two buffers (x = chi, y = conj(chi))
+    if ((err = pairs(true))) return err;
   }
   if (K % 2)
     for (uint32_t u = 0; u < T; ++u) {

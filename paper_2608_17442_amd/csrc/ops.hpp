@@ -24,6 +24,20 @@ struct ConvTable {
 };
 hipError_t k_conv_acc_launch(const Context* c, const ConvTable& tab, const uint64_t* bias,
                              uint64_t* acc, uint32_t level, hipStream_t s);
+// Complex pairing of real ciphertexts, up to kPairBatch pairs per launch.
+// pack (split = false): x[r] = x[r] + X^(N/2) y[r];
+// split (split = true): with A = x[r], B = y[r] read first,
+//   first[r] = A + B,  second[r] = X^(3N/2) (A - B),
+// where {first[r], second[r]} = {x[r], y[r]} (in place, element by element).
+constexpr uint32_t kPairBatch = 64;
+struct PairTable {
+  uint64_t* x[kPairBatch];
+  uint64_t* y[kPairBatch];
+  uint64_t* first[kPairBatch];
+  uint64_t* second[kPairBatch];
+};
+hipError_t k_pair_launch(const Context* c, const PairTable& tab, uint32_t count, bool split,
+                         uint32_t level, hipStream_t s);
 hipError_t k_monomial_launch(const Context* c, const uint64_t* in, uint64_t* out,
                              uint32_t level, uint32_t m, hipStream_t s);
 hipError_t k_galois_launch(const Context* c, const uint64_t* in, uint64_t* out, uint32_t rows,
