@@ -200,3 +200,25 @@ def test_hescan_layer_full_size():
             err = np.max(np.abs(dec - ref[t, k * c_state:(k + 1) * c_state]))
             print(f"full-size layer token {t} chunk {k}: max |decoded - fp64| = {err:.3e}")
             assert err <= 2.0 ** -15
+
+
+def test_scan_contract_errors(small):
+    """Argument errors, all rejected before any launch."""
+    S, P = small, small.P
+    z = lambda lvl, k=1: [torch.zeros(lvl * 2 * P.n, dtype=torch.int64, device="cuda")
+                          for _ in range(k)]
+    h, c, o = z(4, 2), z(4, 2), z(3, 2)
+    with pytest.raises(F.FescError, match="distinct"):
+        S.ctx.scan_contract(h, None, c, 8, [o[0], o[0]], 4)
+    with pytest.raises(F.FescError, match="alias"):
+        S.ctx.scan_contract(h, None, c, 8, [o[0], h[1]], 4)
+    with pytest.raises(F.FescError, match="32 tokens"):      # odd chunk count, 33 tokens
+        S.ctx.scan_contract(z(4, 33), None, z(4, 33), 8, z(3, 33), 4, tokens=33)
+    with pytest.raises(F.FescError):                         # decay product needs level >= 3
+        S.ctx.scan_contract(z(2, 2), z(2, 2), z(2, 2), 8, z(1, 2), 2)
+    with pytest.raises(F.FescError):                         # contraction needs level >= 2
+        S.ctx.scan_contract(z(1, 2), None, z(1, 2), 8, z(1, 2), 1)
+    with pytest.raises(F.FescError, match="rotation 8"):     # d_state 16: no key for step 8
+        S.ctx.scan_contract(h, None, c, 16, o, 4)
+    with pytest.raises(F.FescError, match="bad scan-contract"):
+        S.ctx.scan_contract(h, None, c, 6, o, 4)
