@@ -104,7 +104,7 @@ int calib_valu(Context* c, int kind, uint32_t iters, double* rate, hipStream_t s
   hipEvent_t e0, e1;
   if (int rc = hip_check(hipEventCreate(&e0), "hipEventCreate")) return rc;
   if (int rc = hip_check(hipEventCreate(&e1), "hipEventCreate")) {
-    hipEventDestroy(e0);
+    (void)hipEventDestroy(e0);
     return rc;
   }
   auto launch = [&]() {
@@ -118,14 +118,16 @@ int calib_valu(Context* c, int kind, uint32_t iters, double* rate, hipStream_t s
       hipLaunchKernelGGL(k_calib_mac, dim3(blocks), dim3(kThreads), 0, s, q, qinv, iters, out);
   };
   launch();  // warm-up
-  hipEventRecord(e0, s);
-  launch();
-  hipEventRecord(e1, s);
-  int rc = hip_check(hipEventSynchronize(e1), "hipEventSynchronize");
+  int rc = hip_check(hipGetLastError(), "calibration launch");
+  if (!rc) rc = hip_check(hipEventRecord(e0, s), "hipEventRecord");
+  if (!rc) launch();
+  if (!rc) rc = hip_check(hipGetLastError(), "calibration launch");
+  if (!rc) rc = hip_check(hipEventRecord(e1, s), "hipEventRecord");
+  if (!rc) rc = hip_check(hipEventSynchronize(e1), "hipEventSynchronize");
   float ms = 0.f;
   if (!rc) rc = hip_check(hipEventElapsedTime(&ms, e0, e1), "hipEventElapsedTime");
-  hipEventDestroy(e0);
-  hipEventDestroy(e1);
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
   if (rc) return rc;
   const double per_thread = kind == FESC_CALIB_MAC ? 8.0 * iters : 32.0 * iters;
   *rate = (double)blocks * kThreads * per_thread / (ms * 1e-3);

@@ -167,8 +167,8 @@ void* scratch_get(Context* c, size_t bytes, int* err) {
   if (bytes <= c->scratch_bytes) return c->scratch;
   if (c->scratch) {
     // previous users on the context's stream may still read it
-    hipDeviceSynchronize();
-    hipFree(c->scratch);
+    if ((*err = hip_check(hipDeviceSynchronize(), "hipDeviceSynchronize"))) return nullptr;
+    (void)hipFree(c->scratch);
     c->scratch = nullptr;
     c->scratch_bytes = 0;
   }
@@ -261,17 +261,17 @@ static int build_tables(Context* c) {
 
 void destroy(Context* c) {
   if (!c) return;
-  hipDeviceSynchronize();
-  for (auto& kv : c->keys) hipFree(kv.second);
-  for (auto& kv : c->level_tabs) hipFree(kv.second.base);
-  hipFree(c->d_pk);
-  hipFree(c->d_tw_fwd);
-  hipFree(c->d_tw_inv);
-  hipFree(c->d_tw3_fwd);
-  hipFree(c->d_tw3_inv);
-  hipFree(c->d_enc_tw);
-  hipFree(c->d_enc_inv);
-  hipFree(c->scratch);
+  (void)hipDeviceSynchronize();
+  for (auto& kv : c->keys) (void)hipFree(kv.second);
+  for (auto& kv : c->level_tabs) (void)hipFree(kv.second.base);
+  (void)hipFree(c->d_pk);
+  (void)hipFree(c->d_tw_fwd);
+  (void)hipFree(c->d_tw_inv);
+  (void)hipFree(c->d_tw3_fwd);
+  (void)hipFree(c->d_tw3_inv);
+  (void)hipFree(c->d_enc_tw);
+  (void)hipFree(c->d_enc_inv);
+  (void)hipFree(c->scratch);
   delete static_cast<fesc_ctx*>(c);
 }
 
@@ -299,7 +299,10 @@ int create(const fesc_params* p, fesc_ctx** out) {
       if (primes[j] == q) return fail(FESC_ERR_ARG, "primes must be distinct");
   }
   fesc_ctx* c = new fesc_ctx();
-  hipGetDevice(&c->device);
+  if (int rc = hip_check(hipGetDevice(&c->device), "hipGetDevice")) {
+    delete c;
+    return rc;
+  }
   c->log_n = p->log_n;
   c->n = 1u << p->log_n;
   c->L = p->num_q;

@@ -197,28 +197,31 @@ int matvec_plan_create(Context* c, const fesc_matvec_desc* d, const uint64_t* co
              hipSuccess &&
          hipMemcpy(p->d_ct, cts.data(), n_ct * sizeof(void*), hipMemcpyHostToDevice) == hipSuccess;
   }
+  if (ok)
+    for (auto& e : p->ev) ok = ok && hipEventCreate(&e) == hipSuccess;
   if (!ok) {
-    hipFree(p->work);
-    hipFree(p->d_diag);
-    hipFree(p->d_baby);
-    hipFree(p->d_ct);
+    for (auto& e : p->ev)
+      if (e) (void)hipEventDestroy(e);
+    (void)hipFree(p->work);
+    (void)hipFree(p->d_diag);
+    (void)hipFree(p->d_baby);
+    (void)hipFree(p->d_ct);
     delete p;
-    return fail(FESC_ERR_OOM, "matvec workspace allocation failed");
+    return fail(FESC_ERR_OOM, "matvec workspace or event allocation failed");
   }
-  for (auto& e : p->ev) hipEventCreate(&e);
   *out = p;
   return FESC_OK;
 }
 
 void matvec_plan_destroy(fesc_matvec_plan* p) {
   if (!p) return;
-  hipDeviceSynchronize();
-  hipFree(p->work);
-  hipFree(p->d_diag);
-  hipFree(p->d_baby);
-  hipFree(p->d_ct);
+  (void)hipDeviceSynchronize();
+  (void)hipFree(p->work);
+  (void)hipFree(p->d_diag);
+  (void)hipFree(p->d_baby);
+  (void)hipFree(p->d_ct);
   for (auto& e : p->ev)
-    if (e) hipEventDestroy(e);
+    if (e) (void)hipEventDestroy(e);
   delete p;
 }
 

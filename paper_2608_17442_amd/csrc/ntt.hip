@@ -918,7 +918,7 @@ hipError_t launch_ntt_rows(const Context* c, const RowSel& rs, uint32_t batch, u
 hipError_t launch_ntt(const Context* c, uint64_t* d, uint32_t batch, size_t batch_stride,
                       uint32_t limbs, size_t limb_stride, uint32_t prime0, bool inverse,
                       hipStream_t s) {
-  RowSel rs{d, batch_stride, limb_stride, prime0, limbs, 0, 0, 0};
+  RowSel rs{d, batch_stride, limb_stride, prime0, limbs, 0, 0, 0, 0};
   return launch_ntt_rows(c, rs, batch, limbs, inverse, s);
 }
 

@@ -113,7 +113,7 @@ const LevelTables* level_tables(Context* c, uint32_t level, int* err) {
   }
   if ((*err = hip_check(hipMemcpy(d, all.data(), sizeof(double2) * all.size(),
                                   hipMemcpyHostToDevice), "hipMemcpy"))) {
-    hipFree(d);
+    (void)hipFree(d);
     return nullptr;
   }
   T.base = d;
