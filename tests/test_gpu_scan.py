@@ -121,11 +121,12 @@ def test_cfg5_one_token_full_size():
         assert err <= 2.0 ** -15
 
 
-@pytest.mark.parametrize("K,T", [(4, 3), (5, 2), (2, 17)])
+@pytest.mark.parametrize("K,T", [(4, 3), (5, 2), (2, 17), (2, 65)])
 def test_scan_contract_token_block(K, T):
     """Several tokens per call (the reduction batched over all of them, the
     outputs used as its workspace): every token equals the oracle's
-    one-token slice.  K = 2, T = 17 puts 17 pairs in each rotation batch."""
+    one-token slice.  K = 2, T = 17 puts 17 pairs in each rotation batch;
+    T = 65 crosses the 64-pair batches of the pairing kernel."""
     P = C.params_small(12, 50, 5, 2)
     d_s, head_dim, level = 8, 16, 4
     n_slots = P.n // 2
