@@ -366,6 +366,20 @@ int fesc_affine_scan_resident(fesc_ctx* ctx, const uint64_t* const* a, const uin
                               uint32_t level, void* workspace, size_t workspace_bytes,
                               void* stream);
 
+/* Host only (no context, no device): the products fesc_affine_scan_resident
+ * issues for one chunk of L tokens in blocks of `block`, recorded in issue
+ * order with placeholder addresses: 5 words per entry,
+ *     (group, x, y, add, out)   out = x * y (+ add; add = 0: none)
+ *     (group, src, 0, 0, dst)   a copy
+ * where the inputs a[k] and s[k] are 2^24 + k and 2 * 2^24 + k, the outputs
+ * h[k] are 3 * 2^24 + k, and workspace slots lie from 4 * 2^24 on.  Entries
+ * of one group are one batched call: all their operands are read before any
+ * of their outputs is written.  With words = NULL only *count is set;
+ * otherwise cap entries are available and FESC_ERR_ARG is returned (after
+ * *count is set) if the program has more.  1 <= block <= L <= 2^16. */
+int fesc_affine_scan_resident_program(uint32_t L, uint32_t block, uint64_t* words, size_t cap,
+                                      size_t* count);
+
 /* ------------------------------------------------------------------------
  * Small kernels on the same primitives.
  *

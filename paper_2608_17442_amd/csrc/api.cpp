@@ -128,6 +128,8 @@ int op_affine_scan(Context* c, uint64_t* const* a, uint64_t* const* s, uint32_t 
 int op_affine_scan_level(Context* c, uint32_t L, uint32_t level, bool states_only,
                          uint32_t* out_level, uint64_t* products);
 size_t affine_scan_network(uint32_t L, bool states_only, uint32_t* nodes, size_t cap);
+size_t affine_scan_resident_program(uint32_t L, uint32_t block, uint32_t level, uint64_t* words,
+                                    size_t cap, int* err);
 size_t affine_scan_resident_words(const Context* c, uint32_t L, uint32_t chunks, uint32_t block,
                                   uint32_t level);
 int op_affine_scan_resident_level(Context* c, uint32_t L, uint32_t block, uint32_t level,
@@ -386,6 +388,17 @@ int fesc_affine_scan_network(uint32_t L, uint32_t flags, uint32_t* nodes, size_t
     return fail(FESC_ERR_ARG, "bad scan-network arguments");
   *count = affine_scan_network(L, flags & FESC_SCAN_STATES_ONLY, nodes, cap);
   if (nodes && *count > cap) return fail(FESC_ERR_ARG, "node array too small");
+  return FESC_OK;
+}
+
+int fesc_affine_scan_resident_program(uint32_t L, uint32_t block, uint64_t* words, size_t cap,
+                                      size_t* count) {
+  if (!count || L == 0 || L > (1u << 16) || block == 0 || block > L)
+    return fail(FESC_ERR_ARG, "bad resident-program arguments");
+  int err = FESC_OK;
+  *count = affine_scan_resident_program(L, block, 64, words, cap, &err);
+  if (err) return err;
+  if (words && *count > cap) return fail(FESC_ERR_ARG, "program array too small");
   return FESC_OK;
 }
 

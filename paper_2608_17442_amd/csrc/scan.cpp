@@ -122,6 +122,21 @@ struct Seq {
   std::vector<uint64_t*> home_a, home_s;
 };
 
+// The products a driver issues, recorded instead of launched (host-side
+// verification of the schedule with placeholder buffer addresses): per
+// product (group, x, y, add or 0, out) for out = x y (+ add); a copy is
+// (group, src, 0, 0, dst).  Products of one group are one batched call, whose
+// operands are all read before any output is written.
+struct Program {
+  std::vector<uint64_t> words;
+  uint64_t group = 0;
+  void product(const uint64_t* x, const uint64_t* y, const uint64_t* add, const uint64_t* out) {
+    for (uint64_t w : {group, (uint64_t)(uintptr_t)x, (uint64_t)(uintptr_t)y,
+                       (uint64_t)(uintptr_t)add, (uint64_t)(uintptr_t)out})
+      words.push_back(w);
+  }
+};
+
 // Runs the stages over all chunks; lvl[] (shared by the chunks, which have
 // the same structure) tracks each position's level.  need_final[p]: the
 // caller wants position p's final decay (dead decay products are skipped).
@@ -131,7 +146,7 @@ struct Seq {
 // product groups.
 int run_stages(Context* c, const Stages& st, std::vector<Seq>& seqs, std::vector<uint32_t>& lvl,
                const std::vector<char>& need_final, bool dry, hipStream_t s,
-               uint64_t* nprod = nullptr) {
+               uint64_t* nprod = nullptr, Program* prog = nullptr) {
   const std::vector<std::vector<char>> live = live_decay(st, need_final);
   if (nprod)
     for (size_t i = 0; i < st.size(); ++i)
@@ -161,9 +176,14 @@ int run_stages(Context* c, const Stages& st, std::vector<Seq>& seqs, std::vector
             outs.push_back(q.home_a[nd.dst]);
             adds.push_back(nullptr);
           }
-        int err = op_prod_rescale_many(c, (uint32_t)xs.size(), xs.data(), ys.data(), outs.data(),
-                                       adds.data(), l, l - 1, s);
-        if (err) return err;
+        if (prog) {
+          for (size_t i = 0; i < xs.size(); ++i) prog->product(xs[i], ys[i], adds[i], outs[i]);
+          ++prog->group;
+        } else {
+          int err = op_prod_rescale_many(c, (uint32_t)xs.size(), xs.data(), ys.data(),
+                                         outs.data(), adds.data(), l, l - 1, s);
+          if (err) return err;
+        }
       }
       for (uint32_t j : kv.second) {
         const Node& nd = st[si][j];
@@ -257,9 +277,10 @@ size_t affine_scan_resident_words(const Context* c, uint32_t L, uint32_t chunks,
 static int resident(Context* c, const uint64_t* const* a, const uint64_t* const* s, uint32_t L,
                     uint32_t chunks, uint32_t block, uint64_t* const* h, uint32_t level,
                     uint32_t out_level, uint64_t* ws, bool dry, uint32_t* min_out,
-                    hipStream_t st, uint64_t* nprod = nullptr) {
+                    hipStream_t st, uint64_t* nprod = nullptr, Program* prog = nullptr) {
   const uint32_t K = (L + block - 1) / block;
-  const size_t W = (size_t)2 * level * c->n;
+  // recording: one placeholder word per workspace slot
+  const size_t W = prog ? 1 : (size_t)2 * level * c->n;
   const size_t per_chunk = (size_t)(2 * block + 2 * (K - 1)) * W;
   auto blk_a = [&](uint32_t ch, uint32_t t) { return ws + ch * per_chunk + (size_t)t * W; };
   auto blk_s = [&](uint32_t ch, uint32_t t) {
@@ -300,7 +321,7 @@ static int resident(Context* c, const uint64_t* const* a, const uint64_t* const*
     std::vector<uint32_t> lvl(block, level);
     std::vector<char> need(block, 0);
     need[block - 1] = sum_need[j];
-    if ((err = run_stages(c, summary_net, seqs, lvl, need, dry, st, nprod))) return err;
+    if ((err = run_stages(c, summary_net, seqs, lvl, need, dry, st, nprod, prog))) return err;
     lvl_sum.push_back(lvl[block - 1]);
     for (uint32_t ch = 0; ch < nseq; ++ch) {
       carry[ch].cur_a.push_back(seqs[ch].cur_a[block - 1]);
@@ -310,7 +331,8 @@ static int resident(Context* c, const uint64_t* const* a, const uint64_t* const*
     }
   }
   // exclusive scan over the summaries: G_j = carry position j - 1
-  if (K > 1 && (err = run_stages(c, carry_net, carry, lvl_sum, carry_need, dry, st, nprod)))
+  if (K > 1 &&
+      (err = run_stages(c, carry_net, carry, lvl_sum, carry_need, dry, st, nprod, prog)))
     return err;
   // pass 2: replay and carry injection
   uint32_t lo = level;
@@ -321,15 +343,21 @@ static int resident(Context* c, const uint64_t* const* a, const uint64_t* const*
     std::vector<uint32_t> lvl(Bj, level);
     // block 0 gives states; later blocks' decays enter the carry injection
     const std::vector<char> need(Bj, j == 0 ? 0 : 1);
-    if ((err = run_stages(c, bk_network(Bj), seqs, lvl, need, dry, st, nprod))) return err;
+    if ((err = run_stages(c, bk_network(Bj), seqs, lvl, need, dry, st, nprod, prog))) return err;
     if (j == 0) {
       lo = std::min(lo, min_level(lvl));
       if (!dry)
         for (uint32_t ch = 0; ch < chunks; ++ch)
-          for (uint32_t t = 0; t < Bj; ++t)
+          for (uint32_t t = 0; t < Bj; ++t) {
+            if (prog) {
+              prog->product(seqs[ch].cur_s[t], nullptr, nullptr, h[(size_t)ch * L + t]);
+              ++prog->group;
+              continue;
+            }
             HIPCK_RET(hipMemcpyAsync(h[(size_t)ch * L + t], seqs[ch].cur_s[t],
                                      (size_t)2 * out_level * c->n * 8, hipMemcpyDeviceToDevice,
                                      st));
+          }
       continue;
     }
     std::map<uint32_t, std::vector<uint32_t>> by_level;
@@ -349,13 +377,39 @@ static int resident(Context* c, const uint64_t* const* a, const uint64_t* const*
           adds.push_back(seqs[ch].cur_s[t]);
           outs.push_back(h[(size_t)ch * L + (size_t)j * block + t]);
         }
-      if ((err = op_prod_rescale_many(c, (uint32_t)xs.size(), xs.data(), ys.data(), outs.data(),
-                                      adds.data(), l, out_level, st)))
+      if (prog) {
+        for (size_t i = 0; i < xs.size(); ++i) prog->product(xs[i], ys[i], adds[i], outs[i]);
+        ++prog->group;
+      } else if ((err = op_prod_rescale_many(c, (uint32_t)xs.size(), xs.data(), ys.data(),
+                                             outs.data(), adds.data(), l, out_level, st))) {
         return err;
+      }
     }
   }
   *min_out = lo;
   return FESC_OK;
+}
+
+size_t affine_scan_resident_program(uint32_t L, uint32_t block, uint32_t level, uint64_t* words,
+                                    size_t cap, int* err) {
+  // placeholder addresses (never dereferenced): inputs a, s, outputs h and the
+  // workspace each get their own range
+  const uint64_t A0 = 1u << 24, S0 = 2u << 24, H0 = 3u << 24, WS0 = 4u << 24;
+  std::vector<const uint64_t*> a(L), s(L);
+  std::vector<uint64_t*> h(L);
+  for (uint32_t k = 0; k < L; ++k) {
+    a[k] = reinterpret_cast<const uint64_t*>((uintptr_t)(A0 + k));
+    s[k] = reinterpret_cast<const uint64_t*>((uintptr_t)(S0 + k));
+    h[k] = reinterpret_cast<uint64_t*>((uintptr_t)(H0 + k));
+  }
+  Program prog;
+  uint32_t lo;
+  *err = resident(nullptr, a.data(), s.data(), L, 1, block, h.data(), level, 1,
+                  reinterpret_cast<uint64_t*>((uintptr_t)WS0), false, &lo, nullptr, nullptr,
+                  &prog);
+  if (words)
+    for (size_t i = 0; i < prog.words.size() && i < 5 * cap; ++i) words[i] = prog.words[i];
+  return prog.words.size() / 5;
 }
 
 int op_affine_scan_resident_level(Context* c, uint32_t L, uint32_t block, uint32_t level,

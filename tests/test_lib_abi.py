@@ -164,3 +164,41 @@ def test_affine_scan_network_matches_oracle(states_only):
         for k in range(L):
             h = (a0[k] * h + s0[k]) % prime
             assert s[k] == h, (L, k)
+
+
+@pytest.mark.parametrize("L,block", [(2048, 1024), (2048, 256), (2048, 64), (1000, 128),
+                                     (11, 4), (9, 3), (5, 5), (6, 1), (1, 1)])
+def test_resident_schedule_program_gives_the_recurrence(L, block):
+    """The library's resident two-pass driver, recorded on the host
+    (fesc_affine_scan_resident_program), replayed over GF(2^61 - 1): every
+    product out = x y (+ add) in issue order, in launches of 32 products whose
+    operands are all read before any output is written (a batched key
+    switch), a skipped decay never read.  Every state equals the sequential
+    recurrence h_k = a_k h_(k-1) + s_k, at the benchmark's L = 2048 with
+    blocks of 1024 and at ragged and degenerate shapes."""
+    import itertools
+    from paper_2608_17442_amd import fesc as F
+    prime = (1 << 61) - 1
+    A0, S0, H0 = 1 << 24, 2 << 24, 3 << 24
+    prog = F.affine_scan_resident_program(L, block)
+    rng = np.random.default_rng(L * 7919 + block)
+    a = [int(v) for v in rng.integers(1, prime, L)]
+    s = [int(v) for v in rng.integers(0, prime, L)]
+    mem = {A0 + k: a[k] for k in range(L)}
+    mem.update({S0 + k: s[k] for k in range(L)})
+    for _, group in itertools.groupby(prog, key=lambda e: e[0]):
+        group = list(group)
+        for i in range(0, len(group), 32):
+            sub = group[i:i + 32]
+            vals = []
+            for _, x, y, add, out in sub:
+                if y == 0:                                   # copy
+                    vals.append((out, mem[x]))
+                else:
+                    vals.append((out, (mem[x] * mem[y] + (mem[add] if add else 0)) % prime))
+            for out, v in vals:
+                mem[out] = v
+    h = 0
+    for k in range(L):
+        h = (a[k] * h + s[k]) % prime
+        assert mem[H0 + k] == h, (L, block, k)
