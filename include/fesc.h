@@ -366,6 +366,14 @@ int fesc_affine_scan_resident(fesc_ctx* ctx, const uint64_t* const* a, const uin
                               uint32_t level, void* workspace, size_t workspace_bytes,
                               void* stream);
 
+/* Host only (no context, no device): the products fesc_affine_scan issues
+ * for `chunks` sequences of L tokens (flags as there), in the format of
+ * fesc_affine_scan_resident_program below; a[c L + k] and s[c L + k] are
+ * 2^24 + c L + k and 2 * 2^24 + c L + k, and the scan runs in place over
+ * them.  chunks * L <= 2^20. */
+int fesc_affine_scan_program(uint32_t L, uint32_t chunks, uint32_t flags, uint64_t* words,
+                             size_t cap, size_t* count);
+
 /* Host only (no context, no device): the products fesc_affine_scan_resident
  * issues for one chunk of L tokens in blocks of `block`, recorded in issue
  * order with placeholder addresses: 5 words per entry,

@@ -130,6 +130,8 @@ int op_affine_scan_level(Context* c, uint32_t L, uint32_t level, bool states_onl
 size_t affine_scan_network(uint32_t L, bool states_only, uint32_t* nodes, size_t cap);
 size_t affine_scan_resident_program(uint32_t L, uint32_t block, uint32_t level, uint64_t* words,
                                     size_t cap, int* err);
+size_t affine_scan_program(uint32_t L, uint32_t chunks, bool states_only, uint32_t level,
+                           uint64_t* words, size_t cap, int* err);
 size_t affine_scan_resident_words(const Context* c, uint32_t L, uint32_t chunks, uint32_t block,
                                   uint32_t level);
 int op_affine_scan_resident_level(Context* c, uint32_t L, uint32_t block, uint32_t level,
@@ -388,6 +390,18 @@ int fesc_affine_scan_network(uint32_t L, uint32_t flags, uint32_t* nodes, size_t
     return fail(FESC_ERR_ARG, "bad scan-network arguments");
   *count = affine_scan_network(L, flags & FESC_SCAN_STATES_ONLY, nodes, cap);
   if (nodes && *count > cap) return fail(FESC_ERR_ARG, "node array too small");
+  return FESC_OK;
+}
+
+int fesc_affine_scan_program(uint32_t L, uint32_t chunks, uint32_t flags, uint64_t* words,
+                             size_t cap, size_t* count) {
+  if (!count || L == 0 || L > (1u << 16) || chunks == 0 || (uint64_t)chunks * L > (1u << 20) ||
+      (flags & ~FESC_SCAN_STATES_ONLY))
+    return fail(FESC_ERR_ARG, "bad scan-program arguments");
+  int err = FESC_OK;
+  *count = affine_scan_program(L, chunks, flags & FESC_SCAN_STATES_ONLY, 64, words, cap, &err);
+  if (err) return err;
+  if (words && *count > cap) return fail(FESC_ERR_ARG, "program array too small");
   return FESC_OK;
 }
 

@@ -235,9 +235,10 @@ int op_affine_scan_level(Context* c, uint32_t L, uint32_t level, bool states_onl
   return FESC_OK;
 }
 
-int op_affine_scan(Context* c, uint64_t* const* a, uint64_t* const* s, uint32_t L,
-                   uint32_t chunks, uint32_t level, bool states_only, uint32_t* out_level,
-                   hipStream_t st) {
+// The in-place scan of `chunks` sequences; prog: record instead of launch.
+static int scan_in_place(Context* c, uint64_t* const* a, uint64_t* const* s, uint32_t L,
+                         uint32_t chunks, uint32_t level, bool states_only, uint32_t* out_level,
+                         hipStream_t st, Program* prog) {
   const Stages net = bk_network(L);
   const std::vector<char> need(L, states_only ? 0 : 1);
   std::vector<uint32_t> lvl(L, level);
@@ -255,9 +256,15 @@ int op_affine_scan(Context* c, uint64_t* const* a, uint64_t* const* s, uint32_t 
     }
   }
   lvl.assign(L, level);
-  if ((err = run_stages(c, net, seqs, lvl, need, false, st))) return err;
+  if ((err = run_stages(c, net, seqs, lvl, need, false, st, nullptr, prog))) return err;
   *out_level = min_level(lvl);
   return FESC_OK;
+}
+
+int op_affine_scan(Context* c, uint64_t* const* a, uint64_t* const* s, uint32_t L,
+                   uint32_t chunks, uint32_t level, bool states_only, uint32_t* out_level,
+                   hipStream_t st) {
+  return scan_in_place(c, a, s, L, chunks, level, states_only, out_level, st, nullptr);
 }
 
 
@@ -388,6 +395,24 @@ static int resident(Context* c, const uint64_t* const* a, const uint64_t* const*
   }
   *min_out = lo;
   return FESC_OK;
+}
+
+size_t affine_scan_program(uint32_t L, uint32_t chunks, bool states_only, uint32_t level,
+                           uint64_t* words, size_t cap, int* err) {
+  // placeholder addresses as for the resident program; the scan is in place
+  const uint64_t A0 = 1u << 24, S0 = 2u << 24;
+  std::vector<uint64_t*> a((size_t)chunks * L), s((size_t)chunks * L);
+  for (size_t i = 0; i < a.size(); ++i) {
+    a[i] = reinterpret_cast<uint64_t*>((uintptr_t)(A0 + i));
+    s[i] = reinterpret_cast<uint64_t*>((uintptr_t)(S0 + i));
+  }
+  Program prog;
+  uint32_t lo;
+  *err = scan_in_place(nullptr, a.data(), s.data(), L, chunks, level, states_only, &lo, nullptr,
+                       &prog);
+  if (words)
+    for (size_t i = 0; i < prog.words.size() && i < 5 * cap; ++i) words[i] = prog.words[i];
+  return prog.words.size() / 5;
 }
 
 size_t affine_scan_resident_program(uint32_t L, uint32_t block, uint32_t level, uint64_t* words,

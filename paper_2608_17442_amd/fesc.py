@@ -69,6 +69,8 @@ _SIGS = {
     "fesc_affine_scan_network": [_u32, _u32, ctypes.POINTER(_u32), _sz, ctypes.POINTER(_sz)],
     "fesc_affine_scan_resident_program": [_u32, _u32, ctypes.POINTER(_u64), _sz,
                                           ctypes.POINTER(_sz)],
+    "fesc_affine_scan_program": [_u32, _u32, _u32, ctypes.POINTER(_u64), _sz,
+                                 ctypes.POINTER(_sz)],
     "fesc_affine_scan_resident_info": [_vp, _u32, _u32, _u32, _u32, ctypes.POINTER(_u32),
                                        ctypes.POINTER(_sz), ctypes.POINTER(_u64)],
     "fesc_heconv": [_vp, _vp, _u32, ctypes.POINTER(_i32), ctypes.POINTER(_vp), _vp, _vp, _u32,
@@ -340,6 +342,16 @@ def affine_scan_network(L: int, states_only: bool = False):
     buf = (_u32 * (4 * max(cnt.value, 1)))()
     _check(_lib.fesc_affine_scan_network(L, flags, buf, cnt.value, ctypes.byref(cnt)))
     return [tuple(buf[4 * i:4 * i + 4]) for i in range(cnt.value)]
+
+
+def affine_scan_program(L: int, chunks: int, states_only: bool = False):
+    """Products (group, x, y, add, out) of the in-place scan; host-only."""
+    flags = SCAN_STATES_ONLY if states_only else 0
+    cnt = _sz()
+    _check(_lib.fesc_affine_scan_program(L, chunks, flags, None, 0, ctypes.byref(cnt)))
+    buf = (_u64 * (5 * max(cnt.value, 1)))()
+    _check(_lib.fesc_affine_scan_program(L, chunks, flags, buf, cnt.value, ctypes.byref(cnt)))
+    return [tuple(buf[5 * i:5 * i + 5]) for i in range(cnt.value)]
 
 
 def affine_scan_resident_program(L: int, block: int):

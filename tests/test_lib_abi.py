@@ -176,7 +176,6 @@ def test_resident_schedule_program_gives_the_recurrence(L, block):
     switch), a skipped decay never read.  Every state equals the sequential
     recurrence h_k = a_k h_(k-1) + s_k, at the benchmark's L = 2048 with
     blocks of 1024 and at ragged and degenerate shapes."""
-    import itertools
     from paper_2608_17442_amd import fesc as F
     prime = (1 << 61) - 1
     A0, S0, H0 = 1 << 24, 2 << 24, 3 << 24
@@ -186,19 +185,51 @@ def test_resident_schedule_program_gives_the_recurrence(L, block):
     s = [int(v) for v in rng.integers(0, prime, L)]
     mem = {A0 + k: a[k] for k in range(L)}
     mem.update({S0 + k: s[k] for k in range(L)})
-    for _, group in itertools.groupby(prog, key=lambda e: e[0]):
-        group = list(group)
-        for i in range(0, len(group), 32):
-            sub = group[i:i + 32]
-            vals = []
-            for _, x, y, add, out in sub:
-                if y == 0:                                   # copy
-                    vals.append((out, mem[x]))
-                else:
-                    vals.append((out, (mem[x] * mem[y] + (mem[add] if add else 0)) % prime))
-            for out, v in vals:
-                mem[out] = v
+    _replay(prog, mem, prime)
     h = 0
     for k in range(L):
         h = (a[k] * h + s[k]) % prime
         assert mem[H0 + k] == h, (L, block, k)
+
+
+def _replay(prog, mem, prime):
+    """Products out = x y (+ add) / copies, in launches of 32 whose operands are
+    all read before any output is written."""
+    import itertools
+    for _, group in itertools.groupby(prog, key=lambda e: e[0]):
+        group = list(group)
+        for i in range(0, len(group), 32):
+            vals = []
+            for _, x, y, add, out in group[i:i + 32]:
+                vals.append((out, mem[x] if y == 0 else
+                             (mem[x] * mem[y] + (mem[add] if add else 0)) % prime))
+            for out, v in vals:
+                mem[out] = v
+
+
+@pytest.mark.parametrize("L,chunks,states_only", [(2048, 2, True), (2048, 1, False),
+                                                  (128, 12, True), (13, 3, False), (1, 2, True)])
+def test_in_place_scan_program_gives_the_recurrence(L, chunks, states_only):
+    """The library's in-place Brent-Kung driver, recorded on the host
+    (fesc_affine_scan_program) with chunks batched together as on the GPU,
+    replayed over GF(2^61 - 1): every state (and without states_only every
+    decay prefix) equals the sequential recurrence, at the benchmark's shapes
+    (2048 tokens, two chunks per launch; 128 tokens x 12 chunks)."""
+    from paper_2608_17442_amd import fesc as F
+    prime = (1 << 61) - 1
+    A0, S0 = 1 << 24, 2 << 24
+    prog = F.affine_scan_program(L, chunks, states_only)
+    rng = np.random.default_rng(L * 31 + chunks)
+    a = [int(v) for v in rng.integers(1, prime, L * chunks)]
+    s = [int(v) for v in rng.integers(0, prime, L * chunks)]
+    mem = {A0 + i: a[i] for i in range(L * chunks)}
+    mem.update({S0 + i: s[i] for i in range(L * chunks)})
+    _replay(prog, mem, prime)
+    for c in range(chunks):
+        h, pa = 0, 1
+        for k in range(L):
+            i = c * L + k
+            h, pa = (a[i] * h + s[i]) % prime, pa * a[i] % prime
+            assert mem[S0 + i] == h, (c, k)
+            if not states_only:
+                assert mem[A0 + i] == pa, (c, k)
