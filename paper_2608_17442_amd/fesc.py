@@ -108,13 +108,25 @@ def _check(rc: int) -> int:
     return rc
 
 
-def _ptr(t) -> int:
+def _ptr(t, words: int = 0, what: str = "buffer"):
+    """Device address of a contiguous CUDA int64 (residues, coefficients) or
+    int8 (secret) tensor holding at least `words` elements (None -> NULL)."""
     if t is None:
         return None
-    assert isinstance(t, torch.Tensor) and t.is_cuda and t.dtype in (torch.int64, torch.int8), \
-        "device buffers are CUDA int64 (residues, coefficients) or int8 (secret) tensors"
-    assert t.is_contiguous()
+    if not (isinstance(t, torch.Tensor) and t.is_cuda and t.dtype in (torch.int64, torch.int8)):
+        raise TypeError(f"{what}: device buffers are CUDA int64 or int8 tensors")
+    if not t.is_contiguous():
+        raise ValueError(f"{what}: tensor must be contiguous")
+    if t.numel() < words:
+        raise ValueError(f"{what}: {t.numel()} elements, the call reads or writes {words}")
     return t.data_ptr()
+
+
+def _ptrs(ts, count: int, words: int, what: str):
+    """ctypes array of `count` device addresses (each buffer >= words)."""
+    if len(ts) != count:
+        raise ValueError(f"{what}: {len(ts)} buffers, expected {count}")
+    return (_vp * max(count, 1))(*[_ptr(t, words, what) for t in ts])
 
 
 def _stream(stream) -> int:
@@ -167,46 +179,74 @@ class Context:
 
     # -- transforms and Hadamard products --------------------------------
 
+    def _rows(self, batch, batch_stride, limbs, limb_stride):
+        if batch == 0 or limbs == 0:
+            return 0
+        return (batch - 1) * batch_stride + (limbs - 1) * limb_stride + self.n
+
     def ntt_fwd(self, d, batch, batch_stride, limbs, limb_stride, prime0, stream=None):
-        _check(_lib.fesc_ntt_fwd(self._h, _ptr(d), batch, batch_stride, limbs, limb_stride,
-                                 prime0, _stream(stream)))
+        _check(_lib.fesc_ntt_fwd(self._h, _ptr(d, self._rows(batch, batch_stride, limbs,
+                                                             limb_stride), "d"),
+                                 batch, batch_stride, limbs, limb_stride, prime0,
+                                 _stream(stream)))
 
     def ntt_inv(self, d, batch, batch_stride, limbs, limb_stride, prime0, stream=None):
-        _check(_lib.fesc_ntt_inv(self._h, _ptr(d), batch, batch_stride, limbs, limb_stride,
-                                 prime0, _stream(stream)))
+        _check(_lib.fesc_ntt_inv(self._h, _ptr(d, self._rows(batch, batch_stride, limbs,
+                                                             limb_stride), "d"),
+                                 batch, batch_stride, limbs, limb_stride, prime0,
+                                 _stream(stream)))
 
     def mac(self, a, b, out, pairs, pair_stride, limbs, prime0, stream=None):
-        _check(_lib.fesc_mac(self._h, _ptr(a), _ptr(b), _ptr(out), pairs, pair_stride, limbs,
+        w = self._rows(pairs, pair_stride, limbs, self.n)
+        _check(_lib.fesc_mac(self._h, _ptr(a, w, "a"), _ptr(b, w, "b"),
+                             _ptr(out, limbs * self.n, "out"), pairs, pair_stride, limbs,
                              prime0, _stream(stream)))
 
     # -- ciphertext operations -------------------------------------------
 
+    # Buffer sizes of a ciphertext / plaintext at `level`; a level the context
+    # does not have is left to the library's own check (FESC_ERR_LEVEL).
+    def _ct(self, level):
+        return level * 2 * self.n if 1 <= level <= self.L else 0
+
+    def _pt(self, level):
+        return level * self.n if 1 <= level <= self.L else 0
+
     def add(self, a, b, out, level, stream=None):
-        _check(_lib.fesc_add(self._h, _ptr(a), _ptr(b), _ptr(out), level, _stream(stream)))
+        w = self._ct(level)
+        _check(_lib.fesc_add(self._h, _ptr(a, w, "a"), _ptr(b, w, "b"), _ptr(out, w, "out"),
+                             level, _stream(stream)))
 
     def sub(self, a, b, out, level, stream=None):
-        _check(_lib.fesc_sub(self._h, _ptr(a), _ptr(b), _ptr(out), level, _stream(stream)))
+        w = self._ct(level)
+        _check(_lib.fesc_sub(self._h, _ptr(a, w, "a"), _ptr(b, w, "b"), _ptr(out, w, "out"),
+                             level, _stream(stream)))
 
     def mul_plain(self, ct, pt, out, level, stream=None):
-        _check(_lib.fesc_mul_plain(self._h, _ptr(ct), _ptr(pt), _ptr(out), level,
-                                   _stream(stream)))
+        w = self._ct(level)
+        _check(_lib.fesc_mul_plain(self._h, _ptr(ct, w, "ct"), _ptr(pt, self._pt(level), "pt"),
+                                   _ptr(out, w, "out"), level, _stream(stream)))
 
     def mul_monomial(self, ct, out, level, k, stream=None):
-        _check(_lib.fesc_mul_monomial(self._h, _ptr(ct), _ptr(out), level, k, _stream(stream)))
+        w = self._ct(level)
+        _check(_lib.fesc_mul_monomial(self._h, _ptr(ct, w, "ct"), _ptr(out, w, "out"), level, k,
+                                      _stream(stream)))
 
     def mul_relin(self, a, b, out, level, stream=None):
-        _check(_lib.fesc_mul_relin(self._h, _ptr(a), _ptr(b), _ptr(out), level,
-                                   _stream(stream)))
+        w = self._ct(level)
+        _check(_lib.fesc_mul_relin(self._h, _ptr(a, w, "a"), _ptr(b, w, "b"),
+                                   _ptr(out, w, "out"), level, _stream(stream)))
 
     def mul_relin_rescale(self, a, b, outs, level, stream=None):
         """out_i = relin(a_i * b_i) / (P q_{level-1}), batched (level - 1)."""
-        m = len(a)
-        arr = lambda ts: (_vp * m)(*[_ptr(t) for t in ts])
-        _check(_lib.fesc_mul_relin_rescale(self._h, m, arr(a), arr(b), arr(outs), level,
+        m, w = len(a), self._ct(level)
+        _check(_lib.fesc_mul_relin_rescale(self._h, m, _ptrs(a, m, w, "a"), _ptrs(b, m, w, "b"),
+                                           _ptrs(outs, m, self._ct(level - 1), "outs"), level,
                                            _stream(stream)))
 
     def rescale(self, ct, out, level, stream=None):
-        _check(_lib.fesc_rescale(self._h, _ptr(ct), _ptr(out), level, _stream(stream)))
+        _check(_lib.fesc_rescale(self._h, _ptr(ct, self._ct(level), "ct"),
+                                 _ptr(out, self._ct(level - 1), "out"), level, _stream(stream)))
 
     def galois_element(self, step: int) -> int:
         v = _u32()
@@ -214,53 +254,69 @@ class Context:
         return int(v.value)
 
     def rotate(self, ct, out, level, step, stream=None):
-        _check(_lib.fesc_rotate(self._h, _ptr(ct), _ptr(out), level, step, _stream(stream)))
+        w = self._ct(level)
+        _check(_lib.fesc_rotate(self._h, _ptr(ct, w, "ct"), _ptr(out, w, "out"), level, step,
+                                _stream(stream)))
 
     def rotate_hoisted(self, ct, steps, outs, level, stream=None):
-        st = (_i32 * len(steps))(*steps)
-        ptrs = (_vp * len(outs))(*[_ptr(o) for o in outs])
-        _check(_lib.fesc_rotate_hoisted(self._h, _ptr(ct), len(steps), st, ptrs, level,
-                                        _stream(stream)))
+        m, w = len(steps), self._ct(level)
+        _check(_lib.fesc_rotate_hoisted(self._h, _ptr(ct, w, "ct"), m, (_i32 * max(m, 1))(*steps),
+                                        _ptrs(outs, m, w, "outs"), level, _stream(stream)))
 
     def rotate_batch(self, cts, steps, outs, level, stream=None):
-        n = len(cts)
-        a = (_vp * n)(*[_ptr(t) for t in cts])
-        st = (_i32 * n)(*steps)
-        b = (_vp * n)(*[_ptr(t) for t in outs])
-        _check(_lib.fesc_rotate_batch(self._h, n, a, st, b, level, _stream(stream)))
+        m, w = len(cts), self._ct(level)
+        if len(steps) != m:
+            raise ValueError(f"steps: {len(steps)} values, expected {m}")
+        _check(_lib.fesc_rotate_batch(self._h, m, _ptrs(cts, m, w, "cts"),
+                                      (_i32 * max(m, 1))(*steps), _ptrs(outs, m, w, "outs"),
+                                      level, _stream(stream)))
 
     def keygen(self, galois_elt, s, a, e, stream=None):
-        _check(_lib.fesc_keygen(self._h, galois_elt, _ptr(s), _ptr(a), _ptr(e), _stream(stream)))
+        E = self.L + self.alpha
+        _check(_lib.fesc_keygen(self._h, galois_elt, _ptr(s, self.n, "s"),
+                                _ptr(a, self.dnum * E * self.n, "a"),
+                                _ptr(e, self.dnum * self.n, "e"), _stream(stream)))
 
     def key_load(self, galois_elt, key, stream=None):
-        _check(_lib.fesc_key_load(self._h, galois_elt, _ptr(key), _stream(stream)))
+        _check(_lib.fesc_key_load(self._h, galois_elt, _ptr(key, self.key_words(), "key"),
+                                  _stream(stream)))
 
     def key_store(self, galois_elt, key, stream=None):
-        _check(_lib.fesc_key_store(self._h, galois_elt, _ptr(key), _stream(stream)))
+        _check(_lib.fesc_key_store(self._h, galois_elt, _ptr(key, self.key_words(), "key"),
+                                   _stream(stream)))
 
     def encrypt_sk(self, s, m, a, e, ct, level, stream=None):
-        _check(_lib.fesc_encrypt_sk(self._h, _ptr(s), _ptr(m), _ptr(a), _ptr(e), _ptr(ct), level,
-                                    _stream(stream)))
+        _check(_lib.fesc_encrypt_sk(self._h, _ptr(s, self.n, "s"), _ptr(m, self.n, "m"),
+                                    _ptr(a, self._pt(level), "a"), _ptr(e, self.n, "e"),
+                                    _ptr(ct, self._ct(level), "ct"), level, _stream(stream)))
 
     def plain_from_coeffs(self, m, pt, level, stream=None):
-        _check(_lib.fesc_plain_from_coeffs(self._h, _ptr(m), _ptr(pt), level, _stream(stream)))
+        _check(_lib.fesc_plain_from_coeffs(self._h, _ptr(m, self.n, "m"),
+                                           _ptr(pt, self._pt(level), "pt"), level,
+                                           _stream(stream)))
 
     def scan_contract(self, h, decay, cfac, d_state, outs, level, tokens=1, stream=None):
         """Lists of tokens * chunks ciphertexts, token-major; decay None for
         the contraction alone."""
-        m = len(h)
-        arr = lambda ts: (_vp * m)(*[_ptr(t) for t in ts])
-        dec = None if decay is None else arr(decay)
-        _check(_lib.fesc_scan_contract(self._h, arr(h), dec, arr(cfac), m // tokens, tokens,
-                                       d_state, arr(outs), level, _stream(stream)))
+        m, w = len(h), self._ct(level)
+        if tokens < 1 or m % tokens:
+            raise ValueError(f"{m} ciphertexts do not split into {tokens} tokens")
+        lo = level - (1 if decay is None else 2)
+        dec = None if decay is None else _ptrs(decay, m, w, "decay")
+        _check(_lib.fesc_scan_contract(self._h, _ptrs(h, m, w, "h"), dec, _ptrs(cfac, m, w, "cfac"),
+                                       m // tokens, tokens, d_state,
+                                       _ptrs(outs, m, self._ct(max(lo, 0)), "outs"), level,
+                                       _stream(stream)))
 
     def affine_scan(self, a, s, chunks, level, states_only=False, stream=None) -> int:
         """In-place Brent-Kung scan of `chunks` sequences of len(a) // chunks
         token maps (a[c*L + k], s[c*L + k]); returns the output level."""
-        n = len(a)
-        arr = lambda ts: (_vp * n)(*[_ptr(t) for t in ts])
+        n, w = len(a), self._ct(level)
+        if chunks < 1 or n % chunks:
+            raise ValueError(f"{n} tuples do not split into {chunks} chunks")
         out = _u32()
-        _check(_lib.fesc_affine_scan(self._h, arr(a), arr(s), n // chunks, chunks, level,
+        _check(_lib.fesc_affine_scan(self._h, _ptrs(a, n, w, "a"), _ptrs(s, n, w, "s"),
+                                     n // chunks, chunks, level,
                                      SCAN_STATES_ONLY if states_only else 0, ctypes.byref(out),
                                      _stream(stream)))
         return int(out.value)
@@ -283,36 +339,48 @@ class Context:
 
     def affine_scan_resident(self, a, s, chunks, block, h, level, workspace, stream=None):
         """States of the resident block schedule into h (see the C header)."""
-        n = len(a)
-        arr = lambda ts: (_vp * n)(*[_ptr(t) for t in ts])
+        n, w = len(a), self._ct(level)
+        if chunks < 1 or n % chunks:
+            raise ValueError(f"{n} tuples do not split into {chunks} chunks")
+        lo, _, _ = self.affine_scan_resident_info(n // chunks, chunks, block, level)
         ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
-        _check(_lib.fesc_affine_scan_resident(self._h, arr(a), arr(s), n // chunks, chunks, block,
-                                              arr(h), level, _ptr(workspace) if ws_bytes else None,
+        _check(_lib.fesc_affine_scan_resident(self._h, _ptrs(a, n, w, "a"), _ptrs(s, n, w, "s"),
+                                              n // chunks, chunks, block,
+                                              _ptrs(h, n, self._ct(lo), "h"), level,
+                                              _ptr(workspace) if ws_bytes else None,
                                               ws_bytes, _stream(stream)))
 
     def heconv(self, q, deltas, masks, bias, out, level, stream=None):
         """out = RS(sum_r masks[r] (.) rho(q; deltas[r])) + bias (see the C header)."""
         t = len(deltas)
-        _check(_lib.fesc_heconv(self._h, _ptr(q), t, (_i32 * t)(*deltas),
-                                (_vp * t)(*[_ptr(m) for m in masks]), _ptr(bias), _ptr(out),
-                                level, _stream(stream)))
+        _check(_lib.fesc_heconv(self._h, _ptr(q, self._ct(level), "q"), t,
+                                (_i32 * max(t, 1))(*deltas),
+                                _ptrs(masks, t, self._pt(level), "masks"),
+                                _ptr(bias, self._pt(level), "bias"),
+                                _ptr(out, self._ct(level - 1), "out"), level, _stream(stream)))
 
     def post_ssm(self, m, x_skip, d_skip, g, out, level, stream=None):
-        _check(_lib.fesc_post_ssm(self._h, _ptr(m), _ptr(x_skip), _ptr(d_skip), _ptr(g),
-                                  _ptr(out), level, _stream(stream)))
+        w = self._ct(level)
+        _check(_lib.fesc_post_ssm(self._h, _ptr(m, w, "m"), _ptr(x_skip, w, "x_skip"),
+                                  _ptr(d_skip, self._pt(level), "d_skip"), _ptr(g, w, "g"),
+                                  _ptr(out, self._ct(level - 2), "out"), level,
+                                  _stream(stream)))
 
     def add_plain(self, ct, pt, out, level, stream=None):
-        _check(_lib.fesc_add_plain(self._h, _ptr(ct), _ptr(pt), _ptr(out), level,
-                                   _stream(stream)))
+        w = self._ct(level)
+        _check(_lib.fesc_add_plain(self._h, _ptr(ct, w, "ct"), _ptr(pt, self._pt(level), "pt"),
+                                   _ptr(out, w, "out"), level, _stream(stream)))
 
     def encode_plain(self, z, scale, pt, level, stream=None):
         """Device encoding: z a complex128 CUDA tensor [count][N/2] (or [N/2])
         -> evaluation-form plaintexts pt (int64 tensor, [count][level][N])."""
         zr = torch.view_as_real(z.reshape(-1, self.n // 2)).contiguous()
-        assert zr.is_cuda and zr.dtype == torch.float64
+        if not (zr.is_cuda and zr.dtype == torch.float64):
+            raise TypeError("z: a complex128 CUDA tensor")
         count = zr.shape[0]
-        _check(_lib.fesc_encode_plain(self._h, zr.data_ptr(), count, float(scale), _ptr(pt),
-                                      level, _stream(stream)))
+        _check(_lib.fesc_encode_plain(self._h, zr.data_ptr(), count, float(scale),
+                                      _ptr(pt, count * self._pt(level), "pt"), level,
+                                      _stream(stream)))
 
     def key_words(self) -> int:
         return self.dnum * (self.L + self.alpha) * 2 * self.n
@@ -412,8 +480,9 @@ def matvec_bank_words(ctx: Context, desc: _MatvecDesc) -> int:
 
 
 def matvec_bank_pack(ctx: Context, desc: _MatvecDesc, bank, index: int, pt, stream=None):
-    _check(_lib.fesc_matvec_bank_pack(ctx._h, ctypes.byref(desc), _ptr(bank), index, _ptr(pt),
-                                      _stream(stream)))
+    _check(_lib.fesc_matvec_bank_pack(ctx._h, ctypes.byref(desc),
+                                      _ptr(bank, matvec_bank_words(ctx, desc), "bank"), index,
+                                      _ptr(pt, ctx._pt(desc.level), "pt"), _stream(stream)))
 
 
 class MatvecPlan:
@@ -428,18 +497,20 @@ class MatvecPlan:
         h = _vp()
         if bank is not None:
             self._bank = bank
-            _check(_lib.fesc_matvec_plan_create_bank(ctx._h, ctypes.byref(self.desc), _ptr(bank),
-                                                     ctypes.byref(h)))
+            _check(_lib.fesc_matvec_plan_create_bank(
+                ctx._h, ctypes.byref(self.desc),
+                _ptr(bank, matvec_bank_words(ctx, self.desc), "bank"), ctypes.byref(h)))
         else:
             self._diags = list(diags)
-            arr = (_vp * len(self._diags))(*[_ptr(t) for t in self._diags])
+            arr = _ptrs(self._diags, n_out * n2 * n_in * n1, ctx._pt(level), "diags")
             _check(_lib.fesc_matvec_plan_create(ctx._h, ctypes.byref(self.desc), arr,
                                                 ctypes.byref(h)))
         self._h = h
 
     def __call__(self, ins, outs, stream=None):
-        a = (_vp * len(ins))(*[_ptr(t) for t in ins])
-        b = (_vp * len(outs))(*[_ptr(t) for t in outs])
+        d, c = self.desc, self.ctx
+        a = _ptrs(ins, d.n_in, c._ct(d.level), "ins")
+        b = _ptrs(outs, d.n_out, c._ct(d.level - (1 if d.rescale else 0)), "outs")
         _check(_lib.fesc_ptct_matvec(self.ctx._h, self._h, a, b, _stream(stream)))
 
     def phase_ms(self):

@@ -242,3 +242,25 @@ def test_empty_batches_are_rejected():
     with pytest.raises(F.FescError) as e:
         ctx.rotate_batch([], [], [], 3)
     assert e.value.code == -1
+
+
+def test_binding_rejects_short_buffers():
+    """The binding checks every buffer against the words the call touches
+    (and list lengths) before calling the library, so a short tensor is an
+    exception, never an out-of-bounds kernel access."""
+    from paper_2608_17442_amd import fesc as F
+    P = C.params_small(12, 50, 3, 1)
+    ctx = F.Context(P.log_n, P.q, P.p)
+    ct = torch.zeros(3 * 2 * P.n, dtype=torch.int64, device="cuda")
+    short = torch.zeros(2 * 2 * P.n - 1, dtype=torch.int64, device="cuda")
+    with pytest.raises(ValueError, match="out"):
+        ctx.rescale(ct, short, 3)                    # needs 2 limbs x 2 x N
+    with pytest.raises(ValueError, match="^a: "):
+        ctx.add(short, ct, ct, 3)
+    with pytest.raises(ValueError, match="outs"):
+        ctx.rotate_hoisted(ct, [1, 2], [ct], 3)      # two steps, one output
+    with pytest.raises(ValueError, match="steps"):
+        ctx.rotate_batch([ct, ct], [1], [ct, ct], 3)
+    with pytest.raises(TypeError):
+        ctx.add(ct.cpu(), ct, ct, 3)
+    assert torch.count_nonzero(ct).item() == 0
