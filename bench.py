@@ -32,6 +32,8 @@ is data-oblivious) is timed on its own as `components.affine_scan`, and one
 whole HEScan layer at the paper's long-sequence shape (L = 2048, 12 state
 chunks, 23 limbs in: update construction, scan, contraction of every token;
 full-length and two-pass schedules) as `components.hescan_layer`.
+Other modes: --affine-only, --scan-sweep (resident block sizes at L = 2048),
+--hescan-sweep (the HEScan layer at L = 128 .. 2048).
 Prints ONE JSON line on stdout.  --gpus > 1 is refused (single-GPU build).
 """
 from __future__ import annotations
@@ -593,6 +595,8 @@ def main():
     ap.add_argument("--no-hescan", action="store_true",
                     help="skip the HEScan layer component (L=2048: construction, scan, "
                          "contraction)")
+    ap.add_argument("--hescan-sweep", action="store_true",
+                    help="only the HEScan layer at L = 128 .. 2048 (blocks of min(1024, L))")
     ap.add_argument("--scan-sweep", action="store_true",
                     help="only the resident-schedule block-size sweep at L=2048 (one chunk)")
     ap.add_argument("--affine-only", action="store_true",
@@ -618,6 +622,14 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if args.hescan_sweep:
+        W = Workloads(F, torch, np, affine_only=True)
+        sweep = {}
+        for L in (128, 256, 512, 1024, 2048):
+            log(f"HEScan layer sweep: L = {L}")
+            sweep[L] = time_hescan(W, F, torch, np, L=L, block=min(1024, L))
+        print(json.dumps({"hescan_layer_sweep": sweep}), flush=True)
+        return
     if args.scan_sweep:
         W = Workloads(F, torch, np, affine_only=True)
         print(json.dumps({"scan_block_sweep": scan_block_sweep(W, F, torch, np)}), flush=True)
