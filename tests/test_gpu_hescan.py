@@ -164,16 +164,18 @@ def test_hescan_layer(small, L, K, block):
             assert np.max(np.abs(dec - ref[t, k * c_state:(k + 1) * c_state])) <= 2.0 ** -15
 
 
-def test_hescan_layer_full_size():
+@pytest.mark.parametrize("L,block", [(4, None), (5, 2)])
+def test_hescan_layer_full_size(L, block):
     """The layer at the bench's ring and chain (N = 2^16, x and B at 23
-    limbs, d_state 128, Brent-Kung scan in place, contraction of every token
-    in one call), four tokens of one chunk pair: bit-exact against the oracle
-    and within 2^-15 of the fp64 recurrence."""
+    limbs, d_state 128, contraction of every token in one call), one chunk
+    pair: four tokens through the Brent-Kung scan in place, five through the
+    resident schedule with blocks of 2 (summaries, carries, replay): bit-exact
+    against the oracle and within 2^-15 of the fp64 recurrence."""
     P = C.params_p16(24)
-    d_s, head_dim, level, L, K = 128, 64, 23, 4, 2
+    d_s, head_dim, level, K = 128, 64, 23, 2
     S = Setup(P, 64, rot_steps=[d_s >> k for k in range(1, 8)], relin=True, conj=True)
     vals, br = hescan_packets(P, 64, L, K, d_s, head_dim)
-    lo = level - 1 - 2                                  # Brent-Kung depth 2 for 4 tokens
+    lo = level - 1 - {None: 2, 2: 3}[block]             # scan depth: 2 (BK of 4), 3 (resident)
     Xo, Bo, Ao, Co = ([[] for _ in range(K)] for _ in range(4))
     Xd, Bd, Ad, Cd = [], [], [], []
     for k in range(K):
@@ -187,10 +189,10 @@ def test_hescan_layer_full_size():
                 co, cd = S.encrypt(v, sc, lvl, 700 + i + r)
                 o[k].append(co)
                 d.append(cd)
-    step(f"hescan layer full size L={L} K={K} level={level}")
-    outs, lo_out = hescan_gpu(S.ctx, Xd, Bd, Ad, Cd, K, L, d_s, level, None)
+    step(f"hescan layer full size L={L} K={K} block={block} level={level}")
+    outs, lo_out = hescan_gpu(S.ctx, Xd, Bd, Ad, Cd, K, L, d_s, level, block)
     assert lo_out == lo - 1
-    want = OS.hescan(P, Xo, Bo, Ao, Co, S.keys[0], S.keys, d_s, None)
+    want = OS.hescan(P, Xo, Bo, Ao, Co, S.keys[0], S.keys, d_s, block)
     ref = hescan_reference(vals, head_dim)
     c_state = P.n // 2 // d_s
     for t in range(L):
