@@ -631,7 +631,7 @@ def main():
                          "scaling hardware traffic counters")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py: this build runs on one GPU only (no multi-GPU path); use --gpus 1",
+        print("bench.py: the library runs on one GPU per process and has no multi-GPU path; use --gpus 1",
               file=sys.stderr)
         sys.exit(2)
 
