@@ -9,7 +9,9 @@ namespace {
 
 constexpr int kThreads = 256;
 
-// V coefficients per thread (V/2 16-byte loads per operand and pair).
+// V coefficients per thread, as V/2 16-byte loads per operand and pair; load
+// i of thread t covers coefficients 2(i kThreads + t) and the next, so each load
+// instruction of a wave reads one contiguous 1 KiB run.
 template <int V>
 __global__ __launch_bounds__(kThreads) void k_mac(const uint64_t* __restrict__ a,
                                                   const uint64_t* __restrict__ b,
@@ -18,7 +20,7 @@ __global__ __launch_bounds__(kThreads) void k_mac(const uint64_t* __restrict__ a
                                                   uint32_t prime0,
                                                   const PrimeK* __restrict__ pk) {
   const uint32_t limb = blockIdx.y;
-  const uint32_t k = (blockIdx.x * kThreads + threadIdx.x) * V;
+  const uint32_t k = blockIdx.x * kThreads * V + 2 * threadIdx.x;
   if (k >= n) return;
   const double q = pk[prime0 + limb].q, qinv = pk[prime0 + limb].qinv;
   const size_t off = (size_t)limb * n + k;
@@ -31,7 +33,7 @@ __global__ __launch_bounds__(kThreads) void k_mac(const uint64_t* __restrict__ a
     const ulonglong2* pb = reinterpret_cast<const ulonglong2*>(b + j * pair_stride + off);
 #pragma unroll
     for (int v = 0; v < V; v += 2) {
-      const ulonglong2 va = pa[v / 2], vb = pb[v / 2];
+      const ulonglong2 va = pa[v / 2 * kThreads], vb = pb[v / 2 * kThreads];
       acc[v] = red_bal(acc[v] + mm_var(u2d(va.x), u2d(vb.x), q, qinv), q, qinv);
       acc[v + 1] = red_bal(acc[v + 1] + mm_var(u2d(va.y), u2d(vb.y), q, qinv), q, qinv);
     }
@@ -42,7 +44,7 @@ __global__ __launch_bounds__(kThreads) void k_mac(const uint64_t* __restrict__ a
     ulonglong2 r;
     r.x = to_res(acc[v], q, qinv);
     r.y = to_res(acc[v + 1], q, qinv);
-    po[v / 2] = r;
+    po[v / 2 * kThreads] = r;
   }
 }
 
