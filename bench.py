@@ -342,7 +342,8 @@ class Workloads:
         return lo
 
 
-def time_hescan(W, F, torch, np, L=2048, block=1024, level=23, chunks=12, d_s=128, pool=64):
+def time_hescan(W, F, torch, np, L=2048, block=1024, level=23, chunks=12, d_s=128, pool=64,
+                low_q=4, low_alpha=2):
     """One HEScan layer at the paper's long-sequence shape (L tokens, `chunks`
     state chunks of 128 channels x d_state 128, N = 2^16), chunk pair by chunk
     pair (2l, 2l+1): the on-demand update construction s = RS(relin(x B)) from
@@ -357,7 +358,13 @@ def time_hescan(W, F, torch, np, L=2048, block=1024, level=23, chunks=12, d_s=12
     Ciphertexts are uniform residues (the arithmetic is data-oblivious): x, a
     and C per (token, chunk) of the pair, B from a pool of `pool` (B is as
     large as x: holding both for 4,096 tuples next to a would exceed HBM);
-    every pair reuses the buffers; one warm-up pair per schedule."""
+    every pair reuses the buffers; one warm-up pair per schedule.
+    The contraction runs in a second context over the chain prefix
+    q_0..q_{low_q - 1} with the first `low_alpha` special primes: the states'
+    buffers are valid there as they are (same primes, same layout), and its
+    key switches at levels 2-3 work over 4-5 extended rows instead of 10-11.
+    States above level low_q (short sequences, less scan depth) are
+    contracted in the layer's own context."""
     for name in ("af_buf", "af_a", "af_s"):
         if hasattr(W, name):
             delattr(W, name)
@@ -368,6 +375,12 @@ def time_hescan(W, F, torch, np, L=2048, block=1024, level=23, chunks=12, d_s=12
         W.keygen(W.ctx.galois_element(st), seed)
     W.keygen(2 * W.n - 1, seed)
     ctx, n = W.ctx, W.n
+    # contraction context: chain prefix, fewer special primes, its own keys
+    lq, lp = W.q[:low_q], W.p[:low_alpha]
+    cctx = F.Context(W.log_n, lq, lp)
+    for g in [0, 2 * n - 1] + [ctx.galois_element(d_s >> k) for k in range(1, d_s.bit_length())]:
+        a, e = W.synth.switch_key_draws(seed, lq + lp, n, -(-low_q // low_alpha), g)
+        cctx.keygen(g, W.s_dev, W.dev(a), W.dev(e))
     words = lambda lvl: lvl * 2 * n
     rnd = lambda rows, lvl: torch.randint(0, 1 << 49, (rows, words(lvl)), dtype=torch.int64,
                                           device="cuda")
@@ -375,7 +388,10 @@ def time_hescan(W, F, torch, np, L=2048, block=1024, level=23, chunks=12, d_s=12
     out = {"tokens": L, "chunks": chunks, "d_state": d_s, "level_in": level,
            "paper_context": "HEScan 284.2 s/layer on one A100-40GB at this shape (two-pass, "
                             "blocks of 1024, chain of 23 ciphertext primes; construction, scan "
-                            "and contraction; 372K key switches)"}
+                            "and contraction; 372K key switches)",
+           "contraction_context": {"ciphertext_primes": low_q, "special_primes": low_alpha,
+                                   "note": "chain prefix q_0..q_%d of the layer's context "
+                                           "(8 special primes), own keys" % (low_q - 1)}}
     pairs = chunks // 2
     red_ks = L * (d_s.bit_length() - 1) + L            # rotations + conjugations per pair
 
@@ -413,12 +429,14 @@ def time_hescan(W, F, torch, np, L=2048, block=1024, level=23, chunks=12, d_s=12
     def full_pair(spans):
         span(spans, "construct_s", lambda: ctx.mul_relin_rescale(xs, bs, xs, level))
         span(spans, "scan_s", lambda: ctx.affine_scan(as_, xs, 2, level - 1, states_only=True))
-        span(spans, "contract_s", lambda: ctx.scan_contract(tm(xs, 2), None, tm(cs, 2), d_s,
-                                                            tm(os_, 2), lo, tokens=L))
+        span(spans, "contract_s", lambda: cc.scan_contract(tm(xs, 2), None, tm(cs, 2), d_s,
+                                                           tm(os_, 2), lo, tokens=L))
+    cc = cctx if lo <= low_q else ctx
     r = run(full_pair)
     total_ks = pairs * (2 * L + 2 * ks + 2 * L + red_ks)
     r.update({"level_states": lo, "level_out": lo - 1, "key_switches": total_ks,
-              "keyswitch_per_s": round(total_ks / r["s_per_layer"], 1)})
+              "keyswitch_per_s": round(total_ks / r["s_per_layer"], 1),
+              "contraction_in": "prefix context" if cc is cctx else "layer context"})
     out["full_length"] = r
     del X, A, Cc, O, Bp, xs, as_, cs, os_, bs
     torch.cuda.empty_cache()
@@ -436,12 +454,14 @@ def time_hescan(W, F, torch, np, L=2048, block=1024, level=23, chunks=12, d_s=12
             span(spans, "construct_s", lambda: ctx.mul_relin_rescale(xs, bs, xs, level))
             span(spans, "scan_s", lambda: ctx.affine_scan_resident(
                 as_, xs, 1, block, hs[c * L:(c + 1) * L], level - 1, ws))
-        span(spans, "contract_s", lambda: ctx.scan_contract(tm(hs, 2), None, tm(cs, 2), d_s,
-                                                            tm(os_, 2), lo, tokens=L))
+        span(spans, "contract_s", lambda: cc.scan_contract(tm(hs, 2), None, tm(cs, 2), d_s,
+                                                           tm(os_, 2), lo, tokens=L))
+    cc = cctx if lo <= low_q else ctx
     r = run(two_pass_pair)
     total_ks = pairs * (2 * L + 2 * ks + 2 * L + red_ks)
     r.update({"block": block, "level_states": lo, "level_out": lo - 1,
-              "key_switches": total_ks, "keyswitch_per_s": round(total_ks / r["s_per_layer"], 1)})
+              "key_switches": total_ks, "keyswitch_per_s": round(total_ks / r["s_per_layer"], 1),
+              "contraction_in": "prefix context" if cc is cctx else "layer context"})
     out["two_pass"] = r
     del X, A, H, Cc, O, Bp, ws, xs, as_, hs, cs, os_, bs
     torch.cuda.empty_cache()

@@ -64,6 +64,12 @@ typedef struct fesc_params {
 
 /* Context: validates the primes (prime, < 2^50, = 1 mod 2N, distinct),
  * derives psi for each and uploads twiddle tables to the current device.
+ * psi and the evaluation order depend only on (N, prime), so two contexts of
+ * one N whose ciphertext chains share the prefix q_0..q_{m-1} hold every
+ * ciphertext or plaintext of level l <= m in the same buffer format: a buffer
+ * may be passed from one to the other as it is.  A context over a short
+ * prefix with few special primes (and its own switching keys) makes key
+ * switching at low levels cheaper, its extended basis being l + alpha' rows.
  * Errors: FESC_ERR_ARG, FESC_ERR_OOM, FESC_ERR_HIP. */
 int fesc_ctx_create(const fesc_params* params, fesc_ctx** out);
 void fesc_ctx_destroy(fesc_ctx* ctx);

@@ -157,7 +157,7 @@ def resident_scan(P: C.Params, a: list, s: list, block: int, rlk) -> list:
 
 
 def hescan(P: C.Params, x: list, B: list, a: list, cfac: list, rlk, keys: dict, d_s: int,
-           block: int | None = None) -> list:
+           block: int | None = None, contract: tuple | None = None) -> list:
     """HEScan of one sequence over K state chunks (Sec. "On-Demand
     Construction and Contraction", Eqs. "fesc_recurrence", "fesc_contract" and
     "hescan-contract-output").  x, B, a, cfac: [K][L] ciphertexts, broadcast
@@ -166,7 +166,13 @@ def hescan(P: C.Params, x: list, B: list, a: list, cfac: list, rlk, keys: dict, 
     (level l - 1), the states h_k by the Brent-Kung scan (block None) or the
     resident schedule, at one common level; then per token the contraction
     (the scan-contract slice without the decay product).  Returns per token
-    the slice's outputs."""
+    the slice's outputs.
+
+    contract = (P_c, rlk_c, keys_c) runs the contraction under another
+    parameter set whose ciphertext chain begins with the states' primes (the
+    same residues then denote the same ciphertexts), typically with fewer
+    special primes, so that its key switches work over a smaller extended
+    basis; the contraction's arithmetic is otherwise unchanged."""
     from . import workloads as W
     K, L = len(x), len(x[0])
     H = []
@@ -176,7 +182,11 @@ def hescan(P: C.Params, x: list, B: list, a: list, cfac: list, rlk, keys: dict, 
         ak = [_drop(a[k][t], lvl) for t in range(L)]
         H.append(affine_scan(P, ak, s, rlk)[1] if block is None
                  else resident_scan(P, ak, s, block, rlk))
-    return [W.scan_contract_token(P, [H[k][t] for k in range(K)], None,
-                                  [cfac[k][t] for k in range(K)], rlk, keys, d_s)
+    Pc, rlk_c, keys_c = contract if contract is not None else (P, rlk, keys)
+    if contract is not None:
+        lvl = max(H[0][0].shape[0], cfac[0][0].shape[0])
+        assert list(Pc.q[:lvl]) == list(P.q[:lvl]), "contraction chain must extend the states'"
+    return [W.scan_contract_token(Pc, [H[k][t] for k in range(K)], None,
+                                  [cfac[k][t] for k in range(K)], rlk_c, keys_c, d_s)
             for t in range(L)]
 

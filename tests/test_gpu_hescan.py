@@ -110,10 +110,12 @@ def test_scan_contract_contraction_only(small, K, T, level):
             _eq(od, oo, f"token {u} output {k}")
 
 
-def hescan_gpu(ctx, X, Bc, A, Cc, K, L, d_s, level, block):
+def hescan_gpu(ctx, X, Bc, A, Cc, K, L, d_s, level, block, cctx=None):
     """The layer from library calls (x, B at `level`, a at level - 1; chunk-
     major lists [k * L + t]): construction in place over x, the scan, the
-    contraction of every token.  Returns token-major outputs and their level."""
+    contraction of every token (in context cctx when given: a context over a
+    prefix of the chain, which takes the states' buffers as they are).
+    Returns token-major outputs and their level."""
     ctx.mul_relin_rescale(X, Bc, X, level)
     if block is None:
         lo = ctx.affine_scan(A, X, K, level - 1, states_only=True)
@@ -127,7 +129,7 @@ def hescan_gpu(ctx, X, Bc, A, Cc, K, L, d_s, level, block):
     tm = lambda v: [v[k * L + t] for t in range(L) for k in range(K)]
     n = X[0].numel() // (2 * level)
     outs = [torch.zeros((lo - 1) * 2 * n, dtype=torch.int64, device="cuda") for _ in range(K * L)]
-    ctx.scan_contract(tm(H), None, tm(Cc), d_s, outs, lo, tokens=L)
+    (cctx or ctx).scan_contract(tm(H), None, tm(Cc), d_s, outs, lo, tokens=L)
     return outs, lo - 1
 
 
@@ -164,16 +166,23 @@ def test_hescan_layer(small, L, K, block):
             assert np.max(np.abs(dec - ref[t, k * c_state:(k + 1) * c_state])) <= 2.0 ** -15
 
 
-@pytest.mark.parametrize("L,block", [(4, None), (5, 2)])
-def test_hescan_layer_full_size(L, block):
+@pytest.mark.parametrize("L,block,low", [(4, None, False), (5, 2, False), (4, None, True)])
+def test_hescan_layer_full_size(L, block, low):
     """The layer at the bench's ring and chain (N = 2^16, x and B at 23
     limbs, d_state 128, contraction of every token in one call), one chunk
     pair: four tokens through the Brent-Kung scan in place, five through the
     resident schedule with blocks of 2 (summaries, carries, replay): bit-exact
-    against the oracle and within 2^-15 of the fp64 recurrence."""
+    against the oracle and within 2^-15 of the fp64 recurrence.  With `low`
+    the inputs start at 7 limbs so that the states reach level 4, and the
+    contraction runs in the bench's low-level context (chain prefix
+    q_0..q_3, two special primes instead of eight: two digits at level 4) on
+    the states' buffers as they are."""
     P = C.params_p16(24)
-    d_s, head_dim, level, K = 128, 64, 23, 2
-    S = Setup(P, 64, rot_steps=[d_s >> k for k in range(1, 8)], relin=True, conj=True)
+    d_s, head_dim, level, K = 128, 64, 7 if low else 23, 2
+    rots = [d_s >> k for k in range(1, 8)]
+    S = Setup(P, 64, rot_steps=rots, relin=True, conj=True)
+    Sc = Setup(C.Params(P.log_n, P.q[:4], P.p[:2]), 64, rot_steps=rots, relin=True,
+               conj=True) if low else S
     vals, br = hescan_packets(P, 64, L, K, d_s, head_dim)
     lo = level - 1 - {None: 2, 2: 3}[block]             # scan depth: 2 (BK of 4), 3 (resident)
     Xo, Bo, Ao, Co = ([[] for _ in range(K)] for _ in range(4))
@@ -189,10 +198,11 @@ def test_hescan_layer_full_size(L, block):
                 co, cd = S.encrypt(v, sc, lvl, 700 + i + r)
                 o[k].append(co)
                 d.append(cd)
-    step(f"hescan layer full size L={L} K={K} block={block} level={level}")
-    outs, lo_out = hescan_gpu(S.ctx, Xd, Bd, Ad, Cd, K, L, d_s, level, block)
+    step(f"hescan layer full size L={L} K={K} block={block} level={level} low={low}")
+    outs, lo_out = hescan_gpu(S.ctx, Xd, Bd, Ad, Cd, K, L, d_s, level, block, Sc.ctx)
     assert lo_out == lo - 1
-    want = OS.hescan(P, Xo, Bo, Ao, Co, S.keys[0], S.keys, d_s, block)
+    want = OS.hescan(P, Xo, Bo, Ao, Co, S.keys[0], S.keys, d_s, block,
+                     (Sc.P, Sc.keys[0], Sc.keys) if low else None)
     ref = hescan_reference(vals, head_dim)
     c_state = P.n // 2 // d_s
     for t in range(L):

@@ -199,10 +199,13 @@ def hescan_reference(vals, head_dim):
     return np.array(out)
 
 
-@pytest.mark.parametrize("L,block", [(4, None), (5, 2)])
-def test_hescan_layer_follows_the_recurrence(L, block):
+@pytest.mark.parametrize("L,block,low", [(4, None, False), (5, 2, False), (4, None, True)])
+def test_hescan_layer_follows_the_recurrence(L, block, low):
     """Update construction, the encrypted scan (Brent-Kung or resident) and
-    the contraction of every token decode to the fp64 recurrence."""
+    the contraction of every token decode to the fp64 recurrence; with `low`
+    the contraction runs under a parameter set over the chain prefix
+    q_0..q_4 with one special prime instead of two (five one-prime digits at
+    the contraction's level 5, each switched with the smaller special modulus)."""
     from oracle import scan as OS
     P = C.params_small(10, 50, 8, 2)
     seed, d_s, head_dim, K, level = 6, 8, 16, 2, 8
@@ -211,6 +214,13 @@ def test_hescan_layer_follows_the_recurrence(L, block):
     keys = _keys(P, sk, seed, [1, 2, 4], conj=True)
     vals, br = hescan_packets(P, seed, L, K, d_s, head_dim)
     lo = {(4, None): 5, (5, 2): 4}[(L, block)]      # states' level: 8 - 1 - depth
+    contract = None
+    if low:
+        Pc = C.Params(P.log_n, P.q[:lo], P.p[:1])
+        skc = C.secret_key(Pc, synth.secret(seed, P.n))
+        contract = (Pc, C.keygen_from_seed(Pc, skc, seed, 0),
+                    _keys(Pc, skc, seed, [1, 2, 4], conj=True))
+        assert Pc.alpha == 1 and Pc.dnum == lo
 
     def enc(v, scale, lvl, tag, idx):
         return C.encrypt(P, sk, C.encode_plain(P, v.astype(complex), scale, lvl), lvl,
@@ -225,7 +235,7 @@ def test_hescan_layer_follows_the_recurrence(L, block):
                    for t, c in enumerate(cols)])
         Cc.append([enc(c[3], float(P.q[lo - 1]), lo, "hC", k * L + t)
                    for t, c in enumerate(cols)])
-    outs = OS.hescan(P, X, Bc, A, Cc, rlk, keys, d_s, block)
+    outs = OS.hescan(P, X, Bc, A, Cc, rlk, keys, d_s, block, contract)
     want = hescan_reference(vals, head_dim)
     c_state = P.n // 2 // d_s
     for t in range(L):
