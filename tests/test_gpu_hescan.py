@@ -110,6 +110,46 @@ def test_scan_contract_contraction_only(small, K, T, level):
             _eq(od, oo, f"token {u} output {k}")
 
 
+@pytest.fixture(scope="module")
+def prefix16():
+    """The bench's contraction context: N = 2^16, chain prefix q_0..q_3 of
+    the 24-prime chain, the two largest special primes, d_state 128 keys."""
+    P = C.params_p16(24)
+    return Setup(C.Params(P.log_n, P.q[:4], P.p[:2]), 65,
+                 rot_steps=[128 >> k for k in range(1, 8)], relin=True, conj=True)
+
+
+@pytest.mark.parametrize("level", [2, 3])
+def test_contraction_in_prefix_context_full_ring(prefix16, level):
+    """The bench's contraction levels (2 -> 1 full length, 3 -> 2 two-pass) in
+    the prefix context: one digit at level 2, two at level 3; one token of a
+    chunk pair, bit-exact against the oracle under the same parameter set and
+    within 2^-15 of the fp64 contraction."""
+    S, P = prefix16, prefix16.P
+    d_s, K, n_slots = 128, 2, P.n // 2
+    j = np.arange(n_slots)
+    ho, hd, co, cd, want = [], [], [], [], []
+    for k in range(K):
+        hv = synth.normal(65, "ph", n_slots, 1.0, k)
+        cv = synth.normal(65, "pc", d_s, 1.0, k)
+        want.append((hv * cv[j % d_s]).reshape(-1, d_s).sum(axis=1))
+        x, y = S.encrypt(hv, 2.0 ** 40, level, 900 + 2 * k)
+        ho.append(x)
+        hd.append(y)
+        x, y = S.encrypt(cv[j % d_s], float(P.q[level - 1]), level, 901 + 2 * k)
+        co.append(x)
+        cd.append(y)
+    outs = [torch.zeros((level - 1) * 2 * P.n, dtype=torch.int64, device="cuda")
+            for _ in range(K)]
+    step(f"prefix-context contraction N=2^16 level={level}")
+    S.ctx.scan_contract(hd, None, cd, d_s, outs, level, tokens=1)
+    got = OW.scan_contract_token(P, ho, None, co, S.keys[0], S.keys, d_s)
+    for k in range(K):
+        _eq(outs[k], got[k], f"chunk {k}")
+        dec = C.decrypt(P, S.sk, got[k], 2.0 * 2.0 ** 40).real[::d_s]
+        assert np.max(np.abs(dec - want[k])) <= 2.0 ** -15
+
+
 def hescan_gpu(ctx, X, Bc, A, Cc, K, L, d_s, level, block, cctx=None):
     """The layer from library calls (x, B at `level`, a at level - 1; chunk-
     major lists [k * L + t]): construction in place over x, the scan, the
