@@ -417,6 +417,22 @@ def time_hescan(W, F, torch, np, L=2048, block=1024, level=23, chunks=12, d_s=12
         return r
 
     tm = lambda v, K: [v[k * L + t] for t in range(L) for k in range(K)]
+
+    def ks_rates(r, layer_ks, contract_ks, prefix):
+        """Key switches per context: construction and scan run in the layer's
+        context (l + 8 extended rows); the contraction's run in the prefix
+        context (l + 2 rows) when the states' level allows it, so their rates
+        are reported apart (a combined rate would mix two key-switch sizes)."""
+        d = {"key_switches": layer_ks + contract_ks,
+             "layer_context": {"key_switches": layer_ks,
+                               "keyswitch_per_s": round(
+                                   layer_ks / (r["construct_s"] + r["scan_s"]), 1)},
+             "contraction": {"key_switches": contract_ks,
+                             "keyswitch_per_s": round(contract_ks / r["contract_s"], 1),
+                             "context": "prefix context" if prefix else "layer context"}}
+        if not prefix:
+            d["keyswitch_per_s"] = round((layer_ks + contract_ks) / r["s_per_layer"], 1)
+        return d
     # full length: both chunks of a pair in place
     lo, ks = ctx.affine_scan_info(L, level - 1, states_only=True)
     gb = (2 * L * (2 * level - 1 + 2 * lo - 1) + pool * level) * 16 * n / 1e9
@@ -433,10 +449,8 @@ def time_hescan(W, F, torch, np, L=2048, block=1024, level=23, chunks=12, d_s=12
                                                            tm(os_, 2), lo, tokens=L))
     cc = cctx if lo <= low_q else ctx
     r = run(full_pair)
-    total_ks = pairs * (2 * L + 2 * ks + 2 * L + red_ks)
-    r.update({"level_states": lo, "level_out": lo - 1, "key_switches": total_ks,
-              "keyswitch_per_s": round(total_ks / r["s_per_layer"], 1),
-              "contraction_in": "prefix context" if cc is cctx else "layer context"})
+    r.update({"level_states": lo, "level_out": lo - 1})
+    r.update(ks_rates(r, pairs * (2 * L + 2 * ks), pairs * (2 * L + red_ks), cc is cctx))
     out["full_length"] = r
     del X, A, Cc, O, Bp, xs, as_, cs, os_, bs
     torch.cuda.empty_cache()
@@ -458,10 +472,8 @@ def time_hescan(W, F, torch, np, L=2048, block=1024, level=23, chunks=12, d_s=12
                                                            tm(os_, 2), lo, tokens=L))
     cc = cctx if lo <= low_q else ctx
     r = run(two_pass_pair)
-    total_ks = pairs * (2 * L + 2 * ks + 2 * L + red_ks)
-    r.update({"block": block, "level_states": lo, "level_out": lo - 1,
-              "key_switches": total_ks, "keyswitch_per_s": round(total_ks / r["s_per_layer"], 1),
-              "contraction_in": "prefix context" if cc is cctx else "layer context"})
+    r.update({"block": block, "level_states": lo, "level_out": lo - 1})
+    r.update(ks_rates(r, pairs * (2 * L + 2 * ks), pairs * (2 * L + red_ks), cc is cctx))
     out["two_pass"] = r
     del X, A, H, Cc, O, Bp, ws, xs, as_, hs, cs, os_, bs
     torch.cuda.empty_cache()
@@ -551,78 +563,250 @@ def time_affine(W, F, torch, np):
 
 # ---------------------------------------------------------------- baseline
 
-def cpu_baseline(ntt_reps: int = 16):
-    """The CPU reference timed on a bounded sample of the same workloads
-    (about 10 s of CPU work): `ntt_reps` forward + inverse NTTs of the full
-    64 x 24 x 2^16 batch, and the whole 32-ciphertext rotation set (30 key
-    switches at 24 limbs) with reference-generated keys."""
+def _omp_threads() -> int:
+    """Threads the oracle's OpenMP loops use in this process."""
+    import ctypes
+    try:
+        return int(ctypes.CDLL("libgomp.so.1").omp_get_max_threads())
+    except OSError:
+        return int(os.environ.get("OMP_NUM_THREADS", "1"))
+
+
+def cpu_sample(mode: str) -> dict:
+    """The oracle (CPU reference, as it stands) on bounded samples of every
+    configuration, in this process's OpenMP thread count.  mode "all": the
+    all-core samples; "single": smaller samples for one thread.  Inputs,
+    keys and diagonals are prepared outside the timed regions; every timed
+    region runs the oracle's operations in the order the workload issues
+    them.  Each entry gives the sample, its seconds, the factor that scales it
+    to the whole configuration and the extrapolated seconds.  The modular
+    arithmetic does not depend on the values, so the projection's sampled
+    blocks multiply uniform random plaintexts in place of encoded diagonals,
+    and the affine-scan-style inputs are not needed."""
     import numpy as np
 
     import synth
     import synth.workloads as WL
     from oracle import ckks as C
+    from oracle import workloads as OW
+
+    single = mode == "single"
+    res = {"threads": _omp_threads()}
+    tick = time.perf_counter
+
+    def entry(sample, t, factor):
+        return {"sample": sample, "sample_s": round(t, 3), "factor": factor,
+                "extrapolated_s": round(t * factor, 3)}
+
+    # cfg1: N = 2^12 diagonal matvec, in full on either thread count
+    P = C.params_p12()
+    U, x = WL.cfg1_values()
+    d, ns = WL.CFG1["dim"], P.n // 2
+    sk = C.secret_key(P, synth.secret(WL.CFG1["seed"], P.n))
+    keys = {P.galois_elt(r): C.keygen_from_seed(P, sk, WL.CFG1["seed"], P.galois_elt(r))
+            for r in range(1, d)}
+    a, e = synth.encrypt_draws(WL.CFG1["seed"], P.qs(3), P.n, "cfg1", 0)
+    ct = C.encrypt(P, sk, C.encode_plain(P, np.tile(x, ns // d), float(P.q[2]), 3), 3, a, e)
+    desc = OW.MatvecDesc(3, 1, 1, d, 1, 1, False, True)
+    dg = {q: C.encode_plain(P, OW.bsgs_diagonal_slots(U.T, ns, 1, d, d, 0, 0, 0, q, False),
+                            2.0 ** 30, 3) for q in range(d)}
+    t0 = tick()
+    OW.bsgs_matvec(P, desc, [ct], lambda b, p_, u, q: dg[q], keys)
+    res["cfg1"] = entry("the whole N=2^12 diagonal matvec (63 hoisted rotations, 64 ptmul, "
+                        "rescale)", tick() - t0, 1)
 
     P = C.params_p16()
-    mods = P.q
+    n = P.n
+    # cfg2: forward NTT, 64-pair MAC, inverse NTT of the 64 x 24 x 2^16 batch
     B = WL.CFG2["batch"]
-    A = WL.cfg2_polys("A", mods, P.n, B).reshape(-1, P.n)
-    rows = mods * B
-    t0 = time.perf_counter()
-    for _ in range(ntt_reps):
-        f = C.ntt(P, A, rows)
-        C.intt(P, f, rows)
-    dt = time.perf_counter() - t0
-    gbs = ntt_reps * 2 * (2 * 8 * P.n * len(rows)) / dt / 1e9
+    nb = 4 if single else 16
+    A = WL.cfg2_polys("A", P.q, n, nb).reshape(-1, n)
+    Bm = WL.cfg2_polys("B", P.q, n, nb).reshape(nb, len(P.q), n)
+    rows = P.q * nb
+    t0 = tick()
+    f = C.ntt(P, A, rows)
+    t1 = tick()
+    fr = f.reshape(nb, len(P.q), n)
+    acc = C.pmul(fr[0], Bm[0], P.q)
+    for j in range(1, nb):
+        acc = C.padd(acc, C.pmul(fr[j], Bm[j], P.q), P.q)
+    t2 = tick()
+    C.intt(P, f, rows)
+    t3 = tick()
+    res["cfg2"] = entry(f"forward NTT + {nb}-pair MAC + inverse NTT of {nb} of the 64 "
+                        "polynomials x 24 limbs", t3 - t0, B // nb)
+    res["cfg2"]["ntt_gbs"] = round(2 * 2 * 8 * n * len(rows) / (t1 - t0 + t3 - t2) / 1e9, 3)
+
+    # cfg3: the 32-ciphertext rotation set (30 key switches)
     seed = WL.CFG3["seed"]
-    sk = C.secret_key(P, synth.secret(seed, P.n))
+    sk = C.secret_key(P, synth.secret(seed, n))
     steps = WL.cfg3_steps()
+    take = [0, 1] if single else list(range(len(steps)))
     keys = {}
-    for r in steps:
-        if r % (P.n // 2):
-            g = P.galois_elt(r)
-            if g not in keys:
-                keys[g] = C.keygen_from_seed(P, sk, seed, g)
-    cts = []
-    for i in range(len(steps)):
-        a, e = synth.encrypt_draws(seed, P.qs(24), P.n, "cfg3", i)
-        cts.append(C.encrypt(P, sk, C.encode_plain(P, WL.cfg3_slots(i, P.n // 2), 2.0 ** 40, 24),
-                             24, a, e))
-    n_ks = sum(1 for r in steps if r % (P.n // 2))
-    t1 = time.perf_counter()
-    for i, r in enumerate(steps):
-        C.rotate(P, cts[i], r, keys)
-    dks = time.perf_counter() - t1
-    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    out = {"value": round(gbs, 3), "unit": "GB/s", "cores": cores, "kind": "oracle",
-           "sample": f"{ntt_reps} x forward+inverse NTT of the full 64 x 24 x 2^16 batch "
-                     f"({2 * ntt_reps * len(rows)} limb transforms, {dt:.2f} s); plus the "
-                     f"32-ciphertext rotation set at 24 limbs ({n_ks} key switches, "
-                     f"{dks:.2f} s)",
-           "keyswitch_per_s": round(n_ks / dks, 3)}
+    for i in take:
+        g = P.galois_elt(steps[i])
+        if steps[i] % (n // 2) and g not in keys:
+            keys[g] = C.keygen_from_seed(P, sk, seed, g)
+    cts = {}
+    for i in take:
+        a, e = synth.encrypt_draws(seed, P.qs(24), n, "cfg3", i)
+        cts[i] = C.encrypt(P, sk, C.encode_plain(P, WL.cfg3_slots(i, n // 2), 2.0 ** 40, 24),
+                           24, a, e)
+    t0 = tick()
+    for i in take:
+        C.rotate(P, cts[i], steps[i], keys)
+    t = tick() - t0
+    n_ks = sum(1 for i in take if steps[i] % (n // 2))
+    res["cfg3"] = entry(f"{n_ks} of the 30 key switches of the rotation set (24 limbs)", t,
+                        30 / n_ks)
+    res["cfg3"]["keyswitch_per_s"] = round(n_ks / t, 3)
+
+    # cfg4: the 768 x 1536 projection at 16 limbs, n1 = 16, n2 = 2, 12 inputs,
+    # 48 outputs: baby steps of one input (x 12) plus whole output blocks
+    # (pt-MAC over all inputs and baby steps, giant step, conjugation,
+    # rescale; x 24 for blocks {0, 47}) -- one thread: 2 of the 15 baby
+    # rotations of one input (x 90), the pt-MAC of one input for one block
+    # (x 576) and one block's giant step, conjugation and rescale (x 48)
+    cfg = WL.CFG4
+    seed, lvl, seg = cfg["seed"], cfg["level"], cfg["tokens"]
+    n1, n2 = cfg["n1"], cfg["n2"]
+    sk = C.secret_key(P, synth.secret(seed, n))
+    baby = [q * seg for q in range(n1)]
+    giant = [p * n1 * seg for p in range(n2)]
+    bsteps = baby[1:3] if single else baby[1:]
+    need = set(bsteps) | set(giant[1:])
+    keys = {P.galois_elt(r): C.keygen_from_seed(P, sk, seed, P.galois_elt(r)) for r in need}
+    keys[P.conj_elt] = C.keygen_from_seed(P, sk, seed, P.conj_elt)
+    X, _ = WL.cfg4_values()
+    Cc = (n // 2) // seg
+    a, e = synth.encrypt_draws(seed, P.qs(lvl), n, "cfg4", 0)
+    z0 = OW.pack_input(X, n // 2, seg, Cc, 0) + 1j * OW.pack_input(X, n // 2, seg, Cc, 1)
+    x0 = C.encrypt(P, sk, C.encode_plain(P, z0, 2.0 ** 40, lvl), lvl, a, e)
+    t0 = tick()
+    bb = C.rotate_hoisted(P, x0, [0] + bsteps, keys)
+    t_baby = tick() - t0
+    n_in = cfg["d_in"] // Cc // 2
+    rnd = synth.uniform_residues(seed, "cpu-diag", P.qs(lvl), n)
+    blocks = [0] if single else [0, cfg["d_out"] // Cc - 1]
+    n_u = 1 if single else n_in
+    t0 = tick()
+    for _ in blocks:
+        y = None
+        for p_ in range(n2):
+            acc = None
+            for _u in range(n_u):
+                for q in range(n1):
+                    tq = C.mul_plain(P, bb[q % len(bb)], rnd)
+                    acc = tq if acc is None else C.ct_add(P, acc, tq)
+            if not single:
+                acc = C.rotate(P, acc, giant[p_], keys)
+                y = acc if y is None else C.ct_add(P, y, acc)
+        if not single:
+            y = C.rescale(P, C.ct_add(P, y, C.conjugate(P, y, keys)))
+    t_blocks = tick() - t0
+    if single:
+        t0 = tick()
+        y = C.rotate(P, bb[0], giant[1], keys)
+        y = C.rescale(P, C.ct_add(P, y, C.conjugate(P, y, keys)))
+        t_tail = tick() - t0
+        res["cfg4"] = {"sample": "2 of the 15 hoisted baby rotations of one input (x 90); the "
+                                 "pt-MAC of one input into one output block (x 576); one "
+                                 "block's giant step, conjugation and rescale (x 48)",
+                       "sample_s": round(t_baby + t_blocks + t_tail, 3),
+                       "factors": [90, 576, 48],
+                       "extrapolated_s": round(90 * t_baby + 576 * t_blocks + 48 * t_tail, 3)}
+    else:
+        res["cfg4"] = {"sample": "the hoisted baby steps of one input (15 key switches, x 12); "
+                                 "output blocks 0 and 47 whole (pt-MAC over 12 inputs x 32 "
+                                 "baby/giant terms, giant step, conjugation, rescale; x 24)",
+                       "sample_s": round(t_baby + t_blocks, 3), "factors": [12, 24],
+                       "extrapolated_s": round(12 * t_baby + 24 * t_blocks, 3)}
+
+    # cfg5: the scan-contract slice of one Mamba-base token (pool entry 0);
+    # the 2048-token sequence is 2048 such tokens -- one thread: the two
+    # products of one chunk (x 12) and the reduction of one chunk pair (x 6)
+    cfg = WL.CFG5
+    seed, lvl, d_s, hd = cfg["seed"], cfg["level"], cfg["d_state"], cfg["head_dim"]
+    s_state = 16384
+    K = cfg["heads"] * hd * d_s // s_state
+    sk = C.secret_key(P, synth.secret(seed, n))
+    rlk = C.keygen_from_seed(P, sk, seed, 0)
+    keys = {P.galois_elt(d_s >> k): C.keygen_from_seed(P, sk, seed, P.galois_elt(d_s >> k))
+            for k in range(1, 8)}
+    keys[P.conj_elt] = C.keygen_from_seed(P, sk, seed, P.conj_elt)
+    z, cvec, H = WL.cfg5_token(0)
+    decay = 1.0 / (1.0 + np.exp(z))
+    j = np.arange(n // 2)
+    kk = 1 if single else K
+    ins = ([], [], [])
+    for k in range(kk):
+        e_idx = np.minimum(k * (s_state // d_s) + j // d_s, H.shape[0] - 1)
+        ok = j < s_state
+        vals = (np.where(ok, H[e_idx, j % d_s], 0.0), np.where(ok, decay[e_idx // hd], 0.0),
+                np.where(ok, cvec[j % d_s], 0.0))
+        scales = (2.0 ** 40, float(P.q[lvl - 1]), float(P.q[lvl - 2]))
+        for r in range(3):
+            a, e = synth.encrypt_draws(seed, P.qs(lvl), n, "cfg5", 3 * k + r)
+            ins[r].append(C.encrypt(P, sk, C.encode_plain(P, vals[r].astype(complex), scales[r],
+                                                          lvl), lvl, a, e))
+    if single:
+        t0 = tick()
+        t1 = C.mul_relin_rescale(P, ins[1][0], ins[0][0], rlk)
+        t2 = C.mul_relin_rescale(P, t1, ins[2][0][:t1.shape[0]], rlk)
+        t_prod = tick() - t0
+        t0 = tick()
+        chi = C.ct_add(P, t2, C.mul_monomial(P, t2, n // 2))
+        xi = OW.reduce_axis(P, chi, d_s, keys)
+        C.conjugate(P, xi, keys)
+        t_red = tick() - t0
+        res["cfg5"] = {"sample": "the two relinearised products of one state chunk (x 12 "
+                                 "chunks x 2048 tokens) and the reduction of one chunk pair "
+                                 "(7 rotations + conjugation; x 6 pairs x 2048 tokens)",
+                       "sample_s": round(t_prod + t_red, 3), "factors": [12 * 2048, 6 * 2048],
+                       "extrapolated_s": round(2048 * (12 * t_prod + 6 * t_red), 3)}
+    else:
+        t0 = tick()
+        OW.scan_contract_token(P, ins[0], ins[1], ins[2], rlk, keys, d_s)
+        res["cfg5"] = entry("the slice of one token (12 chunks: 24 products, 6 complex-paired "
+                            "reductions; 72 key switches), x 2048 tokens", tick() - t0, 2048)
+    return res
+
+
+def cpu_baseline() -> dict:
+    """The oracle timed on this host on bounded samples (about 30 s of CPU
+    work in all), in two child processes: all cores (the OpenMP default of
+    the environment) and one thread (OMP_NUM_THREADS=1; OpenMP fixes its
+    thread count per process)."""
+    import subprocess
+    out = {"kind": "oracle"}
+    for mode in ("all", "single"):
+        env = dict(os.environ)
+        if mode == "single":
+            env["OMP_NUM_THREADS"] = "1"
+        t0 = time.perf_counter()
+        r = subprocess.run([sys.executable, os.path.abspath(__file__), "--cpu-sample", mode],
+                           capture_output=True, text=True, timeout=900, env=env)
+        if r.returncode != 0:
+            out[mode] = f"not measured: {r.stderr.strip().splitlines()[-1:]}"
+            continue
+        out[mode] = json.loads(r.stdout.strip().splitlines()[-1])
+        out[mode]["wall_s"] = round(time.perf_counter() - t0, 1)
+    allc = out.get("all")
+    if isinstance(allc, dict):
+        out["value"] = allc["cfg2"]["ntt_gbs"]
+        out["unit"] = "GB/s"
+        out["cores"] = allc["threads"]
+        out["keyswitch_per_s"] = allc["cfg3"]["keyswitch_per_s"]
+        out["matvec_ms"] = round(allc["cfg4"]["extrapolated_s"] * 1e3, 1)
+        out["sample"] = ("bounded samples of all five configurations (see all / single: "
+                         "sample, seconds, factor to the whole configuration)")
+    out["nproc"] = len(os.sched_getaffinity(0))
     try:
-        with open("/proc/cpuinfo") as f:
-            out["cpu_model"] = next(l.split(":", 1)[1].strip() for l in f
-                                    if l.startswith("model name"))
-    except (OSError, StopIteration):
+        lscpu = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=30).stdout
+        out["cpu_model"] = next(l.split(":", 1)[1].strip() for l in lscpu.splitlines()
+                                if l.startswith("Model name"))
+    except (OSError, StopIteration, subprocess.SubprocessError):
         pass
-    # one thread: OpenMP fixes its thread count per process, so a child
-    # interpreter (CPU only) times one forward + inverse pass of the batch
-    code = ("import sys, time; sys.path.insert(0, %r)\n"
-            "import synth.workloads as WL\nfrom oracle import ckks as C\n"
-            "P = C.params_p16(); B = WL.CFG2['batch']\n"
-            "A = WL.cfg2_polys('A', P.q, P.n, B).reshape(-1, P.n); rows = P.q * B\n"
-            "t = time.perf_counter(); C.intt(P, C.ntt(P, A, rows), rows)\n"
-            "print(time.perf_counter() - t)\n") % ROOT
-    try:
-        import subprocess
-        r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True,
-                           timeout=300, env={**os.environ, "OMP_NUM_THREADS": "1"})
-        t1 = float(r.stdout.strip().splitlines()[-1])
-        out["single_thread"] = {"value": round(2 * (2 * 8 * P.n * len(rows)) / t1 / 1e9, 3),
-                                "unit": "GB/s", "cores": 1,
-                                "sample": f"1 x forward+inverse NTT of the batch ({t1:.2f} s)"}
-    except Exception as e:  # the baseline is reported, not required
-        out["single_thread"] = f"not measured: {e}"
     return out
 
 
@@ -646,10 +830,16 @@ def main():
                     help="only the resident-schedule block-size sweep at L=2048 (one chunk)")
     ap.add_argument("--affine-only", action="store_true",
                     help="set up and time only the affine prefix scan component (profiling)")
+    ap.add_argument("--cpu-sample", choices=("all", "single"),
+                    help="(internal) time the oracle's bounded samples in this process and "
+                         "print them as JSON; no GPU is used")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run one 1 GiB device-to-device copy, the reference kernel for "
                          "scaling hardware traffic counters")
     args = ap.parse_args()
+    if args.cpu_sample:
+        print(json.dumps(cpu_sample(args.cpu_sample)), flush=True)
+        return
     if args.gpus != 1:
         print("bench.py: the library runs on one GPU per process and has no multi-GPU path; use --gpus 1",
               file=sys.stderr)
@@ -765,6 +955,27 @@ def main():
     ks_macs = (sum(a * (lv + al - a) for a in digits) + 2 * al * lv + 2 * beta * (lv + al)) * n
     ks_valu_frac = ((inv_rows * half_logn / peak["gs"] + fwd_rows * half_logn / peak["ct"]
                      + ks_macs / peak["mac"]) * W.n_ks / (ks * 1e-3))
+    # whole-operation fractions against the benchmark spec's target (>= 60% of the
+    # HBM or VALU roofline for the N = 2^16 NTT and for key switching): NTT
+    # bytes = one read + one write of the data per direction; a key switch's
+    # bytes = its key 2 beta (l + alpha) 8N plus the ciphertext read and
+    # written 2 * 2l * 8N (151 MB at 24 limbs; keys shared by two jobs of the
+    # set make the set's own minimum lower, so this fraction is generous)
+    ks_bytes = (2 * beta * (lv + al) + 2 * 2 * lv) * 8 * n
+    ks_hbm_frac = ks_bytes * W.n_ks / (ks * 1e-3) / (HBM_PEAK_GBS * 1e9)
+    targets = {
+        "target_frac": 0.6,
+        "ntt": {"hbm_frac": round(ntt_gbs / HBM_PEAK_GBS, 4),
+                "valu_frac": round(ntt_valu_frac, 4),
+                "met": bool(max(ntt_gbs / HBM_PEAK_GBS, ntt_valu_frac) >= 0.6)},
+        "keyswitch": {"valu_frac": round(ks_valu_frac, 4), "hbm_frac": round(ks_hbm_frac, 4),
+                      "bytes_per_key_switch": ks_bytes,
+                      "us_per_key_switch": round(ks * 1e3 / W.n_ks, 2),
+                      "met": bool(max(ks_valu_frac, ks_hbm_frac) >= 0.6)},
+        "note": "whole operations timed with HIP events in the step; the per-kernel key-switch "
+                "fraction in rooflines_other is a diagnostic (it scores each kernel against "
+                "its own floor, so intermediate round trips count as useful work)",
+    }
     out = {
         "metric": METRIC,
         "value": round(ntt_gbs, 2),
@@ -813,6 +1024,7 @@ def main():
             "traffic": profiled_traffic(PTMAC_PROFILE, PTMAC_SOURCES),
             "algorithmic_bytes": ptmac_bytes,
         },
+        "targets": targets,
         "rooflines_other": {
             "ntt_valu": {"bound": "alu",
                          "achieved": round(2 * ntt_bfly / ((fwd + inv) * 1e-3) / 1e12, 4),
@@ -823,7 +1035,7 @@ def main():
                                  "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                  "frac": round(2 * ntt_gbs / HBM_PEAK_GBS, 4),
                                  "note": "two passes each read and write the data once"},
-            "keyswitch_per_kernel": keyswitch_per_kernel(),
+            "keyswitch_per_kernel_diagnostic": keyswitch_per_kernel(),
             "keyswitch_valu": {"bound": "alu", "frac": round(ks_valu_frac, 4),
                                "per_key_switch": {"butterflies": ks_bfly, "mod_macs": ks_macs},
                                "peak_butterflies_per_s": round(peak["ct"], -9),

@@ -70,6 +70,9 @@ typedef struct fesc_params {
  * may be passed from one to the other as it is.  A context over a short
  * prefix with few special primes (and its own switching keys) makes key
  * switching at low levels cheaper, its extended basis being l + alpha' rows.
+ * Its keys must be drawn with randomness independent of the first context's
+ * keys: two keys of one Galois element sharing their uniform rows and errors
+ * differ on a digit row only by (P - P') s', which reveals the secret.
  * Errors: FESC_ERR_ARG, FESC_ERR_OOM, FESC_ERR_HIP. */
 int fesc_ctx_create(const fesc_params* params, fesc_ctx** out);
 void fesc_ctx_destroy(fesc_ctx* ctx);
@@ -88,7 +91,13 @@ int fesc_root_of_unity(uint32_t log_n, uint64_t q, uint64_t* psi);
 int fesc_get_psi(const fesc_ctx* ctx, uint32_t idx, uint64_t* psi);
 
 /* Negacyclic NTT in place (forward: coefficients -> evaluation form in the
- * order above; inverse: the exact inverse).  Row (b, i), b < batch, i < limbs,
+ * order above; inverse: the exact inverse).  The paper works in the ring
+ * R_Q = Z_Q[X]/(X^N + 1) with N/2 complex slots (Sec. 2.1) and multiplies
+ * ciphertexts and plaintexts elementwise (Sec. 4.1 table: ptmul, ctmul); the
+ * evaluation form is the residue of a polynomial at the N roots of X^N + 1
+ * mod q, where those products are pointwise, so this transform is the map
+ * between the two forms (the paper does not print it; it is standard in RNS
+ * CKKS).  Row (b, i), b < batch, i < limbs,
  * starts at d + b*batch_stride + i*limb_stride (strides in uint64 words) and
  * uses extended prime prime0 + i.  Inputs must be canonical residues; outputs
  * are canonical.  Rows must not overlap.  FESC_ERR_ARG on bad indices or an
@@ -200,9 +209,25 @@ int fesc_rotate_batch(fesc_ctx* ctx, uint32_t count, const uint64_t* const* ins,
 int fesc_keygen(fesc_ctx* ctx, uint32_t galois_elt, const int8_t* s, const uint64_t* a,
                 const int64_t* e, void* stream);
 
-/* Copy a key (layout above, device memory) into / out of the context. */
+/* Copy a key (layout above, device memory) into / out of the context.
+ * galois_elt: 0 (relinearisation) or odd in (1, 2N), else FESC_ERR_ARG;
+ * store: FESC_ERR_NO_KEY if the context holds no key of that element. */
 int fesc_key_load(fesc_ctx* ctx, uint32_t galois_elt, const uint64_t* key, void* stream);
 int fesc_key_store(fesc_ctx* ctx, uint32_t galois_elt, uint64_t* key, void* stream);
+
+/* Upload a switching key generated elsewhere (by the client, who holds the
+ * secret; Sec. 2.1: the server only receives evaluation keys) from HOST
+ * memory.  host_key: uint64[ceil(key_level/alpha)][key_level+alpha][2][N],
+ * the layout above over the chain prefix q_0..q_{key_level-1} and the special
+ * primes (digit j covers q_{j*alpha}.., as everywhere).  1 <= key_level <= L
+ * (else FESC_ERR_LEVEL); a key with key_level < L serves key switches at
+ * levels <= key_level only, and any operation that would use it above that
+ * level fails with FESC_ERR_LEVEL.  galois_elt as for fesc_key_load.  The
+ * host buffer is owned by the caller and read before the call returns (the
+ * call synchronises `stream`); the context keeps its own copy, replacing
+ * any earlier key of that element. */
+int fesc_key_upload(fesc_ctx* ctx, uint32_t galois_elt, const uint64_t* host_key,
+                    uint32_t key_level, void* stream);
 
 /* Secret-key encryption from caller-drawn randomness: c1 = a,
  * c0 = -a s + m + e.  s: int8[N]; m: int64[N] plaintext coefficients;

@@ -277,24 +277,78 @@ int fesc_rotate_batch(fesc_ctx* ctx, uint32_t count, const uint64_t* const* ins,
   return op_rotate_batch(ctx, count, ins, steps, outs, nullptr, level, S(stream));
 }
 
-int fesc_keygen(fesc_ctx* ctx, uint32_t galois_elt, const int8_t* s, const uint64_t* a,
-                const int64_t* e, void* stream) {
-  if (!ctx || !s || !a || !e) return fail(FESC_ERR_ARG, "null argument");
+static int check_galois(const fesc_ctx* ctx, uint32_t galois_elt) {
   if (galois_elt != 0 && (galois_elt % 2 == 0 || galois_elt >= 2 * ctx->n || galois_elt == 1))
-    return fail(FESC_ERR_ARG, "Galois element must be odd, in (1, 2N)");
-  return op_keygen(ctx, galois_elt, s, a, e, S(stream));
+    return fail(FESC_ERR_ARG, "Galois element must be 0 or odd in (1, 2N)");
+  return FESC_OK;
 }
 
-int fesc_key_load(fesc_ctx* ctx, uint32_t galois_elt, const uint64_t* key, void* stream) {
-  if (!ctx || !key) return fail(FESC_ERR_ARG, "null argument");
+// The context's key slot of `galois_elt` (allocated on first use).
+static int key_slot(fesc_ctx* ctx, uint32_t galois_elt, uint64_t** out) {
   const size_t bytes = (size_t)ctx->dnum * (ctx->L + ctx->alpha) * 2 * ctx->n * 8;
   uint64_t*& dst = ctx->keys[galois_elt];
   if (!dst && hipMalloc(&dst, bytes) != hipSuccess) {
     ctx->keys.erase(galois_elt);
     return fail(FESC_ERR_OOM, "key allocation failed");
   }
+  *out = dst;
+  return FESC_OK;
+}
+
+int fesc_keygen(fesc_ctx* ctx, uint32_t galois_elt, const int8_t* s, const uint64_t* a,
+                const int64_t* e, void* stream) {
+  if (!ctx || !s || !a || !e) return fail(FESC_ERR_ARG, "null argument");
+  int rc = check_galois(ctx, galois_elt);
+  if (rc) return rc;
+  if ((rc = op_keygen(ctx, galois_elt, s, a, e, S(stream)))) return rc;
+  ctx->key_cap.erase(ctx->keys[galois_elt]);
+  return FESC_OK;
+}
+
+int fesc_key_load(fesc_ctx* ctx, uint32_t galois_elt, const uint64_t* key, void* stream) {
+  if (!ctx || !key) return fail(FESC_ERR_ARG, "null argument");
+  int rc = check_galois(ctx, galois_elt);
+  if (rc) return rc;
+  uint64_t* dst;
+  if ((rc = key_slot(ctx, galois_elt, &dst))) return rc;
+  ctx->key_cap.erase(dst);
+  const size_t bytes = (size_t)ctx->dnum * (ctx->L + ctx->alpha) * 2 * ctx->n * 8;
   return hip_check(hipMemcpyAsync(dst, key, bytes, hipMemcpyDeviceToDevice, S(stream)),
                    "key_load");
+}
+
+int fesc_key_upload(fesc_ctx* ctx, uint32_t galois_elt, const uint64_t* host_key,
+                    uint32_t key_level, void* stream) {
+  if (!ctx || !host_key) return fail(FESC_ERR_ARG, "null argument");
+  int rc = check_galois(ctx, galois_elt);
+  if (rc) return rc;
+  if (key_level < 1 || key_level > ctx->L)
+    return fail(FESC_ERR_LEVEL, "key_level must be in 1 .. L");
+  uint64_t* dst;
+  if ((rc = key_slot(ctx, galois_elt, &dst))) return rc;
+  const size_t n = ctx->n, E = ctx->L + ctx->alpha, Ek = key_level + ctx->alpha;
+  const uint32_t dk = (key_level + ctx->alpha - 1) / ctx->alpha;
+  hipStream_t st = S(stream);
+  // rows the prefix key does not hold stay zero; the key-switch driver
+  // refuses this key above key_level
+  rc = hip_check(hipMemsetAsync(dst, 0, (size_t)ctx->dnum * E * 2 * n * 8, st), "key_upload");
+  for (uint32_t j = 0; j < dk && !rc; ++j) {
+    const uint64_t* src = host_key + (size_t)j * Ek * 2 * n;
+    uint64_t* d = dst + (size_t)j * E * 2 * n;
+    rc = hip_check(hipMemcpyAsync(d, src, (size_t)key_level * 2 * n * 8, hipMemcpyHostToDevice,
+                                  st), "key_upload");
+    if (!rc)
+      rc = hip_check(hipMemcpyAsync(d + (size_t)ctx->L * 2 * n, src + (size_t)key_level * 2 * n,
+                                    (size_t)ctx->alpha * 2 * n * 8, hipMemcpyHostToDevice, st),
+                     "key_upload");
+  }
+  if (!rc) rc = hip_check(hipStreamSynchronize(st), "key_upload");
+  if (rc) return rc;
+  if (key_level < ctx->L)
+    ctx->key_cap[dst] = key_level;
+  else
+    ctx->key_cap.erase(dst);
+  return FESC_OK;
 }
 
 int fesc_key_store(fesc_ctx* ctx, uint32_t galois_elt, uint64_t* key, void* stream) {

@@ -141,6 +141,9 @@ struct Context {
   int32_t* d_enc_inv = nullptr;
   // keys: Galois element (0 = relinearisation) -> device [dnum][L+alpha][2][N]
   std::map<uint32_t, uint64_t*> keys;
+  // keys uploaded over a chain prefix: key buffer -> the highest level it
+  // serves (keys absent here serve every level)
+  std::map<const uint64_t*, uint32_t> key_cap;
   // basis-conversion / rescale constants, built on first use per level
   std::map<uint32_t, LevelTables> level_tabs;
   // scratch (grown on demand, freed with the context)

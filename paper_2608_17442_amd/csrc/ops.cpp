@@ -200,8 +200,14 @@ int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& sr
   // ModUp of every source (the scratch capacity covers all of them)
   const uint32_t ns = (uint32_t)srcs.size();
   if (ns > S.cap) return fail(FESC_ERR_ARG, "key-switch sources exceed the scratch capacity");
-  for (const KsJob& J : jobs)
+  for (const KsJob& J : jobs) {
     if (J.src >= ns) return fail(FESC_ERR_ARG, "key-switch job names a missing source");
+    auto cap = c->key_cap.find(J.key);
+    if (cap != c->key_cap.end() && level > cap->second)
+      return fail(FESC_ERR_LEVEL, "switching key uploaded for levels up to " +
+                                      std::to_string(cap->second) + ", used at level " +
+                                      std::to_string(level));
+  }
   // iNTT of the sources, stored as centred ModUp digits; ModUp fused with the
   // first forward pass of the extended rows; second pass (own-digit rows are
   // never written: the inner product reads them from the source)

@@ -57,6 +57,7 @@ _SIGS = {
     "fesc_keygen": [_vp, _u32, _vp, _vp, _vp, _vp],
     "fesc_key_load": [_vp, _u32, _vp, _vp],
     "fesc_key_store": [_vp, _u32, _vp, _vp],
+    "fesc_key_upload": [_vp, _u32, _vp, _u32, _vp],
     "fesc_encrypt_sk": [_vp, _vp, _vp, _vp, _vp, _vp, _u32, _vp],
     "fesc_plain_from_coeffs": [_vp, _vp, _vp, _u32, _vp],
     "fesc_encode": [_u32, _vp, _vp, ctypes.c_double, _vp],
@@ -108,17 +109,22 @@ def _check(rc: int) -> int:
     return rc
 
 
-def _ptr(t, words: int = 0, what: str = "buffer"):
-    """Device address of a contiguous CUDA int64 (residues, coefficients) or
-    int8 (secret) tensor holding at least `words` elements (None -> NULL)."""
+def _ptr(t, words: int = 0, what: str = "buffer", dtype=torch.int64):
+    """Device address of a contiguous CUDA tensor of `dtype` holding at least
+    `words` elements of that type (None -> NULL).  Residues, coefficients and
+    keys are int64 (8 bytes per word); only the secret is int8.  The size
+    check is in bytes, so no other element type can pass for a shorter
+    buffer than the library reads or writes."""
     if t is None:
         return None
-    if not (isinstance(t, torch.Tensor) and t.is_cuda and t.dtype in (torch.int64, torch.int8)):
-        raise TypeError(f"{what}: device buffers are CUDA int64 or int8 tensors")
+    if not (isinstance(t, torch.Tensor) and t.is_cuda and t.dtype == dtype):
+        raise TypeError(f"{what}: expected a CUDA {dtype} tensor")
     if not t.is_contiguous():
         raise ValueError(f"{what}: tensor must be contiguous")
-    if t.numel() < words:
-        raise ValueError(f"{what}: {t.numel()} elements, the call reads or writes {words}")
+    need = words * torch.empty((), dtype=dtype).element_size()
+    have = t.numel() * t.element_size()
+    if have < need:
+        raise ValueError(f"{what}: {have} bytes, the call reads or writes {need}")
     return t.data_ptr()
 
 
@@ -273,7 +279,7 @@ class Context:
 
     def keygen(self, galois_elt, s, a, e, stream=None):
         E = self.L + self.alpha
-        _check(_lib.fesc_keygen(self._h, galois_elt, _ptr(s, self.n, "s"),
+        _check(_lib.fesc_keygen(self._h, galois_elt, _ptr(s, self.n, "s", torch.int8),
                                 _ptr(a, self.dnum * E * self.n, "a"),
                                 _ptr(e, self.dnum * self.n, "e"), _stream(stream)))
 
@@ -281,12 +287,24 @@ class Context:
         _check(_lib.fesc_key_load(self._h, galois_elt, _ptr(key, self.key_words(), "key"),
                                   _stream(stream)))
 
+    def key_upload(self, galois_elt, host_key, key_level, stream=None):
+        """Host numpy uint64 key over the chain prefix of key_level primes,
+        [ceil(key_level/alpha)][key_level+alpha][2][N]."""
+        import numpy as np
+        hk = np.ascontiguousarray(host_key, dtype=np.uint64)
+        dk = -(-int(key_level) // self.alpha)
+        need = dk * (int(key_level) + self.alpha) * 2 * self.n
+        if hk.size < need:
+            raise ValueError(f"host_key: {hk.size} words, the call reads {need}")
+        _check(_lib.fesc_key_upload(self._h, galois_elt, hk.ctypes.data, key_level,
+                                    _stream(stream)))
+
     def key_store(self, galois_elt, key, stream=None):
         _check(_lib.fesc_key_store(self._h, galois_elt, _ptr(key, self.key_words(), "key"),
                                    _stream(stream)))
 
     def encrypt_sk(self, s, m, a, e, ct, level, stream=None):
-        _check(_lib.fesc_encrypt_sk(self._h, _ptr(s, self.n, "s"), _ptr(m, self.n, "m"),
+        _check(_lib.fesc_encrypt_sk(self._h, _ptr(s, self.n, "s", torch.int8), _ptr(m, self.n, "m"),
                                     _ptr(a, self._pt(level), "a"), _ptr(e, self.n, "e"),
                                     _ptr(ct, self._ct(level), "ct"), level, _stream(stream)))
 

@@ -25,6 +25,7 @@ __all__ = [
     "rounded_gaussian",
     "uniform_pm1",
     "normal",
+    "moduli_tag",
 ]
 
 
@@ -105,20 +106,38 @@ def secret(seed: int, n: int, h: int = SECRET_HAMMING_WEIGHT) -> np.ndarray:
     return ternary_secret(seed, n, h, tag="secret")
 
 
+def moduli_tag(moduli) -> str:
+    """Short digest of an ordered list of moduli.
+
+    Draws that belong to one modulus chain carry it in their tag: two key
+    sets (or encryptions) over chains that share a prefix then use
+    independent randomness.  Shared uniform rows and errors would let anyone
+    holding both sets subtract them and recover the secret (for two switching
+    keys of one Galois element, b - b' = (P - P') s' on the digit's rows)."""
+    h = hashlib.sha256(b"".join(int(m).to_bytes(8, "little") for m in moduli)).hexdigest()
+    return h[:16]
+
+
 def switch_key_draws(seed: int, ext_moduli, n: int, dnum: int, elt: int):
     """Raw draws of one switching key: ``a`` is ``u64[dnum][len(ext_moduli)][n]``
     uniform per modulus (already in evaluation form), ``e`` is
     ``int64[dnum][n]`` rounded-Gaussian coefficients.  ``elt`` names the key
-    (Galois element; 0 for the relinearisation key)."""
-    a = np.stack([uniform_residues(seed, "ksk-a", ext_moduli, n, elt, j) for j in range(dnum)])
-    e = np.stack([rounded_gaussian(seed, "ksk-e", n, ERROR_SIGMA, ERROR_BOUND, elt, j)
+    (Galois element; 0 for the relinearisation key).  The tags include the
+    extended modulus chain, so keys of one element in two contexts (e.g. a
+    context over a chain prefix with fewer special primes) are independent."""
+    mt = moduli_tag(ext_moduli)
+    a = np.stack([uniform_residues(seed, "ksk-a/" + mt, ext_moduli, n, elt, j)
+                  for j in range(dnum)])
+    e = np.stack([rounded_gaussian(seed, "ksk-e/" + mt, n, ERROR_SIGMA, ERROR_BOUND, elt, j)
                   for j in range(dnum)])
     return np.ascontiguousarray(a), np.ascontiguousarray(e)
 
 
 def encrypt_draws(seed: int, moduli, n: int, tag: str, *idx: int):
     """Raw draws of one secret-key encryption: ``a`` uniform ``u64[l][n]``
-    (evaluation form), ``e`` rounded-Gaussian ``int64[n]``."""
-    a = uniform_residues(seed, "enc-a/" + tag, moduli, n, *idx)
-    e = rounded_gaussian(seed, "enc-e/" + tag, n, ERROR_SIGMA, ERROR_BOUND, *idx)
+    (evaluation form), ``e`` rounded-Gaussian ``int64[n]``.  The tags include
+    the moduli, as for switching keys."""
+    mt = moduli_tag(moduli)
+    a = uniform_residues(seed, "enc-a/" + tag + "/" + mt, moduli, n, *idx)
+    e = rounded_gaussian(seed, "enc-e/" + tag + "/" + mt, n, ERROR_SIGMA, ERROR_BOUND, *idx)
     return a, e

@@ -43,12 +43,16 @@ class Setup:
             self.keys[g] = C.relin_key(P, self.sk, a, e) if g == 0 else \
                 C.galois_key(P, self.sk, g, a, e)
 
-    def encrypt(self, z, scale, level, idx):
-        """Encrypt on both sides from the same draws; returns (oracle, device)."""
+    def encrypt(self, z, scale, level, idx, oracle=True):
+        """Encrypt on both sides from the same draws; returns (oracle, device)
+        (oracle None when not asked for)."""
         P = self.P
         m = C.enc.encode(np.asarray(z, dtype=np.complex128), scale, P.n)
         a, e = synth.encrypt_draws(self.seed, P.qs(level), P.n, "gpu", idx)
-        ct_o = C.encrypt(P, self.sk, C.ntt(P, C.lift(m, P.qs(level)), P.qs(level)), level, a, e)
+        ct_o = None
+        if oracle:
+            ct_o = C.encrypt(P, self.sk, C.ntt(P, C.lift(m, P.qs(level)), P.qs(level)), level,
+                             a, e)
         ct_d = torch.zeros(level * 2 * P.n, dtype=torch.int64, device="cuda")
         step(f"encrypt level={level} idx={idx}")
         self.ctx.encrypt_sk(self.s_dev, torch.from_numpy(m).cuda(), to_dev(a),
@@ -162,7 +166,10 @@ def test_mul_relin(log_n, bits, L, alpha):
         # aliasing the first operand
         S.ctx.mul_relin(ad, bd, ad, level)
         _eq(ad, want, "mul_relin in place")
-        # value check only: operands at scale 2^20 carry encryption noise ~2^-15
+        # value check only.  A fresh ciphertext at scale 2^20 carries slot noise
+        # of about sigma sqrt(N) / 2^20 <= 3.2 * 2^6.5 / 2^20 ~ 2^-11.8 (N <= 2^13);
+        # the product's error is about |z1| e2 + |z2| e1 (|z| <= sqrt 2), ~2^-10.3
+        # typical and a few times that at the worst slot: 2^-7 leaves a margin
         np.testing.assert_allclose(C.decrypt(P, S.sk, want, 2.0 ** 40), z1 * z2, atol=2.0 ** -7)
 
 
@@ -228,6 +235,106 @@ def test_cfg3_full_size_rotations():
         assert np.max(np.abs(got - np.roll(z, -r))) < 2.0 ** -15
 
 
+def test_cfg3_rotation_set_as_benched():
+    """The rotation set in the launch configuration the benchmark times: all
+    32 fresh ciphertexts (N = 2^16, 24 limbs, dnum 3, 8 special primes) in ONE
+    fesc_rotate_batch call, ciphertext i by 2^(i mod 16): 30 key switches
+    under 15 keys (two jobs per key group of the key-stationary inner
+    product) and two identity copies.  Every output is compared residue by
+    residue with the oracle's single rotation and decoded within 2^-15."""
+    import synth.workloads as WL
+    P = C.params_p16()
+    steps = WL.cfg3_steps()
+    S = Setup(P, WL.CFG3["seed"], rot_steps=steps)
+    assert len(S.keys) == 15
+    cts = []
+    for i in range(len(steps)):
+        cts.append(S.encrypt(WL.cfg3_slots(i, P.n // 2), 2.0 ** 40, 24, 1000 + i))
+    outs = [torch.zeros_like(cts[0][1]) for _ in steps]
+    step("cfg3 rotate_batch of 32 ciphertexts")
+    S.ctx.rotate_batch([d for _, d in cts], steps, outs, 24)
+    torch.cuda.synchronize()
+    for i, ((co, _), r, o) in enumerate(zip(cts, steps, outs)):
+        want = C.rotate(P, co, r, S.keys)
+        _eq(o, want, f"cfg3 batch item {i} step {r}")
+        got = C.decrypt(P, S.sk, want, 2.0 ** 40)
+        err = np.max(np.abs(got - np.roll(WL.cfg3_slots(i, P.n // 2), -r)))
+        assert err < 2.0 ** -15, f"item {i}: decoded error {err:.3e}"
+
+
+def test_mul_relin_full_size_and_square():
+    """Relinearised product at N = 2^16 with the 24-limb chain (dnum 3,
+    8 special primes): a * b at levels 24 and 20 (a partial last digit), and
+    the square a * a with a, b and out the same buffer (the NeRMS square),
+    bit-exact against the oracle and decoded within 2^-15 at scale 2^80."""
+    P = C.params_p16()
+    S = Setup(P, 15, relin=True)
+    for level in (24, 20):
+        z1, z2 = _z(60 + level, P.n // 2), _z(70 + level, P.n // 2)
+        ao, ad = S.encrypt(z1, 2.0 ** 40, level, 600 + level)
+        bo, bd = S.encrypt(z2, 2.0 ** 40, level, 700 + level)
+        out = torch.zeros_like(ad)
+        step(f"mul_relin full size level={level}")
+        S.ctx.mul_relin(ad, bd, out, level)
+        want = C.mul_relin(P, ao, bo, S.keys[0])
+        _eq(out, want, f"mul_relin full size level={level}")
+        err = np.max(np.abs(C.decrypt(P, S.sk, want, 2.0 ** 80) - z1 * z2))
+        assert err < 2.0 ** -15, f"product level {level}: {err:.3e}"
+        step(f"square in place level={level}")
+        S.ctx.mul_relin(ad, ad, ad, level)
+        want_sq = C.mul_relin(P, ao, ao, S.keys[0])
+        _eq(ad, want_sq, f"square in place level={level}")
+        err = np.max(np.abs(C.decrypt(P, S.sk, want_sq, 2.0 ** 80) - z1 * z1))
+        assert err < 2.0 ** -15, f"square level {level}: {err:.3e}"
+
+
+def test_key_upload_from_host_over_a_chain_prefix():
+    """fesc_key_upload: a key made by the oracle (the client's side) over the
+    chain prefix of key_level = 3 primes ([2 digits][3 + 2 rows][2][N]) and
+    uploaded from host memory serves rotations at levels 3, 2 and 1
+    bit-exactly and is refused at level 4; a full-chain upload equals the
+    oracle's key word for word; Galois elements that name no automorphism are
+    refused by upload and load alike."""
+    from paper_2608_17442_amd import fesc as F
+    P = C.params_small(12, 50, 5, 2)
+    S = Setup(P, 16)
+    g = P.galois_elt(3)
+    a, e = synth.switch_key_draws(16, P.ext(P.L), P.n, P.dnum, g)
+    kfull = C.galois_key(P, S.sk, g, a, e)
+    key_level = 3
+    dk = -(-key_level // P.alpha)
+    host = np.ascontiguousarray(np.concatenate([kfull[:dk, :key_level], kfull[:dk, P.L:]],
+                                               axis=1))
+    step("key_upload prefix key")
+    S.ctx.key_upload(g, host, key_level)
+    for level in (3, 2, 1):
+        co, cd = S.encrypt(_z(90 + level, P.n // 2), 2.0 ** 30, level, 900 + level)
+        out = torch.zeros_like(cd)
+        step(f"rotate with uploaded prefix key, level {level}")
+        S.ctx.rotate(cd, out, level, 3)
+        _eq(out, C.rotate(P, co, 3, {g: kfull}), f"uploaded key level {level}")
+    _, c4 = S.encrypt(_z(94, P.n // 2), 2.0 ** 30, 4, 904)
+    with pytest.raises(F.FescError) as err:
+        S.ctx.rotate(c4, torch.zeros_like(c4), 4, 3)
+    assert err.value.code == -2
+    step("key_upload full chain")
+    S.ctx.key_upload(g, kfull, P.L)
+    back = torch.zeros(S.ctx.key_words(), dtype=torch.int64, device="cuda")
+    S.ctx.key_store(g, back)
+    _eq(back, kfull, "full-chain upload")
+    co, cd = S.encrypt(_z(95, P.n // 2), 2.0 ** 30, P.L, 905)
+    out = torch.zeros_like(cd)
+    S.ctx.rotate(cd, out, P.L, 3)
+    _eq(out, C.rotate(P, co, 3, {g: kfull}), "uploaded key at the top level")
+    for bad in (1, 2, 2 * P.n + 1):
+        with pytest.raises(F.FescError) as err:
+            S.ctx.key_upload(bad, kfull, P.L)
+        assert err.value.code == -1
+        with pytest.raises(F.FescError) as err:
+            S.ctx.key_load(bad, back)
+        assert err.value.code == -1
+
+
 def test_empty_batches_are_rejected():
     """A zero batch is an argument error (nothing launched), for the NTT and
     for batched rotations."""
@@ -263,4 +370,16 @@ def test_binding_rejects_short_buffers():
         ctx.rotate_batch([ct, ct], [1], [ct, ct], 3)
     with pytest.raises(TypeError):
         ctx.add(ct.cpu(), ct, ct, 3)
+    # a tensor of another element type holding as many elements as the call
+    # needs words is 1/8 (int8) of the bytes, or no residues at all (fp64):
+    # rejected by type, whatever its length
+    for dt in (torch.int8, torch.int32, torch.float64):
+        other = torch.zeros(3 * 2 * P.n, dtype=dt, device="cuda")
+        with pytest.raises(TypeError, match="out"):
+            ctx.rescale(ct, other, 3)
+        with pytest.raises(TypeError, match="^a: "):
+            ctx.add(other, ct, ct, 3)
+    # the secret is the one int8 argument, and it must be int8
+    with pytest.raises(TypeError, match="^s: "):
+        ctx.encrypt_sk(ct[:P.n], ct[:P.n], ct, ct[:P.n], ct, 1)
     assert torch.count_nonzero(ct).item() == 0

@@ -1,7 +1,8 @@
 """GPU parity of the device encoder (fesc_encode_plain) against the oracle's
 encoding.  The integer coefficients are recovered from the first limb and must
-equal the oracle's except where Delta m_k lies within the FFTs' rounding of a
-half-integer (+-1 there, as for the host encoder); every limb must then equal
+equal the oracle's except where Delta m_k lies within the FFTs' rounding error
+of a half-integer (+-1 there, as for the host encoder; the band is derived from
+the fp64 FFT error); every limb must then equal
 the oracle's lift and NTT of those coefficients exactly.  N = 2^12 (one pass),
 2^13 (a 2-point column pass) and 2^16 (16-point columns), and more plaintexts
 than one scratch round holds."""
@@ -50,7 +51,13 @@ def test_encode_plain_matches_oracle(log_n, L, level, count, kind):
         want = E.encode(zs[b], scale, n)
         raw = E.encode_real_coeffs(zs[b], scale, n)
         diff = m - want
-        near_tie = np.abs(np.abs(raw - np.trunc(raw)) - 0.5) < 1e-2
+        # Each fp64 FFT (the device's and the oracle's) leaves an error on
+        # Delta m_k of order est = Delta 2^-53 log2(N) rms|z| / sqrt(N) (the
+        # oracle's stays below est against a long-double direct sum, a CPU
+        # test); only a coefficient within 8 est of a half-integer may round
+        # differently on the two sides.
+        band = 8 * scale * 2.0 ** -53 * log_n * np.sqrt(np.mean(np.abs(zs[b]) ** 2)) / np.sqrt(n)
+        near_tie = np.abs(np.abs(raw - np.trunc(raw)) - 0.5) < band
         assert np.all(np.abs(diff) <= 1), b
         assert not np.any(diff[~near_tie]), (b, np.flatnonzero(diff[~near_tie])[:8])
         # every limb is the exact lift and transform of those coefficients

@@ -1,8 +1,8 @@
 """GPU parity of the scan-contract slice against the oracle: a small ring with
-five chunks, blocks of tokens, and one full-size Mamba-2-base token (N = 2^16,
+five chunks, blocks of tokens, one full-size Mamba-2-base token (N = 2^16,
 12 state chunks of 128 channels x d_state 128, level 20 -> 18), also run as a
-16-token block (the benchmark's launch configuration) of copies that must all
-equal it."""
+16-token block of copies that must all equal it, and the benchmark's pool of
+16 distinct tokens in one call (tokens 0, 7 and 15 compared)."""
 import numpy as np
 import pytest
 import torch
@@ -119,6 +119,45 @@ def test_cfg5_one_token_full_size():
         err = np.max(np.abs(dec - want[k * c_state:(k + 1) * c_state]))
         print(f"cfg5 chunk {k}: max |decoded - fp64| = {err:.3e}")
         assert err <= 2.0 ** -15
+
+
+def test_cfg5_pool_of_distinct_tokens():
+    """The benchmark's launch configuration with its real inputs: the 16
+    distinct tokens of the cfg5 pool (N = 2^16, 12 state chunks, level
+    20 -> 18) in ONE fesc_scan_contract call, token-major.  Tokens 0, 7 and 15
+    are compared with the oracle's one-token slice on every residue of all 12
+    chunk outputs, so a token-index mix-up in the batched products, the
+    rotation batches over all tokens or the pairing kernel would show."""
+    P = C.params_p16(24)
+    cfg = WL.CFG5
+    d_s, head_dim, level, T = cfg["d_state"], cfg["head_dim"], cfg["level"], cfg["pool"]
+    n_slots, s_state = P.n // 2, 16384
+    K = cfg["heads"] * head_dim * d_s // s_state
+    S = Setup(P, cfg["seed"], rot_steps=[d_s >> k for k in range(1, 8)], relin=True, conj=True)
+    check = (0, 7, T - 1)
+    dev = ([], [], [])
+    orc = {u: ([], [], []) for u in check}
+    for u in range(T):
+        z, cvec, H = WL.cfg5_token(u)
+        for k, vals in enumerate(chunk_slots(z, cvec, H, K, n_slots, d_s, head_dim, s_state)):
+            scales = (2.0 ** 40, float(P.q[level - 1]), float(P.q[level - 2]))
+            for r in range(3):
+                co, cd = S.encrypt(vals[r].astype(complex), scales[r], level,
+                                   9000 + 3 * (u * K + k) + r, oracle=u in check)
+                dev[r].append(cd)
+                if u in check:
+                    orc[u][r].append(co)
+    outs = [torch.zeros((level - 2) * 2 * P.n, dtype=torch.int64, device="cuda")
+            for _ in range(K * T)]
+    step(f"scan_contract cfg5 pool: {T} distinct tokens x {K} chunks")
+    S.ctx.scan_contract(dev[0], dev[1], dev[2], d_s, outs, level, tokens=T)
+    torch.cuda.synchronize()
+    for u in check:
+        want = OW.scan_contract_token(P, *orc[u], S.keys[0], S.keys, d_s)
+        for k in range(K):
+            got = to_host(outs[u * K + k]).reshape(want[k].shape)
+            assert np.array_equal(got, want[k]), \
+                f"pool token {u} chunk {k}: {first_mismatch(got, want[k])}"
 
 
 @pytest.mark.parametrize("K,T", [(4, 3), (5, 2), (2, 17), (2, 65)])

@@ -64,6 +64,26 @@ def test_encode_rounding_half_away_from_zero():
     assert E.encode(np.zeros(n // 2), 2.0 ** 30, n).dtype == np.int64
 
 
+@pytest.mark.parametrize("log_n,scale", [(12, 2.0 ** 30), (14, 2.0 ** 40)])
+def test_encode_fft_error_within_estimate(log_n, scale):
+    """The encoder's fp64 FFT error on Delta m_k stays below
+    est = Delta 2^-53 log2(N) rms|z| / sqrt(N) (checked against a direct
+    long-double sum over the definition on a sample of coefficients); the
+    device encoder's parity band is a multiple of this estimate."""
+    n = 1 << log_n
+    z = _z(80 + log_n, n // 2)
+    raw = E.encode_real_coeffs(z, scale, n)
+    e = E.slot_exponents(n // 2, 2 * n).astype(np.longdouble)
+    pi = np.longdouble("3.14159265358979323846264338327950288")
+    zl = z.astype(np.clongdouble)
+    ks = np.arange(0, n, n // 256)
+    exact = np.array([2 * np.sum(zl * np.exp(-1j * pi * ((e * k) % (2 * n)) / n)).real / n
+                      for k in ks], dtype=np.longdouble) * np.longdouble(scale)
+    err = np.abs(raw[ks].astype(np.longdouble) - exact).astype(float)
+    est = scale * 2.0 ** -53 * log_n * np.sqrt(np.mean(np.abs(z) ** 2)) / np.sqrt(n)
+    assert err.max() < est, (err.max(), est)
+
+
 def test_encoding_is_a_ring_homomorphism():
     """encode(z1) * encode(z2) (negacyclic) decodes to z1 * z2;
     X -> X^(5^r) rotates left by r; X -> X^(2N-1) conjugates;
@@ -323,3 +343,42 @@ def test_p12_parameters_roundtrip():
     out = C.rotate_hoisted(P, ct, [1], keys)[0]
     np.testing.assert_allclose(C.decrypt(P, sk, out, float(P.q[2])), np.roll(z, -1),
                                atol=2.0 ** -20)
+
+
+def test_key_sets_over_a_shared_chain_prefix_are_independent():
+    """A second key set over the chain prefix q_0..q_3 with fewer special
+    primes (the contraction's context) must not reuse the first set's
+    randomness: with shared uniform rows and errors, two keys of one Galois
+    element differ on a digit row only by (P - P') s', which gives the secret
+    away.  The draws are tagged with the modulus chain, so the attack fails;
+    planting shared draws shows that it would succeed."""
+    Pf = C.params_small(10, 50, 8, 4)
+    Pc = C.Params(Pf.log_n, Pf.q[:4], Pf.p[:2], dict(Pf.psi))
+    s = synth.secret(9, Pf.n)
+    skf, skc = C.secret_key(Pf, s), C.secret_key(Pc, s)
+    g = Pf.galois_elt(1)
+    af, ef = synth.switch_key_draws(9, Pf.ext(Pf.L), Pf.n, Pf.dnum, g)
+    ac, ec = synth.switch_key_draws(9, Pc.ext(Pc.L), Pc.n, Pc.dnum, g)
+    assert not np.array_equal(af[0, :4], ac[0, :4])
+    assert not np.array_equal(ef[0], ec[0])
+    # encryptions over one chain at two lengths are independent as well
+    e1 = synth.encrypt_draws(9, Pf.qs(8), Pf.n, "t", 0)
+    e2 = synth.encrypt_draws(9, Pf.qs(4), Pf.n, "t", 0)
+    assert not np.array_equal(e1[0][:4], e2[0]) and not np.array_equal(e1[1], e2[1])
+
+    q0 = Pf.q[0]
+    s_g = C.ntt(Pf, C.automorph_coef(Pf, C.lift(s.astype(np.int64), [q0]), [q0], g), [q0])[0]
+    inv = pow((Pf.P - Pc.P) % q0, -1, q0)
+
+    def recovered(kc):
+        kf = C.galois_key(Pf, skf, g, af, ef)
+        d = (kf[0, 0, 0].astype(object) - kc[0, 0, 0].astype(object)) % q0
+        return np.array([(int(v) * inv) % q0 for v in d], dtype=np.uint64)
+
+    assert not np.array_equal(recovered(C.galois_key(Pc, skc, g, ac, ec)), s_g)
+    # the planted mistake: the prefix context's rows taken from the first set
+    rows = list(range(4)) + [Pf.L + k for k in range(Pc.alpha)]
+    a_shared = np.ascontiguousarray(af[:Pc.dnum][:, rows])
+    e_shared = np.ascontiguousarray(ef[:Pc.dnum])
+    np.testing.assert_array_equal(
+        recovered(C.galois_key(Pc, skc, g, a_shared, e_shared)), s_g)
