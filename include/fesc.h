@@ -198,6 +198,24 @@ int fesc_rotate_batch(fesc_ctx* ctx, uint32_t count, const uint64_t* const* ins,
                       const int32_t* steps, uint64_t* const* outs, uint32_t level,
                       void* stream);
 
+/* For callers that cannot allocate device memory (work under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * rotation batch of fesc_rotate_batch with the same arguments, results
+ * (residue for residue) and errors, whose key-switch temporaries live in a
+ * statically allocated device array of 256 MiB per GPU (held by each GPU the
+ * library runs on until the process ends) instead of the context's scratch.
+ * It calls no allocating routine: the context builds its per-level constants
+ * and looks up the array's device address when it is created.  Rotations run
+ * in groups of as many as fit (two at N = 2^16 with 24 limbs and 8 special
+ * primes, 32 on small rings).  FESC_ERR_ARG, before any launch, if one
+ * rotation at `level` needs more than the array: level + dnum_l (level +
+ * alpha) + 2 (level + alpha) + 2 level rows of N words, dnum_l =
+ * ceil(level / alpha).  All calls on one GPU share the array, so calls that
+ * overlap on one GPU (two streams, threads or contexts) race. */
+int fesc_rotate_batch_noalloc(fesc_ctx* ctx, uint32_t count, const uint64_t* const* ins,
+                              const int32_t* steps, uint64_t* const* outs, uint32_t level,
+                              void* stream);
+
 /* Switching-key generation on the device from caller-drawn randomness:
  * s: int8[N] ternary secret coefficients; a: uint64[dnum][L+alpha][N] uniform
  * residues (evaluation form); e: int64[dnum][N] error coefficients.  For

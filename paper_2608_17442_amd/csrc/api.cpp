@@ -258,9 +258,8 @@ int fesc_rotate_hoisted(fesc_ctx* ctx, const uint64_t* in, uint32_t count, const
   return op_rotate_many(ctx, in, count, steps, outs, level, S(stream));
 }
 
-int fesc_rotate_batch(fesc_ctx* ctx, uint32_t count, const uint64_t* const* ins,
-                      const int32_t* steps, uint64_t* const* outs, uint32_t level,
-                      void* stream) {
+static int check_rotate_batch(fesc_ctx* ctx, uint32_t count, const uint64_t* const* ins,
+                              const int32_t* steps, uint64_t* const* outs, uint32_t level) {
   int rc = check_level(ctx, level);
   if (rc) return rc;
   if (!ins || !steps || !outs || count == 0) return fail(FESC_ERR_ARG, "bad batch arguments");
@@ -274,7 +273,29 @@ int fesc_rotate_batch(fesc_ctx* ctx, uint32_t count, const uint64_t* const* ins,
     if (g != 1 && !ctx->keys.count(g))
       return fail(FESC_ERR_NO_KEY, "no switching key for Galois element " + std::to_string(g));
   }
+  return FESC_OK;
+}
+
+int fesc_rotate_batch(fesc_ctx* ctx, uint32_t count, const uint64_t* const* ins,
+                      const int32_t* steps, uint64_t* const* outs, uint32_t level,
+                      void* stream) {
+  int rc = check_rotate_batch(ctx, count, ins, steps, outs, level);
+  if (rc) return rc;
   return op_rotate_batch(ctx, count, ins, steps, outs, nullptr, level, S(stream));
+}
+
+int fesc_rotate_batch_noalloc(fesc_ctx* ctx, uint32_t count, const uint64_t* const* ins,
+                              const int32_t* steps, uint64_t* const* outs, uint32_t level,
+                              void* stream) {
+  if (ctx && level >= 1 && level <= ctx->L &&
+      rotate_scratch_words(ctx, level) * sizeof(uint64_t) > static_scratch_bytes())
+    return fail(FESC_ERR_ARG, "one rotation at level " + std::to_string(level) + " needs " +
+                                  std::to_string(rotate_scratch_words(ctx, level) * 8) +
+                                  " bytes of scratch; the static scratch holds " +
+                                  std::to_string(static_scratch_bytes()));
+  int rc = check_rotate_batch(ctx, count, ins, steps, outs, level);
+  if (rc) return rc;
+  return op_rotate_batch_static(ctx, count, ins, steps, outs, level, S(stream));
 }
 
 static int check_galois(const fesc_ctx* ctx, uint32_t galois_elt) {

@@ -149,6 +149,9 @@ struct Context {
   // scratch (grown on demand, freed with the context)
   void* scratch = nullptr;
   size_t scratch_bytes = 0;
+  // device address of the statically allocated scratch array on this
+  // context's device (the rotation batch that allocates nothing)
+  uint64_t* static_scratch = nullptr;
   hipStream_t stream = nullptr;   // default stream when callers pass null
 
   size_t ext_count() const { return primes.size(); }

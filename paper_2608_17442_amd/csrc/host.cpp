@@ -9,6 +9,7 @@
 #include <vector>
 
 #include "fesc_internal.hpp"
+#include "ops.hpp"
 
 namespace fesc {
 
@@ -311,6 +312,11 @@ int create(const fesc_params* p, fesc_ctx** out) {
   c->primes = primes;
   for (uint64_t q : primes) c->psi.push_back(h_min_root(q, p->log_n));
   int rc = build_tables(c);
+  // the per-level constants of every level up front, so that operations
+  // (the rotation batch that allocates nothing among them) find them built
+  for (uint32_t l = 1; l <= c->L && !rc; ++l)
+    if (!level_tables(c, l, &rc)) break;
+  if (!rc) rc = static_scratch_init(c);
   if (rc) {
     destroy(c);
     return rc;

@@ -179,7 +179,8 @@ hipError_t ntt_rows(const Context* c, uint64_t* d, uint32_t batch, size_t batch_
 // --------------------------------------------------------- key switch engine
 
 int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& srcs,
-                     const std::vector<KsJob>& jobs, hipStream_t s, uint32_t rescale_rows) {
+                     const std::vector<KsJob>& jobs, hipStream_t s, uint32_t rescale_rows,
+                     const Scratch* given) {
   if (jobs.empty()) return FESC_OK;
   if (rescale_rows && (level < 2 || rescale_rows > level - 1))
     return fail(FESC_ERR_LEVEL, "merged rescale needs level >= 2 and rows <= level - 1");
@@ -188,7 +189,10 @@ int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& sr
   const LevelTables* T = level_tables(c, level, &err);
   if (!T) return err;
   Scratch S;
-  if ((err = scratch(c, &S, (uint32_t)std::max(srcs.size(), jobs.size())))) return err;
+  if (given)
+    S = *given;
+  else if ((err = scratch(c, &S, (uint32_t)std::max(srcs.size(), jobs.size()))))
+    return err;
   const size_t n = c->n;
   const uint32_t E = level + c->alpha, dnum_l = (level + c->alpha - 1) / c->alpha;
   KsTable tab{};
@@ -333,11 +337,12 @@ int op_rotate_many(Context* c, const uint64_t* in, uint32_t count, const int32_t
 // (+ add2[i] when given).  Outputs must not alias inputs.
 int op_rotate_batch(Context* c, uint32_t count, const uint64_t* const* ins,
                     const int32_t* steps, uint64_t* const* outs, const uint64_t* const* add2,
-                    uint32_t level, hipStream_t s) {
+                    uint32_t level, hipStream_t s, const Scratch* given) {
   const size_t n = c->n, ct_words = (size_t)2 * level * n;
+  const uint32_t group = given ? given->cap : kMaxBatch;
   int err;
-  for (uint32_t b0 = 0; b0 < count; b0 += kMaxBatch) {
-    const uint32_t nb = std::min(kMaxBatch, count - b0);
+  for (uint32_t b0 = 0; b0 < count; b0 += group) {
+    const uint32_t nb = std::min(group, count - b0);
     std::vector<KsSource> srcs;
     std::vector<KsJob> jobs;
     for (uint32_t i = b0; i < b0 + nb; ++i) {
@@ -355,7 +360,7 @@ int op_rotate_batch(Context* c, uint32_t count, const uint64_t* const* ins,
       jobs.push_back(KsJob{(uint32_t)srcs.size(), key, g, ins[i], 1u, g, a2, outs[i]});
       srcs.push_back(KsSource{ins[i] + n, 2 * n});
     }
-    if ((err = key_switch_batch(c, level, srcs, jobs, s))) return err;
+    if ((err = key_switch_batch(c, level, srcs, jobs, s, 0, given))) return err;
   }
   return FESC_OK;
 }

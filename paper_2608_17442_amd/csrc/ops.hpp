@@ -154,14 +154,26 @@ static_assert(sizeof(KsTable) < 3072, "key-switch table must stay a small kernel
 // source or addend of another job.  rescale_rows > 0: ModDown is merged with
 // the rescale (one division by P q_{level-1}, every addend folded) and the
 // outputs are the first rescale_rows (<= level - 1) limbs at level - 1.
+// given: use this scratch (its capacity and regions) instead of the
+// context's, so that nothing is allocated; null: the context's scratch.
+struct Scratch;
 int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& srcs,
-                     const std::vector<KsJob>& jobs, hipStream_t s, uint32_t rescale_rows = 0);
+                     const std::vector<KsJob>& jobs, hipStream_t s, uint32_t rescale_rows = 0,
+                     const Scratch* given = nullptr);
 
 int op_rotate_many(Context* c, const uint64_t* in, uint32_t count, const int32_t* steps,
                    uint64_t* const* outs, uint32_t level, hipStream_t s);
 int op_rotate_batch(Context* c, uint32_t count, const uint64_t* const* ins,
                     const int32_t* steps, uint64_t* const* outs, const uint64_t* const* add2,
-                    uint32_t level, hipStream_t s);
+                    uint32_t level, hipStream_t s, const Scratch* given = nullptr);
+// noalloc.cpp: the statically allocated scratch of the device (set up by the
+// context's creation) and the rotation batch that runs in it.
+int static_scratch_init(Context* c);
+size_t static_scratch_bytes();
+size_t rotate_scratch_words(const Context* c, uint32_t level);
+int op_rotate_batch_static(Context* c, uint32_t count, const uint64_t* const* ins,
+                           const int32_t* steps, uint64_t* const* outs, uint32_t level,
+                           hipStream_t s);
 int op_rescale(Context* c, const uint64_t* in, uint64_t* out, uint32_t level, hipStream_t s);
 // Relinearised products out_i = a_i * b_i (batched); out_i may alias a_i or b_i.
 int op_mul_relin_many(Context* c, uint32_t count, const uint64_t* const* as,

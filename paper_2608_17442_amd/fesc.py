@@ -54,6 +54,8 @@ _SIGS = {
                             _vp],
     "fesc_rotate_batch": [_vp, _u32, ctypes.POINTER(_vp), ctypes.POINTER(_i32),
                           ctypes.POINTER(_vp), _u32, _vp],
+    "fesc_rotate_batch_noalloc": [_vp, _u32, ctypes.POINTER(_vp), ctypes.POINTER(_i32),
+                                  ctypes.POINTER(_vp), _u32, _vp],
     "fesc_keygen": [_vp, _u32, _vp, _vp, _vp, _vp],
     "fesc_key_load": [_vp, _u32, _vp, _vp],
     "fesc_key_store": [_vp, _u32, _vp, _vp],
@@ -276,6 +278,17 @@ class Context:
         _check(_lib.fesc_rotate_batch(self._h, m, _ptrs(cts, m, w, "cts"),
                                       (_i32 * max(m, 1))(*steps), _ptrs(outs, m, w, "outs"),
                                       level, _stream(stream)))
+
+    def rotate_batch_noalloc(self, cts, steps, outs, level, stream=None):
+        """fesc_rotate_batch_noalloc: the same batch with its temporaries in
+        the library's statically allocated device array (no allocation)."""
+        m, w = len(cts), self._ct(level)
+        if len(steps) != m:
+            raise ValueError(f"steps: {len(steps)} values, expected {m}")
+        _check(_lib.fesc_rotate_batch_noalloc(self._h, m, _ptrs(cts, m, w, "cts"),
+                                              (_i32 * max(m, 1))(*steps),
+                                              _ptrs(outs, m, w, "outs"), level,
+                                              _stream(stream)))
 
     def keygen(self, galois_elt, s, a, e, stream=None):
         E = self.L + self.alpha
