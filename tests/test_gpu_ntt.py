@@ -85,6 +85,54 @@ def test_ntt_strided_rows_leave_gaps_untouched():
     assert np.all(got[mask] == 7)
 
 
+@pytest.mark.parametrize("batch,limbs,gap", [(26, 5, 256), (128, 1, 0), (43, 3, 64)])
+def test_ntt_large_strided_batches(batch, limbs, gap):
+    """N = 2^16 launches of 128 to 130 rows: a row count that is not a
+    multiple of 8, one long batch of single limbs, strided rows with gaps that
+    must stay untouched; forward, round trip and inverse of arbitrary
+    residues against the oracle."""
+    P = C.params_small(16, 50, 6, 2)
+    ctx = _ctx(P)
+    n = P.n
+    mods = P.ext(P.L)
+    prime0 = 1
+    rows_p = [mods[prime0 + i] for i in range(limbs)]
+    ls, bs = n + gap, limbs * (n + gap) + gap
+    buf = np.full(batch * bs, 7, dtype=np.uint64)
+    data = {}
+    for b in range(batch):
+        for i in range(limbs):
+            r = synth.uniform_residues(90 + b, "sp", [rows_p[i]], n, i)[0]
+            if b == 0 and i == 0:
+                r[:4] = [0, 1, rows_p[0] - 1, rows_p[0] - 2]
+            data[(b, i)] = r
+            buf[b * bs + i * ls:b * bs + i * ls + n] = r
+    mask = np.ones_like(buf, dtype=bool)
+    for (b, i) in data:
+        mask[b * bs + i * ls:b * bs + i * ls + n] = False
+    d = to_dev(buf)
+    step(f"ntt_fwd batch={batch} limbs={limbs} gap={gap}")
+    ctx.ntt_fwd(d, batch, bs, limbs, ls, prime0)
+    got = to_host(d)
+    assert np.all(got[mask] == 7)
+    for (b, i), r in data.items():
+        o = b * bs + i * ls
+        want = C.ntt(P, r[None], [rows_p[i]])[0]
+        assert np.array_equal(got[o:o + n], want), (b, i, first_mismatch(got[o:o + n], want))
+    step("ntt_inv (round trip)")
+    ctx.ntt_inv(d, batch, bs, limbs, ls, prime0)
+    got = to_host(d)
+    assert np.array_equal(got, buf), first_mismatch(got, buf)
+    step("ntt_inv of arbitrary residues")
+    ctx.ntt_inv(d, batch, bs, limbs, ls, prime0)
+    got = to_host(d)
+    assert np.all(got[mask] == 7)
+    for (b, i), r in data.items():
+        o = b * bs + i * ls
+        want = C.intt(P, r[None], [rows_p[i]])[0]
+        assert np.array_equal(got[o:o + n], want), (b, i, first_mismatch(got[o:o + n], want))
+
+
 def test_bad_prime_range_is_rejected_before_launch():
     from paper_2608_17442_amd import fesc as F
     P = C.params_small(12, 50, 2, 1)
