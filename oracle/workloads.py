@@ -9,7 +9,9 @@ For output block b, giant step p and baby step q,
 
     c~_p = sum_u sum_q Phi^q(x~_u) * D~_{b,u,p,q},     y = sum_p Phi^(p n1)(c~_p),
 
-and the real lane is extracted as c + conj(c).  The paper leaves the content
+and the real lane is extracted as c + conj(c) (or, with complex-paired
+outputs, two real blocks leave as one ciphertext y_2P + conj(y_2P+1); see
+bsgs_pair_diagonal_slots).  The paper leaves the content
 of D~ implicit ("the two real weight slices"); the reading used here is
 
     diag_t^(g,b)[idx(r, s)] = W[g*C + (s + t) mod C, b*C + s]   (0 if out of range)
@@ -56,6 +58,9 @@ class MatvecDesc:
     unit: int            # slots per segment (Phi^1 = rotation by `unit`)
     real_extract: bool
     rescale: bool
+    # outputs in pairs: the n_out diagonal sets are taken as (2P, 2P+1) and
+    # output P is y_2P + conj(y_2P+1) (n_out / 2 output ciphertexts)
+    complex_pair: bool = False
 
     def baby_steps(self):
         return [q * self.unit for q in range(self.n1)]
@@ -77,8 +82,8 @@ def bsgs_matvec(P: C.Params, desc: MatvecDesc, ins: list, diag, keys: dict,
     steps and the conjugation are ordinary key switches."""
     assert len(ins) == desc.n_in
     baby = [C.rotate_hoisted(P, x, desc.baby_steps(), keys) for x in ins]
-    outs = []
-    for b in (range(desc.n_out) if blocks is None else blocks):
+
+    def giant_sum(b):
         y = None
         for p in range(desc.n2):
             acc = None
@@ -88,6 +93,17 @@ def bsgs_matvec(P: C.Params, desc: MatvecDesc, ins: list, diag, keys: dict,
                     acc = t if acc is None else C.ct_add(P, acc, t)
             acc = C.rotate(P, acc, desc.giant_steps()[p], keys)
             y = acc if y is None else C.ct_add(P, y, acc)
+        return y
+
+    outs = []
+    if desc.complex_pair:
+        # output P = y_2P + conj(y_2P+1); `blocks` names pairs P
+        for pair in (range(desc.n_out // 2) if blocks is None else blocks):
+            y = C.ct_add(P, giant_sum(2 * pair), C.conjugate(P, giant_sum(2 * pair + 1), keys))
+            outs.append(C.rescale(P, y) if desc.rescale else y)
+        return outs
+    for b in (range(desc.n_out) if blocks is None else blocks):
+        y = giant_sum(b)
         if desc.real_extract:
             y = C.ct_add(P, y, C.conjugate(P, y, keys))
         if desc.rescale:
@@ -142,6 +158,32 @@ def bsgs_diagonal_slots(W, n_slots, seg_len, C_, n1, b, p, u, q, paired: bool):
     else:
         d = diagonal(W, n_slots, seg_len, C_, u, b, t).astype(np.complex128)
     return shift_segments(d, -p * n1, seg_len)
+
+
+def bsgs_pair_diagonal_slots(W, n_slots, seg_len, C_, n1, v, p, u, q):
+    """Diagonal set v = 2P + e of complex-paired outputs (paired inputs).
+
+    Output pair P carries real blocks b = 2P (real part) and b' = 2P + 1
+    (imaginary part).  Per slot, with x~ = x0 + i x1 the paired input and
+    a = diag^(2u,b), c = diag^(2u+1,b), d = diag^(2u,b'), f = diag^(2u+1,b'),
+    the wanted S_b + i S_b' = (a x0 + c x1) + i (d x0 + f x1) equals
+    alpha x~ + beta conj(x~) with alpha = ((a + f) + i (d - c)) / 2 and
+    beta = ((a - f) + i (d + c)) / 2.  Rotations commute with conjugation, so
+    the beta part is the conjugate of a second accumulation over the same
+    baby steps with conj(beta): set e = 0 holds alpha, set e = 1 holds
+    conj(beta), and output P = y_2P + conj(y_2P+1).  With b' = b this is the
+    real extraction (alpha = conj(beta))."""
+    t = p * n1 + q
+    pair, e = v // 2, v % 2
+    a = diagonal(W, n_slots, seg_len, C_, 2 * u, 2 * pair, t)
+    c = diagonal(W, n_slots, seg_len, C_, 2 * u + 1, 2 * pair, t)
+    d = diagonal(W, n_slots, seg_len, C_, 2 * u, 2 * pair + 1, t)
+    f = diagonal(W, n_slots, seg_len, C_, 2 * u + 1, 2 * pair + 1, t)
+    if e == 0:
+        z = 0.5 * (a + f) + 1j * (0.5 * (d - c))
+    else:
+        z = 0.5 * (a - f) - 1j * (0.5 * (d + c))
+    return shift_segments(z, -p * n1, seg_len)
 
 
 # -------------------------------------------------- scan-contract slice

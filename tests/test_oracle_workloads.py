@@ -60,6 +60,37 @@ def test_bsgs_slot_algebra_is_the_matrix_product(paired):
             np.testing.assert_allclose(y.imag, 0, atol=1e-12)
 
 
+def test_bsgs_complex_paired_outputs_slot_algebra():
+    """Complex-paired outputs: set 2P accumulates alpha, set 2P+1 conj(beta),
+    and y_2P + conj(y_2P+1) carries output blocks 2P and 2P+1 as its real and
+    imaginary parts (checked on plain slot vectors against X W in fp64)."""
+    n_slots, seg_len, Cc = 256, 8, 32
+    T, d_in, d_out = 8, 128, 128
+    X = synth.normal(5, "X", (T, d_in))
+    Wm = synth.normal(5, "W", (d_in, d_out), 0.1)
+    Y = X @ Wm
+    n_in, n_out = d_in // Cc // 2, d_out // Cc
+    xs = [W.pack_input(X, n_slots, seg_len, Cc, 2 * u)
+          + 1j * W.pack_input(X, n_slots, seg_len, Cc, 2 * u + 1) for u in range(n_in)]
+    r, s = W.segment_indices(n_slots, seg_len, Cc)
+    for n1, n2 in [(8, 4), (32, 1), (4, 8)]:
+        ys = []
+        for v in range(n_out):
+            y = 0
+            for p in range(n2):
+                acc = 0
+                for u in range(n_in):
+                    for q in range(n1):
+                        acc = acc + W.shift_segments(xs[u], q, seg_len) * \
+                            W.bsgs_pair_diagonal_slots(Wm, n_slots, seg_len, Cc, n1, v, p, u, q)
+                y = y + W.shift_segments(acc, p * n1, seg_len)
+            ys.append(y)
+        for pair in range(n_out // 2):
+            out = ys[2 * pair] + np.conj(ys[2 * pair + 1])
+            np.testing.assert_allclose(out.real, Y[r, 2 * pair * Cc + s], atol=1e-12)
+            np.testing.assert_allclose(out.imag, Y[r, (2 * pair + 1) * Cc + s], atol=1e-12)
+
+
 def test_replicated_diagonal_method_slot_algebra():
     """cfg1 shape: U x with x replicated to fill the slots, n1 = d, n2 = 1."""
     d, n_slots = 16, 128
@@ -97,6 +128,40 @@ def test_encrypted_bsgs_matvec_paired():
         dec = C.decrypt(P, sk, y, 2.0 ** 40)
         np.testing.assert_allclose(dec.real, Y[r, b * Cc + s], atol=2.0 ** -15)
         np.testing.assert_allclose(dec.imag, 0, atol=2.0 ** -15)
+
+
+def test_encrypted_bsgs_matvec_complex_paired_outputs():
+    """The encrypted projection with complex-paired outputs decodes to output
+    blocks 2P (real part) and 2P+1 (imaginary part) within 2^-15."""
+    P = C.params_small(10, 50, 4, 2)
+    sk = C.secret_key(P, synth.secret(3, P.n))
+    n_slots, seg_len, Cc = P.n // 2, 16, 32
+    T, d_in, d_out = 16, 128, 128
+    n1, n2 = 8, 4
+    level = 4
+    X = synth.normal(6, "X", (T, d_in))
+    Wm = synth.normal(6, "W", (d_in, d_out), 0.02)
+    desc = W.MatvecDesc(level, d_in // Cc // 2, d_out // Cc, n1, n2, seg_len, False, True,
+                        complex_pair=True)
+    keys = _keys(P, sk, 3, W.required_rotations(desc, n_slots), conj=True)
+    ins = []
+    for u in range(desc.n_in):
+        z = (W.pack_input(X, n_slots, seg_len, Cc, 2 * u)
+             + 1j * W.pack_input(X, n_slots, seg_len, Cc, 2 * u + 1))
+        a, e = synth.encrypt_draws(3, P.qs(level), P.n, "xp", u)
+        ins.append(C.encrypt(P, sk, C.encode_plain(P, z, 2.0 ** 40, level), level, a, e))
+    ql = float(P.q[level - 1])
+    diag = lambda v, p, u, q: C.encode_plain(
+        P, W.bsgs_pair_diagonal_slots(Wm, n_slots, seg_len, Cc, n1, v, p, u, q), ql, level)
+    outs = W.bsgs_matvec(P, desc, ins, diag, keys)
+    assert len(outs) == desc.n_out // 2
+    Y = X @ Wm
+    r, s = W.segment_indices(n_slots, seg_len, Cc)
+    for pair, y in enumerate(outs):
+        assert y.shape[0] == level - 1
+        dec = C.decrypt(P, sk, y, 2.0 ** 40)
+        np.testing.assert_allclose(dec.real, Y[r, 2 * pair * Cc + s], atol=2.0 ** -15)
+        np.testing.assert_allclose(dec.imag, Y[r, (2 * pair + 1) * Cc + s], atol=2.0 ** -15)
 
 
 def test_scan_contract_slice_small():
