@@ -12,9 +12,9 @@ Metric (three workloads, all N = 2^16 with ~50-bit primes = 1 mod 2N; the
          (seed 2): 30 key switches + 2 identity copies.  keyswitch/s = 30 / t.
   MATVEC 768 x 1536 plaintext weight (N(0, 0.02^2)) times 1024 tokens x 768
          features (N(0,1)) packed as 12 complex-paired ciphertexts at 16 limbs,
-         BSGS n1 = 16, n2 = 2 over 32 segments of 1024 slots, real extraction
-         and rescale -> 48 ciphertexts (seed 3); 18,432 pre-encoded diagonals
-         (154.6 GB) resident in HBM.
+         BSGS n1 = 16, n2 = 2 over 32 segments of 1024 slots, complex-paired
+         outputs and rescale -> 24 ciphertexts carrying the 48 output blocks
+         (seed 3); 18,432 pre-encoded diagonals (154.6 GB) resident in HBM.
 
   SCAN   scan-contract slice of a block of 16 distinct Mamba-base tokens (24
          heads x 64 channels x d_state 128 in 12 state chunks of 16,384 slots,
@@ -39,7 +39,6 @@ Prints ONE JSON line on stdout.  --gpus > 1 is refused (single-GPU build).
 from __future__ import annotations
 
 import argparse
-import concurrent.futures as cf
 import json
 import os
 import sys
@@ -212,43 +211,34 @@ class Workloads:
         X, W = WL.cfg4_values()
         self.mv_in = [self.encrypt(PK.paired_input(X, u, n_slots, seg, Cc), 2.0 ** 40, level,
                                    seed, "cfg4", u) for u in range(n_in)]
+        # complex-paired outputs: 48 diagonal sets, output blocks (2P, 2P+1)
+        # leave as the real and imaginary parts of output ciphertext P
         n_diag = n_out * n2 * n_in * n1
-        desc = self.F.matvec_desc(level, n_in, n_out, n1, n2, seg, True, True)
+        desc = self.F.matvec_desc(level, n_in, n_out, n1, n2, seg, False, True, True)
         self.bank_bytes = 8 * self.F.matvec_bank_words(self.ctx, desc)
         log(f"encoding {n_diag} diagonals ({self.bank_bytes / 1e9:.1f} GB bank)")
         self.bank = torch.empty(self.bank_bytes // 8, dtype=torch.int64, device="cuda")
         scale = float(self.q[level - 1])
-        index = [(b, p, u, q) for b in range(n_out) for p in range(n2) for u in range(n_in)
-                 for q in range(n1)]
-
-        def slots_one(t):
-            b, p, u, q = index[t]
-            return PK.diagonal_slots(W, b, p, u, q, n1, n_slots, seg, Cc, True)
-
-        # slot values on the host (numpy, threads); encoding, lift, NTT and
-        # packing on the device
+        # slot values, encoding, lift, NTT and packing all on the device
         t0 = time.perf_counter()
         chunk = 128
-        workers = min(16, os.cpu_count() or 1)
+        Wd = torch.from_numpy(np.ascontiguousarray(W)).cuda()
+        zs = torch.empty((chunk, n_slots), dtype=torch.complex128, device="cuda")
         pts = torch.empty((chunk, level * self.n), dtype=torch.int64, device="cuda")
-        host_s = 0.0
-        with cf.ThreadPoolExecutor(workers) as ex:
-            for c0 in range(0, n_diag, chunk):
-                ids = list(range(c0, min(c0 + chunk, n_diag)))
-                h0 = time.perf_counter()
-                z = torch.from_numpy(np.stack(list(ex.map(slots_one, ids)))).cuda()
-                host_s += time.perf_counter() - h0
-                self.ctx.encode_plain(z, scale, pts[:len(ids)], level)
-                for j, t in enumerate(ids):
-                    self.F.matvec_bank_pack(self.ctx, desc, self.bank, t, pts[j])
+        for c0 in range(0, n_diag, chunk):
+            m = min(chunk, n_diag - c0)
+            self.F.bsgs_diagonal_slots(self.ctx, desc, Wd, Cc, c0, m, zs)
+            self.ctx.encode_plain(zs[:m], scale, pts[:m], level)
+            for j in range(m):
+                self.F.matvec_bank_pack(self.ctx, desc, self.bank, c0 + j, pts[j])
         torch.cuda.synchronize()
+        del Wd, zs, pts
         self.bank_build_s = time.perf_counter() - t0
-        self.bank_slots_s = host_s
-        log(f"diagonals ready in {self.bank_build_s:.1f} s (host slot values {host_s:.1f} s)")
-        self.mv_plan = self.F.MatvecPlan(self.ctx, level, n_in, n_out, n1, n2, seg, True, True,
-                                         bank=self.bank)
+        log(f"diagonals ready in {self.bank_build_s:.1f} s (all on the device)")
+        self.mv_plan = self.F.MatvecPlan(self.ctx, level, n_in, n_out, n1, n2, seg, False, True,
+                                         bank=self.bank, complex_pair=True)
         self.mv_out = [torch.empty((level - 1) * 2 * self.n, dtype=torch.int64, device="cuda")
-                       for _ in range(n_out)]
+                       for _ in range(n_out // 2)]
         self.mv_shape = dict(n_in=n_in, n_out=n_out, n1=n1, n2=n2, n_diag=n_diag)
 
     def run_matvec(self, ev):
@@ -662,11 +652,12 @@ def cpu_sample(mode: str) -> dict:
     res["cfg3"]["keyswitch_per_s"] = round(n_ks / t, 3)
 
     # cfg4: the 768 x 1536 projection at 16 limbs, n1 = 16, n2 = 2, 12 inputs,
-    # 48 outputs: baby steps of one input (x 12) plus whole output blocks
-    # (pt-MAC over all inputs and baby steps, giant step, conjugation,
-    # rescale; x 24 for blocks {0, 47}) -- one thread: 2 of the 15 baby
-    # rotations of one input (x 90), the pt-MAC of one input for one block
-    # (x 576) and one block's giant step, conjugation and rescale (x 48)
+    # 48 diagonal sets -> 24 complex-paired outputs: baby steps of one input
+    # (x 12) plus whole output pairs (pt-MAC of both sets over all inputs and
+    # baby steps, two giant steps, conjugation, rescale; x 12 for pairs
+    # {0, 23}) -- one thread: 2 of the 15 baby rotations of one input (x 90),
+    # the pt-MAC of one input into one set (x 576) and one pair's two giant
+    # steps, conjugation and rescale (x 24)
     cfg = WL.CFG4
     seed, lvl, seg = cfg["seed"], cfg["level"], cfg["tokens"]
     n1, n2 = cfg["n1"], cfg["n2"]
@@ -687,10 +678,8 @@ def cpu_sample(mode: str) -> dict:
     t_baby = tick() - t0
     n_in = cfg["d_in"] // Cc // 2
     rnd = synth.uniform_residues(seed, "cpu-diag", P.qs(lvl), n)
-    blocks = [0] if single else [0, cfg["d_out"] // Cc - 1]
-    n_u = 1 if single else n_in
-    t0 = tick()
-    for _ in blocks:
+
+    def giant_sum(n_u):
         y = None
         for p_ in range(n2):
             acc = None
@@ -698,29 +687,38 @@ def cpu_sample(mode: str) -> dict:
                 for q in range(n1):
                     tq = C.mul_plain(P, bb[q % len(bb)], rnd)
                     acc = tq if acc is None else C.ct_add(P, acc, tq)
-            if not single:
+            if n_u == n_in:
                 acc = C.rotate(P, acc, giant[p_], keys)
                 y = acc if y is None else C.ct_add(P, y, acc)
-        if not single:
-            y = C.rescale(P, C.ct_add(P, y, C.conjugate(P, y, keys)))
-    t_blocks = tick() - t0
+        return y
+
     if single:
         t0 = tick()
-        y = C.rotate(P, bb[0], giant[1], keys)
-        y = C.rescale(P, C.ct_add(P, y, C.conjugate(P, y, keys)))
+        giant_sum(1)
+        t_mac = tick() - t0
+        t0 = tick()
+        y1 = C.rotate(P, bb[0], giant[1], keys)
+        y2 = C.rotate(P, bb[1], giant[1], keys)
+        C.rescale(P, C.ct_add(P, y1, C.conjugate(P, y2, keys)))
         t_tail = tick() - t0
         res["cfg4"] = {"sample": "2 of the 15 hoisted baby rotations of one input (x 90); the "
-                                 "pt-MAC of one input into one output block (x 576); one "
-                                 "block's giant step, conjugation and rescale (x 48)",
-                       "sample_s": round(t_baby + t_blocks + t_tail, 3),
-                       "factors": [90, 576, 48],
-                       "extrapolated_s": round(90 * t_baby + 576 * t_blocks + 48 * t_tail, 3)}
+                                 "pt-MAC of one input into one diagonal set (x 576); one output "
+                                 "pair's two giant steps, conjugation and rescale (x 24)",
+                       "sample_s": round(t_baby + t_mac + t_tail, 3),
+                       "factors": [90, 576, 24],
+                       "extrapolated_s": round(90 * t_baby + 576 * t_mac + 24 * t_tail, 3)}
     else:
+        t0 = tick()
+        for _pair in (0, 1):
+            y = C.ct_add(P, giant_sum(n_in), C.conjugate(P, giant_sum(n_in), keys))
+            C.rescale(P, y)
+        t_pairs = tick() - t0
         res["cfg4"] = {"sample": "the hoisted baby steps of one input (15 key switches, x 12); "
-                                 "output blocks 0 and 47 whole (pt-MAC over 12 inputs x 32 "
-                                 "baby/giant terms, giant step, conjugation, rescale; x 24)",
-                       "sample_s": round(t_baby + t_blocks, 3), "factors": [12, 24],
-                       "extrapolated_s": round(12 * t_baby + 24 * t_blocks, 3)}
+                                 "output pairs 0 and 23 whole (pt-MAC of both diagonal sets over "
+                                 "12 inputs x 32 baby/giant terms, two giant steps, "
+                                 "conjugation, rescale; x 12)",
+                       "sample_s": round(t_baby + t_pairs, 3), "factors": [12, 12],
+                       "extrapolated_s": round(12 * t_baby + 12 * t_pairs, 3)}
 
     # cfg5: the scan-contract slice of one Mamba-base token (pool entry 0);
     # the 2048-token sequence is 2048 such tokens -- one thread: the two
@@ -993,7 +991,7 @@ def main():
                 "affine scan)",
         "config": {"workload": "N=2^16, 24 limbs: NTT microbench (64 polys fwd + 64-pair MAC + "
                                "inv) + 32-ciphertext rotation set (30 key switches, dnum 3, 8 "
-                               "special primes) + 768x1536 BSGS projection (12 -> 48 cts, "
+                               "special primes) + 768x1536 BSGS projection (12 -> 24 cts, "
                                "16 limbs) + scan-contract slice of a block of 16 Mamba-base "
                                "tokens (12 state chunks each, 20 -> 18 limbs)",
                    "log_n": 16, "limbs": 24, "special_primes": 8, "parallelism": "single GPU"},
@@ -1009,11 +1007,18 @@ def main():
             "scan_contract_ms_per_token": round(sc / W.sc_shape["tokens"], 3),
             "scan_contract_tokens_per_call": W.sc_shape["tokens"],
             "scan_contract_sequence": sc_seq,
+            "matvec_outputs": {"ciphertexts": W.mv_shape["n_out"] // 2,
+                               "blocks": W.mv_shape["n_out"],
+                               "packing": "complex-paired outputs: block 2P real part, "
+                                          "2P+1 imaginary part of output P",
+                               "tail_key_switches": W.mv_shape["n_out"] * (W.mv_shape["n2"] - 1)
+                               + W.mv_shape["n_out"] // 2},
             "diagonal_bank_build_s": {"total": round(W.bank_build_s, 2),
-                                      "host_slot_values": round(W.bank_slots_s, 2),
+                                      "host_slot_values": 0.0,
                                       "diagonals": W.mv_shape["n_diag"],
-                                      "note": "offline: slot values on the host, device "
-                                              "encoding + lift + NTT + bank packing"},
+                                      "note": "offline, all on the device: slot values "
+                                              "(fesc_bsgs_diagonal_slots), encoding, lift, NTT, "
+                                              "bank packing"},
             "affine_scan": affine,
             "hescan_layer": hescan,
         },

@@ -268,15 +268,23 @@ int fesc_plain_from_coeffs(fesc_ctx* ctx, const int64_t* m, uint64_t* pt, uint32
  * Baby steps are hoisted (one ModUp per input); giant steps and the
  * conjugation are single key switches.  With real_extract the caller folds
  * the 1/2 of the real-part extraction into the diagonals.
+ * complex_pair = 1 (n_out even, real_extract = 0): two real output blocks
+ * leave as one ciphertext, output P = y_{2P} + conj(y_{2P+1}) (then rescaled),
+ * n_out / 2 outputs in all: 3 key switches per pair for n2 = 2 instead of the
+ * 4 of two extracted outputs, and half the rescales.  With paired inputs
+ * x~ = x0 + i x1 the diagonal sets 2P and 2P+1 hold alpha and conj(beta) of
+ * S + i S' = alpha x~ + beta conj(x~) (fesc_bsgs_diagonal_slots), so that
+ * the real and imaginary parts of output P are blocks 2P and 2P+1. 
  * ------------------------------------------------------------------------ */
 typedef struct fesc_matvec_desc {
   uint32_t level;        /* level of the inputs (and diagonals) */
   uint32_t n_in;         /* input ciphertexts x~_u */
-  uint32_t n_out;        /* output ciphertexts y_b */
+  uint32_t n_out;        /* diagonal sets y_b (outputs unless complex_pair) */
   uint32_t n1, n2;       /* baby and giant steps */
   uint32_t unit;         /* slots per segment */
   uint32_t real_extract; /* 0 or 1 */
   uint32_t rescale;      /* 0 or 1 */
+  uint32_t complex_pair; /* 0 or 1: outputs in pairs, see below */
 } fesc_matvec_desc;
 
 typedef struct fesc_matvec_plan fesc_matvec_plan;
@@ -291,8 +299,8 @@ int fesc_matvec_plan_create(fesc_ctx* ctx, const fesc_matvec_desc* desc,
 void fesc_matvec_plan_destroy(fesc_matvec_plan* plan);
 
 /* in: host array of n_in device ciphertexts [level][2][N]; out: host array of
- * n_out device ciphertexts ([level-1][2][N] with rescale, else [level][2][N]).
- * Outputs must not alias inputs. */
+ * n_out (n_out / 2 with complex_pair) device ciphertexts ([level-1][2][N] with
+ * rescale, else [level][2][N]).  Outputs must not alias inputs. */
 int fesc_ptct_matvec(fesc_ctx* ctx, fesc_matvec_plan* plan, const uint64_t* const* in,
                      uint64_t* const* out, void* stream);
 
@@ -309,6 +317,29 @@ int fesc_matvec_bank_pack(fesc_ctx* ctx, const fesc_matvec_desc* desc, uint64_t*
                           uint32_t index, const uint64_t* pt, void* stream);
 int fesc_matvec_plan_create_bank(fesc_ctx* ctx, const fesc_matvec_desc* desc,
                                  const uint64_t* bank, fesc_matvec_plan** plan);
+
+/* Slot vectors of the projection's diagonals on the device (offline
+ * preparation; the appendix encodes all plaintext diagonals offline), for
+ * fesc_encode_plain and fesc_matvec_bank_pack.  W: device fp64 weight matrix,
+ * row-major [d_in][d_out], d_in = n_in * C (2 n_in * C with real_extract or
+ * complex_pair: paired inputs), d_out = n_out * C, with C = segs segments of
+ * `unit` slots (segs must divide (N/2) / unit; slot j lies in segment
+ * (j / unit) mod segs, so a shorter vector repeats); entries outside W read
+ * as 0.  z: device [count][N/2] complex slots
+ * (interleaved re, im) of the diagonals first .. first + count - 1 in bank
+ * order ((b n2 + p) n_in + u) n1 + q.  With t = p n1 + q and
+ * diag_t^(g,b)[idx(r, s)] = W[g C + (s + t) mod C, b C + s], each vector is
+ * Phi^(-p n1) of:
+ *   diag_t^(u,b)                                   (plain),
+ *   (diag_t^(2u,b) - i diag_t^(2u+1,b)) / 2        (real_extract),
+ *   alpha or conj(beta) of the pair (b = 2P + e):  (complex_pair)
+ *     e = 0: ((a + f) + i (d - c)) / 2,  e = 1: ((a - f) - i (d + c)) / 2,
+ *     a = diag^(2u,2P), c = diag^(2u+1,2P), d = diag^(2u,2P+1), f = diag^(2u+1,2P+1).
+ * FESC_ERR_ARG for a range past the last diagonal, or unit * segs not
+ * dividing N/2. */
+int fesc_bsgs_diagonal_slots(fesc_ctx* ctx, const fesc_matvec_desc* desc, const double* W,
+                             uint32_t d_in, uint32_t d_out, uint32_t segs, uint32_t first,
+                             uint32_t count, double* z, void* stream);
 
 /* Phase durations of the plan's last completed run, from HIP events recorded
  * on its stream: baby steps, pt-MAC (one kernel), giant steps + extraction +

@@ -137,6 +137,52 @@ __global__ __launch_bounds__(kThreads) void k_bank_pack(const uint64_t* __restri
       pt[(size_t)i * n + (size_t)tile * kThreads + threadIdx.x];
 }
 
+// Slot vectors of the diagonals first .. first + count - 1 (bank order) of a
+// projection: z[k][j] for slot j, the vector Phi^(-p n1) of the diagonal's
+// combination (plain / real_extract / complex_pair), from W [d_in][d_out].
+// Slot j reads segment s = ((j - p n1 unit) mod n_slots) / unit mod C of the
+// unshifted vector.  Grid: (n_slots / kThreads, count).
+struct SlotDesc {
+  uint32_t n_in, n1, n2, unit, C, n_slots, d_in, d_out, first, mode;  // mode 0/1/2
+};
+__device__ __forceinline__ double wdiag(const double* W, const SlotDesc& S, uint32_t g,
+                                        uint32_t b, uint32_t t, uint32_t s) {
+  const uint32_t row = g * S.C + (s + t) % S.C, col = b * S.C + s;
+  return (row < S.d_in && col < S.d_out) ? W[(size_t)row * S.d_out + col] : 0.0;
+}
+__global__ __launch_bounds__(kThreads) void k_bsgs_slots(const double* __restrict__ W,
+                                                         SlotDesc S, double2* __restrict__ z) {
+  const uint32_t j = blockIdx.x * kThreads + threadIdx.x;
+  if (j >= S.n_slots) return;
+  const uint32_t idx = S.first + blockIdx.y;
+  const uint32_t q = idx % S.n1, u = (idx / S.n1) % S.n_in, p = (idx / (S.n1 * S.n_in)) % S.n2,
+                 b = idx / (S.n1 * S.n_in * S.n2);
+  const uint32_t t = p * S.n1 + q;
+  const uint32_t shift = (uint32_t)(((uint64_t)p * S.n1 * S.unit) % S.n_slots);
+  const uint32_t s = ((j + S.n_slots - shift) % S.n_slots / S.unit) % S.C;
+  double re, im;
+  if (S.mode == 0) {
+    re = wdiag(W, S, u, b, t, s);
+    im = 0.0;
+  } else if (S.mode == 1) {
+    re = 0.5 * wdiag(W, S, 2 * u, b, t, s);
+    im = 0.5 * -wdiag(W, S, 2 * u + 1, b, t, s);
+  } else {
+    const uint32_t P = b / 2;
+    const double a = wdiag(W, S, 2 * u, 2 * P, t, s), c = wdiag(W, S, 2 * u + 1, 2 * P, t, s);
+    const double d = wdiag(W, S, 2 * u, 2 * P + 1, t, s);
+    const double f = wdiag(W, S, 2 * u + 1, 2 * P + 1, t, s);
+    if (b % 2 == 0) {
+      re = 0.5 * (a + f);
+      im = 0.5 * (d - c);
+    } else {
+      re = 0.5 * (a - f);
+      im = -(0.5 * (d + c));
+    }
+  }
+  z[(size_t)blockIdx.y * S.n_slots + j] = double2{re, im};
+}
+
 #define HIPCK(expr)                                   \
   do {                                                \
     hipError_t e_ = (expr);                           \
@@ -151,7 +197,15 @@ int check_desc(const Context* c, const fesc_matvec_desc* d) {
   if (d->rescale && d->level < 2) return fail(FESC_ERR_LEVEL, "rescale needs level >= 2");
   if (!d->n_in || !d->n_out || !d->n1 || !d->n2 || !d->unit)
     return fail(FESC_ERR_ARG, "matvec sizes must be positive");
+  if (d->real_extract > 1 || d->rescale > 1 || d->complex_pair > 1)
+    return fail(FESC_ERR_ARG, "matvec flags must be 0 or 1");
+  if (d->complex_pair && (d->real_extract || d->n_out % 2))
+    return fail(FESC_ERR_ARG, "complex_pair needs an even n_out and real_extract = 0");
   return FESC_OK;
+}
+
+static uint32_t matvec_outputs(const fesc_matvec_desc& d) {
+  return d.complex_pair ? d.n_out / 2 : d.n_out;
 }
 
 int matvec_plan_create(Context* c, const fesc_matvec_desc* d, const uint64_t* const* diags,
@@ -173,7 +227,7 @@ int matvec_plan_create(Context* c, const fesc_matvec_desc* d, const uint64_t* co
     if (g != 1 && !c->keys.count(g))
       return fail(FESC_ERR_NO_KEY, "matvec needs the key of rotation " + std::to_string(st));
   }
-  if (d->real_extract && !c->keys.count(2 * c->n - 1))
+  if ((d->real_extract || d->complex_pair) && !c->keys.count(2 * c->n - 1))
     return fail(FESC_ERR_NO_KEY, "matvec real extraction needs the conjugation key");
 
   fesc_matvec_plan* p = new fesc_matvec_plan();
@@ -298,10 +352,26 @@ int ptct_matvec(Context* c, fesc_matvec_plan* p, const uint64_t* const* in,
       return err;
     for (uint32_t b = 0; b < d.n_out; ++b) res[b] = gout[b];
   }
+  if (d.complex_pair) {
+    // output P = y_2P + conj(y_2P+1), one batch of conjugations
+    const uint32_t np_ = d.n_out / 2;
+    std::vector<const uint64_t*> even(np_);
+    for (uint32_t P = 0; P < np_; ++P) {
+      gin[P] = res[2 * P + 1];
+      even[P] = res[2 * P];
+      gout[P] = tmp + (size_t)P * W;
+      gst[P] = INT32_MIN;
+    }
+    if ((err = op_rotate_batch(c, np_, gin.data(), gst.data(), gout.data(), even.data(), level,
+                               s)))
+      return err;
+    for (uint32_t P = 0; P < np_; ++P) res[P] = gout[P];
+  }
+  const uint32_t n_res = matvec_outputs(d);
   if (d.rescale) {
-    if ((err = op_rescale_many(c, d.n_out, res.data(), out, level, s))) return err;
+    if ((err = op_rescale_many(c, n_res, res.data(), out, level, s))) return err;
   } else {
-    for (uint32_t b = 0; b < d.n_out; ++b)
+    for (uint32_t b = 0; b < n_res; ++b)
       HIPCK(hipMemcpyAsync(out[b], res[b], W * 8, hipMemcpyDeviceToDevice, s));
   }
   HIPCK(hipEventRecord(p->ev[3], s));
@@ -341,6 +411,29 @@ int fesc_matvec_bank_pack(fesc_ctx* ctx, const fesc_matvec_desc* desc, uint64_t*
   return fesc::hip_check(hipGetLastError(), "bank_pack");
 }
 
+int fesc_bsgs_diagonal_slots(fesc_ctx* ctx, const fesc_matvec_desc* desc, const double* W,
+                             uint32_t d_in, uint32_t d_out, uint32_t segs, uint32_t first,
+                             uint32_t count, double* z, void* stream) {
+  if (!ctx || !W || !z) return fesc::fail(FESC_ERR_ARG, "null argument");
+  int rc = fesc::check_desc(ctx, desc);
+  if (rc) return rc;
+  const uint32_t n_slots = ctx->n / 2;
+  if (!segs || n_slots % desc->unit || (n_slots / desc->unit) % segs)
+    return fesc::fail(FESC_ERR_ARG, "unit * segs must divide N/2");
+  const uint64_t total = (uint64_t)desc->n_out * desc->n2 * desc->n_in * desc->n1;
+  if ((uint64_t)first + count > total) return fesc::fail(FESC_ERR_ARG, "diagonal range");
+  if (count == 0) return FESC_OK;
+  if (count > 65535) return fesc::fail(FESC_ERR_ARG, "at most 65535 diagonals per call");
+  const fesc::SlotDesc S{desc->n_in, desc->n1, desc->n2, desc->unit, segs,
+                         n_slots, d_in, d_out, first,
+                         desc->complex_pair ? 2u : (desc->real_extract ? 1u : 0u)};
+  hipLaunchKernelGGL(fesc::k_bsgs_slots, dim3((n_slots + fesc::kThreads - 1) / fesc::kThreads,
+                                              count),
+                     dim3(fesc::kThreads), 0, reinterpret_cast<hipStream_t>(stream), W, S,
+                     reinterpret_cast<double2*>(z));
+  return fesc::hip_check(hipGetLastError(), "bsgs_diagonal_slots");
+}
+
 int fesc_matvec_plan_create_bank(fesc_ctx* ctx, const fesc_matvec_desc* desc,
                                  const uint64_t* bank, fesc_matvec_plan** plan) {
   if (!ctx) return fesc::fail(FESC_ERR_ARG, "null context");
@@ -355,7 +448,7 @@ int fesc_ptct_matvec(fesc_ctx* ctx, fesc_matvec_plan* plan, const uint64_t* cons
   if (!ctx || !plan || !in || !out) return fesc::fail(FESC_ERR_ARG, "null argument");
   for (uint32_t u = 0; u < plan->d.n_in; ++u)
     if (!in[u]) return fesc::fail(FESC_ERR_ARG, "null input");
-  for (uint32_t b = 0; b < plan->d.n_out; ++b)
+  for (uint32_t b = 0; b < fesc::matvec_outputs(plan->d); ++b)
     if (!out[b]) return fesc::fail(FESC_ERR_ARG, "null output");
   return fesc::ptct_matvec(ctx, plan, in, out, reinterpret_cast<hipStream_t>(stream));
 }

@@ -476,7 +476,7 @@ def encode(log_n: int, z, scale: float):
 
 class _MatvecDesc(ctypes.Structure):
     _fields_ = [(f, _u32) for f in ("level", "n_in", "n_out", "n1", "n2", "unit",
-                                    "real_extract", "rescale")]
+                                    "real_extract", "rescale", "complex_pair")]
 
 
 _lib.fesc_matvec_plan_create.argtypes = [_vp, ctypes.POINTER(_MatvecDesc), ctypes.POINTER(_vp),
@@ -500,8 +500,33 @@ _lib.fesc_matvec_plan_create_bank.argtypes = [_vp, ctypes.POINTER(_MatvecDesc), 
 _lib.fesc_matvec_plan_create_bank.restype = ctypes.c_int
 
 
-def matvec_desc(level, n_in, n_out, n1, n2, unit, real_extract, rescale) -> _MatvecDesc:
-    return _MatvecDesc(level, n_in, n_out, n1, n2, unit, int(real_extract), int(rescale))
+def matvec_desc(level, n_in, n_out, n1, n2, unit, real_extract, rescale,
+                complex_pair=False) -> _MatvecDesc:
+    return _MatvecDesc(level, n_in, n_out, n1, n2, unit, int(real_extract), int(rescale),
+                       int(complex_pair))
+
+
+_lib.fesc_bsgs_diagonal_slots.argtypes = [_vp, ctypes.POINTER(_MatvecDesc), _vp, _u32, _u32,
+                                          _u32, _u32, _u32, _vp, _vp]
+_lib.fesc_bsgs_diagonal_slots.restype = ctypes.c_int
+
+
+def bsgs_diagonal_slots(ctx: Context, desc: _MatvecDesc, W, segs: int, first: int, count: int,
+                        z, stream=None):
+    """Slot vectors of diagonals first .. first+count-1 (bank order) into the
+    device complex128 tensor z [>= count][N/2]; W a device float64
+    [d_in][d_out]; segs segments of desc.unit slots per period."""
+    if not (isinstance(W, torch.Tensor) and W.is_cuda and W.dtype == torch.float64
+            and W.dim() == 2 and W.is_contiguous()):
+        raise TypeError("W: expected a contiguous 2-D CUDA float64 tensor")
+    if not (isinstance(z, torch.Tensor) and z.is_cuda and z.dtype == torch.complex128
+            and z.is_contiguous()):
+        raise TypeError("z: expected a contiguous CUDA complex128 tensor")
+    if z.numel() < count * (ctx.n // 2):
+        raise ValueError(f"z: {z.numel()} slots, the call writes {count * (ctx.n // 2)}")
+    _check(_lib.fesc_bsgs_diagonal_slots(ctx._h, ctypes.byref(desc), W.data_ptr(), W.shape[0],
+                                         W.shape[1], segs, first, count, z.data_ptr(),
+                                         _stream(stream)))
 
 
 def matvec_bank_words(ctx: Context, desc: _MatvecDesc) -> int:
@@ -522,9 +547,10 @@ class MatvecPlan:
     tiled device buffer (see fesc_matvec_bank_pack).  Inputs are kept alive."""
 
     def __init__(self, ctx: Context, level, n_in, n_out, n1, n2, unit, real_extract, rescale,
-                 diags=None, bank=None):
+                 diags=None, bank=None, complex_pair=False):
         self.ctx = ctx
-        self.desc = matvec_desc(level, n_in, n_out, n1, n2, unit, real_extract, rescale)
+        self.desc = matvec_desc(level, n_in, n_out, n1, n2, unit, real_extract, rescale,
+                                complex_pair)
         h = _vp()
         if bank is not None:
             self._bank = bank
@@ -541,7 +567,8 @@ class MatvecPlan:
     def __call__(self, ins, outs, stream=None):
         d, c = self.desc, self.ctx
         a = _ptrs(ins, d.n_in, c._ct(d.level), "ins")
-        b = _ptrs(outs, d.n_out, c._ct(d.level - (1 if d.rescale else 0)), "outs")
+        n_res = d.n_out // 2 if d.complex_pair else d.n_out
+        b = _ptrs(outs, n_res, c._ct(d.level - (1 if d.rescale else 0)), "outs")
         _check(_lib.fesc_ptct_matvec(self.ctx._h, self._h, a, b, _stream(stream)))
 
     def phase_ms(self):

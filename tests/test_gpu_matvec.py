@@ -1,7 +1,9 @@
 """GPU parity of the plaintext-matrix x ciphertext projection (BSGS) against
 the oracle, on the N = 2^12 diagonal-method workload (64 x 64 matrix, 63
-hoisted rotations, rescale) and on a complex-paired BSGS instance with
-several inputs, outputs and giant steps."""
+hoisted rotations, rescale), on a complex-paired BSGS instance with several
+inputs, outputs and giant steps, with complex-paired outputs (small ring and
+the full cfg4 shape), and the device generator of the diagonals' slot
+vectors against the oracle's."""
 import numpy as np
 import pytest
 import torch
@@ -44,18 +46,19 @@ def _run(P, S, desc, X_slots, scale_x, diag_slots, scale_d, seed_tag):
     step(f"matvec plan n_in={desc.n_in} n_out={desc.n_out} n1={desc.n1} n2={desc.n2}")
     args = (desc.level, desc.n_in, desc.n_out, desc.n1, desc.n2, desc.unit, desc.real_extract,
             desc.rescale)
-    plan = F.MatvecPlan(S.ctx, *args, diags=flat)
+    cp = desc.complex_pair
+    plan = F.MatvecPlan(S.ctx, *args, diags=flat, complex_pair=cp)
     out_level = level - 1 if desc.rescale else level
     outs_d = [torch.zeros(out_level * 2 * P.n, dtype=torch.int64, device="cuda")
-              for _ in range(desc.n_out)]
+              for _ in range(desc.n_out // 2 if cp else desc.n_out)]
     step("matvec run")
     plan(ins_d, outs_d)
     # the same diagonals through a tiled bank give the same residues
-    fd = F.matvec_desc(*args)
+    fd = F.matvec_desc(*args, cp)
     bank = torch.zeros(F.matvec_bank_words(S.ctx, fd), dtype=torch.int64, device="cuda")
     for t, pt in enumerate(flat):
         F.matvec_bank_pack(S.ctx, fd, bank, t, pt)
-    plan_b = F.MatvecPlan(S.ctx, *args, bank=bank)
+    plan_b = F.MatvecPlan(S.ctx, *args, bank=bank, complex_pair=cp)
     outs_b = [torch.zeros_like(o) for o in outs_d]
     step("matvec run (bank)")
     plan_b(ins_d, outs_b)
@@ -189,4 +192,159 @@ def test_cfg4_full_size_projection():
         dec = C.decrypt(P, S.sk, ct, 2.0 ** 40)
         worst = max(worst, float(np.max(np.abs(dec.real - Y[r, b * Cc + s]))))
     print(f"cfg4 max |decoded - fp64| over 48 blocks = {worst:.3e} (2^{np.log2(worst):.1f})")
+    assert worst <= 2.0 ** -15
+
+
+def _slot_fn(mode, Wm, n_slots, seg, Cc, n1):
+    if mode == "pair":
+        return lambda b, p, u, q: OW.bsgs_pair_diagonal_slots(Wm, n_slots, seg, Cc, n1, b, p, u, q)
+    return lambda b, p, u, q: OW.bsgs_diagonal_slots(Wm, n_slots, seg, Cc, n1, b, p, u, q,
+                                                     mode == "paired")
+
+
+@pytest.mark.parametrize("mode,segs", [("plain", 32), ("paired", 32), ("pair", 32),
+                                       ("plain", 16)])
+def test_bsgs_diagonal_slots_on_device(mode, segs):
+    """fesc_bsgs_diagonal_slots against the oracle's slot vectors, every
+    diagonal of a small projection, bit for bit (segs = 16 < (N/2)/unit: a
+    repeated shorter vector)."""
+    from paper_2608_17442_amd import fesc as F
+    P = C.params_small(12, 50, 3, 1)
+    ctx = F.Context(P.log_n, P.q, P.p)
+    n_slots, seg = P.n // 2, 64
+    n1, n2 = 8, 4
+    gin = 2 if mode != "plain" else 1
+    n_in, n_out = 2, 4
+    d_in, d_out = gin * n_in * segs - 5, n_out * segs - 3      # ragged: W shorter than blocks
+    Wm = synth.normal(23, "W", (d_in, d_out), 0.1)
+    desc = F.matvec_desc(2, n_in, n_out, n1, n2, seg, mode == "paired", True, mode == "pair")
+    total = n_out * n2 * n_in * n1
+    z = torch.zeros((total, n_slots), dtype=torch.complex128, device="cuda")
+    Wd = torch.from_numpy(Wm).cuda()
+    step(f"bsgs slots {mode} segs={segs}")
+    F.bsgs_diagonal_slots(ctx, desc, Wd, segs, 0, 7, z)
+    F.bsgs_diagonal_slots(ctx, desc, Wd, segs, 7, total - 7, z[7:])
+    got = z.cpu().numpy()
+    fn = _slot_fn(mode, Wm, n_slots, seg, segs, n1)
+    t = 0
+    for b in range(n_out):
+        for p in range(n2):
+            for u in range(n_in):
+                for q in range(n1):
+                    want = fn(b, p, u, q)
+                    assert np.array_equal(got[t], want), (mode, t, b, p, u, q)
+                    t += 1
+    with pytest.raises(F.FescError):
+        F.bsgs_diagonal_slots(ctx, desc, Wd, segs, total - 1, 2, z)
+    with pytest.raises(F.FescError):
+        F.bsgs_diagonal_slots(ctx, desc, Wd, 48, 0, 1, z)          # 48 does not divide 32
+
+
+def test_complex_paired_outputs_small():
+    """Complex-paired outputs on a small ring (n_out = 4 diagonal sets -> 2
+    output ciphertexts, n2 = 4 giant steps), table and bank plans, bit-exact
+    against the oracle; the real and imaginary parts decode to blocks 2P and
+    2P + 1 of X W within 2^-15."""
+    P = C.params_small(12, 50, 5, 2)
+    n_slots, seg_len, Cc = P.n // 2, 64, 32
+    T, d_in, d_out, n1, n2 = 64, 128, 128, 8, 4
+    level = 4
+    X = synth.normal(24, "X", (T, d_in))
+    Wm = synth.normal(24, "W", (d_in, d_out), 0.02)
+    desc = OW.MatvecDesc(level, d_in // Cc // 2, d_out // Cc, n1, n2, seg_len, False, True,
+                         complex_pair=True)
+    S = Setup(P, 24, rot_steps=sorted(OW.required_rotations(desc, n_slots)), conj=True)
+    xs = [OW.pack_input(X, n_slots, seg_len, Cc, 2 * u)
+          + 1j * OW.pack_input(X, n_slots, seg_len, Cc, 2 * u + 1) for u in range(desc.n_in)]
+    diag = _slot_fn("pair", Wm, n_slots, seg_len, Cc, n1)
+    outs_o, outs_d = _run(P, S, desc, xs, 2.0 ** 40, diag, float(P.q[level - 1]), "pair")
+    assert len(outs_o) == len(outs_d) == desc.n_out // 2
+    Y = X @ Wm
+    r, s = OW.segment_indices(n_slots, seg_len, Cc)
+    for pair in range(desc.n_out // 2):
+        got = to_host(outs_d[pair]).reshape(outs_o[pair].shape)
+        assert np.array_equal(got, outs_o[pair]), f"pair {pair}: {first_mismatch(got, outs_o[pair])}"
+        dec = C.decrypt(P, S.sk, outs_o[pair], 2.0 ** 40)
+        assert np.max(np.abs(dec.real - Y[r, 2 * pair * Cc + s])) <= 2.0 ** -15
+        assert np.max(np.abs(dec.imag - Y[r, (2 * pair + 1) * Cc + s])) <= 2.0 ** -15
+
+
+def test_cfg4_full_size_complex_paired_outputs():
+    """The 768 x 1536 projection with complex-paired outputs, as the benchmark
+    runs it: 18,432 diagonals (48 sets = 24 output pairs) whose slot vectors
+    come from the device generator and are encoded on the device, one tiled
+    bank, 24 output ciphertexts (48 giant-step and 24 conjugation key
+    switches).  Pairs 0 and 23 (output blocks 0, 1, 46, 47) are compared
+    residue by residue with the oracle (their diagonals encoded by the
+    oracle); all 24 outputs decode to X W within 2^-15 (real part block 2P,
+    imaginary part block 2P + 1)."""
+    from paper_2608_17442_amd import fesc as F
+    cfg = WL.CFG4
+    P = C.params_p16()
+    level, seg = cfg["level"], cfg["tokens"]
+    n_slots = P.n // 2
+    Cc = n_slots // seg
+    n1, n2 = cfg["n1"], cfg["n2"]
+    n_in, n_out = cfg["d_in"] // Cc // 2, cfg["d_out"] // Cc
+    desc = OW.MatvecDesc(level, n_in, n_out, n1, n2, seg, False, True, complex_pair=True)
+    S = Setup(P, cfg["seed"], rot_steps=sorted(OW.required_rotations(desc, n_slots)), conj=True)
+    X, Wm = WL.cfg4_values()
+    ins_o, ins_d = [], []
+    for u in range(n_in):
+        z = OW.pack_input(X, n_slots, seg, Cc, 2 * u) + 1j * OW.pack_input(X, n_slots, seg, Cc,
+                                                                            2 * u + 1)
+        co, cd = S.encrypt(z, 2.0 ** 40, level, 3000 + u)
+        ins_o.append(co)
+        ins_d.append(cd)
+    n_pairs = n_out // 2
+    check = (0, n_pairs - 1)
+    scale = float(P.q[level - 1])
+    index = [(b, p, u, q) for b in range(n_out) for p in range(n2) for u in range(n_in)
+             for q in range(n1)]
+    fd = F.matvec_desc(level, n_in, n_out, n1, n2, seg, False, True, True)
+    bank = torch.zeros(F.matvec_bank_words(S.ctx, fd), dtype=torch.int64, device="cuda")
+    Wd = torch.from_numpy(Wm).cuda()
+    chunk = 128
+    zs = torch.empty((chunk, n_slots), dtype=torch.complex128, device="cuda")
+    pts = torch.empty((chunk, level * P.n), dtype=torch.int64, device="cuda")
+    step(f"cfg4 paired-output bank: {len(index)} diagonals, slots and encoding on the device")
+    for c0 in range(0, len(index), chunk):
+        m = min(chunk, len(index) - c0)
+        F.bsgs_diagonal_slots(S.ctx, fd, Wd, Cc, c0, m, zs)
+        S.ctx.encode_plain(zs[:m], scale, pts[:m], level)
+        for j in range(m):
+            F.matvec_bank_pack(S.ctx, fd, bank, c0 + j, pts[j])
+    # the compared pairs' diagonals from the oracle's encoder (the device
+    # encoder may round a near-tie coefficient differently)
+    oracle_pt = {}
+    step("cfg4 oracle diagonals of the compared pairs")
+    for t, (b, p, u, q) in enumerate(index):
+        if b // 2 in check:
+            v = OW.bsgs_pair_diagonal_slots(Wm, n_slots, seg, Cc, n1, b, p, u, q)
+            oracle_pt[(b, p, u, q)] = C.encode_plain(P, v, scale, level)
+            F.matvec_bank_pack(S.ctx, fd, bank, t, to_dev(oracle_pt[(b, p, u, q)]))
+    torch.cuda.synchronize()
+    plan = F.MatvecPlan(S.ctx, level, n_in, n_out, n1, n2, seg, False, True, bank=bank,
+                        complex_pair=True)
+    outs_d = [torch.zeros((level - 1) * 2 * P.n, dtype=torch.int64, device="cuda")
+              for _ in range(n_pairs)]
+    step("cfg4 paired-output matvec run")
+    plan(ins_d, outs_d)
+    torch.cuda.synchronize()
+    del bank
+    step("cfg4 oracle pairs")
+    outs_o = OW.bsgs_matvec(P, desc, ins_o, lambda b, p, u, q: oracle_pt[(b, p, u, q)], S.keys,
+                            blocks=check)
+    for pair, want in zip(check, outs_o):
+        got = to_host(outs_d[pair]).reshape(want.shape)
+        assert np.array_equal(got, want), f"pair {pair}: {first_mismatch(got, want)}"
+    Y = X @ Wm
+    r, s = OW.segment_indices(n_slots, seg, Cc)
+    worst = 0.0
+    for pair in range(n_pairs):
+        ct = to_host(outs_d[pair]).reshape(level - 1, 2, P.n)
+        dec = C.decrypt(P, S.sk, ct, 2.0 ** 40)
+        worst = max(worst, float(np.max(np.abs(dec.real - Y[r, 2 * pair * Cc + s]))),
+                    float(np.max(np.abs(dec.imag - Y[r, (2 * pair + 1) * Cc + s]))))
+    print(f"cfg4 paired outputs: max |decoded - fp64| over 48 blocks = {worst:.3e}")
     assert worst <= 2.0 ** -15
