@@ -517,6 +517,16 @@ def scan_block_sweep(W, F, torch, np, L=2048, level=22, blocks=(64, 128, 256, 51
             "rows": rows}
 
 
+def modmul_probe(ctx, F) -> dict:
+    """The residue product alone, fp64 (the library's form) against 64-bit
+    integer Shoup, on every CU with no memory traffic (products per second)."""
+    f = ctx.calib_valu(F.CALIB_MODMUL_F64)
+    u = ctx.calib_valu(F.CALIB_MODMUL_U64)
+    return {"fp64_shoup_per_s": round(f, -9), "u64_shoup_per_s": round(u, -9),
+            "fp64_over_u64": round(f / u, 2),
+            "kernels": "k_calib_modmul_f64 / k_calib_modmul_u64 (fesc_calib_valu)"}
+
+
 def keyswitch_per_kernel():
     f = profiled_fields(KS_PROFILE, KS_SOURCES)
     if f is None or "keyswitch_bound_fraction" not in f:
@@ -828,6 +838,9 @@ def main():
                     help="only the resident-schedule block-size sweep at L=2048 (one chunk)")
     ap.add_argument("--affine-only", action="store_true",
                     help="set up and time only the affine prefix scan component (profiling)")
+    ap.add_argument("--calibrate-only", action="store_true",
+                    help="only the register-resident VALU calibrations and the fp64 / int64 "
+                         "modular-product probe (one JSON line)")
     ap.add_argument("--cpu-sample", choices=("all", "single"),
                     help="(internal) time the oracle's bounded samples in this process and "
                          "print them as JSON; no GPU is used")
@@ -855,6 +868,14 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if args.calibrate_only:
+        pr = F.find_primes(16, 50, 32)
+        ctx = F.Context(16, pr[8:], pr[:8])
+        out = {"valu_peaks_per_s": {k: round(ctx.calib_valu(v), -9) for k, v in (
+            ("ct_butterflies", F.CALIB_CT), ("gs_butterflies", F.CALIB_GS),
+            ("mod_macs", F.CALIB_MAC))}, "modmul_probe": modmul_probe(ctx, F)}
+        print(json.dumps(out), flush=True)
+        return
     if args.hescan_sweep:
         W = Workloads(F, torch, np, affine_only=True)
         sweep = {}
@@ -879,6 +900,7 @@ def main():
     # register-resident arithmetic peaks of this device (VALU roof)
     peak = {k: W.ctx.calib_valu(v) for k, v in (("ct", F.CALIB_CT), ("gs", F.CALIB_GS),
                                                  ("mac", F.CALIB_MAC))}
+    modmul = modmul_probe(W.ctx, F)
 
     def new_events(k):
         return [torch.cuda.Event(enable_timing=True) for _ in range(k)]
@@ -1050,6 +1072,7 @@ def main():
                                  "peak": HBM_PEAK_GBS, "unit": "GB/s"},
             "mac": {"bound": "hbm", "achieved": round(mac_bytes / (mac * 1e-3) / 1e9, 1),
                     "peak": HBM_PEAK_GBS, "unit": "GB/s"},
+            "modmul_probe": modmul,
         },
     }
     if not args.no_cpu_baseline:

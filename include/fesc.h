@@ -537,12 +537,19 @@ int fesc_encode(uint32_t log_n, const double* re, const double* im, double scale
  * butterflies (radix-2 Cooley-Tukey with the transform's lazy reduction);
  * FESC_CALIB_GS: inverse NTT butterflies (Gentleman-Sande); FESC_CALIB_MAC:
  * modular multiply-accumulates as in basis conversion and the key inner
- * product (reduced after every four terms).  Each thread runs `iters`
- * iterations (1 .. 2^20) of 32 butterflies or 8 MACs.  Synchronises `stream`;
- * uses context scratch; FESC_ERR_ARG for a bad kind or count. */
+ * product (reduced after every four terms); FESC_CALIB_MODMUL_F64 and
+ * FESC_CALIB_MODMUL_U64: the residue product alone in the library's fp64 form
+ * (exact product split by one FMA, quotient from the precomputed w / q) and
+ * in the 64-bit integer Shoup form (quotient from the high half of
+ * x * floor(w 2^64 / q)), the evidence for the fp64 choice.  Each thread
+ * runs `iters` iterations (1 .. 2^20) of 32 butterflies or 8 products.
+ * Synchronises `stream`; uses context scratch; FESC_ERR_ARG for a bad kind
+ * or count. */
 #define FESC_CALIB_CT 0
 #define FESC_CALIB_GS 1
 #define FESC_CALIB_MAC 2
+#define FESC_CALIB_MODMUL_F64 3
+#define FESC_CALIB_MODMUL_U64 4
 int fesc_calib_valu(fesc_ctx* ctx, int kind, uint32_t iters, double* rate, void* stream);
 
 #ifdef __cplusplus

@@ -82,10 +82,49 @@ __global__ __launch_bounds__(kThreads) void k_calib_mac(double q, double qinv, u
   out[t] = s;
 }
 
+// The residue product alone, in the two forms considered for the VALU:
+// eight independent chains x <- x w mod q per thread and iteration.
+//   fp64 (the library's): h = x w, l = fma(x, w, -h), c = rint(x w'),
+//     x = fma(-c, q, h) + l  (w' = w / q in fp64);
+//   u64 (Shoup's integer form): c = hi64(x w'), x = x w - c q  (mod 2^64,
+//     w' = floor(w 2^64 / q); the result stays below 2q).
+__global__ __launch_bounds__(kThreads) void k_calib_modmul_f64(double q, double w, double wp,
+                                                               uint32_t iters, double* out) {
+  const uint32_t t = blockIdx.x * kThreads + threadIdx.x;
+  double x[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) x[j] = (double)((t * 8u + j) % 1000003u);
+  for (uint32_t i = 0; i < iters; ++i) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) x[j] = mm_shoup(x[j], w, wp, q);
+  }
+  double s = 0.0;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) s += x[j];
+  out[t] = s;
+}
+
+__global__ __launch_bounds__(kThreads) void k_calib_modmul_u64(uint64_t q, uint64_t w,
+                                                               uint64_t wp, uint32_t iters,
+                                                               double* out) {
+  const uint32_t t = blockIdx.x * kThreads + threadIdx.x;
+  uint64_t x[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) x[j] = (uint64_t)((t * 8u + j) % 1000003u);
+  for (uint32_t i = 0; i < iters; ++i) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) x[j] = x[j] * w - __umul64hi(x[j], wp) * q;
+  }
+  uint64_t s = 0;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) s += x[j];
+  out[t] = (double)(s & 0xFFFFFFFFull);
+}
+
 }  // namespace
 
 int calib_valu(Context* c, int kind, uint32_t iters, double* rate, hipStream_t s) {
-  if (kind < FESC_CALIB_CT || kind > FESC_CALIB_MAC || iters == 0 || iters > (1u << 20))
+  if (kind < FESC_CALIB_CT || kind > FESC_CALIB_MODMUL_U64 || iters == 0 || iters > (1u << 20))
     return fail(FESC_ERR_ARG, "bad calibration arguments");
   int cus = 0;
   if (int rc = hip_check(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount,
@@ -107,8 +146,17 @@ int calib_valu(Context* c, int kind, uint32_t iters, double* rate, hipStream_t s
     (void)hipEventDestroy(e0);
     return rc;
   }
+  // the product's operands for the modmul probes: w < q, w' its Shoup constant
+  const uint64_t qu = c->primes[0], wu = qu / 3 + 12345;
+  const uint64_t wpu = (uint64_t)(((unsigned __int128)wu << 64) / qu);
   auto launch = [&]() {
-    if (kind == FESC_CALIB_CT)
+    if (kind == FESC_CALIB_MODMUL_F64)
+      hipLaunchKernelGGL(k_calib_modmul_f64, dim3(blocks), dim3(kThreads), 0, s, q, (double)wu,
+                         (double)wu / q, iters, out);
+    else if (kind == FESC_CALIB_MODMUL_U64)
+      hipLaunchKernelGGL(k_calib_modmul_u64, dim3(blocks), dim3(kThreads), 0, s, qu, wu, wpu,
+                         iters, out);
+    else if (kind == FESC_CALIB_CT)
       hipLaunchKernelGGL(k_calib_bfly<false>, dim3(blocks), dim3(kThreads), 0, s, tw, q, qinv,
                          iters, out);
     else if (kind == FESC_CALIB_GS)
@@ -129,7 +177,8 @@ int calib_valu(Context* c, int kind, uint32_t iters, double* rate, hipStream_t s
   (void)hipEventDestroy(e0);
   (void)hipEventDestroy(e1);
   if (rc) return rc;
-  const double per_thread = kind == FESC_CALIB_MAC ? 8.0 * iters : 32.0 * iters;
+  const double per_thread =
+      (kind == FESC_CALIB_CT || kind == FESC_CALIB_GS) ? 32.0 * iters : 8.0 * iters;
   *rate = (double)blocks * kThreads * per_thread / (ms * 1e-3);
   return FESC_OK;
 }

@@ -204,7 +204,8 @@ def test_calib_valu_rates_are_positive_and_ordered():
     P = C.params_small(12, 36, 3, 1)
     ctx = F.Context(P.log_n, P.q, P.p)
     step("calib valu")
-    r = {k: ctx.calib_valu(k, 256) for k in (F.CALIB_CT, F.CALIB_GS, F.CALIB_MAC)}
+    r = {k: ctx.calib_valu(k, 256) for k in (F.CALIB_CT, F.CALIB_GS, F.CALIB_MAC,
+                                              F.CALIB_MODMUL_F64, F.CALIB_MODMUL_U64)}
     print({k: f"{v / 1e12:.3f} T/s" for k, v in r.items()})
     for v in r.values():
         assert np.isfinite(v) and 1e9 < v < 1e14
