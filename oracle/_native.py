@@ -38,6 +38,8 @@ def lib():
         u64, i32, lng = ctypes.c_uint64, ctypes.c_int, ctypes.c_long
         sig = {
             "or_mulmod": (u64, [u64, u64, u64]),
+            "or_philox4x64": (None, [_u64p, u64, u64, _u64p]),
+            "or_seeded_key_a": (None, [_u64p, i32, i32, lng, _u64p, _u64p, u64, u64, u64]),
             "or_powmod": (u64, [u64, u64, u64]),
             "or_invmod": (u64, [u64, u64]),
             "or_is_prime": (i32, [u64]),

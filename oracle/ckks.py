@@ -248,6 +248,34 @@ def relin_key(P: Params, sk: SecretKey, a, e) -> np.ndarray:
     return switch_key(P, sk, pmul(sk.ntt_ext, sk.ntt_ext, mods), a, e)
 
 
+def philox4x64(ctr, k0: int, k1: int) -> list:
+    """Philox4x64-10 block of a 4-word counter under a 2-word key."""
+    c = np.ascontiguousarray(ctr, dtype=np.uint64)
+    out = np.empty(4, dtype=np.uint64)
+    nat.lib().or_philox4x64(nat.u64p(c), int(k0), int(k1), nat.u64p(out))
+    return [int(v) for v in out]
+
+
+def seeded_key_a(P: Params, seed_words, elt: int) -> np.ndarray:
+    """Uniform half of a seed-expanded switching key, ``u64[dnum][L+alpha][N]``
+    (evaluation form), regenerated from two 64-bit seed words (see the C core
+    or_seeded_key_a for the counter layout and the residue rule)."""
+    mods = P.ext(P.L)
+    out = np.empty((P.dnum, len(mods), P.n), dtype=np.uint64)
+    row_ids = np.arange(len(mods), dtype=np.uint64)
+    nat.lib().or_seeded_key_a(nat.u64p(out), P.dnum, len(mods), P.n,
+                              nat.u64p(nat.moduli(mods)), nat.u64p(row_ids),
+                              int(seed_words[0]), int(seed_words[1]), int(elt))
+    return out
+
+
+def keygen_seeded(P: Params, sk: SecretKey, seed_words, e, elt: int) -> np.ndarray:
+    """Switching key for ``elt`` (0: relinearisation) whose uniform half is
+    regenerated from ``seed_words``; returned in the full layout."""
+    a = seeded_key_a(P, seed_words, elt)
+    return relin_key(P, sk, a, e) if elt == 0 else galois_key(P, sk, elt, a, e)
+
+
 def keygen_from_seed(P: Params, sk: SecretKey, seed: int, elt: int) -> np.ndarray:
     """Key for Galois element ``elt`` (0: relinearisation), randomness drawn
     by the shared recipe."""

@@ -302,3 +302,71 @@ void or_fast_bconv(const u64* src, int ns, const u64* sq, u64* dst, int nd, cons
   free(qhat_inv);
   free(qhat_mod);
 }
+
+/* ------------------------------------------------- seed-expanded key halves
+ *
+ * Philox4x64-10 (Salmon, Moraes, Dror and Shaw, "Parallel random numbers: as
+ * easy as 1, 2, 3", SC 2011): a counter-based generator; the block function
+ * maps a 4-word counter and a 2-word key to 4 words by ten rounds of
+ *   (x0, x1, x2, x3) <- (hi(M1 x2) ^ x1 ^ k0, lo(M1 x2), hi(M0 x0) ^ x3 ^ k1,
+ *                        lo(M0 x0)),  (k0, k1) += (W0, W1)
+ * with M0 = 0xD2E7470EE14C6C93, M1 = 0xCA5A826395121157 and the Weyl
+ * increments W0 = 0x9E3779B97F4A7C15, W1 = 0xBB67AE8584CAA73B.
+ */
+void or_philox4x64(const u64* ctr, u64 k0, u64 k1, u64* out) {
+  u64 x0 = ctr[0], x1 = ctr[1], x2 = ctr[2], x3 = ctr[3];
+  for (int r = 0; r < 10; ++r) {
+    const u128 p0 = (u128)0xD2E7470EE14C6C93ull * x0;
+    const u128 p1 = (u128)0xCA5A826395121157ull * x2;
+    const u64 y0 = (u64)(p1 >> 64) ^ x1 ^ k0, y1 = (u64)p1;
+    const u64 y2 = (u64)(p0 >> 64) ^ x3 ^ k1, y3 = (u64)p0;
+    x0 = y0; x1 = y1; x2 = y2; x3 = y3;
+    k0 += 0x9E3779B97F4A7C15ull;
+    k1 += 0xBB67AE8584CAA73Bull;
+  }
+  out[0] = x0; out[1] = x1; out[2] = x2; out[3] = x3;
+}
+
+static int bitlen(u64 q) {
+  int b = 0;
+  while (q >> b) ++b;
+  return b;
+}
+
+/* The uniform half a_j[row][k] of a switching key, regenerated from a
+ * 2-word seed instead of being stored.  For coefficient k, extended prime
+ * `row_id` (the prime's index in the full chain: q_i -> i, p_k -> L + k),
+ * Galois element `elt` (0: relinearisation) and digit block c (digits
+ * 3c .. 3c + 2), one Philox call on the counter (k, row_id, c, elt) gives
+ * words w0..w3; digit 3c + i takes w_i masked to the bit length of q if that
+ * is below q, else the spare w3 (masked) if no earlier digit of the block
+ * took it and it is below q, else w_i mod q.
+ * out: [dnum][rows][n]; moduli and row_ids: [rows]. */
+void or_seeded_key_a(u64* out, int dnum, int rows, long n, const u64* moduli, const u64* row_ids,
+                     u64 k0, u64 k1, u64 elt) {
+#pragma omp parallel for schedule(static)
+  for (long t = 0; t < (long)rows * n; ++t) {
+    const int r = (int)(t / n);
+    const long k = t % n;
+    const u64 q = moduli[r], mask = (q >> 63) ? ~0ull : ((1ull << bitlen(q)) - 1);
+    for (int c = 0; 3 * c < dnum; ++c) {
+      const u64 ctr[4] = {(u64)k, row_ids[r], (u64)c, elt};
+      u64 w[4];
+      or_philox4x64(ctr, k0, k1, w);
+      int spare = 1;
+      for (int i = 0; i < 3 && 3 * c + i < dnum; ++i) {
+        u64 v = w[i] & mask;
+        if (v >= q) {
+          const u64 s = w[3] & mask;
+          if (spare && s < q) {
+            v = s;
+            spare = 0;
+          } else {
+            v = w[i] % q;
+          }
+        }
+        out[((size_t)(3 * c + i) * rows + r) * n + k] = v;
+      }
+    }
+  }
+}

@@ -26,6 +26,7 @@ __all__ = [
     "uniform_pm1",
     "normal",
     "moduli_tag",
+    "switch_key_seed_draws",
 ]
 
 
@@ -131,6 +132,19 @@ def switch_key_draws(seed: int, ext_moduli, n: int, dnum: int, elt: int):
     e = np.stack([rounded_gaussian(seed, "ksk-e/" + mt, n, ERROR_SIGMA, ERROR_BOUND, elt, j)
                   for j in range(dnum)])
     return np.ascontiguousarray(a), np.ascontiguousarray(e)
+
+
+def switch_key_seed_draws(seed: int, ext_moduli, n: int, dnum: int, elt: int):
+    """Raw draws of one seed-expanded switching key: two 64-bit seed words
+    (the uniform half is regenerated from them by the counter-based generator
+    on either side) and ``int64[dnum][n]`` rounded-Gaussian errors.  Tags
+    differ from switch_key_draws' (a seeded and a stored key of one element
+    must not share errors) and include the extended modulus chain."""
+    mt = moduli_tag(ext_moduli)
+    words = rng(seed, "ksk-seed/" + mt, elt).integers(0, 2 ** 64, size=2, dtype=np.uint64)
+    e = np.stack([rounded_gaussian(seed, "ksk-se/" + mt, n, ERROR_SIGMA, ERROR_BOUND, elt, j)
+                  for j in range(dnum)])
+    return words, np.ascontiguousarray(e)
 
 
 def encrypt_draws(seed: int, moduli, n: int, tag: str, *idx: int):

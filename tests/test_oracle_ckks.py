@@ -382,3 +382,70 @@ def test_key_sets_over_a_shared_chain_prefix_are_independent():
     e_shared = np.ascontiguousarray(ef[:Pc.dnum])
     np.testing.assert_array_equal(
         recovered(C.galois_key(Pc, skc, g, a_shared, e_shared)), s_g)
+
+
+# ------------------------------------------------- seed-expanded key halves
+
+
+def test_philox4x64_matches_numpy():
+    """The oracle's Philox4x64-10 block function equals numpy's Philox bit
+    generator (which advances its counter before each block)."""
+    for key, ctr in [((1, 2), (6, 0, 0, 0)), ((0xDEADBEEF, 7), (1, 2, 3, 4)),
+                     ((2 ** 64 - 1, 2 ** 63), (2 ** 64 - 1, 5, 0, 2 ** 40))]:
+        prev = list(ctr)
+        i = 0
+        while prev[i] == 0:          # counter - 1 with borrow
+            prev[i] = 2 ** 64 - 1
+            i += 1
+        prev[i] -= 1
+        bg = np.random.Philox(key=np.array(key, dtype=np.uint64),
+                              counter=np.array(prev, dtype=np.uint64))
+        assert [int(v) for v in bg.random_raw(4)] == C.philox4x64(ctr, *key)
+
+
+def test_seeded_key_halves_are_uniform_residues():
+    """Regenerated key halves: every value below its prime, deterministic,
+    different for another seed, element or row, and close to uniform; with a
+    modulus just above a power of two (half of the masked words rejected) the
+    spare word and the fallback keep every value in range and uniform."""
+    P = C.params_small(10, 50, 5, 2)
+    a = C.seeded_key_a(P, (11, 22), 5)
+    b = C.seeded_key_a(P, (11, 22), 5)
+    assert np.array_equal(a, b)
+    mods = np.array(P.ext(P.L), dtype=np.uint64)[None, :, None]
+    assert np.all(a < mods)
+    assert not np.array_equal(a, C.seeded_key_a(P, (11, 23), 5))
+    assert not np.array_equal(a, C.seeded_key_a(P, (11, 22), 7))
+    assert not np.array_equal(a[0, 0], a[0, 1]) and not np.array_equal(a[0, 0], a[1, 0])
+    u = (a / mods).ravel()
+    assert abs(u.mean() - 0.5) < 0.01 and abs(u.var() - 1 / 12) < 0.01
+    # a contrived modulus 2^49 + 1 (not a ring prime: the expansion rule alone)
+    q = (1 << 49) + 1
+    out = np.empty((3, 1, 4096), dtype=np.uint64)
+    C.nat.lib().or_seeded_key_a(C.nat.u64p(out), 3, 1, 4096,
+                                C.nat.u64p(np.array([q], dtype=np.uint64)),
+                                C.nat.u64p(np.array([0], dtype=np.uint64)), 5, 6, 0)
+    assert np.all(out < q)
+    v = out.ravel() / q
+    assert abs(v.mean() - 0.5) < 0.02
+    hist = np.histogram(v, bins=8, range=(0, 1))[0]
+    assert hist.min() > 0.8 * len(v) / 8
+
+
+def test_seeded_keys_switch_keys():
+    """A rotation and a relinearisation with seed-expanded keys decrypt to
+    the rotated / multiplied message."""
+    P = C.params_small(10, 50, 4, 2)
+    sk = C.secret_key(P, synth.secret(8, P.n))
+    g = P.galois_elt(3)
+    w, e = synth.switch_key_seed_draws(8, P.ext(P.L), P.n, P.dnum, g)
+    keys = {g: C.keygen_seeded(P, sk, w, e, g)}
+    w0, e0 = synth.switch_key_seed_draws(8, P.ext(P.L), P.n, P.dnum, 0)
+    rlk = C.keygen_seeded(P, sk, w0, e0, 0)
+    z1, z2 = _z(90, P.n // 2), _z(91, P.n // 2)
+    c1 = _enc(P, sk, z1, 2.0 ** 40, P.L, "seeded", 0)
+    c2 = _enc(P, sk, z2, 2.0 ** 40, P.L, "seeded", 1)
+    np.testing.assert_allclose(C.decrypt(P, sk, C.rotate(P, c1, 3, keys), 2.0 ** 40),
+                               np.roll(z1, -3), atol=2.0 ** -20)
+    np.testing.assert_allclose(C.decrypt(P, sk, C.mul_relin(P, c1, c2, rlk), 2.0 ** 80),
+                               z1 * z2, atol=2.0 ** -20)
