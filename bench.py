@@ -111,8 +111,19 @@ def log(msg):
 
 # --------------------------------------------------------------- workloads
 
+def keygen_into(W, ctx, elt, seed, moduli, dnum):
+    """Switching key of `elt` in `ctx` from the synthetic draws: seed-expanded
+    (W.seeded_keys) or stored."""
+    if W.seeded_keys:
+        w, e = W.synth.switch_key_seed_draws(seed, moduli, W.n, dnum, elt)
+        ctx.keygen_seeded(elt, W.s_dev, w, W.dev(e))
+    else:
+        a, e = W.synth.switch_key_draws(seed, moduli, W.n, dnum, elt)
+        ctx.keygen(elt, W.s_dev, W.dev(a), W.dev(e))
+
+
 class Workloads:
-    def __init__(self, F, torch, np, skip_matvec=False, affine_only=False):
+    def __init__(self, F, torch, np, skip_matvec=False, affine_only=False, seeded_keys=True):
         import synth
         import synth.workloads as WL
         self.F, self.torch, self.np, self.WL, self.synth = F, torch, np, WL, synth
@@ -126,6 +137,10 @@ class Workloads:
         self.s = synth.secret(WL.CFG3["seed"], self.n)
         self.s_dev = torch.from_numpy(self.s).cuda()
         self._keys = set()
+        # switching keys seed-expanded (the context keeps the seed and the b
+        # half; the key switch regenerates the uniform half) unless asked
+        # for stored keys
+        self.seeded_keys = seeded_keys
         if affine_only:
             return
         self.setup_ntt()
@@ -144,8 +159,7 @@ class Workloads:
     def keygen(self, elt, seed):
         if elt in self._keys:
             return
-        a, e = self.synth.switch_key_draws(seed, self.q + self.p, self.n, 3, elt)
-        self.ctx.keygen(elt, self.s_dev, self.dev(a), self.dev(e))
+        keygen_into(self, self.ctx, elt, seed, self.q + self.p, 3)
         self._keys.add(elt)
 
     def encrypt(self, z, scale, level, seed, tag, idx):
@@ -369,8 +383,7 @@ def time_hescan(W, F, torch, np, L=2048, block=1024, level=23, chunks=12, d_s=12
     lq, lp = W.q[:low_q], W.p[:low_alpha]
     cctx = F.Context(W.log_n, lq, lp)
     for g in [0, 2 * n - 1] + [ctx.galois_element(d_s >> k) for k in range(1, d_s.bit_length())]:
-        a, e = W.synth.switch_key_draws(seed, lq + lp, n, -(-low_q // low_alpha), g)
-        cctx.keygen(g, W.s_dev, W.dev(a), W.dev(e))
+        keygen_into(W, cctx, g, seed, lq + lp, -(-low_q // low_alpha))
     words = lambda lvl: lvl * 2 * n
     rnd = lambda rows, lvl: torch.randint(0, 1 << 49, (rows, words(lvl)), dtype=torch.int64,
                                           device="cuda")
@@ -844,6 +857,9 @@ def main():
     ap.add_argument("--cpu-sample", choices=("all", "single"),
                     help="(internal) time the oracle's bounded samples in this process and "
                          "print them as JSON; no GPU is used")
+    ap.add_argument("--stored-keys", action="store_true",
+                    help="switching keys stored whole (both halves read by every key switch) "
+                         "instead of seed-expanded")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run one 1 GiB device-to-device copy, the reference kernel for "
                          "scaling hardware traffic counters")
@@ -877,7 +893,7 @@ def main():
         print(json.dumps(out), flush=True)
         return
     if args.hescan_sweep:
-        W = Workloads(F, torch, np, affine_only=True)
+        W = Workloads(F, torch, np, affine_only=True, seeded_keys=not args.stored_keys)
         sweep = {}
         for L in (128, 256, 512, 1024, 2048):
             log(f"HEScan layer sweep: L = {L}")
@@ -885,17 +901,17 @@ def main():
         print(json.dumps({"hescan_layer_sweep": sweep}), flush=True)
         return
     if args.scan_sweep:
-        W = Workloads(F, torch, np, affine_only=True)
+        W = Workloads(F, torch, np, affine_only=True, seeded_keys=not args.stored_keys)
         print(json.dumps({"scan_block_sweep": scan_block_sweep(W, F, torch, np)}), flush=True)
         return
     if args.affine_only:
-        W = Workloads(F, torch, np, affine_only=True)
+        W = Workloads(F, torch, np, affine_only=True, seeded_keys=not args.stored_keys)
         comp = {"affine_scan": time_affine(W, F, torch, np)}
         if not args.no_hescan:
             comp["hescan_layer"] = time_hescan(W, F, torch, np)
         print(json.dumps({"components": comp}), flush=True)
         return
-    W = Workloads(F, torch, np)
+    W = Workloads(F, torch, np, seeded_keys=not args.stored_keys)
     torch.cuda.synchronize()
     # register-resident arithmetic peaks of this device (VALU roof)
     peak = {k: W.ctx.calib_valu(v) for k, v in (("ct", F.CALIB_CT), ("gs", F.CALIB_GS),
@@ -1016,7 +1032,9 @@ def main():
                                "special primes) + 768x1536 BSGS projection (12 -> 24 cts, "
                                "16 limbs) + scan-contract slice of a block of 16 Mamba-base "
                                "tokens (12 state chunks each, 20 -> 18 limbs)",
-                   "log_n": 16, "limbs": 24, "special_primes": 8, "parallelism": "single GPU"},
+                   "log_n": 16, "limbs": 24, "special_primes": 8, "parallelism": "single GPU",
+                   "switching_keys": "seed-expanded (seed and b half stored, a regenerated "
+                                     "in the key switch)" if W.seeded_keys else "stored whole"},
         "components": {
             "ntt_gbs": round(ntt_gbs, 2),
             "ntt_fwd_ms": round(fwd, 4), "ntt_inv_ms": round(inv, 4),

@@ -227,9 +227,25 @@ int fesc_rotate_batch_noalloc(fesc_ctx* ctx, uint32_t count, const uint64_t* con
 int fesc_keygen(fesc_ctx* ctx, uint32_t galois_elt, const int8_t* s, const uint64_t* a,
                 const int64_t* e, void* stream);
 
+/* The same key with its uniform half drawn from a seed instead of passed in:
+ * seed: uint64[2] in HOST memory.  a_j[i][k] comes from the counter-based
+ * generator Philox4x64-10 (Salmon et al., SC 2011) keyed by the seed: the
+ * block of counter (k, i, c, galois_elt), i the extended prime's index in the
+ * full chain (q_i -> i, p_m -> L + m), gives words w0..w3 for digits 3c ..
+ * 3c + 2; digit 3c + t takes w_t masked to the bit length of the prime when
+ * that is below the prime, else the spare word w3 (masked) if no earlier
+ * digit of the block took it and it is below the prime, else w_t mod the
+ * prime.  The context stores only the seed and the b half (half the bytes);
+ * key switching regenerates a where it reads the key, so rotations,
+ * conjugations and relinearisation give the residues they give with the full
+ * key.  fesc_key_store writes the full layout. */
+int fesc_keygen_seeded(fesc_ctx* ctx, uint32_t galois_elt, const int8_t* s,
+                       const uint64_t* seed, const int64_t* e, void* stream);
+
 /* Copy a key (layout above, device memory) into / out of the context.
  * galois_elt: 0 (relinearisation) or odd in (1, 2N), else FESC_ERR_ARG;
- * store: FESC_ERR_NO_KEY if the context holds no key of that element. */
+ * store: FESC_ERR_NO_KEY if the context holds no key of that element; a
+ * seed-expanded key is written in the full layout (a regenerated). */
 int fesc_key_load(fesc_ctx* ctx, uint32_t galois_elt, const uint64_t* key, void* stream);
 int fesc_key_store(fesc_ctx* ctx, uint32_t galois_elt, uint64_t* key, void* stream);
 

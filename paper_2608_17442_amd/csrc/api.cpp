@@ -98,8 +98,6 @@ int op_rotate_many(Context* c, const uint64_t* in, uint32_t count, const int32_t
 int op_mul_relin(Context* c, const uint64_t* a, const uint64_t* b, uint64_t* out,
                  uint32_t level, hipStream_t s);
 int op_rescale(Context* c, const uint64_t* in, uint64_t* out, uint32_t level, hipStream_t s);
-int op_keygen(Context* c, uint32_t galois, const int8_t* sk, const uint64_t* a, const int64_t* e,
-              hipStream_t s);
 int op_encrypt(Context* c, const int8_t* sk, const int64_t* m, const uint64_t* a,
                const int64_t* e, uint64_t* ct, uint32_t level, hipStream_t s);
 int op_plain_from_coeffs(Context* c, const int64_t* m, uint64_t* pt, uint32_t level,
@@ -304,26 +302,20 @@ static int check_galois(const fesc_ctx* ctx, uint32_t galois_elt) {
   return FESC_OK;
 }
 
-// The context's key slot of `galois_elt` (allocated on first use).
-static int key_slot(fesc_ctx* ctx, uint32_t galois_elt, uint64_t** out) {
-  const size_t bytes = (size_t)ctx->dnum * (ctx->L + ctx->alpha) * 2 * ctx->n * 8;
-  uint64_t*& dst = ctx->keys[galois_elt];
-  if (!dst && hipMalloc(&dst, bytes) != hipSuccess) {
-    ctx->keys.erase(galois_elt);
-    return fail(FESC_ERR_OOM, "key allocation failed");
-  }
-  *out = dst;
-  return FESC_OK;
-}
-
 int fesc_keygen(fesc_ctx* ctx, uint32_t galois_elt, const int8_t* s, const uint64_t* a,
                 const int64_t* e, void* stream) {
   if (!ctx || !s || !a || !e) return fail(FESC_ERR_ARG, "null argument");
   int rc = check_galois(ctx, galois_elt);
   if (rc) return rc;
-  if ((rc = op_keygen(ctx, galois_elt, s, a, e, S(stream)))) return rc;
-  ctx->key_cap.erase(ctx->keys[galois_elt]);
-  return FESC_OK;
+  return op_keygen(ctx, galois_elt, s, a, e, nullptr, S(stream));
+}
+
+int fesc_keygen_seeded(fesc_ctx* ctx, uint32_t galois_elt, const int8_t* s,
+                       const uint64_t* seed, const int64_t* e, void* stream) {
+  if (!ctx || !s || !seed || !e) return fail(FESC_ERR_ARG, "null argument");
+  int rc = check_galois(ctx, galois_elt);
+  if (rc) return rc;
+  return op_keygen(ctx, galois_elt, s, nullptr, e, seed, S(stream));
 }
 
 int fesc_key_load(fesc_ctx* ctx, uint32_t galois_elt, const uint64_t* key, void* stream) {
@@ -331,10 +323,9 @@ int fesc_key_load(fesc_ctx* ctx, uint32_t galois_elt, const uint64_t* key, void*
   int rc = check_galois(ctx, galois_elt);
   if (rc) return rc;
   uint64_t* dst;
-  if ((rc = key_slot(ctx, galois_elt, &dst))) return rc;
-  ctx->key_cap.erase(dst);
-  const size_t bytes = (size_t)ctx->dnum * (ctx->L + ctx->alpha) * 2 * ctx->n * 8;
-  return hip_check(hipMemcpyAsync(dst, key, bytes, hipMemcpyDeviceToDevice, S(stream)),
+  if ((rc = key_buffer(ctx, galois_elt, full_key_words(ctx), &dst))) return rc;
+  return hip_check(hipMemcpyAsync(dst, key, full_key_words(ctx) * 8, hipMemcpyDeviceToDevice,
+                                  S(stream)),
                    "key_load");
 }
 
@@ -346,13 +337,13 @@ int fesc_key_upload(fesc_ctx* ctx, uint32_t galois_elt, const uint64_t* host_key
   if (key_level < 1 || key_level > ctx->L)
     return fail(FESC_ERR_LEVEL, "key_level must be in 1 .. L");
   uint64_t* dst;
-  if ((rc = key_slot(ctx, galois_elt, &dst))) return rc;
+  if ((rc = key_buffer(ctx, galois_elt, full_key_words(ctx), &dst))) return rc;
   const size_t n = ctx->n, E = ctx->L + ctx->alpha, Ek = key_level + ctx->alpha;
   const uint32_t dk = (key_level + ctx->alpha - 1) / ctx->alpha;
   hipStream_t st = S(stream);
   // rows the prefix key does not hold stay zero; the key-switch driver
   // refuses this key above key_level
-  rc = hip_check(hipMemsetAsync(dst, 0, (size_t)ctx->dnum * E * 2 * n * 8, st), "key_upload");
+  rc = hip_check(hipMemsetAsync(dst, 0, full_key_words(ctx) * 8, st), "key_upload");
   for (uint32_t j = 0; j < dk && !rc; ++j) {
     const uint64_t* src = host_key + (size_t)j * Ek * 2 * n;
     uint64_t* d = dst + (size_t)j * E * 2 * n;
@@ -365,10 +356,7 @@ int fesc_key_upload(fesc_ctx* ctx, uint32_t galois_elt, const uint64_t* host_key
   }
   if (!rc) rc = hip_check(hipStreamSynchronize(st), "key_upload");
   if (rc) return rc;
-  if (key_level < ctx->L)
-    ctx->key_cap[dst] = key_level;
-  else
-    ctx->key_cap.erase(dst);
+  if (key_level < ctx->L) ctx->key_cap[dst] = key_level;
   return FESC_OK;
 }
 
@@ -376,8 +364,10 @@ int fesc_key_store(fesc_ctx* ctx, uint32_t galois_elt, uint64_t* key, void* stre
   if (!ctx || !key) return fail(FESC_ERR_ARG, "null argument");
   auto it = ctx->keys.find(galois_elt);
   if (it == ctx->keys.end()) return fail(FESC_ERR_NO_KEY, "no such key");
-  const size_t bytes = (size_t)ctx->dnum * (ctx->L + ctx->alpha) * 2 * ctx->n * 8;
-  return hip_check(hipMemcpyAsync(key, it->second, bytes, hipMemcpyDeviceToDevice, S(stream)),
+  if (ctx->key_seeded.count(it->second))  // expanded to the full layout
+    return hip_check(k_key_expand_launch(ctx, it->second, key, S(stream)), "key_store");
+  return hip_check(hipMemcpyAsync(key, it->second, full_key_words(ctx) * 8,
+                                  hipMemcpyDeviceToDevice, S(stream)),
                    "key_store");
 }
 

@@ -9,6 +9,7 @@
 // so the prime of row r is r >> 1.
 #include "fesc_internal.hpp"
 #include "ops.hpp"
+#include "seedkey.hpp"
 
 namespace fesc {
 
@@ -199,21 +200,57 @@ __global__ __launch_bounds__(kThreads) void k_keygen(const uint64_t* __restrict_
                                                      uint64_t* __restrict__ key, uint32_t n,
                                                      uint32_t L, uint32_t alpha,
                                                      const double2* __restrict__ pmod,
-                                                     const PrimeK* __restrict__ pk) {
+                                                     const PrimeK* __restrict__ pk, KeySeed sd) {
   const uint32_t i = blockIdx.y, j = blockIdx.z, E = L + alpha;
   const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
+  if (sd.seeded && blockIdx.x == 0 && i == 0 && j == 0 && threadIdx.x < kSeedHeaderWords)
+    key[threadIdx.x] = threadIdx.x == 0 ? sd.s0 : threadIdx.x == 1 ? sd.s1
+                     : threadIdx.x == 2 ? sd.elt : 0;
   if (k >= n) return;
   const PrimeK P = pk[i];
   const size_t oj = ((size_t)j * E + i) * n + k;
-  const double av = ld(a + oj);
+  double av;
+  uint64_t au;
+  if (sd.seeded) {  // the uniform half regenerated from the seed
+    uint64_t blk[3] = {0, 0, 0};
+    seeded_key_block(blk, k, i, j / 3, sd.elt, sd.s0, sd.s1, sd.dnum, P);
+    au = blk[j % 3];
+  } else {
+    au = a[oj];
+  }
+  av = u2d(au);
   double b = ld(e_ntt + oj) - mm_var(av, ld(s + (size_t)i * n + k), P.q, P.qinv);
   if (i < L && i >= j * alpha && i < (j + 1) * alpha) {
     const double2 pm = pmod[i];
     b += mm_shoup(ld(s_from + (size_t)i * n + k), pm.x, pm.y, P.q);
   }
+  if (sd.seeded) {  // compact layout: header, then b only
+    st(key + kSeedHeaderWords + oj, b, P.q, P.qinv);
+    return;
+  }
   const size_t ok = (((size_t)j * E + i) * 2) * n + k;
   st(key + ok, b, P.q, P.qinv);
-  key[ok + n] = a[oj];
+  key[ok + n] = au;
+}
+
+// Full layout [dnum][L+alpha][2][N] of a compact seed-expanded key: b copied,
+// a regenerated (one generator block per thread: digits 3*blockIdx.z ..).
+__global__ __launch_bounds__(kThreads) void k_key_expand(const uint64_t* __restrict__ compact,
+                                                         uint64_t* __restrict__ full, uint32_t n,
+                                                         uint32_t E, uint32_t dnum,
+                                                         const PrimeK* __restrict__ pk) {
+  const uint32_t i = blockIdx.y, c = blockIdx.z;
+  const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
+  if (k >= n) return;
+  const PrimeK P = pk[i];
+  uint64_t blk[3] = {0, 0, 0};
+  seeded_key_block(blk, k, i, c, compact[2], compact[0], compact[1], dnum, P);
+  for (uint32_t t = 0; t < 3 && 3 * c + t < dnum; ++t) {
+    const uint32_t j = 3 * c + t;
+    const size_t ok = (((size_t)j * E + i) * 2) * n + k;
+    full[ok] = compact[kSeedHeaderWords + ((size_t)j * E + i) * n + k];
+    full[ok + n] = blk[t];
+  }
 }
 
 // ct[i][0] = -a*s + me, ct[i][1] = a
@@ -299,9 +336,17 @@ hipError_t k_lift_launch(const Context* c, const int64_t* x, const int8_t* x8, u
 
 hipError_t k_keygen_launch(const Context* c, const uint64_t* a, const uint64_t* e_ntt,
                            const uint64_t* s, const uint64_t* s_from, uint64_t* key,
-                           const double2* pmod, hipStream_t st) {
+                           const double2* pmod, const KeySeed& sd, hipStream_t st) {
   hipLaunchKernelGGL(k_keygen, grid_rows(c->n, c->L + c->alpha, c->dnum), dim3(kThreads), 0, st,
-                     a, e_ntt, s, s_from, key, c->n, c->L, c->alpha, pmod, c->d_pk);
+                     a, e_ntt, s, s_from, key, c->n, c->L, c->alpha, pmod, c->d_pk, sd);
+  return hipGetLastError();
+}
+
+hipError_t k_key_expand_launch(const Context* c, const uint64_t* compact, uint64_t* full,
+                               hipStream_t st) {
+  hipLaunchKernelGGL(k_key_expand, grid_rows(c->n, c->L + c->alpha, (c->dnum + 2) / 3),
+                     dim3(kThreads), 0, st, compact, full, c->n, c->L + c->alpha, c->dnum,
+                     c->d_pk);
   return hipGetLastError();
 }
 

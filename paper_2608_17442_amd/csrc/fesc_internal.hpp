@@ -17,6 +17,7 @@
 #include <stddef.h>
 
 #include <map>
+#include <set>
 #include <string>
 #include <vector>
 
@@ -140,7 +141,10 @@ struct Context {
   double2* d_enc_tw = nullptr;
   int32_t* d_enc_inv = nullptr;
   // keys: Galois element (0 = relinearisation) -> device [dnum][L+alpha][2][N]
+  // (seed-expanded keys: the compact layout, see seedkey.hpp)
   std::map<uint32_t, uint64_t*> keys;
+  std::map<const uint64_t*, size_t> key_alloc;  // key buffer -> words allocated
+  std::set<const uint64_t*> key_seeded;          // key buffers in the compact layout
   // keys uploaded over a chain prefix: key buffer -> the highest level it
   // serves (keys absent here serve every level)
   std::map<const uint64_t*, uint32_t> key_cap;

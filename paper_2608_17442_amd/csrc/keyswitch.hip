@@ -26,6 +26,7 @@
 // are p_0..p_{alpha-1} (extended prime index L + k).
 #include "fesc_internal.hpp"
 #include "ops.hpp"
+#include "seedkey.hpp"
 
 namespace fesc {
 
@@ -46,7 +47,9 @@ __device__ __forceinline__ uint32_t ext_prime(uint32_t row, uint32_t level, uint
 // and reused by every job of the group.  With tab.fold the level rows
 // (row < level) store acc * P^-1 plus the job's addend components instead
 // (the addend read through the same permutation), so that the combine only
-// has to subtract y * P^-1.  D = number of digits at this level (compile
+// has to subtract y * P^-1.  A seed-expanded key (bit kg of tab.kg_seeded)
+// stores only its b half; its a half is regenerated here from the seed, which
+// halves the key bytes read.  D = number of digits at this level (compile
 // time).
 template <int D>
 __global__ __launch_bounds__(kThreads) void k_ip(KsTable tab, const uint64_t* __restrict__ ext,
@@ -67,11 +70,26 @@ __global__ __launch_bounds__(kThreads) void k_ip(KsTable tab, const uint64_t* __
   const uint32_t src = galois ? galois_src(k, galois, log_n) : k;
   const uint32_t own = row < level ? row / alpha : D;  // digit whose rows hold `row`
   double kb[D], ka[D];
+  if ((tab.kg_seeded >> kg) & 1u) {
+    // seed-expanded key: b read from the compact rows, a regenerated
+    const uint64_t s0 = key[0], s1 = key[1], elt = key[2];
 #pragma unroll
-  for (int j = 0; j < D; ++j) {
-    const size_t ko = (((size_t)j * KE + prime) * 2) * n + k;
-    kb[j] = u2d(key[ko]);
-    ka[j] = u2d(key[ko + n]);
+    for (int j = 0; j < D; ++j)
+      kb[j] = u2d(key[kSeedHeaderWords + ((size_t)j * KE + prime) * n + k]);
+#pragma unroll
+    for (int c = 0; 3 * c < D; ++c) {
+      uint64_t blk[3] = {0, 0, 0};
+      seeded_key_block(blk, k, prime, c, elt, s0, s1, D, M);
+#pragma unroll
+      for (int t = 0; t < 3 && 3 * c + t < D; ++t) ka[3 * c + t] = u2d(blk[t]);
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < D; ++j) {
+      const size_t ko = (((size_t)j * KE + prime) * 2) * n + k;
+      kb[j] = u2d(key[ko]);
+      ka[j] = u2d(key[ko + n]);
+    }
   }
   for (uint32_t job = j0; job < j1; ++job) {
     const uint32_t s = tab.job_src[job];

@@ -13,6 +13,7 @@
 #include "fesc_internal.hpp"
 #include "ops.hpp"
 #include "scratch.hpp"
+#include "seedkey.hpp"
 
 namespace fesc {
 
@@ -236,6 +237,7 @@ int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& sr
     for (uint32_t j = 0; j < nj; ++j) {
       const KsJob& J = jobs[order[j0 + j]];
       if (j == 0 || J.key != t.key[j - 1] || J.galois != t.galois[j - 1]) {
+        if (c->key_seeded.count(J.key)) t.kg_seeded |= 1u << nkeys;
         t.kg_first[nkeys] = j;
         t.kg_count[nkeys++] = 0;
       }
@@ -487,8 +489,42 @@ int op_rescale(Context* c, const uint64_t* in, uint64_t* out, uint32_t level, hi
   return op_rescale_many(c, 1, &in, &out, level, s);
 }
 
+size_t full_key_words(const Context* c) {
+  return (size_t)c->dnum * (c->L + c->alpha) * 2 * c->n;
+}
+
+size_t seeded_key_words(const Context* c) {
+  return kSeedHeaderWords + (size_t)c->dnum * (c->L + c->alpha) * c->n;
+}
+
+int key_buffer(Context* c, uint32_t galois, size_t words, uint64_t** out) {
+  auto it = c->keys.find(galois);
+  if (it != c->keys.end() && c->key_alloc[it->second] < words) {
+    uint64_t* old = it->second;
+    // work in flight may still read the old key
+    const int rc = hip_check(hipDeviceSynchronize(), "key replacement");
+    if (rc) return rc;
+    c->key_alloc.erase(old);
+    c->key_cap.erase(old);
+    c->key_seeded.erase(old);
+    c->keys.erase(it);
+    (void)hipFree(old);
+    it = c->keys.end();
+  }
+  if (it == c->keys.end()) {
+    uint64_t* key = nullptr;
+    if (hipMalloc(&key, words * 8) != hipSuccess) return fail(FESC_ERR_OOM, "key allocation failed");
+    it = c->keys.emplace(galois, key).first;
+    c->key_alloc[key] = words;
+  }
+  c->key_cap.erase(it->second);
+  c->key_seeded.erase(it->second);
+  *out = it->second;
+  return FESC_OK;
+}
+
 int op_keygen(Context* c, uint32_t galois, const int8_t* sk, const uint64_t* a, const int64_t* e,
-              hipStream_t s) {
+              const uint64_t* seed, hipStream_t s) {
   const size_t n = c->n;
   const uint32_t E = c->L + c->alpha;
   int err;
@@ -497,14 +533,8 @@ int op_keygen(Context* c, uint32_t galois, const int8_t* sk, const uint64_t* a, 
   Scratch S;
   if ((err = scratch(c, &S))) return err;
   uint64_t* key = nullptr;
-  auto it = c->keys.find(galois);
-  if (it != c->keys.end()) {
-    key = it->second;
-  } else {
-    if (hipMalloc(&key, (size_t)c->dnum * E * 2 * n * 8) != hipSuccess)
-      return fail(FESC_ERR_OOM, "key allocation failed");
-    c->keys[galois] = key;
-  }
+  if ((err = key_buffer(c, galois, seed ? seeded_key_words(c) : full_key_words(c), &key)))
+    return err;
   uint64_t* s_ext = S.acc;            // [E][N]
   uint64_t* s_from = S.acc + E * n;   // [E][N]
   uint64_t* e_ntt = S.ext;            // [dnum][E][N]
@@ -517,7 +547,10 @@ int op_keygen(Context* c, uint32_t galois, const int8_t* sk, const uint64_t* a, 
   for (uint32_t j = 0; j < c->dnum; ++j)
     HIPCK(k_lift_launch(c, e + (size_t)j * n, nullptr, e_ntt + (size_t)j * E * n, E, 0, E, 0, s));
   HIPCK(ntt_rows(c, e_ntt, c->dnum, (size_t)E * n, E, 0, false, s));
-  HIPCK(k_keygen_launch(c, a, e_ntt, s_ext, s_from, key, T->pmod, s));
+  KeySeed sd{};
+  if (seed) sd = KeySeed{seed[0], seed[1], galois, c->dnum, 1u};
+  HIPCK(k_keygen_launch(c, a, e_ntt, s_ext, s_from, key, T->pmod, sd, s));
+  if (seed) c->key_seeded.insert(key);
   return FESC_OK;
 }
 

@@ -45,9 +45,17 @@ hipError_t k_galois_launch(const Context* c, const uint64_t* in, uint64_t* out, 
 hipError_t k_lift_launch(const Context* c, const int64_t* x, const int8_t* x8, uint64_t* out,
                          uint32_t rows, uint32_t prime0, uint32_t split, uint32_t prime1,
                          hipStream_t s);
+// Seed of a seed-expanded switching key (seeded = 0: a full key, `a` given).
+struct KeySeed {
+  uint64_t s0, s1, elt;
+  uint32_t dnum, seeded;
+};
 hipError_t k_keygen_launch(const Context* c, const uint64_t* a, const uint64_t* e_ntt,
                            const uint64_t* s, const uint64_t* s_from, uint64_t* key,
-                           const double2* pmod, hipStream_t st);
+                           const double2* pmod, const KeySeed& sd, hipStream_t st);
+// full layout [dnum][L+alpha][2][N] of a compact seed-expanded key
+hipError_t k_key_expand_launch(const Context* c, const uint64_t* compact, uint64_t* full,
+                               hipStream_t st);
 hipError_t k_encrypt_launch(const Context* c, const uint64_t* a, const uint64_t* s,
                             const uint64_t* me, uint64_t* ct, uint32_t level, hipStream_t st);
 
@@ -87,6 +95,9 @@ struct KsTable {
   // group g holds jobs kg_first[g] .. kg_first[g] + kg_count[g] - 1
   uint32_t kg_first[kMaxBatch];
   uint32_t kg_count[kMaxBatch];
+  // bit g set: key group g's key is seed-expanded (compact layout, its
+  // uniform half regenerated in the inner product)
+  uint32_t kg_seeded;
   // 1 when every job's addend uses the job's own Galois element (or there is
   // none): the inner product then stores acc * P^-1 + add on the level rows
   // and the combine only subtracts y * P^-1
@@ -175,6 +186,19 @@ int op_rotate_batch_static(Context* c, uint32_t count, const uint64_t* const* in
                            const int32_t* steps, uint64_t* const* outs, uint32_t level,
                            hipStream_t s);
 int op_rescale(Context* c, const uint64_t* in, uint64_t* out, uint32_t level, hipStream_t s);
+// Switching key of `galois` from the secret s (int8 coefficients) and the
+// error e ([dnum][N]); seed null: uniform half `a` given ([dnum][L+alpha][N]),
+// full layout; seed (two host words): `a` regenerated from it, compact layout.
+int op_keygen(Context* c, uint32_t galois, const int8_t* sk, const uint64_t* a, const int64_t* e,
+              const uint64_t* seed, hipStream_t s);
+// Words of a key in the full layout [dnum][L+alpha][2][N] and in the compact
+// seed-expanded layout (header + [dnum][L+alpha][N]).
+size_t full_key_words(const Context* c);
+size_t seeded_key_words(const Context* c);
+// The key buffer of `galois` with room for `words` words (the present one
+// reused if large enough, else replaced); its prefix-level and seed records
+// are cleared.
+int key_buffer(Context* c, uint32_t galois, size_t words, uint64_t** out);
 // Relinearised products out_i = a_i * b_i (batched); out_i may alias a_i or b_i.
 int op_mul_relin_many(Context* c, uint32_t count, const uint64_t* const* as,
                       const uint64_t* const* bs, uint64_t* const* outs, uint32_t level,

@@ -57,6 +57,7 @@ _SIGS = {
     "fesc_rotate_batch_noalloc": [_vp, _u32, ctypes.POINTER(_vp), ctypes.POINTER(_i32),
                                   ctypes.POINTER(_vp), _u32, _vp],
     "fesc_keygen": [_vp, _u32, _vp, _vp, _vp, _vp],
+    "fesc_keygen_seeded": [_vp, _u32, _vp, _vp, _vp, _vp],
     "fesc_key_load": [_vp, _u32, _vp, _vp],
     "fesc_key_store": [_vp, _u32, _vp, _vp],
     "fesc_key_upload": [_vp, _u32, _vp, _u32, _vp],
@@ -295,6 +296,17 @@ class Context:
         _check(_lib.fesc_keygen(self._h, galois_elt, _ptr(s, self.n, "s", torch.int8),
                                 _ptr(a, self.dnum * E * self.n, "a"),
                                 _ptr(e, self.dnum * self.n, "e"), _stream(stream)))
+
+    def keygen_seeded(self, galois_elt, s, seed_words, e, stream=None):
+        """fesc_keygen_seeded: the key's uniform half drawn from two 64-bit
+        seed words (host integers); the context keeps the seed and b only."""
+        w = [int(v) for v in seed_words]
+        if len(w) != 2 or not all(0 <= v < 1 << 64 for v in w):
+            raise ValueError("seed_words: two integers in [0, 2^64)")
+        seed = (ctypes.c_uint64 * 2)(*w)
+        _check(_lib.fesc_keygen_seeded(self._h, galois_elt, _ptr(s, self.n, "s", torch.int8),
+                                       ctypes.addressof(seed),
+                                       _ptr(e, self.dnum * self.n, "e"), _stream(stream)))
 
     def key_load(self, galois_elt, key, stream=None):
         _check(_lib.fesc_key_load(self._h, galois_elt, _ptr(key, self.key_words(), "key"),

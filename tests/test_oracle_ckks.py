@@ -432,6 +432,55 @@ def test_seeded_key_halves_are_uniform_residues():
     assert hist.min() > 0.8 * len(v) / 8
 
 
+def _numpy_philox_block(ctr, key):
+    prev = list(ctr)
+    i = 0
+    while prev[i] == 0:          # counter - 1 with borrow
+        prev[i] = 2 ** 64 - 1
+        i += 1
+    prev[i] -= 1
+    bg = np.random.Philox(key=np.array(key, dtype=np.uint64),
+                          counter=np.array(prev, dtype=np.uint64))
+    return [int(v) for v in bg.random_raw(4)]
+
+
+def test_seeded_key_counter_layout_and_rule_from_numpy_philox():
+    """Brute force of the key-half expansion on a tiny case with words from
+    numpy's Philox (not the oracle's block function): counter (k, row id,
+    digit block, element), digit 3c + t from word t masked, the spare word 3
+    for the first rejected digit of a block, the remainder after that.  Four
+    digits span two blocks; one modulus sits just above a power of two."""
+    mods = [C.find_primes(12, 50, 1)[0], (1 << 45) + 1, (1 << 47) + 5]
+    row_ids, n, dnum, key, elt = [3, 9, 30], 64, 4, (0x1234, 0xFEDC), 7
+    got = np.empty((dnum, len(mods), n), dtype=np.uint64)
+    C.nat.lib().or_seeded_key_a(C.nat.u64p(got), dnum, len(mods), n,
+                                C.nat.u64p(np.array(mods, dtype=np.uint64)),
+                                C.nat.u64p(np.array(row_ids, dtype=np.uint64)), key[0], key[1],
+                                elt)
+    branches = {"masked": 0, "spare": 0, "rem": 0}
+    for r, (q, rid) in enumerate(zip(mods, row_ids)):
+        mask = (1 << q.bit_length()) - 1
+        for k in range(n):
+            for c in range((dnum + 2) // 3):
+                w = _numpy_philox_block((k, rid, c, elt), key)
+                spare_free = True
+                for t in range(3):
+                    d = 3 * c + t
+                    if d >= dnum:
+                        break
+                    v = w[t] & mask
+                    if v < q:
+                        branches["masked"] += 1
+                    elif spare_free and (w[3] & mask) < q:
+                        v, spare_free = w[3] & mask, False
+                        branches["spare"] += 1
+                    else:
+                        v = w[t] % q
+                        branches["rem"] += 1
+                    assert int(got[d, r, k]) == v, (d, r, k)
+    assert min(branches.values()) > 0, branches
+
+
 def test_seeded_keys_switch_keys():
     """A rotation and a relinearisation with seed-expanded keys decrypt to
     the rotated / multiplied message."""
