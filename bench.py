@@ -535,9 +535,12 @@ def modmul_probe(ctx, F) -> dict:
     integer Shoup, on every CU with no memory traffic (products per second)."""
     f = ctx.calib_valu(F.CALIB_MODMUL_F64)
     u = ctx.calib_valu(F.CALIB_MODMUL_U64)
+    ph = ctx.calib_valu(F.CALIB_PHILOX, 1 << 12)
     return {"fp64_shoup_per_s": round(f, -9), "u64_shoup_per_s": round(u, -9),
             "fp64_over_u64": round(f / u, 2),
-            "kernels": "k_calib_modmul_f64 / k_calib_modmul_u64 (fesc_calib_valu)"}
+            "philox4x64_blocks_per_s": round(ph, -8),
+            "kernels": "k_calib_modmul_f64 / k_calib_modmul_u64 / k_calib_philox "
+                       "(fesc_calib_valu)"}
 
 
 def keyswitch_per_kernel():

@@ -557,8 +557,10 @@ int fesc_encode(uint32_t log_n, const double* re, const double* im, double scale
  * FESC_CALIB_MODMUL_U64: the residue product alone in the library's fp64 form
  * (exact product split by one FMA, quotient from the precomputed w / q) and
  * in the 64-bit integer Shoup form (quotient from the high half of
- * x * floor(w 2^64 / q)), the evidence for the fp64 choice.  Each thread
- * runs `iters` iterations (1 .. 2^20) of 32 butterflies or 8 products.
+ * x * floor(w 2^64 / q)), the evidence for the fp64 choice;
+ * FESC_CALIB_PHILOX: Philox4x64-10 blocks, the generator of seed-expanded
+ * keys (rate in blocks per second).  Each thread runs `iters` iterations
+ * (1 .. 2^20) of 32 butterflies, 8 products or 2 generator blocks.
  * Synchronises `stream`; uses context scratch; FESC_ERR_ARG for a bad kind
  * or count. */
 #define FESC_CALIB_CT 0
@@ -566,6 +568,7 @@ int fesc_encode(uint32_t log_n, const double* re, const double* im, double scale
 #define FESC_CALIB_MAC 2
 #define FESC_CALIB_MODMUL_F64 3
 #define FESC_CALIB_MODMUL_U64 4
+#define FESC_CALIB_PHILOX 5
 int fesc_calib_valu(fesc_ctx* ctx, int kind, uint32_t iters, double* rate, void* stream);
 
 #ifdef __cplusplus

@@ -7,6 +7,7 @@
 
 #include "butterfly.hpp"
 #include "fesc_internal.hpp"
+#include "seedkey.hpp"
 
 namespace fesc {
 
@@ -121,10 +122,23 @@ __global__ __launch_bounds__(kThreads) void k_calib_modmul_u64(uint64_t q, uint6
   out[t] = (double)(s & 0xFFFFFFFFull);
 }
 
+// The generator of seed-expanded keys: two independent chains of
+// Philox4x64-10 blocks per thread, each block's output the next counter.
+__global__ __launch_bounds__(kThreads) void k_calib_philox(uint64_t k0, uint64_t k1,
+                                                           uint32_t iters, double* out) {
+  const uint32_t t = blockIdx.x * kThreads + threadIdx.x;
+  uint64_t x[4] = {t, 1, 2, 3}, y[4] = {t, 5, 6, 7};
+  for (uint32_t i = 0; i < iters; ++i) {
+    philox4x64_10(x, k0, k1);
+    philox4x64_10(y, k1, k0);
+  }
+  out[t] = (double)((x[0] ^ x[1] ^ x[2] ^ x[3] ^ y[0] ^ y[1] ^ y[2] ^ y[3]) & 0xFFFFFFFFull);
+}
+
 }  // namespace
 
 int calib_valu(Context* c, int kind, uint32_t iters, double* rate, hipStream_t s) {
-  if (kind < FESC_CALIB_CT || kind > FESC_CALIB_MODMUL_U64 || iters == 0 || iters > (1u << 20))
+  if (kind < FESC_CALIB_CT || kind > FESC_CALIB_PHILOX || iters == 0 || iters > (1u << 20))
     return fail(FESC_ERR_ARG, "bad calibration arguments");
   int cus = 0;
   if (int rc = hip_check(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount,
@@ -150,7 +164,10 @@ int calib_valu(Context* c, int kind, uint32_t iters, double* rate, hipStream_t s
   const uint64_t qu = c->primes[0], wu = qu / 3 + 12345;
   const uint64_t wpu = (uint64_t)(((unsigned __int128)wu << 64) / qu);
   auto launch = [&]() {
-    if (kind == FESC_CALIB_MODMUL_F64)
+    if (kind == FESC_CALIB_PHILOX)
+      hipLaunchKernelGGL(k_calib_philox, dim3(blocks), dim3(kThreads), 0, s,
+                         0x0123456789ABCDEFull, 0xFEDCBA9876543210ull, iters, out);
+    else if (kind == FESC_CALIB_MODMUL_F64)
       hipLaunchKernelGGL(k_calib_modmul_f64, dim3(blocks), dim3(kThreads), 0, s, q, (double)wu,
                          (double)wu / q, iters, out);
     else if (kind == FESC_CALIB_MODMUL_U64)
@@ -178,7 +195,9 @@ int calib_valu(Context* c, int kind, uint32_t iters, double* rate, hipStream_t s
   (void)hipEventDestroy(e1);
   if (rc) return rc;
   const double per_thread =
-      (kind == FESC_CALIB_CT || kind == FESC_CALIB_GS) ? 32.0 * iters : 8.0 * iters;
+      (kind == FESC_CALIB_CT || kind == FESC_CALIB_GS) ? 32.0 * iters
+      : kind == FESC_CALIB_PHILOX                      ? 2.0 * iters
+                                                       : 8.0 * iters;
   *rate = (double)blocks * kThreads * per_thread / (ms * 1e-3);
   return FESC_OK;
 }

@@ -89,7 +89,7 @@ _SIGS = {
 }
 
 CONJ = -(2 ** 31)
-CALIB_CT, CALIB_GS, CALIB_MAC, CALIB_MODMUL_F64, CALIB_MODMUL_U64 = 0, 1, 2, 3, 4
+CALIB_CT, CALIB_GS, CALIB_MAC, CALIB_MODMUL_F64, CALIB_MODMUL_U64, CALIB_PHILOX = 0, 1, 2, 3, 4, 5
 SCAN_STATES_ONLY = 1
 
 for _name, _args in _SIGS.items():

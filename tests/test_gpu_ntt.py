@@ -205,9 +205,13 @@ def test_calib_valu_rates_are_positive_and_ordered():
     ctx = F.Context(P.log_n, P.q, P.p)
     step("calib valu")
     r = {k: ctx.calib_valu(k, 256) for k in (F.CALIB_CT, F.CALIB_GS, F.CALIB_MAC,
-                                              F.CALIB_MODMUL_F64, F.CALIB_MODMUL_U64)}
+                                              F.CALIB_MODMUL_F64, F.CALIB_MODMUL_U64,
+                                              F.CALIB_PHILOX)}
     print({k: f"{v / 1e12:.3f} T/s" for k, v in r.items()})
     for v in r.values():
         assert np.isfinite(v) and 1e9 < v < 1e14
+    # a generator block is ten rounds of two 64 x 64 -> 128-bit products:
+    # far dearer than one modular product
+    assert r[F.CALIB_PHILOX] < r[F.CALIB_MODMUL_F64] / 4
     with pytest.raises(F.FescError):
         ctx.calib_valu(7, 16)
