@@ -827,9 +827,16 @@ def cpu_baseline() -> dict:
     out["nproc"] = len(os.sched_getaffinity(0))
     try:
         lscpu = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=30).stdout
-        out["cpu_model"] = next(l.split(":", 1)[1].strip() for l in lscpu.splitlines()
-                                if l.startswith("Model name"))
-    except (OSError, StopIteration, subprocess.SubprocessError):
+        fields = dict(l.split(":", 1) for l in lscpu.splitlines() if ":" in l)
+        fields = {k.strip(): v.strip() for k, v in fields.items()}
+        out["cpu_model"] = fields.get("Model name")
+        # the model string can be generic under virtualisation: keep the
+        # identifying fields lscpu reports next to it
+        out["lscpu"] = {k: fields[k] for k in (
+            "Architecture", "Vendor ID", "Model name", "CPU family", "Model", "Stepping",
+            "CPU(s)", "Thread(s) per core", "Core(s) per socket", "Socket(s)", "CPU max MHz",
+            "L3 cache", "Hypervisor vendor", "Virtualization type") if k in fields}
+    except (OSError, ValueError, subprocess.SubprocessError):
         pass
     return out
 

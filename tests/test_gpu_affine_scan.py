@@ -159,15 +159,17 @@ def test_affine_scan_down_to_level_one(small, L, level, states_only):
 
 def test_affine_scan_bench_configuration():
     """The benchmark's launch: 128 tokens x 12 chunks at 16 limbs (N = 2^16),
-    states only, in place.  Prefix k depends only on tokens 0..k and the
-    network forms positions below 2^m exactly as a 2^m-token network does, so
-    the oracle checks sampled prefixes from the first tokens: chunk 0 through
-    32 tokens, chunk 11 through 8; every other tuple is uniform residues.
-    Compared on the leading limbs of the common output level."""
+    states only, in place.  Chunk 0 holds 128 real tokens and is compared
+    whole against the oracle's 128-token network (every up- and down-sweep
+    position, down to the deepest); chunk 11 holds 8 real tokens, compared
+    through prefix 8 (prefix k depends only on tokens 0..k and the network
+    forms positions below 2^m exactly as a 2^m-token network does); every
+    other tuple is uniform residues.  Compared on the leading limbs of the
+    common output level."""
     P = C.params_p16(24)
     S = Setup(P, 54, relin=True)
     L, chunks, level = 128, 12, 16
-    real = {0: 32, chunks - 1: 8}
+    real = {0: L, chunks - 1: 8}
     words = level * 2 * P.n
     ad, sd, ao, so = [], [], {}, {}
     for c in range(chunks):
