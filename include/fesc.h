@@ -539,6 +539,22 @@ int fesc_c2m_level(const uint64_t* q, uint32_t level, uint32_t ell, uint32_t sig
 int fesc_encode_plain(fesc_ctx* ctx, const double* z, uint32_t count, double scale, uint64_t* pt,
                       uint32_t level, void* stream);
 
+/* Decoding on the device, the inverse of fesc_encode_plain (Sec. 2.1: slot j is
+ * the evaluation at zeta^(5^j mod 2N), zeta = exp(i pi / N)): evaluation-form
+ * plaintexts pt[count][level][N] (device, canonical residues) -> slot vectors
+ * z[count][N/2] (device, complex as interleaved re/im doubles),
+ *     z_j = m(zeta^(5^j)) / scale,
+ * m the plaintext's centred integer coefficients in (-Q/2, Q/2], Q the product
+ * of the level's primes.  m is reconstructed exactly by a mixed-radix CRT with
+ * balanced digits and evaluated in fp64 (a relative error of about level units
+ * in the last place; coefficients beyond the double range give infinities),
+ * then transformed by an fp64 FFT.  Decoding needs no secret key: a client
+ * decodes after decrypting.  pt is left unchanged.  FESC_ERR_LEVEL for a level
+ * outside 1..L, FESC_ERR_ARG for a zero or non-finite scale or a null buffer;
+ * count 0 does nothing.  Uses the context's scratch. */
+int fesc_decode_plain(fesc_ctx* ctx, const uint64_t* pt, uint32_t count, uint32_t level,
+                      double scale, double* z, void* stream);
+
 /* Host helper: CKKS encoding of n = N/2 complex slots (re, im host arrays;
  * im may be NULL) at scale Delta into int64 coefficients, rounded half away
  * from zero; slot j is the evaluation at exp(i pi 5^j / N).  FESC_ERR_ARG if

@@ -289,6 +289,13 @@ def encode_plain(P: Params, z, scale: float, level: int) -> np.ndarray:
     return ntt(P, lift(m, P.qs(level)), P.qs(level))
 
 
+def decode_plain(P: Params, pt: np.ndarray, scale: float) -> np.ndarray:
+    """Slots of an evaluation-form plaintext ``u64[level][N]``: its centred
+    integer coefficients (exact CRT) evaluated at zeta^(5^j), over scale."""
+    mods = P.qs(pt.shape[0])
+    return enc.decode_coeffs(enc.crt_centered(intt(P, pt, mods), mods), scale, P.n)
+
+
 def encrypt(P: Params, sk: SecretKey, pt: np.ndarray, level: int, a, e) -> np.ndarray:
     """Secret-key encryption: c1 = a, c0 = -a*s + m + e.  ``u64[level][2][N]``."""
     mods = P.qs(level)

@@ -120,6 +120,8 @@ int c2m_level(const uint64_t* q, uint32_t level, uint32_t ell, uint32_t sigma, d
 int scratch_slots(Context* c, uint64_t** cts, uint32_t* cap);
 int op_encode_plain(Context* c, const double2* z, uint32_t count, double scale, uint64_t* pt,
                     uint32_t level, uint64_t* slots, uint32_t nslots, hipStream_t s);
+int op_decode_plain(Context* c, const uint64_t* pt, uint32_t count, uint32_t level, double scale,
+                    double2* z, uint64_t* slots, uint32_t nslots, hipStream_t s);
 int op_affine_scan(Context* c, uint64_t* const* a, uint64_t* const* s, uint32_t L,
                    uint32_t chunks, uint32_t level, bool states_only, uint32_t* out_level,
                    hipStream_t st);
@@ -583,6 +585,20 @@ int fesc_encode_plain(fesc_ctx* ctx, const double* z, uint32_t count, double sca
   if ((rc = scratch_slots(ctx, &slots, &cap))) return rc;
   return op_encode_plain(ctx, reinterpret_cast<const double2*>(z), count, scale, pt, level, slots,
                          cap, S(stream));
+}
+
+int fesc_decode_plain(fesc_ctx* ctx, const uint64_t* pt, uint32_t count, uint32_t level,
+                      double scale, double* z, void* stream) {
+  int rc = check_level(ctx, level);
+  if (rc) return rc;
+  if (!(std::fabs(scale) > 0.0 && std::fabs(scale) < HUGE_VAL)) return fail(FESC_ERR_ARG, "bad scale");
+  if (count == 0) return FESC_OK;
+  if (!z || !pt) return fail(FESC_ERR_ARG, "null buffer");
+  uint64_t* slots;
+  uint32_t cap;
+  if ((rc = scratch_slots(ctx, &slots, &cap))) return rc;
+  return op_decode_plain(ctx, pt, count, level, scale, reinterpret_cast<double2*>(z), slots, cap,
+                         S(stream));
 }
 
 int fesc_c2m_level(const uint64_t* q, uint32_t level, uint32_t ell, uint32_t sigma, double delta,

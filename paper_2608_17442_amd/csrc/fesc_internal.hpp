@@ -140,6 +140,9 @@ struct Context {
   // conj(z_j) if inv[p] = ~j)
   double2* d_enc_tw = nullptr;
   int32_t* d_enc_inv = nullptr;
+  // device decoding's mixed-radix CRT: [L][L], entry [i][j] (j < i) =
+  // q_j^-1 mod q_i as {w, w / q_i}, w the balanced representative
+  double2* d_garner = nullptr;
   // keys: Galois element (0 = relinearisation) -> device [dnum][L+alpha][2][N]
   // (seed-expanded keys: the compact layout, see seedkey.hpp)
   std::map<uint32_t, uint64_t*> keys;

@@ -232,7 +232,19 @@ static int build_tables(Context* c) {
       e = e * 5 % (2ull * n);
     }
   }
+  std::vector<double2> garner((size_t)c->L * c->L, double2{0.0, 0.0});
+  for (uint32_t i = 0; i < c->L; ++i)
+    for (uint32_t j = 0; j < i; ++j) {
+      const uint64_t qi = c->primes[i];
+      const uint64_t v = h_inv(c->primes[j] % qi, qi);
+      const double w = v > qi / 2 ? -(double)(qi - v) : (double)v;
+      garner[(size_t)i * c->L + j] = double2{w, w / (double)qi};
+    }
   int rc;
+  if ((rc = hip_check(hipMalloc(&c->d_garner, sizeof(double2) * garner.size()), "hipMalloc")) ||
+      (rc = hip_check(hipMemcpy(c->d_garner, garner.data(), sizeof(double2) * garner.size(),
+                                hipMemcpyHostToDevice), "hipMemcpy")))
+    return rc == FESC_ERR_HIP ? fail(FESC_ERR_OOM, "decoding table allocation failed") : rc;
   if ((rc = hip_check(hipMalloc(&c->d_enc_tw, sizeof(double2) * enc_tw.size()), "hipMalloc")) ||
       (rc = hip_check(hipMalloc(&c->d_enc_inv, sizeof(int32_t) * enc_inv.size()), "hipMalloc")) ||
       (rc = hip_check(hipMemcpy(c->d_enc_tw, enc_tw.data(), sizeof(double2) * enc_tw.size(),
@@ -272,6 +284,7 @@ void destroy(Context* c) {
   (void)hipFree(c->d_tw3_inv);
   (void)hipFree(c->d_enc_tw);
   (void)hipFree(c->d_enc_inv);
+  (void)hipFree(c->d_garner);
   (void)hipFree(c->scratch);
   delete static_cast<fesc_ctx*>(c);
 }

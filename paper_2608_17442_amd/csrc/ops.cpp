@@ -535,6 +535,9 @@ int op_keygen(Context* c, uint32_t galois, const int8_t* sk, const uint64_t* a, 
   uint64_t* key = nullptr;
   if ((err = key_buffer(c, galois, seed ? seeded_key_words(c) : full_key_words(c), &key)))
     return err;
+  // recorded before any launch: should one fail, the buffer is still read
+  // with the layout it was allocated for
+  if (seed) c->key_seeded.insert(key);
   uint64_t* s_ext = S.acc;            // [E][N]
   uint64_t* s_from = S.acc + E * n;   // [E][N]
   uint64_t* e_ntt = S.ext;            // [dnum][E][N]
@@ -550,7 +553,6 @@ int op_keygen(Context* c, uint32_t galois, const int8_t* sk, const uint64_t* a, 
   KeySeed sd{};
   if (seed) sd = KeySeed{seed[0], seed[1], galois, c->dnum, 1u};
   HIPCK(k_keygen_launch(c, a, e_ntt, s_ext, s_from, key, T->pmod, sd, s));
-  if (seed) c->key_seeded.insert(key);
   return FESC_OK;
 }
 

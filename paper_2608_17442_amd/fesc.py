@@ -82,6 +82,7 @@ _SIGS = {
     "fesc_post_ssm": [_vp, _vp, _vp, _vp, _vp, _vp, _u32, _vp],
     "fesc_add_plain": [_vp, _vp, _vp, _vp, _u32, _vp],
     "fesc_encode_plain": [_vp, _vp, _u32, ctypes.c_double, _vp, _u32, _vp],
+    "fesc_decode_plain": [_vp, _vp, _u32, _u32, ctypes.c_double, _vp, _vp],
     "fesc_c2m_level": [ctypes.POINTER(_u64), _u32, _u32, _u32, ctypes.c_double, ctypes.c_double,
                        ctypes.POINTER(_u32)],
     "fesc_affine_scan_resident": [_vp, ctypes.POINTER(_vp), ctypes.POINTER(_vp), _u32, _u32,
@@ -424,6 +425,17 @@ class Context:
         _check(_lib.fesc_encode_plain(self._h, zr.data_ptr(), count, float(scale),
                                       _ptr(pt, count * self._pt(level), "pt"), level,
                                       _stream(stream)))
+
+    def decode_plain(self, pt, count, level, scale, z, stream=None):
+        """Device decoding: evaluation-form plaintexts pt (int64 tensor,
+        [count][level][N]) -> slot vectors z (complex128 CUDA tensor,
+        [count][N/2])."""
+        if not (z.is_cuda and z.dtype == torch.complex128 and z.is_contiguous()):
+            raise TypeError("z: a contiguous complex128 CUDA tensor")
+        if z.numel() < count * (self.n // 2):
+            raise ValueError(f"z: {z.numel()} slots, the call writes {count * (self.n // 2)}")
+        _check(_lib.fesc_decode_plain(self._h, _ptr(pt, count * self._pt(level), "pt"), count,
+                                      level, float(scale), z.data_ptr(), _stream(stream)))
 
     def key_words(self) -> int:
         return self.dnum * (self.L + self.alpha) * 2 * self.n

@@ -57,6 +57,22 @@ def test_encode_matches_direct_definition(log_n):
     np.testing.assert_allclose(ev, z, atol=1e-12)
 
 
+def test_decode_plain_inverts_encode_plain_across_primes():
+    """decode_plain of an evaluation-form encoding returns the slots; the
+    limb-wise product of two encodings (coefficients near 2^60, beyond one
+    36-bit prime) decodes to the slot product at the squared scale, which
+    needs the CRT over several primes (a single limb's centred residue is
+    far off)."""
+    P = C.params_small(10, 36, 4, 1)
+    z1, z2 = _z(61, P.n // 2), _z(62, P.n // 2)
+    d = 2.0 ** 30
+    p1, p2 = C.encode_plain(P, z1, d, 4), C.encode_plain(P, z2, d, 4)
+    np.testing.assert_allclose(C.decode_plain(P, p1, d), z1, atol=2.0 ** -20)
+    prod = C.pmul(p1, p2, P.qs(4))
+    np.testing.assert_allclose(C.decode_plain(P, prod, d * d), z1 * z2, atol=2.0 ** -18)
+    assert np.max(np.abs(C.decode_plain(P, prod[:1], d * d) - z1 * z2)) > 1.0
+
+
 def test_encode_rounding_half_away_from_zero():
     n = 8
     x = np.array([0.5, -0.5, 1.5, -1.5, 2.4999, -2.5001, 0.0, 3.0])
