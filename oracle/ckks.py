@@ -535,6 +535,64 @@ def rotate_hoisted(P: Params, ct: np.ndarray, rs, keys: dict) -> list:
     return outs
 
 
+def rotate_hoisted_ext(P: Params, ct: np.ndarray, rs, keys: dict) -> list:
+    """Hoisted rotations left in the extended basis Q u P: one ModUp of c1,
+    then per rotation the key product acc (as in rotate_hoisted) plus the
+    rotated c0 multiplied by the special modulus P, with no ModDown
+    (Bossuat et al., Eurocrypt 2021, double hoisting).  Each result is
+    ``u64[2][level+alpha][N]`` (component, extended row, coefficient) and
+    moddown_ct of it is the ordinary rotation.  r = 0 mod N/2 gives
+    (P c0, P c1), zero on the special-prime rows."""
+    level = ct.shape[0]
+    qs, ext = P.qs(level), P.ext(level)
+    pm = [P.P % q for q in qs]
+    ext_coef = modup(P, intt(P, ct[:, 1], qs), level)
+    outs = []
+    for r in rs:
+        x = np.zeros((2, len(ext), P.n), dtype=np.uint64)
+        if r % (P.n // 2) == 0:
+            x[0, :level] = pscalar(ct[:, 0], pm, qs)
+            x[1, :level] = pscalar(ct[:, 1], pm, qs)
+            outs.append(x)
+            continue
+        g = P.galois_elt(r)
+        digits = [ntt(P, automorph_coef(P, d, ext, g), ext) for d in ext_coef]
+        acc = key_inner_product(P, digits, keys[g], level)
+        x[0] = acc[0]
+        x[0, :level] = padd(acc[0][:level], pscalar(automorph(P, ct[:, 0], qs, g), pm, qs), qs)
+        x[1] = acc[1]
+        outs.append(x)
+    return outs
+
+
+def moddown_ct(P: Params, x: np.ndarray, level: int) -> np.ndarray:
+    """ModDown of both components of an extended-basis ciphertext
+    ``u64[2][level+alpha][N]`` into ``u64[level][2][N]``."""
+    out = np.empty((level, 2, P.n), dtype=np.uint64)
+    for t in range(2):
+        out[:, t] = moddown(P, x[t], level)
+    return out
+
+
+def encode_plain_ext(P: Params, z, scale: float, level: int) -> np.ndarray:
+    """Encoded slot vector over the extended basis Q_level u P (evaluation
+    form), ``u64[level+alpha][N]``."""
+    ext = P.ext(level)
+    m = enc.encode(np.asarray(z, dtype=np.complex128), scale, P.n)
+    return ntt(P, lift(m, ext), ext)
+
+
+def mul_plain_ext(P: Params, x: np.ndarray, pt: np.ndarray) -> np.ndarray:
+    """Extended-basis ciphertext times an extended-basis plaintext."""
+    ext = P.ext(x.shape[1] - P.alpha)
+    return np.stack([pmul(x[t], pt, ext) for t in range(2)])
+
+
+def ext_add(P: Params, x: np.ndarray, y: np.ndarray) -> np.ndarray:
+    ext = P.ext(x.shape[1] - P.alpha)
+    return np.stack([padd(x[t], y[t], ext) for t in range(2)])
+
+
 def rescale(P: Params, ct: np.ndarray) -> np.ndarray:
     """Divide by the last prime with rounding: c' = (c - v) * q_last^-1 where
     v is the centred residue of c modulo q_last."""

@@ -61,6 +61,10 @@ class MatvecDesc:
     # outputs in pairs: the n_out diagonal sets are taken as (2P, 2P+1) and
     # output P is y_2P + conj(y_2P+1) (n_out / 2 output ciphertexts)
     complex_pair: bool = False
+    # double hoisting: baby steps stay in the extended basis Q u P (no
+    # ModDown), the plaintext MAC runs there with diagonals encoded over
+    # Q u P, and each giant step's inner sum takes one ModDown
+    lazy_moddown: bool = False
 
     def baby_steps(self):
         return [q * self.unit for q in range(self.n1)]
@@ -78,10 +82,15 @@ def required_rotations(desc: MatvecDesc, n_slots: int) -> set:
 def bsgs_matvec(P: C.Params, desc: MatvecDesc, ins: list, diag, keys: dict,
                 blocks=None) -> list:
     """``diag(b, p, u, q)`` returns the evaluation-form plaintext D~_{b,u,p,q}
-    (``u64[level][N]``).  Baby steps are hoisted (one ModUp per input); giant
-    steps and the conjugation are ordinary key switches."""
+    (``u64[level][N]``; with lazy_moddown over Q u P, ``u64[level+alpha][N]``).
+    Baby steps are hoisted (one ModUp per input); with lazy_moddown they are
+    also left in Q u P and each inner sum over (u, q) takes one ModDown
+    (double hoisting).  Giant steps and the conjugation are ordinary key
+    switches."""
     assert len(ins) == desc.n_in
-    baby = [C.rotate_hoisted(P, x, desc.baby_steps(), keys) for x in ins]
+    lazy = desc.lazy_moddown
+    hoist = C.rotate_hoisted_ext if lazy else C.rotate_hoisted
+    baby = [hoist(P, x, desc.baby_steps(), keys) for x in ins]
 
     def giant_sum(b):
         y = None
@@ -89,8 +98,14 @@ def bsgs_matvec(P: C.Params, desc: MatvecDesc, ins: list, diag, keys: dict,
             acc = None
             for u in range(desc.n_in):
                 for q in range(desc.n1):
-                    t = C.mul_plain(P, baby[u][q], diag(b, p, u, q))
-                    acc = t if acc is None else C.ct_add(P, acc, t)
+                    if lazy:
+                        t = C.mul_plain_ext(P, baby[u][q], diag(b, p, u, q))
+                        acc = t if acc is None else C.ext_add(P, acc, t)
+                    else:
+                        t = C.mul_plain(P, baby[u][q], diag(b, p, u, q))
+                        acc = t if acc is None else C.ct_add(P, acc, t)
+            if lazy:
+                acc = C.moddown_ct(P, acc, desc.level)
             acc = C.rotate(P, acc, desc.giant_steps()[p], keys)
             y = acc if y is None else C.ct_add(P, y, acc)
         return y

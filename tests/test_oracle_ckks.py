@@ -348,6 +348,30 @@ def test_rotate_conjugate_hoisted(small):
                                atol=2.0 ** -20)
 
 
+def test_extended_basis_rotation_takes_one_moddown_to_the_rotation(small):
+    """A hoisted rotation left in Q u P (P sigma(c0) + acc, acc') is the
+    ordinary rotation after ModDown, residue for residue (ModDown divides by
+    P exactly on the P sigma(c0) term, which vanishes modulo every special
+    prime); the identity step gives (P c0, P c1)."""
+    P, sk = small
+    level = 5
+    ct = _enc(P, sk, _z(76, P.n // 2), 2.0 ** 30, level, "rot-ext")
+    rs = [0, 1, 3, P.n // 2]
+    keys = {P.galois_elt(r): C.keygen_from_seed(P, sk, 3, P.galois_elt(r)) for r in (1, 3)}
+    exts = C.rotate_hoisted_ext(P, ct, rs, keys)
+    for r, x in zip(rs, exts):
+        assert x.shape == (2, level + P.alpha, P.n)
+        np.testing.assert_array_equal(C.moddown_ct(P, x, level), C.rotate(P, ct, r, keys))
+    assert not np.any(exts[0][:, level:])
+    # one plaintext factor taken before the ModDown: the product decodes to
+    # the rotated slots times the plaintext's
+    w = _z(77, P.n // 2)
+    pt = C.encode_plain_ext(P, w, float(P.q[level - 1]), level)
+    y = C.rescale(P, C.moddown_ct(P, C.mul_plain_ext(P, exts[2], pt), level))
+    z = C.decrypt(P, sk, ct, 2.0 ** 30)
+    np.testing.assert_allclose(C.decrypt(P, sk, y, 2.0 ** 30), np.roll(z, -3) * w, atol=2.0 ** -12)
+
+
 def test_p12_parameters_roundtrip():
     """The N = 2^12 ring: alpha = 1, three single-prime digits."""
     P = C.params_p12()

@@ -164,6 +164,58 @@ def test_encrypted_bsgs_matvec_complex_paired_outputs():
         np.testing.assert_allclose(dec.imag, Y[r, (2 * pair + 1) * Cc + s], atol=2.0 ** -15)
 
 
+@pytest.mark.parametrize("paired", [False, True])
+def test_encrypted_bsgs_matvec_double_hoisted(paired):
+    """Double hoisting (baby steps left in Q u P, the plaintext MAC over
+    Q u P with diagonals encoded there, one ModDown per giant step's inner
+    sum) decodes to X W within 2^-15, with real extraction or with
+    complex-paired outputs, and within 2^-20 of the ordinary projection (the
+    two differ only in where the ModDown rounds)."""
+    P = C.params_small(10, 50, 4, 2)
+    sk = C.secret_key(P, synth.secret(3, P.n))
+    n_slots, seg_len, Cc = P.n // 2, 16, 32
+    T, d_in, d_out = 16, 128, 128
+    n1, n2 = 8, 4
+    level = 4
+    X = synth.normal(8, "X", (T, d_in))
+    Wm = synth.normal(8, "W", (d_in, d_out), 0.02)
+    args = (level, d_in // Cc // 2, d_out // Cc, n1, n2, seg_len, not paired, True)
+    desc = W.MatvecDesc(*args, complex_pair=paired, lazy_moddown=True)
+    plain = W.MatvecDesc(*args, complex_pair=paired)
+    keys = _keys(P, sk, 3, W.required_rotations(desc, n_slots), conj=True)
+    ins = []
+    for u in range(desc.n_in):
+        z = (W.pack_input(X, n_slots, seg_len, Cc, 2 * u)
+             + 1j * W.pack_input(X, n_slots, seg_len, Cc, 2 * u + 1))
+        a, e = synth.encrypt_draws(3, P.qs(level), P.n, "xdh", u)
+        ins.append(C.encrypt(P, sk, C.encode_plain(P, z, 2.0 ** 40, level), level, a, e))
+    ql = float(P.q[level - 1])
+
+    def slots(b, p, u, q):
+        if paired:
+            return W.bsgs_pair_diagonal_slots(Wm, n_slots, seg_len, Cc, n1, b, p, u, q)
+        return W.bsgs_diagonal_slots(Wm, n_slots, seg_len, Cc, n1, b, p, u, q, True)
+
+    blocks = [0, desc.n_out // 2 - 1] if paired else [0, desc.n_out - 1]
+    outs = W.bsgs_matvec(P, desc, ins,
+                         lambda b, p, u, q: C.encode_plain_ext(P, slots(b, p, u, q), ql, level),
+                         keys, blocks)
+    ref = W.bsgs_matvec(P, plain, ins,
+                        lambda b, p, u, q: C.encode_plain(P, slots(b, p, u, q), ql, level),
+                        keys, blocks)
+    Y = X @ Wm
+    r, s = W.segment_indices(n_slots, seg_len, Cc)
+    for blk, y, y0 in zip(blocks, outs, ref):
+        assert y.shape[0] == level - 1
+        assert not np.array_equal(y, y0)
+        dec = C.decrypt(P, sk, y, 2.0 ** 40)
+        re_blk, im_blk = (2 * blk, 2 * blk + 1) if paired else (blk, None)
+        np.testing.assert_allclose(dec.real, Y[r, re_blk * Cc + s], atol=2.0 ** -15)
+        if paired:
+            np.testing.assert_allclose(dec.imag, Y[r, im_blk * Cc + s], atol=2.0 ** -15)
+        np.testing.assert_allclose(dec, C.decrypt(P, sk, y0, 2.0 ** 40), atol=2.0 ** -20)
+
+
 def test_scan_contract_slice_small():
     P = C.params_small(10, 50, 4, 2)
     sk = C.secret_key(P, synth.secret(4, P.n))
