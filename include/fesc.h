@@ -301,8 +301,17 @@ typedef struct fesc_matvec_desc {
   uint32_t real_extract; /* 0 or 1 */
   uint32_t rescale;      /* 0 or 1 */
   uint32_t complex_pair; /* 0 or 1: outputs in pairs, see below */
+  uint32_t lazy_moddown; /* 0 or 1: double hoisting, see below */
 } fesc_matvec_desc;
 
+/* lazy_moddown = 1 (double hoisting; Bossuat, Mouchet, Troncoso-Pastoriza and
+ * Hubaux, Eurocrypt 2021): the baby steps stay in the extended basis Q u P
+ * (P Phi^q(c0) + acc, acc' with no ModDown), the pt-MAC runs over the
+ * level + alpha rows q_0 .. q_{level-1}, p_0 .. p_{alpha-1} with diagonals
+ * encoded there (fesc_encode_plain_ext: every diagonal and bank slot then has
+ * level + alpha rows), and each c~_{b,p} takes one ModDown before its giant
+ * step.  The results differ from lazy_moddown = 0 only in where ModDown
+ * rounds; the plan holds (n_in n1 + n_out n2) extended ciphertexts more. */
 typedef struct fesc_matvec_plan fesc_matvec_plan;
 
 /* Plan: `diags` is a host array of n_out*n2*n_in*n1 device pointers to
@@ -324,7 +333,8 @@ int fesc_ptct_matvec(fesc_ctx* ctx, fesc_matvec_plan* plan, const uint64_t* cons
  * streaming, [limb][N/256][n_out*n2][n_in*n1][256] (256-coefficient tiles;
  * one workgroup of the plaintext MAC then reads a contiguous region).
  * fesc_matvec_bank_words gives its size in uint64 words (level*N per
- * diagonal); fesc_matvec_bank_pack copies plaintext `pt` ([level][N]) into
+ * diagonal, (level+alpha)*N with lazy_moddown); fesc_matvec_bank_pack copies
+ * plaintext `pt` ([level][N], or [level+alpha][N]) into
  * slot `index` = ((b*n2 + p)*n_in + u)*n1 + q of the bank; a plan created
  * from a bank reads it instead of a pointer table (results are identical).
  * The bank must stay valid for the plan's lifetime. */
@@ -538,6 +548,13 @@ int fesc_c2m_level(const uint64_t* q, uint32_t level, uint32_t ell, uint32_t sig
  * the device).  Uses context scratch; asynchronous on `stream`. */
 int fesc_encode_plain(fesc_ctx* ctx, const double* z, uint32_t count, double scale, uint64_t* pt,
                       uint32_t level, void* stream);
+
+/* The same encoding over the extended basis of `level` (q_0 .. q_{level-1},
+ * then the special primes p_0 .. p_{alpha-1}): pt ([count][level+alpha][N],
+ * device), for the double-hoisted projection (fesc_matvec_desc.lazy_moddown),
+ * whose plaintext MAC runs before the ModDown. */
+int fesc_encode_plain_ext(fesc_ctx* ctx, const double* z, uint32_t count, double scale,
+                          uint64_t* pt, uint32_t level, void* stream);
 
 /* Decoding on the device, the inverse of fesc_encode_plain (Sec. 2.1: slot j is
  * the evaluation at zeta^(5^j mod 2N), zeta = exp(i pi / N)): evaluation-form

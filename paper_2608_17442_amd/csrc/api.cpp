@@ -119,7 +119,7 @@ int c2m_level(const uint64_t* q, uint32_t level, uint32_t ell, uint32_t sigma, d
               double bmax, uint32_t* out);
 int scratch_slots(Context* c, uint64_t** cts, uint32_t* cap);
 int op_encode_plain(Context* c, const double2* z, uint32_t count, double scale, uint64_t* pt,
-                    uint32_t level, uint64_t* slots, uint32_t nslots, hipStream_t s);
+                    uint32_t level, uint64_t* slots, uint32_t nslots, hipStream_t s, bool ext);
 int op_decode_plain(Context* c, const uint64_t* pt, uint32_t count, uint32_t level, double scale,
                     double2* z, uint64_t* slots, uint32_t nslots, hipStream_t s);
 int op_affine_scan(Context* c, uint64_t* const* a, uint64_t* const* s, uint32_t L,
@@ -573,8 +573,8 @@ int fesc_add_plain(fesc_ctx* ctx, const uint64_t* ct, const uint64_t* pt, uint64
   return op_add_plain(ctx, ct, pt, out, level, S(stream));
 }
 
-int fesc_encode_plain(fesc_ctx* ctx, const double* z, uint32_t count, double scale, uint64_t* pt,
-                      uint32_t level, void* stream) {
+static int encode_plain(fesc_ctx* ctx, const double* z, uint32_t count, double scale,
+                        uint64_t* pt, uint32_t level, void* stream, bool ext) {
   int rc = check_level(ctx, level);
   if (rc) return rc;
   if (!(std::fabs(scale) < 4611686018427387904.0)) return fail(FESC_ERR_ARG, "bad scale");
@@ -584,7 +584,17 @@ int fesc_encode_plain(fesc_ctx* ctx, const double* z, uint32_t count, double sca
   uint32_t cap;
   if ((rc = scratch_slots(ctx, &slots, &cap))) return rc;
   return op_encode_plain(ctx, reinterpret_cast<const double2*>(z), count, scale, pt, level, slots,
-                         cap, S(stream));
+                         cap, S(stream), ext);
+}
+
+int fesc_encode_plain(fesc_ctx* ctx, const double* z, uint32_t count, double scale, uint64_t* pt,
+                      uint32_t level, void* stream) {
+  return encode_plain(ctx, z, count, scale, pt, level, stream, false);
+}
+
+int fesc_encode_plain_ext(fesc_ctx* ctx, const double* z, uint32_t count, double scale,
+                          uint64_t* pt, uint32_t level, void* stream) {
+  return encode_plain(ctx, z, count, scale, pt, level, stream, true);
 }
 
 int fesc_decode_plain(fesc_ctx* ctx, const uint64_t* pt, uint32_t count, uint32_t level,

@@ -159,14 +159,17 @@ __global__ __launch_bounds__(kThreads) void k_enc_inner(const double2* __restric
 }
 
 // Lift: coefficient k (m at row k % M, position bitrev12(k / M)) of plaintext
-// blockIdx.z reduced into limb i = blockIdx.y of pt[b][level][N].
+// blockIdx.z reduced into row i = blockIdx.y of pt[b][rows][N]; row i uses
+// prime i below `split`, prime1 + (i - split) from there (the special primes
+// of an extended-basis plaintext).
 __global__ __launch_bounds__(kThreads) void k_enc_lift(const int64_t* __restrict__ mt,
                                                        uint64_t* __restrict__ pt, uint32_t n,
                                                        uint32_t M, uint32_t level,
+                                                       uint32_t split, uint32_t prime1,
                                                        const PrimeK* __restrict__ pk) {
   const uint32_t i = blockIdx.y, b = blockIdx.z;
   const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
-  const PrimeK P = pk[i];
+  const PrimeK P = pk[i < split ? i : prime1 + (i - split)];
   const uint32_t k1 = k % M, k2 = k / M;
   const int64_t v = mt[(size_t)b * n + (size_t)k1 * kRow + (__builtin_bitreverse32(k2) >> 20)];
   // exact for |v| < 2^63: hi * 2^32 + lo, each part reduced
@@ -180,12 +183,14 @@ __global__ __launch_bounds__(kThreads) void k_enc_lift(const int64_t* __restrict
 }  // namespace
 
 // Encodes `count` slot vectors z[count][N/2] (complex, device) at scale
-// `scale` into evaluation-form plaintexts pt[count][level][N], 32 per round
+// `scale` into evaluation-form plaintexts pt[count][rows][N], 32 per round
 // through the scratch ciphertext region (X and m of each plaintext in one
-// ciphertext slot: 3N words <= 2 L N).
+// ciphertext slot: 3N words <= 2 L N); rows = level, or level + alpha over
+// the extended basis q_0 .. q_{level-1}, p_0 .. p_{alpha-1} (ext).
 int op_encode_plain(Context* c, const double2* z, uint32_t count, double scale, uint64_t* pt,
-                    uint32_t level, uint64_t* slots, uint32_t nslots, hipStream_t s) {
+                    uint32_t level, uint64_t* slots, uint32_t nslots, hipStream_t s, bool ext) {
   const uint32_t n = c->n, M = n / kRow;
+  const uint32_t rows = ext ? level + c->alpha : level;
   const size_t W = (size_t)2 * c->L * n;
   for (uint32_t b0 = 0; b0 < count; b0 += nslots) {
     const uint32_t m = std::min(nslots, count - b0);
@@ -205,12 +210,12 @@ int op_encode_plain(Context* c, const double2* z, uint32_t count, double scale, 
     if (int rc = hip_check(hipGetLastError(), "k_enc_outer")) return rc;
     k_enc_inner<<<dim3(M, m), kThreads, 0, s>>>(X, c->d_enc_tw, mt, n, M, scale);
     if (int rc = hip_check(hipGetLastError(), "k_enc_inner")) return rc;
-    uint64_t* pb = pt + (size_t)b0 * level * n;
-    k_enc_lift<<<dim3(n / kThreads, level, m), kThreads, 0, s>>>(mt, pb, n, M, level, c->d_pk);
+    uint64_t* pb = pt + (size_t)b0 * rows * n;
+    k_enc_lift<<<dim3(n / kThreads, rows, m), kThreads, 0, s>>>(mt, pb, n, M, rows, level, c->L,
+                                                               c->d_pk);
     if (int rc = hip_check(hipGetLastError(), "k_enc_lift")) return rc;
-    if (int rc = hip_check(launch_ntt(c, pb, m, (size_t)level * n, level, n, 0, false, s),
-                           "encode NTT"))
-      return rc;
+    const RowSel rs{pb, (size_t)rows * n, (size_t)n, 0, level, c->L, 0, 0, 0};
+    if (int rc = hip_check(launch_ntt_rows(c, rs, m, rows, false, s), "encode NTT")) return rc;
   }
   return FESC_OK;
 }

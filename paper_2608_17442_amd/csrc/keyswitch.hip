@@ -44,10 +44,12 @@ __device__ __forceinline__ uint32_t ext_prime(uint32_t row, uint32_t level, uint
 //     acc[j][t][row][k] = sum_d D_d(src_j)[row][gsrc(k)] * key[d][prime(row)][t][k],
 // D_d(src) the ModUp digit d of the job's source, whose own-digit rows are the
 // source polynomial itself.  The key values of a coefficient are loaded once
-// and reused by every job of the group.  With tab.fold the level rows
+// and reused by every job of the group.  With tab.fold == 1 the level rows
 // (row < level) store acc * P^-1 plus the job's addend components instead
 // (the addend read through the same permutation), so that the combine only
-// has to subtract y * P^-1.  A seed-expanded key (bit kg of tab.kg_seeded)
+// has to subtract y * P^-1.  With tab.fold == 2 (extended-basis outputs, no
+// ModDown) every row goes to the job's output [2][level+alpha][N] and the
+// level rows add the addend times P (pinv then holds P mod q_row).  A seed-expanded key (bit kg of tab.kg_seeded)
 // stores only its b half; its a half is regenerated here from the seed, which
 // halves the key bytes read.  D = number of digits at this level (compile
 // time).
@@ -116,7 +118,16 @@ __global__ __launch_bounds__(kThreads) void k_ip(KsTable tab, const uint64_t* __
         aa = red_bal(aa, M.q, M.qinv);
       }
     }
-    if (tab.fold && row < level) {
+    if (tab.fold == 2 && row < level) {
+      // extended-basis output: the addend enters multiplied by P (pinv holds
+      // P mod q_row here), no ModDown follows
+      const double2 f = pinv[row];
+      const uint64_t* add = tab.add[job];
+      const uint32_t mask = tab.add_mask[job];
+      const size_t o0 = (size_t)2 * row * n + src, o1 = o0 + n;
+      if (add && (mask & 1u)) ab += mm_shoup(u2d(add[o0]), f.x, f.y, M.q);
+      if (add && (mask & 2u)) aa += mm_shoup(u2d(add[o1]), f.x, f.y, M.q);
+    } else if (tab.fold && row < level) {
       const double2 f = pinv[row];
       ab = mm_shoup(ab, f.x, f.y, M.q);
       aa = mm_shoup(aa, f.x, f.y, M.q);
@@ -134,7 +145,7 @@ __global__ __launch_bounds__(kThreads) void k_ip(KsTable tab, const uint64_t* __
         if (add && (mask & 2u)) aa += u2d(add[o1]);
       }
     }
-    uint64_t* out = acc + (size_t)job * 2 * E * n;
+    uint64_t* out = tab.fold == 2 ? tab.out[job] : acc + (size_t)job * 2 * E * n;
     out[(size_t)row * n + k] = to_res(ab, M.q, M.qinv);
     out[((size_t)E + row) * n + k] = to_res(aa, M.q, M.qinv);
   }

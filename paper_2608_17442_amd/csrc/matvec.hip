@@ -6,7 +6,10 @@
 //
 // Phi^delta is one rotation by delta * unit slots.  Baby steps Phi^q(x~_u)
 // share one ModUp per input (hoisted); giant steps and the conjugation are
-// ordinary key switches.
+// ordinary key switches.  Double hoisting (lazy_moddown; Bossuat et al.,
+// Eurocrypt 2021) also leaves the baby steps in the extended basis Q u P
+// (P Phi^q(c0) + acc, no ModDown), runs the pt-MAC there with diagonals
+// encoded over Q u P, and takes one ModDown per c~_{b,p}.
 //
 // The pt-MAC streams every plaintext diagonal once.  A thread owns one
 // coefficient of one limb and accumulates G outputs (b, p) at a time, so each
@@ -23,8 +26,11 @@ struct fesc_matvec_plan {
   std::vector<const uint64_t*> diag;  // host copy of the table [n_out][n2][n_in][n1]
   const uint64_t** d_diag = nullptr;  // device copy
   uint64_t* work = nullptr;           // baby [n_in][n1], c~ [n_out][n2], extraction [n_out] cts
-  const uint64_t** d_baby = nullptr;  // device table of baby pointers
-  uint64_t** d_ct = nullptr;          // device table of c~ pointers
+  // double hoisting: baby steps and c~ over the extended basis,
+  // [n_in n1 + n_out n2][2][level+alpha][N]
+  uint64_t* ext_work = nullptr;
+  const uint64_t** d_baby = nullptr;  // device table of baby pointers (pt-MAC inputs)
+  uint64_t** d_ct = nullptr;          // device table of c~ pointers (pt-MAC outputs)
   size_t ct_words = 0;
   const uint64_t* bank = nullptr;     // tiled diagonal bank (instead of the table), or null
   hipEvent_t ev[4] = {};               // phase marks of the last run
@@ -57,6 +63,13 @@ __host__ __device__ __forceinline__ size_t bank_offset(uint32_t i, uint32_t tile
 }
 
 // BANK: diagonals from a tiled bank; otherwise from the table of plaintexts.
+// Ciphertext rows: component c of limb i at i * row_stride + c * comp_stride
+// ([limbs][2][N]: 2N and N; extended basis [2][limbs][N]: N and limbs N);
+// limb i uses prime i below `split`, prime1 + (i - split) from there.
+struct PtLayout {
+  uint32_t row_stride, comp_stride, split, prime1;
+};
+
 template <int G, bool BANK>
 __global__ __launch_bounds__(kThreads) void k_ptmac(const uint64_t* const* __restrict__ baby,
                                                     const uint64_t* const* __restrict__ diag,
@@ -64,7 +77,7 @@ __global__ __launch_bounds__(kThreads) void k_ptmac(const uint64_t* const* __res
                                                     uint64_t* const* __restrict__ outs,
                                                     uint32_t n_outputs, uint32_t terms,
                                                     uint32_t n, uint32_t limbs,
-                                                    const PrimeK* __restrict__ pk) {
+                                                    const PrimeK* __restrict__ pk, PtLayout lay) {
   // 1-D grid over (coefficient tile, limb, output group).  Workgroups are
   // dealt to the 8 XCDs round-robin; the decode keeps all output groups of one
   // tile on the same XCD and adjacent in time, so the tile's baby-step values
@@ -84,12 +97,13 @@ __global__ __launch_bounds__(kThreads) void k_ptmac(const uint64_t* const* __res
   const uint32_t k = tile * kThreads + threadIdx.x;
   const uint32_t o0 = grp * G;
   if (i >= limbs) return;
-  const PrimeK P = pk[i];
+  const PrimeK P = pk[i < lay.split ? i : lay.prime1 + (i - lay.split)];
   const uint32_t g_end = min((uint32_t)G, n_outputs - o0);
   double a0[G], a1[G];
 #pragma unroll
   for (int g = 0; g < G; ++g) a0[g] = a1[g] = 0.0;
-  const size_t pi = (size_t)i * n + k, c0 = (size_t)2 * i * n + k, c1 = c0 + n;
+  const size_t pi = (size_t)i * n + k, c0 = (size_t)i * lay.row_stride + k,
+               c1 = c0 + lay.comp_stride;
   const uint64_t* bk =
       BANK ? bank + bank_offset(i, tile, o0, 0, n, n_outputs, terms) + threadIdx.x : nullptr;
   const size_t t_stride = (size_t)n_outputs * kThreads;
@@ -135,6 +149,25 @@ __global__ __launch_bounds__(kThreads) void k_bank_pack(const uint64_t* __restri
   const uint32_t i = blockIdx.y, tile = blockIdx.x;
   bank[bank_offset(i, tile, o, t, n, n_outputs, terms) + threadIdx.x] =
       pt[(size_t)i * n + (size_t)tile * kThreads + threadIdx.x];
+}
+
+// Identity baby step over the extended basis: x[t][i] = P c_t[i] on the
+// level rows (c = ct [level][2][N]), 0 on the special-prime rows.
+__global__ __launch_bounds__(kThreads) void k_ext_identity(const uint64_t* __restrict__ ct,
+                                                           uint64_t* __restrict__ x, uint32_t n,
+                                                           uint32_t level, uint32_t E,
+                                                           const double2* __restrict__ pmod,
+                                                           const PrimeK* __restrict__ pk) {
+  const uint32_t row = blockIdx.y, t = blockIdx.z;
+  const uint32_t k = blockIdx.x * kThreads + threadIdx.x;
+  if (k >= n) return;
+  uint64_t v = 0;
+  if (row < level) {
+    const PrimeK P = pk[row];
+    const double2 f = pmod[row];
+    v = to_res(mm_shoup(u2d(ct[((size_t)2 * row + t) * n + k]), f.x, f.y, P.q), P.q, P.qinv);
+  }
+  x[((size_t)t * E + row) * n + k] = v;
 }
 
 // Slot vectors of the diagonals first .. first + count - 1 (bank order) of a
@@ -197,7 +230,7 @@ int check_desc(const Context* c, const fesc_matvec_desc* d) {
   if (d->rescale && d->level < 2) return fail(FESC_ERR_LEVEL, "rescale needs level >= 2");
   if (!d->n_in || !d->n_out || !d->n1 || !d->n2 || !d->unit)
     return fail(FESC_ERR_ARG, "matvec sizes must be positive");
-  if (d->real_extract > 1 || d->rescale > 1 || d->complex_pair > 1)
+  if (d->real_extract > 1 || d->rescale > 1 || d->complex_pair > 1 || d->lazy_moddown > 1)
     return fail(FESC_ERR_ARG, "matvec flags must be 0 or 1");
   if (d->complex_pair && (d->real_extract || d->n_out % 2))
     return fail(FESC_ERR_ARG, "complex_pair needs an even n_out and real_extract = 0");
@@ -206,6 +239,12 @@ int check_desc(const Context* c, const fesc_matvec_desc* d) {
 
 static uint32_t matvec_outputs(const fesc_matvec_desc& d) {
   return d.complex_pair ? d.n_out / 2 : d.n_out;
+}
+
+// Rows of each diagonal: the level's primes, plus the special primes when the
+// pt-MAC runs over the extended basis.
+static uint32_t diag_rows(const Context* c, const fesc_matvec_desc& d) {
+  return d.level + (d.lazy_moddown ? c->alpha : 0);
 }
 
 int matvec_plan_create(Context* c, const fesc_matvec_desc* d, const uint64_t* const* diags,
@@ -238,13 +277,20 @@ int matvec_plan_create(Context* c, const fesc_matvec_desc* d, const uint64_t* co
   const size_t n_baby = (size_t)d->n_in * d->n1, n_ct = (size_t)d->n_out * d->n2;
   std::vector<const uint64_t*> baby(n_baby);
   std::vector<uint64_t*> cts(n_ct);
+  const size_t ext_words = (size_t)2 * diag_rows(c, *d) * c->n;
   bool ok = hipMalloc(&p->work, (n_baby + n_ct + d->n_out) * p->ct_words * 8) == hipSuccess &&
+            (!d->lazy_moddown ||
+             hipMalloc(&p->ext_work, (n_baby + n_ct) * ext_words * 8) == hipSuccess) &&
             (bank || hipMalloc(&p->d_diag, n_diag * sizeof(void*)) == hipSuccess) &&
             hipMalloc(&p->d_baby, n_baby * sizeof(void*)) == hipSuccess &&
             hipMalloc(&p->d_ct, n_ct * sizeof(void*)) == hipSuccess;
   if (ok) {
-    for (size_t t = 0; t < n_baby; ++t) baby[t] = p->work + t * p->ct_words;
-    for (size_t t = 0; t < n_ct; ++t) cts[t] = p->work + (n_baby + t) * p->ct_words;
+    // the pt-MAC's operands: the ciphertext regions, or the extended ones
+    for (size_t t = 0; t < n_baby; ++t)
+      baby[t] = d->lazy_moddown ? p->ext_work + t * ext_words : p->work + t * p->ct_words;
+    for (size_t t = 0; t < n_ct; ++t)
+      cts[t] = d->lazy_moddown ? p->ext_work + (n_baby + t) * ext_words
+                               : p->work + (n_baby + t) * p->ct_words;
     ok = (bank || hipMemcpy(p->d_diag, p->diag.data(), n_diag * sizeof(void*),
                             hipMemcpyHostToDevice) == hipSuccess) &&
          hipMemcpy(p->d_baby, baby.data(), n_baby * sizeof(void*), hipMemcpyHostToDevice) ==
@@ -257,6 +303,7 @@ int matvec_plan_create(Context* c, const fesc_matvec_desc* d, const uint64_t* co
     for (auto& e : p->ev)
       if (e) (void)hipEventDestroy(e);
     (void)hipFree(p->work);
+    (void)hipFree(p->ext_work);
     (void)hipFree(p->d_diag);
     (void)hipFree(p->d_baby);
     (void)hipFree(p->d_ct);
@@ -271,6 +318,7 @@ void matvec_plan_destroy(fesc_matvec_plan* p) {
   if (!p) return;
   (void)hipDeviceSynchronize();
   (void)hipFree(p->work);
+  (void)hipFree(p->ext_work);
   (void)hipFree(p->d_diag);
   (void)hipFree(p->d_baby);
   (void)hipFree(p->d_ct);
@@ -289,23 +337,35 @@ int ptct_matvec(Context* c, fesc_matvec_plan* p, const uint64_t* const* in,
   uint64_t* tmp = ct + (size_t)d.n_out * d.n2 * W;
   const size_t n = c->n;
   int err;
+  const bool lazy = d.lazy_moddown;
+  const uint32_t rows = diag_rows(c, d);
+  const size_t ext_words = (size_t)2 * rows * n;
+  const LevelTables* T = nullptr;
+  if (lazy && !(T = level_tables(c, level, &err))) return err;
   HIPCK(hipEventRecord(p->ev[0], s));
-  // baby steps: one ModUp per input, all (u, q) key switches batched
+  // baby steps: one ModUp per input, all (u, q) key switches batched; with
+  // double hoisting their outputs stay in the extended basis
   std::vector<KsSource> srcs;
   std::vector<KsJob> jobs;
   for (uint32_t u = 0; u < d.n_in; ++u) {
     for (uint32_t q = 0; q < d.n1; ++q) {
-      uint64_t* o = baby + ((size_t)u * d.n1 + q) * W;
+      const size_t t = (size_t)u * d.n1 + q;
+      uint64_t* o = lazy ? p->ext_work + t * ext_words : baby + t * W;
       const uint32_t g = galois_of_step(c, (int32_t)(((int64_t)q * d.unit) % (c->n / 2)));
       if (g == 1) {
-        HIPCK(hipMemcpyAsync(o, in[u], W * 8, hipMemcpyDeviceToDevice, s));
+        if (lazy)
+          hipLaunchKernelGGL(k_ext_identity, dim3(c->n / kThreads, rows, 2), dim3(kThreads), 0,
+                             s, in[u], o, c->n, level, rows, T->pmod, c->d_pk);
+        else
+          HIPCK(hipMemcpyAsync(o, in[u], W * 8, hipMemcpyDeviceToDevice, s));
+        HIPCK(hipGetLastError());
         continue;
       }
       jobs.push_back(KsJob{(uint32_t)srcs.size(), c->keys.at(g), g, in[u], 1u, g, nullptr, o});
     }
     srcs.push_back(KsSource{in[u] + n, 2 * n});
     if (srcs.size() == kMaxBatch || u + 1 == d.n_in) {
-      if ((err = key_switch_batch(c, level, srcs, jobs, s))) return err;
+      if ((err = key_switch_batch(c, level, srcs, jobs, s, 0, nullptr, lazy))) return err;
       srcs.clear();
       jobs.clear();
     }
@@ -313,16 +373,26 @@ int ptct_matvec(Context* c, fesc_matvec_plan* p, const uint64_t* const* in,
   HIPCK(hipEventRecord(p->ev[1], s));
   // pt-MAC over all (b, p)
   const uint32_t n_outputs = d.n_out * d.n2;
-  dim3 grid((c->n / kThreads) * level * ((n_outputs + kGroup - 1) / kGroup));
+  const PtLayout lay = lazy ? PtLayout{(uint32_t)n, rows * (uint32_t)n, level, c->L}
+                            : PtLayout{2 * (uint32_t)n, (uint32_t)n, level, c->L};
+  dim3 grid((c->n / kThreads) * rows * ((n_outputs + kGroup - 1) / kGroup));
   if (p->bank)
     hipLaunchKernelGGL((k_ptmac<kGroup, true>), grid, dim3(kThreads), 0, s, p->d_baby,
                        (const uint64_t* const*)nullptr, p->bank, p->d_ct, n_outputs,
-                       (uint32_t)n_baby, c->n, level, c->d_pk);
+                       (uint32_t)n_baby, c->n, rows, c->d_pk, lay);
   else
     hipLaunchKernelGGL((k_ptmac<kGroup, false>), grid, dim3(kThreads), 0, s, p->d_baby,
                        p->d_diag, (const uint64_t*)nullptr, p->d_ct, n_outputs,
-                       (uint32_t)n_baby, c->n, level, c->d_pk);
+                       (uint32_t)n_baby, c->n, rows, c->d_pk, lay);
   HIPCK(hipGetLastError());
+  if (lazy) {
+    // one ModDown per c~_{b,p}, into the ciphertext regions
+    std::vector<uint64_t*> cts(n_outputs);
+    for (uint32_t t = 0; t < n_outputs; ++t) cts[t] = ct + (size_t)t * W;
+    if ((err = op_moddown_many(c, n_outputs, p->ext_work + n_baby * ext_words, cts.data(), level,
+                               s)))
+      return err;
+  }
   HIPCK(hipEventRecord(p->ev[2], s));
   // giant steps: y_b += Phi^(p n1)(c~_{b,p}), one batch over b per p
   std::vector<const uint64_t*> gin(d.n_out);
@@ -393,7 +463,8 @@ int fesc_matvec_bank_words(const fesc_ctx* ctx, const fesc_matvec_desc* desc, si
   if (!ctx || !words) return fesc::fail(FESC_ERR_ARG, "null argument");
   int rc = fesc::check_desc(ctx, desc);
   if (rc) return rc;
-  *words = (size_t)desc->n_out * desc->n2 * desc->n_in * desc->n1 * desc->level * ctx->n;
+  *words = (size_t)desc->n_out * desc->n2 * desc->n_in * desc->n1 *
+           fesc::diag_rows(ctx, *desc) * ctx->n;
   return FESC_OK;
 }
 
@@ -405,7 +476,7 @@ int fesc_matvec_bank_pack(fesc_ctx* ctx, const fesc_matvec_desc* desc, uint64_t*
   const uint32_t terms = desc->n_in * desc->n1, outputs = desc->n_out * desc->n2;
   if ((uint64_t)index >= (uint64_t)terms * outputs)
     return fesc::fail(FESC_ERR_ARG, "diagonal index out of range");
-  hipLaunchKernelGGL(fesc::k_bank_pack, dim3(ctx->n / fesc::kThreads, desc->level),
+  hipLaunchKernelGGL(fesc::k_bank_pack, dim3(ctx->n / fesc::kThreads, fesc::diag_rows(ctx, *desc)),
                      dim3(fesc::kThreads), 0, reinterpret_cast<hipStream_t>(stream), pt, bank,
                      index / terms, index % terms, ctx->n, outputs, terms);
   return fesc::hip_check(hipGetLastError(), "bank_pack");

@@ -181,8 +181,9 @@ hipError_t ntt_rows(const Context* c, uint64_t* d, uint32_t batch, size_t batch_
 
 int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& srcs,
                      const std::vector<KsJob>& jobs, hipStream_t s, uint32_t rescale_rows,
-                     const Scratch* given) {
+                     const Scratch* given, bool ext_out) {
   if (jobs.empty()) return FESC_OK;
+  if (ext_out && rescale_rows) return fail(FESC_ERR_ARG, "extended outputs take no rescale");
   if (rescale_rows && (level < 2 || rescale_rows > level - 1))
     return fail(FESC_ERR_LEVEL, "merged rescale needs level >= 2 and rows <= level - 1");
   if (srcs.size() > kMaxBatch) return fail(FESC_ERR_ARG, "too many key-switch sources");
@@ -256,6 +257,14 @@ int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& sr
     for (uint32_t j = 0; j < nj && !t.fold; ++j)
       if (t.add_y[j]) return fail(FESC_ERR_ARG, "a tensor addend needs the folded combine");
     if (rescale_rows && !t.fold) return fail(FESC_ERR_ARG, "merged rescale needs folded addends");
+    if (ext_out) {
+      for (uint32_t j = 0; j < nj; ++j)
+        if (t.add_y[j]) return fail(FESC_ERR_ARG, "extended outputs take plain addends");
+      if (!t.fold) return fail(FESC_ERR_ARG, "extended outputs need addends under the job's element");
+      t.fold = 2;
+      HIPCK(k_ip_launch(c, t, nkeys, S.ext, S.acc, level, T->pmod, s));
+      continue;
+    }
     HIPCK(k_ip_launch(c, t, nkeys, S.ext, S.acc, level, T->md_pinv, s));
     if (rescale_rows) {
       // rows q_{level-1}, p_0 .. p_{alpha-1} (adjacent in acc): iNTT to the
@@ -275,6 +284,32 @@ int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& sr
     HIPCK(launch_ntt_inv_digits(c, rp, 2 * nj, c->alpha, T->md_inv_n, s));
     HIPCK(launch_moddown_outer(c, *T, S.acc, S.y, nj, level, s));
     HIPCK(launch_ntt_fwd_ks_combine(c, S.y, nj, level, level, level, t, S.acc, T->md_pinv,
+                                    nullptr, s));
+  }
+  return FESC_OK;
+}
+
+int op_moddown_many(Context* c, uint32_t count, uint64_t* ext, uint64_t* const* outs,
+                    uint32_t level, hipStream_t s) {
+  int err;
+  const LevelTables* T = level_tables(c, level, &err);
+  if (!T) return err;
+  Scratch S;
+  if ((err = scratch(c, &S, count))) return err;
+  const size_t n = c->n, E = level + c->alpha;
+  // the ciphertexts play the inner products' part (component-major rows
+  // over the extended basis): inverse transform of the special-prime rows to
+  // centred digits (in place), conversion to the level rows fused with the
+  // first forward pass, second pass with the combine (acc - y) P^-1
+  for (uint32_t j0 = 0; j0 < count; j0 += S.cap) {
+    const uint32_t nj = std::min(S.cap, count - j0);
+    uint64_t* acc = ext + (size_t)j0 * 2 * E * n;
+    KsTable t{};
+    for (uint32_t j = 0; j < nj; ++j) t.out[j] = outs[j0 + j];
+    const RowSel rp{acc + (size_t)level * n, E * n, n, c->L, c->alpha, 0, 0, 0, 0};
+    HIPCK(launch_ntt_inv_digits(c, rp, 2 * nj, c->alpha, T->md_inv_n, s));
+    HIPCK(launch_moddown_outer(c, *T, acc, S.y, nj, level, s));
+    HIPCK(launch_ntt_fwd_ks_combine(c, S.y, nj, level, level, level, t, acc, T->md_pinv,
                                     nullptr, s));
   }
   return FESC_OK;

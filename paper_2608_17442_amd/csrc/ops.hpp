@@ -100,7 +100,9 @@ struct KsTable {
   uint32_t kg_seeded;
   // 1 when every job's addend uses the job's own Galois element (or there is
   // none): the inner product then stores acc * P^-1 + add on the level rows
-  // and the combine only subtracts y * P^-1
+  // and the combine only subtracts y * P^-1; 2: extended-basis outputs (the
+  // inner product writes acc + P add into out[job], [2][level+alpha][N], and
+  // no ModDown follows)
   uint32_t fold;
 };
 
@@ -168,9 +170,17 @@ static_assert(sizeof(KsTable) < 3072, "key-switch table must stay a small kernel
 // given: use this scratch (its capacity and regions) instead of the
 // context's, so that nothing is allocated; null: the context's scratch.
 struct Scratch;
+// ext_out: the jobs' outputs stay in the extended basis (out = P sigma_g(add)
+// + acc over every row, [2][level+alpha][N]; addends must use the job's own
+// Galois element, plain only): double hoisting's baby steps.
 int key_switch_batch(Context* c, uint32_t level, const std::vector<KsSource>& srcs,
                      const std::vector<KsJob>& jobs, hipStream_t s, uint32_t rescale_rows = 0,
-                     const Scratch* given = nullptr);
+                     const Scratch* given = nullptr, bool ext_out = false);
+// ModDown of `count` extended-basis ciphertexts stored contiguously,
+// ext[count][2][level+alpha][N], into outs[i] ([level][2][N]); the special-
+// prime rows of ext are overwritten (they become the conversion's digits).
+int op_moddown_many(Context* c, uint32_t count, uint64_t* ext, uint64_t* const* outs,
+                    uint32_t level, hipStream_t s);
 
 int op_rotate_many(Context* c, const uint64_t* in, uint32_t count, const int32_t* steps,
                    uint64_t* const* outs, uint32_t level, hipStream_t s);

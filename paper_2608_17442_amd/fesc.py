@@ -82,6 +82,7 @@ _SIGS = {
     "fesc_post_ssm": [_vp, _vp, _vp, _vp, _vp, _vp, _u32, _vp],
     "fesc_add_plain": [_vp, _vp, _vp, _vp, _u32, _vp],
     "fesc_encode_plain": [_vp, _vp, _u32, ctypes.c_double, _vp, _u32, _vp],
+    "fesc_encode_plain_ext": [_vp, _vp, _u32, ctypes.c_double, _vp, _u32, _vp],
     "fesc_decode_plain": [_vp, _vp, _u32, _u32, ctypes.c_double, _vp, _vp],
     "fesc_c2m_level": [ctypes.POINTER(_u64), _u32, _u32, _u32, ctypes.c_double, ctypes.c_double,
                        ctypes.POINTER(_u32)],
@@ -426,6 +427,17 @@ class Context:
                                       _ptr(pt, count * self._pt(level), "pt"), level,
                                       _stream(stream)))
 
+    def encode_plain_ext(self, z, scale, pt, level, stream=None):
+        """Device encoding over the extended basis of `level` (q_0..q_{level-1},
+        p_0..p_{alpha-1}): pt [count][level+alpha][N]."""
+        zr = torch.view_as_real(z.reshape(-1, self.n // 2)).contiguous()
+        if not (zr.is_cuda and zr.dtype == torch.float64):
+            raise TypeError("z: a complex128 CUDA tensor")
+        count = zr.shape[0]
+        _check(_lib.fesc_encode_plain_ext(self._h, zr.data_ptr(), count, float(scale),
+                                          _ptr(pt, count * (level + self.alpha) * self.n, "pt"),
+                                          level, _stream(stream)))
+
     def decode_plain(self, pt, count, level, scale, z, stream=None):
         """Device decoding: evaluation-form plaintexts pt (int64 tensor,
         [count][level][N]) -> slot vectors z (complex128 CUDA tensor,
@@ -500,7 +512,8 @@ def encode(log_n: int, z, scale: float):
 
 class _MatvecDesc(ctypes.Structure):
     _fields_ = [(f, _u32) for f in ("level", "n_in", "n_out", "n1", "n2", "unit",
-                                    "real_extract", "rescale", "complex_pair")]
+                                    "real_extract", "rescale", "complex_pair",
+                                    "lazy_moddown")]
 
 
 _lib.fesc_matvec_plan_create.argtypes = [_vp, ctypes.POINTER(_MatvecDesc), ctypes.POINTER(_vp),
@@ -525,9 +538,15 @@ _lib.fesc_matvec_plan_create_bank.restype = ctypes.c_int
 
 
 def matvec_desc(level, n_in, n_out, n1, n2, unit, real_extract, rescale,
-                complex_pair=False) -> _MatvecDesc:
+                complex_pair=False, lazy_moddown=False) -> _MatvecDesc:
     return _MatvecDesc(level, n_in, n_out, n1, n2, unit, int(real_extract), int(rescale),
-                       int(complex_pair))
+                       int(complex_pair), int(lazy_moddown))
+
+
+def _diag_words(ctx, desc) -> int:
+    """Words of one diagonal plaintext (over the extended basis with
+    lazy_moddown)."""
+    return (desc.level + (ctx.alpha if desc.lazy_moddown else 0)) * ctx.n
 
 
 _lib.fesc_bsgs_diagonal_slots.argtypes = [_vp, ctypes.POINTER(_MatvecDesc), _vp, _u32, _u32,
@@ -562,7 +581,7 @@ def matvec_bank_words(ctx: Context, desc: _MatvecDesc) -> int:
 def matvec_bank_pack(ctx: Context, desc: _MatvecDesc, bank, index: int, pt, stream=None):
     _check(_lib.fesc_matvec_bank_pack(ctx._h, ctypes.byref(desc),
                                       _ptr(bank, matvec_bank_words(ctx, desc), "bank"), index,
-                                      _ptr(pt, ctx._pt(desc.level), "pt"), _stream(stream)))
+                                      _ptr(pt, _diag_words(ctx, desc), "pt"), _stream(stream)))
 
 
 class MatvecPlan:
@@ -571,10 +590,10 @@ class MatvecPlan:
     tiled device buffer (see fesc_matvec_bank_pack).  Inputs are kept alive."""
 
     def __init__(self, ctx: Context, level, n_in, n_out, n1, n2, unit, real_extract, rescale,
-                 diags=None, bank=None, complex_pair=False):
+                 diags=None, bank=None, complex_pair=False, lazy_moddown=False):
         self.ctx = ctx
         self.desc = matvec_desc(level, n_in, n_out, n1, n2, unit, real_extract, rescale,
-                                complex_pair)
+                                complex_pair, lazy_moddown)
         h = _vp()
         if bank is not None:
             self._bank = bank
@@ -583,7 +602,8 @@ class MatvecPlan:
                 _ptr(bank, matvec_bank_words(ctx, self.desc), "bank"), ctypes.byref(h)))
         else:
             self._diags = list(diags)
-            arr = _ptrs(self._diags, n_out * n2 * n_in * n1, ctx._pt(level), "diags")
+            arr = _ptrs(self._diags, n_out * n2 * n_in * n1, _diag_words(ctx, self.desc),
+                        "diags")
             _check(_lib.fesc_matvec_plan_create(ctx._h, ctypes.byref(self.desc), arr,
                                                 ctypes.byref(h)))
         self._h = h
