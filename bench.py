@@ -543,6 +543,92 @@ def modmul_probe(ctx, F) -> dict:
                        "(fesc_calib_valu)"}
 
 
+def matvec_double_hoisting(F, torch, np) -> dict:
+    """The projection with and without double hoisting (lazy ModDown), timed
+    on the diagonal-method workload (N = 2^12, 64 x 64, 63 hoisted rotations)
+    and on the 768 x 1536 shape (N = 2^16, 16 limbs, complex-paired outputs,
+    tiled bank).  The modular arithmetic does not depend on the values, so
+    diagonals and inputs are uniform residues; the two 2^16 banks (154.6 and
+    231.9 GB) are built one after the other."""
+    import synth
+    import synth.workloads as WL
+
+    def timed(plan, ins, outs, reps):
+        plan(ins, outs)
+        torch.cuda.synchronize()
+        ts, ph = [], []
+        for _ in range(reps):
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            ev[0].record()
+            plan(ins, outs)
+            ev[1].record()
+            torch.cuda.synchronize()
+            ts.append(ev[0].elapsed_time(ev[1]))
+            ph.append(plan.phase_ms())
+        med = lambda v: round(float(np.median(v)), 3)
+        return {"ms": med(ts), "baby_ms": med([x[0] for x in ph]),
+                "pt_mac_ms": med([x[1] for x in ph]), "tail_ms": med([x[2] for x in ph])}
+
+    out = {}
+    # diagonal method, N = 2^12
+    pr = F.find_primes(12, 36, 4)
+    q, p = pr[1:4], pr[0:1]
+    n = 1 << 12
+    ctx = F.Context(12, q, p)
+    sd = torch.from_numpy(synth.secret(0, n)).cuda()
+    for r in range(1, 64):
+        g = ctx.galois_element(r)
+        w, e = synth.switch_key_seed_draws(0, q + p, n, 3, g)
+        ctx.keygen_seeded(g, sd, w, torch.from_numpy(e).cuda())
+    ins = [torch.randint(0, 1 << 35, (3 * 2 * n,), dtype=torch.int64, device="cuda")]
+    outs = [torch.empty(2 * 2 * n, dtype=torch.int64, device="cuda")]
+    res = {}
+    for lazy in (False, True):
+        diags = [torch.randint(0, 1 << 35, ((3 + int(lazy)) * n,), dtype=torch.int64,
+                               device="cuda") for _ in range(64)]
+        plan = F.MatvecPlan(ctx, 3, 1, 1, 64, 1, 1, False, True, diags=diags,
+                            lazy_moddown=lazy)
+        res["double_hoisted" if lazy else "plain"] = timed(plan, ins, outs, 20)
+        plan.close()
+    out["n4096_64x64_diagonal_method"] = res
+    del ctx
+    # 768 x 1536, N = 2^16
+    pr = F.find_primes(16, 50, 32)
+    q, p = pr[8:], pr[:8]
+    n = 1 << 16
+    ctx = F.Context(16, q, p)
+    cfg = WL.CFG4
+    level, seg, n1, n2 = cfg["level"], cfg["tokens"], cfg["n1"], cfg["n2"]
+    Cc = (n // 2) // seg
+    n_in, n_out = cfg["d_in"] // Cc // 2, cfg["d_out"] // Cc
+    sd = torch.from_numpy(synth.secret(3, n)).cuda()
+    steps = [k * seg for k in range(1, n1)] + [k * n1 * seg for k in range(1, n2)]
+    for g in sorted({ctx.galois_element(st) for st in steps} | {2 * n - 1}):
+        w, e = synth.switch_key_seed_draws(3, q + p, n, 3, g)
+        ctx.keygen_seeded(g, sd, w, torch.from_numpy(e).cuda())
+    ins = [torch.randint(0, 1 << 49, (level * 2 * n,), dtype=torch.int64, device="cuda")
+           for _ in range(n_in)]
+    outs = [torch.empty((level - 1) * 2 * n, dtype=torch.int64, device="cuda")
+            for _ in range(n_out // 2)]
+    res = {}
+    for lazy in (False, True):
+        desc = F.matvec_desc(level, n_in, n_out, n1, n2, seg, False, True, True, lazy)
+        words = F.matvec_bank_words(ctx, desc)
+        bank = torch.empty(words, dtype=torch.int64, device="cuda")
+        for o in range(0, words, 1 << 30):
+            bank[o:o + (1 << 30)].random_(0, 1 << 49)
+        plan = F.MatvecPlan(ctx, level, n_in, n_out, n1, n2, seg, False, True, bank=bank,
+                            complex_pair=True, lazy_moddown=lazy)
+        r = timed(plan, ins, outs, 5)
+        r["bank_gb"] = round(words * 8 / 1e9, 1)
+        res["double_hoisted" if lazy else "plain"] = r
+        plan.close()
+        del plan, bank
+        torch.cuda.empty_cache()
+    out["n65536_768x1536_complex_paired"] = res
+    return out
+
+
 def keyswitch_per_kernel():
     f = profiled_fields(KS_PROFILE, KS_SOURCES)
     if f is None or "keyswitch_bound_fraction" not in f:
@@ -867,6 +953,9 @@ def main():
     ap.add_argument("--cpu-sample", choices=("all", "single"),
                     help="(internal) time the oracle's bounded samples in this process and "
                          "print them as JSON; no GPU is used")
+    ap.add_argument("--matvec-double-hoisting", action="store_true",
+                    help="only the projection with and without double hoisting (lazy "
+                         "ModDown), at N = 2^12 (64 x 64) and at the 768 x 1536 shape")
     ap.add_argument("--stored-keys", action="store_true",
                     help="switching keys stored whole (both halves read by every key switch) "
                          "instead of seed-expanded")
@@ -894,6 +983,10 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if args.matvec_double_hoisting:
+        print(json.dumps({"matvec_double_hoisting": matvec_double_hoisting(F, torch, np)}),
+              flush=True)
+        return
     if args.calibrate_only:
         pr = F.find_primes(16, 50, 32)
         ctx = F.Context(16, pr[8:], pr[:8])
