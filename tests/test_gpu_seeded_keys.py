@@ -256,3 +256,35 @@ def test_seeded_keys_full_size_rotation_set():
         got = C.decrypt(P, S.sk, want, 2.0 ** 40)
         err = np.max(np.abs(got - np.roll(WL.cfg3_slots(i, P.n // 2), -r)))
         assert err < 2.0 ** -15, f"item {i}: decoded error {err:.3e}"
+
+
+def test_thirty_two_distinct_keys_in_one_group():
+    """32 rotations by 32 different steps in one launch group: 32 key groups,
+    so the seeded-group mask uses every bit (the last group included);
+    seeded and stored keys alternate."""
+    P = _chain((12, 50, 3, 3))
+    steps = list(range(1, 33))
+    elts = [P.galois_elt(r) for r in steps]
+    S = SeededSetup(P, 26, elts, stored=set(elts[::2]))
+    level = P.L
+    cts = [S.encrypt(_z(800 + i, P.n // 2), 2.0 ** 30, level, 800 + i) for i in range(32)]
+    outs = [torch.zeros_like(cts[0][1]) for _ in range(32)]
+    step("rotate_batch of 32 distinct keys (mixed)")
+    S.ctx.rotate_batch([d for _, d in cts], steps, outs, level)
+    for i, ((co, _), r, o) in enumerate(zip(cts, steps, outs)):
+        _eq(o, C.rotate(P, co, r, S.keys), f"item {i} step {r}")
+
+
+def test_seeded_relinearisation_with_merged_rescale():
+    """fesc_mul_relin_rescale (ModDown merged with the rescale, the scan's
+    product) with a seed-expanded relinearisation key, against the oracle's
+    mul_relin_rescale, at the top level and at level 2."""
+    P = _chain((12, 50, 5, 2))
+    S = SeededSetup(P, 27, [0])
+    for level in (P.L, 2):
+        ao, ad = S.encrypt(_z(850 + level, P.n // 2), 2.0 ** 30, level, 850 + level)
+        bo, bd = S.encrypt(_z(860 + level, P.n // 2), 2.0 ** 30, level, 860 + level)
+        out = torch.zeros((level - 1) * 2 * P.n, dtype=torch.int64, device="cuda")
+        step(f"mul_relin_rescale seeded level={level}")
+        S.ctx.mul_relin_rescale([ad], [bd], [out], level)
+        _eq(out, C.mul_relin_rescale(P, ao, bo, S.keys[0]), f"mul_relin_rescale level={level}")

@@ -1,9 +1,9 @@
 """The rotation batch that allocates nothing (fesc_rotate_batch_noalloc)
 against the batch that uses the context's scratch (fesc_rotate_batch): equal
 residue for residue on two calls in a row, the second with a smaller input,
-on a small ring (one group of up to 32 rotations) and at N = 2^16 with 24
-limbs (two rotations per group of the 256 MiB static array), and the oracle
-confirms one output.  A level whose single rotation exceeds the array is
+on a small ring (one group of up to 32 rotations), with seed-expanded keys,
+and at N = 2^16 with 24 limbs (two rotations per group of the 256 MiB static
+array), and the oracle confirms one output.  A level whose single rotation exceeds the array is
 refused before any launch."""
 import numpy as np
 import pytest
@@ -69,6 +69,25 @@ def test_rotate_batch_noalloc_full_size_two_calls():
     assert np.array_equal(got, want), first_mismatch(got, want)
     cts2 = [S.encrypt(_z(800 + i, P.n // 2), 2.0 ** 40, 16, 800 + i) for i in range(2)]
     _both(S, [d for _, d in cts2], [32, 1], 16, "full size call 2")
+
+
+def test_rotate_batch_noalloc_with_seed_expanded_keys():
+    """The same comparison with seed-expanded keys (the inner product
+    regenerates each key's uniform half in the static scratch's key
+    switches as well), two calls, the oracle confirming one output."""
+    from tests.test_gpu_seeded_keys import SeededSetup
+    P = C.params_small(12, 50, 5, 2)
+    base = [1, 3, -2]
+    S = SeededSetup(P, 20, [P.galois_elt(r) for r in base])
+    level = P.L
+    cts = [S.encrypt(_z(900 + i, P.n // 2), 2.0 ** 30, level, 900 + i) for i in range(6)]
+    steps = [base[i % len(base)] for i in range(6)]
+    outs = _both(S, [d for _, d in cts], steps, level, "seeded call 1")
+    want = C.rotate(P, cts[4][0], steps[4], S.keys)
+    got = to_host(outs[4]).reshape(want.shape)
+    assert np.array_equal(got, want), first_mismatch(got, want)
+    cts2 = [S.encrypt(_z(950 + i, P.n // 2), 2.0 ** 30, 3, 950 + i) for i in range(2)]
+    _both(S, [d for _, d in cts2], [3, -2], 3, "seeded call 2")
 
 
 def test_rotate_batch_noalloc_refuses_a_level_beyond_the_array():
