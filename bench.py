@@ -992,7 +992,10 @@ def main():
         ctx = F.Context(16, pr[8:], pr[:8])
         out = {"valu_peaks_per_s": {k: round(ctx.calib_valu(v), -9) for k, v in (
             ("ct_butterflies", F.CALIB_CT), ("gs_butterflies", F.CALIB_GS),
-            ("mod_macs", F.CALIB_MAC))}, "modmul_probe": modmul_probe(ctx, F)}
+            ("mod_macs", F.CALIB_MAC))}, "modmul_probe": modmul_probe(ctx, F),
+            "hbm_measured_ceilings_gbs": {
+                "read": round(ctx.calib_hbm(F.CALIB_HBM_READ) / 1e9, 1),
+                "copy": round(ctx.calib_hbm(F.CALIB_HBM_COPY) / 1e9, 1)}}
         print(json.dumps(out), flush=True)
         return
     if args.hescan_sweep:
@@ -1016,6 +1019,9 @@ def main():
         return
     W = Workloads(F, torch, np, seeded_keys=not args.stored_keys)
     torch.cuda.synchronize()
+    # the device's practical streaming ceilings (8 GiB read; 8 GiB copied)
+    hbm = {"read_gbs": round(W.ctx.calib_hbm(F.CALIB_HBM_READ) / 1e9, 1),
+           "copy_gbs": round(W.ctx.calib_hbm(F.CALIB_HBM_COPY) / 1e9, 1)}
     # register-resident arithmetic peaks of this device (VALU roof)
     peak = {k: W.ctx.calib_valu(v) for k, v in (("ct", F.CALIB_CT), ("gs", F.CALIB_GS),
                                                  ("mac", F.CALIB_MAC))}
@@ -1171,9 +1177,14 @@ def main():
             "frac": round(ptmac_gbs / HBM_PEAK_GBS, 4),
             "traffic": profiled_traffic(PTMAC_PROFILE, PTMAC_SOURCES),
             "algorithmic_bytes": ptmac_bytes,
+            "frac_of_measured_read_ceiling": round(ptmac_gbs / hbm["read_gbs"], 4),
         },
         "targets": targets,
         "rooflines_other": {
+            "hbm_measured_ceilings": dict(hbm, note="fesc_calib_hbm: a streaming read with "
+                                          "16-byte loads and a 16-byte copy (read + write), "
+                                          "8 GiB each; the practical ceilings of HBM-bound "
+                                          "kernels on this device, against the 8 TB/s peak"),
             "ntt_valu": {"bound": "alu",
                          "achieved": round(2 * ntt_bfly / ((fwd + inv) * 1e-3) / 1e12, 4),
                          "peak": round(2 / (1 / peak["ct"] + 1 / peak["gs"]) / 1e12, 4),

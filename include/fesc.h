@@ -604,6 +604,18 @@ int fesc_encode(uint32_t log_n, const double* re, const double* im, double scale
 #define FESC_CALIB_PHILOX 5
 int fesc_calib_valu(fesc_ctx* ctx, int kind, uint32_t iters, double* rate, void* stream);
 
+/* Measurement helper, not part of the method: the device's practical HBM
+ * ceilings for streaming kernels.  kind FESC_CALIB_HBM_READ: every 16-byte
+ * word of a `bytes` buffer read once; FESC_CALIB_HBM_COPY: a `bytes` buffer
+ * copied (read plus write).  *rate = bytes moved per second (2 * bytes per
+ * copy).  Allocates and frees its buffers (bytes, and bytes or a small
+ * output) and synchronises `stream`; FESC_ERR_ARG for an unknown kind or a
+ * size outside 1 MiB .. 64 GiB or not a multiple of 16, FESC_ERR_OOM if the
+ * buffers do not fit. */
+#define FESC_CALIB_HBM_READ 0
+#define FESC_CALIB_HBM_COPY 1
+int fesc_calib_hbm(fesc_ctx* ctx, int kind, size_t bytes, double* rate, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

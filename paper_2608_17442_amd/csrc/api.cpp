@@ -108,6 +108,7 @@ int op_scan_contract(Context* c, const uint64_t* const* h, const uint64_t* const
                      uint64_t* const* out, uint32_t level, hipStream_t s);
 int encode(uint32_t log_n, const double* re, const double* im, double scale, int64_t* out);
 int calib_valu(Context* c, int kind, uint32_t iters, double* rate, hipStream_t s);
+int calib_hbm(Context* c, int kind, size_t bytes, double* rate, hipStream_t s);
 int op_heconv(Context* c, const uint64_t* q, uint32_t taps, const int32_t* deltas,
               const uint64_t* const* masks, const uint64_t* bias, uint64_t* out, uint32_t level,
               hipStream_t s);
@@ -619,6 +620,11 @@ int fesc_c2m_level(const uint64_t* q, uint32_t level, uint32_t ell, uint32_t sig
 int fesc_calib_valu(fesc_ctx* ctx, int kind, uint32_t iters, double* rate, void* stream) {
   if (!ctx || !rate) return fail(FESC_ERR_ARG, "null argument");
   return calib_valu(ctx, kind, iters, rate, S(stream));
+}
+
+int fesc_calib_hbm(fesc_ctx* ctx, int kind, size_t bytes, double* rate, void* stream) {
+  if (!ctx || !rate) return fail(FESC_ERR_ARG, "null argument");
+  return calib_hbm(ctx, kind, bytes, rate, S(stream));
 }
 
 }  // extern "C"

@@ -135,7 +135,80 @@ __global__ __launch_bounds__(kThreads) void k_calib_philox(uint64_t k0, uint64_t
   out[t] = (double)((x[0] ^ x[1] ^ x[2] ^ x[3] ^ y[0] ^ y[1] ^ y[2] ^ y[3]) & 0xFFFFFFFFull);
 }
 
+// Streaming HBM ceilings: every 16-byte word of `src` read once (grid-
+// stride; an XOR per thread keeps the loads live), or copied to `dst`.
+__global__ __launch_bounds__(kThreads) void k_calib_read(const ulonglong2* __restrict__ src,
+                                                         size_t words2, uint64_t* __restrict__ out) {
+  const size_t t = (size_t)blockIdx.x * kThreads + threadIdx.x, nt = (size_t)gridDim.x * kThreads;
+  uint64_t x = 0;
+  for (size_t i = t; i < words2; i += nt) {
+    const ulonglong2 v = src[i];
+    x ^= v.x ^ v.y;
+  }
+  out[t] = x;
+}
+
+__global__ __launch_bounds__(kThreads) void k_calib_copy(const ulonglong2* __restrict__ src,
+                                                         ulonglong2* __restrict__ dst,
+                                                         size_t words2) {
+  const size_t t = (size_t)blockIdx.x * kThreads + threadIdx.x, nt = (size_t)gridDim.x * kThreads;
+  for (size_t i = t; i < words2; i += nt) dst[i] = src[i];
+}
+
 }  // namespace
+
+int calib_hbm(Context* c, int kind, size_t bytes, double* rate, hipStream_t s) {
+  if ((kind != FESC_CALIB_HBM_READ && kind != FESC_CALIB_HBM_COPY) || bytes < ((size_t)1 << 20) ||
+      bytes > ((size_t)64 << 30) || bytes % 16)
+    return fail(FESC_ERR_ARG, "bad HBM calibration arguments");
+  int cus = 0;
+  if (int rc = hip_check(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount,
+                                               c->device), "hipDeviceGetAttribute"))
+    return rc;
+  // grids from a sweep on MI355X: 8 workgroups per CU for reads, 64 for copies
+  const uint32_t blocks = (uint32_t)cus * (kind == FESC_CALIB_HBM_READ ? 8 : 64);
+  void *src = nullptr, *dst = nullptr;
+  const size_t out_bytes = (size_t)blocks * kThreads * 8;
+  if (hipMalloc(&src, bytes) != hipSuccess ||
+      hipMalloc(&dst, kind == FESC_CALIB_HBM_COPY ? bytes : out_bytes) != hipSuccess) {
+    (void)hipFree(src);
+    return fail(FESC_ERR_OOM, "HBM calibration buffers");
+  }
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  int rc = hip_check(hipMemsetAsync(src, 1, bytes, s), "hipMemsetAsync");
+  if (!rc) rc = hip_check(hipEventCreate(&e0), "hipEventCreate");
+  if (!rc) rc = hip_check(hipEventCreate(&e1), "hipEventCreate");
+  const size_t w2 = bytes / 16;
+  auto launch = [&]() {
+    if (kind == FESC_CALIB_HBM_READ)
+      hipLaunchKernelGGL(k_calib_read, dim3(blocks), dim3(kThreads), 0, s,
+                         static_cast<const ulonglong2*>(src), w2, static_cast<uint64_t*>(dst));
+    else
+      hipLaunchKernelGGL(k_calib_copy, dim3(blocks), dim3(kThreads), 0, s,
+                         static_cast<const ulonglong2*>(src), static_cast<ulonglong2*>(dst), w2);
+  };
+  float ms = 0.f;
+  if (!rc) {
+    launch();  // warm-up
+    rc = hip_check(hipGetLastError(), "HBM calibration launch");
+  }
+  if (!rc) rc = hip_check(hipEventRecord(e0, s), "hipEventRecord");
+  if (!rc) {
+    launch();
+    rc = hip_check(hipGetLastError(), "HBM calibration launch");
+  }
+  if (!rc) rc = hip_check(hipEventRecord(e1, s), "hipEventRecord");
+  if (!rc) rc = hip_check(hipEventSynchronize(e1), "hipEventSynchronize");
+  if (!rc) rc = hip_check(hipEventElapsedTime(&ms, e0, e1), "hipEventElapsedTime");
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  (void)hipStreamSynchronize(s);
+  (void)hipFree(src);
+  (void)hipFree(dst);
+  if (rc) return rc;
+  *rate = (double)bytes * (kind == FESC_CALIB_HBM_COPY ? 2.0 : 1.0) / (ms * 1e-3);
+  return FESC_OK;
+}
 
 int calib_valu(Context* c, int kind, uint32_t iters, double* rate, hipStream_t s) {
   if (kind < FESC_CALIB_CT || kind > FESC_CALIB_PHILOX || iters == 0 || iters > (1u << 20))

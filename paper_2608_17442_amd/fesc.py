@@ -92,12 +92,16 @@ _SIGS = {
 
 CONJ = -(2 ** 31)
 CALIB_CT, CALIB_GS, CALIB_MAC, CALIB_MODMUL_F64, CALIB_MODMUL_U64, CALIB_PHILOX = 0, 1, 2, 3, 4, 5
+CALIB_HBM_READ, CALIB_HBM_COPY = 0, 1
 SCAN_STATES_ONLY = 1
 
 for _name, _args in _SIGS.items():
     _f = getattr(_lib, _name)
     _f.argtypes = _args
     _f.restype = ctypes.c_int
+_lib.fesc_calib_hbm.argtypes = [_vp, ctypes.c_int, ctypes.c_size_t, ctypes.POINTER(ctypes.c_double),
+                               _vp]
+_lib.fesc_calib_hbm.restype = ctypes.c_int
 _lib.fesc_ctx_destroy.restype = None
 _lib.fesc_last_error.restype = ctypes.c_char_p
 
@@ -451,6 +455,14 @@ class Context:
 
     def key_words(self) -> int:
         return self.dnum * (self.L + self.alpha) * 2 * self.n
+
+    def calib_hbm(self, kind: int, nbytes: int = 8 << 30, stream=None) -> float:
+        """Measured streaming HBM rate (bytes/s): CALIB_HBM_READ or
+        CALIB_HBM_COPY (read plus write) over an nbytes buffer."""
+        r = ctypes.c_double()
+        _check(_lib.fesc_calib_hbm(self._h, kind, ctypes.c_size_t(nbytes), ctypes.byref(r),
+                                   _stream(stream)))
+        return float(r.value)
 
     def calib_valu(self, kind: int, iters: int = 4096, stream=None) -> float:
         """Measured register-resident rate (operations/s) of NTT butterflies

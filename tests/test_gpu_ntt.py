@@ -215,3 +215,11 @@ def test_calib_valu_rates_are_positive_and_ordered():
     assert r[F.CALIB_PHILOX] < r[F.CALIB_MODMUL_F64] / 4
     with pytest.raises(F.FescError):
         ctx.calib_valu(7, 16)
+    # streaming HBM ceilings: below the 8 TB/s peak, well above a slow path
+    for kind in (F.CALIB_HBM_READ, F.CALIB_HBM_COPY):
+        v = ctx.calib_hbm(kind, 1 << 30)
+        assert 1e12 < v < 8.1e12, (kind, v)
+    with pytest.raises(F.FescError):
+        ctx.calib_hbm(2, 1 << 30)
+    with pytest.raises(F.FescError):
+        ctx.calib_hbm(F.CALIB_HBM_READ, (1 << 30) + 8)
