@@ -22,29 +22,39 @@ form G contiguous groups of H / G, g(h) = floor(h G / H) (0-based), as in
 Mamba-2's grouped heads.
 
 Homomorphic realisation (the paper gives the maps, not their CKKS form; this
-is the reading the library implements).  A broadcast is one *slot map*
+is the reading the library implements).  A broadcast is one *slot map* over
+terms t = p n1 + q < n (q < n1 baby index, p giant index):
 
-    y[j]   = v[j + r0 + t d]     for j in run_t = [j0 + t J, j0 + t J + w), t < n,
-    y[j]   = 0                   elsewhere,
+    y[j]   = v[j + r0 + q d + p g]   for j in run_t = [j0 + q J + p Jg, ... + w),
+    y[j]   = 0                       elsewhere,
     out[j] = sum_{u < R} y[j - u S]
 
-(indices mod n_slots; R a power of two), evaluated in three steps:
+(indices mod n_slots; runs disjoint; R a power of two), evaluated in three
+steps:
     1. rho(v; r0), one key switch (a copy when r0 = 0 mod n_slots);
-    2. the diagonal method sum_t M_t (.) rho(.; t d) with M_t = 1 on run_t,
-       split baby-step/giant-step over t = p n1 + q (baby steps rho(.; q d)
-       hoisted, giant steps rho(.; p n1 d), each mask rotated by -p n1 d
-       before encoding), the masks encoded at the scale of q_{l-1} and the
-       sum rescaled once (level l -> l - 1);
+    2. the diagonal method sum_t M_t (.) rho(.; q d + p g), M_t = 1 on run_t,
+       baby-step/giant-step: the baby steps rho(.; q d) share one ModUp, the
+       giant steps are rho(.; p g), each mask is rotated by -p g before
+       encoding; the masks are encoded at the scale of q_{l-1} and the sum is
+       rescaled once (level l -> l - 1);
     3. log2 R doublings out <- out + rho(out; -2^s S).
-Per factor (c channels per chunk, Eg = P H / G channels per group):
-    x:  r0 = k E + kappa c, d = 1 - d_s, n = c, run_t = {t d_s}, R = d_s, S = 1;
-    a:  r0 = k H + kappa c / P, d = 1 - P d_s, n = c / P, run_t = {t P d_s},
-        R = P d_s, S = 1 (P divides c);
-    B, C, chunk inside group g: r0 = k G d_s + g d_s, n = 1, run_0 = [0, d_s),
+Replication by doubling adds the key-switching noise of every slot of R
+shifted copies, so the error of an output slot grows as sqrt(R); the decay's
+broadcast, whose natural replication is the P d_s slots of a head, places
+each head at P d_s / R_a positions and replicates R_a = min(P d_s, 512)
+times (512 keeps the decoded error below 2^-15 at N = 2^16 and scale 2^40:
+about 8e-6 was measured at R = 128 and 4e-5 at R = 8192).
+Per factor (c channels per chunk, Eg = P H / G channels per group, n1 the
+smallest power of two whose square reaches n unless stated, g = n1 d and
+Jg = n1 J unless stated):
+    x:  r0 = k E + kappa c, d = 1 - d_s, n = c, J = d_s, w = 1, R = d_s, S = 1;
+    a:  r0 = k H + kappa c / P, n1 = P d_s / R_a positions per head (d = -R_a,
+        J = R_a), n2 = c / P heads (g = 1 - P d_s, Jg = P d_s), w = 1, R = R_a,
+        S = 1 (P divides c);
+    B, C, chunk inside group g0: r0 = k G d_s + g0 d_s, n = 1, run_0 = [0, d_s),
         R = c, S = d_s;
     B, C, chunk over whole groups g0, g0 + 1, ...: r0 = k G d_s + g0 d_s,
-        d = d_s - Eg d_s, n = c / Eg, run_t = [t Eg d_s, t Eg d_s + d_s),
-        R = Eg, S = d_s.
+        d = d_s - Eg d_s, n = c / Eg, J = Eg d_s, w = d_s, R = Eg, S = d_s.
 """
 from __future__ import annotations
 
@@ -53,7 +63,6 @@ from dataclasses import dataclass
 import numpy as np
 
 from . import ckks as C
-from . import workloads as OW
 
 KINDS = ("a", "x", "B", "C")
 
@@ -149,11 +158,13 @@ def sigma(D: Dims, u: np.ndarray, kappa: int) -> np.ndarray:
 class SlotMap:
     level: int
     r0: int
-    d: int
-    n: int
-    n1: int
+    d: int       # rotation per baby step
+    n: int       # terms
+    n1: int      # baby steps
+    g: int       # rotation per giant step
     j0: int
-    J: int
+    J: int       # run offset per baby step
+    Jg: int      # run offset per giant step
     w: int
     R: int
     S: int
@@ -161,6 +172,13 @@ class SlotMap:
     @property
     def n2(self) -> int:
         return -(-self.n // self.n1)
+
+    def terms(self):
+        """(p, q) of every term t = p n1 + q < n."""
+        return [divmod(t, self.n1) for t in range(self.n)]
+
+
+R_MAX_DECAY = 512
 
 
 def _pow2(x: int) -> bool:
@@ -175,6 +193,11 @@ def _baby(n: int) -> int:
     return n1
 
 
+def _progression(level, r0, d, n, J, w, R, S) -> SlotMap:
+    n1 = _baby(n)
+    return SlotMap(level, r0, d, n, n1, n1 * d, 0, J, n1 * J, w, R, S)
+
+
 def br_slot_map(D: Dims, kind: str, k: int, kappa: int, level: int) -> SlotMap:
     """The slot map that realises br^(kappa) of token k's factor (module
     docstring); ValueError where the reading does not cover the shape."""
@@ -184,14 +207,15 @@ def br_slot_map(D: Dims, kind: str, k: int, kappa: int, level: int) -> SlotMap:
     if kind == "x":
         if not _pow2(D.d_s) or (k + 1) * D.E > D.n_slots:
             raise ValueError("x")
-        return SlotMap(level, k * D.E + kappa * c, 1 - D.d_s, c, _baby(c), 0, D.d_s, 1,
-                       D.d_s, 1)
+        return _progression(level, k * D.E + kappa * c, 1 - D.d_s, c, D.d_s, 1, D.d_s, 1)
     if kind == "a":
         if c % D.P or not _pow2(D.P * D.d_s) or (k + 1) * D.H > D.n_slots:
             raise ValueError("a")
-        n = c // D.P
-        return SlotMap(level, k * D.H + kappa * n, 1 - D.P * D.d_s, n, _baby(n), 0,
-                       D.P * D.d_s, 1, D.P * D.d_s, 1)
+        heads, span = c // D.P, D.P * D.d_s
+        R = min(span, R_MAX_DECAY)
+        pos = span // R
+        return SlotMap(level, k * D.H + kappa * heads, -R, heads * pos, pos, 1 - span, 0, R,
+                       span, 1, R, 1)
     if kind not in ("B", "C") or D.H % D.G or (k + 1) * D.G * D.d_s > D.n_slots:
         raise ValueError("B/C")
     Eg = D.P * D.H // D.G
@@ -199,22 +223,25 @@ def br_slot_map(D: Dims, kind: str, k: int, kappa: int, level: int) -> SlotMap:
     if lo == hi:
         if not _pow2(c):
             raise ValueError("B/C")
-        return SlotMap(level, k * D.G * D.d_s + lo * D.d_s, 0, 1, 1, 0, 0, D.d_s, c, D.d_s)
+        return _progression(level, k * D.G * D.d_s + lo * D.d_s, 0, 1, 0, D.d_s, c, D.d_s)
     if c % Eg or not _pow2(Eg):
         raise ValueError("B/C")
-    n = c // Eg
-    return SlotMap(level, k * D.G * D.d_s + lo * D.d_s, D.d_s - Eg * D.d_s, n, _baby(n), 0,
-                   Eg * D.d_s, D.d_s, Eg, D.d_s)
+    return _progression(level, k * D.G * D.d_s + lo * D.d_s, D.d_s - Eg * D.d_s, c // Eg,
+                        Eg * D.d_s, D.d_s, Eg, D.d_s)
+
+
+def _run_start(M: SlotMap, p: int, q: int) -> int:
+    return M.j0 + q * M.J + p * M.Jg
 
 
 def slot_map_plain(M: SlotMap, v: np.ndarray) -> np.ndarray:
     """The slot map's action on a plain slot vector (the definition above)."""
     ns = len(v)
     y = np.zeros(ns, np.complex128)
-    for t in range(M.n):
+    for p, q in M.terms():
         for o in range(M.w):
-            j = (M.j0 + t * M.J + o) % ns
-            y[j] = v[(j + M.r0 + t * M.d) % ns]
+            j = (_run_start(M, p, q) + o) % ns
+            y[j] = v[(j + M.r0 + q * M.d + p * M.g) % ns]
     out = np.zeros(ns, np.complex128)
     for u in range(M.R):
         out += np.roll(y, u * M.S)          # out[j] += y[j - u S]
@@ -222,15 +249,14 @@ def slot_map_plain(M: SlotMap, v: np.ndarray) -> np.ndarray:
 
 
 def mask_slots(M: SlotMap, n_slots: int, p: int, q: int) -> np.ndarray:
-    """Mask of term t = p n1 + q rotated by -p n1 d (zero past the last term):
-    entry j is 1 where j - p n1 d falls in run_t."""
+    """Mask of term (p, q) rotated by -p g (zero past the last term): entry j
+    is 1 where j - p g falls in the term's run."""
     z = np.zeros(n_slots, np.complex128)
-    t = p * M.n1 + q
-    if t >= M.n:
+    if p * M.n1 + q >= M.n:
         return z
     for o in range(M.w):
-        j = (M.j0 + t * M.J + o) % n_slots
-        z[(j + p * M.n1 * M.d) % n_slots] = 1.0
+        j = (_run_start(M, p, q) + o) % n_slots
+        z[(j + p * M.g) % n_slots] = 1.0
     return z
 
 
@@ -238,7 +264,7 @@ def slot_map_rotations(M: SlotMap, n_slots: int) -> set:
     """Rotation steps (mod n_slots, nonzero) the realisation key-switches by."""
     r = {M.r0 % n_slots}
     r |= {(q * M.d) % n_slots for q in range(M.n1)}
-    r |= {(p * M.n1 * M.d) % n_slots for p in range(M.n2)}
+    r |= {(p * M.g) % n_slots for p in range(M.n2)}
     s = 1
     while s < M.R:
         r.add((-s * M.S) % n_slots)
@@ -249,11 +275,19 @@ def slot_map_rotations(M: SlotMap, n_slots: int) -> set:
 
 def slot_map_ct(P: C.Params, ct: np.ndarray, M: SlotMap, masks, keys: dict) -> np.ndarray:
     """The three steps on a ciphertext at level M.level; masks(p, q) gives the
-    encoded mask of term p n1 + q (scale q_{l-1}).  Output at level - 1."""
+    encoded mask of term (p, q) (scale q_{l-1}; zero past the last term).
+    Output at level - 1."""
     v = C.rotate(P, ct, M.r0, keys)
-    unit = M.d % (P.n // 2) or 1
-    desc = OW.MatvecDesc(M.level, 1, 1, M.n1, M.n2, unit, False, True)
-    y = OW.bsgs_matvec(P, desc, [v], lambda b, p, u, q: masks(p, q), keys)[0]
+    baby = C.rotate_hoisted(P, v, [q * M.d for q in range(M.n1)], keys)
+    y = None
+    for p in range(M.n2):
+        acc = None
+        for q in range(M.n1):
+            t = C.mul_plain(P, baby[q], masks(p, q))
+            acc = t if acc is None else C.ct_add(P, acc, t)
+        acc = C.rotate(P, acc, p * M.g, keys)
+        y = acc if y is None else C.ct_add(P, y, acc)
+    y = C.rescale(P, y)
     s = 1
     while s < M.R:
         y = C.ct_add(P, y, C.rotate(P, y, -s * M.S, keys))

@@ -13,6 +13,8 @@ realisation:
 * the slot-map decomposition reproduces br exactly, its masked baby-step /
   giant-step sum equals the unsplit diagonal sum, and the encrypted
   realisation decrypts to br within 2^-15 on a small ring."""
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -140,7 +142,7 @@ def _rot(v, r):
 
 @pytest.mark.parametrize("D", SHAPES[1:], ids=lambda D: f"H{D.H}P{D.P}G{D.G}")
 def test_masked_bsgs_is_the_diagonal_sum(D):
-    """sum_{p,q} rho(M'_{p,q} * rho(v; q d); p n1 d) = sum_t M_t * rho(v; t d)
+    """sum_{p,q} rho(M'_{p,q} * rho(v; q d); p g) = sum_t M_t * rho(v; q d + p g)
     with the pre-rotated masks, and equals the first two steps of the map."""
     rng = np.random.default_rng(12)
     v = rng.standard_normal(D.n_slots)
@@ -150,15 +152,16 @@ def test_masked_bsgs_is_the_diagonal_sum(D):
         got = np.zeros(D.n_slots, np.complex128)
         for p in range(M.n2):
             acc = sum(BR.mask_slots(M, D.n_slots, p, q) * _rot(v0, q * M.d) for q in range(M.n1))
-            got += _rot(acc, p * M.n1 * M.d)
-        y = BR.slot_map_plain(BR.SlotMap(M.level, M.r0, M.d, M.n, M.n1, M.j0, M.J, M.w, 1,
-                                         M.S), v)
+            got += _rot(acc, p * M.g)
+        y = BR.slot_map_plain(dataclasses.replace(M, R=1), v)
         np.testing.assert_allclose(got, y, atol=1e-12)
 
 
 def test_slot_map_rejects_uncovered_shapes():
-    with pytest.raises(ValueError):        # 6 channels per chunk: not whole heads of 4
-        BR.br_slot_map(BR.Dims(2, 4, 1, 2, 6, 64), "a", 0, 0, 3)
+    with pytest.raises(ValueError, match="a"):   # 6 channels per chunk: not whole heads of 4
+        BR.br_slot_map(BR.Dims(3, 4, 1, 2, 6, 64), "a", 0, 0, 3)
+    with pytest.raises(ValueError, match="B/C"):  # 12-channel groups, 16-channel chunks
+        BR.br_slot_map(BR.Dims(24, 2, 4, 2, 16, 2048), "B", 0, 1, 3)
     with pytest.raises(ValueError):        # d_s = 3 cannot be replicated by doubling
         BR.br_slot_map(BR.Dims(2, 4, 1, 3, 4, 64), "x", 0, 0, 3)
     with pytest.raises(ValueError):        # token 8 of x does not fit 64 slots
@@ -187,3 +190,25 @@ def test_encrypted_broadcast_decrypts_to_br(kind):
     dec = C.decrypt(P, sk, out, 2.0 ** 40)
     want = BR.br(D, kind, v, k, kappa)
     np.testing.assert_allclose(dec, want, atol=2.0 ** -15)
+
+
+def test_encrypted_decay_broadcast_over_positions():
+    """A head span of P d_s = 1024 slots is placed at two positions per head
+    and replicated 512 times (terms (p, q): two heads x two positions):
+    N = 2^12, H = 2, P = 64, d_s = 16, one chunk of 128 channels."""
+    P = C.params_small(12, 50, 4, 2)
+    D = BR.Dims(H=2, P=64, G=1, d_s=16, c_state=128, n_slots=P.n // 2)
+    M = BR.br_slot_map(D, "a", 5, 0, 4)
+    assert (M.n1, M.n2, M.R, M.d, M.g) == (2, 2, 512, -512, 1 - 1024)
+    sk = C.secret_key(P, synth.secret(14, P.n))
+    keys = {P.galois_elt(r): C.keygen_from_seed(P, sk, 14, P.galois_elt(r))
+            for r in BR.slot_map_rotations(M, D.n_slots)}
+    v = synth.normal(14, "dr", D.n_slots) + 1j * synth.normal(14, "di", D.n_slots)
+    a, e = synth.encrypt_draws(14, P.qs(4), P.n, "dec", 0)
+    ct = C.encrypt(P, sk, C.encode_plain(P, v, 2.0 ** 40, 4), 4, a, e)
+    ql = float(P.q[3])
+    masks = {(p, q): C.encode_plain(P, BR.mask_slots(M, D.n_slots, p, q), ql, 4)
+             for p in range(M.n2) for q in range(M.n1)}
+    out = BR.slot_map_ct(P, ct, M, lambda p, q: masks[(p, q)], keys)
+    dec = C.decrypt(P, sk, out, 2.0 ** 40)
+    np.testing.assert_allclose(dec, BR.br(D, "a", v, 5, 0), atol=2.0 ** -15)
