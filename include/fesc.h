@@ -495,6 +495,100 @@ int fesc_affine_scan_resident_program(uint32_t L, uint32_t block, uint64_t* word
                                       size_t* count);
 
 /* ------------------------------------------------------------------------
+ * Public slot maps and the HEScan broadcasts (Sec. "CKKS Primitives and Slot
+ * Maps": br expands a compact factor into the state packing, br^(kappa)
+ * restricts it to chunk kappa; exact maps in Appendix "HEScan Kernel Packing
+ * and Correctness", paragraph "Exact State and Slot Maps").
+ *
+ * A slot map (slots j mod n_slots = N/2, rho(v; r)_j = v_{j+r}) over terms
+ * t = p n1 + q < terms (q < n1 baby index, p < n2 = ceil(terms / n1)):
+ *     y[j]   = v[j + offset + q stride + p giant_stride]   for j in run(p, q),
+ *              run(p, q) = [dst0 + q dst_stride + p dst_giant, ... + width)
+ *     y[j]   = 0                                           elsewhere
+ *     out[j] = sum_{u < rep_count} y[j - u rep_stride]
+ * evaluated homomorphically as
+ *     1. rho(v; offset)                           (one key switch; none if 0)
+ *     2. sum_t M_t (.) rho(.; q stride + p giant_stride) (M_t = 1 on the run):
+ *        the baby steps rho(.; q stride) share one ModUp, the giant steps are
+ *        rho(.; p giant_stride); then one rescale
+ *     3. log2(rep_count) doublings out += rho(out; -2^s rep_stride).
+ * Key switches: [offset != 0] + (n1 - 1) + (n2 - 1) + log2(rep_count); one
+ * level (input `level` >= 2, output level - 1).  The runs must be disjoint
+ * in the order of t: width <= dst_stride (n1 > 1) and (n1 - 1) dst_stride +
+ * width <= dst_giant (n2 > 1), the last run inside the slots.  The error of
+ * an output slot grows with the square root of rep_count (each doubling adds
+ * the key-switching noise of every slot of the copies it sums). */
+typedef struct fesc_slot_map_desc {
+  uint32_t level;        /* input level */
+  int32_t offset;        /* rotation applied first */
+  int32_t stride;        /* rotation per baby step */
+  int32_t giant_stride;  /* rotation per giant step */
+  uint32_t terms;        /* >= 1 */
+  uint32_t n1;           /* baby steps, >= 1 */
+  uint32_t dst0, dst_stride, dst_giant, width;  /* runs */
+  int32_t rep_stride;
+  uint32_t rep_count;    /* power of two, 1 = no replication */
+} fesc_slot_map_desc;
+
+/* Shape of the HEScan packing: H heads of width P (E = H P channels
+ * e = h P + p), G groups of B and C (heads in G contiguous groups of H / G,
+ * group g(h) = floor(h G / H)), state size d_s per channel, c_state channels
+ * per chunk (chunk kappa holds (e, i) at slot (e - kappa c_state) d_s + i). */
+typedef struct fesc_br_shape {
+  uint32_t H, P, G, d_s, c_state;
+} fesc_br_shape;
+
+#define FESC_BR_A 0  /* decay a_k, compact at slot k H + h */
+#define FESC_BR_X 1  /* input x_k, compact at slot k E + e */
+#define FESC_BR_B 2  /* B_k, compact at slot k G d_s + g d_s + i */
+#define FESC_BR_C 3  /* C_k, same packing as B_k */
+
+/* Host only: the slot map realising br^(kappa) of token k's factor `kind`
+ * from its compact packing, for ring degree N = 2^log_n and input level
+ * `level` (giant steps continue the baby steps, giant_stride = n1 stride and
+ * dst_giant = n1 dst_stride, unless stated):
+ *   x:  offset k E + kappa c, stride 1 - d_s, terms c, runs {t d_s},
+ *       replication d_s x 1                   (d_s a power of two);
+ *   a:  offset k H + kappa c / P; R = min(P d_s, 512); head p of the chunk
+ *       at P d_s / R positions: n1 = P d_s / R, stride -R, dst_stride R,
+ *       giant_stride 1 - P d_s, dst_giant P d_s, terms (c / P) n1, width 1;
+ *       replication R x 1                      (P | c, P d_s a power of 2);
+ *   B, C with chunk kappa inside group g: offset k G d_s + g d_s, one run
+ *       [0, d_s), replication c x d_s         (c a power of two);
+ *   B, C with chunk kappa over whole groups g0, g0 + 1, ... (Eg = H P / G
+ *       channels each): offset k G d_s + g0 d_s, stride d_s - Eg d_s, terms
+ *       c / Eg, runs [t Eg d_s, t Eg d_s + d_s), replication Eg x d_s.
+ * n1 (x, B, C) = the smallest power of two whose square reaches the term
+ * count.  FESC_ERR_ARG for shapes outside these cases, or a token whose
+ * compact factor or a chunk that does not fit N/2 slots. */
+int fesc_br_desc(uint32_t log_n, const fesc_br_shape* shape, uint32_t kind, uint32_t k,
+                 uint32_t kappa, uint32_t level, fesc_slot_map_desc* out);
+
+/* Slot vectors of the masks, rotated for the giant steps: mask m = p n1 + q
+ * (m < n1 * n2) is 1 at slot j where j - p giant_stride (mod n_slots) lies
+ * in run(p, q), and 0 elsewhere (all zero for m >= terms).  z: device
+ * [count][N/2] complex (interleaved re, im) for masks first .. first +
+ * count - 1, to be encoded at the scale of q_{level-1} (fesc_encode_plain). */
+int fesc_slot_map_mask_slots(fesc_ctx* ctx, const fesc_slot_map_desc* desc, uint32_t first,
+                             uint32_t count, double* z, void* stream);
+
+typedef struct fesc_slot_map_plan fesc_slot_map_plan;
+
+/* masks: host array of `terms` device plaintexts [level][N] (the encoded
+ * mask slot vectors m < terms); they must stay valid for the plan's lifetime.
+ * Allocates the plan's workspace.  FESC_ERR_NO_KEY if a key of the schedule
+ * is missing; FESC_ERR_ARG for runs that overlap or leave the slots, or a
+ * replication count that is not a power of two. */
+int fesc_slot_map_plan_create(fesc_ctx* ctx, const fesc_slot_map_desc* desc,
+                              const uint64_t* const* masks, fesc_slot_map_plan** plan);
+void fesc_slot_map_plan_destroy(fesc_slot_map_plan* plan);
+
+/* in: device ciphertext [level][2][N]; out: device [level-1][2][N] (may
+ * alias in: the input is read before the output is written). */
+int fesc_slot_map(fesc_ctx* ctx, fesc_slot_map_plan* plan, const uint64_t* in, uint64_t* out,
+                  void* stream);
+
+/* ------------------------------------------------------------------------
  * Small kernels on the same primitives.
  *
  * HEConv (Sec. "Causal Depthwise Convolution"): causal depthwise convolution

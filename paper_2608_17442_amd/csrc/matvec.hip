@@ -33,6 +33,7 @@ struct fesc_matvec_plan {
   uint64_t** d_ct = nullptr;          // device table of c~ pointers (pt-MAC outputs)
   size_t ct_words = 0;
   const uint64_t* bank = nullptr;     // tiled diagonal bank (instead of the table), or null
+  int64_t giant = 0;                  // rotation per giant step (n1 unit unless given)
   hipEvent_t ev[4] = {};               // phase marks of the last run
 };
 
@@ -247,8 +248,10 @@ static uint32_t diag_rows(const Context* c, const fesc_matvec_desc& d) {
   return d.level + (d.lazy_moddown ? c->alpha : 0);
 }
 
+// giant_unit: the rotation of one giant step, INT64_MIN for n1 * unit (the
+// projection); the slot maps give their own.
 int matvec_plan_create(Context* c, const fesc_matvec_desc* d, const uint64_t* const* diags,
-                       const uint64_t* bank, fesc_matvec_plan** out) {
+                       const uint64_t* bank, fesc_matvec_plan** out, int64_t giant_unit) {
   if (!out || (!diags && !bank)) return fail(FESC_ERR_ARG, "null argument");
   *out = nullptr;
   int rc = check_desc(c, d);
@@ -260,7 +263,8 @@ int matvec_plan_create(Context* c, const fesc_matvec_desc* d, const uint64_t* co
   // every Galois key the schedule needs must be present
   std::vector<int64_t> steps;
   for (uint32_t q = 1; q < d->n1; ++q) steps.push_back((int64_t)q * d->unit);
-  for (uint32_t p = 1; p < d->n2; ++p) steps.push_back((int64_t)p * d->n1 * d->unit);
+  const int64_t giant = giant_unit == INT64_MIN ? (int64_t)d->n1 * d->unit : giant_unit;
+  for (uint32_t p = 1; p < d->n2; ++p) steps.push_back((int64_t)p * giant % (c->n / 2));
   for (int64_t st : steps) {
     const uint32_t g = galois_of_step(c, (int32_t)(st % (c->n / 2)));
     if (g != 1 && !c->keys.count(g))
@@ -271,6 +275,7 @@ int matvec_plan_create(Context* c, const fesc_matvec_desc* d, const uint64_t* co
 
   fesc_matvec_plan* p = new fesc_matvec_plan();
   p->d = *d;
+  p->giant = giant;
   p->bank = bank;
   if (!bank) p->diag.assign(diags, diags + n_diag);
   p->ct_words = (size_t)2 * d->level * c->n;
@@ -402,7 +407,7 @@ int ptct_matvec(Context* c, fesc_matvec_plan* p, const uint64_t* const* in,
     for (uint32_t b = 0; b < d.n_out; ++b) {
       gin[b] = ct + ((size_t)b * d.n2 + g) * W;
       gout[b] = ct + (size_t)b * d.n2 * W;
-      gst[b] = (int32_t)(((int64_t)g * d.n1 * d.unit) % (c->n / 2));
+      gst[b] = (int32_t)(((int64_t)g * p->giant) % (c->n / 2));
     }
     if ((err = op_rotate_batch(c, d.n_out, gin.data(), gst.data(), gout.data(),
                                (const uint64_t* const*)gout.data(), level, s)))
@@ -456,7 +461,7 @@ int fesc_matvec_plan_create(fesc_ctx* ctx, const fesc_matvec_desc* desc,
                             const uint64_t* const* diags, fesc_matvec_plan** plan) {
   if (!ctx) return fesc::fail(FESC_ERR_ARG, "null context");
   if (!diags) return fesc::fail(FESC_ERR_ARG, "null diagonal table");
-  return fesc::matvec_plan_create(ctx, desc, diags, nullptr, plan);
+  return fesc::matvec_plan_create(ctx, desc, diags, nullptr, plan, INT64_MIN);
 }
 
 int fesc_matvec_bank_words(const fesc_ctx* ctx, const fesc_matvec_desc* desc, size_t* words) {
@@ -509,7 +514,7 @@ int fesc_matvec_plan_create_bank(fesc_ctx* ctx, const fesc_matvec_desc* desc,
                                  const uint64_t* bank, fesc_matvec_plan** plan) {
   if (!ctx) return fesc::fail(FESC_ERR_ARG, "null context");
   if (!bank) return fesc::fail(FESC_ERR_ARG, "null bank");
-  return fesc::matvec_plan_create(ctx, desc, nullptr, bank, plan);
+  return fesc::matvec_plan_create(ctx, desc, nullptr, bank, plan, INT64_MIN);
 }
 
 void fesc_matvec_plan_destroy(fesc_matvec_plan* plan) { fesc::matvec_plan_destroy(plan); }

@@ -643,3 +643,91 @@ class MatvecPlan:
             self.close()
         except Exception:
             pass
+
+
+# ------------------------------------------------- slot maps and broadcasts
+
+BR_A, BR_X, BR_B, BR_C = 0, 1, 2, 3
+_BR_KIND = {"a": BR_A, "x": BR_X, "B": BR_B, "C": BR_C}
+
+
+class SlotMapDesc(ctypes.Structure):
+    _fields_ = [("level", _u32), ("offset", _i32), ("stride", _i32), ("giant_stride", _i32),
+                ("terms", _u32), ("n1", _u32), ("dst0", _u32), ("dst_stride", _u32),
+                ("dst_giant", _u32), ("width", _u32), ("rep_stride", _i32), ("rep_count", _u32)]
+
+    @property
+    def n2(self) -> int:
+        return -(-self.terms // self.n1)
+
+
+class _BrShape(ctypes.Structure):
+    _fields_ = [(f, _u32) for f in ("H", "P", "G", "d_s", "c_state")]
+
+
+_lib.fesc_br_desc.argtypes = [_u32, ctypes.POINTER(_BrShape), _u32, _u32, _u32, _u32,
+                              ctypes.POINTER(SlotMapDesc)]
+_lib.fesc_br_desc.restype = ctypes.c_int
+_lib.fesc_slot_map_mask_slots.argtypes = [_vp, ctypes.POINTER(SlotMapDesc), _u32, _u32, _vp,
+                                          _vp]
+_lib.fesc_slot_map_mask_slots.restype = ctypes.c_int
+_lib.fesc_slot_map_plan_create.argtypes = [_vp, ctypes.POINTER(SlotMapDesc),
+                                           ctypes.POINTER(_vp), ctypes.POINTER(_vp)]
+_lib.fesc_slot_map_plan_create.restype = ctypes.c_int
+_lib.fesc_slot_map_plan_destroy.argtypes = [_vp]
+_lib.fesc_slot_map_plan_destroy.restype = None
+_lib.fesc_slot_map.argtypes = [_vp, _vp, _vp, _vp, _vp]
+_lib.fesc_slot_map.restype = ctypes.c_int
+
+
+def br_desc(log_n: int, H: int, P: int, G: int, d_s: int, c_state: int, kind: str, k: int,
+            kappa: int, level: int) -> SlotMapDesc:
+    """Slot map of br^(kappa) for token k's factor `kind` ("a", "x", "B" or
+    "C"); host only."""
+    d = SlotMapDesc()
+    _check(_lib.fesc_br_desc(log_n, ctypes.byref(_BrShape(H, P, G, d_s, c_state)),
+                             _BR_KIND[kind], k, kappa, level, ctypes.byref(d)))
+    return d
+
+
+def slot_map_mask_slots(ctx: Context, desc: SlotMapDesc, first: int, count: int, z,
+                        stream=None):
+    """Mask slot vectors first .. first+count-1 into the device complex128
+    tensor z [>= count][N/2] (encode them at the scale of q_{level-1})."""
+    if not (isinstance(z, torch.Tensor) and z.is_cuda and z.dtype == torch.complex128
+            and z.is_contiguous()):
+        raise TypeError("z: expected a contiguous CUDA complex128 tensor")
+    if z.numel() < count * (ctx.n // 2):
+        raise ValueError(f"z: {z.numel()} slots, the call writes {count * (ctx.n // 2)}")
+    _check(_lib.fesc_slot_map_mask_slots(ctx._h, ctypes.byref(desc), first, count,
+                                         z.data_ptr(), _stream(stream)))
+
+
+class SlotMapPlan:
+    """Homomorphic slot map over encoded masks (device plaintexts, one per
+    term, [level][N]); inputs are kept alive."""
+
+    def __init__(self, ctx: Context, desc: SlotMapDesc, masks):
+        self.ctx, self.desc = ctx, desc
+        self._masks = list(masks)
+        h = _vp()
+        _check(_lib.fesc_slot_map_plan_create(
+            ctx._h, ctypes.byref(desc), _ptrs(self._masks, desc.terms, ctx._pt(desc.level),
+                                               "masks"), ctypes.byref(h)))
+        self._h = h
+
+    def __call__(self, ct, out, stream=None):
+        c, d = self.ctx, self.desc
+        _check(_lib.fesc_slot_map(c._h, self._h, _ptr(ct, c._ct(d.level), "ct"),
+                                  _ptr(out, c._ct(d.level - 1), "out"), _stream(stream)))
+
+    def close(self):
+        if getattr(self, "_h", None):
+            _lib.fesc_slot_map_plan_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -233,3 +233,54 @@ def test_in_place_scan_program_gives_the_recurrence(L, chunks, states_only):
             assert mem[S0 + i] == h, (c, k)
             if not states_only:
                 assert mem[A0 + i] == pa, (c, k)
+
+
+def _br_shapes():
+    from oracle import broadcast as BR
+    return [(BR.Dims(2, 4, 1, 2, 4, 64), 7), (BR.Dims(4, 2, 2, 4, 4, 128), 8),
+            (BR.Dims(8, 2, 4, 2, 8, 128), 8), (BR.Dims(8, 2, 2, 4, 4, 256), 9),
+            (BR.Dims(4, 4, 2, 8, 8, 512), 10), (BR.Dims(24, 64, 1, 128, 128, 32768), 16)]
+
+
+@pytest.mark.parametrize("i", range(6))
+def test_broadcast_slot_maps_match_the_appendix_maps(i):
+    """fesc_br_desc (host only): the library's decomposition of br^(kappa),
+    applied on plain slot vectors by the oracle's slot-map definition, gives
+    exactly the appendix's broadcast of the oracle; and its fields equal the
+    oracle's decomposition of the same reading."""
+    from oracle import broadcast as BR
+    from paper_2608_17442_amd import fesc as F
+    D, log_n = _br_shapes()[i]
+    assert D.n_slots == 1 << (log_n - 1)
+    rng = np.random.default_rng(i)
+    v = rng.standard_normal(D.n_slots) + 1j * rng.standard_normal(D.n_slots)
+    L = D.n_slots // max(D.E, D.H, D.G * D.d_s)
+    for kind in BR.KINDS:
+        for k in sorted({0, L // 2, L - 1}):
+            for kappa in sorted({0, D.K_s // 2, D.K_s - 1}):
+                d = F.br_desc(log_n, D.H, D.P, D.G, D.d_s, D.c_state, kind, k, kappa, 5)
+                M = BR.SlotMap(d.level, d.offset, d.stride, d.terms, d.n1, d.giant_stride,
+                               d.dst0, d.dst_stride, d.dst_giant, d.width, d.rep_count,
+                               d.rep_stride)
+                assert np.array_equal(BR.slot_map_plain(M, v), BR.br(D, kind, v, k, kappa))
+                O = BR.br_slot_map(D, kind, k, kappa, 5)
+                assert (M.r0 - O.r0) % D.n_slots == 0 and M.n == O.n and M.n1 == O.n1
+                assert (M.j0, M.w, M.R, M.S) == (O.j0, O.w, O.R, O.S)
+                if M.n1 > 1:
+                    assert (M.d, M.J) == (O.d, O.J)
+                if M.n2 > 1:
+                    assert (M.g, M.Jg) == (O.g, O.Jg)
+
+
+def test_broadcast_slot_map_rejects_uncovered_shapes():
+    from paper_2608_17442_amd import fesc as F
+    with pytest.raises(F.FescError, match="a broadcast"):    # 6 channels: not whole heads of 4
+        F.br_desc(7, 3, 4, 1, 2, 6, "a", 0, 0, 3)
+    with pytest.raises(F.FescError, match="x broadcast"):    # d_s = 3
+        F.br_desc(7, 2, 4, 1, 3, 4, "x", 0, 0, 3)
+    with pytest.raises(F.FescError, match="x broadcast"):    # token 8 leaves 64 slots
+        F.br_desc(7, 2, 4, 1, 2, 4, "x", 8, 0, 3)
+    with pytest.raises(F.FescError, match="chunks"):         # kappa past the last chunk
+        F.br_desc(7, 2, 4, 1, 2, 4, "B", 0, 2, 3)
+    with pytest.raises(F.FescError, match="groups"):         # 12-channel groups, 16-channel chunks
+        F.br_desc(12, 24, 2, 4, 2, 16, "B", 0, 1, 3)
