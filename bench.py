@@ -31,7 +31,9 @@ configuration); keyswitch/s, matvec ms and scan-contract ms are reported in
 is data-oblivious) is timed on its own as `components.affine_scan`, and one
 whole HEScan layer at the paper's long-sequence shape (L = 2048, 12 state
 chunks, 23 limbs in: update construction, scan, contraction of every token;
-full-length and two-pass schedules) as `components.hescan_layer`.
+full-length and two-pass schedules) as `components.hescan_layer`; then the
+broadcasts br^(kappa) of one token's factors from their compact packings
+(homomorphic slot maps) as `components.broadcast`.
 Other modes: --affine-only, --scan-sweep (resident block sizes at L = 2048),
 --hescan-sweep (the HEScan layer at L = 128 .. 2048).
 Prints ONE JSON line on stdout.  --gpus > 1 is refused (single-GPU build).
@@ -663,6 +665,66 @@ def time_affine(W, F, torch, np):
                        "stages batched over chunks"}
 
 
+def time_broadcast(W, F, torch, np, level=24, k=3, kappa=7, reps=3):
+    """The broadcasts br^(kappa) of one token's factors from their compact
+    packings (Mamba-2 base: 24 heads of 64 channels, d_s = 128, 128 channels
+    per chunk, one group), input level 24 -> 23, as homomorphic slot maps.
+    Masks are generated and encoded on the device beforehand (offline, not
+    timed); one warm-up, then the mean of `reps` runs (HIP events).  B and C
+    share one map."""
+    shape = dict(H=24, P=64, G=1, d_s=128, c_state=128)
+    n, ns, seed = W.n, W.n // 2, 97
+    z = W.synth.normal(seed, "br-re", ns) + 1j * W.synth.normal(seed, "br-im", ns)
+    ct = W.encrypt(z, 2.0 ** 40, level, seed, "br", 0)
+    ql = float(W.q[level - 1])
+    res = {}
+    for kind in ("x", "a", "B"):
+        d = F.br_desc(W.log_n, shape["H"], shape["P"], shape["G"], shape["d_s"],
+                      shape["c_state"], kind, k, kappa, level)
+        n2 = d.n2
+        steps = {d.offset} | {q * d.stride for q in range(1, d.n1)} | \
+            {p * d.giant_stride for p in range(1, n2)}
+        r = 1
+        while r < d.rep_count:
+            steps.add(-r * d.rep_stride)
+            r *= 2
+        for st in steps:
+            g = W.ctx.galois_element(st % ns)
+            if g != 1:
+                W.keygen(g, seed)
+        cnt = d.n1 * n2
+        zs = torch.empty((cnt, ns), dtype=torch.complex128, device="cuda")
+        pts = torch.empty(cnt * level * n, dtype=torch.int64, device="cuda")
+        F.slot_map_mask_slots(W.ctx, d, 0, cnt, zs)
+        W.ctx.encode_plain(zs, ql, pts, level)
+        plan = F.SlotMapPlan(W.ctx, d, [pts[t * level * n:(t + 1) * level * n]
+                                        for t in range(d.terms)])
+        out = torch.empty((level - 1) * 2 * n, dtype=torch.int64, device="cuda")
+        plan(ct, out)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        ev[0].record()
+        for _ in range(reps):
+            plan(ct, out)
+        ev[1].record()
+        torch.cuda.synchronize()
+        ms = ev[0].elapsed_time(ev[1]) / reps
+        n_ks = int(d.offset % ns != 0) + (d.n1 - 1) + (n2 - 1) + (d.rep_count.bit_length() - 1)
+        res[kind] = {"ms": round(ms, 3), "key_switches": n_ks, "terms": d.terms, "n1": d.n1,
+                     "n2": n2, "copies": d.rep_count}
+        plan.close()
+        del zs, pts
+    L, K = 2048, 12
+    layer_ms = L * K * (res["x"]["ms"] + res["a"]["ms"]) + 2 * L * res["B"]["ms"]
+    return {"token": k, "chunk": kappa, "level_in": level, "maps": res,
+            "layer_s_if_homomorphic": round(layer_ms / 1e3, 1),
+            "layer_key_switches_if_homomorphic":
+                L * K * (res["x"]["key_switches"] + res["a"]["key_switches"])
+                + 2 * L * res["B"]["key_switches"],
+            "note": "per layer (2048 tokens, 12 chunks): x and a per token and chunk, B and C "
+                    "per token (one group: the same map for every chunk)"}
+
+
 # ---------------------------------------------------------------- baseline
 
 def _omp_threads() -> int:
@@ -1065,7 +1127,7 @@ def main():
     baby_ms, ptmac_ms, tail_ms = phases[-1]
     # HEScan affine prefix scan, timed after the steps with the projection's
     # diagonal bank released (its 128 x 12 x 2 ciphertexts take 51.5 GB)
-    affine = hescan = sc_seq = None
+    affine = hescan = sc_seq = broadcast = None
     if not args.no_affine:
         sc_seq = W.time_scan_contract_sequence()
         del W.mv_plan, W.bank, W.sc_in, W.sc_out
@@ -1073,6 +1135,7 @@ def main():
         affine = time_affine(W, F, torch, np)
         if not args.no_hescan:
             hescan = time_hescan(W, F, torch, np)
+        broadcast = time_broadcast(W, F, torch, np)
     n, rows = W.n, W.limbs * W.batch
     bytes_dir = 2 * 8 * n * rows
     ntt_gbs = 2 * bytes_dir / ((fwd + inv) * 1e-3) / 1e9
@@ -1170,6 +1233,7 @@ def main():
                                               "bank packing"},
             "affine_scan": affine,
             "hescan_layer": hescan,
+            "broadcast": broadcast,
         },
         "roofline": {
             "bound": "hbm", "kernel": "k_ptmac (projection plaintext-diagonal MAC)",
