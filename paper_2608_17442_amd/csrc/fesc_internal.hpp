@@ -118,6 +118,12 @@ struct LevelTables {
   // sources m_0 = q_{level-1}, m_{1+k} = p_k
   double2* mr_inv_n = nullptr; // [alpha+1]  N^-1 (M/m_j)^-1 mod m_j (m_0: N^-1, the row holding x P^-1)
   double2* mr_hat = nullptr;   // [level-1][alpha+1]  (M/m_j) mod q_i
+  // int8 operands of the matrix-core basis conversion (k_bconv_mfma, alpha
+  // <= 8): per target row 512 bytes [tau 8][lane group 4][16]; byte b of
+  // (tau, lg) is the balanced base-256 digit tau of 256^s hat_a mod m_row,
+  // a = 2 lg + b / 8, s = b % 8 (zero for s = 7 and past the digit's primes)
+  int8_t* mu_bytes = nullptr;  // [dnum][level+alpha][512]  of mu_hat
+  int8_t* md_bytes = nullptr;  // [level][512]              of md_hat
 };
 
 struct Context {

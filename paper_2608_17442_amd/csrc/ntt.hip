@@ -343,6 +343,7 @@ struct ModupMap {
   uint64_t* ext;
   const double2* mu_hat;
   uint32_t level, L, alpha, dnum_l, n;
+  const int8_t* mu_bytes;  // matrix-core operands (LevelTables::mu_bytes), or null
   __device__ uint32_t lo(uint32_t g) const { return (g % dnum_l) * alpha; }
   __device__ uint32_t aj(uint32_t g) const { return min(alpha, level - lo(g)); }
   __device__ uint32_t targets(uint32_t g) const { return level + alpha - aj(g); }
@@ -360,6 +361,9 @@ struct ModupMap {
   __device__ uint64_t* out(uint32_t g, uint32_t r) const {
     return ext + ((size_t)g * (level + alpha) + r) * n;
   }
+  __device__ const int8_t* bytes(uint32_t g, uint32_t r) const {
+    return mu_bytes + ((size_t)(g % dnum_l) * (level + alpha) + r) * 512;
+  }
 };
 
 // ModDown: group g = 2 * job + component, digits = the alpha special-prime
@@ -369,6 +373,7 @@ struct ModdownMap {
   uint64_t* y;
   const double2* md_hat;
   uint32_t level, alpha, n;
+  const int8_t* md_bytes;  // matrix-core operands (LevelTables::md_bytes), or null
   __device__ uint32_t aj(uint32_t) const { return alpha; }
   __device__ uint32_t targets(uint32_t) const { return level; }
   __device__ uint32_t row(uint32_t, uint32_t t) const { return t; }
@@ -380,6 +385,7 @@ struct ModdownMap {
   __device__ uint64_t* out(uint32_t g, uint32_t r) const {
     return y + ((size_t)g * level + r) * n;
   }
+  __device__ const int8_t* bytes(uint32_t, uint32_t r) const { return md_bytes + (size_t)r * 512; }
 };
 
 // ModDown merged with the rescale: group g = 2 * job + component, digits =
@@ -421,6 +427,111 @@ struct RescaleMap {
   __device__ const double2* hat(uint32_t, uint32_t r) const { return one + r; }
   __device__ uint64_t* out(uint32_t g, uint32_t r) const { return w + ((size_t)g * last + r) * n; }
 };
+
+// ------------------------- basis conversion on the matrix cores (N = 2^16)
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+// Balanced base-256 digits of an integer-valued x, |x| < 2^49, as 8 signed
+// bytes (the top one zero): the bytes of x + B, B = 0x80 in each of the low
+// seven bytes, each less 128 (x + 1.5 2^52 holds x in its low bits).
+__device__ __forceinline__ uint64_t bal_bytes(double x) {
+  const int64_t xi = __double_as_longlong(x + 6755399441055744.0) - 0x4338000000000000ll;
+  return (uint64_t)(xi + 0x0080808080808080ll) ^ 0x0080808080808080ull;
+}
+
+// The conversion of k_bconv_outer for N = 2^16 and digits of at most 8
+// primes, as an integer matrix product.  With x_a = sum_s x_a^s 256^s and
+// c_(a,s) = 256^s hat_a mod m = sum_tau c^tau_(a,s) 256^tau (balanced
+// base-256 digits, LevelTables::mu_bytes),
+//     y = sum_a x_a hat_a = sum_tau 256^tau Q_tau  (mod m),
+//     Q_tau = sum_(a,s) x_a^s c^tau_(a,s),
+// an exact int32 (56 products of magnitude <= 2^14).  A wavefront owns the
+// 16 columns c0 .. c0 + 15 of the outer pass (values c0 + u + 4096 m) for
+// every target of its group.  Per quad of targets and index m, two
+// 16 x 16 x 64 int8 products (rows: 4 targets x tau 0..3, then tau 4..7;
+// columns: u; k: 8 sources x 8 digit bytes) give every Q, so that lane
+// (g, u) ends up with y of target g at c0 + u + 4096 m for all 16 m: the
+// column of the outer pass, which then runs in registers as in
+// k_bconv_outer.
+template <class Map>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void k_bconv_mfma(Map map, const PrimeK* __restrict__ pk,
+                                                         const double2* __restrict__ twf) {
+  constexpr uint32_t n = 1u << 16, LOGM = 4, M = 16;
+  const uint32_t wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const uint32_t lg = lane >> 4, col = lane & 15;
+  const uint32_t g = blockIdx.z;
+  const uint32_t c = (blockIdx.x * (kThreads / 64) + wave) * 16 + col;  // this lane's column
+  const uint32_t aj = map.aj(g), nt = map.targets(g);
+  // B operands: column col of product m holds value c + 4096 m of sources
+  // 2 lg (bytes 0..7) and 2 lg + 1 (bytes 8..15); a source past the digit
+  // reads a valid row and contributes zero
+  v4i b[16];
+  {
+    const double* dig = map.digits(g);
+    const uint32_t a0 = 2 * lg, a1 = a0 + 1;
+    const double* r0 = dig + (size_t)min(a0, aj - 1) * n + c;
+    const double* r1 = dig + (size_t)min(a1, aj - 1) * n + c;
+    const uint64_t k0 = a0 < aj ? ~0ull : 0ull, k1 = a1 < aj ? ~0ull : 0ull;
+#pragma unroll
+    for (int m = 0; m < 16; ++m) {
+      const uint64_t p0 = bal_bytes(r0[kBlock * m]) & k0, p1 = bal_bytes(r1[kBlock * m]) & k1;
+      b[m] = v4i{(int)(uint32_t)p0, (int)(uint32_t)(p0 >> 32), (int)(uint32_t)p1,
+                 (int)(uint32_t)(p1 >> 32)};
+    }
+  }
+  for (uint32_t q0 = 0; q0 < nt; q0 += 4) {
+    // A operands: product row col = target q0 + col / 4, digit tau = col % 4
+    // (first product) or 4 + col % 4 (second)
+    const int8_t* tb = map.bytes(g, map.row(g, min(q0 + col / 4, nt - 1)));
+    const v4i alo = *reinterpret_cast<const v4i*>(tb + ((col % 4) * 4 + lg) * 16);
+    const v4i ahi = *reinterpret_cast<const v4i*>(tb + ((4 + col % 4) * 4 + lg) * 16);
+    // this lane's results: target q0 + lg (rows 4 lg .. 4 lg + 3 of each
+    // product); in a partial last quad the idle lane groups still join the
+    // products (a product needs the whole wavefront) and store nothing
+    const uint32_t tt = q0 + lg;
+    const uint32_t prime = map.prime(map.row(g, min(tt, nt - 1)));
+    const double q = pk[prime].q, qinv = pk[prime].qinv, k32 = 4294967296.0 * qinv;
+    const v4i zero = {0, 0, 0, 0};
+    double x[16];
+#pragma unroll
+    for (int m = 0; m < 16; ++m) {
+      const v4i dl = __builtin_amdgcn_mfma_i32_16x16x64_i8(alo, b[m], zero, 0, 0, 0);
+      const v4i dh = __builtin_amdgcn_mfma_i32_16x16x64_i8(ahi, b[m], zero, 0, 0, 0);
+      // R = hi 2^32 + lo exactly (|lo| < 2^45, |hi| < 2^37); y = R - c q with
+      // c = round(R / q), formed exactly (the fma's result is below 2^51)
+      const double lo = __builtin_fma(
+          __builtin_fma(__builtin_fma((double)dl[3], 256.0, (double)dl[2]), 256.0, (double)dl[1]),
+          256.0, (double)dl[0]);
+      const double hi =
+          __builtin_fma(__builtin_fma((double)dh[2], 256.0, (double)dh[1]), 256.0, (double)dh[0]);
+      const double cq = __builtin_rint(__builtin_fma(hi, k32, lo * qinv));
+      x[m] = red_bal(__builtin_fma(-cq, q, hi * 4294967296.0) + lo, q, qinv);
+      // consume each pair of products here: otherwise the combination sinks
+      // below the branch on tt and all 32 products (128 registers of
+      // results) are held at once
+      asm volatile("" : "+v"(x[m]));
+    }
+    if (tt >= nt) continue;
+    const double2* tw = twf + (size_t)prime * n;
+#pragma unroll
+    for (int s = 0; s < LOGM; ++s) {
+      const int H = M >> (s + 1);
+#pragma unroll
+      for (int m = 0; m < M; ++m) {
+        if (m & H) continue;
+        const double2 w = tw[(1 << s) + (m >> (LOGM - s))];
+        const double u = (s % 2 == 0) ? red_bal(x[m], q, qinv) : x[m];
+        const double v = mm_shoup(x[m + H], w.x, w.y, q);
+        x[m] = u + v;
+        x[m + H] = u - v;
+      }
+    }
+    double* outd = reinterpret_cast<double*>(map.out(g, map.row(g, tt)));
+#pragma unroll
+    for (int m = 0; m < 16; ++m) outd[c + kBlock * m] = x[m];
+  }
+}
 
 // ------------------------------------------------------------- inner pass
 
@@ -791,10 +902,29 @@ hipError_t launch_inverse(const Context* c, const RowSel& rs, uint32_t batch, ui
 
 constexpr int kBconvTargets = 3;
 
+// The matrix-core conversion serves N = 2^16 for the maps that carry its
+// operand tables (ModUp and ModDown with digits of at most 8 primes).
+template <class Map>
+constexpr bool kMfmaMap = false;
+template <>
+constexpr bool kMfmaMap<ModupMap> = true;
+template <>
+constexpr bool kMfmaMap<ModdownMap> = true;
+
+__host__ inline const int8_t* mfma_bytes(const ModupMap& m) { return m.mu_bytes; }
+__host__ inline const int8_t* mfma_bytes(const ModdownMap& m) { return m.md_bytes; }
+
 template <class Map>
 hipError_t launch_bconv_outer(const Context* c, const Map& map, uint32_t targets, uint32_t groups,
                               hipStream_t s) {
   constexpr int T = kBconvTargets;
+  if constexpr (kMfmaMap<Map>) {
+    if (c->log_n == 16 && mfma_bytes(map)) {
+      k_bconv_mfma<Map><<<dim3(kBlock / (16 * (kThreads / 64)), 1, groups), kThreads, 0, s>>>(
+          map, c->d_pk, c->d_tw_fwd);
+      return hipGetLastError();
+    }
+  }
   const dim3 grid(c->n / kBlock, (targets + T - 1) / T, groups), blk(kThreads);
   const double2* tw = c->d_tw_fwd;
   switch (c->log_n) {
@@ -862,7 +992,7 @@ hipError_t launch_modup_outer(const Context* c, const LevelTables& T, const uint
   const uint32_t dnum_l = (level + c->alpha - 1) / c->alpha;
   const uint32_t aj_min = level - (dnum_l - 1) * c->alpha;
   const ModupMap map{reinterpret_cast<const double*>(cc), ext, T.mu_hat, level, c->L, c->alpha,
-                     dnum_l, c->n};
+                     dnum_l, c->n, T.mu_bytes};
   return launch_bconv_outer(c, map, level + c->alpha - aj_min, nsrc * dnum_l, s);
 }
 
@@ -870,7 +1000,7 @@ hipError_t launch_modup_outer(const Context* c, const LevelTables& T, const uint
 // launch_ntt_inv_digits) fused with the first forward pass of y.
 hipError_t launch_moddown_outer(const Context* c, const LevelTables& T, const uint64_t* acc,
                                 uint64_t* y, uint32_t njobs, uint32_t level, hipStream_t s) {
-  const ModdownMap map{acc, y, T.md_hat, level, c->alpha, c->n};
+  const ModdownMap map{acc, y, T.md_hat, level, c->alpha, c->n, T.md_bytes};
   return launch_bconv_outer(c, map, level, 2 * njobs, s);
 }
 

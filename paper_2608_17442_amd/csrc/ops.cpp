@@ -30,6 +30,20 @@ uint64_t prod_mod_except(const std::vector<uint64_t>& ps, size_t skip, uint64_t 
 
 double2 entry(uint64_t v, uint64_t m) { return double2{(double)v, (double)v / (double)m}; }
 
+// The 512 operand bytes of one target row of the matrix-core conversion
+// (LevelTables::mu_bytes): hats[a] for a < aj (aj <= 8), target prime m.
+void conversion_bytes(int8_t* dst, const uint64_t* hats, uint32_t aj, uint64_t m) {
+  for (uint32_t a = 0; a < 8; ++a)
+    for (uint32_t s = 0; s < 8; ++s) {
+      int64_t v = (a < aj && s < 7) ? (int64_t)h_mulmod(hats[a] % m, h_powmod(2, 8 * s, m), m) : 0;
+      for (uint32_t tau = 0; tau < 8; ++tau) {
+        const int64_t d = ((v + 128) & 255) - 128;  // balanced digit in [-128, 127]
+        v = (v - d) / 256;
+        dst[(tau * 4 + a / 2) * 16 + (a % 2) * 8 + s] = (int8_t)d;
+      }
+    }
+}
+
 }  // namespace
 
 const LevelTables* level_tables(Context* c, uint32_t level, int* err) {
@@ -43,6 +57,9 @@ const LevelTables* level_tables(Context* c, uint32_t level, int* err) {
 
   std::vector<double2> mu_inv((size_t)dnum_l * alpha), mu_hat((size_t)dnum_l * E * alpha),
       mu_inv_n(level);
+  const bool mfma = alpha <= 8;  // the matrix-core conversion's operand tables
+  std::vector<int8_t> mu_bytes(mfma ? (size_t)dnum_l * E * 512 : 0),
+      md_bytes(mfma ? (size_t)level * 512 : 0);
   for (uint32_t j = 0; j < dnum_l; ++j) {
     const uint32_t lo = j * alpha, hi = std::min(lo + alpha, level);
     std::vector<uint64_t> dq(c->primes.begin() + lo, c->primes.begin() + hi);
@@ -55,6 +72,13 @@ const LevelTables* level_tables(Context* c, uint32_t level, int* err) {
         mu_hat[((size_t)j * E + row) * alpha + a] = entry(prod_mod_except(dq, a, m), m);
       }
     }
+    if (mfma)
+      for (uint32_t row = 0; row < E; ++row) {
+        const uint64_t m = ext_prime(row);
+        uint64_t hats[8];
+        for (uint32_t a = 0; a < hi - lo; ++a) hats[a] = prod_mod_except(dq, a, m);
+        conversion_bytes(mu_bytes.data() + ((size_t)j * E + row) * 512, hats, hi - lo, m);
+      }
   }
   std::vector<double2> md_inv(alpha), md_hat((size_t)level * alpha), md_pinv(level), pmod(L),
       rs_inv(level), md_inv_n(alpha);
@@ -69,8 +93,12 @@ const LevelTables* level_tables(Context* c, uint32_t level, int* err) {
     pmod[i] = entry(P, q);
     if (i < level) {
       md_pinv[i] = entry(h_inv(P, q), q);
-      for (uint32_t a = 0; a < alpha; ++a)
-        md_hat[(size_t)i * alpha + a] = entry(prod_mod_except(ps, a, q), q);
+      uint64_t hats[FESC_MAX_ALPHA];
+      for (uint32_t a = 0; a < alpha; ++a) {
+        hats[a] = prod_mod_except(ps, a, q);
+        md_hat[(size_t)i * alpha + a] = entry(hats[a], q);
+      }
+      if (mfma) conversion_bytes(md_bytes.data() + (size_t)i * 512, hats, alpha, q);
       if (i + 1 < level) rs_inv[i] = entry(h_inv(c->primes[level - 1] % q, q), q);
     }
   }
@@ -107,15 +135,27 @@ const LevelTables* level_tables(Context* c, uint32_t level, int* err) {
     off[p] = all.size();
     all.insert(all.end(), parts[p]->begin(), parts[p]->end());
   }
+  // one allocation: the double2 tables, then the conversion bytes
+  const size_t words = sizeof(double2) * all.size();
+  const size_t total = words + mu_bytes.size() + md_bytes.size();
   double2* d = nullptr;
-  if (hipMalloc(&d, sizeof(double2) * all.size()) != hipSuccess) {
+  if (hipMalloc(&d, total) != hipSuccess) {
     *err = fail(FESC_ERR_OOM, "level table allocation failed");
     return nullptr;
   }
-  if ((*err = hip_check(hipMemcpy(d, all.data(), sizeof(double2) * all.size(),
-                                  hipMemcpyHostToDevice), "hipMemcpy"))) {
+  int8_t* bytes = reinterpret_cast<int8_t*>(d) + words;
+  if ((*err = hip_check(hipMemcpy(d, all.data(), words, hipMemcpyHostToDevice), "hipMemcpy")) ||
+      (mfma && ((*err = hip_check(hipMemcpy(bytes, mu_bytes.data(), mu_bytes.size(),
+                                            hipMemcpyHostToDevice), "hipMemcpy")) ||
+                (*err = hip_check(hipMemcpy(bytes + mu_bytes.size(), md_bytes.data(),
+                                            md_bytes.size(), hipMemcpyHostToDevice),
+                                  "hipMemcpy"))))) {
     (void)hipFree(d);
     return nullptr;
+  }
+  if (mfma) {
+    T.mu_bytes = bytes;
+    T.md_bytes = bytes + mu_bytes.size();
   }
   T.base = d;
   T.mu_inv = d + off[0];
