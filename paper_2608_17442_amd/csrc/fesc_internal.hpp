@@ -124,6 +124,7 @@ struct LevelTables {
   // a = 2 lg + b / 8, s = b % 8 (zero for s = 7 and past the digit's primes)
   int8_t* mu_bytes = nullptr;  // [dnum][level+alpha][512]  of mu_hat
   int8_t* md_bytes = nullptr;  // [level][512]              of md_hat
+  int8_t* mr_bytes = nullptr;  // [level-1][512]            of mr_hat, digit sources 0..7
 };
 
 struct Context {

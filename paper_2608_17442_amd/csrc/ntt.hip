@@ -30,6 +30,8 @@
 // next to the data and generates those of bits 3..0 from one power per
 // thread (Context::d_tw3_*), so that no global load is waited on
 // between its butterflies.
+#include <type_traits>
+
 #include "butterfly.hpp"
 #include "fesc_internal.hpp"
 #include "ops.hpp"
@@ -397,6 +399,7 @@ struct ModdownRescaleMap {
   uint64_t* y;
   const double2* mr_hat;
   uint32_t level, E, alpha, rows, n;  // alpha = number of digits (special primes + 1)
+  const int8_t* mr_bytes;  // matrix-core operands of digits 0..7 (LevelTables::mr_bytes), or null
   __device__ uint32_t aj(uint32_t) const { return alpha; }
   __device__ uint32_t targets(uint32_t) const { return rows; }
   __device__ uint32_t row(uint32_t, uint32_t t) const { return t; }
@@ -408,6 +411,7 @@ struct ModdownRescaleMap {
   __device__ uint64_t* out(uint32_t g, uint32_t r) const {
     return y + ((size_t)g * (level - 1) + r) * n;
   }
+  __device__ const int8_t* bytes(uint32_t, uint32_t r) const { return mr_bytes + (size_t)r * 512; }
 };
 
 // Rescale lift: group g = 2 b + t (component t of ciphertext b), one digit =
@@ -441,7 +445,8 @@ __device__ __forceinline__ uint64_t bal_bytes(double x) {
 }
 
 // The conversion of k_bconv_outer for N = 2^16 and digits of at most 8
-// primes, as an integer matrix product.  With x_a = sum_s x_a^s 256^s and
+// primes (a ninth source, for ModDown merged with the rescale, as one
+// Shoup product per value on the VALU), as an integer matrix product.  With x_a = sum_s x_a^s 256^s and
 // c_(a,s) = 256^s hat_a mod m = sum_tau c^tau_(a,s) 256^tau (balanced
 // base-256 digits, LevelTables::mu_bytes),
 //     y = sum_a x_a hat_a = sum_tau 256^tau Q_tau  (mod m),
@@ -454,15 +459,18 @@ __device__ __forceinline__ uint64_t bal_bytes(double x) {
 // (g, u) ends up with y of target g at c0 + u + 4096 m for all 16 m: the
 // column of the outer pass, which then runs in registers as in
 // k_bconv_outer.
-template <class Map>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void k_bconv_mfma(Map map, const PrimeK* __restrict__ pk,
-                                                         const double2* __restrict__ twf) {
+template <class Map, bool NINTH>
+__device__ __forceinline__ void bconv_mfma(const Map& map, const PrimeK* __restrict__ pk,
+                                           const double2* __restrict__ twf) {
   constexpr uint32_t n = 1u << 16, LOGM = 4, M = 16;
   const uint32_t wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const uint32_t lg = lane >> 4, col = lane & 15;
   const uint32_t g = blockIdx.z;
   const uint32_t c = (blockIdx.x * (kThreads / 64) + wave) * 16 + col;  // this lane's column
   const uint32_t aj = map.aj(g), nt = map.targets(g);
+  // a ninth digit source (ModDown merged with the rescale: q_{l-1} and eight
+  // special primes) is added on the VALU
+  const double* d8 = map.digits(g) + (size_t)8 * n + c;  // read only with NINTH (aj = 9)
   // B operands: column col of product m holds value c + 4096 m of sources
   // 2 lg (bytes 0..7) and 2 lg + 1 (bytes 8..15); a source past the digit
   // reads a valid row and contributes zero
@@ -490,8 +498,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     // product); in a partial last quad the idle lane groups still join the
     // products (a product needs the whole wavefront) and store nothing
     const uint32_t tt = q0 + lg;
-    const uint32_t prime = map.prime(map.row(g, min(tt, nt - 1)));
+    const uint32_t trow = map.row(g, min(tt, nt - 1));
+    const uint32_t prime = map.prime(trow);
     const double q = pk[prime].q, qinv = pk[prime].qinv, k32 = 4294967296.0 * qinv;
+    double2 h8{0.0, 0.0};
+    if constexpr (NINTH) h8 = map.hat(g, trow)[8];
     const v4i zero = {0, 0, 0, 0};
     double x[16];
 #pragma unroll
@@ -506,7 +517,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
       const double hi =
           __builtin_fma(__builtin_fma((double)dh[2], 256.0, (double)dh[1]), 256.0, (double)dh[0]);
       const double cq = __builtin_rint(__builtin_fma(hi, k32, lo * qinv));
-      x[m] = red_bal(__builtin_fma(-cq, q, hi * 4294967296.0) + lo, q, qinv);
+      double r = __builtin_fma(-cq, q, hi * 4294967296.0) + lo;
+      if constexpr (NINTH) r += mm_shoup(d8[kBlock * m], h8.x, h8.y, q);  // |r| < 1.2 q
+      x[m] = red_bal(r, q, qinv);
       // consume each pair of products here: otherwise the combination sinks
       // below the branch on tt and all 32 products (128 registers of
       // results) are held at once
@@ -531,6 +544,20 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
 #pragma unroll
     for (int m = 0; m < 16; ++m) outd[c + kBlock * m] = x[m];
   }
+}
+
+// Three waves per SIMD fit without spilling; the ninth-digit variant keeps
+// two (its extra loads would spill at three).
+template <class Map>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void k_bconv_mfma(
+    Map map, const PrimeK* __restrict__ pk, const double2* __restrict__ twf) {
+  bconv_mfma<Map, false>(map, pk, twf);
+}
+
+template <class Map>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void k_bconv_mfma9(
+    Map map, const PrimeK* __restrict__ pk, const double2* __restrict__ twf) {
+  bconv_mfma<Map, true>(map, pk, twf);
 }
 
 // ------------------------------------------------------------- inner pass
@@ -903,16 +930,22 @@ hipError_t launch_inverse(const Context* c, const RowSel& rs, uint32_t batch, ui
 constexpr int kBconvTargets = 3;
 
 // The matrix-core conversion serves N = 2^16 for the maps that carry its
-// operand tables (ModUp and ModDown with digits of at most 8 primes).
+// operand tables (ModUp, ModDown and ModDown merged with the rescale, with
+// digits of at most 8 primes plus at most one on the VALU).
 template <class Map>
 constexpr bool kMfmaMap = false;
 template <>
 constexpr bool kMfmaMap<ModupMap> = true;
 template <>
 constexpr bool kMfmaMap<ModdownMap> = true;
+template <>
+constexpr bool kMfmaMap<ModdownRescaleMap> = true;
 
 __host__ inline const int8_t* mfma_bytes(const ModupMap& m) { return m.mu_bytes; }
 __host__ inline const int8_t* mfma_bytes(const ModdownMap& m) { return m.md_bytes; }
+__host__ inline const int8_t* mfma_bytes(const ModdownRescaleMap& m) {
+  return m.alpha <= 9 ? m.mr_bytes : nullptr;  // at most one digit past the eight
+}
 
 template <class Map>
 hipError_t launch_bconv_outer(const Context* c, const Map& map, uint32_t targets, uint32_t groups,
@@ -920,8 +953,14 @@ hipError_t launch_bconv_outer(const Context* c, const Map& map, uint32_t targets
   constexpr int T = kBconvTargets;
   if constexpr (kMfmaMap<Map>) {
     if (c->log_n == 16 && mfma_bytes(map)) {
-      k_bconv_mfma<Map><<<dim3(kBlock / (16 * (kThreads / 64)), 1, groups), kThreads, 0, s>>>(
-          map, c->d_pk, c->d_tw_fwd);
+      const dim3 grid(kBlock / (16 * (kThreads / 64)), 1, groups);
+      if constexpr (std::is_same_v<Map, ModdownRescaleMap>) {
+        if (map.alpha > 8) {  // q_{l-1} and eight special primes
+          k_bconv_mfma9<Map><<<grid, kThreads, 0, s>>>(map, c->d_pk, c->d_tw_fwd);
+          return hipGetLastError();
+        }
+      }
+      k_bconv_mfma<Map><<<grid, kThreads, 0, s>>>(map, c->d_pk, c->d_tw_fwd);
       return hipGetLastError();
     }
   }
@@ -1017,7 +1056,7 @@ hipError_t launch_moddown_rescale_outer(const Context* c, const LevelTables& T,
                                         const uint64_t* acc, uint64_t* y, uint32_t njobs,
                                         uint32_t level, uint32_t rows, hipStream_t s) {
   const ModdownRescaleMap map{acc, y, T.mr_hat, level, level + c->alpha, c->alpha + 1, rows,
-                              c->n};
+                              c->n, T.mr_bytes};
   return launch_bconv_outer(c, map, rows, 2 * njobs, s);
 }
 

@@ -59,7 +59,7 @@ const LevelTables* level_tables(Context* c, uint32_t level, int* err) {
       mu_inv_n(level);
   const bool mfma = alpha <= 8;  // the matrix-core conversion's operand tables
   std::vector<int8_t> mu_bytes(mfma ? (size_t)dnum_l * E * 512 : 0),
-      md_bytes(mfma ? (size_t)level * 512 : 0);
+      md_bytes(mfma ? (size_t)level * 512 : 0), mr_bytes(mfma ? (size_t)(level - 1) * 512 : 0);
   for (uint32_t j = 0; j < dnum_l; ++j) {
     const uint32_t lo = j * alpha, hi = std::min(lo + alpha, level);
     std::vector<uint64_t> dq(c->primes.begin() + lo, c->primes.begin() + hi);
@@ -118,10 +118,13 @@ const LevelTables* level_tables(Context* c, uint32_t level, int* err) {
     }
     for (uint32_t i = 0; i + 1 < level; ++i) {
       const uint64_t q = c->primes[i];
-      mr_hat[(size_t)i * (alpha + 1)] = entry(prod_mod_except(ps, ps.size(), q), q);  // P
+      uint64_t hats[FESC_MAX_ALPHA + 1];
+      hats[0] = prod_mod_except(ps, ps.size(), q);  // P
       for (uint32_t a = 0; a < alpha; ++a)
-        mr_hat[(size_t)i * (alpha + 1) + 1 + a] =
-            entry(h_mulmod(prod_mod_except(ps, a, q), ql % q, q), q);  // (P/p_a) q_{l-1}
+        hats[1 + a] = h_mulmod(prod_mod_except(ps, a, q), ql % q, q);  // (P/p_a) q_{l-1}
+      for (uint32_t a = 0; a <= alpha; ++a) mr_hat[(size_t)i * (alpha + 1) + a] = entry(hats[a], q);
+      // sources 0..7 on the matrix cores (the ninth, p_7 for alpha = 8, on the VALU)
+      if (mfma) conversion_bytes(mr_bytes.data() + (size_t)i * 512, hats, std::min(alpha + 1, 8u), q);
     }
   }
   std::vector<double2> all;
@@ -137,7 +140,7 @@ const LevelTables* level_tables(Context* c, uint32_t level, int* err) {
   }
   // one allocation: the double2 tables, then the conversion bytes
   const size_t words = sizeof(double2) * all.size();
-  const size_t total = words + mu_bytes.size() + md_bytes.size();
+  const size_t total = words + mu_bytes.size() + md_bytes.size() + mr_bytes.size();
   double2* d = nullptr;
   if (hipMalloc(&d, total) != hipSuccess) {
     *err = fail(FESC_ERR_OOM, "level table allocation failed");
@@ -149,6 +152,10 @@ const LevelTables* level_tables(Context* c, uint32_t level, int* err) {
                                             hipMemcpyHostToDevice), "hipMemcpy")) ||
                 (*err = hip_check(hipMemcpy(bytes + mu_bytes.size(), md_bytes.data(),
                                             md_bytes.size(), hipMemcpyHostToDevice),
+                                  "hipMemcpy")) ||
+                (*err = hip_check(hipMemcpy(bytes + mu_bytes.size() + md_bytes.size(),
+                                            mr_bytes.data(), mr_bytes.size(),
+                                            hipMemcpyHostToDevice),
                                   "hipMemcpy"))))) {
     (void)hipFree(d);
     return nullptr;
@@ -156,6 +163,7 @@ const LevelTables* level_tables(Context* c, uint32_t level, int* err) {
   if (mfma) {
     T.mu_bytes = bytes;
     T.md_bytes = bytes + mu_bytes.size();
+    T.mr_bytes = bytes + mu_bytes.size() + md_bytes.size();
   }
   T.base = d;
   T.mu_inv = d + off[0];
