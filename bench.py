@@ -665,13 +665,14 @@ def time_affine(W, F, torch, np):
                        "stages batched over chunks"}
 
 
-def time_broadcast(W, F, torch, np, level=24, k=3, kappa=7, reps=3):
+def time_broadcast(W, F, torch, np, level=24, k=3, kappa=7, reps=3, batch=16):
     """The broadcasts br^(kappa) of one token's factors from their compact
     packings (Mamba-2 base: 24 heads of 64 channels, d_s = 128, 128 channels
     per chunk, one group), input level 24 -> 23, as homomorphic slot maps.
     Masks are generated and encoded on the device beforehand (offline, not
     timed); one warm-up, then the mean of `reps` runs (HIP events).  B and C
-    share one map."""
+    share one map.  Each map is also timed over a block of `batch` tokens in
+    one call (batched_ms_per_token)."""
     shape = dict(H=24, P=64, G=1, d_s=128, c_state=128)
     n, ns, seed = W.n, W.n // 2, 97
     z = W.synth.normal(seed, "br-re", ns) + 1j * W.synth.normal(seed, "br-im", ns)
@@ -712,12 +713,36 @@ def time_broadcast(W, F, torch, np, level=24, k=3, kappa=7, reps=3):
         n_ks = int(d.offset % ns != 0) + (d.n1 - 1) + (n2 - 1) + (d.rep_count.bit_length() - 1)
         res[kind] = {"ms": round(ms, 3), "key_switches": n_ks, "terms": d.terms, "n1": d.n1,
                      "n2": n2, "copies": d.rep_count}
+        # the same map for a block of tokens 0 .. batch-1 of the chunk under one
+        # plan (fesc_slot_map_batch), each with its own first rotation
+        offs = [F.br_desc(W.log_n, shape["H"], shape["P"], shape["G"], shape["d_s"],
+                          shape["c_state"], kind, kt, kappa, level).offset
+                for kt in range(batch)]
+        for st in offs:
+            g = W.ctx.galois_element(st % ns)
+            if g != 1:
+                W.keygen(g, seed)
+        outs = [torch.empty((level - 1) * 2 * n, dtype=torch.int64, device="cuda")
+                for _ in range(batch)]
+        plan.batch([ct] * batch, offs, outs)
+        torch.cuda.synchronize()
+        ev[0].record()
+        for _ in range(reps):
+            plan.batch([ct] * batch, offs, outs)
+        ev[1].record()
+        torch.cuda.synchronize()
+        res[kind]["batched_ms_per_token"] = round(ev[0].elapsed_time(ev[1]) / reps / batch, 3)
+        del outs
         plan.close()
         del zs, pts
     L, K = 2048, 12
     layer_ms = L * K * (res["x"]["ms"] + res["a"]["ms"]) + 2 * L * res["B"]["ms"]
+    layer_ms_b = L * K * (res["x"]["batched_ms_per_token"] + res["a"]["batched_ms_per_token"]) \
+        + 2 * L * res["B"]["batched_ms_per_token"]
     return {"token": k, "chunk": kappa, "level_in": level, "maps": res,
             "layer_s_if_homomorphic": round(layer_ms / 1e3, 1),
+            "layer_s_if_homomorphic_batched": round(layer_ms_b / 1e3, 1),
+            "batch_tokens": batch,
             "layer_key_switches_if_homomorphic":
                 L * K * (res["x"]["key_switches"] + res["a"]["key_switches"])
                 + 2 * L * res["B"]["key_switches"],

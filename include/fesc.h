@@ -588,6 +588,20 @@ void fesc_slot_map_plan_destroy(fesc_slot_map_plan* plan);
 int fesc_slot_map(fesc_ctx* ctx, fesc_slot_map_plan* plan, const uint64_t* in, uint64_t* out,
                   void* stream);
 
+/* The plan's map over `count` (1 .. 65535) inputs at once, item i with its
+ * own first rotation offsets[i] in place of the plan's offset (the rest of
+ * the map is the plan's; for br^(kappa) the tokens of one kind and chunk
+ * differ only there, Appendix "HEScan Kernel Packing and Correctness").
+ * ins[i]: device ciphertext [level][2][N]; outs[i]: device [level-1][2][N]
+ * (may alias ins[i]).  Groups of up to 16 items share their key-switch launches:
+ * the offset rotations one launch, every doubling one launch with all jobs
+ * under one key.  Allocates the plan's batch workspace on first use.
+ * FESC_ERR_NO_KEY (before any launch) if an offset's rotation key is
+ * missing; the plan must not be used from two streams at once. */
+int fesc_slot_map_batch(fesc_ctx* ctx, fesc_slot_map_plan* plan, uint32_t count,
+                        const uint64_t* const* ins, const int32_t* offsets,
+                        uint64_t* const* outs, void* stream);
+
 /* ------------------------------------------------------------------------
  * Small kernels on the same primitives.
  *

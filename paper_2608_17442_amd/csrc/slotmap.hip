@@ -15,6 +15,7 @@
 // slot grows as the square root of R: R doublings add the key-switching noise
 // of R shifted copies); B and C select a group's d_s values and tile them over
 // the chunk's channels.
+#include <algorithm>
 #include <string>
 #include <vector>
 
@@ -26,6 +27,8 @@ struct fesc_slot_map_plan {
   fesc_matvec_plan* mv = nullptr;  // step 2 (n_in = n_out = 1, rescale)
   uint64_t* zero = nullptr;        // [level][N] zero plaintext for masks past `terms`
   uint64_t* work = nullptr;        // rotated input [level][2][N], two [level-1][2][N]
+  uint64_t* bwork = nullptr;       // the same per item of a batch (up to kSlotMapGroup items)
+  uint32_t bcap = 0;               // items bwork holds
 };
 
 namespace fesc {
@@ -189,6 +192,7 @@ void slot_map_plan_destroy(fesc_slot_map_plan* p) {
   matvec_plan_destroy(p->mv);
   (void)hipFree(p->zero);
   (void)hipFree(p->work);
+  (void)hipFree(p->bwork);
   delete p;
 }
 
@@ -270,6 +274,87 @@ int slot_map(Context* c, fesc_slot_map_plan* p, const uint64_t* in, uint64_t* ou
   return FESC_OK;
 }
 
+// Items of a batched slot map processed together (their workspaces at once).
+constexpr uint32_t kSlotMapGroup = 16;
+
+// The plan's map for `count` inputs with their own first rotations: the
+// offset rotations of a group share one key-switch launch, the step-2 sums run
+// per item, and every doubling is one launch over the group, all its jobs
+// under one key.
+int slot_map_batch(Context* c, fesc_slot_map_plan* p, uint32_t count, const uint64_t* const* ins,
+                   const int32_t* offsets, uint64_t* const* outs, hipStream_t s) {
+  if (!ins || !offsets || !outs) return fail(FESC_ERR_ARG, "null argument");
+  if (!count || count > 65535) return fail(FESC_ERR_ARG, "batch of 1 .. 65535 items");
+  const fesc_slot_map_desc& d = p->d;
+  const size_t n = c->n, lo = d.level - 1;
+  const uint32_t ns = c->n / 2;
+  for (uint32_t i = 0; i < count; ++i) {
+    if (!ins[i] || !outs[i]) return fail(FESC_ERR_ARG, "null item " + std::to_string(i));
+    const uint32_t g = galois_of_step(c, slot_step(offsets[i], ns));
+    if (g != 1 && !c->keys.count(g))
+      return fail(FESC_ERR_NO_KEY, "slot map needs the key of rotation " +
+                                       std::to_string(slot_step(offsets[i], ns)));
+  }
+  const size_t item = (2 * d.level + 4 * lo) * n;  // words per item
+  const uint32_t want = std::min(kSlotMapGroup, count);
+  if (p->bcap < want) {
+    (void)hipStreamSynchronize(s);  // earlier batches may still use the old workspace
+    (void)hipFree(p->bwork);
+    p->bcap = 0;
+    if (hipMalloc(&p->bwork, want * item * 8) != hipSuccess) {
+      p->bwork = nullptr;
+      return fail(FESC_ERR_OOM, "slot-map batch workspace");
+    }
+    p->bcap = want;
+  }
+  int err;
+  for (uint32_t b0 = 0; b0 < count; b0 += p->bcap) {
+    const uint32_t nb = std::min(p->bcap, count - b0);
+    std::vector<const uint64_t*> src(nb), rin;
+    std::vector<uint64_t*> rout, y0(nb), y1(nb);
+    std::vector<int32_t> rst;
+    for (uint32_t i = 0; i < nb; ++i) {
+      uint64_t* w = p->bwork + i * item;
+      y0[i] = w + 2 * d.level * n;
+      y1[i] = y0[i] + 2 * lo * n;
+      const int32_t off = slot_step(offsets[b0 + i], ns);
+      src[i] = ins[b0 + i];
+      if (off) {
+        rin.push_back(ins[b0 + i]);
+        rout.push_back(w);
+        rst.push_back(off);
+        src[i] = w;
+      }
+    }
+    if (!rst.empty() && (err = op_rotate_batch(c, (uint32_t)rst.size(), rin.data(), rst.data(),
+                                              rout.data(), nullptr, d.level, s, nullptr)))
+      return err;
+    for (uint32_t i = 0; i < nb; ++i)
+      if ((err = ptct_matvec(c, p->mv, &src[i], &y0[i], s))) return err;
+    if (d.rep_count == 1) {
+      for (uint32_t i = 0; i < nb; ++i)
+        if ((err = hip_check(hipMemcpyAsync(outs[b0 + i], y0[i], 2 * lo * n * 8,
+                                            hipMemcpyDeviceToDevice, s), "slot-map copy")))
+          return err;
+      continue;
+    }
+    std::vector<uint64_t*>* cur = &y0;
+    std::vector<uint64_t*>* nxt = &y1;
+    for (uint32_t r = 1; r < d.rep_count; r *= 2) {
+      const std::vector<int32_t> st(nb, slot_step(-(int64_t)r * d.rep_stride, ns));
+      std::vector<const uint64_t*> a(cur->begin(), cur->end());
+      std::vector<uint64_t*> dst = 2 * r == d.rep_count
+                                       ? std::vector<uint64_t*>(outs + b0, outs + b0 + nb)
+                                       : *nxt;
+      if ((err = op_rotate_batch(c, nb, a.data(), st.data(), dst.data(), a.data(), (uint32_t)lo,
+                                 s, nullptr)))
+        return err;
+      std::swap(cur, nxt);
+    }
+  }
+  return FESC_OK;
+}
+
 }  // namespace fesc
 
 extern "C" {
@@ -299,6 +384,14 @@ int fesc_slot_map(fesc_ctx* ctx, fesc_slot_map_plan* plan, const uint64_t* in, u
   if (!ctx || !plan || !in || !out) return fesc::fail(FESC_ERR_ARG, "null argument");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   return fesc::slot_map(ctx, plan, in, out, s);
+}
+
+int fesc_slot_map_batch(fesc_ctx* ctx, fesc_slot_map_plan* plan, uint32_t count,
+                        const uint64_t* const* ins, const int32_t* offsets,
+                        uint64_t* const* outs, void* stream) {
+  if (!ctx || !plan) return fesc::fail(FESC_ERR_ARG, "null argument");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  return fesc::slot_map_batch(ctx, plan, count, ins, offsets, outs, s);
 }
 
 }  // extern "C"

@@ -678,6 +678,9 @@ _lib.fesc_slot_map_plan_destroy.argtypes = [_vp]
 _lib.fesc_slot_map_plan_destroy.restype = None
 _lib.fesc_slot_map.argtypes = [_vp, _vp, _vp, _vp, _vp]
 _lib.fesc_slot_map.restype = ctypes.c_int
+_lib.fesc_slot_map_batch.argtypes = [_vp, _vp, _u32, ctypes.POINTER(_vp), ctypes.POINTER(_i32),
+                                     ctypes.POINTER(_vp), _vp]
+_lib.fesc_slot_map_batch.restype = ctypes.c_int
 
 
 def br_desc(log_n: int, H: int, P: int, G: int, d_s: int, c_state: int, kind: str, k: int,
@@ -720,6 +723,17 @@ class SlotMapPlan:
         c, d = self.ctx, self.desc
         _check(_lib.fesc_slot_map(c._h, self._h, _ptr(ct, c._ct(d.level), "ct"),
                                   _ptr(out, c._ct(d.level - 1), "out"), _stream(stream)))
+
+    def batch(self, cts, offsets, outs, stream=None):
+        """fesc_slot_map_batch: the map over several inputs, item i rotated
+        first by offsets[i]."""
+        c, d, m = self.ctx, self.desc, len(cts)
+        if len(offsets) != m:
+            raise ValueError(f"offsets: {len(offsets)} values, expected {m}")
+        _check(_lib.fesc_slot_map_batch(c._h, self._h, m, _ptrs(cts, m, c._ct(d.level), "cts"),
+                                        (_i32 * max(m, 1))(*offsets),
+                                        _ptrs(outs, m, c._ct(d.level - 1), "outs"),
+                                        _stream(stream)))
 
     def close(self):
         if getattr(self, "_h", None):

@@ -8,6 +8,8 @@ oracle:
   head (giant steps over heads with their own stride), and the output written
   over the input;
 * the device's mask slot vectors equal the oracle's exactly;
+* the batched map (several tokens under one plan, each with its own first
+  rotation) bit-exact against the oracle's map of each token;
 * at N = 2^16, 23 limbs and the Mamba-2 base shape (24 heads of 64, d_s = 128,
   128 channels per chunk), with masks generated and encoded on the device,
   every output decrypts to the plain broadcast within 2^-15 (a property that
@@ -98,6 +100,59 @@ def test_broadcast_small(log_n, L, alpha, D, kind, k, kappa, level):
         assert np.array_equal(zh[t], BR.mask_slots(M, ns, *divmod(t, M.n1))), f"mask {t}"
 
 
+BATCH_CASES = [(12, 6, 2, SHAPE_A, kind, 1, 6) for kind in ("x", "a", "B")] + [
+    (13, 5, 3, SHAPE_D, "a", 1, 5),
+    (12, 6, 2, SHAPE_B, "C", 0, 3),
+]
+
+
+@pytest.mark.parametrize("log_n,L,alpha,D,kind,kappa,level", BATCH_CASES,
+                         ids=[f"n{c[0]}-{c[4]}-c{c[5]}-H{c[3].H}G{c[3].G}-l{c[6]}"
+                              for c in BATCH_CASES])
+def test_broadcast_batch_small(log_n, L, alpha, D, kind, kappa, level):
+    """fesc_slot_map_batch over tokens 0, 1, 2 and 4 (token 0: an offset that
+    may be zero) under the plan of token 1, each item with its own offset:
+    every output bit-exact against the oracle's map of its own token, also
+    written over the inputs."""
+    P = C.params_small(log_n, 50, L, alpha)
+    ns = P.n // 2
+    toks = [0, 1, 2, 4]
+    ds = {k: F.br_desc(P.log_n, D.H, D.P, D.G, D.d_s, D.c_state, kind, k, kappa, level)
+          for k in toks}
+    Ms = {k: _oracle_map(d) for k, d in ds.items()}
+    rots = set()
+    for M in Ms.values():
+        rots |= BR.slot_map_rotations(M, ns)
+    S = Setup(P, 74, rot_steps=sorted(rots))
+    ql = float(P.q[level - 1])
+    M1 = Ms[1]
+    masks_o = {(p, q): C.encode_plain(P, BR.mask_slots(M1, ns, p, q), ql, level)
+               for p in range(M1.n2) for q in range(M1.n1)}
+    masks_d = [to_dev(masks_o[divmod(t, M1.n1)]) for t in range(M1.n)]
+    plan = F.SlotMapPlan(S.ctx, ds[1], masks_d)
+    cts_o, cts_d = [], []
+    for k in toks:
+        v = synth.normal(74, "bbv" + kind, ns, 1.0, k) + 1j * synth.normal(74, "bbw" + kind, ns,
+                                                                          1.0, k)
+        o, d = S.encrypt(v, 2.0 ** 40, level, 7400 + k)
+        cts_o.append(o)
+        cts_d.append(d)
+    outs = [torch.zeros((level - 1) * 2 * P.n, dtype=torch.int64, device="cuda") for _ in toks]
+    step(f"slot map batch {kind} log_n={log_n} kappa={kappa} tokens={toks}")
+    plan.batch(cts_d, [ds[k].offset for k in toks], outs)
+    wants = [BR.slot_map_ct(P, o, Ms[k], lambda p, q: masks_o[(p, q)], S.keys)
+             for k, o in zip(toks, cts_o)]
+    for k, out, want in zip(toks, outs, wants):
+        got = to_host(out).reshape(want.shape)
+        assert np.array_equal(got, want), f"{kind} token {k}: {first_mismatch(got, want)}"
+    step(f"slot map batch {kind} in place")
+    xs = [c.clone() for c in cts_d]
+    plan.batch(xs, [ds[k].offset for k in toks], xs)
+    for k, x, want in zip(toks, xs, wants):
+        got = to_host(x)[: want.size].reshape(want.shape)
+        assert np.array_equal(got, want), f"{kind} token {k} in place: {first_mismatch(got, want)}"
+
+
 def test_slot_map_errors():
     P = C.params_small(12, 50, 6, 2)
     S = Setup(P, 72)
@@ -126,6 +181,19 @@ def test_slot_map_errors():
     z = torch.empty((2, P.n // 2), dtype=torch.complex128, device="cuda")
     with pytest.raises(F.FescError, match="mask range"):
         F.slot_map_mask_slots(S.ctx, d, d.n1 * d.n2 - 1, 2, z)
+    # a batch whose offset has no key: refused before any launch
+    rots = BR.slot_map_rotations(_oracle_map(d), P.n // 2)
+    S2 = Setup(P, 72, rot_steps=sorted(rots))
+    plan = F.SlotMapPlan(S2.ctx, d, pts[:d.terms])
+    ct = torch.zeros(5 * 2 * P.n, dtype=torch.int64, device="cuda")
+    out = torch.full((4 * 2 * P.n,), 7, dtype=torch.int64, device="cuda")
+    keyless = next(o for o in range(1, P.n // 2) if o not in rots)
+    with pytest.raises(F.FescError) as ex:
+        plan.batch([ct, ct], [d.offset, keyless], [out, out])
+    assert ex.value.code == -3
+    assert bool((out == 7).all())
+    with pytest.raises(F.FescError):
+        plan.batch([], [], [])
 
 
 def test_broadcast_full_size():
