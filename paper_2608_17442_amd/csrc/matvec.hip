@@ -399,19 +399,45 @@ int ptct_matvec(Context* c, fesc_matvec_plan* p, const uint64_t* const* in,
       return err;
   }
   HIPCK(hipEventRecord(p->ev[2], s));
-  // giant steps: y_b += Phi^(p n1)(c~_{b,p}), one batch over b per p
+  // giant steps: y_b = sum_p Phi^(p n1)(c~_{b,p}).  One giant step: one batch
+  // over b with the sum folded into the key switch's combine.  More: every
+  // rotation of every (b, p >= 1) in one batch, in place, then the sums (the
+  // same residues: the rotations do not depend on the partial sums, and the
+  // additions are exact mod q)
   std::vector<const uint64_t*> gin(d.n_out);
   std::vector<uint64_t*> gout(d.n_out);
   std::vector<int32_t> gst(d.n_out);
-  for (uint32_t g = 1; g < d.n2; ++g) {
+  if (d.n2 == 2) {
     for (uint32_t b = 0; b < d.n_out; ++b) {
-      gin[b] = ct + ((size_t)b * d.n2 + g) * W;
+      gin[b] = ct + ((size_t)b * d.n2 + 1) * W;
       gout[b] = ct + (size_t)b * d.n2 * W;
-      gst[b] = (int32_t)(((int64_t)g * p->giant) % (c->n / 2));
+      gst[b] = (int32_t)(p->giant % (c->n / 2));
     }
     if ((err = op_rotate_batch(c, d.n_out, gin.data(), gst.data(), gout.data(),
                                (const uint64_t* const*)gout.data(), level, s)))
       return err;
+  } else if (d.n2 > 2) {
+    std::vector<const uint64_t*> rin;
+    std::vector<uint64_t*> rout;
+    std::vector<int32_t> rst;
+    for (uint32_t b = 0; b < d.n_out; ++b)
+      for (uint32_t g = 1; g < d.n2; ++g) {
+        uint64_t* cg = ct + ((size_t)b * d.n2 + g) * W;
+        rin.push_back(cg);
+        rout.push_back(cg);
+        rst.push_back((int32_t)(((int64_t)g * p->giant) % (c->n / 2)));
+      }
+    // in place: each job's c0 addend is read by the inner product and its c1
+    // by the ModUp, both before the combine writes the job's output (rotation
+    // jobs fold their addend, so the combine reads neither)
+    if ((err = op_rotate_batch(c, (uint32_t)rin.size(), rin.data(), rst.data(), rout.data(),
+                               nullptr, level, s)))
+      return err;
+    for (uint32_t b = 0; b < d.n_out; ++b) {
+      uint64_t* y = ct + (size_t)b * d.n2 * W;
+      for (uint32_t g = 1; g < d.n2; ++g)
+        HIPCK(k_binary_launch(c, y, y + (size_t)g * W, y, 2 * level, 1, 0, s));
+    }
   }
   // real extraction: t_b = conj(y_b) + y_b, one batch
   std::vector<uint64_t*> res(d.n_out);
