@@ -35,6 +35,12 @@ struct fesc_matvec_plan {
   const uint64_t* bank = nullptr;     // tiled diagonal bank (instead of the table), or null
   int64_t giant = 0;                  // rotation per giant step (n1 unit unless given)
   hipEvent_t ev[4] = {};               // phase marks of the last run
+  // several independent vectors at once (ptct_matvec_many): per vector baby
+  // [n1] and c~ [n2] cts, with device tables of their pointers; mcap vectors
+  uint64_t* mwork = nullptr;
+  const uint64_t** d_mbaby = nullptr;
+  uint64_t** d_mct = nullptr;
+  uint32_t mcap = 0;
 };
 
 namespace fesc {
@@ -327,6 +333,9 @@ void matvec_plan_destroy(fesc_matvec_plan* p) {
   (void)hipFree(p->d_diag);
   (void)hipFree(p->d_baby);
   (void)hipFree(p->d_ct);
+  (void)hipFree(p->mwork);
+  (void)hipFree(p->d_mbaby);
+  (void)hipFree(p->d_mct);
   for (auto& e : p->ev)
     if (e) (void)hipEventDestroy(e);
   delete p;
@@ -476,6 +485,134 @@ int ptct_matvec(Context* c, fesc_matvec_plan* p, const uint64_t* const* in,
       HIPCK(hipMemcpyAsync(out[b], res[b], W * 8, hipMemcpyDeviceToDevice, s));
   }
   HIPCK(hipEventRecord(p->ev[3], s));
+  return FESC_OK;
+}
+
+// The plan's projection of `count` independent vectors (plans with one input
+// and one output block, no extraction, no double hoisting): vector v's
+// ciphertext in[v] -> out[v], the same residues as ptct_matvec on each.  Up
+// to kMaxBatch vectors at a time share the launches: one ModUp launch for all
+// of them and their baby steps batched with jobs of one rotation under one
+// key, one pt-MAC per vector, every giant-step rotation in one batch, one
+// batched rescale.
+int ptct_matvec_many(Context* c, fesc_matvec_plan* p, uint32_t count, const uint64_t* const* in,
+                     uint64_t* const* out, hipStream_t s) {
+  const fesc_matvec_desc& d = p->d;
+  if (d.n_in != 1 || d.n_out != 1 || d.lazy_moddown || d.real_extract || d.complex_pair)
+    return fail(FESC_ERR_ARG, "batched projection: one input and one output block, "
+                              "no extraction, no double hoisting");
+  if (!count) return FESC_OK;
+  const uint32_t level = d.level, n1 = d.n1, n2 = d.n2;
+  const size_t W = p->ct_words, n = c->n, per = (size_t)n1 + n2;
+  int err;
+  const uint32_t want = std::min<uint32_t>(count, kMaxBatch);
+  if (p->mcap < want) {
+    (void)hipStreamSynchronize(s);  // earlier calls may still use the old workspace
+    (void)hipFree(p->mwork);
+    (void)hipFree(p->d_mbaby);
+    (void)hipFree(p->d_mct);
+    p->mwork = nullptr;
+    p->d_mbaby = nullptr;
+    p->d_mct = nullptr;
+    p->mcap = 0;
+    std::vector<const uint64_t*> baby((size_t)want * n1);
+    std::vector<uint64_t*> cts((size_t)want * n2);
+    bool ok = hipMalloc(&p->mwork, want * per * W * 8) == hipSuccess &&
+              hipMalloc(&p->d_mbaby, baby.size() * sizeof(void*)) == hipSuccess &&
+              hipMalloc(&p->d_mct, cts.size() * sizeof(void*)) == hipSuccess;
+    if (ok) {
+      for (size_t v = 0; v < want; ++v) {
+        for (size_t q = 0; q < n1; ++q) baby[v * n1 + q] = p->mwork + (v * per + q) * W;
+        for (size_t g = 0; g < n2; ++g) cts[v * n2 + g] = p->mwork + (v * per + n1 + g) * W;
+      }
+      ok = hipMemcpy(p->d_mbaby, baby.data(), baby.size() * sizeof(void*),
+                     hipMemcpyHostToDevice) == hipSuccess &&
+           hipMemcpy(p->d_mct, cts.data(), cts.size() * sizeof(void*), hipMemcpyHostToDevice) ==
+               hipSuccess;
+    }
+    if (!ok) {
+      (void)hipFree(p->mwork);
+      (void)hipFree(p->d_mbaby);
+      (void)hipFree(p->d_mct);
+      p->mwork = nullptr;
+      p->d_mbaby = nullptr;
+      p->d_mct = nullptr;
+      return fail(FESC_ERR_OOM, "batched projection workspace");
+    }
+    p->mcap = want;
+  }
+  auto baby_of = [&](uint32_t v, uint32_t q) { return p->mwork + ((size_t)v * per + q) * W; };
+  auto ct_of = [&](uint32_t v, uint32_t g) { return p->mwork + ((size_t)v * per + n1 + g) * W; };
+  for (uint32_t b0 = 0; b0 < count; b0 += p->mcap) {
+    const uint32_t nb = std::min(p->mcap, count - b0);
+    // baby steps
+    std::vector<KsSource> srcs;
+    std::vector<KsJob> jobs;
+    for (uint32_t v = 0; v < nb; ++v) {
+      const uint64_t* x = in[b0 + v];
+      for (uint32_t q = 0; q < n1; ++q) {
+        const uint32_t g = galois_of_step(c, (int32_t)(((int64_t)q * d.unit) % (c->n / 2)));
+        if (g == 1) {
+          HIPCK(hipMemcpyAsync(baby_of(v, q), x, W * 8, hipMemcpyDeviceToDevice, s));
+          continue;
+        }
+        jobs.push_back(KsJob{v, c->keys.at(g), g, x, 1u, g, nullptr, baby_of(v, q)});
+      }
+      srcs.push_back(KsSource{x + n, 2 * n});
+    }
+    if ((err = key_switch_batch(c, level, srcs, jobs, s, 0, nullptr, false))) return err;
+    // pt-MAC per vector
+    const uint32_t rows = diag_rows(c, d);
+    const PtLayout lay{2 * (uint32_t)n, (uint32_t)n, level, c->L};
+    const dim3 grid((c->n / kThreads) * rows * ((n2 + kGroup - 1) / kGroup));
+    for (uint32_t v = 0; v < nb; ++v) {
+      if (p->bank)
+        hipLaunchKernelGGL((k_ptmac<kGroup, true>), grid, dim3(kThreads), 0, s,
+                           p->d_mbaby + (size_t)v * n1, (const uint64_t* const*)nullptr, p->bank,
+                           p->d_mct + (size_t)v * n2, n2, n1, c->n, rows, c->d_pk, lay);
+      else
+        hipLaunchKernelGGL((k_ptmac<kGroup, false>), grid, dim3(kThreads), 0, s,
+                           p->d_mbaby + (size_t)v * n1, p->d_diag, (const uint64_t*)nullptr,
+                           p->d_mct + (size_t)v * n2, n2, n1, c->n, rows, c->d_pk, lay);
+      HIPCK(hipGetLastError());
+    }
+    // giant steps (as in ptct_matvec)
+    std::vector<const uint64_t*> gin;
+    std::vector<uint64_t*> gout;
+    std::vector<int32_t> gst;
+    if (n2 == 2) {
+      for (uint32_t v = 0; v < nb; ++v) {
+        gin.push_back(ct_of(v, 1));
+        gout.push_back(ct_of(v, 0));
+        gst.push_back((int32_t)(p->giant % (c->n / 2)));
+      }
+      if ((err = op_rotate_batch(c, nb, gin.data(), gst.data(), gout.data(),
+                                 (const uint64_t* const*)gout.data(), level, s)))
+        return err;
+    } else if (n2 > 2) {
+      for (uint32_t v = 0; v < nb; ++v)
+        for (uint32_t g = 1; g < n2; ++g) {
+          gin.push_back(ct_of(v, g));
+          gout.push_back(ct_of(v, g));
+          gst.push_back((int32_t)(((int64_t)g * p->giant) % (c->n / 2)));
+        }
+      // in place, as in ptct_matvec
+      if ((err = op_rotate_batch(c, (uint32_t)gin.size(), gin.data(), gst.data(), gout.data(),
+                                 nullptr, level, s)))
+        return err;
+      for (uint32_t v = 0; v < nb; ++v)
+        for (uint32_t g = 1; g < n2; ++g)
+          HIPCK(k_binary_launch(c, ct_of(v, 0), ct_of(v, g), ct_of(v, 0), 2 * level, 1, 0, s));
+    }
+    std::vector<uint64_t*> res(nb);
+    for (uint32_t v = 0; v < nb; ++v) res[v] = ct_of(v, 0);
+    if (d.rescale) {
+      if ((err = op_rescale_many(c, nb, res.data(), out + b0, level, s))) return err;
+    } else {
+      for (uint32_t v = 0; v < nb; ++v)
+        HIPCK(hipMemcpyAsync(out[b0 + v], res[v], W * 8, hipMemcpyDeviceToDevice, s));
+    }
+  }
   return FESC_OK;
 }
 

@@ -36,6 +36,8 @@ namespace fesc {
 int matvec_plan_create(Context* c, const fesc_matvec_desc* d, const uint64_t* const* diags,
                        const uint64_t* bank, fesc_matvec_plan** out, int64_t giant_unit);
 void matvec_plan_destroy(fesc_matvec_plan* p);
+int ptct_matvec_many(Context* c, fesc_matvec_plan* p, uint32_t count, const uint64_t* const* in,
+                     uint64_t* const* out, hipStream_t s);
 int ptct_matvec(Context* c, fesc_matvec_plan* p, const uint64_t* const* in,
                 uint64_t* const* out, hipStream_t s);
 
@@ -278,9 +280,9 @@ int slot_map(Context* c, fesc_slot_map_plan* p, const uint64_t* in, uint64_t* ou
 constexpr uint32_t kSlotMapGroup = 16;
 
 // The plan's map for `count` inputs with their own first rotations: the
-// offset rotations of a group share one key-switch launch, the step-2 sums run
-// per item, and every doubling is one launch over the group, all its jobs
-// under one key.
+// offset rotations of a group share one key-switch launch, the step-2 sums of
+// the group run as one batched projection (ptct_matvec_many), and every
+// doubling is one launch over the group, all its jobs under one key.
 int slot_map_batch(Context* c, fesc_slot_map_plan* p, uint32_t count, const uint64_t* const* ins,
                    const int32_t* offsets, uint64_t* const* outs, hipStream_t s) {
   if (!ins || !offsets || !outs) return fail(FESC_ERR_ARG, "null argument");
@@ -329,8 +331,7 @@ int slot_map_batch(Context* c, fesc_slot_map_plan* p, uint32_t count, const uint
     if (!rst.empty() && (err = op_rotate_batch(c, (uint32_t)rst.size(), rin.data(), rst.data(),
                                               rout.data(), nullptr, d.level, s, nullptr)))
       return err;
-    for (uint32_t i = 0; i < nb; ++i)
-      if ((err = ptct_matvec(c, p->mv, &src[i], &y0[i], s))) return err;
+    if ((err = ptct_matvec_many(c, p->mv, nb, src.data(), y0.data(), s))) return err;
     if (d.rep_count == 1) {
       for (uint32_t i = 0; i < nb; ++i)
         if ((err = hip_check(hipMemcpyAsync(outs[b0 + i], y0[i], 2 * lo * n * 8,
