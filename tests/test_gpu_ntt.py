@@ -133,6 +133,48 @@ def test_ntt_large_strided_batches(batch, limbs, gap):
         assert np.array_equal(got[o:o + n], want), (b, i, first_mismatch(got[o:o + n], want))
 
 
+def test_ntt_maximum_launch_sizes():
+    """The largest launches the entry points take: N = 2^12 with the maximum
+    batch of 65,535 single-limb rows (2.1 GB; rows 0, 32,767 and 65,534
+    against the oracle, the whole batch by its round trip), N = 2^16 with every
+    prime of the extended basis in one batch element (32 limbs, against the
+    oracle row by row), and one row past the batch limit refused before any
+    launch."""
+    from paper_2608_17442_amd import fesc as F
+    P = C.params_small(12, 50, 3, 1)
+    ctx = _ctx(P)
+    n, batch, q = P.n, 65535, P.q[0]
+    gen = torch.Generator(device="cuda").manual_seed(11)
+    d = torch.randint(0, q, (batch * n,), generator=gen, device="cuda", dtype=torch.int64)
+    orig = d.clone()
+    step(f"ntt_fwd batch={batch} x 2^12")
+    ctx.ntt_fwd(d, batch, n, 1, n, 0)
+    for b in (0, 32767, batch - 1):
+        a = orig[b * n:(b + 1) * n].cpu().numpy().view(np.uint64)
+        g = d[b * n:(b + 1) * n].cpu().numpy().view(np.uint64)
+        want = C.ntt(P, a[None], [q])[0]
+        assert np.array_equal(g, want), (b, first_mismatch(g, want))
+    step("ntt_inv (round trip)")
+    ctx.ntt_inv(d, batch, n, 1, n, 0)
+    assert torch.equal(d, orig)
+    with pytest.raises(F.FescError) as e:
+        ctx.ntt_fwd(d, batch + 1, 0, 1, n, 0)
+    assert e.value.code == -1
+    del d, orig
+    P = C.params_p16()
+    ctx = _ctx(P)
+    mods = P.ext(P.L)
+    a = np.stack([synth.uniform_residues(12, "ntt-max", mods, P.n)])
+    dv = to_dev(a)
+    step(f"ntt_fwd 2^16 x {len(mods)} limbs (the whole extended basis)")
+    ctx.ntt_fwd(dv, 1, 0, len(mods), P.n, 0)
+    got = to_host(dv).reshape(len(mods), P.n)
+    want = C.ntt(P, a[0], mods)
+    assert np.array_equal(got, want), first_mismatch(got, want)
+    ctx.ntt_inv(dv, 1, 0, len(mods), P.n, 0)
+    assert np.array_equal(to_host(dv).reshape(len(mods), P.n), a[0])
+
+
 def test_bad_prime_range_is_rejected_before_launch():
     from paper_2608_17442_amd import fesc as F
     P = C.params_small(12, 50, 2, 1)
