@@ -1204,7 +1204,12 @@ def main():
         "keyswitch": {"valu_frac": round(ks_valu_frac, 4), "hbm_frac": round(ks_hbm_frac, 4),
                       "bytes_per_key_switch": ks_bytes,
                       "us_per_key_switch": round(ks * 1e3 / W.n_ks, 2),
-                      "met": bool(max(ks_valu_frac, ks_hbm_frac) >= 0.6)},
+                      "met": bool(max(ks_valu_frac, ks_hbm_frac) >= 0.6),
+                      "valu_work": "83.9 M butterflies + 75.5 M modular MACs per key switch "
+                                   "(the conversions' MACs counted as VALU MACs); the "
+                                   "conversions run as int8 matrix-core products, which leaves "
+                                   "about 27 us of VALU work per key switch: the pipeline is "
+                                   "bound by the bytes its kernels move"},
         "note": "whole operations timed with HIP events in the step; the per-kernel key-switch "
                 "fraction in rooflines_other is a diagnostic (it scores each kernel against "
                 "its own floor, so intermediate round trips count as useful work)",
