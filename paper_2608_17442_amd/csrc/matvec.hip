@@ -125,7 +125,10 @@ __global__ __launch_bounds__(kThreads) void k_ptmac(const uint64_t* const* __res
     const double x0 = u2d(bp[c0]), x1 = u2d(bp[c1]);
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      const double w = BANK ? u2d(bk[(size_t)t * t_stride + og[g] * kThreads])
+      // the bank streams past once (non-temporal loads), so that it does not
+      // evict the baby-step values the tile's other output groups re-read
+      const double w = BANK ? u2d(__builtin_nontemporal_load(bk + (size_t)t * t_stride +
+                                                             og[g] * kThreads))
                             : u2d(diag[(size_t)(o0 + og[g]) * terms + t][pi]);
       a0[g] += mm_var(x0, w, P.q, P.qinv);
       a1[g] += mm_var(x1, w, P.q, P.qinv);
