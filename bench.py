@@ -1276,7 +1276,8 @@ def main():
         "targets": targets,
         "rooflines_other": {
             "hbm_measured_ceilings": dict(hbm, note="fesc_calib_hbm: a streaming read with "
-                                          "16-byte loads and a 16-byte copy (read + write), "
+                                          "16-byte non-temporal loads and a 16-byte copy "
+                                          "(read + write), "
                                           "8 GiB each; the practical ceilings of HBM-bound "
                                           "kernels on this device, against the 8 TB/s peak"),
             "ntt_valu": {"bound": "alu",

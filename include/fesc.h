@@ -714,7 +714,8 @@ int fesc_calib_valu(fesc_ctx* ctx, int kind, uint32_t iters, double* rate, void*
 
 /* Measurement helper, not part of the method: the device's practical HBM
  * ceilings for streaming kernels.  kind FESC_CALIB_HBM_READ: every 16-byte
- * word of a `bytes` buffer read once; FESC_CALIB_HBM_COPY: a `bytes` buffer
+ * word of a `bytes` buffer read once (non-temporal loads, as the read-once
+ * kernels use); FESC_CALIB_HBM_COPY: a `bytes` buffer
  * copied (read plus write).  *rate = bytes moved per second (2 * bytes per
  * copy).  Allocates and frees its buffers (bytes, and bytes or a small
  * output) and synchronises `stream`; FESC_ERR_ARG for an unknown kind or a

@@ -141,8 +141,10 @@ __global__ __launch_bounds__(kThreads) void k_calib_read(const ulonglong2* __res
                                                          size_t words2, uint64_t* __restrict__ out) {
   const size_t t = (size_t)blockIdx.x * kThreads + threadIdx.x, nt = (size_t)gridDim.x * kThreads;
   uint64_t x = 0;
+  typedef unsigned long long u64x2 __attribute__((ext_vector_type(2)));
   for (size_t i = t; i < words2; i += nt) {
-    const ulonglong2 v = src[i];
+    // streaming (non-temporal) loads, as the read-once kernels use
+    const u64x2 v = __builtin_nontemporal_load(reinterpret_cast<const u64x2*>(src) + i);
     x ^= v.x ^ v.y;
   }
   out[t] = x;

@@ -9,9 +9,12 @@ namespace {
 
 constexpr int kThreads = 256;
 
+typedef unsigned long long u64x2 __attribute__((ext_vector_type(2)));
+
 // V coefficients per thread, as V/2 16-byte loads per operand and pair; load
 // i of thread t covers coefficients 2(i kThreads + t) and the next, so each load
 // instruction of a wave reads one contiguous 1 KiB run.
+
 template <int V>
 __global__ __launch_bounds__(kThreads) void k_mac(const uint64_t* __restrict__ a,
                                                   const uint64_t* __restrict__ b,
@@ -29,11 +32,13 @@ __global__ __launch_bounds__(kThreads) void k_mac(const uint64_t* __restrict__ a
   for (int v = 0; v < V; ++v) acc[v] = 0.0;
 #pragma unroll 4
   for (uint32_t j = 0; j < pairs; ++j) {
-    const ulonglong2* pa = reinterpret_cast<const ulonglong2*>(a + j * pair_stride + off);
-    const ulonglong2* pb = reinterpret_cast<const ulonglong2*>(b + j * pair_stride + off);
+    // every operand is read once: streaming (non-temporal) loads
+    const u64x2* pa = reinterpret_cast<const u64x2*>(a + j * pair_stride + off);
+    const u64x2* pb = reinterpret_cast<const u64x2*>(b + j * pair_stride + off);
 #pragma unroll
     for (int v = 0; v < V; v += 2) {
-      const ulonglong2 va = pa[v / 2 * kThreads], vb = pb[v / 2 * kThreads];
+      const u64x2 va = __builtin_nontemporal_load(pa + v / 2 * kThreads);
+      const u64x2 vb = __builtin_nontemporal_load(pb + v / 2 * kThreads);
       acc[v] = red_bal(acc[v] + mm_var(u2d(va.x), u2d(vb.x), q, qinv), q, qinv);
       acc[v + 1] = red_bal(acc[v + 1] + mm_var(u2d(va.y), u2d(vb.y), q, qinv), q, qinv);
     }
