@@ -14,7 +14,8 @@ Metric (three workloads, all N = 2^16 with ~50-bit primes = 1 mod 2N; the
          features (N(0,1)) packed as 12 complex-paired ciphertexts at 16 limbs,
          BSGS n1 = 16, n2 = 2 over 32 segments of 1024 slots, complex-paired
          outputs and rescale -> 24 ciphertexts carrying the 48 output blocks
-         (seed 3); 18,432 pre-encoded diagonals (154.6 GB) resident in HBM.
+         (seed 3); 18,432 pre-encoded diagonals resident in HBM (a 120.8 GB
+         bank: 50 bits per residue).
 
   SCAN   scan-contract slice of a block of 16 distinct Mamba-base tokens (24
          heads x 64 channels x d_state 128 in 12 state chunks of 16,384 slots,
@@ -550,8 +551,8 @@ def matvec_double_hoisting(F, torch, np) -> dict:
     on the diagonal-method workload (N = 2^12, 64 x 64, 63 hoisted rotations)
     and on the 768 x 1536 shape (N = 2^16, 16 limbs, complex-paired outputs,
     tiled bank).  The modular arithmetic does not depend on the values, so
-    diagonals and inputs are uniform residues; the two 2^16 banks (154.6 and
-    231.9 GB) are built one after the other."""
+    diagonals and inputs are uniform residues; the two 2^16 banks (120.8 and
+    181.2 GB at 50 bits per residue) are built one after the other."""
     import synth
     import synth.workloads as WL
 

@@ -329,15 +329,25 @@ void fesc_matvec_plan_destroy(fesc_matvec_plan* plan);
 int fesc_ptct_matvec(fesc_ctx* ctx, fesc_matvec_plan* plan, const uint64_t* const* in,
                      uint64_t* const* out, void* stream);
 
-/* Diagonal bank: the same diagonals in one device buffer tiled for
- * streaming, [limb][N/256][n_out*n2][n_in*n1][256] (256-coefficient tiles;
- * one workgroup of the plaintext MAC then reads a contiguous region).
- * fesc_matvec_bank_words gives its size in uint64 words (level*N per
- * diagonal, (level+alpha)*N with lazy_moddown); fesc_matvec_bank_pack copies
- * plaintext `pt` ([level][N], or [level+alpha][N]) into
- * slot `index` = ((b*n2 + p)*n_in + u)*n1 + q of the bank; a plan created
- * from a bank reads it instead of a pointer table (results are identical).
- * The bank must stay valid for the plan's lifetime. */
+/* Diagonal bank: the same diagonals in one device buffer laid out for
+ * streaming, each residue in 50 bits (every prime is below 2^50).  With
+ * O = n_out*n2 outputs (b, p) and T = n_in*n1 terms (u, q), the buffer holds
+ * 32-bit words [limb][N/256][T][O + ceil(O/2) + ceil(O/16)][256]: per
+ * 256-coefficient tile and term, O planes of the residues' low 32 bits, then
+ * ceil(O/2) planes holding bits 32..47 of outputs 2j (low half) and 2j+1
+ * (high half), then ceil(O/16) planes holding bits 48..49 of output o at bit
+ * 2 (o mod 16).  One workgroup of the plaintext MAC then reads contiguous
+ * runs, 6.25 bytes per residue instead of 8.
+ * fesc_matvec_bank_words gives its size in uint64 words (level*N*T*(O +
+ * ceil(O/2) + ceil(O/16))/2; level+alpha rows with lazy_moddown);
+ * fesc_matvec_bank_pack writes plaintext `pt` ([level][N], or
+ * [level+alpha][N]; canonical residues, as every encoder here produces) into
+ * slot `index` = ((b*n2 + p)*n_in + u)*n1 + q of the bank.  It touches only
+ * that diagonal's bits (shared words are updated with atomic AND / OR), so
+ * the bank needs no clearing and packs of different slots may run in any
+ * order or on different streams.  A plan created from a bank reads it
+ * instead of a pointer table (results are identical).  The bank must stay
+ * valid for the plan's lifetime. */
 int fesc_matvec_bank_words(const fesc_ctx* ctx, const fesc_matvec_desc* desc, size_t* words);
 int fesc_matvec_bank_pack(fesc_ctx* ctx, const fesc_matvec_desc* desc, uint64_t* bank,
                           uint32_t index, const uint64_t* pt, void* stream);

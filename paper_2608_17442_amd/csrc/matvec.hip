@@ -14,7 +14,10 @@
 // The pt-MAC streams every plaintext diagonal once.  A thread owns one
 // coefficient of one limb and accumulates G outputs (b, p) at a time, so each
 // baby-step value it loads is reused G times; the diagonals are read with
-// coalesced 8-byte loads and nothing else is written until the final sums.
+// coalesced loads and nothing else is written until the final sums.  Every
+// prime is below 2^50, so a diagonal bank stores each residue in 50 bits
+// (6.25 bytes instead of 8) as three word planes: the low 32 bits, bits
+// 32..47 (two outputs per word) and bits 48..49 (16 outputs per word).
 #include <string>
 #include <vector>
 
@@ -32,7 +35,7 @@ struct fesc_matvec_plan {
   const uint64_t** d_baby = nullptr;  // device table of baby pointers (pt-MAC inputs)
   uint64_t** d_ct = nullptr;          // device table of c~ pointers (pt-MAC outputs)
   size_t ct_words = 0;
-  const uint64_t* bank = nullptr;     // tiled diagonal bank (instead of the table), or null
+  const uint32_t* bank = nullptr;     // diagonal bank (instead of the table), or null
   int64_t giant = 0;                  // rotation per giant step (n1 unit unless given)
   hipEvent_t ev[4] = {};               // phase marks of the last run
   // several independent vectors at once (ptct_matvec_many): per vector baby
@@ -56,17 +59,38 @@ namespace {
 
 constexpr int kThreads = 256;  // also the coefficient tile of the diagonal bank
 constexpr int kGroup = 16;     // outputs accumulated per thread
+static_assert(kGroup % 16 == 0, "an output group covers whole top-bit words");
 
-// Diagonal (o, t) of a bank: tiles of kThreads coefficients, ordered
-// [limb][tile][term][output][coefficient]: for each term a workgroup reads
-// its G outputs' tiles as one contiguous G * 2 KB run, and the output groups
-// of one tile (kept on one XCD, adjacent in time) sweep one contiguous
-// terms * outputs * 2 KB region together.
-__host__ __device__ __forceinline__ size_t bank_offset(uint32_t i, uint32_t tile, uint32_t o,
-                                                       uint32_t t, uint32_t n,
-                                                       uint32_t n_outputs, uint32_t terms) {
+// Diagonal bank.  For each (limb i, tile of kThreads coefficients, term t) a
+// record of bank_record_words(n_outputs) 32-bit words per coefficient, laid
+// out as planes of kThreads words (coefficient-minor, so every plane load is
+// coalesced):
+//   plane o                          bits 0..31 of output o's residue
+//   plane n_outputs + o/2            bits 32..47 of outputs 2j, 2j+1 (low, high half)
+//   plane n_outputs + H + o/16       bits 48..49 of output o at bit 2 (o mod 16)
+// with H = ceil(n_outputs / 2).  Records are ordered [limb][tile][term]: a
+// workgroup reads its G outputs' planes of a term as three contiguous runs, and
+// the output groups of one tile (kept on one XCD, adjacent in time) sweep one
+// contiguous terms-long region together.
+__host__ __device__ __forceinline__ uint32_t bank_hi_planes(uint32_t n_outputs) {
+  return (n_outputs + 1) / 2;
+}
+__host__ __device__ __forceinline__ uint32_t bank_record_words(uint32_t n_outputs) {
+  return n_outputs + bank_hi_planes(n_outputs) + (n_outputs + 15) / 16;
+}
+// first word of record (i, tile, t)
+__host__ __device__ __forceinline__ size_t bank_record(uint32_t i, uint32_t tile, uint32_t t,
+                                                       uint32_t n, uint32_t n_outputs,
+                                                       uint32_t terms) {
   const size_t tiles = n / kThreads;
-  return ((((size_t)i * tiles + tile) * terms + t) * n_outputs + o) * kThreads;
+  return (((size_t)i * tiles + tile) * terms + t) * bank_record_words(n_outputs) * kThreads;
+}
+
+// Residue from its three bank fields: an exact fp64 integer below 2^50.
+__device__ __forceinline__ double bank_value(uint32_t lo, uint32_t hi_word, uint32_t hi_shift,
+                                             uint32_t top_word, uint32_t top_shift) {
+  const uint32_t hi = ((hi_word >> hi_shift) & 0xFFFFu) | (((top_word >> top_shift) & 3u) << 16);
+  return __hiloint2double((int)(hi | 0x43300000u), (int)lo) - kTwo52;
 }
 
 // BANK: diagonals from a tiled bank; otherwise from the table of plaintexts.
@@ -77,10 +101,17 @@ struct PtLayout {
   uint32_t row_stride, comp_stride, split, prime1;
 };
 
+// Device memory seen through a pointer read from a table: the cast tells the
+// compiler the address is global, so it emits global (not flat) loads and
+// stores, whose completions it can count in order; flat loads would make it
+// drain every outstanding load before the first use of each one.
+typedef __attribute__((address_space(1))) const uint64_t gcu64;
+typedef __attribute__((address_space(1))) uint64_t gu64;
+
 template <int G, bool BANK>
 __global__ __launch_bounds__(kThreads) void k_ptmac(const uint64_t* const* __restrict__ baby,
                                                     const uint64_t* const* __restrict__ diag,
-                                                    const uint64_t* __restrict__ bank,
+                                                    const uint32_t* __restrict__ bank,
                                                     uint64_t* const* __restrict__ outs,
                                                     uint32_t n_outputs, uint32_t terms,
                                                     uint32_t n, uint32_t limbs,
@@ -111,27 +142,52 @@ __global__ __launch_bounds__(kThreads) void k_ptmac(const uint64_t* const* __res
   for (int g = 0; g < G; ++g) a0[g] = a1[g] = 0.0;
   const size_t pi = (size_t)i * n + k, c0 = (size_t)i * lay.row_stride + k,
                c1 = c0 + lay.comp_stride;
-  const uint64_t* bk =
-      BANK ? bank + bank_offset(i, tile, o0, 0, n, n_outputs, terms) + threadIdx.x : nullptr;
-  const size_t t_stride = (size_t)n_outputs * kThreads;
   // Outputs past the end of a partial group re-read the group's last valid
   // diagonal (results discarded at the store), which keeps the loop body free
-  // of branches so the G loads of a term are issued together.
+  // of branches so the loads of a term are issued together.
   uint32_t og[G];
 #pragma unroll
   for (int g = 0; g < G; ++g) og[g] = min((uint32_t)g, g_end - 1);
+  // bank: this thread's words of record (i, tile, 0); the planes of the group
+  const uint32_t* bk =
+      BANK ? bank + bank_record(i, tile, 0, n, n_outputs, terms) + threadIdx.x : nullptr;
+  const size_t rec_stride = (size_t)bank_record_words(n_outputs) * kThreads;
+  const uint32_t hi_plane = n_outputs, top_plane = n_outputs + bank_hi_planes(n_outputs);
   for (uint32_t t = 0; t < terms; ++t) {
-    const uint64_t* bp = baby[t];
+    const gcu64* bp = (const gcu64*)baby[t];
     const double x0 = u2d(bp[c0]), x1 = u2d(bp[c1]);
+    double w[G];
+    if (BANK) {
+      // every bank word streams past once (non-temporal loads), so that the
+      // bank does not evict the baby-step values the tile's other output
+      // groups re-read
+      const uint32_t* rec = bk + (size_t)t * rec_stride;
+      uint32_t lo[G], hw[G / 2], tw[G / 16];
+#pragma unroll
+      for (int g = 0; g < G; ++g)
+        lo[g] = __builtin_nontemporal_load(rec + (size_t)(o0 + og[g]) * kThreads);
+#pragma unroll
+      for (int j = 0; j < G / 2; ++j)
+        hw[j] = __builtin_nontemporal_load(rec + (size_t)(hi_plane + ((o0 + og[2 * j]) >> 1)) *
+                                                     kThreads);
+#pragma unroll
+      for (int m = 0; m < G / 16; ++m)
+        tw[m] = __builtin_nontemporal_load(rec + (size_t)(top_plane + ((o0 + og[16 * m]) >> 4)) *
+                                                     kThreads);
+      // o0 is a multiple of 16: output o0 + og[g] sits at half og[g] & 1 of its
+      // hi word and at bit 2 (og[g] & 15) of its top word
+#pragma unroll
+      for (int g = 0; g < G; ++g)
+        w[g] = bank_value(lo[g], hw[g / 2], 16u * (og[g] & 1u), tw[g / 16], 2u * (og[g] & 15u));
+    } else {
+#pragma unroll
+      for (int g = 0; g < G; ++g)
+        w[g] = u2d(((const gcu64*)diag[(size_t)(o0 + og[g]) * terms + t])[pi]);
+    }
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      // the bank streams past once (non-temporal loads), so that it does not
-      // evict the baby-step values the tile's other output groups re-read
-      const double w = BANK ? u2d(__builtin_nontemporal_load(bk + (size_t)t * t_stride +
-                                                             og[g] * kThreads))
-                            : u2d(diag[(size_t)(o0 + og[g]) * terms + t][pi]);
-      a0[g] += mm_var(x0, w, P.q, P.qinv);
-      a1[g] += mm_var(x1, w, P.q, P.qinv);
+      a0[g] += mm_var(x0, w[g], P.q, P.qinv);
+      a1[g] += mm_var(x1, w[g], P.q, P.qinv);
     }
     if ((t & 3) == 3) {
 #pragma unroll
@@ -144,21 +200,33 @@ __global__ __launch_bounds__(kThreads) void k_ptmac(const uint64_t* const* __res
 #pragma unroll
   for (int g = 0; g < G; ++g) {
     if ((uint32_t)g < g_end) {
-      uint64_t* o = outs[o0 + g];
+      gu64* o = (gu64*)outs[o0 + g];
       o[c0] = to_res(a0[g], P.q, P.qinv);
       o[c1] = to_res(a1[g], P.q, P.qinv);
     }
   }
 }
 
-// bank tile (i, tile, o, t) <- plaintext limb i, coefficients of the tile
+// bank fields of diagonal (o, t) <- plaintext limb i, coefficients of the tile.
+// The hi and top words are shared with other outputs: each diagonal clears and
+// sets only its own bits with atomic AND / OR, so packs of different diagonals
+// may run in any order or concurrently.
 __global__ __launch_bounds__(kThreads) void k_bank_pack(const uint64_t* __restrict__ pt,
-                                                        uint64_t* __restrict__ bank, uint32_t o,
+                                                        uint32_t* __restrict__ bank, uint32_t o,
                                                         uint32_t t, uint32_t n,
                                                         uint32_t n_outputs, uint32_t terms) {
   const uint32_t i = blockIdx.y, tile = blockIdx.x;
-  bank[bank_offset(i, tile, o, t, n, n_outputs, terms) + threadIdx.x] =
-      pt[(size_t)i * n + (size_t)tile * kThreads + threadIdx.x];
+  const uint64_t v = pt[(size_t)i * n + (size_t)tile * kThreads + threadIdx.x];
+  uint32_t* rec = bank + bank_record(i, tile, t, n, n_outputs, terms) + threadIdx.x;
+  rec[(size_t)o * kThreads] = (uint32_t)v;
+  uint32_t* hw = rec + (size_t)(n_outputs + o / 2) * kThreads;
+  const uint32_t hs = 16u * (o & 1u);
+  atomicAnd(hw, ~(0xFFFFu << hs));
+  atomicOr(hw, (uint32_t)((v >> 32) & 0xFFFFu) << hs);
+  uint32_t* tw = rec + (size_t)(n_outputs + bank_hi_planes(n_outputs) + o / 16) * kThreads;
+  const uint32_t ts = 2u * (o & 15u);
+  atomicAnd(tw, ~(3u << ts));
+  atomicOr(tw, (uint32_t)((v >> 48) & 3u) << ts);
 }
 
 // Identity baby step over the extended basis: x[t][i] = P c_t[i] on the
@@ -285,7 +353,7 @@ int matvec_plan_create(Context* c, const fesc_matvec_desc* d, const uint64_t* co
   fesc_matvec_plan* p = new fesc_matvec_plan();
   p->d = *d;
   p->giant = giant;
-  p->bank = bank;
+  p->bank = reinterpret_cast<const uint32_t*>(bank);
   if (!bank) p->diag.assign(diags, diags + n_diag);
   p->ct_words = (size_t)2 * d->level * c->n;
   const size_t n_baby = (size_t)d->n_in * d->n1, n_ct = (size_t)d->n_out * d->n2;
@@ -399,7 +467,7 @@ int ptct_matvec(Context* c, fesc_matvec_plan* p, const uint64_t* const* in,
                        (uint32_t)n_baby, c->n, rows, c->d_pk, lay);
   else
     hipLaunchKernelGGL((k_ptmac<kGroup, false>), grid, dim3(kThreads), 0, s, p->d_baby,
-                       p->d_diag, (const uint64_t*)nullptr, p->d_ct, n_outputs,
+                       p->d_diag, (const uint32_t*)nullptr, p->d_ct, n_outputs,
                        (uint32_t)n_baby, c->n, rows, c->d_pk, lay);
   HIPCK(hipGetLastError());
   if (lazy) {
@@ -575,7 +643,7 @@ int ptct_matvec_many(Context* c, fesc_matvec_plan* p, uint32_t count, const uint
                            p->d_mct + (size_t)v * n2, n2, n1, c->n, rows, c->d_pk, lay);
       else
         hipLaunchKernelGGL((k_ptmac<kGroup, false>), grid, dim3(kThreads), 0, s,
-                           p->d_mbaby + (size_t)v * n1, p->d_diag, (const uint64_t*)nullptr,
+                           p->d_mbaby + (size_t)v * n1, p->d_diag, (const uint32_t*)nullptr,
                            p->d_mct + (size_t)v * n2, n2, n1, c->n, rows, c->d_pk, lay);
       HIPCK(hipGetLastError());
     }
@@ -634,8 +702,10 @@ int fesc_matvec_bank_words(const fesc_ctx* ctx, const fesc_matvec_desc* desc, si
   if (!ctx || !words) return fesc::fail(FESC_ERR_ARG, "null argument");
   int rc = fesc::check_desc(ctx, desc);
   if (rc) return rc;
-  *words = (size_t)desc->n_out * desc->n2 * desc->n_in * desc->n1 *
-           fesc::diag_rows(ctx, *desc) * ctx->n;
+  // 32-bit words: rows * N * terms * record words, an even count (N is even)
+  const uint32_t outputs = desc->n_out * desc->n2;
+  *words = (size_t)desc->n_in * desc->n1 * fesc::bank_record_words(outputs) *
+           fesc::diag_rows(ctx, *desc) * ctx->n / 2;
   return FESC_OK;
 }
 
@@ -648,8 +718,9 @@ int fesc_matvec_bank_pack(fesc_ctx* ctx, const fesc_matvec_desc* desc, uint64_t*
   if ((uint64_t)index >= (uint64_t)terms * outputs)
     return fesc::fail(FESC_ERR_ARG, "diagonal index out of range");
   hipLaunchKernelGGL(fesc::k_bank_pack, dim3(ctx->n / fesc::kThreads, fesc::diag_rows(ctx, *desc)),
-                     dim3(fesc::kThreads), 0, reinterpret_cast<hipStream_t>(stream), pt, bank,
-                     index / terms, index % terms, ctx->n, outputs, terms);
+                     dim3(fesc::kThreads), 0, reinterpret_cast<hipStream_t>(stream), pt,
+                     reinterpret_cast<uint32_t*>(bank), index / terms, index % terms, ctx->n,
+                     outputs, terms);
   return fesc::hip_check(hipGetLastError(), "bank_pack");
 }
 

@@ -55,11 +55,13 @@ def _run(P, S, desc, X_slots, scale_x, diag_slots, scale_d, seed_tag):
               for _ in range(desc.n_out // 2 if cp else desc.n_out)]
     step("matvec run")
     plan(ins_d, outs_d)
-    # the same diagonals through a tiled bank give the same residues
+    # the same diagonals through a diagonal bank give the same residues; the
+    # bank starts with every bit set and is packed in reverse order, so each
+    # diagonal must clear its own bits of the words it shares with others
     fd = F.matvec_desc(*args, cp, lazy)
-    bank = torch.zeros(F.matvec_bank_words(S.ctx, fd), dtype=torch.int64, device="cuda")
-    for t, pt in enumerate(flat):
-        F.matvec_bank_pack(S.ctx, fd, bank, t, pt)
+    bank = torch.full((F.matvec_bank_words(S.ctx, fd),), -1, dtype=torch.int64, device="cuda")
+    for t in reversed(range(len(flat))):
+        F.matvec_bank_pack(S.ctx, fd, bank, t, flat[t])
     plan_b = F.MatvecPlan(S.ctx, *args, bank=bank, complex_pair=cp, lazy_moddown=lazy)
     outs_b = [torch.zeros_like(o) for o in outs_d]
     step("matvec run (bank)")
@@ -91,6 +93,21 @@ def test_cfg1_diagonal_matvec(lazy):
     err = np.max(np.abs(dec - np.tile(U @ x, n_slots // d)))
     print(f"cfg1 max |decoded - fp64| = {err:.3e} (2^{np.log2(err):.1f})")
     assert err <= 2.0 ** -15
+
+
+def test_bank_partial_output_groups():
+    """19 outputs (b, p) per term: one full group of 16 and a partial group of
+    3, an odd last pair of 16-bit fields and a second word of top bits; the
+    bank plan, the table plan and the oracle agree on every residue."""
+    P = C.params_p12()
+    n_slots = P.n // 2
+    desc = OW.MatvecDesc(3, 1, 1, 2, 19, 1, False, True)
+    S = Setup(P, 31, rot_steps=sorted(OW.required_rotations(desc, n_slots)))
+    xs = [synth.uniform_pm1(31, "x", (n_slots,)).astype(complex)]
+    diag = lambda b, p, u, q: synth.uniform_pm1(31, "diag", (n_slots,), b, p, u, q).astype(complex)
+    outs_o, outs_d = _run(P, S, desc, xs, float(P.q[2]), diag, 2.0 ** 30, "groups")
+    got = to_host(outs_d[0]).reshape(outs_o[0].shape)
+    assert np.array_equal(got, outs_o[0]), first_mismatch(got, outs_o[0])
 
 
 @pytest.mark.parametrize("lazy", [False, True])
