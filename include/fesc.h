@@ -337,7 +337,8 @@ int fesc_ptct_matvec(fesc_ctx* ctx, fesc_matvec_plan* plan, const uint64_t* cons
  * ceil(O/2) planes holding bits 32..47 of outputs 2j (low half) and 2j+1
  * (high half), then ceil(O/16) planes holding bits 48..49 of output o at bit
  * 2 (o mod 16).  One workgroup of the plaintext MAC then reads contiguous
- * runs, 6.25 bytes per residue instead of 8.
+ * runs, 6.25 bytes per residue instead of 8 when O is a multiple of 16 (the
+ * shared planes are partly empty otherwise: 8 bytes at O = 2, 12 at O = 1).
  * fesc_matvec_bank_words gives its size in uint64 words (level*N*T*(O +
  * ceil(O/2) + ceil(O/16))/2; level+alpha rows with lazy_moddown);
  * fesc_matvec_bank_pack writes plaintext `pt` ([level][N], or
