@@ -325,6 +325,23 @@ static uint32_t diag_rows(const Context* c, const fesc_matvec_desc& d) {
   return d.level + (d.lazy_moddown ? c->alpha : 0);
 }
 
+// Every Galois key the schedule needs must be present (checked when a plan is
+// made and again before a run launches anything: a key may have been replaced
+// since, and a failed replacement leaves none).
+static int check_plan_keys(const Context* c, const fesc_matvec_desc& d, int64_t giant) {
+  std::vector<int64_t> steps;
+  for (uint32_t q = 1; q < d.n1; ++q) steps.push_back((int64_t)q * d.unit);
+  for (uint32_t p = 1; p < d.n2; ++p) steps.push_back((int64_t)p * giant);
+  for (int64_t st : steps) {
+    const uint32_t g = galois_of_step(c, (int32_t)(st % (c->n / 2)));
+    if (g != 1 && !c->keys.count(g))
+      return fail(FESC_ERR_NO_KEY, "matvec needs the key of rotation " + std::to_string(st));
+  }
+  if ((d.real_extract || d.complex_pair) && !c->keys.count(2 * c->n - 1))
+    return fail(FESC_ERR_NO_KEY, "matvec real extraction needs the conjugation key");
+  return FESC_OK;
+}
+
 // giant_unit: the rotation of one giant step, INT64_MIN for n1 * unit (the
 // projection); the slot maps give their own.
 int matvec_plan_create(Context* c, const fesc_matvec_desc* d, const uint64_t* const* diags,
@@ -337,18 +354,8 @@ int matvec_plan_create(Context* c, const fesc_matvec_desc* d, const uint64_t* co
   if (!bank)
     for (size_t t = 0; t < n_diag; ++t)
       if (!diags[t]) return fail(FESC_ERR_ARG, "null diagonal " + std::to_string(t));
-  // every Galois key the schedule needs must be present
-  std::vector<int64_t> steps;
-  for (uint32_t q = 1; q < d->n1; ++q) steps.push_back((int64_t)q * d->unit);
   const int64_t giant = giant_unit == INT64_MIN ? (int64_t)d->n1 * d->unit : giant_unit;
-  for (uint32_t p = 1; p < d->n2; ++p) steps.push_back((int64_t)p * giant % (c->n / 2));
-  for (int64_t st : steps) {
-    const uint32_t g = galois_of_step(c, (int32_t)(st % (c->n / 2)));
-    if (g != 1 && !c->keys.count(g))
-      return fail(FESC_ERR_NO_KEY, "matvec needs the key of rotation " + std::to_string(st));
-  }
-  if ((d->real_extract || d->complex_pair) && !c->keys.count(2 * c->n - 1))
-    return fail(FESC_ERR_NO_KEY, "matvec real extraction needs the conjugation key");
+  if ((rc = check_plan_keys(c, *d, giant))) return rc;
 
   fesc_matvec_plan* p = new fesc_matvec_plan();
   p->d = *d;
@@ -425,6 +432,7 @@ int ptct_matvec(Context* c, fesc_matvec_plan* p, const uint64_t* const* in,
   const bool lazy = d.lazy_moddown;
   const uint32_t rows = diag_rows(c, d);
   const size_t ext_words = (size_t)2 * rows * n;
+  if ((err = check_plan_keys(c, d, p->giant))) return err;
   const LevelTables* T = nullptr;
   if (lazy && !(T = level_tables(c, level, &err))) return err;
   HIPCK(hipEventRecord(p->ev[0], s));
@@ -446,7 +454,8 @@ int ptct_matvec(Context* c, fesc_matvec_plan* p, const uint64_t* const* in,
         HIPCK(hipGetLastError());
         continue;
       }
-      jobs.push_back(KsJob{(uint32_t)srcs.size(), c->keys.at(g), g, in[u], 1u, g, nullptr, o});
+      jobs.push_back(KsJob{(uint32_t)srcs.size(), c->keys.find(g)->second, g, in[u], 1u, g,
+                           nullptr, o});
     }
     srcs.push_back(KsSource{in[u] + n, 2 * n});
     if (srcs.size() == kMaxBatch || u + 1 == d.n_in) {
@@ -576,6 +585,7 @@ int ptct_matvec_many(Context* c, fesc_matvec_plan* p, uint32_t count, const uint
   const uint32_t level = d.level, n1 = d.n1, n2 = d.n2;
   const size_t W = p->ct_words, n = c->n, per = (size_t)n1 + n2;
   int err;
+  if ((err = check_plan_keys(c, d, p->giant))) return err;
   const uint32_t want = std::min<uint32_t>(count, kMaxBatch);
   if (p->mcap < want) {
     (void)hipStreamSynchronize(s);  // earlier calls may still use the old workspace
@@ -627,7 +637,7 @@ int ptct_matvec_many(Context* c, fesc_matvec_plan* p, uint32_t count, const uint
           HIPCK(hipMemcpyAsync(baby_of(v, q), x, W * 8, hipMemcpyDeviceToDevice, s));
           continue;
         }
-        jobs.push_back(KsJob{v, c->keys.at(g), g, x, 1u, g, nullptr, baby_of(v, q)});
+        jobs.push_back(KsJob{v, c->keys.find(g)->second, g, x, 1u, g, nullptr, baby_of(v, q)});
       }
       srcs.push_back(KsSource{x + n, 2 * n});
     }
