@@ -509,13 +509,13 @@ __device__ __forceinline__ void bconv_mfma(const Map& map, const PrimeK* __restr
     for (int m = 0; m < 16; ++m) {
       const v4i dl = __builtin_amdgcn_mfma_i32_16x16x64_i8(alo, b[m], zero, 0, 0, 0);
       const v4i dh = __builtin_amdgcn_mfma_i32_16x16x64_i8(ahi, b[m], zero, 0, 0, 0);
-      // R = hi 2^32 + lo exactly (|lo| < 2^45, |hi| < 2^37); y = R - c q with
+      // R = hi 2^32 + lo exactly (|lo| < 2^45, |hi| < 2^37), each |Q_tau| <=
+      // 64 * 2^14 = 2^20, so digit pairs Q_t + 256 Q_t+1 still fit an int32
+      // and are combined before the conversion to fp64; y = R - c q with
       // c = round(R / q), formed exactly (the fma's result is below 2^51)
-      const double lo = __builtin_fma(
-          __builtin_fma(__builtin_fma((double)dl[3], 256.0, (double)dl[2]), 256.0, (double)dl[1]),
-          256.0, (double)dl[0]);
-      const double hi =
-          __builtin_fma(__builtin_fma((double)dh[2], 256.0, (double)dh[1]), 256.0, (double)dh[0]);
+      const double lo = __builtin_fma((double)(dl[2] + dl[3] * 256), 65536.0,
+                                      (double)(dl[0] + dl[1] * 256));
+      const double hi = __builtin_fma((double)dh[2], 65536.0, (double)(dh[0] + dh[1] * 256));
       const double cq = __builtin_rint(__builtin_fma(hi, k32, lo * qinv));
       double r = __builtin_fma(-cq, q, hi * 4294967296.0) + lo;
       if constexpr (NINTH) r += mm_shoup(d8[kBlock * m], h8.x, h8.y, q);  // |r| < 1.2 q
