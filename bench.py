@@ -550,9 +550,10 @@ def matvec_double_hoisting(F, torch, np) -> dict:
     """The projection with and without double hoisting (lazy ModDown), timed
     on the diagonal-method workload (N = 2^12, 64 x 64, 63 hoisted rotations)
     and on the 768 x 1536 shape (N = 2^16, 16 limbs, complex-paired outputs,
-    tiled bank).  The modular arithmetic does not depend on the values, so
-    diagonals and inputs are uniform residues; the two 2^16 banks (120.8 and
-    181.2 GB at 50 bits per residue) are built one after the other."""
+    diagonal bank).  The modular arithmetic does not depend on the values, so
+    the inputs are uniform residues and the banks random words (values below
+    2^50); the two 2^16 banks (120.8 and 181.2 GB at 50 bits per residue) are
+    built one after the other."""
     import synth
     import synth.workloads as WL
 

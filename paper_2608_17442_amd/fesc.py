@@ -599,7 +599,7 @@ def matvec_bank_pack(ctx: Context, desc: _MatvecDesc, bank, index: int, pt, stre
 class MatvecPlan:
     """BSGS projection plan over pre-encoded diagonals: either ``diags``, a
     flat list of device plaintexts in [b][p][u][q] order, or ``bank``, one
-    tiled device buffer (see fesc_matvec_bank_pack).  Inputs are kept alive."""
+    diagonal bank (see fesc_matvec_bank_pack).  Inputs are kept alive."""
 
     def __init__(self, ctx: Context, level, n_in, n_out, n1, n2, unit, real_extract, rescale,
                  diags=None, bank=None, complex_pair=False, lazy_moddown=False):
