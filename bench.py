@@ -246,8 +246,7 @@ class Workloads:
             m = min(chunk, n_diag - c0)
             self.F.bsgs_diagonal_slots(self.ctx, desc, Wd, Cc, c0, m, zs)
             self.ctx.encode_plain(zs[:m], scale, pts[:m], level)
-            for j in range(m):
-                self.F.matvec_bank_pack(self.ctx, desc, self.bank, c0 + j, pts[j])
+            self.F.matvec_bank_pack_many(self.ctx, desc, self.bank, c0, pts[:m])
         torch.cuda.synchronize()
         del Wd, zs, pts
         self.bank_build_s = time.perf_counter() - t0

@@ -352,6 +352,14 @@ int fesc_ptct_matvec(fesc_ctx* ctx, fesc_matvec_plan* plan, const uint64_t* cons
 int fesc_matvec_bank_words(const fesc_ctx* ctx, const fesc_matvec_desc* desc, size_t* words);
 int fesc_matvec_bank_pack(fesc_ctx* ctx, const fesc_matvec_desc* desc, uint64_t* bank,
                           uint32_t index, const uint64_t* pt, void* stream);
+/* The same for `count` (at most 65535) consecutive slots first ..
+ * first + count - 1 in one launch: slot first + j from plaintext
+ * pts + j * pt_stride (uint64 words, at least the plaintext's rows * N when
+ * count > 1).  count = 0 does nothing; a slot range past the bank's
+ * n_out*n2*n_in*n1 slots is FESC_ERR_ARG before any launch. */
+int fesc_matvec_bank_pack_many(fesc_ctx* ctx, const fesc_matvec_desc* desc, uint64_t* bank,
+                               uint32_t first, uint32_t count, const uint64_t* pts,
+                               size_t pt_stride, void* stream);
 int fesc_matvec_plan_create_bank(fesc_ctx* ctx, const fesc_matvec_desc* desc,
                                  const uint64_t* bank, fesc_matvec_plan** plan);
 

@@ -211,11 +211,15 @@ __global__ __launch_bounds__(kThreads) void k_ptmac(const uint64_t* const* __res
 // The hi and top words are shared with other outputs: each diagonal clears and
 // sets only its own bits with atomic AND / OR, so packs of different diagonals
 // may run in any order or concurrently.
-__global__ __launch_bounds__(kThreads) void k_bank_pack(const uint64_t* __restrict__ pt,
-                                                        uint32_t* __restrict__ bank, uint32_t o,
-                                                        uint32_t t, uint32_t n,
+// Diagonal `first + blockIdx.z` from plaintext pts + blockIdx.z * pt_stride.
+__global__ __launch_bounds__(kThreads) void k_bank_pack(const uint64_t* __restrict__ pts,
+                                                        size_t pt_stride,
+                                                        uint32_t* __restrict__ bank,
+                                                        uint32_t first, uint32_t n,
                                                         uint32_t n_outputs, uint32_t terms) {
-  const uint32_t i = blockIdx.y, tile = blockIdx.x;
+  const uint32_t i = blockIdx.y, tile = blockIdx.x, index = first + blockIdx.z;
+  const uint32_t o = index / terms, t = index % terms;
+  const uint64_t* pt = pts + (size_t)blockIdx.z * pt_stride;
   const uint64_t v = pt[(size_t)i * n + (size_t)tile * kThreads + threadIdx.x];
   uint32_t* rec = bank + bank_record(i, tile, t, n, n_outputs, terms) + threadIdx.x;
   rec[(size_t)o * kThreads] = (uint32_t)v;
@@ -719,19 +723,31 @@ int fesc_matvec_bank_words(const fesc_ctx* ctx, const fesc_matvec_desc* desc, si
   return FESC_OK;
 }
 
-int fesc_matvec_bank_pack(fesc_ctx* ctx, const fesc_matvec_desc* desc, uint64_t* bank,
-                          uint32_t index, const uint64_t* pt, void* stream) {
-  if (!ctx || !bank || !pt) return fesc::fail(FESC_ERR_ARG, "null argument");
+int fesc_matvec_bank_pack_many(fesc_ctx* ctx, const fesc_matvec_desc* desc, uint64_t* bank,
+                               uint32_t first, uint32_t count, const uint64_t* pts,
+                               size_t pt_stride, void* stream) {
+  if (!ctx || !bank) return fesc::fail(FESC_ERR_ARG, "null argument");
   int rc = fesc::check_desc(ctx, desc);
   if (rc) return rc;
   const uint32_t terms = desc->n_in * desc->n1, outputs = desc->n_out * desc->n2;
-  if ((uint64_t)index >= (uint64_t)terms * outputs)
+  const uint32_t rows = fesc::diag_rows(ctx, *desc);
+  if (count == 0) return FESC_OK;
+  if (!pts) return fesc::fail(FESC_ERR_ARG, "null plaintexts");
+  if (count > 65535) return fesc::fail(FESC_ERR_ARG, "at most 65535 diagonals per call");
+  if ((uint64_t)first + count > (uint64_t)terms * outputs)
     return fesc::fail(FESC_ERR_ARG, "diagonal index out of range");
-  hipLaunchKernelGGL(fesc::k_bank_pack, dim3(ctx->n / fesc::kThreads, fesc::diag_rows(ctx, *desc)),
-                     dim3(fesc::kThreads), 0, reinterpret_cast<hipStream_t>(stream), pt,
-                     reinterpret_cast<uint32_t*>(bank), index / terms, index % terms, ctx->n,
-                     outputs, terms);
+  if (count > 1 && pt_stride < (size_t)rows * ctx->n)
+    return fesc::fail(FESC_ERR_ARG, "plaintext stride below rows * N");
+  hipLaunchKernelGGL(fesc::k_bank_pack, dim3(ctx->n / fesc::kThreads, rows, count),
+                     dim3(fesc::kThreads), 0, reinterpret_cast<hipStream_t>(stream), pts,
+                     pt_stride, reinterpret_cast<uint32_t*>(bank), first, ctx->n, outputs,
+                     terms);
   return fesc::hip_check(hipGetLastError(), "bank_pack");
+}
+
+int fesc_matvec_bank_pack(fesc_ctx* ctx, const fesc_matvec_desc* desc, uint64_t* bank,
+                          uint32_t index, const uint64_t* pt, void* stream) {
+  return fesc_matvec_bank_pack_many(ctx, desc, bank, index, 1, pt, 0, stream);
 }
 
 int fesc_bsgs_diagonal_slots(fesc_ctx* ctx, const fesc_matvec_desc* desc, const double* W,

@@ -544,6 +544,9 @@ _lib.fesc_matvec_bank_words.argtypes = [_vp, ctypes.POINTER(_MatvecDesc),
 _lib.fesc_matvec_bank_words.restype = ctypes.c_int
 _lib.fesc_matvec_bank_pack.argtypes = [_vp, ctypes.POINTER(_MatvecDesc), _vp, _u32, _vp, _vp]
 _lib.fesc_matvec_bank_pack.restype = ctypes.c_int
+_lib.fesc_matvec_bank_pack_many.argtypes = [_vp, ctypes.POINTER(_MatvecDesc), _vp, _u32, _u32,
+                                            _vp, _sz, _vp]
+_lib.fesc_matvec_bank_pack_many.restype = ctypes.c_int
 _lib.fesc_matvec_plan_create_bank.argtypes = [_vp, ctypes.POINTER(_MatvecDesc), _vp,
                                               ctypes.POINTER(_vp)]
 _lib.fesc_matvec_plan_create_bank.restype = ctypes.c_int
@@ -594,6 +597,18 @@ def matvec_bank_pack(ctx: Context, desc: _MatvecDesc, bank, index: int, pt, stre
     _check(_lib.fesc_matvec_bank_pack(ctx._h, ctypes.byref(desc),
                                       _ptr(bank, matvec_bank_words(ctx, desc), "bank"), index,
                                       _ptr(pt, _diag_words(ctx, desc), "pt"), _stream(stream)))
+
+
+def matvec_bank_pack_many(ctx: Context, desc: _MatvecDesc, bank, first: int, pts, stream=None):
+    """Slots first .. first + len(pts) - 1 from the rows of ``pts``, a 2-D
+    tensor [count][words >= the plaintext's rows * N], in one launch."""
+    count, stride = (pts.shape[0], pts.shape[1]) if pts.dim() == 2 else (0, 0)
+    if pts.dim() != 2 or stride < _diag_words(ctx, desc):
+        raise ValueError("pts: expected [count][rows * N] plaintexts")
+    _check(_lib.fesc_matvec_bank_pack_many(ctx._h, ctypes.byref(desc),
+                                           _ptr(bank, matvec_bank_words(ctx, desc), "bank"),
+                                           first, count, _ptr(pts, count * stride, "pts"),
+                                           stride, _stream(stream)))
 
 
 class MatvecPlan:

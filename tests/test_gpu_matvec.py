@@ -111,6 +111,45 @@ def test_bank_partial_output_groups():
 
 
 @pytest.mark.parametrize("lazy", [False, True])
+def test_bank_pack_many_matches_single_packs(lazy):
+    """36 diagonals (9 outputs x 4 terms: a partial hi pair and a partly used
+    top word) packed one at a time, in two batched calls, and in batched
+    calls in reverse order give the same bank word for word; out-of-range
+    slots and a short plaintext stride are refused before any launch."""
+    import ctypes
+    from paper_2608_17442_amd import fesc as F
+    P = C.params_small(12, 50, 4, 2)
+    ctx = F.Context(P.log_n, P.q, P.p)
+    level = 3
+    fd = F.matvec_desc(level, 2, 3, 2, 3, 1, False, True, False, lazy)
+    mods = P.qs(level) + (list(P.p) if lazy else [])
+    n_diag = 36
+    pts = torch.stack([to_dev(synth.uniform_residues(41, "bank", mods, P.n, t)).reshape(-1)
+                       for t in range(n_diag)])
+    words = F.matvec_bank_words(ctx, fd)
+    banks = [torch.full((words,), -1, dtype=torch.int64, device="cuda") for _ in range(3)]
+    for t in range(n_diag):
+        F.matvec_bank_pack(ctx, fd, banks[0], t, pts[t])
+    F.matvec_bank_pack_many(ctx, fd, banks[1], 0, pts[:20])
+    F.matvec_bank_pack_many(ctx, fd, banks[1], 20, pts[20:])
+    for c0 in reversed(range(0, n_diag, 7)):
+        F.matvec_bank_pack_many(ctx, fd, banks[2], c0, pts[c0:c0 + 7])
+    F.matvec_bank_pack_many(ctx, fd, banks[2], 0, pts[:0])  # empty: nothing
+    torch.cuda.synchronize()
+    assert torch.equal(banks[1], banks[0])
+    assert torch.equal(banks[2], banks[0])
+    with pytest.raises(RuntimeError):
+        F.matvec_bank_pack_many(ctx, fd, banks[1], 30, pts[:7])
+    rc = F._lib.fesc_matvec_bank_pack_many(ctx._h, ctypes.byref(fd), banks[1].data_ptr(), 0, 2,
+                                           pts.data_ptr(), len(mods) * P.n - 1,
+                                           torch.cuda.current_stream().cuda_stream)
+    assert rc == -1
+    torch.cuda.synchronize()
+    assert torch.equal(banks[1], banks[0])
+    ctx.close()
+
+
+@pytest.mark.parametrize("lazy", [False, True])
 def test_paired_bsgs_small(lazy):
     P = C.params_small(12, 50, 5, 2)
     n_slots, seg_len, Cc = P.n // 2, 64, 32
