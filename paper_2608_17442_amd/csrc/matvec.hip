@@ -93,7 +93,7 @@ __device__ __forceinline__ double bank_value(uint32_t lo, uint32_t hi_word, uint
   return __hiloint2double((int)(hi | 0x43300000u), (int)lo) - kTwo52;
 }
 
-// BANK: diagonals from a tiled bank; otherwise from the table of plaintexts.
+// BANK: diagonals from the diagonal bank; otherwise from the table of plaintexts.
 // Ciphertext rows: component c of limb i at i * row_stride + c * comp_stride
 // ([limbs][2][N]: 2N and N; extended basis [2][limbs][N]: N and limbs N);
 // limb i uses prime i below `split`, prime1 + (i - split) from there.
